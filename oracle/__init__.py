@@ -1,0 +1,31 @@
+"""CPU oracle for the SAGIPS single-rank step (test infrastructure only).
+
+A plain, slow, float64 statement of what the step computes, written from the
+paper (Sec. II problem statement, Sec. III GAN optimiser, Sec. V-A loop-closure
+settings and its inverse-CDF sampler) and from the stated workload choices
+(Philox4x32-10 counter-based draws, a Kumaraswamy inverse CDF, a LeakyReLU
+discriminator with a BCE loss).
+
+Only the test-suite, the smoke check and the CPU-baseline leg of the benchmark
+may import this package.  It shares no code with the HIP library and imports
+nothing from it.
+
+Parity status per function (what pins it, see tests/test_oracle_*.py):
+  philox4x32_10      pinned: bit-exact against an independent open-source
+                     implementation compiled from source (PyTorch ATen).
+  uniform            pinned: exact-arithmetic identities.
+  kumaraswamy_icdf   pinned: CDF round trip, a=b=1 identity, Beta(1,b) and
+                     Beta(a,1) special cases (scipy), median, moments.
+  pathwise           pinned: finite differences, chain-rule form, signs,
+                     expectation identities (digamma), theta=1 closed form.
+  features_hd8       pinned: definition checks (log features vs values).
+  mlp forward/back   pinned: finite differences, torch float64 autograd,
+                     zero-last-layer and logistic-regression special cases.
+  bce                pinned: closed values at z=0, derivative identity.
+  bf16 emulation     pinned: RNE rounding against torch's bfloat16 cast.
+"""
+from .philox import philox4x32_10, event_words  # noqa: F401
+from .sampler import (uniform_from_words, kumaraswamy_icdf, kumaraswamy_cdf,  # noqa: F401
+                      pathwise, sample, features_hd8, features_hd8_jacobian)
+from .mlp import mlp_forward, bce_losses, disc_fwd_bwd, round_bf16  # noqa: F401
+from .step import param_grad, quadratic_critic, run_step  # noqa: F401

@@ -1,0 +1,134 @@
+"""Pins the oracle's discriminator forward/backward and BCE losses."""
+import numpy as np
+import pytest
+import torch
+
+from oracle.mlp import bce_losses, disc_fwd_bwd, mlp_forward, round_bf16, sigmoid
+
+
+def _net(widths, seed):
+    rng = np.random.default_rng(seed)
+    W = [rng.standard_normal((o, i)) * 0.7 for i, o in zip(widths[:-1], widths[1:])]
+    b = [rng.standard_normal(o) * 0.3 for o in widths[1:]]
+    return W, b
+
+
+def _batches(F, n, seed):
+    rng = np.random.default_rng(seed)
+    return rng.uniform(0.05, 0.95, (n, F)), rng.uniform(0.05, 0.95, (n + 3, F))
+
+
+@pytest.mark.parametrize("widths", [(2, 8, 8, 1), (3, 5, 7, 4, 1), (8, 6, 1)])
+def test_backward_vs_finite_differences(widths):
+    W, b = _net(widths, 1)
+    xf, xr = _batches(widths[0], 13, 2)
+    r = disc_fwd_bwd(W, b, xf, xr)
+    h = 1e-6
+
+    def LD(W_, b_):
+        zf, _, _ = mlp_forward(W_, b_, xf)
+        zr, _, _ = mlp_forward(W_, b_, xr)
+        return bce_losses(zf, zr)[0]
+
+    for l in range(len(W)):
+        for idx in [(0, 0), (W[l].shape[0] - 1, W[l].shape[1] - 1), (W[l].shape[0] // 2, 0)]:
+            Wp = [w.copy() for w in W]; Wm = [w.copy() for w in W]
+            Wp[l][idx] += h; Wm[l][idx] -= h
+            fd = (LD(Wp, b) - LD(Wm, b)) / (2 * h)
+            assert abs(r["dW"][l][idx] - fd) < 1e-7 + 1e-6 * abs(fd)
+        bp = [v.copy() for v in b]; bm = [v.copy() for v in b]
+        bp[l][-1] += h; bm[l][-1] -= h
+        fd = (LD(W, bp) - LD(W, bm)) / (2 * h)
+        assert abs(r["db"][l][-1] - fd) < 1e-7 + 1e-6 * abs(fd)
+    # dL_G / d fake input
+    for k in (0, 5, 12):
+        for j in range(widths[0]):
+            xp = xf.copy(); xm = xf.copy()
+            xp[k, j] += h; xm[k, j] -= h
+            fd = (bce_losses(mlp_forward(W, b, xp)[0], mlp_forward(W, b, xr)[0])[1]
+                  - bce_losses(mlp_forward(W, b, xm)[0], mlp_forward(W, b, xr)[0])[1]) / (2 * h)
+            assert abs(r["dLg_din"][k, j] - fd) < 1e-8 + 1e-6 * abs(fd)
+
+
+def test_against_torch_float64_autograd():
+    widths = (2, 16, 16, 16, 1)
+    W, b = _net(widths, 3)
+    xf, xr = _batches(2, 40, 4)
+    r = disc_fwd_bwd(W, b, xf, xr)
+    tW = [torch.tensor(w, requires_grad=True) for w in W]
+    tb = [torch.tensor(v, requires_grad=True) for v in b]
+    tf = torch.tensor(xf, requires_grad=True)
+    tr = torch.tensor(xr)
+
+    def fwd(h):
+        for l in range(len(tW)):
+            h = h @ tW[l].T + tb[l]
+            if l < len(tW) - 1:
+                h = torch.nn.functional.leaky_relu(h, 0.2)
+        return h[:, 0]
+
+    zf, zr = fwd(tf), fwd(tr)
+    bce = torch.nn.functional.binary_cross_entropy_with_logits
+    LD = bce(zr, torch.ones_like(zr)) + bce(zf, torch.zeros_like(zf))
+    gW = torch.autograd.grad(LD, tW + tb, retain_graph=True)
+    LG = bce(zf, torch.ones_like(zf))
+    gx, = torch.autograd.grad(LG, [tf])
+    assert abs(float(LD) - r["loss_d"]) < 1e-12 and abs(float(LG) - r["loss_g"]) < 1e-12
+    for l in range(len(W)):
+        np.testing.assert_allclose(r["dW"][l], gW[l].numpy(), rtol=1e-10, atol=1e-14)
+        np.testing.assert_allclose(r["db"][l], gW[len(W) + l].numpy(), rtol=1e-10, atol=1e-14)
+    np.testing.assert_allclose(r["dLg_din"], gx.numpy(), rtol=1e-10, atol=1e-16)
+    np.testing.assert_allclose(r["logits_fake"], zf.detach().numpy(), rtol=1e-12)
+
+
+def test_zero_last_layer():
+    W, b = _net((2, 8, 8, 1), 5)
+    W[-1][:] = 0
+    b[-1][:] = 0
+    xf, xr = _batches(2, 17, 6)
+    r = disc_fwd_bwd(W, b, xf, xr)
+    assert abs(r["loss_d"] - 2 * np.log(2)) < 1e-15 and abs(r["loss_g"] - np.log(2)) < 1e-15
+    assert np.all(r["dLg_din"] == 0)
+    assert all(np.all(r["dW"][l] == 0) for l in range(len(W) - 1))
+    # logit layer gradient: 1/2 mean over fakes of h minus 1/2 mean over reals of h
+    _, _, hf = mlp_forward(W, b, xf)
+    _, _, hr = mlp_forward(W, b, xr)
+    np.testing.assert_allclose(r["dW"][-1][0], 0.5 * hf[-1].mean(0) - 0.5 * hr[-1].mean(0), rtol=1e-12)
+
+
+def test_logistic_regression_closed_form():
+    W, b = _net((3, 1), 8)
+    xf, xr = _batches(3, 21, 9)
+    r = disc_fwd_bwd(W, b, xf, xr)
+    zf = xf @ W[0][0] + b[0][0]
+    zr = xr @ W[0][0] + b[0][0]
+    dW = (sigmoid(zf)[:, None] * xf).mean(0) + ((sigmoid(zr) - 1)[:, None] * xr).mean(0)
+    np.testing.assert_allclose(r["dW"][0][0], dW, rtol=1e-12)
+    np.testing.assert_allclose(r["db"][0][0], sigmoid(zf).mean() + (sigmoid(zr) - 1).mean(), rtol=1e-12)
+    np.testing.assert_allclose(r["dLg_din"], ((sigmoid(zf) - 1) / len(zf))[:, None] * W[0][0][None, :], rtol=1e-12)
+
+
+def test_bce_at_zero_and_large_logits():
+    LD, LG = bce_losses(np.zeros(5), np.zeros(7))
+    assert abs(LD - 2 * np.log(2)) < 1e-15 and abs(LG - np.log(2)) < 1e-15
+    LD, LG = bce_losses(np.array([-800.0]), np.array([800.0]))
+    assert LD < 1e-300 and abs(LG - 800.0) < 1e-12
+
+
+def test_bf16_rounding_matches_torch():
+    rng = np.random.default_rng(10)
+    a = np.concatenate([rng.standard_normal(20000) * 10.0 ** rng.integers(-30, 30, 20000),
+                        [0.0, -0.0, 1.0, 1.00390625, 1.005859375, 3e38, 1e-40]])
+    a32 = a.astype(np.float32)
+    ref = torch.tensor(a32).to(torch.bfloat16).to(torch.float64).numpy()
+    np.testing.assert_array_equal(round_bf16(a32), ref)
+
+
+def test_bf16_mode_is_close_to_fp64():
+    W, b = _net((2, 32, 32, 32, 1), 11)
+    xf, xr = _batches(2, 64, 12)
+    r = disc_fwd_bwd(W, b, xf, xr)
+    q = disc_fwd_bwd(W, b, xf, xr, bf16=True)
+    rel = lambda p, t: np.linalg.norm(p - t) / np.linalg.norm(t)
+    assert 0 < rel(q["logits_fake"], r["logits_fake"]) < 2e-2
+    assert 0 < rel(q["dW"][1], r["dW"][1]) < 5e-2

@@ -1,0 +1,67 @@
+"""The five synthetic workloads of the single-rank step.
+
+Shapes follow the paper's step (Sec. V-A, Tab. gen_settings: a batch of
+parameter samples, a fixed number of events per sample, an equal-sized real
+batch) scaled to MI355X sizes.  Each workload is a frozen description; the
+arrays are drawn by :mod:`workloads.gen`.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass
+from typing import Optional, Tuple
+
+
+@dataclass(frozen=True)
+class Workload:
+    name: str
+    n_theta: int                 # parameter samples per step
+    d: int                       # observables per event (2 or 3); theta has 2d entries
+    events_per_theta: int        # E
+    widths: Optional[Tuple[int, ...]]   # discriminator widths incl. input and the 1-wide logit; None = quadratic critic
+    precision: str               # "f32" or "bf16" (hidden-layer GEMM operands)
+    features: str                # "identity" or "hd8"
+    theta_source: str            # "uniform" (U(1,6)) or "generator" (16->64->64->4 MLP)
+    theta_seed: int = 0
+    fake_seed: int = 0           # Philox key of the fake events
+    real_seed: int = 1           # Philox key of the real events
+    weight_seed: int = 2
+    generator_seed: int = 3
+
+    @property
+    def n_events(self) -> int:
+        return self.n_theta * self.events_per_theta
+
+    @property
+    def n_params(self) -> int:
+        return 2 * self.d
+
+    @property
+    def theta_star(self) -> Tuple[float, ...]:
+        # (a1,b1,a2,b2) as the workload states; the third pair for d=3 is a
+        # chosen value (the paper names no distribution at all).
+        return (2.0, 5.0, 1.5, 3.0) if self.d == 2 else (2.0, 5.0, 1.5, 3.0, 3.0, 2.0)
+
+    def mlp_macs(self) -> int:
+        """Multiply-accumulates per sample through the discriminator."""
+        if self.widths is None:
+            return 0
+        return sum(a * b for a, b in zip(self.widths[:-1], self.widths[1:]))
+
+
+CONFIGS = {
+    "pr1_tiny": Workload("pr1_tiny", 1, 2, 16384, (2, 64, 64, 1), "f32", "identity", "uniform"),
+    "small": Workload("small", 32, 2, 8192, (2, 128, 128, 128, 1), "f32", "identity", "generator"),
+    "medium": Workload("medium", 256, 2, 16384, (2, 256, 256, 256, 256, 1), "bf16", "identity", "uniform"),
+    "higher_dim": Workload("higher_dim", 1024, 3, 16384, (8, 512, 512, 512, 512, 1), "bf16", "hd8", "uniform"),
+    "stress": Workload("stress", 64, 2, 4194304, None, "f32", "identity", "uniform"),
+}
+
+
+def get(name: str) -> Workload:
+    return CONFIGS[name]
+
+
+def scaled(w: Workload, n_theta: Optional[int] = None, events_per_theta: Optional[int] = None) -> Workload:
+    """Same workload with fewer parameter samples or events (parity-size cases)."""
+    from dataclasses import replace
+    return replace(w, n_theta=n_theta or w.n_theta, events_per_theta=events_per_theta or w.events_per_theta)
