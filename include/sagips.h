@@ -1,0 +1,175 @@
+/*
+ * sagips.h -- C ABI of libsagips.so: one rank's sample -> discriminate ->
+ * backward step of SAGIPS (arXiv 2407.00051) on an AMD Instinct MI355X (gfx950).
+ *
+ * The calls follow the paper's problem statement (Sec. II, eqs. def_inv,
+ * def_x_hat, def_optim): parameters p are turned into events by a pipeline
+ * whose sampler module uses an inverse CDF (Sec. V-A); an objective (the GAN
+ * discriminator, Sec. II-B.2 and III-A) scores synthetic against reference
+ * events; gradients flow back through every differentiable module to p
+ * (Sec. III-B).
+ *
+ * Conventions shared by every call
+ *   - Pointers are DEVICE pointers on the context's device unless marked
+ *     "host".  The caller allocates and owns every input and output; the
+ *     library owns only the context and its workspace.
+ *   - Every call is asynchronous on the context's HIP stream.  Arguments are
+ *     validated before anything is launched; on a validation error nothing is
+ *     launched, a negative status is returned and sagips_last_error() says why.
+ *     Faults during execution surface at the caller's stream synchronisation.
+ *   - Outputs are overwritten, never accumulated.  Results are bitwise
+ *     reproducible for fixed inputs (fixed reduction order, no float atomics).
+ *   - Device arrays must be 16-byte aligned and densely packed, row-major.
+ *   - A context is not thread-safe; calls on one context must not overlap
+ *     from several host threads.
+ *
+ * Event sampling (shared by all calls that take a sagips_source)
+ *   Event k of parameter row i has id = counter_base + i*E + k.  Its random
+ *   block is Philox4x32-10 (Salmon et al., SC'11) with
+ *       key = (seed & 0xffffffff, seed >> 32),
+ *       counter = (id & 0xffffffff, id >> 32, stream, 0),
+ *   words w0..w3.  Coordinate j < d uses u_j = ((w_j >> 9) + 1/2) * 2^-23 and
+ *   the Kumaraswamy quantile x_j = (1 - (1 - u_j)^(1/b_j))^(1/a_j) with
+ *   (a_j, b_j) = (theta[i][2j], theta[i][2j+1]).
+ */
+#ifndef SAGIPS_H
+#define SAGIPS_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define SAGIPS_MAX_LAYERS 8
+
+typedef struct sagips_ctx sagips_ctx;
+
+typedef enum {
+  SAGIPS_OK = 0,
+  SAGIPS_E_INVAL = -1,       /* bad argument: NULL, size, alignment, unsupported shape */
+  SAGIPS_E_ARCH = -2,        /* device is not gfx950 */
+  SAGIPS_E_NOMEM = -3,       /* workspace allocation failed */
+  SAGIPS_E_HIP = -4,         /* a HIP runtime call or a launch failed */
+  SAGIPS_E_UNSUPPORTED = -5  /* valid request the library does not implement */
+} sagips_status;
+
+typedef enum { SAGIPS_F32 = 0, SAGIPS_BF16 = 1 } sagips_precision;
+typedef enum { SAGIPS_FEAT_IDENTITY = 0, SAGIPS_FEAT_HD8 = 1 } sagips_features;
+typedef enum { SAGIPS_CRITIC_BUFFER = 0, SAGIPS_CRITIC_QUADRATIC = 1 } sagips_critic;
+
+/* Parameters -> events source (host struct holding a device pointer).
+ *   theta            device, [n_theta][2d] fp32, rows (a1,b1,a2,b2[,a3,b3]);
+ *                    shape parameters must be > 0 (the workloads use >= 1).
+ *   n_theta          >= 1
+ *   d                observables per event, 2 or 3
+ *   events_per_theta E >= 1; n_theta * E < 2^31 and counter_base + n_theta*E < 2^64
+ *   seed, counter_base, stream   see "Event sampling" above            */
+typedef struct {
+  const float* theta;
+  int32_t n_theta;
+  int32_t d;
+  int64_t events_per_theta;
+  uint64_t seed;
+  uint64_t counter_base;
+  uint32_t stream;
+} sagips_source;
+
+/* Discriminator (paper Sec. V-A: LeakyReLU hidden layers).  Layer l maps
+ * width[l] -> width[l+1]; W[l] is [width[l+1]][width[l]] fp32 (torch.nn.Linear
+ * layout), b[l] is [width[l+1]] fp32.  Hidden layers apply
+ * LeakyReLU(leaky_slope); the last layer has width 1 and emits a logit.
+ *   features   IDENTITY: width[0] == d;  HD8 (d == 3): width[0] == 8 and the
+ *              input is [x1,x2,x3,x1x2,x2x3,x1x3,ln x1,ln(1-x3)].
+ *   precision  F32: every product in fp32.  BF16: hidden-to-hidden layers use
+ *              bf16 operands (weights rounded once per call, activations and
+ *              backward signals rounded to nearest even) with fp32 accumulate;
+ *              the first and the logit layer stay fp32.
+ * Supported shapes: n_layers >= 2; all hidden widths equal, one of 64, 128
+ * (F32) or 256, 512 (BF16); width[0] in {2, 3, 8}.                       */
+typedef struct {
+  int32_t n_layers;
+  int32_t width[SAGIPS_MAX_LAYERS + 1];
+  const float* W[SAGIPS_MAX_LAYERS];
+  const float* b[SAGIPS_MAX_LAYERS];
+  float leaky_slope;
+  int32_t precision;  /* sagips_precision */
+  int32_t features;   /* sagips_features  */
+} sagips_mlp;
+
+/* Discriminator outputs; any pointer may be NULL ("not requested").
+ *   logits_fake [n_fake], logits_real [n_real]
+ *   loss_d [1]  L_D = mean_real softplus(-z) + mean_fake softplus(z)
+ *   loss_g [1]  L_G = mean_fake softplus(-z)   (non-saturating generator loss)
+ *   dW[l], db[l]  gradients of L_D, shaped like W[l], b[l] (all or none)
+ *   dLg_dx [n_fake][d]  dL_G / d fake event
+ *   dLg_dtheta [n_theta][2d]  dL_G / d theta; only with a fake source      */
+typedef struct {
+  float* logits_fake;
+  float* logits_real;
+  float* loss_d;
+  float* loss_g;
+  float* dW[SAGIPS_MAX_LAYERS];
+  float* db[SAGIPS_MAX_LAYERS];
+  float* dLg_dx;
+  float* dLg_dtheta;
+} sagips_disc_out;
+
+/* Create a context on HIP device `hip_device` using `hip_stream` (a
+ * hipStream_t; NULL = the device's null stream).  Fails with SAGIPS_E_ARCH
+ * unless the device is gfx950.  *out is set to NULL on failure.          */
+sagips_status sagips_create(sagips_ctx** out, int hip_device, void* hip_stream);
+
+/* Release the context and its workspace.  Synchronises the context's stream
+ * first.  NULL is accepted.                                               */
+sagips_status sagips_destroy(sagips_ctx* ctx);
+
+/* Switch subsequent calls to another stream of the same device.           */
+sagips_status sagips_set_stream(sagips_ctx* ctx, void* hip_stream);
+
+/* Message of the last failed call on ctx (ctx may be NULL: message of the
+ * last failed sagips_create in this process).  Never NULL.               */
+const char* sagips_last_error(const sagips_ctx* ctx);
+
+/* Kernel timing: when enabled, each kernel launch of the following calls is
+ * bracketed by HIP events on the context's stream.  sagips_kernel_times()
+ * synchronises the stream and returns, per kernel name, the number of
+ * launches and the summed milliseconds since the last reset (host arrays of
+ * `cap` entries; names point to static strings).  Returns the number of
+ * distinct kernels, or a negative status.                                 */
+sagips_status sagips_set_timing(sagips_ctx* ctx, int enable);
+int sagips_kernel_times(sagips_ctx* ctx, const char** names, int64_t* launches, double* total_ms, int cap);
+
+/* 1. Parameters -> events (paper Sec. V-A, inverse-CDF sampler module).
+ *   x_out      [N][d] fp32, N = n_theta * E; may be NULL if words_out is set
+ *   words_out  [N][4] uint32 raw Philox words, or NULL                     */
+sagips_status sagips_sample_events(sagips_ctx* ctx, const sagips_source* src, float* x_out,
+                                   uint32_t* words_out);
+
+/* 2. Events -> discriminator -> BCE loss -> backward (paper Sec. II-B.2,
+ * Sec. III-A; the discriminator labels reference events 1 and synthetic 0).
+ * Fake events come either as a buffer fake_x [n_fake][d] or as a source
+ * fake_src that is sampled inside the kernel (exactly one of the two is
+ * non-NULL; with a source, n_fake must equal n_theta * E and the call can
+ * also return dLg_dtheta).  real_x is [n_real][d] fp32.  d is taken from
+ * fake_src, or from width[0] for IDENTITY features, or is 3 for HD8.       */
+sagips_status sagips_disc_fwd_bwd(sagips_ctx* ctx, const sagips_mlp* D, const float* fake_x,
+                                  const sagips_source* fake_src, int64_t n_fake,
+                                  const float* real_x, int64_t n_real, sagips_disc_out* out);
+
+/* 3. dL/dx -> pathwise dx/dtheta -> per-parameter reduction (paper Sec. II,
+ * gradient of the objective with respect to p through the sampler).  The
+ * events are regenerated from the source, never read.  With
+ * critic == BUFFER, dL_dx is [N][d] fp32 and loss_out must be NULL; with
+ * critic == QUADRATIC the critic is L = sum over events and coordinates of
+ * (x - 1/2)^2, dL_dx must be NULL, and loss_out [1] (may be NULL) gets L.
+ *   dL_dtheta  [n_theta][2d]: sum over the row's events of
+ *              dL/dx_j * (dx_j/da_j, dx_j/db_j)                            */
+sagips_status sagips_param_grad(sagips_ctx* ctx, const sagips_source* src, sagips_critic critic,
+                                const float* dL_dx, float* dL_dtheta, float* loss_out);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SAGIPS_H */

@@ -58,6 +58,22 @@ def _hidden(l, n_layers):
     return 0 < l < n_layers - 1
 
 
+def kink_margin(W, b, hs, pres):
+    """Per event, the smallest relative distance of any hidden pre-activation
+    from the LeakyReLU kink: min over units of |pre| / (sum_k |W h_k| + |b|).
+
+    LeakyReLU (Sec. V-A) has a jump in its derivative at 0, so the backward
+    signal of an event whose margin is at rounding level depends on which side
+    of 0 a given precision lands; such events are not comparable elementwise
+    between an fp32 and a float64 evaluation."""
+    n = len(W)
+    m = np.full(hs[0].shape[0], np.inf)
+    for l in range(n - 1):
+        scale = np.abs(hs[l]) @ np.abs(np.asarray(W[l], dtype=np.float64)).T + np.abs(np.asarray(b[l], dtype=np.float64))
+        m = np.minimum(m, (np.abs(pres[l]) / np.maximum(scale, 1e-300)).min(axis=1))
+    return m
+
+
 def mlp_forward(W, b, h0, slope=0.2, bf16=False):
     """Returns (z[N], pres, hs) where hs[0] is the input and hs[l+1] = act(pres[l])."""
     n = len(W)
@@ -125,6 +141,7 @@ def disc_fwd_bwd(W, b, fake_in, real_in, slope=0.2, bf16=False):
     dW_r, db_r, _ = _backward(W, pres_r, hs_r, gD_r, slope, bf16, False)
     _, _, g_in = _backward(W, pres_f, hs_f, gG_f, slope, bf16, True)
     return {
+        "kink_margin_fake": kink_margin(W, b, hs_f, pres_f),
         "logits_fake": z_f, "logits_real": z_r, "loss_d": L_D, "loss_g": L_G,
         "dW": [p + q for p, q in zip(dW_f, dW_r)], "db": [p + q for p, q in zip(db_f, db_r)],
         "dLg_din": g_in,

@@ -1,0 +1,300 @@
+"""Python binding of libsagips.so, the MI355X (gfx950) implementation of one
+rank's SAGIPS sample -> discriminate -> backward step (arXiv 2407.00051).
+
+The binding only marshals arguments: every step runs in the library's HIP
+kernels.  PyTorch supplies device memory and the stream (the context runs on
+torch's current stream of its device unless another is set).  There is no
+CPU fallback: if the library is missing or fails to load, importing the
+calls raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Dict, List, Optional, Sequence
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libsagips.so")
+MAX_LAYERS = 8
+
+OK, E_INVAL, E_ARCH, E_NOMEM, E_HIP, E_UNSUPPORTED = 0, -1, -2, -3, -4, -5
+F32, BF16 = 0, 1
+FEAT_IDENTITY, FEAT_HD8 = 0, 1
+CRITIC_BUFFER, CRITIC_QUADRATIC = 0, 1
+
+EXPORTED = ("sagips_create", "sagips_destroy", "sagips_set_stream", "sagips_last_error", "sagips_set_timing",
+            "sagips_kernel_times", "sagips_sample_events", "sagips_disc_fwd_bwd", "sagips_param_grad")
+
+
+class SagipsError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"sagips status {status}: {message}")
+        self.status = status
+
+
+class Source(ctypes.Structure):
+    _fields_ = [("theta", ctypes.c_void_p), ("n_theta", ctypes.c_int32), ("d", ctypes.c_int32),
+                ("events_per_theta", ctypes.c_int64), ("seed", ctypes.c_uint64),
+                ("counter_base", ctypes.c_uint64), ("stream", ctypes.c_uint32)]
+
+
+class Mlp(ctypes.Structure):
+    _fields_ = [("n_layers", ctypes.c_int32), ("width", ctypes.c_int32 * (MAX_LAYERS + 1)),
+                ("W", ctypes.c_void_p * MAX_LAYERS), ("b", ctypes.c_void_p * MAX_LAYERS),
+                ("leaky_slope", ctypes.c_float), ("precision", ctypes.c_int32), ("features", ctypes.c_int32)]
+
+
+class DiscOut(ctypes.Structure):
+    _fields_ = [("logits_fake", ctypes.c_void_p), ("logits_real", ctypes.c_void_p),
+                ("loss_d", ctypes.c_void_p), ("loss_g", ctypes.c_void_p),
+                ("dW", ctypes.c_void_p * MAX_LAYERS), ("db", ctypes.c_void_p * MAX_LAYERS),
+                ("dLg_dx", ctypes.c_void_p), ("dLg_dtheta", ctypes.c_void_p)]
+
+
+_lib = None
+
+
+def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
+    """Load libsagips.so (once) and declare its signatures."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise ImportError(f"{path} is not built; run python -m paper_2407_00051_amd.build")
+    lib = ctypes.CDLL(path)
+    vp, i32, i64 = ctypes.c_void_p, ctypes.c_int, ctypes.c_int64
+    lib.sagips_create.argtypes = [ctypes.POINTER(vp), i32, vp]
+    lib.sagips_destroy.argtypes = [vp]
+    lib.sagips_set_stream.argtypes = [vp, vp]
+    lib.sagips_last_error.argtypes = [vp]
+    lib.sagips_last_error.restype = ctypes.c_char_p
+    lib.sagips_set_timing.argtypes = [vp, i32]
+    lib.sagips_kernel_times.argtypes = [vp, ctypes.POINTER(ctypes.c_char_p), ctypes.POINTER(i64),
+                                        ctypes.POINTER(ctypes.c_double), i32]
+    lib.sagips_sample_events.argtypes = [vp, ctypes.POINTER(Source), vp, vp]
+    lib.sagips_disc_fwd_bwd.argtypes = [vp, ctypes.POINTER(Mlp), vp, ctypes.POINTER(Source), i64, vp, i64,
+                                        ctypes.POINTER(DiscOut)]
+    lib.sagips_param_grad.argtypes = [vp, ctypes.POINTER(Source), i32, vp, vp, vp]
+    for name in ("sagips_create", "sagips_destroy", "sagips_set_stream", "sagips_set_timing",
+                 "sagips_kernel_times", "sagips_sample_events", "sagips_disc_fwd_bwd", "sagips_param_grad"):
+        getattr(lib, name).restype = ctypes.c_int
+    _lib = lib
+    return lib
+
+
+def _ptr(t) -> Optional[int]:
+    return None if t is None else t.data_ptr()
+
+
+def _check_tensor(t, name, dtype=None, shape=None, device=None):
+    import torch
+    if t is None:
+        return
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be on a GPU device")
+    if device is not None and t.device.index != device:
+        raise ValueError(f"{name} is on cuda:{t.device.index}, the context on cuda:{device}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if dtype is not None and t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if shape is not None and tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} must have shape {tuple(shape)}, got {tuple(t.shape)}")
+
+
+class Context:
+    """A library context on one GPU, running on torch's current stream of that device."""
+
+    def __init__(self, device: int = 0, stream=None):
+        import torch
+        self.lib = load_library()
+        self.device = device
+        if stream is None:
+            stream = torch.cuda.current_stream(device)
+        self._stream = stream
+        h = ctypes.c_void_p()
+        st = self.lib.sagips_create(ctypes.byref(h), device, ctypes.c_void_p(stream.cuda_stream))
+        if st != OK:
+            raise SagipsError(st, self.lib.sagips_last_error(None).decode())
+        self.h = h
+
+    # -- plumbing -------------------------------------------------------------
+    def _check(self, st: int):
+        if st != OK:
+            raise SagipsError(st, self.lib.sagips_last_error(self.h).decode())
+
+    def close(self):
+        if getattr(self, "h", None):
+            self.lib.sagips_destroy(self.h)
+            self.h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    @property
+    def stream(self):
+        return self._stream
+
+    def set_stream(self, stream):
+        self._check(self.lib.sagips_set_stream(self.h, ctypes.c_void_p(stream.cuda_stream)))
+        self._stream = stream
+
+    def set_timing(self, enable: bool):
+        self._check(self.lib.sagips_set_timing(self.h, 1 if enable else 0))
+
+    def kernel_times(self) -> Dict[str, tuple]:
+        """{kernel name: (launches, total ms)} since the last call; syncs the stream."""
+        cap = 64
+        names = (ctypes.c_char_p * cap)()
+        launches = (ctypes.c_int64 * cap)()
+        ms = (ctypes.c_double * cap)()
+        n = self.lib.sagips_kernel_times(self.h, names, launches, ms, cap)
+        if n < 0:
+            self._check(n)
+        return {names[i].decode(): (int(launches[i]), float(ms[i])) for i in range(min(n, cap))}
+
+    def source(self, theta, events_per_theta: int, seed: int, counter_base: int = 0, stream: int = 0) -> Source:
+        import torch
+        _check_tensor(theta, "theta", torch.float32, device=self.device)
+        if theta.dim() != 2 or theta.shape[1] not in (4, 6):
+            raise ValueError("theta must be [n_theta][4] or [n_theta][6]")
+        return Source(theta.data_ptr(), theta.shape[0], theta.shape[1] // 2, int(events_per_theta), int(seed),
+                      int(counter_base), int(stream))
+
+    # -- 1. parameters -> events ---------------------------------------------------
+    def sample_events(self, theta, events_per_theta: int, seed: int, counter_base: int = 0, stream: int = 0,
+                      want_x: bool = True, want_words: bool = False, out=None, words_out=None):
+        """Events [N][d] fp32 (and optionally the raw Philox words [N][4] int32)."""
+        import torch
+        src = self.source(theta, events_per_theta, seed, counter_base, stream)
+        N = src.n_theta * src.events_per_theta
+        x = None
+        w = None
+        if want_x:
+            x = out if out is not None else torch.empty((N, src.d), dtype=torch.float32, device=theta.device)
+            _check_tensor(x, "out", torch.float32, (N, src.d), self.device)
+        if want_words:
+            w = words_out if words_out is not None else torch.empty((N, 4), dtype=torch.int32, device=theta.device)
+            _check_tensor(w, "words_out", torch.int32, (N, 4), self.device)
+        self._check(self.lib.sagips_sample_events(self.h, ctypes.byref(src), _ptr(x), _ptr(w)))
+        self._keep = (theta,)
+        if want_words and want_x:
+            return x, w
+        return x if want_x else w
+
+    # -- 2. events -> discriminator -> BCE -> backward -------------------------------
+    def disc_fwd_bwd(self, W: Sequence, b: Sequence, real_x, fake_x=None, fake_source: Optional[dict] = None,
+                     precision: int = F32, features: int = FEAT_IDENTITY, slope: float = 0.2,
+                     want_logits: bool = True, want_grads: bool = True, want_dx: bool = True,
+                     want_dtheta: bool = True, outputs: Optional[dict] = None) -> dict:
+        """One discriminator step.  fake_source = dict(theta=, events_per_theta=, seed=[, counter_base=, stream=])
+        samples the fake events inside the kernel and also returns dLg_dtheta."""
+        import torch
+        n_layers = len(W)
+        if n_layers != len(b) or not 1 <= n_layers <= MAX_LAYERS:
+            raise ValueError("W and b must have the same length, 1..8")
+        widths = [W[0].shape[1]] + [w.shape[0] for w in W]
+        mlp = Mlp()
+        mlp.n_layers = n_layers
+        for i, wd in enumerate(widths):
+            mlp.width[i] = wd
+        for l in range(n_layers):
+            _check_tensor(W[l], f"W[{l}]", torch.float32, (widths[l + 1], widths[l]), self.device)
+            _check_tensor(b[l], f"b[{l}]", torch.float32, (widths[l + 1],), self.device)
+            mlp.W[l] = W[l].data_ptr()
+            mlp.b[l] = b[l].data_ptr()
+        mlp.leaky_slope = float(slope)
+        mlp.precision = int(precision)
+        mlp.features = int(features)
+        dev = real_x.device
+        _check_tensor(real_x, "real_x", torch.float32, device=self.device)
+        src = None
+        if fake_source is not None:
+            fs = dict(fake_source)
+            src = self.source(fs.pop("theta"), fs.pop("events_per_theta"), fs.pop("seed"), **fs)
+            n_fake = src.n_theta * src.events_per_theta
+            d = src.d
+        elif fake_x is not None:
+            _check_tensor(fake_x, "fake_x", torch.float32, device=self.device)
+            n_fake = fake_x.shape[0]
+            d = fake_x.shape[1]
+        else:                       # no fake input: the library rejects the call
+            n_fake, d = 0, widths[0]
+        n_real = real_x.shape[0]
+        d_in = 3 if features == FEAT_HD8 else widths[0]
+        if (fake_x is not None and d != d_in) or real_x.dim() != 2 or real_x.shape[1] != d_in:
+            raise ValueError(f"events must be [n][{d_in}] for this network and feature map")
+        o = dict(outputs or {})
+        f32 = dict(dtype=torch.float32, device=dev)
+        if want_logits:
+            o.setdefault("logits_fake", torch.empty(max(n_fake, 1), **f32))
+            o.setdefault("logits_real", torch.empty(n_real, **f32))
+        o.setdefault("loss_d", torch.empty(1, **f32))
+        o.setdefault("loss_g", torch.empty(1, **f32))
+        if want_grads:
+            o.setdefault("dW", [torch.empty_like(w) for w in W])
+            o.setdefault("db", [torch.empty_like(v) for v in b])
+        if want_dx:
+            o.setdefault("dLg_dx", torch.empty((max(n_fake, 1), d), **f32))
+        if want_dtheta and src is not None:
+            o.setdefault("dLg_dtheta", torch.empty((src.n_theta, 2 * src.d), **f32))
+        out = DiscOut()
+        for k in ("logits_fake", "logits_real", "loss_d", "loss_g", "dLg_dx", "dLg_dtheta"):
+            if o.get(k) is not None:
+                _check_tensor(o[k], k, torch.float32, device=self.device)
+                setattr(out, k, o[k].data_ptr())
+        if "dW" in o:
+            for l in range(n_layers):
+                out.dW[l] = o["dW"][l].data_ptr()
+                out.db[l] = o["db"][l].data_ptr()
+        st = self.lib.sagips_disc_fwd_bwd(self.h, ctypes.byref(mlp), _ptr(fake_x),
+                                          ctypes.byref(src) if src is not None else None, n_fake,
+                                          real_x.data_ptr(), n_real, ctypes.byref(out))
+        self._check(st)
+        return o
+
+    # -- 3. dL/dx -> pathwise dx/dtheta -> per-parameter reduction ---------------------------
+    def param_grad(self, theta, events_per_theta: int, seed: int, dL_dx=None, counter_base: int = 0,
+                   stream: int = 0, out=None, loss_out=None, want_loss: bool = True):
+        """dL/dtheta [n_theta][2d]; with dL_dx None the quadratic critic is used and its loss returned too."""
+        import torch
+        src = self.source(theta, events_per_theta, seed, counter_base, stream)
+        g = out if out is not None else torch.empty((src.n_theta, 2 * src.d), dtype=torch.float32, device=theta.device)
+        _check_tensor(g, "out", torch.float32, (src.n_theta, 2 * src.d), self.device)
+        loss = None
+        if dL_dx is None:
+            critic = CRITIC_QUADRATIC
+            if want_loss:
+                loss = loss_out if loss_out is not None else torch.empty(1, dtype=torch.float32, device=theta.device)
+        else:
+            critic = CRITIC_BUFFER
+            _check_tensor(dL_dx, "dL_dx", torch.float32, (src.n_theta * src.events_per_theta, src.d), self.device)
+        self._check(self.lib.sagips_param_grad(self.h, ctypes.byref(src), critic, _ptr(dL_dx), g.data_ptr(),
+                                               _ptr(loss)))
+        return (g, loss) if critic == CRITIC_QUADRATIC else g
+
+
+_default: Dict[int, Context] = {}
+
+
+def default_context(device: int = 0) -> Context:
+    if device not in _default:
+        _default[device] = Context(device)
+    return _default[device]
+
+
+def sample_events(theta, events_per_theta: int, seed: int, **kw):
+    return default_context(theta.device.index).sample_events(theta, events_per_theta, seed, **kw)
+
+
+def disc_fwd_bwd(W, b, real_x, **kw):
+    return default_context(real_x.device.index).disc_fwd_bwd(W, b, real_x, **kw)
+
+
+def param_grad(theta, events_per_theta: int, seed: int, **kw):
+    return default_context(theta.device.index).param_grad(theta, events_per_theta, seed, **kw)

@@ -1,0 +1,644 @@
+// Fused fp32 discriminator step on gfx950: forward on fake and real events,
+// BCE loss, backward to the weights (dL_D) and to the fake events (dL_G),
+// and, when the fake events come from a source, the sampler and the
+// per-parameter reduction as well -- one persistent kernel per call.
+//
+// Network: F -> H -> (H -> H) x NH -> 1, LeakyReLU on the hidden layers
+// (paper Sec. V-A), weights in torch.nn.Linear layout.
+//
+// Work decomposition
+//   * One workgroup (4 waves) per CU loops over tiles of T = 64 events; a
+//     tile is all fake or all real.  The tile's activations A_1..A_{NH+1} and
+//     one spare buffer live in LDS as [T][H+4] fp32 (event-major, padded so
+//     that the 16-byte fragment reads below are bank-conflict free).
+//   * The H x H products run on the fp32 matrix cores
+//     (v_mfma_f32_16x16x4_f32).  Forward and backward-data products compute
+//     out^T = W' * in^T with M = output feature, N = event, K = input
+//     feature; wave w owns output features [w H/4, (w+1) H/4).  The W'
+//     fragment of lane l is 4 consecutive K values of one row, a 16-byte
+//     load from global memory (L2-resident); the activation fragment is the
+//     matching 16 bytes of one event's row in LDS.  Because the K order of a
+//     product is free, this one mapping serves all four K steps of a load.
+//     Backward-data products use a transposed copy of W made per call.
+//   * Weight gradients dW = sum_events e * delta^T A (K = events) accumulate
+//     in registers across all of the workgroup's tiles: wave w owns rows
+//     [w H/4, (w+1) H/4) of every hidden dW.  They are written once per
+//     workgroup and summed over workgroups in a fixed order afterwards.
+//   * One backward chain with a unit seed per event serves both losses: the
+//     signals are linear in the seed, so dL_D terms are scaled by
+//     e_D = dL_D/dz and the fake-input gradient by e_G = dL_G/dz.
+//   * The first layer (K = F) and the logit layer (N = 1) are plain VALU work.
+#include "device_math.hpp"
+#include "kernels.hpp"
+
+#include <string.h>
+
+namespace sagips {
+namespace {
+
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int kThreads = 256;
+constexpr int kT = 64;         // events per tile
+constexpr int kMaxNH = 4;
+
+struct F32Params {
+  // network
+  const float* W1;             // [H][F]
+  const float* b1;             // [H]
+  const float* Wh[kMaxNH];     // [H][H]
+  const float* WhT[kMaxNH];    // [H][H] transposed copies
+  const float* bh[kMaxNH];     // [H]
+  const float* Wo;             // [H]
+  const float* bo;             // [1]
+  float slope;
+  // inputs
+  const float* fake_x;         // [n_fake][F] or NULL (then sampled)
+  const float* real_x;         // [n_real][F]
+  SourceArgs src;              // valid when fake_x == NULL
+  int64_t n_fake, n_real;
+  int n_fake_tiles, n_tiles;
+  int tiles_per_row;           // E / T for the source path
+  float inv_nf, inv_nr;
+  // outputs
+  float* logits_fake;
+  float* logits_real;
+  float* dLg_dx;               // [n_fake][F] or NULL
+  // workspace
+  float* wg_part;              // [gridDim.x][P]
+  float* loss_part;            // [n_tiles][2]
+  float* theta_part;           // [n_fake_tiles][2F] (source path)
+};
+
+__device__ __forceinline__ f32x4 mfma4(float a, float b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
+}
+
+__device__ __forceinline__ float leaky(float v, float s) { return v > 0.0f ? v : s * v; }
+__device__ __forceinline__ float leaky_grad(float h, float s) { return h > 0.0f ? 1.0f : s; }
+
+__device__ __forceinline__ float softplus(float t) { return fmaxf(t, 0.0f) + log1pf(expf(-fabsf(t))); }
+
+template <int H, int NH, int F>
+struct Fused {
+  static constexpr int LD = H + 4;             // LDS row stride in floats
+  static constexpr int NB = NH + 2;            // activation + spare buffers
+  static constexpr int RB = H / 64;            // 16-row blocks per wave
+  static constexpr int CB = kT / 16;           // 16-event column blocks
+  static constexpr int KB = H / 16;            // 16-wide K blocks
+  static constexpr int PPO = kThreads / H;     // threads per output feature in VALU loops
+  // per-workgroup partial layout (floats)
+  static constexpr int P_DWH = H * H + H;      // dW + db of one hidden layer
+  static constexpr int OFF_W1 = NH * P_DWH;    // dW1 [H][F], then db1 [H]
+  static constexpr int OFF_WO = OFF_W1 + H * F + H;  // dWo [H], then dbo
+  static constexpr int P = OFF_WO + H + 1;
+
+  struct Smem {
+    float act[NB][kT][LD];
+    float X[kT][F];
+    float dxd[kT][F][2];
+    float eD[kT];
+    float eG[kT];
+    float red[2 * kT * 4];   // >= kThreads and >= 2 T F
+  };
+
+  // Index of the buffer that holds delta_l (l = 1 .. NH+1).
+  static constexpr __device__ int dbuf(int l) { return NH + ((NH + 1 - l) & 1); }
+
+  // out^T (this wave's RB x CB fragments) = Wg * in^T, K = H.
+  static __device__ __forceinline__ void gemm(const float* __restrict__ Wg, const float* in, f32x4 (&acc)[RB][CB],
+                                              int o0, int lr, int lg) {
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+      for (int cb = 0; cb < CB; ++cb) acc[rb][cb] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int kb = 0; kb < KB; ++kb) {
+      f32x4 a[RB], b[CB];
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb)
+        a[rb] = *reinterpret_cast<const f32x4*>(Wg + (o0 + 16 * rb + lr) * H + 16 * kb + 4 * lg);
+#pragma unroll
+      for (int cb = 0; cb < CB; ++cb)
+        b[cb] = *reinterpret_cast<const f32x4*>(in + (16 * cb + lr) * LD + 16 * kb + 4 * lg);
+#pragma unroll
+      for (int s = 0; s < 4; ++s)
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+          for (int cb = 0; cb < CB; ++cb) acc[rb][cb] = mfma4(a[rb][s], b[cb][s], acc[rb][cb]);
+    }
+  }
+
+  // accW += sum_ev e[ev] * delta[ev][o] * A[ev][k] over the tile, o in this wave's rows.
+  static __device__ __forceinline__ void wgrad(const float* dlt, const float* A, const float* e,
+                                               f32x4 (&accW)[RB][KB], int o0, int lr, int lg) {
+#pragma unroll 4
+    for (int q = 0; q < kT / 4; ++q) {
+      const int ev = 4 * q + lg;
+      const float ee = e[ev];
+      float a[RB], b[KB];
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb) a[rb] = ee * dlt[ev * LD + o0 + 16 * rb + lr];
+#pragma unroll
+      for (int kb = 0; kb < KB; ++kb) b[kb] = A[ev * LD + 16 * kb + lr];
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+        for (int kb = 0; kb < KB; ++kb) accW[rb][kb] = mfma4(a[rb], b[kb], accW[rb][kb]);
+    }
+  }
+
+  static __device__ void run(const F32Params& p) {
+    __shared__ Smem sm;
+    const int tid = threadIdx.x;
+    const int lane = tid & 63, wave = tid >> 6;
+    const int lr = lane & 15, lg = lane >> 4;
+    const int o0 = wave * (H / 4);
+    const float slope = p.slope;
+
+    f32x4 accW[NH][RB][KB];
+#pragma unroll
+    for (int l = 0; l < NH; ++l)
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+        for (int kb = 0; kb < KB; ++kb) accW[l][rb][kb] = f32x4{0.f, 0.f, 0.f, 0.f};
+    // VALU accumulators: thread (o = tid % H, part = tid / H) over events ev = part (mod PPO)
+    const int vo = tid % H, vpart = tid / H;
+    float acc_dbh[NH];
+#pragma unroll
+    for (int l = 0; l < NH; ++l) acc_dbh[l] = 0.f;
+    float acc_dW1[F];
+#pragma unroll
+    for (int j = 0; j < F; ++j) acc_dW1[j] = 0.f;
+    float acc_db1 = 0.f, acc_dWo = 0.f, acc_dbo = 0.f;
+    float w1r[F];
+#pragma unroll
+    for (int j = 0; j < F; ++j) w1r[j] = p.W1[vo * F + j];
+    const float b1r = p.b1[vo];
+
+    for (int tile = blockIdx.x; tile < p.n_tiles; tile += gridDim.x) {
+      const bool fake = tile < p.n_fake_tiles;
+      const int64_t ev0 = (int64_t)(fake ? tile : tile - p.n_fake_tiles) * kT;
+      const int64_t n_here = fake ? p.n_fake : p.n_real;
+      const bool sampled = fake && p.fake_x == nullptr;
+
+      // ---- 1. tile inputs ---------------------------------------------------
+      if (tid < kT) {
+        const int64_t i = ev0 + tid;
+        const bool valid = i < n_here;
+        if (sampled) {
+          // E is a multiple of T here, so the whole tile uses one parameter row.
+          const int row = tile / p.tiles_per_row;
+          const Words w = event_words(p.src.base + (uint64_t)i, p.src.stream, p.src.k0, p.src.k1);
+#pragma unroll
+          for (int j = 0; j < F; ++j) {
+            const Shape sh = make_shape(p.src.theta[row * 2 * F + 2 * j], p.src.theta[row * 2 * F + 2 * j + 1]);
+            const Quantile q = kumaraswamy(uniform_u(w.w[j]), sh);
+            float da, db;
+            pathwise(q, sh, da, db);
+            sm.X[tid][j] = q.x;
+            sm.dxd[tid][j][0] = da;
+            sm.dxd[tid][j][1] = db;
+          }
+        } else {
+          const float* src = fake ? p.fake_x : p.real_x;
+#pragma unroll
+          for (int j = 0; j < F; ++j) sm.X[tid][j] = valid ? src[i * F + j] : 0.5f;
+        }
+      }
+      __syncthreads();
+
+      // ---- 2. first layer (VALU): A_1 = leaky(X W1^T + b1) -------------------
+      for (int ev = vpart; ev < kT; ev += PPO) {
+        float v = b1r;
+#pragma unroll
+        for (int j = 0; j < F; ++j) v = fmaf(w1r[j], sm.X[ev][j], v);
+        sm.act[0][ev][vo] = leaky(v, slope);
+      }
+      __syncthreads();
+
+      // ---- 3. hidden layers on the matrix cores -----------------------------
+#pragma unroll
+      for (int l = 0; l < NH; ++l) {
+        f32x4 acc[RB][CB];
+        gemm(p.Wh[l], &sm.act[l][0][0], acc, o0, lr, lg);
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb) {
+          const int o = o0 + 16 * rb + 4 * lg;
+          const f32x4 bias = *reinterpret_cast<const f32x4*>(p.bh[l] + o);
+#pragma unroll
+          for (int cb = 0; cb < CB; ++cb) {
+            f32x4 v = acc[rb][cb] + bias;
+            v.x = leaky(v.x, slope); v.y = leaky(v.y, slope);
+            v.z = leaky(v.z, slope); v.w = leaky(v.w, slope);
+            *reinterpret_cast<f32x4*>(&sm.act[l + 1][16 * cb + lr][o]) = v;
+          }
+        }
+        __syncthreads();
+      }
+
+      // ---- 4. logits and BCE seeds ------------------------------------------
+      {
+        // thread (ev = tid / 4, part = tid % 4) sums H/4 features
+        const int ev = tid >> 2, part = tid & 3;
+        const float* hrow = &sm.act[NH][ev][part * (H / 4)];
+        const float* wo = p.Wo + part * (H / 4);
+        float z = 0.f;
+#pragma unroll
+        for (int k = 0; k < H / 4; k += 4) {
+          const f32x4 hv = *reinterpret_cast<const f32x4*>(hrow + k);
+          const f32x4 wv = *reinterpret_cast<const f32x4*>(wo + k);
+          z = fmaf(hv.x, wv.x, z); z = fmaf(hv.y, wv.y, z);
+          z = fmaf(hv.z, wv.z, z); z = fmaf(hv.w, wv.w, z);
+        }
+        z += __shfl_xor(z, 1, 64);
+        z += __shfl_xor(z, 2, 64);
+        z += p.bo[0];
+        const int64_t i = ev0 + ev;
+        const bool valid = i < n_here;
+        float l0 = 0.f, l1 = 0.f;
+        if (part == 0) {
+          float eD = 0.f, eG = 0.f;
+          if (valid) {
+            const float sig_neg = 1.0f / (1.0f + expf(z));   // sigmoid(-z)
+            if (fake) {
+              eD = (1.0f - sig_neg) * p.inv_nf;                // dL_D/dz = sigmoid(z)/N_f
+              eG = -sig_neg * p.inv_nf;                        // dL_G/dz = (sigmoid(z)-1)/N_f
+              l0 = softplus(z);
+              l1 = softplus(-z);
+              if (p.logits_fake) p.logits_fake[i] = z;
+            } else {
+              eD = -sig_neg * p.inv_nr;                        // (sigmoid(z)-1)/N_r
+              l0 = softplus(-z);
+              if (p.logits_real) p.logits_real[i] = z;
+            }
+          }
+          sm.eD[ev] = eD;
+          sm.eG[ev] = eG;
+        }
+        l0 = wave_sum(l0);
+        l1 = wave_sum(l1);
+        if (lane == 0) { sm.red[2 * wave] = l0; sm.red[2 * wave + 1] = l1; }
+      }
+      __syncthreads();
+      if (tid < 2) {
+        float s = 0.f;
+#pragma unroll
+        for (int w = 0; w < kThreads / 64; ++w) s += sm.red[2 * w + tid];
+        p.loss_part[(int64_t)tile * 2 + tid] = s;
+      }
+
+      // ---- 5. logit-layer gradients; delta_{NH+1} in place --------------------
+      for (int ev = vpart; ev < kT; ev += PPO) {
+        const float e = sm.eD[ev];
+        acc_dWo = fmaf(e, sm.act[NH][ev][vo], acc_dWo);
+        if (vo == 0) acc_dbo += e;
+      }
+      __syncthreads();
+      {
+        const float wo = p.Wo[vo];
+        for (int ev = vpart; ev < kT; ev += PPO) {
+          float& h = sm.act[NH][ev][vo];
+          h = wo * leaky_grad(h, slope);
+        }
+      }
+      __syncthreads();
+
+      // ---- 6. hidden layers backward ------------------------------------------
+#pragma unroll
+      for (int l = NH - 1; l >= 0; --l) {
+        // layer l maps A_{l+1} (act[l]) -> A_{l+2}; its output signal is delta_{l+2}
+        const float* dout = &sm.act[dbuf(l + 2)][0][0];
+        float* din = &sm.act[dbuf(l + 1)][0][0];
+        const float* Ain = &sm.act[l][0][0];
+        wgrad(dout, Ain, sm.eD, accW[l], o0, lr, lg);
+        for (int ev = vpart; ev < kT; ev += PPO) acc_dbh[l] = fmaf(sm.eD[ev], dout[ev * LD + vo], acc_dbh[l]);
+        f32x4 acc[RB][CB];
+        gemm(p.WhT[l], dout, acc, o0, lr, lg);
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb) {
+          const int k = o0 + 16 * rb + 4 * lg;
+#pragma unroll
+          for (int cb = 0; cb < CB; ++cb) {
+            const int ev = 16 * cb + lr;
+            const f32x4 h = *reinterpret_cast<const f32x4*>(Ain + ev * LD + k);
+            f32x4 v = acc[rb][cb];
+            v.x *= leaky_grad(h.x, slope); v.y *= leaky_grad(h.y, slope);
+            v.z *= leaky_grad(h.z, slope); v.w *= leaky_grad(h.w, slope);
+            *reinterpret_cast<f32x4*>(din + ev * LD + k) = v;
+          }
+        }
+        __syncthreads();
+      }
+
+      // ---- 7. first-layer gradients --------------------------------------------
+      const float* d1 = &sm.act[dbuf(1)][0][0];
+      for (int ev = vpart; ev < kT; ev += PPO) {
+        const float ed = sm.eD[ev] * d1[ev * LD + vo];
+        acc_db1 += ed;
+#pragma unroll
+        for (int j = 0; j < F; ++j) acc_dW1[j] = fmaf(ed, sm.X[ev][j], acc_dW1[j]);
+      }
+
+      // ---- 8. fake events: dL_G/dx and the per-parameter partial ---------------
+      if (fake) {
+        float ta = 0.f, tb = 0.f;
+        int jj = 0;
+        if (tid < kT * F) {
+          const int ev = tid / F;
+          jj = tid % F;
+          float g = 0.f;
+          const float* drow = d1 + ev * LD;
+#pragma unroll 8
+          for (int o = 0; o < H; ++o) g = fmaf(drow[o], p.W1[o * F + jj], g);
+          g *= sm.eG[ev];
+          const int64_t i = ev0 + ev;
+          if (p.dLg_dx && i < n_here) p.dLg_dx[i * F + jj] = g;
+          if (sampled) {
+            ta = g * sm.dxd[ev][jj][0];
+            tb = g * sm.dxd[ev][jj][1];
+          }
+        }
+        if (sampled) {
+          __syncthreads();
+          if (tid < kT * F) {
+            sm.red[2 * tid] = ta;
+            sm.red[2 * tid + 1] = tb;
+          }
+          __syncthreads();
+          if (tid < 2 * F) {
+            // component c = 2 j + (a|b); terms stored at red[2 (ev F + j) + ab]
+            const int j = tid >> 1, ab = tid & 1;
+            float s = 0.f;
+            for (int ev = 0; ev < kT; ++ev) s += sm.red[2 * (ev * F + j) + ab];
+            p.theta_part[(int64_t)tile * 2 * F + tid] = s;
+          }
+        }
+        (void)jj;
+      }
+      __syncthreads();
+    }
+
+    // ---- per-workgroup partials ------------------------------------------------
+    float* out = p.wg_part + (int64_t)blockIdx.x * P;
+#pragma unroll
+    for (int l = 0; l < NH; ++l)
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+        for (int kb = 0; kb < KB; ++kb)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int o = o0 + 16 * rb + 4 * lg + r, k = 16 * kb + lr;
+            out[l * P_DWH + o * H + k] = accW[l][rb][kb][r];
+          }
+    // VALU partials: combine the PPO parts of each feature in a fixed order
+    float* red = &sm.act[0][0][0];
+    constexpr int NV = NH + F + 2;  // dbh[NH], dW1[F], db1, dWo per feature
+    __syncthreads();
+#pragma unroll
+    for (int l = 0; l < NH; ++l) red[(0 * NV + l) * kThreads + tid] = acc_dbh[l];
+#pragma unroll
+    for (int j = 0; j < F; ++j) red[(NH + j) * kThreads + tid] = acc_dW1[j];
+    red[(NH + F) * kThreads + tid] = acc_db1;
+    red[(NH + F + 1) * kThreads + tid] = acc_dWo;
+    red[NV * kThreads + tid] = acc_dbo;
+    __syncthreads();
+    if (tid < H) {
+      float v[NV];
+#pragma unroll
+      for (int c = 0; c < NV; ++c) {
+        float s = 0.f;
+        for (int q = 0; q < PPO; ++q) s += red[c * kThreads + q * H + tid];
+        v[c] = s;
+      }
+#pragma unroll
+      for (int l = 0; l < NH; ++l) out[l * P_DWH + H * H + tid] = v[l];
+#pragma unroll
+      for (int j = 0; j < F; ++j) out[OFF_W1 + tid * F + j] = v[NH + j];
+      out[OFF_W1 + H * F + tid] = v[NH + F];
+      out[OFF_WO + tid] = v[NH + F + 1];
+    }
+    if (tid == 0) {
+      float s = 0.f;
+      for (int q = 0; q < kThreads; ++q) s += red[NV * kThreads + q];
+      out[OFF_WO + H] = s;
+    }
+  }
+};
+
+template <int H, int NH, int F>
+__global__ __launch_bounds__(kThreads, 1) void k_disc_f32(F32Params p) {
+  Fused<H, NH, F>::run(p);
+}
+
+// WT[k][o] = W[o][k] for one H x H layer.
+__global__ __launch_bounds__(256) void k_transpose(const float* __restrict__ W, float* __restrict__ WT, int H) {
+  __shared__ float t[32][33];
+  const int bx = blockIdx.x * 32, by = blockIdx.y * 32;
+  const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;
+  for (int r = ty; r < 32; r += 8) t[r][tx] = W[(by + r) * H + bx + tx];
+  __syncthreads();
+  for (int r = ty; r < 32; r += 8) WT[(bx + r) * H + by + tx] = t[tx][r];
+}
+
+// Fixed-order sum over workgroups of every partial element, scattered to the
+// caller's gradient arrays through a segment table.
+struct Segments {
+  int n;
+  int off[2 * kMaxNH + 4];
+  int len[2 * kMaxNH + 4];
+  float* dst[2 * kMaxNH + 4];
+};
+
+__global__ __launch_bounds__(256) void k_reduce_wg(const float* __restrict__ part, int n_wg, int P, Segments sg) {
+  const int e = blockIdx.x * 256 + threadIdx.x;
+  if (e >= P) return;
+  float s = 0.f;
+  for (int g = 0; g < n_wg; ++g) s += part[(int64_t)g * P + e];
+  for (int i = 0; i < sg.n; ++i)
+    if (e >= sg.off[i] && e < sg.off[i] + sg.len[i]) {
+      if (sg.dst[i]) sg.dst[i][e - sg.off[i]] = s;
+      break;
+    }
+}
+
+// Losses from the per-tile partial sums (one block, fixed order).
+__global__ __launch_bounds__(256) void k_reduce_loss(const float* __restrict__ loss_part, int n_fake_tiles,
+                                                     int n_tiles, float inv_nf, float inv_nr,
+                                                     float* __restrict__ loss_d, float* __restrict__ loss_g) {
+  __shared__ float red[3][4];
+  float sf = 0.f, sg = 0.f, sr = 0.f;
+  for (int t = threadIdx.x; t < n_tiles; t += 256) {
+    if (t < n_fake_tiles) { sf += loss_part[2 * t]; sg += loss_part[2 * t + 1]; }
+    else sr += loss_part[2 * t];
+  }
+  sf = wave_sum(sf); sg = wave_sum(sg); sr = wave_sum(sr);
+  if ((threadIdx.x & 63) == 0) {
+    red[0][threadIdx.x >> 6] = sf; red[1][threadIdx.x >> 6] = sg; red[2][threadIdx.x >> 6] = sr;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    float a = 0.f, b = 0.f, c = 0.f;
+    for (int w = 0; w < 4; ++w) { a += red[0][w]; b += red[1][w]; c += red[2][w]; }
+    if (loss_d) *loss_d = c * inv_nr + a * inv_nf;
+    if (loss_g) *loss_g = b * inv_nf;
+  }
+}
+
+// dL_G/dtheta[row][c] = fixed-order sum of the row's tile partials.
+__global__ __launch_bounds__(64) void k_reduce_theta(const float* __restrict__ theta_part, int tiles_per_row, int C,
+                                                     float* __restrict__ out) {
+  const int row = blockIdx.x;
+  const int c = threadIdx.x;
+  if (c >= C) return;
+  float s = 0.f;
+  for (int t = 0; t < tiles_per_row; ++t) s += theta_part[((int64_t)row * tiles_per_row + t) * C + c];
+  out[row * C + c] = s;
+}
+
+inline size_t align256(size_t b) { return (b + 255) & ~(size_t)255; }
+
+struct Layout {
+  int H, NH, F, P;
+  size_t off_wt, off_wg, off_loss, off_theta, total;
+};
+
+template <int H, int NH, int F>
+Layout layout_for(const DiscArgs& a, int n_wg) {
+  using K = Fused<H, NH, F>;
+  Layout L;
+  L.H = H; L.NH = NH; L.F = F; L.P = K::P;
+  const int64_t nft = (a.n_fake + kT - 1) / kT, nrt = (a.n_real + kT - 1) / kT;
+  size_t o = 0;
+  L.off_wt = o; o += align256(sizeof(float) * NH * H * H);
+  L.off_wg = o; o += align256(sizeof(float) * (size_t)n_wg * K::P);
+  L.off_loss = o; o += align256(sizeof(float) * 2 * (size_t)(nft + nrt));
+  L.off_theta = o; o += align256(sizeof(float) * 2 * F * (size_t)nft);
+  L.total = o;
+  return L;
+}
+
+typedef void (*KernelFn)(F32Params);
+
+struct Variant {
+  int H, NH, F;
+  KernelFn fn;
+  Layout (*layout)(const DiscArgs&, int);
+  int P;
+};
+
+#define SAGIPS_F32_VARIANT(H_, NH_, F_) \
+  { H_, NH_, F_, k_disc_f32<H_, NH_, F_>, layout_for<H_, NH_, F_>, Fused<H_, NH_, F_>::P }
+
+const Variant kVariants[] = {
+    SAGIPS_F32_VARIANT(64, 1, 2),  SAGIPS_F32_VARIANT(64, 2, 2),  SAGIPS_F32_VARIANT(64, 3, 2),
+    SAGIPS_F32_VARIANT(128, 1, 2), SAGIPS_F32_VARIANT(128, 2, 2),
+    SAGIPS_F32_VARIANT(64, 1, 3),  SAGIPS_F32_VARIANT(64, 2, 3),  SAGIPS_F32_VARIANT(128, 2, 3),
+};
+
+const Variant* find_variant(const sagips_mlp& D) {
+  const int H = D.width[1];
+  const int NH = D.n_layers - 2;
+  const int F = D.width[0];
+  for (const Variant& v : kVariants)
+    if (v.H == H && v.NH == NH && v.F == F) return &v;
+  return nullptr;
+}
+
+}  // namespace
+
+bool disc_f32_supported(const sagips_mlp& D, int d, const char** why) {
+  if (D.features != SAGIPS_FEAT_IDENTITY) { *why = "fp32 discriminator supports IDENTITY features only"; return false; }
+  if (D.width[0] != d) { *why = "width[0] must equal d for IDENTITY features"; return false; }
+  if (D.n_layers < 3) { *why = "fp32 discriminator needs at least one hidden-to-hidden layer"; return false; }
+  for (int l = 1; l < D.n_layers; ++l)
+    if (D.width[l] != D.width[1]) { *why = "all hidden widths must be equal"; return false; }
+  if (D.width[D.n_layers] != 1) { *why = "last layer must have width 1"; return false; }
+  if (!find_variant(D)) { *why = "unsupported fp32 shape (hidden width 64 with 1-3 or 128 with 1-2 hidden-to-hidden layers; d 2, or 3 with fewer layers)"; return false; }
+  return true;
+}
+
+size_t disc_f32_workspace(const DiscArgs& a, int n_cu) {
+  const Variant* v = find_variant(*a.D);
+  return v ? v->layout(a, n_cu).total : 0;
+}
+
+hipError_t launch_disc_f32(const DiscArgs& a, void* ws, int n_cu, hipStream_t st, Timer* tm) {
+  const Variant* v = find_variant(*a.D);
+  const sagips_mlp& D = *a.D;
+  const Layout L = v->layout(a, n_cu);
+  char* base = static_cast<char*>(ws);
+  float* WT = reinterpret_cast<float*>(base + L.off_wt);
+  const int H = v->H, NH = v->NH, F = v->F;
+
+  F32Params p;
+  memset(&p, 0, sizeof(p));
+  p.W1 = D.W[0];
+  p.b1 = D.b[0];
+  for (int l = 0; l < NH; ++l) {
+    p.Wh[l] = D.W[1 + l];
+    p.bh[l] = D.b[1 + l];
+    p.WhT[l] = WT + (size_t)l * H * H;
+  }
+  p.Wo = D.W[NH + 1];
+  p.bo = D.b[NH + 1];
+  p.slope = D.leaky_slope;
+  p.fake_x = a.fake_x;
+  p.real_x = a.real_x;
+  if (a.fake_src) p.src = *a.fake_src;
+  p.n_fake = a.n_fake;
+  p.n_real = a.n_real;
+  p.n_fake_tiles = (int)((a.n_fake + kT - 1) / kT);
+  p.n_tiles = p.n_fake_tiles + (int)((a.n_real + kT - 1) / kT);
+  p.tiles_per_row = a.fake_src ? (int)(a.fake_src->E / kT) : 0;
+  p.inv_nf = 1.0f / (float)a.n_fake;
+  p.inv_nr = 1.0f / (float)a.n_real;
+  p.logits_fake = a.out->logits_fake;
+  p.logits_real = a.out->logits_real;
+  p.dLg_dx = a.out->dLg_dx;
+  p.wg_part = reinterpret_cast<float*>(base + L.off_wg);
+  p.loss_part = reinterpret_cast<float*>(base + L.off_loss);
+  p.theta_part = reinterpret_cast<float*>(base + L.off_theta);
+
+  if (tm) tm->begin("disc_f32_transpose");
+  for (int l = 0; l < NH; ++l)
+    hipLaunchKernelGGL(k_transpose, dim3(H / 32, H / 32), dim3(256), 0, st, p.Wh[l], const_cast<float*>(p.WhT[l]), H);
+  if (tm) tm->end();
+  if (tm) tm->begin("disc_f32_fused");
+  hipLaunchKernelGGL(v->fn, dim3(n_cu), dim3(kThreads), 0, st, p);
+  if (tm) tm->end();
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+
+  if (tm) tm->begin("disc_f32_reduce");
+  if (a.out->dW[0]) {
+    Segments sg;
+    memset(&sg, 0, sizeof(sg));
+    int n = 0;
+    for (int l = 0; l < NH; ++l) {
+      sg.off[n] = l * (H * H + H); sg.len[n] = H * H; sg.dst[n++] = a.out->dW[1 + l];
+      sg.off[n] = l * (H * H + H) + H * H; sg.len[n] = H; sg.dst[n++] = a.out->db[1 + l];
+    }
+    const int offw1 = NH * (H * H + H);
+    sg.off[n] = offw1; sg.len[n] = H * F; sg.dst[n++] = a.out->dW[0];
+    sg.off[n] = offw1 + H * F; sg.len[n] = H; sg.dst[n++] = a.out->db[0];
+    const int offwo = offw1 + H * F + H;
+    sg.off[n] = offwo; sg.len[n] = H; sg.dst[n++] = a.out->dW[NH + 1];
+    sg.off[n] = offwo + H; sg.len[n] = 1; sg.dst[n++] = a.out->db[NH + 1];
+    sg.n = n;
+    hipLaunchKernelGGL(k_reduce_wg, dim3((L.P + 255) / 256), dim3(256), 0, st, p.wg_part, n_cu, L.P, sg);
+  }
+  if (a.out->loss_d || a.out->loss_g)
+    hipLaunchKernelGGL(k_reduce_loss, dim3(1), dim3(256), 0, st, p.loss_part, p.n_fake_tiles, p.n_tiles, p.inv_nf,
+                       p.inv_nr, a.out->loss_d, a.out->loss_g);
+  if (a.fake_src && a.out->dLg_dtheta)
+    hipLaunchKernelGGL(k_reduce_theta, dim3(a.fake_src->n_theta), dim3(64), 0, st, p.theta_part, p.tiles_per_row,
+                       2 * F, a.out->dLg_dtheta);
+  if (tm) tm->end();
+  return hipGetLastError();
+}
+
+}  // namespace sagips

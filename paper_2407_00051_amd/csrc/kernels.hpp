@@ -1,0 +1,67 @@
+// Internal launch interface between the C ABI (api.hip) and the kernel files.
+// Every launcher enqueues on `stream`, validates nothing (the ABI layer has
+// already done so) and returns the launch status.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "../../include/sagips.h"
+
+namespace sagips {
+
+// Records HIP events around one launch when timing is on (api.hip).
+struct Timer {
+  virtual ~Timer() = default;
+  virtual void begin(const char* name) = 0;
+  virtual void end() = 0;
+};
+
+struct SourceArgs {
+  const float* theta;
+  int n_theta;
+  int d;
+  int64_t E;
+  uint32_t k0, k1;
+  uint64_t base;
+  uint32_t stream;
+};
+
+inline SourceArgs source_args(const sagips_source& s) {
+  SourceArgs a;
+  a.theta = s.theta;
+  a.n_theta = s.n_theta;
+  a.d = s.d;
+  a.E = s.events_per_theta;
+  a.k0 = (uint32_t)(s.seed & 0xffffffffu);
+  a.k1 = (uint32_t)(s.seed >> 32);
+  a.base = s.counter_base;
+  a.stream = s.stream;
+  return a;
+}
+
+// sampler.hip ---------------------------------------------------------------
+hipError_t launch_sample(const SourceArgs& s, float* x, uint32_t* words, hipStream_t st, Timer* tm);
+
+// Bytes of workspace launch_param_grad needs.
+size_t param_grad_workspace(const SourceArgs& s);
+// dL/dx from a buffer (dLdx != NULL) or the quadratic critic (dLdx == NULL).
+hipError_t launch_param_grad(const SourceArgs& s, const float* dLdx, float* dLdtheta, float* loss,
+                             void* ws, hipStream_t st, Timer* tm);
+
+// disc_f32.hip ---------------------------------------------------------------
+struct DiscArgs {
+  const sagips_mlp* D;
+  const float* fake_x;         // or NULL with a source
+  const SourceArgs* fake_src;  // or NULL
+  int64_t n_fake;
+  const float* real_x;
+  int64_t n_real;
+  const sagips_disc_out* out;
+  int d;
+};
+bool disc_f32_supported(const sagips_mlp& D, int d, const char** why);
+size_t disc_f32_workspace(const DiscArgs& a, int n_cu);
+hipError_t launch_disc_f32(const DiscArgs& a, void* ws, int n_cu, hipStream_t st, Timer* tm);
+
+}  // namespace sagips

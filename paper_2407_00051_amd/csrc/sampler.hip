@@ -1,0 +1,199 @@
+// Event sampler and per-parameter gradient reduction on gfx950.
+//
+// Both kernels run on a 2D grid: blockIdx.y is the parameter row (so theta
+// and its reciprocals are wave-uniform scalars) and blockIdx.x a chunk of
+// kEPB consecutive events of that row.  Thread t of a chunk handles events
+// chunk*kEPB + t + j*256, j < kEPT, so every store is coalesced.
+#include "device_math.hpp"
+#include "kernels.hpp"
+
+namespace sagips {
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kEPT = 8;
+constexpr int kEPB = kThreads * kEPT;
+
+template <int D>
+__global__ __launch_bounds__(kThreads) void k_sample(SourceArgs s, float* __restrict__ x,
+                                                     uint32_t* __restrict__ words) {
+  const int row = blockIdx.y;
+  Shape sh[D];
+#pragma unroll
+  for (int j = 0; j < D; ++j) sh[j] = make_shape(s.theta[row * 2 * D + 2 * j], s.theta[row * 2 * D + 2 * j + 1]);
+  const int64_t k_first = (int64_t)blockIdx.x * kEPB + threadIdx.x;
+  const int64_t row_base = (int64_t)row * s.E;
+#pragma unroll 2
+  for (int e = 0; e < kEPT; ++e) {
+    const int64_t k = k_first + e * kThreads;
+    if (k >= s.E) break;
+    const int64_t i = row_base + k;
+    const Words w = event_words(s.base + (uint64_t)i, s.stream, s.k0, s.k1);
+    if (words) {
+      uint4 v;
+      v.x = w.w[0]; v.y = w.w[1]; v.z = w.w[2]; v.w = w.w[3];
+      reinterpret_cast<uint4*>(words)[i] = v;
+    }
+    if (x) {
+      float xv[D];
+#pragma unroll
+      for (int j = 0; j < D; ++j) xv[j] = kumaraswamy(uniform_u(w.w[j]), sh[j]).x;
+      if constexpr (D == 2) {
+        reinterpret_cast<float2*>(x)[i] = make_float2(xv[0], xv[1]);
+      } else {
+#pragma unroll
+        for (int j = 0; j < D; ++j) x[i * D + j] = xv[j];
+      }
+    }
+  }
+}
+
+// Per-chunk partial sums of dL/dtheta (2D values) and, for the quadratic
+// critic, of the loss: partial[(row * chunks + chunk) * (2D+1) + c].
+template <int D, bool kQuadratic>
+__global__ __launch_bounds__(kThreads) void k_param_grad(SourceArgs s, const float* __restrict__ dLdx,
+                                                         float* __restrict__ partial) {
+  constexpr int C = 2 * D + 1;
+  __shared__ float red[kThreads / 64][C];
+  const int row = blockIdx.y;
+  Shape sh[D];
+#pragma unroll
+  for (int j = 0; j < D; ++j) sh[j] = make_shape(s.theta[row * 2 * D + 2 * j], s.theta[row * 2 * D + 2 * j + 1]);
+  float acc[C];
+#pragma unroll
+  for (int c = 0; c < C; ++c) acc[c] = 0.0f;
+  const int64_t k_first = (int64_t)blockIdx.x * kEPB + threadIdx.x;
+  const int64_t row_base = (int64_t)row * s.E;
+#pragma unroll 2
+  for (int e = 0; e < kEPT; ++e) {
+    const int64_t k = k_first + e * kThreads;
+    if (k >= s.E) break;
+    const int64_t i = row_base + k;
+    const Words w = event_words(s.base + (uint64_t)i, s.stream, s.k0, s.k1);
+    float gx[D];
+    if constexpr (!kQuadratic) {
+      if constexpr (D == 2) {
+        const float2 v = reinterpret_cast<const float2*>(dLdx)[i];
+        gx[0] = v.x; gx[1] = v.y;
+      } else {
+#pragma unroll
+        for (int j = 0; j < D; ++j) gx[j] = dLdx[i * D + j];
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < D; ++j) {
+      const Quantile q = kumaraswamy(uniform_u(w.w[j]), sh[j]);
+      float da, db;
+      pathwise(q, sh[j], da, db);
+      float g;
+      if constexpr (kQuadratic) {
+        const float r = q.x - 0.5f;
+        g = 2.0f * r;
+        acc[2 * D] = fmaf(r, r, acc[2 * D]);
+      } else {
+        g = gx[j];
+      }
+      acc[2 * j] = fmaf(g, da, acc[2 * j]);
+      acc[2 * j + 1] = fmaf(g, db, acc[2 * j + 1]);
+    }
+  }
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+#pragma unroll
+  for (int c = 0; c < C; ++c) {
+    const float v = wave_sum(acc[c]);
+    if (lane == 0) red[wave][c] = v;
+  }
+  __syncthreads();
+  if (threadIdx.x < C) {
+    float v = 0.0f;
+#pragma unroll
+    for (int w = 0; w < kThreads / 64; ++w) v += red[w][threadIdx.x];
+    partial[((int64_t)row * gridDim.x + blockIdx.x) * C + threadIdx.x] = v;
+  }
+}
+
+// One block per row: fixed-order sum of the row's chunk partials.
+__global__ __launch_bounds__(kThreads) void k_reduce_rows(const float* __restrict__ partial, int chunks, int C,
+                                                          float* __restrict__ dLdtheta, float* __restrict__ row_loss,
+                                                          int has_loss) {
+  __shared__ float red[kThreads / 64];
+  const int row = blockIdx.x;
+  const float* p = partial + (int64_t)row * chunks * C;
+  for (int c = 0; c < C; ++c) {
+    if (c == C - 1 && !has_loss) break;
+    float v = 0.0f;
+    for (int k = threadIdx.x; k < chunks; k += kThreads) v += p[(int64_t)k * C + c];
+    v = wave_sum(v);
+    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      float t = 0.0f;
+      for (int w = 0; w < kThreads / 64; ++w) t += red[w];
+      if (c < C - 1) dLdtheta[row * (C - 1) + c] = t;
+      else row_loss[row] = t;
+    }
+    __syncthreads();
+  }
+}
+
+__global__ __launch_bounds__(kThreads) void k_reduce_loss(const float* __restrict__ row_loss, int n,
+                                                          float* __restrict__ loss) {
+  __shared__ float red[kThreads / 64];
+  float v = 0.0f;
+  for (int k = threadIdx.x; k < n; k += kThreads) v += row_loss[k];
+  v = wave_sum(v);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    float t = 0.0f;
+    for (int w = 0; w < kThreads / 64; ++w) t += red[w];
+    *loss = t;
+  }
+}
+
+inline int chunks_per_row(const SourceArgs& s) { return (int)((s.E + kEPB - 1) / kEPB); }
+
+}  // namespace
+
+hipError_t launch_sample(const SourceArgs& s, float* x, uint32_t* words, hipStream_t st, Timer* tm) {
+  const dim3 grid(chunks_per_row(s), s.n_theta);
+  if (tm) tm->begin("sample_events");
+  if (s.d == 2) hipLaunchKernelGGL(k_sample<2>, grid, dim3(kThreads), 0, st, s, x, words);
+  else hipLaunchKernelGGL(k_sample<3>, grid, dim3(kThreads), 0, st, s, x, words);
+  if (tm) tm->end();
+  return hipGetLastError();
+}
+
+size_t param_grad_workspace(const SourceArgs& s) {
+  const size_t C = 2 * s.d + 1;
+  return ((size_t)s.n_theta * chunks_per_row(s) * C + s.n_theta) * sizeof(float);
+}
+
+hipError_t launch_param_grad(const SourceArgs& s, const float* dLdx, float* dLdtheta, float* loss, void* ws,
+                             hipStream_t st, Timer* tm) {
+  const int chunks = chunks_per_row(s);
+  const int C = 2 * s.d + 1;
+  float* partial = static_cast<float*>(ws);
+  float* row_loss = partial + (size_t)s.n_theta * chunks * C;
+  const dim3 grid(chunks, s.n_theta);
+  const bool quad = (dLdx == nullptr);
+  if (tm) tm->begin("param_grad");
+  if (s.d == 2) {
+    if (quad) hipLaunchKernelGGL((k_param_grad<2, true>), grid, dim3(kThreads), 0, st, s, dLdx, partial);
+    else hipLaunchKernelGGL((k_param_grad<2, false>), grid, dim3(kThreads), 0, st, s, dLdx, partial);
+  } else {
+    if (quad) hipLaunchKernelGGL((k_param_grad<3, true>), grid, dim3(kThreads), 0, st, s, dLdx, partial);
+    else hipLaunchKernelGGL((k_param_grad<3, false>), grid, dim3(kThreads), 0, st, s, dLdx, partial);
+  }
+  if (tm) tm->end();
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  if (tm) tm->begin("param_grad_reduce");
+  hipLaunchKernelGGL(k_reduce_rows, dim3(s.n_theta), dim3(kThreads), 0, st, partial, chunks, C, dLdtheta, row_loss,
+                     quad ? 1 : 0);
+  if (quad && loss) hipLaunchKernelGGL(k_reduce_loss, dim3(1), dim3(kThreads), 0, st, row_loss, s.n_theta, loss);
+  if (tm) tm->end();
+  return hipGetLastError();
+}
+
+}  // namespace sagips

@@ -1,0 +1,85 @@
+"""C-ABI error paths, forced from the host: every invalid request returns the
+documented negative status and a message, launches nothing, never aborts."""
+import ctypes
+
+import pytest
+
+import paper_2407_00051_amd as sg
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+
+def _src(theta, n_theta=2, d=2, E=100):
+    return sg.Source(theta.data_ptr() if theta is not None else None, n_theta, d, E, 1, 0, 0)
+
+
+def test_sample_errors(gpu_ctx):
+    lib, h = gpu_ctx.lib, gpu_ctx.h
+    th = torch.ones((2, 4), device="cuda:0")
+    x = torch.empty((200, 2), device="cuda:0")
+    cases = [
+        (None, x.data_ptr(), sg.E_INVAL),                                  # NULL source
+        (_src(None), x.data_ptr(), sg.E_INVAL),                            # NULL theta
+        (_src(th, n_theta=0), x.data_ptr(), sg.E_INVAL),
+        (_src(th, d=4), x.data_ptr(), sg.E_INVAL),
+        (_src(th, E=0), x.data_ptr(), sg.E_INVAL),
+        (_src(th, E=2**31), x.data_ptr(), sg.E_INVAL),
+        (_src(th), None, sg.E_INVAL),                                      # nothing requested
+        (_src(th), x.data_ptr() + 4, sg.E_INVAL),                          # misaligned
+    ]
+    for src, xp, want in cases:
+        st = lib.sagips_sample_events(h, ctypes.byref(src) if src is not None else None, xp, None)
+        assert st == want
+        assert len(lib.sagips_last_error(h)) > 0
+    torch.cuda.synchronize()
+
+
+def test_param_grad_errors(gpu_ctx):
+    lib, h = gpu_ctx.lib, gpu_ctx.h
+    th = torch.ones((2, 4), device="cuda:0")
+    g = torch.empty((2, 4), device="cuda:0")
+    dx = torch.empty((200, 2), device="cuda:0")
+    loss = torch.empty(1, device="cuda:0")
+    src = _src(th)
+    assert lib.sagips_param_grad(h, ctypes.byref(src), sg.CRITIC_BUFFER, None, g.data_ptr(), None) == sg.E_INVAL
+    assert lib.sagips_param_grad(h, ctypes.byref(src), sg.CRITIC_QUADRATIC, dx.data_ptr(), g.data_ptr(), None) == sg.E_INVAL
+    assert lib.sagips_param_grad(h, ctypes.byref(src), sg.CRITIC_BUFFER, dx.data_ptr(), g.data_ptr(), loss.data_ptr()) == sg.E_INVAL
+    assert lib.sagips_param_grad(h, ctypes.byref(src), 7, None, g.data_ptr(), None) == sg.E_INVAL
+    assert lib.sagips_param_grad(h, ctypes.byref(src), sg.CRITIC_QUADRATIC, None, None, None) == sg.E_INVAL
+
+
+def test_disc_errors(gpu_ctx):
+    dev = "cuda:0"
+    W = [torch.zeros((64, 2), device=dev), torch.zeros((64, 64), device=dev), torch.zeros((1, 64), device=dev)]
+    b = [torch.zeros(64, device=dev), torch.zeros(64, device=dev), torch.zeros(1, device=dev)]
+    real = torch.full((128, 2), 0.5, device=dev)
+    fake = torch.full((128, 2), 0.5, device=dev)
+    th = torch.ones((1, 4), device=dev)
+    with pytest.raises(sg.SagipsError) as e:       # both fake inputs
+        gpu_ctx.disc_fwd_bwd(W, b, real, fake_x=fake, fake_source=dict(theta=th, events_per_theta=128, seed=0))
+    with pytest.raises(sg.SagipsError) as e:       # neither
+        gpu_ctx.disc_fwd_bwd(W, b, real)
+    assert e.value.status == sg.E_INVAL
+    with pytest.raises(sg.SagipsError) as e:       # unsupported hidden width
+        W2 = [torch.zeros((96, 2), device=dev), torch.zeros((96, 96), device=dev), torch.zeros((1, 96), device=dev)]
+        b2 = [torch.zeros(96, device=dev), torch.zeros(96, device=dev), torch.zeros(1, device=dev)]
+        gpu_ctx.disc_fwd_bwd(W2, b2, real, fake_x=fake)
+    assert e.value.status == sg.E_UNSUPPORTED
+    with pytest.raises(ValueError):                # events do not match width[0] (checked by the binding)
+        gpu_ctx.disc_fwd_bwd(W, b, torch.full((128, 3), 0.5, device=dev), fake_x=torch.full((128, 3), 0.5, device=dev))
+    with pytest.raises(sg.SagipsError) as e:       # fake source with d = 3 but width[0] = 2
+        gpu_ctx.disc_fwd_bwd(W, b, real, fake_source=dict(theta=torch.ones((1, 6), device=dev), events_per_theta=128, seed=0))
+    # the context still works afterwards
+    o = gpu_ctx.disc_fwd_bwd(W, b, real, fake_x=fake)
+    torch.cuda.synchronize()
+    assert abs(o["loss_d"].item() - 2 * 0.6931471805599453) < 1e-6
+
+
+def test_create_rejects_bad_device():
+    lib = sg.load_library()
+    h = ctypes.c_void_p()
+    assert lib.sagips_create(ctypes.byref(h), 999, None) == sg.E_INVAL
+    assert h.value is None
+    assert b"device" in lib.sagips_last_error(None)
