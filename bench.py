@@ -1,0 +1,217 @@
+#!/usr/bin/env python3
+"""Benchmark of one rank's SAGIPS step on one MI355X.
+
+A step is one pass of the whole hot path over one batch: theta -> Philox ->
+Kumaraswamy events (sampled inside the kernel) -> discriminator forward on the
+fake and the resident real batch -> BCE -> backward to the weights and to the
+events -> pathwise dx/dtheta -> per-parameter reduction dL_G/dtheta.
+
+Default workload: 32 parameter rows x 8,192 events (262,144 fake + 262,144
+real events), discriminator 2-128-128-128-1, fp32.  Prints one JSON line.
+
+  python bench.py [--steps K] [--warmup W] [--gpus 1] [--workload NAME]
+                  [--no-cpu-baseline] [--calibrate-copy]
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK = {"mfma_f32": 157.3e12, "mfma_bf16": 2.5e15, "hbm": 8.0e12}
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
+KERNEL_SOURCES = {
+    "disc_f32_fused": ["paper_2407_00051_amd/csrc/disc_f32.hip", "paper_2407_00051_amd/csrc/device_math.hpp"],
+    "param_grad": ["paper_2407_00051_amd/csrc/sampler.hip", "paper_2407_00051_amd/csrc/device_math.hpp"],
+}
+
+
+def source_hash(kernel: str) -> str:
+    h = hashlib.sha256()
+    for p in KERNEL_SOURCES[kernel]:
+        with open(os.path.join(ROOT, p), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def mlp_flops_per_fake_event(widths) -> int:
+    """Algorithmic flops of the discriminator per fake event (its real partner included).
+
+    With S = sum in*out MACs per sample: forward 2S on the fake and on the
+    real event; weight gradients 2S on each; backward signal 2S on the fake
+    event (down to dL/dx) and 2(S - F*H) on the real one (it stops at the
+    first layer's output).  Total 12S - 2FH."""
+    S = sum(a * b for a, b in zip(widths[:-1], widths[1:]))
+    return 12 * S - 2 * widths[0] * widths[1]
+
+
+def read_traffic(kernel: str, workload: str):
+    """HBM bytes per launch from the committed counter runs, or None if the kernel changed since."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            t = json.load(f)
+        e = t[kernel][workload]
+        if e.get("source_hash") != source_hash(kernel):
+            return None
+        return float(e["bytes_per_launch"])
+    except (OSError, KeyError, ValueError):
+        return None
+
+
+def cpu_baseline(w, inp, rows: int, events: int, min_seconds: float = 10.0):
+    """The float64 oracle, as it stands, on the first `rows` parameter rows of the workload."""
+    import numpy as np  # noqa: F401
+    import oracle
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        threads = os.cpu_count()
+    th = inp["theta"][:rows]
+    reps = 0
+    t0 = time.perf_counter()
+    while True:                      # repeat the sample until about min_seconds of CPU work
+        if w.widths is None:
+            oracle.run_step(th, events, w.fake_seed, critic="quadratic")
+        else:
+            real = oracle.sample(inp["theta_star"], rows * events, w.real_seed)
+            oracle.run_step(th, events, w.fake_seed, inp["W"], inp["b"], real,
+                            features=w.features, bf16=(w.precision == "bf16"))
+        reps += 1
+        dt = time.perf_counter() - t0
+        if dt >= min_seconds:
+            break
+    n = rows * events
+    return {"value": reps * n / dt, "unit": "events/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"{rows} of {w.n_theta} parameter rows x {events} events ({n} fake + "
+                      f"{n if w.widths else 0} real events), float64 numpy, {reps} repetition(s) in {dt:.1f} s"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="small")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-rows", type=int, default=32)
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="also run one 1 GiB device copy (for counter calibration runs)")
+    args = ap.parse_args()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(f"bench.py measures one GPU only: --gpus {args.gpus} / WORLD_SIZE {world} is not supported "
+              "(the multi-GPU exchange of the paper is not part of this library)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import paper_2407_00051_amd as sg
+    from workloads import gen, get
+
+    w = get(args.workload)
+    inp = gen.make_inputs(w)
+    dev = "cuda:0"
+    torch.cuda.set_device(0)
+    ctx = sg.Context(0)
+    theta = torch.tensor(inp["theta"], device=dev)
+    theta_star = torch.tensor(inp["theta_star"], device=dev)
+    N = w.n_events
+
+    if args.calibrate_copy:
+        a = torch.empty(1 << 28, dtype=torch.float32, device=dev)
+        b = torch.empty_like(a)
+        a.fill_(1.0)
+        torch.cuda.synchronize()
+        b.copy_(a)
+        torch.cuda.synchronize()
+        del a, b
+
+    if w.widths is not None:
+        W = [torch.tensor(m, device=dev) for m in inp["W"]]
+        bias = [torch.tensor(v, device=dev) for v in inp["b"]]
+        real = ctx.sample_events(theta_star, N, w.real_seed)          # resident real batch (untimed)
+        f32 = dict(dtype=torch.float32, device=dev)
+        outs = {"logits_fake": torch.empty(N, **f32), "logits_real": torch.empty(N, **f32),
+                "loss_d": torch.empty(1, **f32), "loss_g": torch.empty(1, **f32),
+                "dW": [torch.empty_like(m) for m in W], "db": [torch.empty_like(v) for v in bias],
+                "dLg_dx": torch.empty((N, w.d), **f32), "dLg_dtheta": torch.empty((w.n_theta, 2 * w.d), **f32)}
+        src = dict(theta=theta, events_per_theta=w.events_per_theta, seed=w.fake_seed)
+        prec = sg.BF16 if w.precision == "bf16" else sg.F32
+        feats = sg.FEAT_HD8 if w.features == "hd8" else sg.FEAT_IDENTITY
+
+        def step():
+            ctx.disc_fwd_bwd(W, bias, real, fake_source=src, outputs=outs, precision=prec, features=feats)
+
+        dominant = "disc_f32_fused" if prec == sg.F32 else "disc_bf16"
+        flops_per_launch = mlp_flops_per_fake_event(w.widths) * N
+        bound, unit, peak = "mfma", "TFLOP/s", PEAK["mfma_f32" if prec == sg.F32 else "mfma_bf16"]
+        dtype = "f32" if prec == sg.F32 else "bf16"
+    else:
+        g = torch.empty((w.n_theta, 2 * w.d), dtype=torch.float32, device=dev)
+        loss = torch.empty(1, dtype=torch.float32, device=dev)
+
+        def step():
+            ctx.param_grad(theta, w.events_per_theta, w.fake_seed, out=g, loss_out=loss)
+
+        dominant = "param_grad"
+        flops_per_launch = None
+        bound, unit, peak = "alu", "Gevents/s", None
+        dtype = "f32"
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    ctx.kernel_times()                      # drop warm-up records
+    ctx.set_timing(True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    ctx.set_timing(False)
+    kt = ctx.kernel_times()
+    ms_per_step = (t1 - t0) * 1e3 / args.steps
+    value = N / (ms_per_step * 1e-3)
+
+    launches, total_ms = kt.get(dominant, (0, 0.0))
+    avg_ms = total_ms / max(launches, 1)
+    if flops_per_launch is not None:
+        achieved = flops_per_launch / (avg_ms * 1e-3)
+        roof = {"bound": bound, "achieved": achieved / 1e12, "peak": peak / 1e12, "unit": unit,
+                "frac": achieved / peak}
+    else:
+        roof = {"bound": bound, "achieved": N / (avg_ms * 1e-3) / 1e9, "peak": None, "unit": unit, "frac": None}
+    tr = read_traffic(dominant, w.name)
+    roof["traffic"] = tr
+    roof["kernel"] = dominant
+    roof["kernel_avg_ms"] = avg_ms
+    roof["kernels"] = {k: {"launches": n, "avg_ms": t / max(n, 1)} for k, (n, t) in kt.items()}
+
+    line = {
+        "metric": "events/sec per sample->discriminate->backward step; % of HBM / MFMA peak",
+        "value": value, "unit": "events/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": ms_per_step, "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": dtype, "data": "synthetic (seeded theta, Philox-sampled events, Xavier-initialised weights)",
+        "config": {"workload": w.name, "n_theta": w.n_theta, "events_per_theta": w.events_per_theta,
+                   "fake_events": N, "real_events": N if w.widths else 0,
+                   "widths": list(w.widths) if w.widths else None, "precision": w.precision,
+                   "features": w.features, "parallelism": "single GPU"},
+        "roofline": roof,
+    }
+    if not args.no_cpu_baseline:
+        ev = w.events_per_theta if w.widths is not None else min(w.events_per_theta, 1 << 20)
+        line["cpu_baseline"] = cpu_baseline(w, inp, min(args.cpu_rows, w.n_theta), ev)
+    ctx.close()
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -453,14 +453,27 @@ struct Segments {
   float* dst[2 * kMaxNH + 4];
 };
 
+constexpr int kRedElems = 32;   // elements per block
+constexpr int kRedSlices = 8;   // workgroup ranges summed side by side, then combined in order
+
 __global__ __launch_bounds__(256) void k_reduce_wg(const float* __restrict__ part, int n_wg, int P, Segments sg) {
-  const int e = blockIdx.x * 256 + threadIdx.x;
-  if (e >= P) return;
+  __shared__ float red[kRedSlices][kRedElems];
+  const int le = threadIdx.x % kRedElems, sl = threadIdx.x / kRedElems;
+  const int e = blockIdx.x * kRedElems + le;
+  const int per = (n_wg + kRedSlices - 1) / kRedSlices;
+  const int g0 = sl * per, g1 = min(n_wg, g0 + per);
   float s = 0.f;
-  for (int g = 0; g < n_wg; ++g) s += part[(int64_t)g * P + e];
+  if (e < P)
+    for (int g = g0; g < g1; ++g) s += part[(int64_t)g * P + e];
+  red[sl][le] = s;
+  __syncthreads();
+  if (sl != 0 || e >= P) return;
+  float t = 0.f;
+#pragma unroll
+  for (int q = 0; q < kRedSlices; ++q) t += red[q][le];
   for (int i = 0; i < sg.n; ++i)
     if (e >= sg.off[i] && e < sg.off[i] + sg.len[i]) {
-      if (sg.dst[i]) sg.dst[i][e - sg.off[i]] = s;
+      if (sg.dst[i]) sg.dst[i][e - sg.off[i]] = t;
       break;
     }
 }
@@ -629,7 +642,8 @@ hipError_t launch_disc_f32(const DiscArgs& a, void* ws, int n_cu, hipStream_t st
     sg.off[n] = offwo; sg.len[n] = H; sg.dst[n++] = a.out->dW[NH + 1];
     sg.off[n] = offwo + H; sg.len[n] = 1; sg.dst[n++] = a.out->db[NH + 1];
     sg.n = n;
-    hipLaunchKernelGGL(k_reduce_wg, dim3((L.P + 255) / 256), dim3(256), 0, st, p.wg_part, n_cu, L.P, sg);
+    hipLaunchKernelGGL(k_reduce_wg, dim3((L.P + kRedElems - 1) / kRedElems), dim3(kRedElems * kRedSlices), 0, st,
+                       p.wg_part, n_cu, L.P, sg);
   }
   if (a.out->loss_d || a.out->loss_g)
     hipLaunchKernelGGL(k_reduce_loss, dim3(1), dim3(256), 0, st, p.loss_part, p.n_fake_tiles, p.n_tiles, p.inv_nf,
