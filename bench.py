@@ -28,6 +28,7 @@ PEAK = {"mfma_f32": 157.3e12, "mfma_bf16": 2.5e15, "hbm": 8.0e12}
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
 KERNEL_SOURCES = {
     "disc_f32_fused": ["paper_2407_00051_amd/csrc/disc_f32.hip", "paper_2407_00051_amd/csrc/device_math.hpp"],
+    "bf16_gemm": ["paper_2407_00051_amd/csrc/disc_bf16.hip", "paper_2407_00051_amd/csrc/device_math.hpp"],
     "param_grad": ["paper_2407_00051_amd/csrc/sampler.hip", "paper_2407_00051_amd/csrc/device_math.hpp"],
 }
 
@@ -149,8 +150,16 @@ def main():
         def step():
             ctx.disc_fwd_bwd(W, bias, real, fake_source=src, outputs=outs, precision=prec, features=feats)
 
-        dominant = "disc_f32_fused" if prec == sg.F32 else "disc_bf16"
-        flops_per_launch = mlp_flops_per_fake_event(w.widths) * N
+        if prec == sg.F32:
+            dominant = "disc_f32_fused"
+            flops_per_launch = mlp_flops_per_fake_event(w.widths) * N
+        else:
+            # the bf16 step runs layer by layer; its dominant kernel is the forward /
+            # backward-data product: per step 2 * NH products of 2 H^2 flops per row
+            dominant = "bf16_gemm"
+            H, NH = w.widths[1], len(w.widths) - 3
+            chunks = 2 * ((N + (1 << 20) - 1) >> 20)
+            flops_per_launch = 2 * NH * 2 * H * H * (2 * N) / (2 * NH * chunks)
         bound, unit, peak = "mfma", "TFLOP/s", PEAK["mfma_f32" if prec == sg.F32 else "mfma_bf16"]
         dtype = "f32" if prec == sg.F32 else "bf16"
     else:
@@ -189,6 +198,8 @@ def main():
                 "frac": achieved / peak}
     else:
         roof = {"bound": bound, "achieved": N / (avg_ms * 1e-3) / 1e9, "peak": None, "unit": unit, "frac": None}
+    if w.widths is not None:
+        roof["step_mfma_frac"] = mlp_flops_per_fake_event(w.widths) * N / (ms_per_step * 1e-3) / peak
     tr = read_traffic(dominant, w.name)
     roof["traffic"] = tr
     roof["kernel"] = dominant

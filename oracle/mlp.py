@@ -14,10 +14,16 @@ Losses (means over each batch):
 The backward pass returns dL_D/dW_l, dL_D/db_l and dL_G/d(input) of the fake
 events, the gradient that flows back through the sampler to theta.
 
-bf16 mode mirrors where a bf16-operand / fp32-accumulate implementation
-rounds: hidden-layer weights, the activations h_1 .. h_{n-1} (after bias and
-LeakyReLU) and the hidden-layer backward signals are rounded to bf16
-(round-to-nearest-even); everything else stays float64.
+bf16 mode states where a bf16-operand / fp32-accumulate evaluation rounds
+to bfloat16 (round to nearest even); everything else stays float64:
+  * hidden-to-hidden weights, once;
+  * the activations h_1 .. h_{n-1}, after bias and LeakyReLU;
+  * the backward signals of the hidden layers, which carry a unit seed per
+    event (backprop is linear in the seed): delta_{n-1} = w_o * leaky'(pre),
+    then delta_{l-1} = (delta_l W_l) * leaky'(pre_{l-1});
+  * the weight-gradient operand e_D * delta_l, rounded again after scaling.
+The first layer and the logit layer keep float64 weights; dL/dx scales the
+first-layer signal by e_G.
 """
 from __future__ import annotations
 
@@ -101,26 +107,70 @@ def bce_losses(z_fake, z_real):
     return L_D, L_G
 
 
-def _backward(W, pres, hs, g_z, slope, bf16, want_input_grad):
-    """Backprop a per-event logit gradient g_z through the network."""
+def _backward(W, pres, hs, g_z, slope, want_input_grad, cond=False):
+    """Backprop a per-event logit gradient g_z through the network (float64).
+    With cond, also the sums over events of |terms| of every dW and db entry."""
     n = len(W)
     W = [np.asarray(w, dtype=np.float64) for w in W]
-    if bf16:
-        W = [round_bf16(w) if _hidden(l, n) else w for l, w in enumerate(W)]
     dW = [None] * n
     db = [None] * n
+    cW = [None] * n
+    cb = [None] * n
     g = g_z[:, None]                       # dL/dpre of the logit layer
     g_in = None
     for l in range(n - 1, -1, -1):
-        if bf16 and _hidden(l, n):
-            g = round_bf16(g)
         dW[l] = g.T @ hs[l]
         db[l] = g.sum(axis=0)
+        if cond:
+            cW[l] = np.abs(g).T @ np.abs(hs[l])
+            cb[l] = np.abs(g).sum(axis=0)
         if l > 0:
             g = (g @ W[l]) * _leaky_grad(pres[l - 1], slope)
         elif want_input_grad:
             g_in = g @ W[0]
+    if cond:
+        return dW, db, g_in, cW, cb
     return dW, db, g_in
+
+
+def _disc_bf16(W, b, fake_in, real_in, slope, rnd):
+    """disc_fwd_bwd with the bf16 rounding points of the module docstring; `rnd`
+    is the rounding map (round_bf16, or the identity to check the structure)."""
+    n = len(W)
+    W = [np.asarray(w, dtype=np.float64) for w in W]
+    b = [np.asarray(v, dtype=np.float64) for v in b]
+    Wq = [rnd(w) if _hidden(l, n) else w for l, w in enumerate(W)]
+
+    def fwd(h0):
+        hs = [np.asarray(h0, dtype=np.float64)]
+        for l in range(n - 1):
+            hs.append(rnd(_leaky(hs[-1] @ Wq[l].T + b[l], slope)))
+        return (hs[-1] @ W[-1].T + b[-1])[:, 0], hs
+
+    z_f, hs_f = fwd(fake_in)
+    z_r, hs_r = fwd(real_in)
+    nf, nr = z_f.shape[0], z_r.shape[0]
+    L_D, L_G = bce_losses(z_f, z_r)
+    e = np.concatenate([sigmoid(z_f) / nf, -sigmoid(-z_r) / nr])
+    eG = -sigmoid(-z_f) / nf
+    hs = [np.concatenate([p, q]) for p, q in zip(hs_f, hs_r)]
+    dW = [None] * n
+    db = [None] * n
+    dW[n - 1] = (e[:, None] * hs[n - 1]).sum(axis=0)[None, :]
+    db[n - 1] = np.array([e.sum()])
+    d = rnd(W[n - 1][0][None, :] * _leaky_grad(hs[n - 1], slope))       # unit-seed signal of layer n-2
+    for l in range(n - 2, 0, -1):                                       # hidden-to-hidden layers
+        dW[l] = rnd(e[:, None] * d).T @ hs[l]
+        db[l] = (e[:, None] * d).sum(axis=0)
+        d = rnd((d @ Wq[l]) * _leaky_grad(hs[l], slope))
+    dW[0] = (e[:, None] * d).T @ hs[0]
+    db[0] = (e[:, None] * d).sum(axis=0)
+    g_in = eG[:, None] * (d[:nf] @ W[0])
+    return {
+        "kink_margin_fake": np.full(nf, np.inf),
+        "logits_fake": z_f, "logits_real": z_r, "loss_d": L_D, "loss_g": L_G,
+        "dW": dW, "db": db, "dLg_din": g_in,
+    }
 
 
 def disc_fwd_bwd(W, b, fake_in, real_in, slope=0.2, bf16=False):
@@ -129,20 +179,23 @@ def disc_fwd_bwd(W, b, fake_in, real_in, slope=0.2, bf16=False):
     Returns a dict with logits_fake, logits_real, loss_d, loss_g, dW, db (of
     L_D) and dLg_din (dL_G / d fake input, [N][F]).
     """
-    z_f, pres_f, hs_f = mlp_forward(W, b, fake_in, slope, bf16)
-    z_r, pres_r, hs_r = mlp_forward(W, b, real_in, slope, bf16)
+    if bf16:
+        return _disc_bf16(W, b, fake_in, real_in, slope, round_bf16)
+    z_f, pres_f, hs_f = mlp_forward(W, b, fake_in, slope)
+    z_r, pres_r, hs_r = mlp_forward(W, b, real_in, slope)
     nf, nr = z_f.shape[0], z_r.shape[0]
     L_D, L_G = bce_losses(z_f, z_r)
     # d softplus(t)/dt = sigmoid(t)
     gD_f = sigmoid(z_f) / nf
     gD_r = -sigmoid(-z_r) / nr
     gG_f = -sigmoid(-z_f) / nf
-    dW_f, db_f, _ = _backward(W, pres_f, hs_f, gD_f, slope, bf16, False)
-    dW_r, db_r, _ = _backward(W, pres_r, hs_r, gD_r, slope, bf16, False)
-    _, _, g_in = _backward(W, pres_f, hs_f, gG_f, slope, bf16, True)
+    dW_f, db_f, _, cW_f, cb_f = _backward(W, pres_f, hs_f, gD_f, slope, False, cond=True)
+    dW_r, db_r, _, cW_r, cb_r = _backward(W, pres_r, hs_r, gD_r, slope, False, cond=True)
+    _, _, g_in = _backward(W, pres_f, hs_f, gG_f, slope, True)
     return {
         "kink_margin_fake": kink_margin(W, b, hs_f, pres_f),
         "logits_fake": z_f, "logits_real": z_r, "loss_d": L_D, "loss_g": L_G,
         "dW": [p + q for p, q in zip(dW_f, dW_r)], "db": [p + q for p, q in zip(db_f, db_r)],
+        "dW_cond": [p + q for p, q in zip(cW_f, cW_r)], "db_cond": [p + q for p, q in zip(cb_f, cb_r)],
         "dLg_din": g_in,
     }

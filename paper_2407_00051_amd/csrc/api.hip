@@ -147,6 +147,45 @@ sagips_status check_source(sagips_ctx* c, const sagips_source* s, const char* na
 
 int64_t source_events(const sagips_source* s) { return (int64_t)s->n_theta * s->events_per_theta; }
 
+// bf16 path: one chunked launcher; dL_G/dtheta by the reduction kernel over dL_G/dx.
+sagips_status disc_bf16(sagips_ctx* c, const sagips_mlp* D, const float* fake_x, const sagips_source* fake_src,
+                        int64_t n_fake, const float* real_x, int64_t n_real, const sagips_disc_out* out, int d) {
+  const char* why = nullptr;
+  if (!disc_bf16_supported(*D, d, &why)) return fail(c, SAGIPS_E_UNSUPPORTED, "%s", why);
+  SourceArgs sa{};
+  if (fake_src) sa = source_args(*fake_src);
+  DiscArgs a;
+  a.D = D;
+  a.fake_x = fake_x;
+  a.fake_src = fake_src ? &sa : nullptr;
+  a.n_fake = n_fake;
+  a.real_x = real_x;
+  a.n_real = n_real;
+  a.d = d;
+  sagips_disc_out o2 = *out;
+  o2.dLg_dtheta = nullptr;
+  a.out = &o2;
+  const size_t disc_ws = (disc_bf16_workspace(a) + 255) & ~(size_t)255;
+  size_t off_g = disc_ws, off_pg = disc_ws, total = disc_ws;
+  const bool want_theta = out->dLg_dtheta != nullptr;
+  if (want_theta) {
+    off_pg = off_g + (((size_t)n_fake * d * sizeof(float) + 255) & ~(size_t)255);
+    total = off_pg + param_grad_workspace(sa);
+  }
+  sagips_status s = ensure_ws(c, total);
+  if (s != SAGIPS_OK) return s;
+  char* ws = static_cast<char*>(c->ws);
+  if (want_theta && !o2.dLg_dx) o2.dLg_dx = reinterpret_cast<float*>(ws + off_g);
+  Timer* tm = timer_of(c);
+  hipError_t e = launch_disc_bf16(a, ws, c->stream, tm);
+  if (e != hipSuccess) return hip_fail(c, e, "disc_fwd_bwd (bf16) launch");
+  if (want_theta) {
+    e = launch_param_grad(sa, o2.dLg_dx, out->dLg_dtheta, nullptr, ws + off_pg, c->stream, tm);
+    if (e != hipSuccess) return hip_fail(c, e, "param_grad launch");
+  }
+  return SAGIPS_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -308,9 +347,8 @@ sagips_status sagips_disc_fwd_bwd(sagips_ctx* c, const sagips_mlp* D, const floa
   if (out->dLg_dtheta && !fake_src) return fail(c, SAGIPS_E_INVAL, "dLg_dtheta needs a fake source");
 
   DeviceGuard g(c->device);
-  if (D->precision != SAGIPS_F32)
-    return fail(c, SAGIPS_E_UNSUPPORTED, "bf16 discriminator path is not available in this build");
   const char* why = nullptr;
+  if (D->precision == SAGIPS_BF16) return disc_bf16(c, D, fake_x, fake_src, n_fake, real_x, n_real, out, d);
   if (!disc_f32_supported(*D, d, &why)) return fail(c, SAGIPS_E_UNSUPPORTED, "%s", why);
 
   // The in-kernel sampler needs every 64-event tile inside one parameter row;

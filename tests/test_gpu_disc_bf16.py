@@ -1,0 +1,180 @@
+"""GPU parity of the bf16-operand discriminator step (medium: 2-256x4-1,
+higher-dim: HD8 features, 8-512x4-1) against the CPU oracle, through the C ABI."""
+import numpy as np
+import pytest
+
+import oracle
+from oracle.sampler import uniform_from_words
+from tests.parity import assert_condition_aware, assert_normwise, to_np
+from workloads import gen, get
+from workloads.configs import scaled
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+import paper_2407_00051_amd as sg  # noqa: E402
+
+TOL = 2e-2        # bf16 operands: normwise per tensor
+
+
+class _T:
+    """Wraps an oracle array so that _check can treat it like a returned tensor."""
+    def __init__(self, a):
+        self.a = np.asarray(a, dtype=np.float64)
+
+    def item(self):
+        return float(self.a)
+
+    def detach(self):
+        return self
+
+    def cpu(self):
+        return self
+
+    def numpy(self):
+        return self.a
+
+
+def emu_as_out(emu):
+    o = {k: _T(emu[k]) for k in ("logits_fake", "logits_real", "loss_d", "loss_g")}
+    o["dW"] = [_T(v) for v in emu["dW"]]
+    o["db"] = [_T(v) for v in emu["db"]]
+    o["dLg_dx"] = _T(emu["dL_dx"])
+    o["dLg_dtheta"] = _T(emu["dL_dtheta"])
+    return o
+
+
+def _setup(w):
+    inp = gen.make_inputs(w)
+    dev = "cuda:0"
+    t = lambda a: torch.tensor(a, device=dev)
+    return inp, t(inp["theta"]), t(inp["theta_star"]), [t(m) for m in inp["W"]], [t(v) for v in inp["b"]]
+
+
+def _run(ctx, w, th, ts, W, b, n_real):
+    real = ctx.sample_events(ts, n_real, w.real_seed)
+    feats = sg.FEAT_HD8 if w.features == "hd8" else sg.FEAT_IDENTITY
+    o = ctx.disc_fwd_bwd(W, b, real, fake_source=dict(theta=th, events_per_theta=w.events_per_theta, seed=w.fake_seed),
+                         precision=sg.BF16, features=feats)
+    torch.cuda.synchronize()
+    return o
+
+
+def _check(o, ref, tol, tag, n_layers, cond_ref=None):
+    """Normwise per tensor; a reduced tensor (dW, db, dL/dtheta) whose normwise error
+    exceeds tol still passes if every entry is within tol * sum|terms| (cancelling
+    sums), with the condition sums taken from the float64 oracle `cond_ref`."""
+    from tests.parity import normwise
+    bad = []
+
+    def nw(got, r, what, cond=None):
+        e = normwise(got, r)
+        msg = f"  {tag} {what}: normwise {e:.3e}"
+        ok = e <= tol
+        if not ok and cond is not None:
+            worst = float(np.max(np.abs(np.asarray(got, np.float64) - r) / np.maximum(cond, 1e-300)))
+            msg += f", max |err|/sum|terms| {worst:.3e}"
+            ok = worst <= tol
+        print(msg + ("" if ok else "  <-- FAIL"), flush=True)
+        if not ok:
+            bad.append(what)
+
+    cr = cond_ref or ref
+    nw(to_np(o["logits_fake"]), ref["logits_fake"], "logits_fake")
+    nw(to_np(o["logits_real"]), ref["logits_real"], "logits_real")
+    nw(o["loss_d"].item(), ref["loss_d"], "loss_d")
+    nw(o["loss_g"].item(), ref["loss_g"], "loss_g")
+    for l in range(n_layers):
+        nw(to_np(o["dW"][l]), ref["dW"][l], f"dW[{l}]", cr["dW_cond"][l])
+        nw(to_np(o["db"][l]), ref["db"][l], f"db[{l}]", cr["db_cond"][l])
+    nw(to_np(o["dLg_dx"]), ref["dL_dx"], "dLg_dx")
+    nw(to_np(o["dLg_dtheta"]), ref["dL_dtheta"], "dLg_dtheta", cr["dL_dtheta_cond"])
+    return bad
+
+
+@pytest.mark.parametrize("name,n_theta,E,n_real", [
+    ("medium", 8, 2048, None),
+    ("medium", 3, 1000, 2999),       # ragged: rows not multiples of the 128-row tile, n_real != n_fake
+    ("higher_dim", 4, 2048, None),
+    ("higher_dim", 2, 777, 1500),
+])
+def test_bf16_reduced(gpu_ctx, name, n_theta, E, n_real):
+    w = scaled(get(name), n_theta, E)
+    n_real = n_real or w.n_events
+    print(f"case {name} n_theta={n_theta} E={E} n_real={n_real}", flush=True)
+    inp, th, ts, W, b = _setup(w)
+    o = _run(gpu_ctx, w, th, ts, W, b, n_real)
+    real_np = oracle.sample(inp["theta_star"], n_real, w.real_seed)
+    ref = oracle.run_step(inp["theta"], E, w.fake_seed, inp["W"], inp["b"], real_np, features=w.features)
+    # The parity bar: the oracle evaluated at the same bf16 operand rounding points.
+    emu = oracle.run_step(inp["theta"], E, w.fake_seed, inp["W"], inp["b"], real_np, features=w.features, bf16=True)
+    bad_emu = _check(o, emu, TOL, "vs bf16-point oracle", len(W), cond_ref=ref)
+    # Against the float64 network: the losses and dL/dtheta at the same bar; the rest is
+    # reported (rounding the operands changes the network, and per-event quantities such as
+    # dL_G/dx and the first-layer gradient are ill-conditioned under that change).
+    bad64 = _check(o, ref, TOL, "vs fp64", len(W))
+    _check(emu_as_out(emu), ref, TOL, "bf16-point oracle vs fp64 (reported)", len(W))
+    bad64 = [k for k in bad64 if k in ("loss_d", "loss_g", "dLg_dtheta")]
+    assert not bad_emu and not bad64, (bad_emu, bad64)
+
+
+def test_bf16_deterministic(gpu_ctx):
+    w = scaled(get("medium"), 4, 4096)
+    inp, th, ts, W, b = _setup(w)
+    o1 = _run(gpu_ctx, w, th, ts, W, b, w.n_events)
+    o2 = _run(gpu_ctx, w, th, ts, W, b, w.n_events)
+    for k in ("logits_fake", "logits_real", "loss_d", "loss_g", "dLg_dx", "dLg_dtheta"):
+        assert torch.equal(o1[k], o2[k]), k
+    for l in range(len(W)):
+        assert torch.equal(o1["dW"][l], o2["dW"][l]) and torch.equal(o1["db"][l], o2["db"][l])
+
+
+def _events_at(theta, E, seed, idx, d):
+    w = oracle.event_words(seed, idx.astype(np.uint64))
+    u = uniform_from_words(w[:, :d])
+    rows = idx // E
+    th = np.asarray(theta, dtype=np.float64)[rows]
+    return oracle.kumaraswamy_icdf(u, th[:, 0::2], th[:, 1::2])
+
+
+@pytest.mark.parametrize("name", ["medium", "higher_dim"])
+def test_bf16_full_size_sampled(gpu_ctx, name):
+    """Full workload in the benchmarked configuration; logits and dL_G/dx of 20k sampled
+    events against the oracle evaluated event by event; losses and db of the logit
+    layer against their definitions over the returned logits."""
+    w = get(name)
+    print(f"case {name} full size: {w.n_events} fake + {w.n_events} real events", flush=True)
+    inp, th, ts, W, b = _setup(w)
+    o = _run(gpu_ctx, w, th, ts, W, b, w.n_events)
+    rng = np.random.default_rng(3)
+    idx = np.unique(np.concatenate([rng.integers(0, w.n_events, 20_000), [0, w.n_events - 1]]))
+    ti = torch.tensor(idx, device="cuda:0")
+    zf = to_np(o["logits_fake"][ti]).astype(np.float64)
+    zr = to_np(o["logits_real"][ti]).astype(np.float64)
+    gx = to_np(o["dLg_dx"][ti]).astype(np.float64)
+    xf = _events_at(inp["theta"], w.events_per_theta, w.fake_seed, idx, w.d)
+    xr = _events_at(inp["theta_star"], w.n_events, w.real_seed, idx, w.d)
+    fin = xf if w.features == "identity" else oracle.features_hd8(xf)
+    rin = xr if w.features == "identity" else oracle.features_hd8(xr)
+    from tests.parity import normwise
+    for tag, bf16 in (("fp64 (reported)", False), ("bf16-point oracle", True)):
+        r = oracle.disc_fwd_bwd(inp["W"], inp["b"], fin, rin, bf16=bf16)
+        g = r["dLg_din"] * (len(idx) / w.n_events)          # the oracle batch mean is over the sample
+        if w.features == "hd8":
+            g = np.einsum("nf,nfd->nd", g, oracle.features_hd8_jacobian(xf))
+        if bf16:
+            assert_normwise(zf, r["logits_fake"], TOL, "sampled logits_fake vs " + tag)
+            assert_normwise(zr, r["logits_real"], TOL, "sampled logits_real vs " + tag)
+            assert_normwise(gx, g, TOL, "sampled dLg_dx vs " + tag)
+        else:
+            print(f"  sampled vs {tag}: logits_fake {normwise(zf, r['logits_fake']):.3e}, logits_real "
+                  f"{normwise(zr, r['logits_real']):.3e}, dLg_dx {normwise(gx, g):.3e}", flush=True)
+    # properties over the whole batch, from the returned logits
+    zf_all = to_np(o["logits_fake"]).astype(np.float64)
+    zr_all = to_np(o["logits_real"]).astype(np.float64)
+    LD, LG = oracle.bce_losses(zf_all, zr_all)
+    assert abs(o["loss_d"].item() - LD) <= 1e-4 * LD and abs(o["loss_g"].item() - LG) <= 1e-4 * LG
+    sig = lambda t: 0.5 * (1 + np.tanh(0.5 * t))
+    dbo = sig(zf_all).mean() - sig(-zr_all).mean()
+    cond = sig(zf_all).mean() + sig(-zr_all).mean()
+    assert abs(o["db"][-1].item() - dbo) <= 1e-4 * cond

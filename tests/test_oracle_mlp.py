@@ -132,3 +132,18 @@ def test_bf16_mode_is_close_to_fp64():
     rel = lambda p, t: np.linalg.norm(p - t) / np.linalg.norm(t)
     assert 0 < rel(q["logits_fake"], r["logits_fake"]) < 2e-2
     assert 0 < rel(q["dW"][1], r["dW"][1]) < 5e-2
+
+
+def test_bf16_mode_structure_reduces_to_fp64():
+    """With the rounding map replaced by the identity, the bf16 evaluation is the float64 one."""
+    from oracle.mlp import _disc_bf16
+    W, b = _net((8, 16, 16, 16, 1), 13)
+    xf, xr = _batches(8, 30, 14)
+    r = disc_fwd_bwd(W, b, xf, xr)
+    q = _disc_bf16(W, b, xf, xr, 0.2, lambda a: a)
+    for k in ("logits_fake", "logits_real", "dLg_din"):
+        np.testing.assert_allclose(q[k], r[k], rtol=1e-12, atol=1e-15)
+    assert abs(q["loss_d"] - r["loss_d"]) < 1e-14
+    for l in range(len(W)):
+        np.testing.assert_allclose(q["dW"][l], r["dW"][l], rtol=1e-11, atol=1e-15)
+        np.testing.assert_allclose(q["db"][l], r["db"][l], rtol=1e-11, atol=1e-15)
