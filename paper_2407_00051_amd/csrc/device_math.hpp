@@ -65,10 +65,35 @@ __device__ __forceinline__ Shape make_shape(float a, float b) {
   return s;
 }
 
+// Elementary functions on the hardware transcendental units (v_log_f32 = log2,
+// v_exp_f32 = 2^x, v_rcp_f32; each within 1 ulp over the ranges used here).
+constexpr float kLn2 = 0.693147180559945309f;
+constexpr float kLog2e = 1.442695040888963407f;
+
+__device__ __forceinline__ float fast_log(float x) { return __builtin_amdgcn_logf(x) * kLn2; }
+__device__ __forceinline__ float fast_exp(float x) { return __builtin_amdgcn_exp2f(x * kLog2e); }
+__device__ __forceinline__ float fast_rcp(float x) { return __builtin_amdgcn_rcpf(x); }
+
+// e^t - 1 by Kahan's method: with w = fl(e^t), (w - 1) t / ln w cancels the
+// rounding error of w, so the result keeps its relative accuracy as t -> 0.
+__device__ __forceinline__ float expm1_k(float t, float w) {
+  if (w == 1.0f) return t;
+  const float wm1 = w - 1.0f;
+  if (wm1 == -1.0f) return -1.0f;       // e^t below half an ulp of 1 (or flushed to 0)
+  return wm1 * t * fast_rcp(fast_log(w));
+}
+
+// ln(1 + y) by Kahan's method: with v = fl(1 + y), ln(v) y / (v - 1).
+__device__ __forceinline__ float log1p_k(float y) {
+  const float v = 1.0f + y;
+  if (v == 1.0f) return y;
+  return fast_log(v) * y * fast_rcp(v - 1.0f);
+}
+
 // Kumaraswamy quantile x = (1 - (1-u)^(1/b))^(1/a), written through logs so
 // that no step cancels: with l = ln(1-u) (1-u is exact), t = l/b,
 // s = e^t = (1-u)^(1/b), g = 1 - s = -expm1(t) and lam = ln g, x = e^(lam/a).
-// ln g is taken as log1p(-s) once s < 1/2, where g is close to 1.
+// ln g is taken as log1p(-s) while s < 1/2, where g is close to 1.
 struct Quantile {
   float x;
   float l;    // ln(1-u)
@@ -77,29 +102,32 @@ struct Quantile {
   float lam;  // ln g = a ln x
 };
 
-__device__ __forceinline__ Quantile kumaraswamy(float u, Shape sh) {
+__device__ __forceinline__ Quantile kumaraswamy_v(float v /* = 1 - u, exact */, Shape sh) {
   Quantile q;
-  q.l = log1pf(-u);
+  q.l = fast_log(v);
   const float t = q.l * sh.rb;
-  q.s = expf(t);
-  q.g = -expm1f(t);
-  q.lam = (q.s < 0.5f) ? log1pf(-q.s) : logf(q.g);
-  q.x = expf(q.lam * sh.ra);
+  q.s = fast_exp(t);
+  q.g = -expm1_k(t, q.s);
+  q.lam = (q.s < 0.5f) ? log1p_k(-q.s) : fast_log(q.g);
+  q.x = fast_exp(q.lam * sh.ra);
   return q;
 }
+
+__device__ __forceinline__ Quantile kumaraswamy(float u, Shape sh) { return kumaraswamy_v(1.0f - u, sh); }
 
 // Pathwise derivatives by the chain rule through the quantile:
 //   dx/da = -x lam / a^2                     (>= 0)
 //   dx/db = x s l / (a b^2 g)                (<= 0)
 __device__ __forceinline__ void pathwise(const Quantile& q, Shape sh, float& dxda, float& dxdb) {
   dxda = -q.x * q.lam * (sh.ra * sh.ra);
-  dxdb = q.x * q.s * q.l * (sh.ra * sh.rb * sh.rb) / q.g;
+  dxdb = q.x * q.s * q.l * (sh.ra * sh.rb * sh.rb) * fast_rcp(q.g);
 }
 
 // ln(1 - e^m) for m < 0 without cancellation (Maechler 2012, "Accurately
-// computing log(1 - exp(-|a|))"): log(-expm1(m)) near 0, log1p(-exp(m)) below -ln 2.
+// computing log(1 - exp(-|a|))"): ln(-expm1(m)) near 0, log1p(-e^m) below -ln 2.
 __device__ __forceinline__ float log1mexp(float m) {
-  return (m > -0.693147180559945f) ? logf(-expm1f(m)) : log1pf(-expf(m));
+  const float w = fast_exp(m);
+  return (m > -kLn2) ? fast_log(-expm1_k(m, w)) : log1p_k(-w);
 }
 
 // Wave-wide sum (64 lanes), same order on every call.

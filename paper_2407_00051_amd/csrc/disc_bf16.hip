@@ -264,14 +264,17 @@ __global__ __launch_bounds__(256) void k_gemm(const u16* __restrict__ in, const 
 // Logit layer and BCE seeds for one chunk.  One wave per row: lanes split H.
 // Writes e_D[r] (0 on padding), e_G[r], delta_L (unit seed, bf16), logits,
 // and per-block partials of the loss sums, dW_o and db_o.
-constexpr int kLogitRowsPerBlock = 64;
+constexpr int kRowBlocks = 512;   // blocks of the row-reduction kernels (fixed partial count)
+
+inline int row_blocks(int rows) { return std::max(1, std::min(kRowBlocks, (rows + 63) / 64)); }
+inline int rows_per_block(int rows, int blocks) { return (rows + blocks - 1) / blocks; }
 
 template <int PER>
 __global__ __launch_bounds__(256) void k_logit(const u16* __restrict__ AL, const float* __restrict__ Wo,
                                                const float* __restrict__ bo, int H, ChunkArgs c, float inv_n,
                                                float slope, float* __restrict__ eD, float* __restrict__ eG,
                                                u16* __restrict__ dL, float* __restrict__ logits,
-                                               float* __restrict__ part /*[blocks][H + 3]*/) {
+                                               float* __restrict__ part /*[blocks][H + 3]*/, int rpb) {
   extern __shared__ float sh_dwo[];   // [4 waves][H]
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   constexpr int per = PER;            // features per lane, H / 64
@@ -282,8 +285,8 @@ __global__ __launch_bounds__(256) void k_logit(const u16* __restrict__ AL, const
 #pragma unroll
   for (int q = 0; q < per; ++q) acc_dwo[q] = 0.f;
   float l0 = 0.f, l1 = 0.f, sum_e = 0.f;
-  const int rbase = blockIdx.x * kLogitRowsPerBlock;
-  for (int rr = wave; rr < kLogitRowsPerBlock; rr += 4) {
+  const int rbase = blockIdx.x * rpb;
+  for (int rr = wave; rr < rpb; rr += 4) {
     const int r = rbase + rr;
     if (r >= c.rows) break;
     const u16* hrow = AL + (int64_t)r * H + lane * per;
@@ -447,14 +450,13 @@ __global__ __launch_bounds__(256) void k_wgrad(const u16* __restrict__ dlt, cons
 // ---------------------------------------------------------------------------
 // First layer backward for one chunk: per-block partials of dW1 [H][F] and
 // db1 [H]; for fake rows dL_G/dx (through the HD8 Jacobian when used).
-constexpr int kFBRows = 256;    // rows per block
 
 template <int D, bool kHD8, int PER>
 __global__ __launch_bounds__(256) void k_first_bwd(const u16* __restrict__ d1, const float* __restrict__ feat,
                                                    const float* __restrict__ xs, const float* __restrict__ W1,
                                                    const float* __restrict__ eD, const float* __restrict__ eG,
                                                    int H, ChunkArgs c, float* __restrict__ dLg_dx,
-                                                   float* __restrict__ part /*[blocks][H*F + H]*/) {
+                                                   float* __restrict__ part /*[blocks][H*F + H]*/, int rpb) {
   constexpr int F = kHD8 ? 8 : D;
   extern __shared__ float smem[];          // W1 [H][F], then the block's accumulators [H][F+1]
   float* sW1 = smem;
@@ -469,8 +471,8 @@ __global__ __launch_bounds__(256) void k_first_bwd(const u16* __restrict__ d1, c
     for (int j = 0; j <= F; ++j) adw[q][j] = 0.f;
   __syncthreads();
   const bool want_dx = c.fake && dLg_dx != nullptr;
-  const int rbase = blockIdx.x * kFBRows;
-  for (int rr = wave; rr < kFBRows; rr += 4) {
+  const int rbase = blockIdx.x * rpb;
+  for (int rr = wave; rr < rpb; rr += 4) {
     const int r = rbase + rr;
     if (r >= c.rows) break;
     const float e = eD[r];
@@ -536,14 +538,37 @@ __global__ __launch_bounds__(256) void k_first_bwd(const u16* __restrict__ d1, c
   }
 }
 
-// acc[e] (+)= sum_s part[s][e] in slice order; first chunk overwrites.
+// acc[e] (+)= sum_k part[k][e], k = 0..n-1, in a fixed order (S contiguous
+// row ranges summed side by side, then combined in order); the first chunk
+// overwrites.  C columns per block, S = 256 / C row slices.
+template <int C>
 __global__ __launch_bounds__(256) void k_accumulate(const float* __restrict__ part, int n, int64_t stride,
                                                     int64_t len, float* __restrict__ acc, int first) {
-  const int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (e >= len) return;
+  constexpr int S = 256 / C;
+  __shared__ float red[S][C];
+  const int lc = threadIdx.x % C, sl = threadIdx.x / C;
+  const int64_t e = (int64_t)blockIdx.x * C + lc;
+  const int per = (n + S - 1) / S;
+  const int k0 = sl * per, k1 = min(n, k0 + per);
   float s = 0.f;
-  for (int k = 0; k < n; ++k) s += part[k * stride + e];
-  acc[e] = first ? s : acc[e] + s;
+  if (e < len) {
+#pragma unroll 8
+    for (int k = k0; k < k1; ++k) s += part[(int64_t)k * stride + e];
+  }
+  red[sl][lc] = s;
+  __syncthreads();
+  if (sl != 0 || e >= len) return;
+  float t = 0.f;
+#pragma unroll
+  for (int q = 0; q < S; ++q) t += red[q][lc];
+  acc[e] = first ? t : acc[e] + t;
+}
+
+void accumulate(const float* part, int n, int64_t stride, int64_t len, float* acc, int first, hipStream_t st) {
+  if (len >= 16384)
+    hipLaunchKernelGGL(k_accumulate<64>, dim3((unsigned)((len + 63) / 64)), dim3(256), 0, st, part, n, stride, len, acc, first);
+  else
+    hipLaunchKernelGGL(k_accumulate<16>, dim3((unsigned)((len + 15) / 16)), dim3(256), 0, st, part, n, stride, len, acc, first);
 }
 
 // Logit-layer scalars of one chunk: sum e_D -> db_o, loss sums -> lacc
@@ -605,8 +630,8 @@ Plan make_plan(const DiscArgs& a) {
   p.D = a.d;
   const int64_t biggest = std::min<int64_t>(std::max(a.n_fake, a.n_real), kChunkRows);
   p.rows_max = pad128(biggest);
-  p.logit_blocks = (p.rows_max + kLogitRowsPerBlock - 1) / kLogitRowsPerBlock;
-  p.fb_blocks = (p.rows_max + kFBRows - 1) / kFBRows;
+  p.logit_blocks = kRowBlocks;
+  p.fb_blocks = kRowBlocks;
   const int tiles = (p.H / kGT) * (p.H / kGT);
   p.slices = std::max(1, 256 / tiles);
   const size_t H = p.H, R = p.rows_max;
@@ -710,19 +735,18 @@ hipError_t launch_disc_bf16(const DiscArgs& a, void* ws, hipStream_t st, Timer* 
         if (tm) tm->end();
       }
 
-      const int lb = (c.rows + kLogitRowsPerBlock - 1) / kLogitRowsPerBlock;
+      const int lb = row_blocks(c.rows), lrpb = rows_per_block(c.rows, lb);
       float* plog = F32(p.off_plog);
       if (H == 256)
         hipLaunchKernelGGL(k_logit<4>, dim3(lb), dim3(256), 4 * H * sizeof(float), st, act + NH * ast, Dm.W[NH + 1],
                            Dm.b[NH + 1], H, c, fake ? inv_nf : inv_nr, slope, eD, eG, dl[0],
-                           fake ? out.logits_fake : out.logits_real, plog);
+                           fake ? out.logits_fake : out.logits_real, plog, lrpb);
       else
         hipLaunchKernelGGL(k_logit<8>, dim3(lb), dim3(256), 4 * H * sizeof(float), st, act + NH * ast, Dm.W[NH + 1],
                            Dm.b[NH + 1], H, c, fake ? inv_nf : inv_nr, slope, eD, eG, dl[0],
-                           fake ? out.logits_fake : out.logits_real, plog);
+                           fake ? out.logits_fake : out.logits_real, plog, lrpb);
       if (want_grads)
-        hipLaunchKernelGGL(k_accumulate, dim3((H + 255) / 256), dim3(256), 0, st, plog, lb, (int64_t)(H + 3),
-                           (int64_t)H, out.dW[NH + 1], first);
+        accumulate(plog, lb, (int64_t)(H + 3), (int64_t)H, out.dW[NH + 1], first, st);
       hipLaunchKernelGGL(k_logit_scalars, dim3(1), dim3(256), 0, st, plog, lb, H, want_grads ? out.db[NH + 1] : nullptr,
                          lacc, c.fake, first, first_batch);
 
@@ -736,10 +760,8 @@ hipError_t launch_disc_bf16(const DiscArgs& a, void* ws, hipStream_t st, Timer* 
           hipLaunchKernelGGL(k_wgrad, dim3(tiles, p.slices), dim3(256), 0, st, dl[cur], act + l * ast, eD, H,
                              rows_per_slice, c.rows, F32(p.off_pw), F32(p.off_pdb));
           if (tm) tm->end();
-          hipLaunchKernelGGL(k_accumulate, dim3((H * H + 255) / 256), dim3(256), 0, st, F32(p.off_pw), p.slices,
-                             (int64_t)H * H, (int64_t)H * H, out.dW[1 + l], first);
-          hipLaunchKernelGGL(k_accumulate, dim3((H + 255) / 256), dim3(256), 0, st, F32(p.off_pdb), p.slices,
-                             (int64_t)H, (int64_t)H, out.db[1 + l], first);
+          accumulate(F32(p.off_pw), p.slices, (int64_t)H * H, (int64_t)H * H, out.dW[1 + l], first, st);
+          accumulate(F32(p.off_pdb), p.slices, (int64_t)H, (int64_t)H, out.db[1 + l], first, st);
         }
         if (tm) tm->begin("bf16_gemm");
         hipLaunchKernelGGL(k_gemm<kEpiBwd>, dim3(H / kGT, c.rows / kGT), dim3(256), 0, st, dl[cur],
@@ -747,22 +769,20 @@ hipError_t launch_disc_bf16(const DiscArgs& a, void* ws, hipStream_t st, Timer* 
         if (tm) tm->end();
         cur ^= 1;
       }
-      const int fbb = (c.rows + kFBRows - 1) / kFBRows;
+      const int fbb = row_blocks(c.rows), frpb = rows_per_block(c.rows, fbb);
       const size_t fb_smem = sizeof(float) * ((size_t)H * p.F + (size_t)H * (p.F + 1));
       float* pfb = F32(p.off_pfb);
       float* gx = fake ? out.dLg_dx : nullptr;
 #define SAGIPS_FIRST_BWD(D_, HD8_, PER_)                                                                   \
   hipLaunchKernelGGL((k_first_bwd<D_, HD8_, PER_>), dim3(fbb), dim3(256), fb_smem, st, dl[cur], feat, xs, Dm.W[0], \
-                     eD, eG, H, c, gx, pfb)
+                     eD, eG, H, c, gx, pfb, frpb)
       if (p.hd8) { if (H == 256) SAGIPS_FIRST_BWD(3, true, 4); else SAGIPS_FIRST_BWD(3, true, 8); }
       else if (p.D == 2) { if (H == 256) SAGIPS_FIRST_BWD(2, false, 4); else SAGIPS_FIRST_BWD(2, false, 8); }
       else { if (H == 256) SAGIPS_FIRST_BWD(3, false, 4); else SAGIPS_FIRST_BWD(3, false, 8); }
 #undef SAGIPS_FIRST_BWD
       if (want_grads) {
-        hipLaunchKernelGGL(k_accumulate, dim3((H * p.F + 255) / 256), dim3(256), 0, st, pfb, fbb,
-                           (int64_t)(H * p.F + H), (int64_t)(H * p.F), out.dW[0], first);
-        hipLaunchKernelGGL(k_accumulate, dim3((H + 255) / 256), dim3(256), 0, st, pfb + (size_t)H * p.F, fbb,
-                           (int64_t)(H * p.F + H), (int64_t)H, out.db[0], first);
+        accumulate(pfb, fbb, (int64_t)(H * p.F + H), (int64_t)(H * p.F), out.dW[0], first, st);
+        accumulate(pfb + (size_t)H * p.F, fbb, (int64_t)(H * p.F + H), (int64_t)H, out.db[0], first, st);
       }
       hipError_t e = hipGetLastError();
       if (e != hipSuccess) return e;
