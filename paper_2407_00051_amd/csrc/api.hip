@@ -351,9 +351,9 @@ sagips_status sagips_disc_fwd_bwd(sagips_ctx* c, const sagips_mlp* D, const floa
   if (D->precision == SAGIPS_BF16) return disc_bf16(c, D, fake_x, fake_src, n_fake, real_x, n_real, out, d);
   if (!disc_f32_supported(*D, d, &why)) return fail(c, SAGIPS_E_UNSUPPORTED, "%s", why);
 
-  // The in-kernel sampler needs every 64-event tile inside one parameter row;
+  // The in-kernel sampler needs every tile inside one parameter row;
   // otherwise sample first, run on the buffer, and reduce dL/dtheta after.
-  const bool fused_src = fake_src && (fake_src->events_per_theta % 64 == 0);
+  const bool fused_src = fake_src && (fake_src->events_per_theta % disc_f32_tile() == 0);
   SourceArgs sa{};
   if (fake_src) sa = source_args(*fake_src);
   DiscArgs a;

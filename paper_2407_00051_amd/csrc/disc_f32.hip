@@ -7,22 +7,25 @@
 // (paper Sec. V-A), weights in torch.nn.Linear layout.
 //
 // Work decomposition
-//   * One workgroup (4 waves) per CU loops over tiles of T = 64 events; a
-//     tile is all fake or all real.  The tile's activations A_1..A_{NH+1} and
-//     one spare buffer live in LDS as [T][H+4] fp32 (event-major, padded so
-//     that the 16-byte fragment reads below are bank-conflict free).
+//   * One persistent workgroup of 8 waves (two per SIMD, so one hides the
+//     other's load latency) per CU loops over tiles of T = 64 events; a tile
+//     is all fake or all real.  The tile's activations
+//     A_1..A_{NH+1} and one spare buffer live in LDS as [T][H+4] fp32
+//     (event-major, padded so that the 16-byte fragment reads below are
+//     bank-conflict free).
 //   * The H x H products run on the fp32 matrix cores
 //     (v_mfma_f32_16x16x4_f32).  Forward and backward-data products compute
 //     out^T = W' * in^T with M = output feature, N = event, K = input
-//     feature; wave w owns output features [w H/4, (w+1) H/4).  The W'
+//     feature; each wave owns 16 output features (and, for H = 64, half of
+//     the tile's events).  The W'
 //     fragment of lane l is 4 consecutive K values of one row, a 16-byte
 //     load from global memory (L2-resident); the activation fragment is the
 //     matching 16 bytes of one event's row in LDS.  Because the K order of a
 //     product is free, this one mapping serves all four K steps of a load.
 //     Backward-data products use a transposed copy of W made per call.
 //   * Weight gradients dW = sum_events e * delta^T A (K = events) accumulate
-//     in registers across all of the workgroup's tiles: wave w owns rows
-//     [w H/4, (w+1) H/4) of every hidden dW.  They are written once per
+//     in registers across all of the workgroup's tiles: each wave owns 16 rows
+//     of every hidden dW (for its events).  They are written once per
 //     workgroup and summed over workgroups in a fixed order afterwards.
 //   * One backward chain with a unit seed per event serves both losses: the
 //     signals are linear in the seed, so dL_D terms are scaled by
@@ -38,8 +41,9 @@ namespace {
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
-constexpr int kThreads = 256;
+constexpr int kThreads = 512;  // 8 waves, two per SIMD
 constexpr int kT = 64;         // events per tile
+constexpr int kWGPerCU = 1;    // resident workgroups per CU (LDS-limited)
 constexpr int kMaxNH = 4;
 
 struct F32Params {
@@ -83,10 +87,16 @@ template <int H, int NH, int F>
 struct Fused {
   static constexpr int LD = H + 4;             // LDS row stride in floats
   static constexpr int NB = NH + 2;            // activation + spare buffers
-  static constexpr int RB = H / 64;            // 16-row blocks per wave
-  static constexpr int CB = kT / 16;           // 16-event column blocks
+  static constexpr int WAVES = kThreads / 64;
+  static constexpr int WR = H / 16;            // waves along the output rows (16 rows each)
+  static constexpr int WE = WAVES / WR;        // waves along the events
+  static constexpr int TE = kT / WE;           // events per wave
+  static constexpr int CB = TE / 16;           // 16-event column blocks per wave
   static constexpr int KB = H / 16;            // 16-wide K blocks
   static constexpr int PPO = kThreads / H;     // threads per output feature in VALU loops
+  static constexpr int PARTS = kThreads / kT;  // threads per event in the per-event dot products
+  static constexpr int PD = 2;                 // weight-fragment prefetch distance (K blocks)
+  static_assert(WR * WE == WAVES && CB >= 1 && TE % 16 == 0, "wave decomposition");
   // per-workgroup partial layout (floats)
   static constexpr int P_DWH = H * H + H;      // dW + db of one hidden layer
   static constexpr int OFF_W1 = NH * P_DWH;    // dW1 [H][F], then db1 [H]
@@ -99,53 +109,51 @@ struct Fused {
     float dxd[kT][F][2];
     float eD[kT];
     float eG[kT];
-    float red[2 * kT * 4];   // >= kThreads and >= 2 T F
+    float W1[H * F];
+    float red[2 * kT * 4];   // >= 2 T F and >= 2 * waves
   };
 
   // Index of the buffer that holds delta_l (l = 1 .. NH+1).
   static constexpr __device__ int dbuf(int l) { return NH + ((NH + 1 - l) & 1); }
 
-  // out^T (this wave's RB x CB fragments) = Wg * in^T, K = H.
-  static __device__ __forceinline__ void gemm(const float* __restrict__ Wg, const float* in, f32x4 (&acc)[RB][CB],
-                                              int o0, int lr, int lg) {
+  // out^T (this wave's 16 rows x CB event blocks) = Wg * in^T, K = H.  The
+  // weight fragments are loaded PD K blocks ahead of their use.
+  static __device__ __forceinline__ void gemm(const float* __restrict__ Wg, const float* in, f32x4 (&acc)[CB],
+                                              int o0, int e0, int lr, int lg) {
 #pragma unroll
-    for (int rb = 0; rb < RB; ++rb)
+    for (int cb = 0; cb < CB; ++cb) acc[cb] = f32x4{0.f, 0.f, 0.f, 0.f};
+    const float* wrow = Wg + (o0 + lr) * H + 4 * lg;
+    f32x4 a[PD + 1];
 #pragma unroll
-      for (int cb = 0; cb < CB; ++cb) acc[rb][cb] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int q = 0; q < PD; ++q) a[q] = *reinterpret_cast<const f32x4*>(wrow + 16 * q);
 #pragma unroll
     for (int kb = 0; kb < KB; ++kb) {
-      f32x4 a[RB], b[CB];
-#pragma unroll
-      for (int rb = 0; rb < RB; ++rb)
-        a[rb] = *reinterpret_cast<const f32x4*>(Wg + (o0 + 16 * rb + lr) * H + 16 * kb + 4 * lg);
+      if (kb + PD < KB) a[(kb + PD) % (PD + 1)] = *reinterpret_cast<const f32x4*>(wrow + 16 * (kb + PD));
+      f32x4 b[CB];
 #pragma unroll
       for (int cb = 0; cb < CB; ++cb)
-        b[cb] = *reinterpret_cast<const f32x4*>(in + (16 * cb + lr) * LD + 16 * kb + 4 * lg);
+        b[cb] = *reinterpret_cast<const f32x4*>(in + (e0 + 16 * cb + lr) * LD + 16 * kb + 4 * lg);
 #pragma unroll
       for (int s = 0; s < 4; ++s)
 #pragma unroll
-        for (int rb = 0; rb < RB; ++rb)
-#pragma unroll
-          for (int cb = 0; cb < CB; ++cb) acc[rb][cb] = mfma4(a[rb][s], b[cb][s], acc[rb][cb]);
+        for (int cb = 0; cb < CB; ++cb) acc[cb] = mfma4(a[kb % (PD + 1)][s], b[cb][s], acc[cb]);
     }
   }
 
-  // accW += sum_ev e[ev] * delta[ev][o] * A[ev][k] over the tile, o in this wave's rows.
+  // accW += sum over this wave's events of e[ev] delta[ev][o] A[ev][k], o in
+  // the wave's 16 rows; dbacc += the e-scaled delta values this lane loaded.
   static __device__ __forceinline__ void wgrad(const float* dlt, const float* A, const float* e,
-                                               f32x4 (&accW)[RB][KB], int o0, int lr, int lg) {
+                                               f32x4 (&accW)[KB], float& dbacc, int o0, int e0, int lr, int lg) {
 #pragma unroll 4
-    for (int q = 0; q < kT / 4; ++q) {
-      const int ev = 4 * q + lg;
-      const float ee = e[ev];
-      float a[RB], b[KB];
-#pragma unroll
-      for (int rb = 0; rb < RB; ++rb) a[rb] = ee * dlt[ev * LD + o0 + 16 * rb + lr];
+    for (int q = 0; q < TE / 4; ++q) {
+      const int ev = e0 + 4 * q + lg;
+      const float a = e[ev] * dlt[ev * LD + o0 + lr];
+      dbacc += a;
+      float b[KB];
 #pragma unroll
       for (int kb = 0; kb < KB; ++kb) b[kb] = A[ev * LD + 16 * kb + lr];
 #pragma unroll
-      for (int rb = 0; rb < RB; ++rb)
-#pragma unroll
-        for (int kb = 0; kb < KB; ++kb) accW[rb][kb] = mfma4(a[rb], b[kb], accW[rb][kb]);
+      for (int kb = 0; kb < KB; ++kb) accW[kb] = mfma4(a, b[kb], accW[kb]);
     }
   }
 
@@ -154,21 +162,21 @@ struct Fused {
     const int tid = threadIdx.x;
     const int lane = tid & 63, wave = tid >> 6;
     const int lr = lane & 15, lg = lane >> 4;
-    const int o0 = wave * (H / 4);
+    const int o0 = (wave % WR) * 16;             // this wave's output rows
+    const int ew = wave / WR;
+    const int e0 = ew * TE;                      // this wave's events
     const float slope = p.slope;
 
-    f32x4 accW[NH][RB][KB];
+    f32x4 accW[NH][KB];
+    float dbacc[NH];
 #pragma unroll
-    for (int l = 0; l < NH; ++l)
+    for (int l = 0; l < NH; ++l) {
+      dbacc[l] = 0.f;
 #pragma unroll
-      for (int rb = 0; rb < RB; ++rb)
-#pragma unroll
-        for (int kb = 0; kb < KB; ++kb) accW[l][rb][kb] = f32x4{0.f, 0.f, 0.f, 0.f};
+      for (int kb = 0; kb < KB; ++kb) accW[l][kb] = f32x4{0.f, 0.f, 0.f, 0.f};
+    }
     // VALU accumulators: thread (o = tid % H, part = tid / H) over events ev = part (mod PPO)
     const int vo = tid % H, vpart = tid / H;
-    float acc_dbh[NH];
-#pragma unroll
-    for (int l = 0; l < NH; ++l) acc_dbh[l] = 0.f;
     float acc_dW1[F];
 #pragma unroll
     for (int j = 0; j < F; ++j) acc_dW1[j] = 0.f;
@@ -177,6 +185,11 @@ struct Fused {
 #pragma unroll
     for (int j = 0; j < F; ++j) w1r[j] = p.W1[vo * F + j];
     const float b1r = p.b1[vo];
+    const float wor = p.Wo[vo];
+    for (int k = tid; k < H * F; k += kThreads) sm.W1[k] = p.W1[k];
+    // per-event dot products: thread (ev = tid / PARTS, part = tid % PARTS) covers H / PARTS features
+    const int dev_ = tid / PARTS, dpart = tid % PARTS;
+    constexpr int DSPAN = H / PARTS;
 
     for (int tile = blockIdx.x; tile < p.n_tiles; tile += gridDim.x) {
       const bool fake = tile < p.n_fake_tiles;
@@ -184,33 +197,30 @@ struct Fused {
       const int64_t n_here = fake ? p.n_fake : p.n_real;
       const bool sampled = fake && p.fake_x == nullptr;
 
-      // ---- 1. tile inputs ---------------------------------------------------
-      if (tid < kT) {
-        const int64_t i = ev0 + tid;
-        const bool valid = i < n_here;
+      // ---- 1. tile inputs: thread (event, coordinate) ---------------------------
+      if (tid < kT * F) {
+        const int ev = tid / F, j = tid % F;
+        const int64_t i = ev0 + ev;
         if (sampled) {
           // E is a multiple of T here, so the whole tile uses one parameter row.
           const int row = tile / p.tiles_per_row;
           const Words w = event_words(p.src.base + (uint64_t)i, p.src.stream, p.src.k0, p.src.k1);
-#pragma unroll
-          for (int j = 0; j < F; ++j) {
-            const Shape sh = make_shape(p.src.theta[row * 2 * F + 2 * j], p.src.theta[row * 2 * F + 2 * j + 1]);
-            const Quantile q = kumaraswamy(uniform_u(w.w[j]), sh);
-            float da, db;
-            pathwise(q, sh, da, db);
-            sm.X[tid][j] = q.x;
-            sm.dxd[tid][j][0] = da;
-            sm.dxd[tid][j][1] = db;
-          }
+          const Shape sh = make_shape(p.src.theta[row * 2 * F + 2 * j], p.src.theta[row * 2 * F + 2 * j + 1]);
+          const Quantile q = kumaraswamy(uniform_u(w.w[j]), sh);
+          float da, db;
+          pathwise(q, sh, da, db);
+          sm.X[ev][j] = q.x;
+          sm.dxd[ev][j][0] = da;
+          sm.dxd[ev][j][1] = db;
         } else {
           const float* src = fake ? p.fake_x : p.real_x;
-#pragma unroll
-          for (int j = 0; j < F; ++j) sm.X[tid][j] = valid ? src[i * F + j] : 0.5f;
+          sm.X[ev][j] = (i < n_here) ? src[i * F + j] : 0.5f;
         }
       }
       __syncthreads();
 
       // ---- 2. first layer (VALU): A_1 = leaky(X W1^T + b1) -------------------
+#pragma unroll 4
       for (int ev = vpart; ev < kT; ev += PPO) {
         float v = b1r;
 #pragma unroll
@@ -222,44 +232,39 @@ struct Fused {
       // ---- 3. hidden layers on the matrix cores -----------------------------
 #pragma unroll
       for (int l = 0; l < NH; ++l) {
-        f32x4 acc[RB][CB];
-        gemm(p.Wh[l], &sm.act[l][0][0], acc, o0, lr, lg);
+        f32x4 acc[CB];
+        gemm(p.Wh[l], &sm.act[l][0][0], acc, o0, e0, lr, lg);
+        const int o = o0 + 4 * lg;
+        const f32x4 bias = *reinterpret_cast<const f32x4*>(p.bh[l] + o);
 #pragma unroll
-        for (int rb = 0; rb < RB; ++rb) {
-          const int o = o0 + 16 * rb + 4 * lg;
-          const f32x4 bias = *reinterpret_cast<const f32x4*>(p.bh[l] + o);
-#pragma unroll
-          for (int cb = 0; cb < CB; ++cb) {
-            f32x4 v = acc[rb][cb] + bias;
-            v.x = leaky(v.x, slope); v.y = leaky(v.y, slope);
-            v.z = leaky(v.z, slope); v.w = leaky(v.w, slope);
-            *reinterpret_cast<f32x4*>(&sm.act[l + 1][16 * cb + lr][o]) = v;
-          }
+        for (int cb = 0; cb < CB; ++cb) {
+          f32x4 v = acc[cb] + bias;
+          v.x = leaky(v.x, slope); v.y = leaky(v.y, slope);
+          v.z = leaky(v.z, slope); v.w = leaky(v.w, slope);
+          *reinterpret_cast<f32x4*>(&sm.act[l + 1][e0 + 16 * cb + lr][o]) = v;
         }
         __syncthreads();
       }
 
       // ---- 4. logits and BCE seeds ------------------------------------------
       {
-        // thread (ev = tid / 4, part = tid % 4) sums H/4 features
-        const int ev = tid >> 2, part = tid & 3;
-        const float* hrow = &sm.act[NH][ev][part * (H / 4)];
-        const float* wo = p.Wo + part * (H / 4);
+        const float* hrow = &sm.act[NH][dev_][dpart * DSPAN];
+        const float* wo = p.Wo + dpart * DSPAN;
         float z = 0.f;
 #pragma unroll
-        for (int k = 0; k < H / 4; k += 4) {
+        for (int k = 0; k < DSPAN; k += 4) {
           const f32x4 hv = *reinterpret_cast<const f32x4*>(hrow + k);
           const f32x4 wv = *reinterpret_cast<const f32x4*>(wo + k);
           z = fmaf(hv.x, wv.x, z); z = fmaf(hv.y, wv.y, z);
           z = fmaf(hv.z, wv.z, z); z = fmaf(hv.w, wv.w, z);
         }
-        z += __shfl_xor(z, 1, 64);
-        z += __shfl_xor(z, 2, 64);
+#pragma unroll
+        for (int m = 1; m < PARTS; m <<= 1) z += __shfl_xor(z, m, 64);
         z += p.bo[0];
-        const int64_t i = ev0 + ev;
+        const int64_t i = ev0 + dev_;
         const bool valid = i < n_here;
         float l0 = 0.f, l1 = 0.f;
-        if (part == 0) {
+        if (dpart == 0) {
           float eD = 0.f, eG = 0.f;
           if (valid) {
             const float sig_neg = 1.0f / (1.0f + expf(z));   // sigmoid(-z)
@@ -275,8 +280,8 @@ struct Fused {
               if (p.logits_real) p.logits_real[i] = z;
             }
           }
-          sm.eD[ev] = eD;
-          sm.eG[ev] = eG;
+          sm.eD[dev_] = eD;
+          sm.eG[dev_] = eG;
         }
         l0 = wave_sum(l0);
         l1 = wave_sum(l1);
@@ -286,23 +291,19 @@ struct Fused {
       if (tid < 2) {
         float s = 0.f;
 #pragma unroll
-        for (int w = 0; w < kThreads / 64; ++w) s += sm.red[2 * w + tid];
+        for (int w = 0; w < WAVES; ++w) s += sm.red[2 * w + tid];
         p.loss_part[(int64_t)tile * 2 + tid] = s;
       }
 
-      // ---- 5. logit-layer gradients; delta_{NH+1} in place --------------------
+      // ---- 5. logit-layer gradients and delta_{NH+1} in place, one pass --------
+#pragma unroll 4
       for (int ev = vpart; ev < kT; ev += PPO) {
         const float e = sm.eD[ev];
-        acc_dWo = fmaf(e, sm.act[NH][ev][vo], acc_dWo);
+        float& h = sm.act[NH][ev][vo];
+        const float hv = h;
+        acc_dWo = fmaf(e, hv, acc_dWo);
         if (vo == 0) acc_dbo += e;
-      }
-      __syncthreads();
-      {
-        const float wo = p.Wo[vo];
-        for (int ev = vpart; ev < kT; ev += PPO) {
-          float& h = sm.act[NH][ev][vo];
-          h = wo * leaky_grad(h, slope);
-        }
+        h = wor * leaky_grad(hv, slope);
       }
       __syncthreads();
 
@@ -313,28 +314,25 @@ struct Fused {
         const float* dout = &sm.act[dbuf(l + 2)][0][0];
         float* din = &sm.act[dbuf(l + 1)][0][0];
         const float* Ain = &sm.act[l][0][0];
-        wgrad(dout, Ain, sm.eD, accW[l], o0, lr, lg);
-        for (int ev = vpart; ev < kT; ev += PPO) acc_dbh[l] = fmaf(sm.eD[ev], dout[ev * LD + vo], acc_dbh[l]);
-        f32x4 acc[RB][CB];
-        gemm(p.WhT[l], dout, acc, o0, lr, lg);
+        wgrad(dout, Ain, sm.eD, accW[l], dbacc[l], o0, e0, lr, lg);
+        f32x4 acc[CB];
+        gemm(p.WhT[l], dout, acc, o0, e0, lr, lg);
+        const int k = o0 + 4 * lg;
 #pragma unroll
-        for (int rb = 0; rb < RB; ++rb) {
-          const int k = o0 + 16 * rb + 4 * lg;
-#pragma unroll
-          for (int cb = 0; cb < CB; ++cb) {
-            const int ev = 16 * cb + lr;
-            const f32x4 h = *reinterpret_cast<const f32x4*>(Ain + ev * LD + k);
-            f32x4 v = acc[rb][cb];
-            v.x *= leaky_grad(h.x, slope); v.y *= leaky_grad(h.y, slope);
-            v.z *= leaky_grad(h.z, slope); v.w *= leaky_grad(h.w, slope);
-            *reinterpret_cast<f32x4*>(din + ev * LD + k) = v;
-          }
+        for (int cb = 0; cb < CB; ++cb) {
+          const int ev = e0 + 16 * cb + lr;
+          const f32x4 h = *reinterpret_cast<const f32x4*>(Ain + ev * LD + k);
+          f32x4 v = acc[cb];
+          v.x *= leaky_grad(h.x, slope); v.y *= leaky_grad(h.y, slope);
+          v.z *= leaky_grad(h.z, slope); v.w *= leaky_grad(h.w, slope);
+          *reinterpret_cast<f32x4*>(din + ev * LD + k) = v;
         }
         __syncthreads();
       }
 
       // ---- 7. first-layer gradients --------------------------------------------
       const float* d1 = &sm.act[dbuf(1)][0][0];
+#pragma unroll 4
       for (int ev = vpart; ev < kT; ev += PPO) {
         const float ed = sm.eD[ev] * d1[ev * LD + vo];
         acc_db1 += ed;
@@ -344,29 +342,42 @@ struct Fused {
 
       // ---- 8. fake events: dL_G/dx and the per-parameter partial ---------------
       if (fake) {
-        float ta = 0.f, tb = 0.f;
-        int jj = 0;
-        if (tid < kT * F) {
-          const int ev = tid / F;
-          jj = tid % F;
-          float g = 0.f;
-          const float* drow = d1 + ev * LD;
-#pragma unroll 8
-          for (int o = 0; o < H; ++o) g = fmaf(drow[o], p.W1[o * F + jj], g);
-          g *= sm.eG[ev];
-          const int64_t i = ev0 + ev;
-          if (p.dLg_dx && i < n_here) p.dLg_dx[i * F + jj] = g;
-          if (sampled) {
-            ta = g * sm.dxd[ev][jj][0];
-            tb = g * sm.dxd[ev][jj][1];
+        // thread (dev_, dpart) sums its H / PARTS first-layer rows for every input j
+        float g[F];
+#pragma unroll
+        for (int j = 0; j < F; ++j) g[j] = 0.f;
+        const float* drow = d1 + dev_ * LD + dpart * DSPAN;
+        const float* wrow = sm.W1 + dpart * DSPAN * F;
+#pragma unroll
+        for (int k = 0; k < DSPAN; k += 4) {
+          const f32x4 dv = *reinterpret_cast<const f32x4*>(drow + k);
+#pragma unroll
+          for (int j = 0; j < F; ++j) {
+            g[j] = fmaf(dv.x, wrow[(k + 0) * F + j], g[j]);
+            g[j] = fmaf(dv.y, wrow[(k + 1) * F + j], g[j]);
+            g[j] = fmaf(dv.z, wrow[(k + 2) * F + j], g[j]);
+            g[j] = fmaf(dv.w, wrow[(k + 3) * F + j], g[j]);
+          }
+        }
+#pragma unroll
+        for (int j = 0; j < F; ++j) {
+#pragma unroll
+          for (int m = 1; m < PARTS; m <<= 1) g[j] += __shfl_xor(g[j], m, 64);
+        }
+        if (dpart == 0) {
+          const float eg = sm.eG[dev_];
+          const int64_t i = ev0 + dev_;
+#pragma unroll
+          for (int j = 0; j < F; ++j) {
+            g[j] *= eg;
+            if (p.dLg_dx && i < n_here) p.dLg_dx[i * F + j] = g[j];
+            if (sampled) {
+              sm.red[2 * (dev_ * F + j)] = g[j] * sm.dxd[dev_][j][0];
+              sm.red[2 * (dev_ * F + j) + 1] = g[j] * sm.dxd[dev_][j][1];
+            }
           }
         }
         if (sampled) {
-          __syncthreads();
-          if (tid < kT * F) {
-            sm.red[2 * tid] = ta;
-            sm.red[2 * tid + 1] = tb;
-          }
           __syncthreads();
           if (tid < 2 * F) {
             // component c = 2 j + (a|b); terms stored at red[2 (ev F + j) + ab]
@@ -376,34 +387,65 @@ struct Fused {
             p.theta_part[(int64_t)tile * 2 * F + tid] = s;
           }
         }
-        (void)jj;
       }
       __syncthreads();
     }
 
     // ---- per-workgroup partials ------------------------------------------------
     float* out = p.wg_part + (int64_t)blockIdx.x * P;
+    // hidden dW: waves with equal rows and different event groups are added in ew order
+    float* stage = &sm.act[0][0][0];           // WE > 1: [NH][16][H] per event group
 #pragma unroll
-    for (int l = 0; l < NH; ++l)
+    for (int g = 0; g < WE; ++g) {
+      if (ew == g) {
 #pragma unroll
-      for (int rb = 0; rb < RB; ++rb)
+        for (int l = 0; l < NH; ++l)
 #pragma unroll
-        for (int kb = 0; kb < KB; ++kb)
+          for (int kb = 0; kb < KB; ++kb)
 #pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const int o = o0 + 16 * rb + 4 * lg + r, k = 16 * kb + lr;
-            out[l * P_DWH + o * H + k] = accW[l][rb][kb][r];
+            for (int r = 0; r < 4; ++r) {
+              const int o = o0 + 4 * lg + r, k = 16 * kb + lr;
+              float v = accW[l][kb][r];
+              if (WE > 1) {
+                float& st = stage[(l * H + o) * H + k];
+                v = (g == 0) ? v : st + v;
+                if (g < WE - 1) st = v;
+              }
+              if (g == WE - 1) out[l * P_DWH + o * H + k] = v;
+            }
+      }
+      if (WE > 1) __syncthreads();
+    }
+    // hidden-layer db: lanes lg = 0..3 hold four event classes of row o0 + lr
+    float* dbst = &sm.red[0];
+#pragma unroll
+    for (int g = 0; g < WE; ++g) {
+      if (ew == g) {
+#pragma unroll
+        for (int l = 0; l < NH; ++l) {
+          float v = dbacc[l];
+          v += __shfl_xor(v, 16, 64);
+          v += __shfl_xor(v, 32, 64);
+          if (lg == 0) {
+            if (WE > 1) {
+              float& st = dbst[l * H + o0 + lr];
+              v = (g == 0) ? v : st + v;
+              if (g < WE - 1) st = v;
+            }
+            if (g == WE - 1) out[l * P_DWH + H * H + o0 + lr] = v;
           }
+        }
+      }
+      if (WE > 1) __syncthreads();
+    }
     // VALU partials: combine the PPO parts of each feature in a fixed order
     float* red = &sm.act[0][0][0];
-    constexpr int NV = NH + F + 2;  // dbh[NH], dW1[F], db1, dWo per feature
+    constexpr int NV = F + 2;  // dW1[F], db1, dWo per feature
     __syncthreads();
 #pragma unroll
-    for (int l = 0; l < NH; ++l) red[(0 * NV + l) * kThreads + tid] = acc_dbh[l];
-#pragma unroll
-    for (int j = 0; j < F; ++j) red[(NH + j) * kThreads + tid] = acc_dW1[j];
-    red[(NH + F) * kThreads + tid] = acc_db1;
-    red[(NH + F + 1) * kThreads + tid] = acc_dWo;
+    for (int j = 0; j < F; ++j) red[j * kThreads + tid] = acc_dW1[j];
+    red[F * kThreads + tid] = acc_db1;
+    red[(F + 1) * kThreads + tid] = acc_dWo;
     red[NV * kThreads + tid] = acc_dbo;
     __syncthreads();
     if (tid < H) {
@@ -415,11 +457,9 @@ struct Fused {
         v[c] = s;
       }
 #pragma unroll
-      for (int l = 0; l < NH; ++l) out[l * P_DWH + H * H + tid] = v[l];
-#pragma unroll
-      for (int j = 0; j < F; ++j) out[OFF_W1 + tid * F + j] = v[NH + j];
-      out[OFF_W1 + H * F + tid] = v[NH + F];
-      out[OFF_WO + tid] = v[NH + F + 1];
+      for (int j = 0; j < F; ++j) out[OFF_W1 + tid * F + j] = v[j];
+      out[OFF_W1 + H * F + tid] = v[F];
+      out[OFF_WO + tid] = v[F + 1];
     }
     if (tid == 0) {
       float s = 0.f;
@@ -527,7 +567,7 @@ Layout layout_for(const DiscArgs& a, int n_wg) {
   const int64_t nft = (a.n_fake + kT - 1) / kT, nrt = (a.n_real + kT - 1) / kT;
   size_t o = 0;
   L.off_wt = o; o += align256(sizeof(float) * NH * H * H);
-  L.off_wg = o; o += align256(sizeof(float) * (size_t)n_wg * K::P);
+  L.off_wg = o; o += align256(sizeof(float) * (size_t)n_wg * kWGPerCU * K::P);
   L.off_loss = o; o += align256(sizeof(float) * 2 * (size_t)(nft + nrt));
   L.off_theta = o; o += align256(sizeof(float) * 2 * F * (size_t)nft);
   L.total = o;
@@ -562,6 +602,8 @@ const Variant* find_variant(const sagips_mlp& D) {
 }
 
 }  // namespace
+
+int disc_f32_tile() { return kT; }
 
 bool disc_f32_supported(const sagips_mlp& D, int d, const char** why) {
   if (D.features != SAGIPS_FEAT_IDENTITY) { *why = "fp32 discriminator supports IDENTITY features only"; return false; }
@@ -621,7 +663,7 @@ hipError_t launch_disc_f32(const DiscArgs& a, void* ws, int n_cu, hipStream_t st
     hipLaunchKernelGGL(k_transpose, dim3(H / 32, H / 32), dim3(256), 0, st, p.Wh[l], const_cast<float*>(p.WhT[l]), H);
   if (tm) tm->end();
   if (tm) tm->begin("disc_f32_fused");
-  hipLaunchKernelGGL(v->fn, dim3(n_cu), dim3(kThreads), 0, st, p);
+  hipLaunchKernelGGL(v->fn, dim3(n_cu * kWGPerCU), dim3(kThreads), 0, st, p);
   if (tm) tm->end();
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
@@ -643,7 +685,7 @@ hipError_t launch_disc_f32(const DiscArgs& a, void* ws, int n_cu, hipStream_t st
     sg.off[n] = offwo + H; sg.len[n] = 1; sg.dst[n++] = a.out->db[NH + 1];
     sg.n = n;
     hipLaunchKernelGGL(k_reduce_wg, dim3((L.P + kRedElems - 1) / kRedElems), dim3(kRedElems * kRedSlices), 0, st,
-                       p.wg_part, n_cu, L.P, sg);
+                       p.wg_part, n_cu * kWGPerCU, L.P, sg);
   }
   if (a.out->loss_d || a.out->loss_g)
     hipLaunchKernelGGL(k_reduce_loss, dim3(1), dim3(256), 0, st, p.loss_part, p.n_fake_tiles, p.n_tiles, p.inv_nf,
