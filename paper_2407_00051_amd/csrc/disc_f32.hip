@@ -109,7 +109,6 @@ struct Fused {
     float dxd[kT][F][2];
     float eD[kT];
     float eG[kT];
-    float W1[H * F];
     float red[2 * kT * 4];   // >= 2 T F and >= 2 * waves
   };
 
@@ -140,22 +139,46 @@ struct Fused {
     }
   }
 
-  // accW += sum over this wave's events of e[ev] delta[ev][o] A[ev][k], o in
-  // the wave's 16 rows; dbacc += the e-scaled delta values this lane loaded.
+  // Weight-gradient tiles use a permuted row / column order against LDS bank
+  // conflicts.  LDS serves a 64-lane 4-byte read as two passes of 32 lanes over
+  // 32 banks; a pass here covers 2 event rows (4 banks apart, row stride H+4
+  // floats) x 16 columns, so the 16 columns of a block sit at 8 (i/4) + (i%4)
+  // and the neighbouring block fills the gaps (+4).  Row i of wave-row wr is
+  // rowmap(wr, i), column j of block kb is colmap(kb, j); both are bijections
+  // onto [0, H).
+  static constexpr __device__ int rowmap(int wr, int i) {
+    return 32 * (wr >> 1) + 8 * (i >> 2) + 4 * (wr & 1) + (i & 3);
+  }
+  static constexpr __device__ int colmap(int kb, int j) {
+    return 32 * (kb >> 1) + 8 * (j >> 2) + 4 * (kb & 1) + (j & 3);
+  }
+
+  // accW += sum over this wave's events of e[ev] delta[ev][o] A[ev][k] for the
+  // wave's rows o = rowmap(wr, .); dbacc += the e-scaled delta values this lane loaded.
   static __device__ __forceinline__ void wgrad(const float* dlt, const float* A, const float* e,
-                                               f32x4 (&accW)[KB], float& dbacc, int o0, int e0, int lr, int lg) {
+                                               f32x4 (&accW)[KB], float& dbacc, int wr, int e0, int lr, int lg) {
+    const int orow = rowmap(wr, lr);
+    int kcol[KB];
+#pragma unroll
+    for (int kb = 0; kb < KB; ++kb) kcol[kb] = colmap(kb, lr);
 #pragma unroll 4
     for (int q = 0; q < TE / 4; ++q) {
       const int ev = e0 + 4 * q + lg;
-      const float a = e[ev] * dlt[ev * LD + o0 + lr];
+      const float a = e[ev] * dlt[ev * LD + orow];
       dbacc += a;
       float b[KB];
 #pragma unroll
-      for (int kb = 0; kb < KB; ++kb) b[kb] = A[ev * LD + 16 * kb + lr];
+      for (int kb = 0; kb < KB; ++kb) b[kb] = A[ev * LD + kcol[kb]];
 #pragma unroll
       for (int kb = 0; kb < KB; ++kb) accW[kb] = mfma4(a, b[kb], accW[kb]);
     }
   }
+
+  // Per-event dot products over the H features: thread part dp (of PARTS)
+  // takes the float4 chunks at 4 dp + 32 c, c < H / (4 PARTS), so that the
+  // eight parts of one event read one contiguous 128-byte row segment.
+  static constexpr int NCH = H / (4 * PARTS);
+  static constexpr __device__ int chunk_off(int dp, int c) { return 4 * dp + 32 * c; }
 
   static __device__ void run(const F32Params& p) {
     __shared__ Smem sm;
@@ -186,10 +209,15 @@ struct Fused {
     for (int j = 0; j < F; ++j) w1r[j] = p.W1[vo * F + j];
     const float b1r = p.b1[vo];
     const float wor = p.Wo[vo];
-    for (int k = tid; k < H * F; k += kThreads) sm.W1[k] = p.W1[k];
     // per-event dot products: thread (ev = tid / PARTS, part = tid % PARTS) covers H / PARTS features
     const int dev_ = tid / PARTS, dpart = tid % PARTS;
-    constexpr int DSPAN = H / PARTS;
+    float w1c[NCH][4][F];     // the first-layer weights of this thread's features
+#pragma unroll
+    for (int c = 0; c < NCH; ++c)
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+#pragma unroll
+        for (int j = 0; j < F; ++j) w1c[c][q][j] = p.W1[(chunk_off(dpart, c) + q) * F + j];
 
     for (int tile = blockIdx.x; tile < p.n_tiles; tile += gridDim.x) {
       const bool fake = tile < p.n_fake_tiles;
@@ -248,13 +276,13 @@ struct Fused {
 
       // ---- 4. logits and BCE seeds ------------------------------------------
       {
-        const float* hrow = &sm.act[NH][dev_][dpart * DSPAN];
-        const float* wo = p.Wo + dpart * DSPAN;
+        const float* hrow = &sm.act[NH][dev_][0];
         float z = 0.f;
 #pragma unroll
-        for (int k = 0; k < DSPAN; k += 4) {
-          const f32x4 hv = *reinterpret_cast<const f32x4*>(hrow + k);
-          const f32x4 wv = *reinterpret_cast<const f32x4*>(wo + k);
+        for (int c = 0; c < NCH; ++c) {
+          const int f = chunk_off(dpart, c);
+          const f32x4 hv = *reinterpret_cast<const f32x4*>(hrow + f);
+          const f32x4 wv = *reinterpret_cast<const f32x4*>(p.Wo + f);
           z = fmaf(hv.x, wv.x, z); z = fmaf(hv.y, wv.y, z);
           z = fmaf(hv.z, wv.z, z); z = fmaf(hv.w, wv.w, z);
         }
@@ -314,7 +342,7 @@ struct Fused {
         const float* dout = &sm.act[dbuf(l + 2)][0][0];
         float* din = &sm.act[dbuf(l + 1)][0][0];
         const float* Ain = &sm.act[l][0][0];
-        wgrad(dout, Ain, sm.eD, accW[l], dbacc[l], o0, e0, lr, lg);
+        wgrad(dout, Ain, sm.eD, accW[l], dbacc[l], wave % WR, e0, lr, lg);
         f32x4 acc[CB];
         gemm(p.WhT[l], dout, acc, o0, e0, lr, lg);
         const int k = o0 + 4 * lg;
@@ -346,17 +374,16 @@ struct Fused {
         float g[F];
 #pragma unroll
         for (int j = 0; j < F; ++j) g[j] = 0.f;
-        const float* drow = d1 + dev_ * LD + dpart * DSPAN;
-        const float* wrow = sm.W1 + dpart * DSPAN * F;
+        const float* drow = d1 + dev_ * LD;
 #pragma unroll
-        for (int k = 0; k < DSPAN; k += 4) {
-          const f32x4 dv = *reinterpret_cast<const f32x4*>(drow + k);
+        for (int c = 0; c < NCH; ++c) {
+          const f32x4 dv = *reinterpret_cast<const f32x4*>(drow + chunk_off(dpart, c));
 #pragma unroll
           for (int j = 0; j < F; ++j) {
-            g[j] = fmaf(dv.x, wrow[(k + 0) * F + j], g[j]);
-            g[j] = fmaf(dv.y, wrow[(k + 1) * F + j], g[j]);
-            g[j] = fmaf(dv.z, wrow[(k + 2) * F + j], g[j]);
-            g[j] = fmaf(dv.w, wrow[(k + 3) * F + j], g[j]);
+            g[j] = fmaf(dv.x, w1c[c][0][j], g[j]);
+            g[j] = fmaf(dv.y, w1c[c][1][j], g[j]);
+            g[j] = fmaf(dv.z, w1c[c][2][j], g[j]);
+            g[j] = fmaf(dv.w, w1c[c][3][j], g[j]);
           }
         }
 #pragma unroll
@@ -404,7 +431,7 @@ struct Fused {
           for (int kb = 0; kb < KB; ++kb)
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
-              const int o = o0 + 4 * lg + r, k = 16 * kb + lr;
+              const int o = rowmap(wave % WR, 4 * lg + r), k = colmap(kb, lr);
               float v = accW[l][kb][r];
               if (WE > 1) {
                 float& st = stage[(l * H + o) * H + k];
@@ -416,7 +443,7 @@ struct Fused {
       }
       if (WE > 1) __syncthreads();
     }
-    // hidden-layer db: lanes lg = 0..3 hold four event classes of row o0 + lr
+    // hidden-layer db: lanes lg = 0..3 hold four event classes of row rowmap(wr, lr)
     float* dbst = &sm.red[0];
 #pragma unroll
     for (int g = 0; g < WE; ++g) {
@@ -427,12 +454,13 @@ struct Fused {
           v += __shfl_xor(v, 16, 64);
           v += __shfl_xor(v, 32, 64);
           if (lg == 0) {
+            const int o = rowmap(wave % WR, lr);
             if (WE > 1) {
-              float& st = dbst[l * H + o0 + lr];
+              float& st = dbst[l * H + o];
               v = (g == 0) ? v : st + v;
               if (g < WE - 1) st = v;
             }
-            if (g == WE - 1) out[l * P_DWH + H * H + o0 + lr] = v;
+            if (g == WE - 1) out[l * P_DWH + H * H + o] = v;
           }
         }
       }
@@ -474,9 +502,16 @@ __global__ __launch_bounds__(kThreads, 1) void k_disc_f32(F32Params p) {
   Fused<H, NH, F>::run(p);
 }
 
-// WT[k][o] = W[o][k] for one H x H layer.
-__global__ __launch_bounds__(256) void k_transpose(const float* __restrict__ W, float* __restrict__ WT, int H) {
+// WT[k][o] = W[o][k] for the H x H hidden layers (blockIdx.z = layer).
+struct TransposeArgs {
+  const float* W[kMaxNH];
+  float* WT[kMaxNH];
+};
+
+__global__ __launch_bounds__(256) void k_transpose(TransposeArgs t_, int H) {
   __shared__ float t[32][33];
+  const float* W = t_.W[blockIdx.z];
+  float* WT = t_.WT[blockIdx.z];
   const int bx = blockIdx.x * 32, by = blockIdx.y * 32;
   const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;
   for (int r = ty; r < 32; r += 8) t[r][tx] = W[(by + r) * H + bx + tx];
@@ -484,8 +519,11 @@ __global__ __launch_bounds__(256) void k_transpose(const float* __restrict__ W, 
   for (int r = ty; r < 32; r += 8) WT[(bx + r) * H + by + tx] = t[tx][r];
 }
 
-// Fixed-order sum over workgroups of every partial element, scattered to the
-// caller's gradient arrays through a segment table.
+// All fixed-order reductions after the fused kernel, in one launch:
+//   blocks [0, wg_blocks)        sum over workgroups of every gradient partial,
+//                                scattered to the caller's arrays (segment table);
+//   block  wg_blocks             the two losses from the per-tile sums;
+//   blocks wg_blocks + 1 + row   dL_G/dtheta of one parameter row from its tiles.
 struct Segments {
   int n;
   int off[2 * kMaxNH + 4];
@@ -493,63 +531,78 @@ struct Segments {
   float* dst[2 * kMaxNH + 4];
 };
 
+struct ReduceArgs {
+  const float* wg_part;
+  int n_wg, P, wg_blocks;
+  Segments sg;
+  const float* loss_part;
+  int n_fake_tiles, n_tiles;
+  float inv_nf, inv_nr;
+  float* loss_d;
+  float* loss_g;
+  const float* theta_part;
+  int tiles_per_row, C;
+  float* dLg_dtheta;
+};
+
 constexpr int kRedElems = 32;   // elements per block
 constexpr int kRedSlices = 8;   // workgroup ranges summed side by side, then combined in order
 
-__global__ __launch_bounds__(256) void k_reduce_wg(const float* __restrict__ part, int n_wg, int P, Segments sg) {
-  __shared__ float red[kRedSlices][kRedElems];
-  const int le = threadIdx.x % kRedElems, sl = threadIdx.x / kRedElems;
-  const int e = blockIdx.x * kRedElems + le;
-  const int per = (n_wg + kRedSlices - 1) / kRedSlices;
-  const int g0 = sl * per, g1 = min(n_wg, g0 + per);
-  float s = 0.f;
-  if (e < P)
-    for (int g = g0; g < g1; ++g) s += part[(int64_t)g * P + e];
-  red[sl][le] = s;
-  __syncthreads();
-  if (sl != 0 || e >= P) return;
-  float t = 0.f;
+__global__ __launch_bounds__(256) void k_reduce_all(ReduceArgs r) {
+  __shared__ float red[256];
+  const int tid = threadIdx.x;
+  if ((int)blockIdx.x < r.wg_blocks) {
+    const int le = tid % kRedElems, sl = tid / kRedElems;
+    const int e = blockIdx.x * kRedElems + le;
+    const int per = (r.n_wg + kRedSlices - 1) / kRedSlices;
+    const int g0 = sl * per, g1 = min(r.n_wg, g0 + per);
+    float s = 0.f;
+    if (e < r.P)
+      for (int g = g0; g < g1; ++g) s += r.wg_part[(int64_t)g * r.P + e];
+    red[sl * kRedElems + le] = s;
+    __syncthreads();
+    if (sl != 0 || e >= r.P) return;
+    float t = 0.f;
 #pragma unroll
-  for (int q = 0; q < kRedSlices; ++q) t += red[q][le];
-  for (int i = 0; i < sg.n; ++i)
-    if (e >= sg.off[i] && e < sg.off[i] + sg.len[i]) {
-      if (sg.dst[i]) sg.dst[i][e - sg.off[i]] = t;
-      break;
+    for (int q = 0; q < kRedSlices; ++q) t += red[q * kRedElems + le];
+    for (int i = 0; i < r.sg.n; ++i)
+      if (e >= r.sg.off[i] && e < r.sg.off[i] + r.sg.len[i]) {
+        if (r.sg.dst[i]) r.sg.dst[i][e - r.sg.off[i]] = t;
+        break;
+      }
+    return;
+  }
+  if ((int)blockIdx.x == r.wg_blocks) {
+    float sf = 0.f, sgg = 0.f, sr = 0.f;
+    for (int t = tid; t < r.n_tiles; t += 256) {
+      if (t < r.n_fake_tiles) { sf += r.loss_part[2 * t]; sgg += r.loss_part[2 * t + 1]; }
+      else sr += r.loss_part[2 * t];
     }
-}
-
-// Losses from the per-tile partial sums (one block, fixed order).
-__global__ __launch_bounds__(256) void k_reduce_loss(const float* __restrict__ loss_part, int n_fake_tiles,
-                                                     int n_tiles, float inv_nf, float inv_nr,
-                                                     float* __restrict__ loss_d, float* __restrict__ loss_g) {
-  __shared__ float red[3][4];
-  float sf = 0.f, sg = 0.f, sr = 0.f;
-  for (int t = threadIdx.x; t < n_tiles; t += 256) {
-    if (t < n_fake_tiles) { sf += loss_part[2 * t]; sg += loss_part[2 * t + 1]; }
-    else sr += loss_part[2 * t];
+    sf = wave_sum(sf); sgg = wave_sum(sgg); sr = wave_sum(sr);
+    if ((tid & 63) == 0) { red[3 * (tid >> 6)] = sf; red[3 * (tid >> 6) + 1] = sgg; red[3 * (tid >> 6) + 2] = sr; }
+    __syncthreads();
+    if (tid == 0) {
+      float a = 0.f, b = 0.f, c = 0.f;
+      for (int w = 0; w < 4; ++w) { a += red[3 * w]; b += red[3 * w + 1]; c += red[3 * w + 2]; }
+      if (r.loss_d) *r.loss_d = c * r.inv_nr + a * r.inv_nf;
+      if (r.loss_g) *r.loss_g = b * r.inv_nf;
+    }
+    return;
   }
-  sf = wave_sum(sf); sg = wave_sum(sg); sr = wave_sum(sr);
-  if ((threadIdx.x & 63) == 0) {
-    red[0][threadIdx.x >> 6] = sf; red[1][threadIdx.x >> 6] = sg; red[2][threadIdx.x >> 6] = sr;
-  }
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    float a = 0.f, b = 0.f, c = 0.f;
-    for (int w = 0; w < 4; ++w) { a += red[0][w]; b += red[1][w]; c += red[2][w]; }
-    if (loss_d) *loss_d = c * inv_nr + a * inv_nf;
-    if (loss_g) *loss_g = b * inv_nf;
-  }
-}
-
-// dL_G/dtheta[row][c] = fixed-order sum of the row's tile partials.
-__global__ __launch_bounds__(64) void k_reduce_theta(const float* __restrict__ theta_part, int tiles_per_row, int C,
-                                                     float* __restrict__ out) {
-  const int row = blockIdx.x;
-  const int c = threadIdx.x;
-  if (c >= C) return;
+  // one parameter row: thread (component c, slice s) sums tiles s, s + S, ...; slices combined in order
+  const int row = blockIdx.x - r.wg_blocks - 1;
+  const int S = 256 / r.C;
+  const int c = tid % r.C, sl = tid / r.C;
   float s = 0.f;
-  for (int t = 0; t < tiles_per_row; ++t) s += theta_part[((int64_t)row * tiles_per_row + t) * C + c];
-  out[row * C + c] = s;
+  if (sl < S)
+    for (int t = sl; t < r.tiles_per_row; t += S) s += r.theta_part[((int64_t)row * r.tiles_per_row + t) * r.C + c];
+  red[tid] = s;
+  __syncthreads();
+  if (tid < r.C) {
+    float t = 0.f;
+    for (int q = 0; q < S; ++q) t += red[q * r.C + tid];
+    r.dLg_dtheta[row * r.C + tid] = t;
+  }
 }
 
 inline size_t align256(size_t b) { return (b + 255) & ~(size_t)255; }
@@ -659,8 +712,12 @@ hipError_t launch_disc_f32(const DiscArgs& a, void* ws, int n_cu, hipStream_t st
   p.theta_part = reinterpret_cast<float*>(base + L.off_theta);
 
   if (tm) tm->begin("disc_f32_transpose");
-  for (int l = 0; l < NH; ++l)
-    hipLaunchKernelGGL(k_transpose, dim3(H / 32, H / 32), dim3(256), 0, st, p.Wh[l], const_cast<float*>(p.WhT[l]), H);
+  {
+    TransposeArgs ta;
+    memset(&ta, 0, sizeof(ta));
+    for (int l = 0; l < NH; ++l) { ta.W[l] = p.Wh[l]; ta.WT[l] = const_cast<float*>(p.WhT[l]); }
+    hipLaunchKernelGGL(k_transpose, dim3(H / 32, H / 32, NH), dim3(256), 0, st, ta, H);
+  }
   if (tm) tm->end();
   if (tm) tm->begin("disc_f32_fused");
   hipLaunchKernelGGL(v->fn, dim3(n_cu * kWGPerCU), dim3(kThreads), 0, st, p);
@@ -668,10 +725,13 @@ hipError_t launch_disc_f32(const DiscArgs& a, void* ws, int n_cu, hipStream_t st
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
 
-  if (tm) tm->begin("disc_f32_reduce");
+  ReduceArgs r;
+  memset(&r, 0, sizeof(r));
+  r.wg_part = p.wg_part;
+  r.n_wg = n_cu * kWGPerCU;
+  r.P = L.P;
   if (a.out->dW[0]) {
-    Segments sg;
-    memset(&sg, 0, sizeof(sg));
+    Segments& sg = r.sg;
     int n = 0;
     for (int l = 0; l < NH; ++l) {
       sg.off[n] = l * (H * H + H); sg.len[n] = H * H; sg.dst[n++] = a.out->dW[1 + l];
@@ -684,15 +744,22 @@ hipError_t launch_disc_f32(const DiscArgs& a, void* ws, int n_cu, hipStream_t st
     sg.off[n] = offwo; sg.len[n] = H; sg.dst[n++] = a.out->dW[NH + 1];
     sg.off[n] = offwo + H; sg.len[n] = 1; sg.dst[n++] = a.out->db[NH + 1];
     sg.n = n;
-    hipLaunchKernelGGL(k_reduce_wg, dim3((L.P + kRedElems - 1) / kRedElems), dim3(kRedElems * kRedSlices), 0, st,
-                       p.wg_part, n_cu * kWGPerCU, L.P, sg);
+    r.wg_blocks = (L.P + kRedElems - 1) / kRedElems;
   }
-  if (a.out->loss_d || a.out->loss_g)
-    hipLaunchKernelGGL(k_reduce_loss, dim3(1), dim3(256), 0, st, p.loss_part, p.n_fake_tiles, p.n_tiles, p.inv_nf,
-                       p.inv_nr, a.out->loss_d, a.out->loss_g);
-  if (a.fake_src && a.out->dLg_dtheta)
-    hipLaunchKernelGGL(k_reduce_theta, dim3(a.fake_src->n_theta), dim3(64), 0, st, p.theta_part, p.tiles_per_row,
-                       2 * F, a.out->dLg_dtheta);
+  r.loss_part = p.loss_part;
+  r.n_fake_tiles = p.n_fake_tiles;
+  r.n_tiles = p.n_tiles;
+  r.inv_nf = p.inv_nf;
+  r.inv_nr = p.inv_nr;
+  r.loss_d = a.out->loss_d;
+  r.loss_g = a.out->loss_g;
+  r.theta_part = p.theta_part;
+  r.tiles_per_row = p.tiles_per_row;
+  r.C = 2 * F;
+  r.dLg_dtheta = a.out->dLg_dtheta;
+  const int theta_blocks = (a.fake_src && a.out->dLg_dtheta) ? a.fake_src->n_theta : 0;
+  if (tm) tm->begin("disc_f32_reduce");
+  hipLaunchKernelGGL(k_reduce_all, dim3(r.wg_blocks + 1 + theta_blocks), dim3(256), 0, st, r);
   if (tm) tm->end();
   return hipGetLastError();
 }
