@@ -50,6 +50,32 @@ __device__ __forceinline__ u16 bf16_bits(float f) {
 }
 __device__ __forceinline__ float bf16_to_f32(u16 h) { return __uint_as_float(((uint32_t)h) << 16); }
 
+// PER consecutive bf16 values (PER = 4 or 8, 8- or 16-byte aligned) <-> fp32.
+template <int PER>
+__device__ __forceinline__ void load_bf16(const u16* p, float (&v)[PER]) {
+  uint32_t w[PER / 2];
+  if constexpr (PER == 4) {
+    const uint2 t = *reinterpret_cast<const uint2*>(p);
+    w[0] = t.x; w[1] = t.y;
+  } else {
+    const uint4 t = *reinterpret_cast<const uint4*>(p);
+    w[0] = t.x; w[1] = t.y; w[2] = t.z; w[3] = t.w;
+  }
+#pragma unroll
+  for (int q = 0; q < PER / 2; ++q) {
+    v[2 * q] = __uint_as_float(w[q] << 16);
+    v[2 * q + 1] = __uint_as_float(w[q] & 0xffff0000u);
+  }
+}
+template <int PER>
+__device__ __forceinline__ void store_bf16(u16* p, const float (&v)[PER]) {
+  uint32_t w[PER / 2];
+#pragma unroll
+  for (int q = 0; q < PER / 2; ++q) w[q] = (uint32_t)bf16_bits(v[2 * q]) | ((uint32_t)bf16_bits(v[2 * q + 1]) << 16);
+  if constexpr (PER == 4) *reinterpret_cast<uint2*>(p) = make_uint2(w[0], w[1]);
+  else *reinterpret_cast<uint4*>(p) = make_uint4(w[0], w[1], w[2], w[3]);
+}
+
 __device__ __forceinline__ float leaky(float v, float s) { return v > 0.0f ? v : s * v; }
 __device__ __forceinline__ float leaky_grad(float h, float s) { return h > 0.0f ? 1.0f : s; }
 __device__ __forceinline__ float softplus(float t) { return fmaxf(t, 0.0f) + log1pf(expf(-fabsf(t))); }
@@ -264,7 +290,7 @@ __global__ __launch_bounds__(256) void k_gemm(const u16* __restrict__ in, const 
 // Logit layer and BCE seeds for one chunk.  One wave per row: lanes split H.
 // Writes e_D[r] (0 on padding), e_G[r], delta_L (unit seed, bf16), logits,
 // and per-block partials of the loss sums, dW_o and db_o.
-constexpr int kRowBlocks = 512;   // blocks of the row-reduction kernels (fixed partial count)
+constexpr int kRowBlocks = 2048;  // blocks of the row-reduction kernels (fixed partial count)
 
 inline int row_blocks(int rows) { return std::max(1, std::min(kRowBlocks, (rows + 63) / 64)); }
 inline int rows_per_block(int rows, int blocks) { return (rows + blocks - 1) / blocks; }
@@ -286,39 +312,53 @@ __global__ __launch_bounds__(256) void k_logit(const u16* __restrict__ AL, const
   for (int q = 0; q < per; ++q) acc_dwo[q] = 0.f;
   float l0 = 0.f, l1 = 0.f, sum_e = 0.f;
   const int rbase = blockIdx.x * rpb;
-  for (int rr = wave; rr < rpb; rr += 4) {
-    const int r = rbase + rr;
-    if (r >= c.rows) break;
-    const u16* hrow = AL + (int64_t)r * H + lane * per;
-    float h[PER];
+  constexpr int R = 4;                 // rows per wave per iteration (independent loads in flight)
+  for (int rr0 = wave * R; rr0 < rpb; rr0 += 4 * R) {
+    float h[R][PER];
+    float z[R];
 #pragma unroll
-    for (int q = 0; q < per; ++q) h[q] = bf16_to_f32(hrow[q]);
-    float z = 0.f;
+    for (int k = 0; k < R; ++k) {
+      const int r = rbase + rr0 + k;
+      if (rr0 + k < rpb && r < c.rows) load_bf16<PER>(AL + (int64_t)r * H + lane * per, h[k]);
+      else {
 #pragma unroll
-    for (int q = 0; q < per; ++q) z = fmaf(h[q], wo[q], z);
-    z = wave_sum(z) + bo[0];
-    const bool valid = r < c.valid;
-    float e = 0.f, g = 0.f;
-    if (valid) {
-      const float sig_neg = 1.0f / (1.0f + expf(z));
-      if (c.fake) {
-        e = (1.0f - sig_neg) * inv_n;
-        g = -sig_neg * inv_n;
-        l0 += softplus(z);
-        l1 += softplus(-z);
-      } else {
-        e = -sig_neg * inv_n;
-        l0 += softplus(-z);
+        for (int q = 0; q < per; ++q) h[k][q] = 0.f;
       }
-      if (lane == 0 && logits) logits[c.row0 + r] = z;
-    }
-    if (lane == 0) { eD[r] = e; eG[r] = g; }
-    sum_e += e;
-    u16* drow = dL + (int64_t)r * H + lane * per;
+      float zz = 0.f;
 #pragma unroll
-    for (int q = 0; q < per; ++q) {
-      acc_dwo[q] = fmaf(e, h[q], acc_dwo[q]);
-      drow[q] = bf16_bits(wo[q] * leaky_grad(h[q], slope));
+      for (int q = 0; q < per; ++q) zz = fmaf(h[k][q], wo[q], zz);
+      z[k] = zz;
+    }
+#pragma unroll
+    for (int k = 0; k < R; ++k) z[k] = wave_sum(z[k]) + bo[0];
+#pragma unroll
+    for (int k = 0; k < R; ++k) {
+      const int r = rbase + rr0 + k;
+      if (rr0 + k >= rpb || r >= c.rows) break;
+      const bool valid = r < c.valid;
+      float e = 0.f, g = 0.f;
+      if (valid) {
+        const float sig_neg = 1.0f / (1.0f + expf(z[k]));
+        if (c.fake) {
+          e = (1.0f - sig_neg) * inv_n;
+          g = -sig_neg * inv_n;
+          l0 += softplus(z[k]);
+          l1 += softplus(-z[k]);
+        } else {
+          e = -sig_neg * inv_n;
+          l0 += softplus(-z[k]);
+        }
+        if (lane == 0 && logits) logits[c.row0 + r] = z[k];
+      }
+      if (lane == 0) { eD[r] = e; eG[r] = g; }
+      sum_e += e;
+      float d[PER];
+#pragma unroll
+      for (int q = 0; q < per; ++q) {
+        acc_dwo[q] = fmaf(e, h[k][q], acc_dwo[q]);
+        d[q] = wo[q] * leaky_grad(h[k][q], slope);
+      }
+      store_bf16<PER>(dL + (int64_t)r * H + lane * per, d);
     }
   }
 #pragma unroll
@@ -482,10 +522,11 @@ __global__ __launch_bounds__(256) void k_first_bwd(const u16* __restrict__ d1, c
     float g[F];
 #pragma unroll
     for (int j = 0; j < F; ++j) g[j] = 0.f;
-    const u16* drow = d1 + (int64_t)r * H + lane * per;
+    float dvs[PER];
+    load_bf16<PER>(d1 + (int64_t)r * H + lane * per, dvs);
 #pragma unroll
     for (int q = 0; q < per; ++q) {
-      const float dv = bf16_to_f32(drow[q]);
+      const float dv = dvs[q];
       const float ed = e * dv;
       const int o = lane * per + q;
 #pragma unroll
