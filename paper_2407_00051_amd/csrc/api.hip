@@ -177,7 +177,7 @@ sagips_status disc_bf16(sagips_ctx* c, const sagips_mlp* D, const float* fake_x,
   char* ws = static_cast<char*>(c->ws);
   if (want_theta && !o2.dLg_dx) o2.dLg_dx = reinterpret_cast<float*>(ws + off_g);
   Timer* tm = timer_of(c);
-  hipError_t e = launch_disc_bf16(a, ws, c->stream, tm);
+  hipError_t e = launch_disc_bf16(a, ws, c->n_cu, c->stream, tm);
   if (e != hipSuccess) return hip_fail(c, e, "disc_fwd_bwd (bf16) launch");
   if (want_theta) {
     e = launch_param_grad(sa, o2.dLg_dx, out->dLg_dtheta, nullptr, ws + off_pg, c->stream, tm);

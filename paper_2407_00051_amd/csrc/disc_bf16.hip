@@ -399,7 +399,9 @@ __device__ __forceinline__ bf16x8 tr_fragment(const u16* tile, int row0, int col
   return bf16x8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
 }
 
-__global__ __launch_bounds__(256) void k_wgrad(const u16* __restrict__ dlt, const u16* __restrict__ A,
+// Global loads run two steps ahead of their LDS writes (two register sets),
+// so a step's HBM latency is covered by the matrix work of the two before it.
+__global__ __launch_bounds__(256, 2) void k_wgrad(const u16* __restrict__ dlt, const u16* __restrict__ A,
                                                const float* __restrict__ eD, int H, int rows_per_slice,
                                                int rows, float* __restrict__ P /*[slices][H][H]*/,
                                                float* __restrict__ Pdb /*[slices][H]*/) {
@@ -418,26 +420,34 @@ __global__ __launch_bounds__(256) void k_wgrad(const u16* __restrict__ dlt, cons
   // staging map: 32 rows x 128 cols = 512 pieces of 8 bf16, 2 per thread (same columns every step)
   const int srow = tid >> 4, scol = (tid & 15) * 8;   // piece p: row srow + 16 p
   float db[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-  auto stage = [&](int buf, int r0) {
+  struct Regs { uint4 d0, d1, a0, a1; float e0, e1; };
+  auto load = [&](Regs& R, int r0) __attribute__((always_inline)) {
+    const int64_t ra = r0 + srow, rb = ra + 16;
+    R.e0 = eD[ra];
+    R.e1 = eD[rb];
+    R.d0 = *reinterpret_cast<const uint4*>(dlt + ra * H + o0 + scol);
+    R.d1 = *reinterpret_cast<const uint4*>(dlt + rb * H + o0 + scol);
+    R.a0 = *reinterpret_cast<const uint4*>(A + ra * H + i0 + scol);
+    R.a1 = *reinterpret_cast<const uint4*>(A + rb * H + i0 + scol);
+  };
+  auto write = [&](const Regs& R, int buf) __attribute__((always_inline)) {
 #pragma unroll
     for (int p = 0; p < 2; ++p) {
       const int row = srow + 16 * p;
-      const int64_t r = r0 + row;
-      const float e = eD[r];
-      const uint4 dv = *reinterpret_cast<const uint4*>(dlt + r * H + o0 + scol);
+      const uint4 dv = p ? R.d1 : R.d0;
+      const float ev = p ? R.e1 : R.e0;
       const uint32_t w[4] = {dv.x, dv.y, dv.z, dv.w};
       uint32_t o[4];
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
-        const float a0 = e * bf16_to_f32((u16)(w[q] & 0xffff));
-        const float a1 = e * bf16_to_f32((u16)(w[q] >> 16));
+        const float a0 = ev * __uint_as_float(w[q] << 16);
+        const float a1 = ev * __uint_as_float(w[q] & 0xffff0000u);
         db[2 * q] += a0;
         db[2 * q + 1] += a1;
         o[q] = (uint32_t)bf16_bits(a0) | ((uint32_t)bf16_bits(a1) << 16);
       }
       *reinterpret_cast<uint4*>(&sD[buf][row * kWLD + scol]) = make_uint4(o[0], o[1], o[2], o[3]);
-      *reinterpret_cast<uint4*>(&sA[buf][row * kWLD + scol]) =
-          *reinterpret_cast<const uint4*>(A + r * H + i0 + scol);
+      *reinterpret_cast<uint4*>(&sA[buf][row * kWLD + scol]) = p ? R.a1 : R.a0;
     }
   };
 
@@ -446,12 +456,7 @@ __global__ __launch_bounds__(256) void k_wgrad(const u16* __restrict__ dlt, cons
   for (int i = 0; i < 4; ++i)
 #pragma unroll
     for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-  const int nsteps = (rend - rbeg) / kWK;   // rows are multiples of 128, slices multiples of 32
-  if (nsteps > 0) stage(0, rbeg);
-  __syncthreads();
-  for (int s = 0; s < nsteps; ++s) {
-    const int buf = s & 1;
-    if (s + 1 < nsteps) stage(buf ^ 1, rbeg + (s + 1) * kWK);
+  auto compute = [&](int buf) __attribute__((always_inline)) {
     bf16x8 a[4], b[4];
 #pragma unroll
     for (int i = 0; i < 4; ++i) a[i] = tr_fragment(sD[buf], 0, wo + 16 * i, lane);
@@ -461,7 +466,26 @@ __global__ __launch_bounds__(256) void k_wgrad(const u16* __restrict__ dlt, cons
     for (int i = 0; i < 4; ++i)
 #pragma unroll
       for (int j = 0; j < 4; ++j) acc[i][j] = mfma_bf16(a[i], b[j], acc[i][j]);
-    __syncthreads();
+  };
+  const int nsteps = (rend - rbeg) / kWK;   // rows are multiples of 128, slices multiples of 32
+  // invariant at the top of step s (parity ph): R[ph ^ 1] holds step s+1, R[ph] holds step s+2
+  Regs R[2];
+  if (nsteps > 0) load(R[0], rbeg);
+  if (nsteps > 1) load(R[1], rbeg + kWK);
+  if (nsteps > 0) write(R[0], 0);
+  if (nsteps > 2) load(R[0], rbeg + 2 * kWK);
+  __syncthreads();
+  for (int s0 = 0; s0 < nsteps; s0 += 2) {
+#pragma unroll
+    for (int ph = 0; ph < 2; ++ph) {
+      const int s = s0 + ph;
+      if (s < nsteps) {
+        compute(ph);
+        if (s + 1 < nsteps) write(R[ph ^ 1], ph ^ 1);
+        if (s + 3 < nsteps) load(R[ph ^ 1], rbeg + (s + 3) * kWK);
+      }
+      __syncthreads();
+    }
   }
   float* out = P + (int64_t)slice * H * H;
 #pragma unroll
@@ -478,11 +502,11 @@ __global__ __launch_bounds__(256) void k_wgrad(const u16* __restrict__ dlt, cons
     for (int q = 0; q < 8; ++q) sdb[tid][q] = db[q];
     __syncthreads();
     if (tid < kGT) {
-      // column tid = scol + q of thread (tid/8)*... : threads with equal (tid & 15) share columns
+      // threads t with equal t & 15 stage the same 8 columns 8 (t & 15) .. + 7
       const int piece = tid >> 3, q = tid & 7;   // column = 8 * piece + q
-      float s = 0.f;
-      for (int t = piece; t < 256; t += 16) s += sdb[t][q];
-      Pdb[(int64_t)slice * H + o0 + 8 * piece + q] = s;
+      float sum = 0.f;
+      for (int t = piece; t < 256; t += 16) sum += sdb[t][q];
+      Pdb[(int64_t)slice * H + o0 + 8 * piece + q] = sum;
     }
   }
 }
@@ -661,6 +685,8 @@ struct Plan {
 
 int pad128(int64_t n) { return (int)((n + 127) / 128 * 128); }
 
+
+
 Plan make_plan(const DiscArgs& a) {
   const sagips_mlp& D = *a.D;
   Plan p;
@@ -674,7 +700,7 @@ Plan make_plan(const DiscArgs& a) {
   p.logit_blocks = kRowBlocks;
   p.fb_blocks = kRowBlocks;
   const int tiles = (p.H / kGT) * (p.H / kGT);
-  p.slices = std::max(1, 256 / tiles);
+  p.slices = std::max(1, 768 / tiles);   // three weight-gradient blocks per CU
   const size_t H = p.H, R = p.rows_max;
   size_t o = 0;
   p.off_wb = o; o += al(2 * H * H * p.NH);
@@ -714,7 +740,7 @@ bool disc_bf16_supported(const sagips_mlp& D, int d, const char** why) {
 
 size_t disc_bf16_workspace(const DiscArgs& a) { return make_plan(a).total; }
 
-hipError_t launch_disc_bf16(const DiscArgs& a, void* ws, hipStream_t st, Timer* tm) {
+hipError_t launch_disc_bf16(const DiscArgs& a, void* ws, int n_cu, hipStream_t st, Timer* tm) {
   const sagips_mlp& Dm = *a.D;
   const Plan p = make_plan(a);
   char* base = static_cast<char*>(ws);

@@ -69,6 +69,6 @@ hipError_t launch_disc_f32(const DiscArgs& a, void* ws, int n_cu, hipStream_t st
 // Samples the fake events itself when a.fake_src is set (any E); never writes dLg_dtheta.
 bool disc_bf16_supported(const sagips_mlp& D, int d, const char** why);
 size_t disc_bf16_workspace(const DiscArgs& a);
-hipError_t launch_disc_bf16(const DiscArgs& a, void* ws, hipStream_t st, Timer* tm);
+hipError_t launch_disc_bf16(const DiscArgs& a, void* ws, int n_cu, hipStream_t st, Timer* tm);
 
 }  // namespace sagips
