@@ -25,7 +25,12 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 PEAK = {"mfma_f32": 157.3e12, "mfma_bf16": 2.5e15, "hbm": 8.0e12}
+# VALU issue: 256 CUs x 4 SIMDs, each issuing per 4-clock quad-cycle either two
+# full-rate wave64 VALU instructions or one half of a transcendental (which
+# takes two quad-cycles and pairs with nothing); 2.4 GHz peak clock.
+SIMD_QUAD_CYCLES_PER_S = 256 * 4 * 2.4e9 / 4
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
+VALU_FILE = os.path.join(ROOT, "profiles", "valu.json")
 KERNEL_SOURCES = {
     "disc_f32_fused": ["paper_2407_00051_amd/csrc/disc_f32.hip", "paper_2407_00051_amd/csrc/device_math.hpp"],
     "bf16_gemm": ["paper_2407_00051_amd/csrc/disc_bf16.hip", "paper_2407_00051_amd/csrc/device_math.hpp"],
@@ -63,6 +68,27 @@ def read_traffic(kernel: str, workload: str):
         return float(e["bytes_per_launch"])
     except (OSError, KeyError, ValueError):
         return None
+
+
+def read_valu_mix(kernel: str, workload: str):
+    """Executed VALU and transcendental instructions per event from the committed counter run,
+    or None if the kernel changed since."""
+    try:
+        with open(VALU_FILE) as f:
+            e = json.load(f)[kernel][workload]
+        if e.get("source_hash") != source_hash(kernel):
+            return None
+        return float(e["valu_per_event"]), float(e["trans_per_event"])
+    except (OSError, KeyError, ValueError):
+        return None
+
+
+def valu_peak_events(valu: float, trans: float) -> float:
+    """Events/s if every SIMD issued this instruction stream with no idle quad-cycle: one wave
+    instruction serves 64 events; full-rate instructions pair two per quad-cycle, transcendentals
+    take two quad-cycles each."""
+    quad_cycles_per_64_events = (valu - trans) / 2 + 2 * trans
+    return SIMD_QUAD_CYCLES_PER_S * 64 / quad_cycles_per_64_events
 
 
 def cpu_baseline(w, inp, rows: int, events: int, min_seconds: float = 10.0):
@@ -197,7 +223,12 @@ def main():
         roof = {"bound": bound, "achieved": achieved / 1e12, "peak": peak / 1e12, "unit": unit,
                 "frac": achieved / peak}
     else:
-        roof = {"bound": bound, "achieved": N / (avg_ms * 1e-3) / 1e9, "peak": None, "unit": unit, "frac": None}
+        achieved = N / (avg_ms * 1e-3)
+        mix = read_valu_mix(dominant, w.name)
+        peak_ev = valu_peak_events(*mix) if mix else None
+        roof = {"bound": bound, "achieved": achieved / 1e9, "peak": peak_ev / 1e9 if mix else None, "unit": unit,
+                "frac": achieved / peak_ev if mix else None,
+                "valu_per_event": mix[0] if mix else None, "trans_per_event": mix[1] if mix else None}
     if w.widths is not None:
         roof["step_mfma_frac"] = mlp_flops_per_fake_event(w.widths) * N / (ms_per_step * 1e-3) / peak
     tr = read_traffic(dominant, w.name)

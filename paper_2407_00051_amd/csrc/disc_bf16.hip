@@ -130,11 +130,11 @@ __global__ __launch_bounds__(256) void k_prep(ChunkArgs c, const float* __restri
 #pragma unroll
       for (int j = 0; j < D; ++j) {
         const Shape sh = make_shape(src.theta[row * 2 * D + 2 * j], src.theta[row * 2 * D + 2 * j + 1]);
-        const Quantile q = kumaraswamy(uniform_u(w.w[j]), sh);
+        const Quantile q = kumaraswamy_w(w.w[j], sh);
         x[j] = q.x;
         if constexpr (kHD8) {
-          if (j == 0) lnx1 = q.lam * sh.ra;
-          if (j == D - 1) ln1mx3 = log1mexp(q.lam * sh.ra);
+          if (j == 0) lnx1 = log_x(q, sh);
+          if (j == D - 1) ln1mx3 = log1mexp(log_x(q, sh));
         }
       }
     } else {

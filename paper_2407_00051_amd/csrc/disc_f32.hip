@@ -234,7 +234,7 @@ struct Fused {
           const int row = tile / p.tiles_per_row;
           const Words w = event_words(p.src.base + (uint64_t)i, p.src.stream, p.src.k0, p.src.k1);
           const Shape sh = make_shape(p.src.theta[row * 2 * F + 2 * j], p.src.theta[row * 2 * F + 2 * j + 1]);
-          const Quantile q = kumaraswamy(uniform_u(w.w[j]), sh);
+          const Quantile q = kumaraswamy_w(w.w[j], sh);
           float da, db;
           pathwise(q, sh, da, db);
           sm.X[ev][j] = q.x;

@@ -37,7 +37,7 @@ __global__ __launch_bounds__(kThreads) void k_sample(SourceArgs s, float* __rest
     if (x) {
       float xv[D];
 #pragma unroll
-      for (int j = 0; j < D; ++j) xv[j] = kumaraswamy(uniform_u(w.w[j]), sh[j]).x;
+      for (int j = 0; j < D; ++j) xv[j] = kumaraswamy_w(w.w[j], sh[j]).x;
       if constexpr (D == 2) {
         reinterpret_cast<float2*>(x)[i] = make_float2(xv[0], xv[1]);
       } else {
@@ -82,7 +82,7 @@ __global__ __launch_bounds__(kThreads) void k_param_grad(SourceArgs s, const flo
     }
 #pragma unroll
     for (int j = 0; j < D; ++j) {
-      const Quantile q = kumaraswamy(uniform_u(w.w[j]), sh[j]);
+      const Quantile q = kumaraswamy_w(w.w[j], sh[j]);
       float da, db;
       pathwise(q, sh[j], da, db);
       float g;
