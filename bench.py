@@ -33,7 +33,9 @@ TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
 VALU_FILE = os.path.join(ROOT, "profiles", "valu.json")
 KERNEL_SOURCES = {
     "disc_f32_fused": ["paper_2407_00051_amd/csrc/disc_f32.hip", "paper_2407_00051_amd/csrc/device_math.hpp"],
-    "bf16_gemm": ["paper_2407_00051_amd/csrc/disc_bf16.hip", "paper_2407_00051_amd/csrc/device_math.hpp"],
+    "bf16_fwd_chain": ["paper_2407_00051_amd/csrc/disc_bf16.hip", "paper_2407_00051_amd/csrc/device_math.hpp"],
+    "bf16_bwd_chain": ["paper_2407_00051_amd/csrc/disc_bf16.hip", "paper_2407_00051_amd/csrc/device_math.hpp"],
+    "bf16_wgrad": ["paper_2407_00051_amd/csrc/disc_bf16.hip", "paper_2407_00051_amd/csrc/device_math.hpp"],
     "param_grad": ["paper_2407_00051_amd/csrc/sampler.hip", "paper_2407_00051_amd/csrc/device_math.hpp"],
 }
 
@@ -180,12 +182,14 @@ def main():
             dominant = "disc_f32_fused"
             flops_per_launch = mlp_flops_per_fake_event(w.widths) * N
         else:
-            # the bf16 step runs layer by layer; its dominant kernel is the forward /
-            # backward-data product: per step 2 * NH products of 2 H^2 flops per row
-            dominant = "bf16_gemm"
+            # The bf16 step runs three kinds of launches per chunk of rows: the forward
+            # chain, the backward chain and one weight-gradient product per hidden layer.
+            # Each kind carries NH hidden products of 2 H^2 flops per row over the fake and
+            # the real batch per step; the dominant kind is chosen after timing.
+            dominant = None
             H, NH = w.widths[1], len(w.widths) - 3
-            chunks = 2 * ((N + (1 << 20) - 1) >> 20)
-            flops_per_launch = 2 * NH * 2 * H * H * (2 * N) / (2 * NH * chunks)
+            flops_per_step_kind = NH * 2 * H * H * (2 * N)
+            flops_per_launch = None
         bound, unit, peak = "mfma", "TFLOP/s", PEAK["mfma_f32" if prec == sg.F32 else "mfma_bf16"]
         dtype = "f32" if prec == sg.F32 else "bf16"
     else:
@@ -216,8 +220,14 @@ def main():
     ms_per_step = (t1 - t0) * 1e3 / args.steps
     value = N / (ms_per_step * 1e-3)
 
+    if dominant is None:
+        kinds = [k for k in ("bf16_fwd_chain", "bf16_bwd_chain", "bf16_wgrad") if k in kt]
+        dominant = max(kinds, key=lambda k: kt[k][1])
+        flops_per_launch = flops_per_step_kind / (kt[dominant][0] / args.steps)
     launches, total_ms = kt.get(dominant, (0, 0.0))
-    avg_ms = total_ms / max(launches, 1)
+    if launches == 0:
+        raise RuntimeError(f"no timed launches of {dominant}")
+    avg_ms = total_ms / launches
     if flops_per_launch is not None:
         achieved = flops_per_launch / (avg_ms * 1e-3)
         roof = {"bound": bound, "achieved": achieved / 1e12, "peak": peak / 1e12, "unit": unit,

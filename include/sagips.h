@@ -86,7 +86,8 @@ typedef struct {
  *              backward signals rounded to nearest even) with fp32 accumulate;
  *              the first and the logit layer stay fp32.
  * Supported shapes: n_layers >= 2; all hidden widths equal, one of 64, 128
- * (F32) or 256, 512 (BF16); width[0] in {2, 3, 8}.                       */
+ * (F32) or 256, 512 (BF16); width[0] in {2, 3, 8}.  BF16 also needs
+ * 0 <= leaky_slope <= 1 (SAGIPS_E_UNSUPPORTED otherwise).                 */
 typedef struct {
   int32_t n_layers;
   int32_t width[SAGIPS_MAX_LAYERS + 1];

@@ -165,7 +165,7 @@ sagips_status disc_bf16(sagips_ctx* c, const sagips_mlp* D, const float* fake_x,
   sagips_disc_out o2 = *out;
   o2.dLg_dtheta = nullptr;
   a.out = &o2;
-  const size_t disc_ws = (disc_bf16_workspace(a) + 255) & ~(size_t)255;
+  const size_t disc_ws = (disc_bf16_workspace(a, c->n_cu) + 255) & ~(size_t)255;
   size_t off_g = disc_ws, off_pg = disc_ws, total = disc_ws;
   const bool want_theta = out->dLg_dtheta != nullptr;
   if (want_theta) {

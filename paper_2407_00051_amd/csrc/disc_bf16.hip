@@ -1,29 +1,30 @@
 // bf16-operand / fp32-accumulate discriminator step on gfx950 for wide
-// networks (hidden width 256 or 512), where weight gradients cannot stay in
-// registers across tiles.  The step is processed in chunks of event rows
-// (all fake or all real); each chunk goes through these kernels:
+// networks (hidden width 256 or 512), where the hidden weight gradients do not
+// fit in registers across tiles.  The step is processed in chunks of event
+// rows (all fake or all real); each chunk goes through these kernels:
 //
-//   k_prep      features of every row (sampling fake events in place, HD8 map)
-//   k_first_fwd A_1 = bf16(LeakyReLU(feat W1^T + b1))          (VALU, K <= 8)
-//   k_gemm<FWD> A_{l+1} = bf16(LeakyReLU(A_l W^T + b))         (bf16 MFMA)
-//   k_logit     z = A_L w_o + b_o, BCE seeds, delta_L = bf16(w_o * leaky'(A_L))
-//   k_wgrad     dW partials = sum_rows (e_D delta) (x) A        (bf16 MFMA, K = rows)
-//   k_gemm<BWD> delta_l = bf16((delta_{l+1} W) * leaky'(A_l))  (bf16 MFMA)
-//   k_first_bwd dW1, db1 partials and dL_G/dx (through the HD8 Jacobian)
+//   k_prep       features of every row (sampling fake events in place, HD8 map)
+//   k_fwd_chain  per tile of rows, in LDS: A_1 = bf16(LeakyReLU(feat W1^T + b1))
+//                (VALU, K <= 8), then every hidden layer on the bf16 matrix
+//                cores, then the logit z and the BCE seeds e_D, e_G; stores
+//                A_1 .. A_NH and the activation sign masks
+//   k_bwd_chain  per tile, in LDS: the unit-seed signal from the logit layer
+//                down to A_1 (matrix cores, LeakyReLU' from the masks); stores
+//                the signals the weight gradients need; first-layer dW_1, db_1
+//                and dL_G/dx (through the HD8 Jacobian)
+//   k_wgrad      dW partials = sum_rows bf16(e_D delta) (x) A  (K = rows)
 //
-// Activations and signals are stored event-major [rows][H] bf16.  Forward
-// and backward-data products compute out^T = W' in^T (M = output feature,
+// Forward and backward products compute outT = W' inT (M = output feature,
 // N = event, K = input feature): both operands then have K contiguous in
 // memory and the accumulator fragment of a lane is 4 consecutive features of
-// one event, an 8-byte event-major store.  The weight-gradient product has
-// K = events; its operands are read from event-major LDS tiles with the
-// gfx950 transpose load ds_read_b64_tr_b16, which hands every lane 4
-// consecutive rows of one column.
+// one event.  The weight-gradient product has K = events; its operands are
+// read from event-major LDS tiles with the gfx950 transpose load
+// ds_read_b64_tr_b16, which hands every lane 4 consecutive rows of one column.
 //
 // Backward signals carry a unit seed per event; the weight gradients scale
 // them by e_D = dL_D/dz while staging (and round to bf16 again), dL_G/dx
 // scales the first-layer signal by e_G = dL_G/dz.  All sums are fixed-order:
-// chunk partials are added to fp32 accumulators chunk by chunk.
+// per-workgroup partials are added to fp32 accumulators chunk by chunk.
 #include "device_math.hpp"
 #include "kernels.hpp"
 
@@ -167,216 +168,541 @@ __global__ __launch_bounds__(256) void k_prep(ChunkArgs c, const float* __restri
   for (int j = 0; j < F; ++j) feat[(int64_t)r * F + j] = f[j];
 }
 
-// A_1[r][o] for 8 consecutive o per thread.
-template <int F>
-__global__ __launch_bounds__(256) void k_first_fwd(const float* __restrict__ feat, const float* __restrict__ W1,
-                                                   const float* __restrict__ b1, int H, int rows, float slope,
-                                                   u16* __restrict__ A1) {
-  const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  const int per_row = H / 8;
-  const int64_t r = t / per_row;
-  const int o0 = (int)(t % per_row) * 8;
-  if (r >= rows) return;
-  float f[F];
-#pragma unroll
-  for (int j = 0; j < F; ++j) f[j] = feat[r * F + j];
-  uint32_t packed[4];
-#pragma unroll
-  for (int q = 0; q < 4; ++q) {
-    float v2[2];
-#pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      const int o = o0 + 2 * q + h;
-      float v = b1[o];
-#pragma unroll
-      for (int j = 0; j < F; ++j) v = fmaf(W1[o * F + j], f[j], v);
-      v2[h] = leaky(v, slope);
-    }
-    packed[q] = (uint32_t)bf16_bits(v2[0]) | ((uint32_t)bf16_bits(v2[1]) << 16);
+// ---------------------------------------------------------------------------
+// Per-tile layer chains.  A persistent workgroup of 4 waves per CU (one per
+// SIMD, so each wave has the whole register file of its SIMD) loops over
+// tiles of T event rows; the tile's activations (forward) or unit-seed signals
+// (backward) live in LDS as [T][H + 8] bf16 and are overwritten layer by
+// layer, so between layers nothing goes through HBM except what the
+// weight-gradient products need later.  Wave w owns output features
+// [16 MI w, 16 MI (w + 1)) of every product outT = W' inT for all T events:
+// MI x JW = 32 MFMA tiles, so each K block of 32 takes MI 16-byte weight
+// loads (global, L2-resident, issued PD blocks ahead) and JW 16-byte LDS
+// reads (issued one block ahead) for 32 MFMAs.  The 16-byte row pad makes
+// each 8-lane group of an LDS fragment read hit distinct banks.  Lane l holds,
+// for MFMA tile (i, j), the outputs o = ow + 16 i + 4 (l / 16) + q, q < 4, of
+// event 16 j + (l % 16); the forward's first layer (K = F, VALU) produces its
+// outputs in the same arrangement.
+//
+// Signs of the hidden activations are kept as lane-local bit masks: the 128
+// outputs a lane holds in one layer are numbered e = 4 (i JW + j) + q and bit
+// 31 - e % 32 of word e / 32 is set where the bf16 activation is > 0; each
+// lane stores its 4 words as one 16-byte vector, [layer][tile][wave][lane].
+// The backward chain has the same lane arrangement and reads them back, so
+// LeakyReLU' costs 16 bytes per lane and layer instead of the activations.
+constexpr int kChainThreads = 256;
+constexpr int kChainBlocksPerCU = 1;
+
+template <int H>
+struct Chain {
+  static constexpr int WAVES = kChainThreads / 64;
+  static constexpr int MI = H / (16 * WAVES);   // 16-feature MFMA tiles per wave
+  static constexpr int JW = 32 / MI;            // 16-event MFMA tiles per wave
+  static constexpr int T = 16 * JW;             // events per tile
+  static constexpr int LDA = H + 8;             // LDS row stride (bf16)
+  static constexpr int PD = 2;                  // weight prefetch distance (K blocks)
+  static_assert(MI * JW == 32 && T * H == 32768, "chain decomposition");
+};
+
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+
+// Two fp32 values -> a packed bf16 pair, round to nearest even
+// (v_cvt_pk_bf16_f32, identical to bf16_bits on every non-NaN input).
+__device__ __forceinline__ uint32_t pack_bf16(float lo, float hi) {
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2{lo, hi}), bf16x2_t));
+}
+__device__ __forceinline__ float lo_bf16(uint32_t p) { return __uint_as_float(p << 16); }
+
+// Row-contiguous copy of a [T][H] bf16 tile from LDS (row stride LDA) to
+// global memory (row stride H): 16 bytes per lane, whole 128-byte lines.
+template <int H, int T, int LDA, int NT>
+__device__ __forceinline__ void copy_out(const u16* act, u16* __restrict__ gdst, int tid) {
+  constexpr int PR = H / 8;   // 16-byte pieces per row
+#pragma unroll 4
+  for (int k = tid; k < T * PR; k += NT) {
+    const int row = k / PR, col = (k % PR) * 8;
+    *reinterpret_cast<uint4*>(gdst + (int64_t)row * H + col) = *reinterpret_cast<const uint4*>(act + row * LDA + col);
   }
-  *reinterpret_cast<uint4*>(A1 + r * H + o0) = make_uint4(packed[0], packed[1], packed[2], packed[3]);
+}
+__device__ __forceinline__ float hi_bf16(uint32_t p) { return __uint_as_float(p & 0xffff0000u); }
+
+// acc[i][j] = init[i] + sum_k Wg[ow + 16 i + 4 lg + q][k] act[16 j + lr][k]
+template <int H>
+__device__ __forceinline__ void chain_gemm(const u16* __restrict__ Wg, const u16* act,
+                                           f32x4 (&acc)[Chain<H>::MI][Chain<H>::JW],
+                                           const f32x4 (&init)[Chain<H>::MI], int ow, int lr, int lg) {
+  using C = Chain<H>;
+  constexpr int KB = H / 32, PD = C::PD, LDA = C::LDA, MI = C::MI, JW = C::JW;
+#pragma unroll
+  for (int i = 0; i < MI; ++i)
+#pragma unroll
+    for (int j = 0; j < JW; ++j) acc[i][j] = init[i];
+  const u16* wrow = Wg + (size_t)(ow + lr) * H + 8 * lg;
+  const u16* brow = act + lr * LDA + 8 * lg;
+  bf16x8 a[PD + 1][MI];
+  bf16x8 b[2][JW];
+#pragma unroll
+  for (int q = 0; q < PD; ++q)
+#pragma unroll
+    for (int i = 0; i < MI; ++i) a[q][i] = *reinterpret_cast<const bf16x8*>(wrow + (size_t)16 * i * H + 32 * q);
+#pragma unroll
+  for (int j = 0; j < JW; ++j) b[0][j] = *reinterpret_cast<const bf16x8*>(brow + 16 * j * LDA);
+#pragma unroll
+  for (int kb = 0; kb < KB; ++kb) {
+    if (kb + PD < KB) {
+#pragma unroll
+      for (int i = 0; i < MI; ++i)
+        a[(kb + PD) % (PD + 1)][i] = *reinterpret_cast<const bf16x8*>(wrow + (size_t)16 * i * H + 32 * (kb + PD));
+    }
+    if (kb + 1 < KB) {
+#pragma unroll
+      for (int j = 0; j < JW; ++j)
+        b[(kb + 1) & 1][j] = *reinterpret_cast<const bf16x8*>(brow + 16 * j * LDA + 32 * (kb + 1));
+    }
+    // keep the prefetches above the products of this block (the scheduler
+    // would otherwise sink each load next to its first use)
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int j = 0; j < JW; ++j)
+#pragma unroll
+      for (int i = 0; i < MI; ++i) acc[i][j] = mfma_bf16(a[kb % (PD + 1)][i], b[kb & 1][j], acc[i][j]);
+    __builtin_amdgcn_sched_barrier(0);
+  }
 }
 
-// ---------------------------------------------------------------------------
-// out[r][n] = epilogue(sum_k in[r][k] Wm[n][k]) for a 128 (n) x 128 (r) tile.
-// Four waves in 2 x 2, each 64 x 64 = 4 x 4 MFMA tiles; K in steps of 32
-// staged through LDS (double-buffered).
-enum { kEpiFwd = 0, kEpiBwd = 1 };
+// LeakyReLU (slope in [0, 1]: max(v, s v)), bf16 rounding and the lane's sign
+// mask of one layer's outputs.  pk[i][j] = packed bf16 of q = 0,1 and 2,3.
+template <int MI, int JW>
+__device__ __forceinline__ void activate(const f32x4 (&v)[MI][JW], float slope, uint2 (&pk)[MI][JW], uint4& mask) {
+  uint32_t m[4] = {0u, 0u, 0u, 0u};
+#pragma unroll
+  for (int i = 0; i < MI; ++i)
+#pragma unroll
+    for (int j = 0; j < JW; ++j) {
+      const int e = 4 * (i * JW + j);
+      const uint32_t p01 = pack_bf16(fmaxf(v[i][j][0], slope * v[i][j][0]), fmaxf(v[i][j][1], slope * v[i][j][1]));
+      const uint32_t p23 = pack_bf16(fmaxf(v[i][j][2], slope * v[i][j][2]), fmaxf(v[i][j][3], slope * v[i][j][3]));
+      pk[i][j] = make_uint2(p01, p23);
+      uint32_t& w = m[e >> 5];
+      w = (w << 1) | (uint32_t)((int32_t)(p01 << 16) > 0);
+      w = (w << 1) | (uint32_t)((int32_t)p01 >= 0x10000);
+      w = (w << 1) | (uint32_t)((int32_t)(p23 << 16) > 0);
+      w = (w << 1) | (uint32_t)((int32_t)p23 >= 0x10000);
+    }
+  mask = make_uint4(m[0], m[1], m[2], m[3]);
+}
 
-constexpr int kGT = 128;            // tile edge
-constexpr int kGK = 32;             // K step
-constexpr int kGLD = kGK + 8;       // LDS row stride (bf16) of a staged [128][32] tile
+// Bit of output e in a lane's mask (see activate).
+__device__ __forceinline__ bool mask_bit(const uint4& m, int e) {
+  const uint32_t w = (e >> 5) == 0 ? m.x : (e >> 5) == 1 ? m.y : (e >> 5) == 2 ? m.z : m.w;
+  return (w >> (31 - (e & 31))) & 1u;
+}
 
-template <int kEpi>
-__global__ __launch_bounds__(256) void k_gemm(const u16* __restrict__ in, const u16* __restrict__ Wm,
-                                              const float* __restrict__ bias, const u16* __restrict__ hmask,
-                                              u16* __restrict__ out, int K, int Nf, float slope) {
-  __shared__ __attribute__((aligned(16))) u16 sA[2][kGT * kGLD];   // weights [n][k]
-  __shared__ __attribute__((aligned(16))) u16 sB[2][kGT * kGLD];   // activations [r][k]
+struct ChainArgs {
+  const float* W0;           // first layer [H][F] fp32
+  const float* b0;           // [H]
+  const u16* Wb;             // hidden layers, bf16 [NH][H][H] ([out][in])
+  const u16* WTb;            // the same, transposed ([in][out])
+  const float* bh[kMaxNH];   // hidden biases
+  const float* wo;           // logit layer [H]
+  const float* bo;           // [1]
+  float slope;
+  int NH;
+  ChunkArgs c;
+  float inv_n;               // 1 / (events of this batch)
+  const float* feat;         // [rows][F]
+  const float* xs;           // [rows][D] (fake chunks)
+  u16* act;                  // [NH][rows][H]: A_1 .. A_NH
+  u16* dlt;                  // [NH][rows][H]: unit-seed signals at A_2 .. A_{NH+1}
+  uint4* mask;               // [NH + 1][rows / T][4 waves][64 lanes]: signs of A_1 .. A_{NH+1}
+  float* eD;                 // [rows] dL_D/dz (0 on padding)
+  float* eG;                 // [rows] dL_G/dz (fake; 0 otherwise)
+  float* logits;             // caller's array (indexed from c.row0) or NULL
+  float* dLg_dx;             // caller's array (indexed from c.row0) or NULL
+  float* plog;               // [gridDim.x][H + 3]: dW_o, then sum softplus(+-z), sum e_D
+  float* pfb;                // [gridDim.x][H F + H]: dW_1, then db_1
+};
+
+// softplus(t) = max(t, 0) + ln(1 + e^-|t|), on the hardware units.
+__device__ __forceinline__ float softplus_fast(float t) { return fmaxf(t, 0.0f) + log1p_k(fast_exp(-fabsf(t))); }
+
+// Forward chain of one chunk: A_1 (VALU, K = F) -> hidden layers (MFMA) ->
+// logit z, BCE seeds e_D and e_G, and per-workgroup partials of dW_o, db_o
+// and the loss sums.  Stores A_1 .. A_NH and the masks for later kernels.
+template <int H, int F>
+__global__ __launch_bounds__(kChainThreads, kChainBlocksPerCU) void k_fwd_chain(ChainArgs p) {
+  using C = Chain<H>;
+  constexpr int T = C::T, LDA = C::LDA, WAVES = C::WAVES, MI = C::MI, JW = C::JW;
+  constexpr int NT = kChainThreads;
+  __shared__ __attribute__((aligned(16))) u16 act[T * LDA];
+  __shared__ float sW0[H * (F + 1)];            // row o: W0[o][0 .. F-1], b0[o]
+  __shared__ float zpart[WAVES][T];
+  __shared__ __attribute__((aligned(16))) float swo[H];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int lr = lane & 15, lg = lane >> 4;
-  const int n0 = blockIdx.x * kGT;             // output-feature tile
-  const int64_t r0 = (int64_t)blockIdx.y * kGT;  // row tile
-  const int wn = (wave >> 1) * 64, wr = (wave & 1) * 64;
-
-  // staging map: 128 rows x 32 k = 512 16-byte pieces per operand, 2 per thread
-  auto stage = [&](int buf, int k0) {
+  const int ow = 16 * MI * wave;
+  const ChunkArgs c = p.c;
+  const int64_t rstride = (int64_t)c.rows;
+  const int ntiles = c.rows / T;
+  const float slope = p.slope;
+  for (int k = tid; k < H * F; k += NT) sW0[(k / F) * (F + 1) + k % F] = p.W0[k];
+  for (int k = tid; k < H; k += NT) {
+    sW0[k * (F + 1) + F] = p.b0[k];
+    swo[k] = p.wo[k];
+  }
+  float dwo[MI][4];
 #pragma unroll
-    for (int p = 0; p < 2; ++p) {
-      const int piece = tid + 256 * p;
-      const int row = piece >> 2, col = (piece & 3) * 8;
-      const uint4 a = *reinterpret_cast<const uint4*>(Wm + (int64_t)(n0 + row) * K + k0 + col);
-      const uint4 b = *reinterpret_cast<const uint4*>(in + (r0 + row) * K + k0 + col);
-      *reinterpret_cast<uint4*>(&sA[buf][row * kGLD + col]) = a;
-      *reinterpret_cast<uint4*>(&sB[buf][row * kGLD + col]) = b;
-    }
+  for (int i = 0; i < MI; ++i)
+#pragma unroll
+    for (int q = 0; q < 4; ++q) dwo[i][q] = 0.f;
+  const float bo = p.bo[0];
+  float l0 = 0.f, l1 = 0.f, se = 0.f;
+  // this lane's features of the next tile, loaded one tile ahead
+  float fnext[JW][F];
+  auto load_feat = [&](int tile) __attribute__((always_inline)) {
+#pragma unroll
+    for (int j = 0; j < JW; ++j)
+#pragma unroll
+      for (int k = 0; k < F; ++k) fnext[j][k] = p.feat[(int64_t)(tile * T + 16 * j + lr) * F + k];
   };
-
-  f32x4 acc[4][4];
-#pragma unroll
-  for (int i = 0; i < 4; ++i)
-#pragma unroll
-    for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-  const int nk = K / kGK;
-  stage(0, 0);
+  if ((int)blockIdx.x < ntiles) load_feat(blockIdx.x);
   __syncthreads();
-  for (int kk = 0; kk < nk; ++kk) {
-    const int buf = kk & 1;
-    if (kk + 1 < nk) stage(buf ^ 1, (kk + 1) * kGK);
-    bf16x8 a[4], b[4];
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-      a[i] = *reinterpret_cast<const bf16x8*>(&sA[buf][(wn + 16 * i + lr) * kGLD + 8 * lg]);
-#pragma unroll
-    for (int j = 0; j < 4; ++j)
-      b[j] = *reinterpret_cast<const bf16x8*>(&sB[buf][(wr + 16 * j + lr) * kGLD + 8 * lg]);
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-      for (int j = 0; j < 4; ++j) acc[i][j] = mfma_bf16(a[i], b[j], acc[i][j]);
-    __syncthreads();
-  }
 
-  // epilogue: lane holds features n0+wn+16i+4lg+q, row r0+wr+16j+lr
+  for (int tile = blockIdx.x; tile < ntiles; tile += gridDim.x) {
+    const int r0 = tile * T;
+    float f[JW][F];
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int n = n0 + wn + 16 * i + 4 * lg;
-    f32x4 bv = f32x4{0.f, 0.f, 0.f, 0.f};
-    if constexpr (kEpi == kEpiFwd) bv = *reinterpret_cast<const f32x4*>(bias + n);
+    for (int j = 0; j < JW; ++j)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int64_t r = r0 + wr + 16 * j + lr;
-      float v[4];
-      if constexpr (kEpi == kEpiFwd) {
-#pragma unroll
-        for (int q = 0; q < 4; ++q) v[q] = leaky(acc[i][j][q] + bv[q], slope);
-      } else {
-        const uint2 hm = *reinterpret_cast<const uint2*>(hmask + r * Nf + n);
-        const float h[4] = {bf16_to_f32((u16)(hm.x & 0xffff)), bf16_to_f32((u16)(hm.x >> 16)),
-                            bf16_to_f32((u16)(hm.y & 0xffff)), bf16_to_f32((u16)(hm.y >> 16))};
-#pragma unroll
-        for (int q = 0; q < 4; ++q) v[q] = acc[i][j][q] * leaky_grad(h[q], slope);
-      }
-      uint2 o;
-      o.x = (uint32_t)bf16_bits(v[0]) | ((uint32_t)bf16_bits(v[1]) << 16);
-      o.y = (uint32_t)bf16_bits(v[2]) | ((uint32_t)bf16_bits(v[3]) << 16);
-      *reinterpret_cast<uint2*>(out + r * Nf + n) = o;
-    }
-  }
-}
+      for (int k = 0; k < F; ++k) f[j][k] = fnext[j][k];
+    if (tile + (int)gridDim.x < ntiles) load_feat(tile + gridDim.x);
+    auto mask_at = [&](int layer) __attribute__((always_inline)) {
+      return p.mask + (((int64_t)layer * ntiles + tile) * WAVES + wave) * 64 + lane;
+    };
 
-// ---------------------------------------------------------------------------
-// Logit layer and BCE seeds for one chunk.  One wave per row: lanes split H.
-// Writes e_D[r] (0 on padding), e_G[r], delta_L (unit seed, bf16), logits,
-// and per-block partials of the loss sums, dW_o and db_o.
-constexpr int kRowBlocks = 2048;  // blocks of the row-reduction kernels (fixed partial count)
-
-inline int row_blocks(int rows) { return std::max(1, std::min(kRowBlocks, (rows + 63) / 64)); }
-inline int rows_per_block(int rows, int blocks) { return (rows + blocks - 1) / blocks; }
-
-template <int PER>
-__global__ __launch_bounds__(256) void k_logit(const u16* __restrict__ AL, const float* __restrict__ Wo,
-                                               const float* __restrict__ bo, int H, ChunkArgs c, float inv_n,
-                                               float slope, float* __restrict__ eD, float* __restrict__ eG,
-                                               u16* __restrict__ dL, float* __restrict__ logits,
-                                               float* __restrict__ part /*[blocks][H + 3]*/, int rpb) {
-  extern __shared__ float sh_dwo[];   // [4 waves][H]
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  constexpr int per = PER;            // features per lane, H / 64
-  float wo[PER];
+    // ---- first layer (VALU, K = F) in the MFMA output arrangement ----------
+    {
+      f32x4 v[MI][JW];
 #pragma unroll
-  for (int q = 0; q < per; ++q) wo[q] = Wo[lane * per + q];
-  float acc_dwo[PER];
+      for (int i = 0; i < MI; ++i)
 #pragma unroll
-  for (int q = 0; q < per; ++q) acc_dwo[q] = 0.f;
-  float l0 = 0.f, l1 = 0.f, sum_e = 0.f;
-  const int rbase = blockIdx.x * rpb;
-  constexpr int R = 4;                 // rows per wave per iteration (independent loads in flight)
-  for (int rr0 = wave * R; rr0 < rpb; rr0 += 4 * R) {
-    float h[R][PER];
-    float z[R];
+        for (int q = 0; q < 4; ++q) {
+          const float* w = &sW0[(ow + 16 * i + 4 * lg + q) * (F + 1)];
+          float wr[F + 1];
 #pragma unroll
-    for (int k = 0; k < R; ++k) {
-      const int r = rbase + rr0 + k;
-      if (rr0 + k < rpb && r < c.rows) load_bf16<PER>(AL + (int64_t)r * H + lane * per, h[k]);
-      else {
+          for (int k = 0; k <= F; ++k) wr[k] = w[k];
 #pragma unroll
-        for (int q = 0; q < per; ++q) h[k][q] = 0.f;
-      }
-      float zz = 0.f;
+          for (int j = 0; j < JW; ++j) {
+            float t = wr[F];
 #pragma unroll
-      for (int q = 0; q < per; ++q) zz = fmaf(h[k][q], wo[q], zz);
-      z[k] = zz;
-    }
-#pragma unroll
-    for (int k = 0; k < R; ++k) z[k] = wave_sum(z[k]) + bo[0];
-#pragma unroll
-    for (int k = 0; k < R; ++k) {
-      const int r = rbase + rr0 + k;
-      if (rr0 + k >= rpb || r >= c.rows) break;
-      const bool valid = r < c.valid;
-      float e = 0.f, g = 0.f;
-      if (valid) {
-        const float sig_neg = 1.0f / (1.0f + expf(z[k]));
-        if (c.fake) {
-          e = (1.0f - sig_neg) * inv_n;
-          g = -sig_neg * inv_n;
-          l0 += softplus(z[k]);
-          l1 += softplus(-z[k]);
-        } else {
-          e = -sig_neg * inv_n;
-          l0 += softplus(-z[k]);
+            for (int k = 0; k < F; ++k) t = fmaf(wr[k], f[j][k], t);
+            v[i][j][q] = t;
+          }
         }
-        if (lane == 0 && logits) logits[c.row0 + r] = z[k];
-      }
-      if (lane == 0) { eD[r] = e; eG[r] = g; }
-      sum_e += e;
-      float d[PER];
+      uint2 pk[MI][JW];
+      uint4 m;
+      activate<MI, JW>(v, slope, pk, m);
+      *mask_at(0) = m;
 #pragma unroll
-      for (int q = 0; q < per; ++q) {
-        acc_dwo[q] = fmaf(e, h[k][q], acc_dwo[q]);
-        d[q] = wo[q] * leaky_grad(h[k][q], slope);
+      for (int i = 0; i < MI; ++i)
+#pragma unroll
+        for (int j = 0; j < JW; ++j) {
+          const int ev = 16 * j + lr, o = ow + 16 * i + 4 * lg;
+          *reinterpret_cast<uint2*>(act + ev * LDA + o) = pk[i][j];
+        }
+    }
+    __syncthreads();
+    copy_out<H, T, LDA, NT>(act, p.act + (int64_t)r0 * H, tid);
+
+    // ---- hidden layers -----------------------------------------------------
+    for (int l = 0; l < p.NH; ++l) {
+      const bool last = l == p.NH - 1;
+      f32x4 bias[MI];
+#pragma unroll
+      for (int i = 0; i < MI; ++i) bias[i] = *reinterpret_cast<const f32x4*>(p.bh[l] + ow + 16 * i + 4 * lg);
+      f32x4 acc[MI][JW];
+      chain_gemm<H>(p.Wb + (size_t)l * H * H, act, acc, bias, ow, lr, lg);
+      uint2 pk[MI][JW];
+      uint4 m;
+      activate<MI, JW>(acc, slope, pk, m);
+      *mask_at(l + 1) = m;
+      if (!last) {
+        __syncthreads();                             // every wave is done reading this layer's input
+#pragma unroll
+        for (int i = 0; i < MI; ++i)
+#pragma unroll
+          for (int j = 0; j < JW; ++j) {
+            const int ev = 16 * j + lr, o = ow + 16 * i + 4 * lg;
+            *reinterpret_cast<uint2*>(act + ev * LDA + o) = pk[i][j];
+          }
+        __syncthreads();
+        copy_out<H, T, LDA, NT>(act, p.act + ((int64_t)(l + 1) * rstride + r0) * H, tid);
+        continue;
       }
-      store_bf16<PER>(dL + (int64_t)r * H + lane * per, d);
+      // ---- logit layer and BCE seeds (fp32 dot over the bf16 activations) --
+#pragma unroll
+      for (int j = 0; j < JW; ++j) {
+        float s = 0.f;
+#pragma unroll
+        for (int i = 0; i < MI; ++i) {
+          const f32x4 w4 = *reinterpret_cast<const f32x4*>(&swo[ow + 16 * i + 4 * lg]);
+          s = fmaf(lo_bf16(pk[i][j].x), w4[0], s);
+          s = fmaf(hi_bf16(pk[i][j].x), w4[1], s);
+          s = fmaf(lo_bf16(pk[i][j].y), w4[2], s);
+          s = fmaf(hi_bf16(pk[i][j].y), w4[3], s);
+        }
+        s += __shfl_xor(s, 16, 64);
+        s += __shfl_xor(s, 32, 64);
+        if (lg == 0) zpart[wave][16 * j + lr] = s;
+      }
+      __syncthreads();
+#pragma unroll
+      for (int j = 0; j < JW; ++j) {
+        const int ev = 16 * j + lr, r = r0 + ev;
+        float z = bo;
+#pragma unroll
+        for (int w = 0; w < WAVES; ++w) z += zpart[w][ev];
+        const bool valid = r < c.valid;
+        float e = 0.f, g = 0.f;
+        if (valid) {
+          const float sig_neg = fast_rcp(1.0f + fast_exp(z));
+          if (c.fake) {
+            e = (1.0f - sig_neg) * p.inv_n;
+            g = -sig_neg * p.inv_n;
+          } else {
+            e = -sig_neg * p.inv_n;
+          }
+        }
+#pragma unroll
+        for (int i = 0; i < MI; ++i) {
+          dwo[i][0] = fmaf(e, lo_bf16(pk[i][j].x), dwo[i][0]);
+          dwo[i][1] = fmaf(e, hi_bf16(pk[i][j].x), dwo[i][1]);
+          dwo[i][2] = fmaf(e, lo_bf16(pk[i][j].y), dwo[i][2]);
+          dwo[i][3] = fmaf(e, hi_bf16(pk[i][j].y), dwo[i][3]);
+        }
+        if (lg == 0 && j % WAVES == wave) {        // one lane per event, spread over the waves
+          p.eD[r] = e;
+          p.eG[r] = g;
+          se += e;
+          if (valid) {
+            if (p.logits) p.logits[c.row0 + r] = z;
+            if (c.fake) {
+              l0 += softplus_fast(z);
+              l1 += softplus_fast(-z);
+            } else {
+              l0 += softplus_fast(-z);
+            }
+          }
+        }
+      }
+      // zpart and act are next written after the next tile's first-layer
+      // barrier, which every wave reaches only after this point.
     }
   }
+
+  // ---- per-workgroup partials, fixed order ---------------------------------
+  float* dst = p.plog + (int64_t)blockIdx.x * (H + 3);
 #pragma unroll
-  for (int q = 0; q < per; ++q) sh_dwo[wave * H + lane * per + q] = acc_dwo[q];
+  for (int i = 0; i < MI; ++i)
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      float v = dwo[i][q];
+      v += __shfl_xor(v, 1, 64);
+      v += __shfl_xor(v, 2, 64);
+      v += __shfl_xor(v, 4, 64);
+      v += __shfl_xor(v, 8, 64);
+      if (lr == 0) dst[ow + 16 * i + 4 * lg + q] = v;
+    }
+  float s3[3] = {l0, l1, se};
+#pragma unroll
+  for (int k = 0; k < 3; ++k) {
+    float v = s3[k];
+    v += __shfl_xor(v, 1, 64);
+    v += __shfl_xor(v, 2, 64);
+    v += __shfl_xor(v, 4, 64);
+    v += __shfl_xor(v, 8, 64);
+    if (lane == 0) zpart[wave][k] = v;
+  }
   __syncthreads();
-  float* p = part + (int64_t)blockIdx.x * (H + 3);
-  for (int o = threadIdx.x; o < H; o += 256)
-    p[o] = sh_dwo[o] + sh_dwo[H + o] + sh_dwo[2 * H + o] + sh_dwo[3 * H + o];
-  __syncthreads();
-  // the scalars: lane 0 of each wave holds its sums
-  if (lane == 0) { sh_dwo[4 * wave] = l0; sh_dwo[4 * wave + 1] = l1; sh_dwo[4 * wave + 2] = sum_e; }
-  __syncthreads();
-  if (threadIdx.x < 3) {
-    float s = 0.f;
-    for (int w = 0; w < 4; ++w) s += sh_dwo[4 * w + threadIdx.x];
-    p[H + threadIdx.x] = s;   // [H] = loss0, [H+1] = loss1, [H+2] = sum e_D (db_o)
+  if (tid < 3) {
+    float v = 0.f;
+#pragma unroll
+    for (int w = 0; w < WAVES; ++w) v += zpart[w][tid];
+    dst[H + tid] = v;
   }
 }
+
+// Backward chain of one chunk: the unit-seed signal from the logit layer down
+// through the hidden layers (MFMA, LeakyReLU' from the masks), storing the
+// signals at A_2 .. A_{NH+1} for the weight-gradient products; then the first
+// layer: per-workgroup partials of dW_1 and db_1 (scaled by e_D) and, for fake
+// chunks, dL_G/dx (scaled by e_G, through the HD8 Jacobian when used).
+template <int H, int F, int D, bool kHD8>
+__global__ __launch_bounds__(kChainThreads, kChainBlocksPerCU) void k_bwd_chain(ChainArgs p) {
+  using C = Chain<H>;
+  constexpr int T = C::T, LDA = C::LDA, WAVES = C::WAVES, MI = C::MI, JW = C::JW;
+  constexpr int NT = kChainThreads;
+  constexpr int FPT = H / NT;        // first-layer features per thread
+  constexpr int P = NT / T;          // threads per event in the input-gradient dot
+  __shared__ __attribute__((aligned(16))) u16 act[T * LDA];
+  __shared__ float sW0[H * F];
+  __shared__ float sfeat[T][F];
+  __shared__ float sx[T][D];
+  __shared__ float se[T][2];
+  __shared__ __attribute__((aligned(16))) float swo[H];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int lr = lane & 15, lg = lane >> 4;
+  const int ow = 16 * MI * wave;
+  const ChunkArgs c = p.c;
+  const int64_t rstride = (int64_t)c.rows;
+  const int ntiles = c.rows / T;
+  for (int k = tid; k < H * F; k += NT) sW0[k] = p.W0[k];
+  for (int k = tid; k < H; k += NT) swo[k] = p.wo[k];
+  float adw[FPT][F + 1];
+#pragma unroll
+  for (int u = 0; u < FPT; ++u)
+#pragma unroll
+    for (int k = 0; k <= F; ++k) adw[u][k] = 0.f;
+  const bool want_dx = c.fake && p.dLg_dx != nullptr;
+  const float slope = p.slope;
+  const int NH = p.NH;
+  f32x4 zero[MI];
+#pragma unroll
+  for (int i = 0; i < MI; ++i) zero[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  for (int tile = blockIdx.x; tile < ntiles; tile += gridDim.x) {
+    const int r0 = tile * T;
+    auto mask_at = [&](int layer) __attribute__((always_inline)) {
+      return p.mask + (((int64_t)layer * ntiles + tile) * WAVES + wave) * 64 + lane;
+    };
+    for (int k = tid; k < T; k += NT) {
+      se[k][0] = p.eD[r0 + k];
+      se[k][1] = p.eG[r0 + k];
+    }
+    for (int k = tid; k < T * F; k += NT) sfeat[k / F][k % F] = p.feat[(int64_t)r0 * F + k];
+    if (want_dx && kHD8)
+      for (int k = tid; k < T * D; k += NT) sx[k / D][k % D] = p.xs[(int64_t)r0 * D + k];
+    // ---- unit-seed signal at A_{NH+1}: w_o * LeakyReLU'(A_{NH+1}) ----------
+    {
+      const uint4 m = *mask_at(NH);
+      u16* gdst = p.dlt + (int64_t)(NH - 1) * rstride * H;
+#pragma unroll
+      for (int i = 0; i < MI; ++i) {
+        const f32x4 w4 = *reinterpret_cast<const f32x4*>(&swo[ow + 16 * i + 4 * lg]);
+#pragma unroll
+        for (int j = 0; j < JW; ++j) {
+          const int e = 4 * (i * JW + j);
+          float d[4];
+#pragma unroll
+          for (int q = 0; q < 4; ++q) d[q] = mask_bit(m, e + q) ? w4[q] : w4[q] * slope;
+          const uint2 v = make_uint2(pack_bf16(d[0], d[1]), pack_bf16(d[2], d[3]));
+          const int ev = 16 * j + lr, o = ow + 16 * i + 4 * lg;
+          *reinterpret_cast<uint2*>(act + ev * LDA + o) = v;
+        }
+      }
+      __syncthreads();
+      copy_out<H, T, LDA, NT>(act, gdst + (int64_t)r0 * H, tid);
+    }
+    // ---- hidden layers, top down ---------------------------------------------
+    for (int l = NH - 1; l >= 0; --l) {
+      f32x4 acc[MI][JW];
+      chain_gemm<H>(p.WTb + (size_t)l * H * H, act, acc, zero, ow, lr, lg);
+      const uint4 m = *mask_at(l);
+      uint2 pk[MI][JW];
+#pragma unroll
+      for (int i = 0; i < MI; ++i)
+#pragma unroll
+        for (int j = 0; j < JW; ++j) {
+          const int e = 4 * (i * JW + j);
+          float d[4];
+#pragma unroll
+          for (int q = 0; q < 4; ++q) d[q] = mask_bit(m, e + q) ? acc[i][j][q] : acc[i][j][q] * slope;
+          pk[i][j] = make_uint2(pack_bf16(d[0], d[1]), pack_bf16(d[2], d[3]));
+        }
+      __syncthreads();                               // every wave is done reading this layer's input
+      u16* gdst = l >= 1 ? p.dlt + (int64_t)(l - 1) * rstride * H : nullptr;
+#pragma unroll
+      for (int i = 0; i < MI; ++i)
+#pragma unroll
+        for (int j = 0; j < JW; ++j) {
+          const int ev = 16 * j + lr, o = ow + 16 * i + 4 * lg;
+          *reinterpret_cast<uint2*>(act + ev * LDA + o) = pk[i][j];
+        }
+      __syncthreads();
+      if (gdst) copy_out<H, T, LDA, NT>(act, gdst + (int64_t)r0 * H, tid);
+    }
+    // ---- first layer: act holds the signal at A_1 ---------------------------
+#pragma unroll 4
+    for (int ev = 0; ev < T; ++ev) {
+      const float e = se[ev][0];
+#pragma unroll
+      for (int u = 0; u < FPT; ++u) {
+        const float ed = e * bf16_to_f32(act[ev * LDA + tid + NT * u]);
+#pragma unroll
+        for (int j = 0; j < F; ++j) adw[u][j] = fmaf(ed, sfeat[ev][j], adw[u][j]);
+        adw[u][F] += ed;
+      }
+    }
+    if (want_dx) {
+      const int ev = tid / P, pp = tid % P;
+      constexpr int OP = H / P;                      // features per thread (a multiple of 8)
+      float g[F];
+#pragma unroll
+      for (int j = 0; j < F; ++j) g[j] = 0.f;
+      const u16* drow = act + ev * LDA + pp * OP;
+#pragma unroll 2
+      for (int k = 0; k < OP; k += 8) {
+        float dv[8];
+        load_bf16<8>(drow + k, dv);
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          const int o = pp * OP + k + u;
+#pragma unroll
+          for (int j = 0; j < F; ++j) g[j] = fmaf(dv[u], sW0[o * F + j], g[j]);
+        }
+      }
+#pragma unroll
+      for (int s = 1; s < P; s <<= 1)
+#pragma unroll
+        for (int j = 0; j < F; ++j) g[j] += __shfl_xor(g[j], s, 64);
+      const int r = r0 + ev;
+      if (pp == 0 && r < c.valid) {
+        const float eg = se[ev][1];
+#pragma unroll
+        for (int j = 0; j < F; ++j) g[j] *= eg;
+        float dx[D];
+        if constexpr (kHD8) {
+          // d features / d x of [x1, x2, x3, x1x2, x2x3, x1x3, ln x1, ln(1 - x3)];
+          // 1/x1 and 1/(1 - x3) from the log features, accurate where fp32 x3 is within ulps of 1
+          const float x1 = sx[ev][0], x2 = sx[ev][1], x3 = sx[ev][2];
+          const float inv_x1 = expf(-sfeat[ev][6]), inv_1mx3 = expf(-sfeat[ev][7]);
+          dx[0] = g[0] + g[3] * x2 + g[5] * x3 + g[6] * inv_x1;
+          dx[1] = g[1] + g[3] * x1 + g[4] * x3;
+          dx[2] = g[2] + g[4] * x2 + g[5] * x1 - g[7] * inv_1mx3;
+        } else {
+#pragma unroll
+          for (int j = 0; j < D; ++j) dx[j] = g[j];
+        }
+#pragma unroll
+        for (int j = 0; j < D; ++j) p.dLg_dx[(c.row0 + r) * D + j] = dx[j];
+      }
+    }
+    __syncthreads();                                 // before the next tile overwrites act and the staged rows
+  }
+
+  // ---- per-workgroup partials of dW_1 and db_1 ------------------------------
+  float* dst = p.pfb + (int64_t)blockIdx.x * (H * F + H);
+#pragma unroll
+  for (int u = 0; u < FPT; ++u) {
+    const int o = tid + NT * u;
+#pragma unroll
+    for (int j = 0; j < F; ++j) dst[o * F + j] = adw[u][j];
+    dst[H * F + o] = adw[u][F];
+  }
+}
+
+constexpr int kGT = 128;            // weight-gradient tile edge
 
 // ---------------------------------------------------------------------------
 // Weight-gradient partial of one layer over a slice of rows:
@@ -511,98 +837,6 @@ __global__ __launch_bounds__(256, 2) void k_wgrad(const u16* __restrict__ dlt, c
   }
 }
 
-// ---------------------------------------------------------------------------
-// First layer backward for one chunk: per-block partials of dW1 [H][F] and
-// db1 [H]; for fake rows dL_G/dx (through the HD8 Jacobian when used).
-
-template <int D, bool kHD8, int PER>
-__global__ __launch_bounds__(256) void k_first_bwd(const u16* __restrict__ d1, const float* __restrict__ feat,
-                                                   const float* __restrict__ xs, const float* __restrict__ W1,
-                                                   const float* __restrict__ eD, const float* __restrict__ eG,
-                                                   int H, ChunkArgs c, float* __restrict__ dLg_dx,
-                                                   float* __restrict__ part /*[blocks][H*F + H]*/, int rpb) {
-  constexpr int F = kHD8 ? 8 : D;
-  extern __shared__ float smem[];          // W1 [H][F], then the block's accumulators [H][F+1]
-  float* sW1 = smem;
-  float* sacc = smem + H * F;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  for (int k = threadIdx.x; k < H * F; k += 256) sW1[k] = W1[k];
-  constexpr int per = PER;   // features per lane, H / 64
-  float adw[PER][F + 1];
-#pragma unroll
-  for (int q = 0; q < PER; ++q)
-#pragma unroll
-    for (int j = 0; j <= F; ++j) adw[q][j] = 0.f;
-  __syncthreads();
-  const bool want_dx = c.fake && dLg_dx != nullptr;
-  const int rbase = blockIdx.x * rpb;
-  for (int rr = wave; rr < rpb; rr += 4) {
-    const int r = rbase + rr;
-    if (r >= c.rows) break;
-    const float e = eD[r];
-    float f[F];
-#pragma unroll
-    for (int j = 0; j < F; ++j) f[j] = feat[(int64_t)r * F + j];
-    float g[F];
-#pragma unroll
-    for (int j = 0; j < F; ++j) g[j] = 0.f;
-    float dvs[PER];
-    load_bf16<PER>(d1 + (int64_t)r * H + lane * per, dvs);
-#pragma unroll
-    for (int q = 0; q < per; ++q) {
-      const float dv = dvs[q];
-      const float ed = e * dv;
-      const int o = lane * per + q;
-#pragma unroll
-      for (int j = 0; j < F; ++j) adw[q][j] = fmaf(ed, f[j], adw[q][j]);
-      adw[q][F] += ed;
-      if (want_dx) {
-#pragma unroll
-        for (int j = 0; j < F; ++j) g[j] = fmaf(dv, sW1[o * F + j], g[j]);
-      }
-    }
-    if (want_dx && r < c.valid) {
-#pragma unroll
-      for (int j = 0; j < F; ++j) g[j] = wave_sum(g[j]) * eG[r];
-      if (lane == 0) {
-        float dx[D];
-        if constexpr (kHD8) {
-          // d features / d x of [x1, x2, x3, x1x2, x2x3, x1x3, ln x1, ln(1 - x3)]
-          // 1/x1 and 1/(1 - x3) from the log features, accurate where fp32 x3 is within ulps of 1
-          const float x1 = xs[(int64_t)r * 3], x2 = xs[(int64_t)r * 3 + 1], x3 = xs[(int64_t)r * 3 + 2];
-          const float inv_x1 = expf(-f[6]), inv_1mx3 = expf(-f[7]);
-          dx[0] = g[0] + g[3] * x2 + g[5] * x3 + g[6] * inv_x1;
-          dx[1] = g[1] + g[3] * x1 + g[4] * x3;
-          dx[2] = g[2] + g[4] * x2 + g[5] * x1 - g[7] * inv_1mx3;
-        } else {
-#pragma unroll
-          for (int j = 0; j < D; ++j) dx[j] = g[j];
-        }
-#pragma unroll
-        for (int j = 0; j < D; ++j) dLg_dx[(c.row0 + r) * D + j] = dx[j];
-      }
-    }
-  }
-  // combine the four waves in a fixed order
-  for (int w = 0; w < 4; ++w) {
-    if (wave == w)
-#pragma unroll
-      for (int q = 0; q < per; ++q)
-#pragma unroll
-        for (int j = 0; j <= F; ++j) {
-          float& dst = sacc[(lane * per + q) * (F + 1) + j];
-          dst = (w == 0) ? adw[q][j] : dst + adw[q][j];
-        }
-    __syncthreads();
-  }
-  float* p = part + (int64_t)blockIdx.x * (H * F + H);
-  for (int k = threadIdx.x; k < H * (F + 1); k += 256) {
-    const int o = k / (F + 1), j = k % (F + 1);
-    if (j < F) p[o * F + j] = sacc[k];
-    else p[H * F + o] = sacc[k];
-  }
-}
-
 // acc[e] (+)= sum_k part[k][e], k = 0..n-1, in a fixed order (S contiguous
 // row ranges summed side by side, then combined in order); the first chunk
 // overwrites.  C columns per block, S = 256 / C row slices.
@@ -677,17 +911,15 @@ struct Plan {
   int H, NH, F, D;
   bool hd8;
   int rows_max;          // padded rows of the largest chunk
-  int logit_blocks, fb_blocks;
+  int blocks;            // workgroups of the chain kernels
   int slices;            // weight-gradient slices per chunk
-  size_t off_wb, off_wtb, off_feat, off_xs, off_act, off_dlt0, off_dlt1, off_eD, off_eG, off_plog, off_pfb,
-      off_pw, off_pdb, off_accl, total;
+  size_t off_wb, off_wtb, off_feat, off_xs, off_act, off_dlt, off_mask, off_eD, off_eG, off_plog, off_pfb, off_pw,
+      off_pdb, off_accl, total;
 };
 
 int pad128(int64_t n) { return (int)((n + 127) / 128 * 128); }
 
-
-
-Plan make_plan(const DiscArgs& a) {
+Plan make_plan(const DiscArgs& a, int n_cu) {
   const sagips_mlp& D = *a.D;
   Plan p;
   p.H = D.width[1];
@@ -697,23 +929,22 @@ Plan make_plan(const DiscArgs& a) {
   p.D = a.d;
   const int64_t biggest = std::min<int64_t>(std::max(a.n_fake, a.n_real), kChunkRows);
   p.rows_max = pad128(biggest);
-  p.logit_blocks = kRowBlocks;
-  p.fb_blocks = kRowBlocks;
+  p.blocks = std::max(1, n_cu * kChainBlocksPerCU);
   const int tiles = (p.H / kGT) * (p.H / kGT);
   p.slices = std::max(1, 768 / tiles);   // three weight-gradient blocks per CU
-  const size_t H = p.H, R = p.rows_max;
+  const size_t H = p.H, R = p.rows_max, NH = p.NH;
   size_t o = 0;
-  p.off_wb = o; o += al(2 * H * H * p.NH);
-  p.off_wtb = o; o += al(2 * H * H * p.NH);
+  p.off_wb = o; o += al(2 * H * H * NH);
+  p.off_wtb = o; o += al(2 * H * H * NH);
   p.off_feat = o; o += al(4 * R * p.F);
   p.off_xs = o; o += al(4 * R * p.D);
-  p.off_act = o; o += al(2 * R * H * (p.NH + 1));
-  p.off_dlt0 = o; o += al(2 * R * H);
-  p.off_dlt1 = o; o += al(2 * R * H);
+  p.off_act = o; o += al(2 * R * H * NH);
+  p.off_dlt = o; o += al(2 * R * H * NH);
+  p.off_mask = o; o += al(8 * R * (H / 64) * (NH + 1));
   p.off_eD = o; o += al(4 * R);
   p.off_eG = o; o += al(4 * R);
-  p.off_plog = o; o += al(4 * (size_t)p.logit_blocks * (H + 3));
-  p.off_pfb = o; o += al(4 * (size_t)p.fb_blocks * (H * p.F + H));
+  p.off_plog = o; o += al(4 * (size_t)p.blocks * (H + 3));
+  p.off_pfb = o; o += al(4 * (size_t)p.blocks * (H * p.F + H));
   p.off_pw = o; o += al(4 * (size_t)p.slices * H * H);
   p.off_pdb = o; o += al(4 * (size_t)p.slices * H);
   p.off_accl = o; o += al(4 * 4);
@@ -721,11 +952,31 @@ Plan make_plan(const DiscArgs& a) {
   return p;
 }
 
+template <int H, int F, int D, bool kHD8>
+void launch_chains(const ChainArgs& ca, int blocks, bool bwd, hipStream_t st) {
+  if (!bwd) hipLaunchKernelGGL((k_fwd_chain<H, F>), dim3(blocks), dim3(kChainThreads), 0, st, ca);
+  else hipLaunchKernelGGL((k_bwd_chain<H, F, D, kHD8>), dim3(blocks), dim3(kChainThreads), 0, st, ca);
+}
+
+void launch_chain(const Plan& p, const ChainArgs& ca, bool bwd, hipStream_t st) {
+  const int blocks = std::min(p.blocks, ca.c.rows / (p.H == 256 ? Chain<256>::T : Chain<512>::T));
+  if (p.H == 256) {
+    if (p.hd8) launch_chains<256, 8, 3, true>(ca, blocks, bwd, st);
+    else if (p.D == 2) launch_chains<256, 2, 2, false>(ca, blocks, bwd, st);
+    else launch_chains<256, 3, 3, false>(ca, blocks, bwd, st);
+  } else {
+    if (p.hd8) launch_chains<512, 8, 3, true>(ca, blocks, bwd, st);
+    else if (p.D == 2) launch_chains<512, 2, 2, false>(ca, blocks, bwd, st);
+    else launch_chains<512, 3, 3, false>(ca, blocks, bwd, st);
+  }
+}
+
 }  // namespace
 
 bool disc_bf16_supported(const sagips_mlp& D, int d, const char** why) {
   const int H = D.width[1];
   if (H != 256 && H != 512) { *why = "bf16 discriminator supports hidden width 256 or 512"; return false; }
+  if (!(D.leaky_slope >= 0.0f && D.leaky_slope <= 1.0f)) { *why = "bf16 discriminator needs leaky_slope in [0, 1]"; return false; }
   if (D.n_layers < 3 || D.n_layers - 2 > kMaxNH) { *why = "bf16 discriminator needs 1-4 hidden-to-hidden layers"; return false; }
   for (int l = 1; l < D.n_layers; ++l)
     if (D.width[l] != H) { *why = "all hidden widths must be equal"; return false; }
@@ -738,24 +989,17 @@ bool disc_bf16_supported(const sagips_mlp& D, int d, const char** why) {
   return true;
 }
 
-size_t disc_bf16_workspace(const DiscArgs& a) { return make_plan(a).total; }
+size_t disc_bf16_workspace(const DiscArgs& a, int n_cu) { return make_plan(a, n_cu).total; }
 
 hipError_t launch_disc_bf16(const DiscArgs& a, void* ws, int n_cu, hipStream_t st, Timer* tm) {
   const sagips_mlp& Dm = *a.D;
-  const Plan p = make_plan(a);
+  const Plan p = make_plan(a, n_cu);
   char* base = static_cast<char*>(ws);
   auto F32 = [&](size_t off) { return reinterpret_cast<float*>(base + off); };
   auto B16 = [&](size_t off) { return reinterpret_cast<u16*>(base + off); };
   const int H = p.H, NH = p.NH;
-  const float slope = Dm.leaky_slope;
   u16* Wb = B16(p.off_wb);
   u16* WTb = B16(p.off_wtb);
-  float* feat = F32(p.off_feat);
-  float* xs = F32(p.off_xs);
-  u16* act = B16(p.off_act);          // A_1 .. A_{NH+1}
-  u16* dl[2] = {B16(p.off_dlt0), B16(p.off_dlt1)};
-  float* eD = F32(p.off_eD);
-  float* eG = F32(p.off_eG);
   const sagips_disc_out& out = *a.out;
   const bool want_grads = out.dW[0] != nullptr;
   const float inv_nf = 1.0f / (float)a.n_fake, inv_nr = 1.0f / (float)a.n_real;
@@ -769,6 +1013,26 @@ hipError_t launch_disc_bf16(const DiscArgs& a, void* ws, int n_cu, hipStream_t s
   SourceArgs src{};
   const bool sampled = a.fake_src != nullptr;
   if (sampled) src = *a.fake_src;
+
+  ChainArgs ca{};
+  ca.W0 = Dm.W[0];
+  ca.b0 = Dm.b[0];
+  ca.Wb = Wb;
+  ca.WTb = WTb;
+  for (int l = 0; l < NH; ++l) ca.bh[l] = Dm.b[1 + l];
+  ca.wo = Dm.W[NH + 1];
+  ca.bo = Dm.b[NH + 1];
+  ca.slope = Dm.leaky_slope;
+  ca.NH = NH;
+  ca.feat = F32(p.off_feat);
+  ca.xs = F32(p.off_xs);
+  ca.act = B16(p.off_act);
+  ca.dlt = B16(p.off_dlt);
+  ca.mask = reinterpret_cast<uint4*>(base + p.off_mask);
+  ca.eD = F32(p.off_eD);
+  ca.eG = F32(p.off_eG);
+  ca.plog = F32(p.off_plog);
+  ca.pfb = F32(p.off_pfb);
 
   int chunk_index = 0;
   float* lacc = F32(p.off_accl);
@@ -786,70 +1050,40 @@ hipError_t launch_disc_bf16(const DiscArgs& a, void* ws, int n_cu, hipStream_t s
       const dim3 g1((c.rows + 255) / 256);
       const float* xin = fake ? a.fake_x : a.real_x;
       const int samp = (fake && sampled) ? 1 : 0;
-      if (p.hd8) hipLaunchKernelGGL((k_prep<3, true>), g1, dim3(256), 0, st, c, xin, src, samp, feat, xs);
-      else if (p.D == 2) hipLaunchKernelGGL((k_prep<2, false>), g1, dim3(256), 0, st, c, xin, src, samp, feat, xs);
-      else hipLaunchKernelGGL((k_prep<3, false>), g1, dim3(256), 0, st, c, xin, src, samp, feat, xs);
-      const int64_t nthr = (int64_t)c.rows * (H / 8);
-      const dim3 gf((unsigned)((nthr + 255) / 256));
-      if (p.F == 8) hipLaunchKernelGGL(k_first_fwd<8>, gf, dim3(256), 0, st, feat, Dm.W[0], Dm.b[0], H, c.rows, slope, act);
-      else if (p.F == 3) hipLaunchKernelGGL(k_first_fwd<3>, gf, dim3(256), 0, st, feat, Dm.W[0], Dm.b[0], H, c.rows, slope, act);
-      else hipLaunchKernelGGL(k_first_fwd<2>, gf, dim3(256), 0, st, feat, Dm.W[0], Dm.b[0], H, c.rows, slope, act);
-      const size_t ast = (size_t)c.rows * H;     // stride between this chunk's activation buffers
-      for (int l = 0; l < NH; ++l) {
-        if (tm) tm->begin("bf16_gemm");
-        hipLaunchKernelGGL(k_gemm<kEpiFwd>, dim3(H / kGT, c.rows / kGT), dim3(256), 0, st, act + l * ast,
-                           Wb + (size_t)l * H * H, Dm.b[1 + l], (const u16*)nullptr, act + (l + 1) * ast, H, H, slope);
-        if (tm) tm->end();
-      }
+      if (p.hd8) hipLaunchKernelGGL((k_prep<3, true>), g1, dim3(256), 0, st, c, xin, src, samp, F32(p.off_feat), F32(p.off_xs));
+      else if (p.D == 2) hipLaunchKernelGGL((k_prep<2, false>), g1, dim3(256), 0, st, c, xin, src, samp, F32(p.off_feat), F32(p.off_xs));
+      else hipLaunchKernelGGL((k_prep<3, false>), g1, dim3(256), 0, st, c, xin, src, samp, F32(p.off_feat), F32(p.off_xs));
 
-      const int lb = row_blocks(c.rows), lrpb = rows_per_block(c.rows, lb);
-      float* plog = F32(p.off_plog);
-      if (H == 256)
-        hipLaunchKernelGGL(k_logit<4>, dim3(lb), dim3(256), 4 * H * sizeof(float), st, act + NH * ast, Dm.W[NH + 1],
-                           Dm.b[NH + 1], H, c, fake ? inv_nf : inv_nr, slope, eD, eG, dl[0],
-                           fake ? out.logits_fake : out.logits_real, plog, lrpb);
-      else
-        hipLaunchKernelGGL(k_logit<8>, dim3(lb), dim3(256), 4 * H * sizeof(float), st, act + NH * ast, Dm.W[NH + 1],
-                           Dm.b[NH + 1], H, c, fake ? inv_nf : inv_nr, slope, eD, eG, dl[0],
-                           fake ? out.logits_fake : out.logits_real, plog, lrpb);
-      if (want_grads)
-        accumulate(plog, lb, (int64_t)(H + 3), (int64_t)H, out.dW[NH + 1], first, st);
-      hipLaunchKernelGGL(k_logit_scalars, dim3(1), dim3(256), 0, st, plog, lb, H, want_grads ? out.db[NH + 1] : nullptr,
+      ca.c = c;
+      ca.inv_n = fake ? inv_nf : inv_nr;
+      ca.logits = fake ? out.logits_fake : out.logits_real;
+      ca.dLg_dx = fake ? out.dLg_dx : nullptr;
+      const int nb = std::min(p.blocks, c.rows / (H == 256 ? Chain<256>::T : Chain<512>::T));
+      if (tm) tm->begin("bf16_fwd_chain");
+      launch_chain(p, ca, false, st);
+      if (tm) tm->end();
+      if (want_grads) accumulate(ca.plog, nb, (int64_t)(H + 3), (int64_t)H, out.dW[NH + 1], first, st);
+      hipLaunchKernelGGL(k_logit_scalars, dim3(1), dim3(256), 0, st, ca.plog, nb, H, want_grads ? out.db[NH + 1] : nullptr,
                          lacc, c.fake, first, first_batch);
 
-      const int tiles = (H / kGT) * (H / kGT);
-      const int rows_per_slice = ((c.rows / p.slices + kWK - 1) / kWK) * kWK;
-      int cur = 0;
-      for (int l = NH - 1; l >= 0; --l) {
-        // hidden layer l maps A_{l+1} (act + l*ast) -> A_{l+2}; its output signal is in dl[cur]
-        if (want_grads) {
+      if (tm) tm->begin("bf16_bwd_chain");
+      launch_chain(p, ca, true, st);
+      if (tm) tm->end();
+      if (want_grads) {
+        accumulate(ca.pfb, nb, (int64_t)(H * p.F + H), (int64_t)(H * p.F), out.dW[0], first, st);
+        accumulate(ca.pfb + (size_t)H * p.F, nb, (int64_t)(H * p.F + H), (int64_t)H, out.db[0], first, st);
+        const int tiles = (H / kGT) * (H / kGT);
+        const int rows_per_slice = ((c.rows / p.slices + kWK - 1) / kWK) * kWK;
+        const size_t bst = (size_t)c.rows * H;   // stride between this chunk's per-layer buffers
+        for (int l = 0; l < NH; ++l) {
+          // hidden layer l maps A_{l+1} -> A_{l+2}: operands A_{l+1} and the signal at A_{l+2}
           if (tm) tm->begin("bf16_wgrad");
-          hipLaunchKernelGGL(k_wgrad, dim3(tiles, p.slices), dim3(256), 0, st, dl[cur], act + l * ast, eD, H,
-                             rows_per_slice, c.rows, F32(p.off_pw), F32(p.off_pdb));
+          hipLaunchKernelGGL(k_wgrad, dim3(tiles, p.slices), dim3(256), 0, st, ca.dlt + l * bst, ca.act + l * bst,
+                             ca.eD, H, rows_per_slice, c.rows, F32(p.off_pw), F32(p.off_pdb));
           if (tm) tm->end();
           accumulate(F32(p.off_pw), p.slices, (int64_t)H * H, (int64_t)H * H, out.dW[1 + l], first, st);
           accumulate(F32(p.off_pdb), p.slices, (int64_t)H, (int64_t)H, out.db[1 + l], first, st);
         }
-        if (tm) tm->begin("bf16_gemm");
-        hipLaunchKernelGGL(k_gemm<kEpiBwd>, dim3(H / kGT, c.rows / kGT), dim3(256), 0, st, dl[cur],
-                           WTb + (size_t)l * H * H, (const float*)nullptr, act + l * ast, dl[cur ^ 1], H, H, slope);
-        if (tm) tm->end();
-        cur ^= 1;
-      }
-      const int fbb = row_blocks(c.rows), frpb = rows_per_block(c.rows, fbb);
-      const size_t fb_smem = sizeof(float) * ((size_t)H * p.F + (size_t)H * (p.F + 1));
-      float* pfb = F32(p.off_pfb);
-      float* gx = fake ? out.dLg_dx : nullptr;
-#define SAGIPS_FIRST_BWD(D_, HD8_, PER_)                                                                   \
-  hipLaunchKernelGGL((k_first_bwd<D_, HD8_, PER_>), dim3(fbb), dim3(256), fb_smem, st, dl[cur], feat, xs, Dm.W[0], \
-                     eD, eG, H, c, gx, pfb, frpb)
-      if (p.hd8) { if (H == 256) SAGIPS_FIRST_BWD(3, true, 4); else SAGIPS_FIRST_BWD(3, true, 8); }
-      else if (p.D == 2) { if (H == 256) SAGIPS_FIRST_BWD(2, false, 4); else SAGIPS_FIRST_BWD(2, false, 8); }
-      else { if (H == 256) SAGIPS_FIRST_BWD(3, false, 4); else SAGIPS_FIRST_BWD(3, false, 8); }
-#undef SAGIPS_FIRST_BWD
-      if (want_grads) {
-        accumulate(pfb, fbb, (int64_t)(H * p.F + H), (int64_t)(H * p.F), out.dW[0], first, st);
-        accumulate(pfb + (size_t)H * p.F, fbb, (int64_t)(H * p.F + H), (int64_t)H, out.db[0], first, st);
       }
       hipError_t e = hipGetLastError();
       if (e != hipSuccess) return e;

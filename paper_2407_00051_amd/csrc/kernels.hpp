@@ -68,7 +68,7 @@ hipError_t launch_disc_f32(const DiscArgs& a, void* ws, int n_cu, hipStream_t st
 // disc_bf16.hip --------------------------------------------------------------
 // Samples the fake events itself when a.fake_src is set (any E); never writes dLg_dtheta.
 bool disc_bf16_supported(const sagips_mlp& D, int d, const char** why);
-size_t disc_bf16_workspace(const DiscArgs& a);
+size_t disc_bf16_workspace(const DiscArgs& a, int n_cu);
 hipError_t launch_disc_bf16(const DiscArgs& a, void* ws, int n_cu, hipStream_t st, Timer* tm);
 
 }  // namespace sagips
