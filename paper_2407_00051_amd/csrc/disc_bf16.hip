@@ -86,19 +86,25 @@ __device__ __forceinline__ f32x4 mfma_bf16(bf16x8 a, bf16x8 b, f32x4 c) {
 }
 
 // ---------------------------------------------------------------------------
-// Weights: bf16 copies of the hidden layers, plain and transposed.
-__global__ __launch_bounds__(256) void k_weights_bf16(const float* __restrict__ W, u16* __restrict__ Wb,
-                                                      u16* __restrict__ WTb, int H) {
-  __shared__ u16 t[32][33];
-  const int bx = blockIdx.x * 32, by = blockIdx.y * 32;
-  const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;
-  for (int r = ty; r < 32; r += 8) {
-    const u16 v = bf16_bits(W[(by + r) * H + bx + tx]);
-    Wb[(by + r) * H + bx + tx] = v;
-    t[r][tx] = v;
+// Weights: bf16 copies of one hidden layer, W ([out][in]) and W^T, in the order
+// the chain kernels consume them as MFMA A fragments: piece (rb, ks, lane)
+// holds rows 32 rb + lane % 32, columns 16 ks + 8 (lane / 32) .. + 7, so the
+// 64 lanes of a wave read one contiguous kilobyte per fragment.
+__global__ __launch_bounds__(256) void k_weights_frag(const float* __restrict__ W, u16* __restrict__ Wf,
+                                                      u16* __restrict__ WTf, int H) {
+  const int t = blockIdx.x * 256 + threadIdx.x;
+  const int KS = H / 16;
+  if (t >= H * H / 8) return;
+  const int rb = t / (KS * 64), rem = t % (KS * 64), ks = rem / 64, lane = rem % 64;
+  const int row = 32 * rb + (lane & 31), col0 = 16 * ks + 8 * (lane >> 5);
+  uint32_t wp[4], wt[4];
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    wp[u] = (uint32_t)bf16_bits(W[row * H + col0 + 2 * u]) | ((uint32_t)bf16_bits(W[row * H + col0 + 2 * u + 1]) << 16);
+    wt[u] = (uint32_t)bf16_bits(W[(col0 + 2 * u) * H + row]) | ((uint32_t)bf16_bits(W[(col0 + 2 * u + 1) * H + row]) << 16);
   }
-  __syncthreads();
-  for (int r = ty; r < 32; r += 8) WTb[(bx + r) * H + by + tx] = t[tx][r];
+  *reinterpret_cast<uint4*>(Wf + (size_t)t * 8) = make_uint4(wp[0], wp[1], wp[2], wp[3]);
+  *reinterpret_cast<uint4*>(WTf + (size_t)t * 8) = make_uint4(wt[0], wt[1], wt[2], wt[3]);
 }
 
 // ---------------------------------------------------------------------------
@@ -171,37 +177,44 @@ __global__ __launch_bounds__(256) void k_prep(ChunkArgs c, const float* __restri
 // ---------------------------------------------------------------------------
 // Per-tile layer chains.  A persistent workgroup of 4 waves per CU (one per
 // SIMD, so each wave has the whole register file of its SIMD) loops over
-// tiles of T event rows; the tile's activations (forward) or unit-seed signals
-// (backward) live in LDS as [T][H + 8] bf16 and are overwritten layer by
-// layer, so between layers nothing goes through HBM except what the
+// tiles of T event rows; the tile's activations (forward) or unit-seed
+// signals (backward) live in LDS as [T][H + 8] bf16 and are overwritten layer
+// by layer, so between layers nothing goes through HBM except what the
 // weight-gradient products need later.  Wave w owns output features
-// [16 MI w, 16 MI (w + 1)) of every product outT = W' inT for all T events:
-// MI x JW = 32 MFMA tiles, so each K block of 32 takes MI 16-byte weight
-// loads (global, L2-resident, issued PD blocks ahead) and JW 16-byte LDS
-// reads (issued one block ahead) for 32 MFMAs.  The 16-byte row pad makes
-// each 8-lane group of an LDS fragment read hit distinct banks.  Lane l holds,
-// for MFMA tile (i, j), the outputs o = ow + 16 i + 4 (l / 16) + q, q < 4, of
-// event 16 j + (l % 16); the forward's first layer (K = F, VALU) produces its
-// outputs in the same arrangement.
+// [32 MT w, 32 MT (w + 1)) of every product outT = W' inT for all T events,
+// as MT x NT 32x32 tiles of v_mfma_f32_32x32x16_bf16 (the 32x32 shape keeps
+// the matrix core busy from a single wave per SIMD; the 16x16 one does not).
+// Each K step of 16 takes MT 16-byte weight loads (global, L2-resident, from
+// the fragment-ordered copies, issued PD steps ahead) and NT 16-byte LDS reads (one step ahead) for MT NT
+// products.  The 16-byte row pad makes each 8-lane group of an LDS fragment
+// read hit distinct banks.
+//
+// Lane l holds, in register 4 g + q of tile (mt, nt), the output of feature
+// ow + 32 mt + 8 g + 4 (l / 32) + q for event 32 nt + (l % 32): each group g
+// is 4 consecutive features of one event (one 8-byte bf16 store).  The
+// forward's first layer (K = F, VALU) produces its outputs in the same
+// arrangement.
 //
 // Signs of the hidden activations are kept as lane-local bit masks: the 128
-// outputs a lane holds in one layer are numbered e = 4 (i JW + j) + q and bit
-// 31 - e % 32 of word e / 32 is set where the bf16 activation is > 0; each
-// lane stores its 4 words as one 16-byte vector, [layer][tile][wave][lane].
+// outputs a lane holds in one layer are numbered e = 16 (mt NT + nt) + 4 g + q
+// and bit 31 - e % 32 of word e / 32 is set where the bf16 activation is > 0;
+// each lane stores its 4 words as one 16-byte vector, [layer][tile][wave][lane].
 // The backward chain has the same lane arrangement and reads them back, so
 // LeakyReLU' costs 16 bytes per lane and layer instead of the activations.
 constexpr int kChainThreads = 256;
 constexpr int kChainBlocksPerCU = 1;
 
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+
 template <int H>
 struct Chain {
   static constexpr int WAVES = kChainThreads / 64;
-  static constexpr int MI = H / (16 * WAVES);   // 16-feature MFMA tiles per wave
-  static constexpr int JW = 32 / MI;            // 16-event MFMA tiles per wave
-  static constexpr int T = 16 * JW;             // events per tile
+  static constexpr int MT = H / (32 * WAVES);   // 32-feature MFMA tiles per wave
+  static constexpr int NT = 8 / MT;             // 32-event MFMA tiles per wave
+  static constexpr int T = 32 * NT;             // events per tile
   static constexpr int LDA = H + 8;             // LDS row stride (bf16)
-  static constexpr int PD = 2;                  // weight prefetch distance (K blocks)
-  static_assert(MI * JW == 32 && T * H == 32768, "chain decomposition");
+  static constexpr int PD = 3;                  // weight prefetch distance (K steps of 16)
+  static_assert(MT * NT == 8 && T * H == 32768, "chain decomposition");
 };
 
 typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
@@ -213,83 +226,90 @@ __device__ __forceinline__ uint32_t pack_bf16(float lo, float hi) {
   return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2{lo, hi}), bf16x2_t));
 }
 __device__ __forceinline__ float lo_bf16(uint32_t p) { return __uint_as_float(p << 16); }
+__device__ __forceinline__ float hi_bf16(uint32_t p) { return __uint_as_float(p & 0xffff0000u); }
 
 // Row-contiguous copy of a [T][H] bf16 tile from LDS (row stride LDA) to
 // global memory (row stride H): 16 bytes per lane, whole 128-byte lines.
-template <int H, int T, int LDA, int NT>
+template <int H, int T, int LDA, int NTH>
 __device__ __forceinline__ void copy_out(const u16* act, u16* __restrict__ gdst, int tid) {
   constexpr int PR = H / 8;   // 16-byte pieces per row
 #pragma unroll 4
-  for (int k = tid; k < T * PR; k += NT) {
+  for (int k = tid; k < T * PR; k += NTH) {
     const int row = k / PR, col = (k % PR) * 8;
     *reinterpret_cast<uint4*>(gdst + (int64_t)row * H + col) = *reinterpret_cast<const uint4*>(act + row * LDA + col);
   }
 }
-__device__ __forceinline__ float hi_bf16(uint32_t p) { return __uint_as_float(p & 0xffff0000u); }
 
-// acc[i][j] = init[i] + sum_k Wg[ow + 16 i + 4 lg + q][k] act[16 j + lr][k]
+// acc[mt][nt] = init[mt] + sum_k Wg[feature][k] act[event][k] (see above for the arrangement)
 template <int H>
 __device__ __forceinline__ void chain_gemm(const u16* __restrict__ Wg, const u16* act,
-                                           f32x4 (&acc)[Chain<H>::MI][Chain<H>::JW],
-                                           const f32x4 (&init)[Chain<H>::MI], int ow, int lr, int lg) {
+                                           f32x16 (&acc)[Chain<H>::MT][Chain<H>::NT],
+                                           const f32x16 (&init)[Chain<H>::MT], int ow, int lane) {
   using C = Chain<H>;
-  constexpr int KB = H / 32, PD = C::PD, LDA = C::LDA, MI = C::MI, JW = C::JW;
+  constexpr int KS = H / 16, PD = C::PD, LDA = C::LDA, MT = C::MT, NT = C::NT;
 #pragma unroll
-  for (int i = 0; i < MI; ++i)
+  for (int m = 0; m < MT; ++m)
 #pragma unroll
-    for (int j = 0; j < JW; ++j) acc[i][j] = init[i];
-  const u16* wrow = Wg + (size_t)(ow + lr) * H + 8 * lg;
-  const u16* brow = act + lr * LDA + 8 * lg;
-  bf16x8 a[PD + 1][MI];
-  bf16x8 b[2][JW];
+    for (int n = 0; n < NT; ++n) acc[m][n] = init[m];
+  const int lr = lane & 31, lh = lane >> 5;
+  // fragment (m, ks) of this wave: piece ((ow / 32 + m) KS + ks) 64 + lane of the fragment-ordered copy
+  const u16* wfr = Wg + ((size_t)(ow / 32) * KS * 64 + lane) * 8;
+  const u16* brow = act + lr * LDA + 8 * lh;
+  bf16x8 a[PD + 1][MT];
+  bf16x8 b[2][NT];
 #pragma unroll
   for (int q = 0; q < PD; ++q)
 #pragma unroll
-    for (int i = 0; i < MI; ++i) a[q][i] = *reinterpret_cast<const bf16x8*>(wrow + (size_t)16 * i * H + 32 * q);
+    for (int m = 0; m < MT; ++m) a[q][m] = *reinterpret_cast<const bf16x8*>(wfr + ((size_t)m * KS + q) * 512);
 #pragma unroll
-  for (int j = 0; j < JW; ++j) b[0][j] = *reinterpret_cast<const bf16x8*>(brow + 16 * j * LDA);
+  for (int n = 0; n < NT; ++n) b[0][n] = *reinterpret_cast<const bf16x8*>(brow + 32 * n * LDA);
 #pragma unroll
-  for (int kb = 0; kb < KB; ++kb) {
-    if (kb + PD < KB) {
+  for (int ks = 0; ks < KS; ++ks) {
+    if (ks + PD < KS) {
 #pragma unroll
-      for (int i = 0; i < MI; ++i)
-        a[(kb + PD) % (PD + 1)][i] = *reinterpret_cast<const bf16x8*>(wrow + (size_t)16 * i * H + 32 * (kb + PD));
+      for (int m = 0; m < MT; ++m)
+        a[(ks + PD) % (PD + 1)][m] = *reinterpret_cast<const bf16x8*>(wfr + ((size_t)m * KS + ks + PD) * 512);
     }
-    if (kb + 1 < KB) {
+    if (ks + 1 < KS) {
 #pragma unroll
-      for (int j = 0; j < JW; ++j)
-        b[(kb + 1) & 1][j] = *reinterpret_cast<const bf16x8*>(brow + 16 * j * LDA + 32 * (kb + 1));
+      for (int n = 0; n < NT; ++n)
+        b[(ks + 1) & 1][n] = *reinterpret_cast<const bf16x8*>(brow + 32 * n * LDA + 16 * (ks + 1));
     }
-    // keep the prefetches above the products of this block (the scheduler
+    // keep the prefetches above the products of this step (the scheduler
     // would otherwise sink each load next to its first use)
     __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-    for (int j = 0; j < JW; ++j)
+    for (int n = 0; n < NT; ++n)
 #pragma unroll
-      for (int i = 0; i < MI; ++i) acc[i][j] = mfma_bf16(a[kb % (PD + 1)][i], b[kb & 1][j], acc[i][j]);
+      for (int m = 0; m < MT; ++m)
+        acc[m][n] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[ks % (PD + 1)][m], b[ks & 1][n], acc[m][n], 0, 0, 0);
     __builtin_amdgcn_sched_barrier(0);
   }
 }
 
 // LeakyReLU (slope in [0, 1]: max(v, s v)), bf16 rounding and the lane's sign
-// mask of one layer's outputs.  pk[i][j] = packed bf16 of q = 0,1 and 2,3.
-template <int MI, int JW>
-__device__ __forceinline__ void activate(const f32x4 (&v)[MI][JW], float slope, uint2 (&pk)[MI][JW], uint4& mask) {
+// mask of one layer's outputs.  pk[mt][nt][g] = packed bf16 of q = 0,1 and 2,3.
+template <int MT, int NT>
+__device__ __forceinline__ void activate(const f32x16 (&v)[MT][NT], float slope, uint2 (&pk)[MT][NT][4],
+                                         uint4& mask) {
   uint32_t m[4] = {0u, 0u, 0u, 0u};
 #pragma unroll
-  for (int i = 0; i < MI; ++i)
+  for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-    for (int j = 0; j < JW; ++j) {
-      const int e = 4 * (i * JW + j);
-      const uint32_t p01 = pack_bf16(fmaxf(v[i][j][0], slope * v[i][j][0]), fmaxf(v[i][j][1], slope * v[i][j][1]));
-      const uint32_t p23 = pack_bf16(fmaxf(v[i][j][2], slope * v[i][j][2]), fmaxf(v[i][j][3], slope * v[i][j][3]));
-      pk[i][j] = make_uint2(p01, p23);
-      uint32_t& w = m[e >> 5];
-      w = (w << 1) | (uint32_t)((int32_t)(p01 << 16) > 0);
-      w = (w << 1) | (uint32_t)((int32_t)p01 >= 0x10000);
-      w = (w << 1) | (uint32_t)((int32_t)(p23 << 16) > 0);
-      w = (w << 1) | (uint32_t)((int32_t)p23 >= 0x10000);
-    }
+    for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const int e = 16 * (mt * NT + nt) + 4 * g;
+        const f32x16& x = v[mt][nt];
+        const uint32_t p01 = pack_bf16(fmaxf(x[4 * g], slope * x[4 * g]), fmaxf(x[4 * g + 1], slope * x[4 * g + 1]));
+        const uint32_t p23 = pack_bf16(fmaxf(x[4 * g + 2], slope * x[4 * g + 2]), fmaxf(x[4 * g + 3], slope * x[4 * g + 3]));
+        pk[mt][nt][g] = make_uint2(p01, p23);
+        uint32_t& w = m[e >> 5];
+        w = (w << 1) | (uint32_t)((int32_t)(p01 << 16) > 0);
+        w = (w << 1) | (uint32_t)((int32_t)p01 >= 0x10000);
+        w = (w << 1) | (uint32_t)((int32_t)(p23 << 16) > 0);
+        w = (w << 1) | (uint32_t)((int32_t)p23 >= 0x10000);
+      }
   mask = make_uint4(m[0], m[1], m[2], m[3]);
 }
 
@@ -299,11 +319,24 @@ __device__ __forceinline__ bool mask_bit(const uint4& m, int e) {
   return (w >> (31 - (e & 31))) & 1u;
 }
 
+// Writes a layer's packed outputs into the LDS tile.
+template <int MT, int NT, int LDA>
+__device__ __forceinline__ void store_tile(u16* act, const uint2 (&pk)[MT][NT][4], int ow, int lane) {
+  const int lr = lane & 31, lh = lane >> 5;
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+      for (int g = 0; g < 4; ++g)
+        *reinterpret_cast<uint2*>(act + (32 * nt + lr) * LDA + ow + 32 * mt + 8 * g + 4 * lh) = pk[mt][nt][g];
+}
+
 struct ChainArgs {
   const float* W0;           // first layer [H][F] fp32
   const float* b0;           // [H]
-  const u16* Wb;             // hidden layers, bf16 [NH][H][H] ([out][in])
-  const u16* WTb;            // the same, transposed ([in][out])
+  const u16* Wb;             // hidden layers, bf16 [NH][H][H] ([out][in]), fragment order
+  const u16* WTb;            // the same, transposed ([in][out]), fragment order
   const float* bh[kMaxNH];   // hidden biases
   const float* wo;           // logit layer [H]
   const float* bo;           // [1]
@@ -333,49 +366,52 @@ __device__ __forceinline__ float softplus_fast(float t) { return fmaxf(t, 0.0f) 
 template <int H, int F>
 __global__ __launch_bounds__(kChainThreads, kChainBlocksPerCU) void k_fwd_chain(ChainArgs p) {
   using C = Chain<H>;
-  constexpr int T = C::T, LDA = C::LDA, WAVES = C::WAVES, MI = C::MI, JW = C::JW;
-  constexpr int NT = kChainThreads;
+  constexpr int T = C::T, LDA = C::LDA, WAVES = C::WAVES, MT = C::MT, NT = C::NT;
+  constexpr int NTH = kChainThreads;
   __shared__ __attribute__((aligned(16))) u16 act[T * LDA];
   __shared__ float sW0[H * (F + 1)];            // row o: W0[o][0 .. F-1], b0[o]
   __shared__ float zpart[WAVES][T];
   __shared__ __attribute__((aligned(16))) float swo[H];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int lr = lane & 15, lg = lane >> 4;
-  const int ow = 16 * MI * wave;
+  const int lr = lane & 31, lh = lane >> 5;
+  const int ow = 32 * MT * wave;
   const ChunkArgs c = p.c;
   const int64_t rstride = (int64_t)c.rows;
   const int ntiles = c.rows / T;
   const float slope = p.slope;
-  for (int k = tid; k < H * F; k += NT) sW0[(k / F) * (F + 1) + k % F] = p.W0[k];
-  for (int k = tid; k < H; k += NT) {
+  for (int k = tid; k < H * F; k += NTH) sW0[(k / F) * (F + 1) + k % F] = p.W0[k];
+  for (int k = tid; k < H; k += NTH) {
     sW0[k * (F + 1) + F] = p.b0[k];
     swo[k] = p.wo[k];
   }
-  float dwo[MI][4];
+  // dW_o partial of feature ow + 32 mt + 8 g + 4 lh + q
+  float dwo[MT][4][4];
 #pragma unroll
-  for (int i = 0; i < MI; ++i)
+  for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-    for (int q = 0; q < 4; ++q) dwo[i][q] = 0.f;
+    for (int g = 0; g < 4; ++g)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) dwo[mt][g][q] = 0.f;
   const float bo = p.bo[0];
   float l0 = 0.f, l1 = 0.f, se = 0.f;
   // this lane's features of the next tile, loaded one tile ahead
-  float fnext[JW][F];
+  float fnext[NT][F];
   auto load_feat = [&](int tile) __attribute__((always_inline)) {
 #pragma unroll
-    for (int j = 0; j < JW; ++j)
+    for (int nt = 0; nt < NT; ++nt)
 #pragma unroll
-      for (int k = 0; k < F; ++k) fnext[j][k] = p.feat[(int64_t)(tile * T + 16 * j + lr) * F + k];
+      for (int k = 0; k < F; ++k) fnext[nt][k] = p.feat[(int64_t)(tile * T + 32 * nt + lr) * F + k];
   };
   if ((int)blockIdx.x < ntiles) load_feat(blockIdx.x);
   __syncthreads();
 
   for (int tile = blockIdx.x; tile < ntiles; tile += gridDim.x) {
     const int r0 = tile * T;
-    float f[JW][F];
+    float f[NT][F];
 #pragma unroll
-    for (int j = 0; j < JW; ++j)
+    for (int nt = 0; nt < NT; ++nt)
 #pragma unroll
-      for (int k = 0; k < F; ++k) f[j][k] = fnext[j][k];
+      for (int k = 0; k < F; ++k) f[nt][k] = fnext[nt][k];
     if (tile + (int)gridDim.x < ntiles) load_feat(tile + gridDim.x);
     auto mask_at = [&](int layer) __attribute__((always_inline)) {
       return p.mask + (((int64_t)layer * ntiles + tile) * WAVES + wave) * 64 + lane;
@@ -383,83 +419,80 @@ __global__ __launch_bounds__(kChainThreads, kChainBlocksPerCU) void k_fwd_chain(
 
     // ---- first layer (VALU, K = F) in the MFMA output arrangement ----------
     {
-      f32x4 v[MI][JW];
+      f32x16 v[MT][NT];
 #pragma unroll
-      for (int i = 0; i < MI; ++i)
+      for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const float* w = &sW0[(ow + 16 * i + 4 * lg + q) * (F + 1)];
-          float wr[F + 1];
+        for (int g = 0; g < 4; ++g)
 #pragma unroll
-          for (int k = 0; k <= F; ++k) wr[k] = w[k];
+          for (int q = 0; q < 4; ++q) {
+            const float* w = &sW0[(ow + 32 * mt + 8 * g + 4 * lh + q) * (F + 1)];
+            float wr[F + 1];
 #pragma unroll
-          for (int j = 0; j < JW; ++j) {
-            float t = wr[F];
+            for (int k = 0; k <= F; ++k) wr[k] = w[k];
 #pragma unroll
-            for (int k = 0; k < F; ++k) t = fmaf(wr[k], f[j][k], t);
-            v[i][j][q] = t;
+            for (int nt = 0; nt < NT; ++nt) {
+              float t = wr[F];
+#pragma unroll
+              for (int k = 0; k < F; ++k) t = fmaf(wr[k], f[nt][k], t);
+              v[mt][nt][4 * g + q] = t;
+            }
           }
-        }
-      uint2 pk[MI][JW];
+      uint2 pk[MT][NT][4];
       uint4 m;
-      activate<MI, JW>(v, slope, pk, m);
+      activate<MT, NT>(v, slope, pk, m);
       *mask_at(0) = m;
-#pragma unroll
-      for (int i = 0; i < MI; ++i)
-#pragma unroll
-        for (int j = 0; j < JW; ++j) {
-          const int ev = 16 * j + lr, o = ow + 16 * i + 4 * lg;
-          *reinterpret_cast<uint2*>(act + ev * LDA + o) = pk[i][j];
-        }
+      store_tile<MT, NT, LDA>(act, pk, ow, lane);
     }
     __syncthreads();
-    copy_out<H, T, LDA, NT>(act, p.act + (int64_t)r0 * H, tid);
+    copy_out<H, T, LDA, NTH>(act, p.act + (int64_t)r0 * H, tid);
 
     // ---- hidden layers -----------------------------------------------------
     for (int l = 0; l < p.NH; ++l) {
       const bool last = l == p.NH - 1;
-      f32x4 bias[MI];
+      f32x16 bias[MT];
 #pragma unroll
-      for (int i = 0; i < MI; ++i) bias[i] = *reinterpret_cast<const f32x4*>(p.bh[l] + ow + 16 * i + 4 * lg);
-      f32x4 acc[MI][JW];
-      chain_gemm<H>(p.Wb + (size_t)l * H * H, act, acc, bias, ow, lr, lg);
-      uint2 pk[MI][JW];
+      for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const f32x4 b4 = *reinterpret_cast<const f32x4*>(p.bh[l] + ow + 32 * mt + 8 * g + 4 * lh);
+#pragma unroll
+          for (int q = 0; q < 4; ++q) bias[mt][4 * g + q] = b4[q];
+        }
+      f32x16 acc[MT][NT];
+      chain_gemm<H>(p.Wb + (size_t)l * H * H, act, acc, bias, ow, lane);
+      uint2 pk[MT][NT][4];
       uint4 m;
-      activate<MI, JW>(acc, slope, pk, m);
+      activate<MT, NT>(acc, slope, pk, m);
       *mask_at(l + 1) = m;
       if (!last) {
         __syncthreads();                             // every wave is done reading this layer's input
-#pragma unroll
-        for (int i = 0; i < MI; ++i)
-#pragma unroll
-          for (int j = 0; j < JW; ++j) {
-            const int ev = 16 * j + lr, o = ow + 16 * i + 4 * lg;
-            *reinterpret_cast<uint2*>(act + ev * LDA + o) = pk[i][j];
-          }
+        store_tile<MT, NT, LDA>(act, pk, ow, lane);
         __syncthreads();
-        copy_out<H, T, LDA, NT>(act, p.act + ((int64_t)(l + 1) * rstride + r0) * H, tid);
+        copy_out<H, T, LDA, NTH>(act, p.act + ((int64_t)(l + 1) * rstride + r0) * H, tid);
         continue;
       }
       // ---- logit layer and BCE seeds (fp32 dot over the bf16 activations) --
 #pragma unroll
-      for (int j = 0; j < JW; ++j) {
+      for (int nt = 0; nt < NT; ++nt) {
         float s = 0.f;
 #pragma unroll
-        for (int i = 0; i < MI; ++i) {
-          const f32x4 w4 = *reinterpret_cast<const f32x4*>(&swo[ow + 16 * i + 4 * lg]);
-          s = fmaf(lo_bf16(pk[i][j].x), w4[0], s);
-          s = fmaf(hi_bf16(pk[i][j].x), w4[1], s);
-          s = fmaf(lo_bf16(pk[i][j].y), w4[2], s);
-          s = fmaf(hi_bf16(pk[i][j].y), w4[3], s);
-        }
-        s += __shfl_xor(s, 16, 64);
+        for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+          for (int g = 0; g < 4; ++g) {
+            const f32x4 w4 = *reinterpret_cast<const f32x4*>(&swo[ow + 32 * mt + 8 * g + 4 * lh]);
+            s = fmaf(lo_bf16(pk[mt][nt][g].x), w4[0], s);
+            s = fmaf(hi_bf16(pk[mt][nt][g].x), w4[1], s);
+            s = fmaf(lo_bf16(pk[mt][nt][g].y), w4[2], s);
+            s = fmaf(hi_bf16(pk[mt][nt][g].y), w4[3], s);
+          }
         s += __shfl_xor(s, 32, 64);
-        if (lg == 0) zpart[wave][16 * j + lr] = s;
+        if (lh == 0) zpart[wave][32 * nt + lr] = s;
       }
       __syncthreads();
 #pragma unroll
-      for (int j = 0; j < JW; ++j) {
-        const int ev = 16 * j + lr, r = r0 + ev;
+      for (int nt = 0; nt < NT; ++nt) {
+        const int ev = 32 * nt + lr, r = r0 + ev;
         float z = bo;
 #pragma unroll
         for (int w = 0; w < WAVES; ++w) z += zpart[w][ev];
@@ -475,13 +508,15 @@ __global__ __launch_bounds__(kChainThreads, kChainBlocksPerCU) void k_fwd_chain(
           }
         }
 #pragma unroll
-        for (int i = 0; i < MI; ++i) {
-          dwo[i][0] = fmaf(e, lo_bf16(pk[i][j].x), dwo[i][0]);
-          dwo[i][1] = fmaf(e, hi_bf16(pk[i][j].x), dwo[i][1]);
-          dwo[i][2] = fmaf(e, lo_bf16(pk[i][j].y), dwo[i][2]);
-          dwo[i][3] = fmaf(e, hi_bf16(pk[i][j].y), dwo[i][3]);
-        }
-        if (lg == 0 && j % WAVES == wave) {        // one lane per event, spread over the waves
+        for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+          for (int gg = 0; gg < 4; ++gg) {
+            dwo[mt][gg][0] = fmaf(e, lo_bf16(pk[mt][nt][gg].x), dwo[mt][gg][0]);
+            dwo[mt][gg][1] = fmaf(e, hi_bf16(pk[mt][nt][gg].x), dwo[mt][gg][1]);
+            dwo[mt][gg][2] = fmaf(e, lo_bf16(pk[mt][nt][gg].y), dwo[mt][gg][2]);
+            dwo[mt][gg][3] = fmaf(e, hi_bf16(pk[mt][nt][gg].y), dwo[mt][gg][3]);
+          }
+        if (lh == 0 && (ev & (WAVES - 1)) == wave) {     // one lane per event, spread over the waves
           p.eD[r] = e;
           p.eG[r] = g;
           se += e;
@@ -504,24 +539,22 @@ __global__ __launch_bounds__(kChainThreads, kChainBlocksPerCU) void k_fwd_chain(
   // ---- per-workgroup partials, fixed order ---------------------------------
   float* dst = p.plog + (int64_t)blockIdx.x * (H + 3);
 #pragma unroll
-  for (int i = 0; i < MI; ++i)
+  for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      float v = dwo[i][q];
-      v += __shfl_xor(v, 1, 64);
-      v += __shfl_xor(v, 2, 64);
-      v += __shfl_xor(v, 4, 64);
-      v += __shfl_xor(v, 8, 64);
-      if (lr == 0) dst[ow + 16 * i + 4 * lg + q] = v;
-    }
+    for (int g = 0; g < 4; ++g)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        float v = dwo[mt][g][q];
+#pragma unroll
+        for (int o = 1; o < 32; o <<= 1) v += __shfl_xor(v, o, 64);
+        if (lr == 0) dst[ow + 32 * mt + 8 * g + 4 * lh + q] = v;
+      }
   float s3[3] = {l0, l1, se};
 #pragma unroll
   for (int k = 0; k < 3; ++k) {
     float v = s3[k];
-    v += __shfl_xor(v, 1, 64);
-    v += __shfl_xor(v, 2, 64);
-    v += __shfl_xor(v, 4, 64);
-    v += __shfl_xor(v, 8, 64);
+#pragma unroll
+    for (int o = 1; o < 32; o <<= 1) v += __shfl_xor(v, o, 64);
     if (lane == 0) zpart[wave][k] = v;
   }
   __syncthreads();
@@ -541,10 +574,10 @@ __global__ __launch_bounds__(kChainThreads, kChainBlocksPerCU) void k_fwd_chain(
 template <int H, int F, int D, bool kHD8>
 __global__ __launch_bounds__(kChainThreads, kChainBlocksPerCU) void k_bwd_chain(ChainArgs p) {
   using C = Chain<H>;
-  constexpr int T = C::T, LDA = C::LDA, WAVES = C::WAVES, MI = C::MI, JW = C::JW;
-  constexpr int NT = kChainThreads;
-  constexpr int FPT = H / NT;        // first-layer features per thread
-  constexpr int P = NT / T;          // threads per event in the input-gradient dot
+  constexpr int T = C::T, LDA = C::LDA, WAVES = C::WAVES, MT = C::MT, NT = C::NT;
+  constexpr int NTH = kChainThreads;
+  constexpr int FPT = H / NTH;       // first-layer features per thread
+  constexpr int P = NTH / T;         // threads per event in the input-gradient dot
   __shared__ __attribute__((aligned(16))) u16 act[T * LDA];
   __shared__ float sW0[H * F];
   __shared__ float sfeat[T][F];
@@ -552,13 +585,13 @@ __global__ __launch_bounds__(kChainThreads, kChainBlocksPerCU) void k_bwd_chain(
   __shared__ float se[T][2];
   __shared__ __attribute__((aligned(16))) float swo[H];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int lr = lane & 15, lg = lane >> 4;
-  const int ow = 16 * MI * wave;
+  const int lh = lane >> 5;
+  const int ow = 32 * MT * wave;
   const ChunkArgs c = p.c;
   const int64_t rstride = (int64_t)c.rows;
   const int ntiles = c.rows / T;
-  for (int k = tid; k < H * F; k += NT) sW0[k] = p.W0[k];
-  for (int k = tid; k < H; k += NT) swo[k] = p.wo[k];
+  for (int k = tid; k < H * F; k += NTH) sW0[k] = p.W0[k];
+  for (int k = tid; k < H; k += NTH) swo[k] = p.wo[k];
   float adw[FPT][F + 1];
 #pragma unroll
   for (int u = 0; u < FPT; ++u)
@@ -567,70 +600,71 @@ __global__ __launch_bounds__(kChainThreads, kChainBlocksPerCU) void k_bwd_chain(
   const bool want_dx = c.fake && p.dLg_dx != nullptr;
   const float slope = p.slope;
   const int NH = p.NH;
-  f32x4 zero[MI];
+  f32x16 zero[MT];
 #pragma unroll
-  for (int i = 0; i < MI; ++i) zero[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) zero[mt][r] = 0.f;
 
   for (int tile = blockIdx.x; tile < ntiles; tile += gridDim.x) {
     const int r0 = tile * T;
     auto mask_at = [&](int layer) __attribute__((always_inline)) {
       return p.mask + (((int64_t)layer * ntiles + tile) * WAVES + wave) * 64 + lane;
     };
-    for (int k = tid; k < T; k += NT) {
+    for (int k = tid; k < T; k += NTH) {
       se[k][0] = p.eD[r0 + k];
       se[k][1] = p.eG[r0 + k];
     }
-    for (int k = tid; k < T * F; k += NT) sfeat[k / F][k % F] = p.feat[(int64_t)r0 * F + k];
+    for (int k = tid; k < T * F; k += NTH) sfeat[k / F][k % F] = p.feat[(int64_t)r0 * F + k];
     if (want_dx && kHD8)
-      for (int k = tid; k < T * D; k += NT) sx[k / D][k % D] = p.xs[(int64_t)r0 * D + k];
+      for (int k = tid; k < T * D; k += NTH) sx[k / D][k % D] = p.xs[(int64_t)r0 * D + k];
     // ---- unit-seed signal at A_{NH+1}: w_o * LeakyReLU'(A_{NH+1}) ----------
     {
       const uint4 m = *mask_at(NH);
-      u16* gdst = p.dlt + (int64_t)(NH - 1) * rstride * H;
+      uint2 pk[MT][NT][4];
 #pragma unroll
-      for (int i = 0; i < MI; ++i) {
-        const f32x4 w4 = *reinterpret_cast<const f32x4*>(&swo[ow + 16 * i + 4 * lg]);
+      for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-        for (int j = 0; j < JW; ++j) {
-          const int e = 4 * (i * JW + j);
-          float d[4];
+        for (int g = 0; g < 4; ++g) {
+          const f32x4 w4 = *reinterpret_cast<const f32x4*>(&swo[ow + 32 * mt + 8 * g + 4 * lh]);
 #pragma unroll
-          for (int q = 0; q < 4; ++q) d[q] = mask_bit(m, e + q) ? w4[q] : w4[q] * slope;
-          const uint2 v = make_uint2(pack_bf16(d[0], d[1]), pack_bf16(d[2], d[3]));
-          const int ev = 16 * j + lr, o = ow + 16 * i + 4 * lg;
-          *reinterpret_cast<uint2*>(act + ev * LDA + o) = v;
+          for (int nt = 0; nt < NT; ++nt) {
+            const int e = 16 * (mt * NT + nt) + 4 * g;
+            float d[4];
+#pragma unroll
+            for (int q = 0; q < 4; ++q) d[q] = mask_bit(m, e + q) ? w4[q] : w4[q] * slope;
+            pk[mt][nt][g] = make_uint2(pack_bf16(d[0], d[1]), pack_bf16(d[2], d[3]));
+          }
         }
-      }
+      store_tile<MT, NT, LDA>(act, pk, ow, lane);
       __syncthreads();
-      copy_out<H, T, LDA, NT>(act, gdst + (int64_t)r0 * H, tid);
+      copy_out<H, T, LDA, NTH>(act, p.dlt + ((int64_t)(NH - 1) * rstride + r0) * H, tid);
     }
     // ---- hidden layers, top down ---------------------------------------------
     for (int l = NH - 1; l >= 0; --l) {
-      f32x4 acc[MI][JW];
-      chain_gemm<H>(p.WTb + (size_t)l * H * H, act, acc, zero, ow, lr, lg);
+      f32x16 acc[MT][NT];
+      chain_gemm<H>(p.WTb + (size_t)l * H * H, act, acc, zero, ow, lane);
       const uint4 m = *mask_at(l);
-      uint2 pk[MI][JW];
+      uint2 pk[MT][NT][4];
 #pragma unroll
-      for (int i = 0; i < MI; ++i)
+      for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-        for (int j = 0; j < JW; ++j) {
-          const int e = 4 * (i * JW + j);
-          float d[4];
+        for (int nt = 0; nt < NT; ++nt)
 #pragma unroll
-          for (int q = 0; q < 4; ++q) d[q] = mask_bit(m, e + q) ? acc[i][j][q] : acc[i][j][q] * slope;
-          pk[i][j] = make_uint2(pack_bf16(d[0], d[1]), pack_bf16(d[2], d[3]));
-        }
+          for (int g = 0; g < 4; ++g) {
+            const int e = 16 * (mt * NT + nt) + 4 * g;
+            float d[4];
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+              const float v = acc[mt][nt][4 * g + q];
+              d[q] = mask_bit(m, e + q) ? v : v * slope;
+            }
+            pk[mt][nt][g] = make_uint2(pack_bf16(d[0], d[1]), pack_bf16(d[2], d[3]));
+          }
       __syncthreads();                               // every wave is done reading this layer's input
-      u16* gdst = l >= 1 ? p.dlt + (int64_t)(l - 1) * rstride * H : nullptr;
-#pragma unroll
-      for (int i = 0; i < MI; ++i)
-#pragma unroll
-        for (int j = 0; j < JW; ++j) {
-          const int ev = 16 * j + lr, o = ow + 16 * i + 4 * lg;
-          *reinterpret_cast<uint2*>(act + ev * LDA + o) = pk[i][j];
-        }
+      store_tile<MT, NT, LDA>(act, pk, ow, lane);
       __syncthreads();
-      if (gdst) copy_out<H, T, LDA, NT>(act, gdst + (int64_t)r0 * H, tid);
+      if (l >= 1) copy_out<H, T, LDA, NTH>(act, p.dlt + ((int64_t)(l - 1) * rstride + r0) * H, tid);
     }
     // ---- first layer: act holds the signal at A_1 ---------------------------
 #pragma unroll 4
@@ -638,7 +672,7 @@ __global__ __launch_bounds__(kChainThreads, kChainBlocksPerCU) void k_bwd_chain(
       const float e = se[ev][0];
 #pragma unroll
       for (int u = 0; u < FPT; ++u) {
-        const float ed = e * bf16_to_f32(act[ev * LDA + tid + NT * u]);
+        const float ed = e * bf16_to_f32(act[ev * LDA + tid + NTH * u]);
 #pragma unroll
         for (int j = 0; j < F; ++j) adw[u][j] = fmaf(ed, sfeat[ev][j], adw[u][j]);
         adw[u][F] += ed;
@@ -695,7 +729,7 @@ __global__ __launch_bounds__(kChainThreads, kChainBlocksPerCU) void k_bwd_chain(
   float* dst = p.pfb + (int64_t)blockIdx.x * (H * F + H);
 #pragma unroll
   for (int u = 0; u < FPT; ++u) {
-    const int o = tid + NT * u;
+    const int o = tid + NTH * u;
 #pragma unroll
     for (int j = 0; j < F; ++j) dst[o * F + j] = adw[u][j];
     dst[H * F + o] = adw[u][F];
@@ -1006,8 +1040,8 @@ hipError_t launch_disc_bf16(const DiscArgs& a, void* ws, int n_cu, hipStream_t s
 
   if (tm) tm->begin("disc_bf16_weights");
   for (int l = 0; l < NH; ++l)
-    hipLaunchKernelGGL(k_weights_bf16, dim3(H / 32, H / 32), dim3(256), 0, st, Dm.W[1 + l], Wb + (size_t)l * H * H,
-                       WTb + (size_t)l * H * H, H);
+    hipLaunchKernelGGL(k_weights_frag, dim3((H * H / 8 + 255) / 256), dim3(256), 0, st, Dm.W[1 + l],
+                       Wb + (size_t)l * H * H, WTb + (size_t)l * H * H, H);
   if (tm) tm->end();
 
   SourceArgs src{};
