@@ -77,9 +77,6 @@ __device__ __forceinline__ void store_bf16(u16* p, const float (&v)[PER]) {
   else *reinterpret_cast<uint4*>(p) = make_uint4(w[0], w[1], w[2], w[3]);
 }
 
-__device__ __forceinline__ float leaky(float v, float s) { return v > 0.0f ? v : s * v; }
-__device__ __forceinline__ float leaky_grad(float h, float s) { return h > 0.0f ? 1.0f : s; }
-__device__ __forceinline__ float softplus(float t) { return fmaxf(t, 0.0f) + log1pf(expf(-fabsf(t))); }
 
 __device__ __forceinline__ f32x4 mfma_bf16(bf16x8 a, bf16x8 b, f32x4 c) {
   return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
@@ -175,9 +172,10 @@ __global__ __launch_bounds__(256) void k_prep(ChunkArgs c, const float* __restri
 }
 
 // ---------------------------------------------------------------------------
-// Per-tile layer chains.  A persistent workgroup of 4 waves per CU (one per
-// SIMD, so each wave has the whole register file of its SIMD) loops over
-// tiles of T event rows; the tile's activations (forward) or unit-seed
+// Per-tile layer chains.  Persistent workgroups of 4 waves (BPC per CU: two
+// for H = 256, so that one workgroup's VALU epilogues and barriers overlap the
+// other's matrix products; one for H = 512, where a wave then has the whole
+// register file of its SIMD) loop over tiles of T = 64 event rows; the tile's activations (forward) or unit-seed
 // signals (backward) live in LDS as [T][H + 8] bf16 and are overwritten layer
 // by layer, so between layers nothing goes through HBM except what the
 // weight-gradient products need later.  Wave w owns output features
@@ -195,14 +193,13 @@ __global__ __launch_bounds__(256) void k_prep(ChunkArgs c, const float* __restri
 // forward's first layer (K = F, VALU) produces its outputs in the same
 // arrangement.
 //
-// Signs of the hidden activations are kept as lane-local bit masks: the 128
-// outputs a lane holds in one layer are numbered e = 16 (mt NT + nt) + 4 g + q
-// and bit 31 - e % 32 of word e / 32 is set where the bf16 activation is > 0;
-// each lane stores its 4 words as one 16-byte vector, [layer][tile][wave][lane].
+// Signs of the hidden activations are kept as lane-local bit masks: the 16 MT
+// NT outputs a lane holds in one layer are numbered e = 16 (mt NT + nt) + 4 g
+// + q and bit 31 - e % 32 of word e / 32 is set where the bf16 activation is
+// > 0; each lane stores its MW words as one vector, [layer][tile][wave][lane].
 // The backward chain has the same lane arrangement and reads them back, so
-// LeakyReLU' costs 16 bytes per lane and layer instead of the activations.
+// LeakyReLU' costs one bit per output instead of re-reading the activations.
 constexpr int kChainThreads = 256;
-constexpr int kChainBlocksPerCU = 1;
 
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 
@@ -210,12 +207,18 @@ template <int H>
 struct Chain {
   static constexpr int WAVES = kChainThreads / 64;
   static constexpr int MT = H / (32 * WAVES);   // 32-feature MFMA tiles per wave
-  static constexpr int NT = 8 / MT;             // 32-event MFMA tiles per wave
+  static constexpr int NT = 2;                  // 32-event MFMA tiles per wave
   static constexpr int T = 32 * NT;             // events per tile
   static constexpr int LDA = H + 8;             // LDS row stride (bf16)
   static constexpr int PD = 3;                  // weight prefetch distance (K steps of 16)
-  static_assert(MT * NT == 8 && T * H == 32768, "chain decomposition");
+  static constexpr int MW = MT * NT / 2;        // mask words per lane and layer (2 or 4)
+  static constexpr int BPC = H <= 256 ? 2 : 1;  // workgroups per CU
+  static_assert((MT == 2 || MT == 4) && (T * H / 8) % kChainThreads == 0, "chain decomposition");
 };
+
+template <int N> struct MaskWords;
+template <> struct MaskWords<2> { typedef uint2 type; };
+template <> struct MaskWords<4> { typedef uint4 type; };
 
 typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
 typedef float f32x2 __attribute__((ext_vector_type(2)));
@@ -228,52 +231,89 @@ __device__ __forceinline__ uint32_t pack_bf16(float lo, float hi) {
 __device__ __forceinline__ float lo_bf16(uint32_t p) { return __uint_as_float(p << 16); }
 __device__ __forceinline__ float hi_bf16(uint32_t p) { return __uint_as_float(p & 0xffff0000u); }
 
-// Row-contiguous copy of a [T][H] bf16 tile from LDS (row stride LDA) to
-// global memory (row stride H): 16 bytes per lane, whole 128-byte lines.
-template <int H, int T, int LDA, int NTH>
-__device__ __forceinline__ void copy_out(const u16* act, u16* __restrict__ gdst, int tid) {
-  constexpr int PR = H / 8;   // 16-byte pieces per row
-#pragma unroll 4
-  for (int k = tid; k < T * PR; k += NTH) {
-    const int row = k / PR, col = (k % PR) * 8;
-    *reinterpret_cast<uint4*>(gdst + (int64_t)row * H + col) = *reinterpret_cast<const uint4*>(act + row * LDA + col);
-  }
+// The first PD weight-fragment steps of the next product, loaded during the
+// tail of the current one.
+template <int H>
+struct WeightPrefetch {
+  bf16x8 a[Chain<H>::PD][Chain<H>::MT];
+};
+
+// Fragment (m, ks) of the wave's rows of a fragment-ordered weight copy is
+// piece ((ow / 32 + m) KS + ks) 64 + lane.
+template <int H>
+__device__ __forceinline__ const u16* frag_base(const u16* Wg, int ow, int lane) {
+  return Wg + ((size_t)(ow / 32) * (H / 16) * 64 + lane) * 8;
 }
 
-// acc[mt][nt] = init[mt] + sum_k Wg[feature][k] act[event][k] (see above for the arrangement)
 template <int H>
-__device__ __forceinline__ void chain_gemm(const u16* __restrict__ Wg, const u16* act,
-                                           f32x16 (&acc)[Chain<H>::MT][Chain<H>::NT],
-                                           const f32x16 (&init)[Chain<H>::MT], int ow, int lane) {
+__device__ __forceinline__ void prefetch_weights(const u16* __restrict__ Wg, WeightPrefetch<H>& pf, int ow, int lane) {
   using C = Chain<H>;
-  constexpr int KS = H / 16, PD = C::PD, LDA = C::LDA, MT = C::MT, NT = C::NT;
+  const u16* wfr = frag_base<H>(Wg, ow, lane);
+#pragma unroll
+  for (int q = 0; q < C::PD; ++q)
+#pragma unroll
+    for (int m = 0; m < C::MT; ++m)
+      pf.a[q][m] = *reinterpret_cast<const bf16x8*>(wfr + ((size_t)m * (H / 16) + q) * 512);
+}
+
+// acc[mt][nt] = init[mt] + sum_k Wg[feature][k] act[event][k] (see above for
+// the arrangement).  pf holds the first PD weight steps of Wg on entry and
+// those of Wnext (the next product) on exit.  Spread over the K steps, the
+// workgroup also copies the LDS tile act (the product's input) to gdst as
+// whole rows, so those HBM writes overlap the matrix work: every thread moves
+// T H / 8 / 256 = 16 pieces of 16 bytes, each read from LDS one copy slot
+// before its store.
+template <int H>
+__device__ __forceinline__ void chain_gemm(const u16* __restrict__ Wg, const u16* __restrict__ Wnext,
+                                           WeightPrefetch<H>& pf, const u16* act,
+                                           f32x16 (&acc)[Chain<H>::MT][Chain<H>::NT],
+                                           const f32x16 (&init)[Chain<H>::MT], int ow, int lane, int tid,
+                                           u16* __restrict__ gdst) {
+  using C = Chain<H>;
+  constexpr int KS = H / 16, PD = C::PD, LDA = C::LDA, MT = C::MT, NT = C::NT, T = C::T;
+  constexpr int PIECES = T * H / 8 / kChainThreads;   // copy pieces per thread
+  constexpr int CDIV = KS / PIECES;                    // K steps per copy slot
+  static_assert(PIECES * CDIV == KS, "copy schedule");
 #pragma unroll
   for (int m = 0; m < MT; ++m)
 #pragma unroll
     for (int n = 0; n < NT; ++n) acc[m][n] = init[m];
   const int lr = lane & 31, lh = lane >> 5;
-  // fragment (m, ks) of this wave: piece ((ow / 32 + m) KS + ks) 64 + lane of the fragment-ordered copy
-  const u16* wfr = Wg + ((size_t)(ow / 32) * KS * 64 + lane) * 8;
+  const u16* wfr = frag_base<H>(Wg, ow, lane);
+  const u16* wnx = frag_base<H>(Wnext, ow, lane);
   const u16* brow = act + lr * LDA + 8 * lh;
   bf16x8 a[PD + 1][MT];
-  bf16x8 b[2][NT];
+  bf16x8 b[3][NT];
 #pragma unroll
   for (int q = 0; q < PD; ++q)
 #pragma unroll
-    for (int m = 0; m < MT; ++m) a[q][m] = *reinterpret_cast<const bf16x8*>(wfr + ((size_t)m * KS + q) * 512);
+    for (int m = 0; m < MT; ++m) a[q][m] = pf.a[q][m];
 #pragma unroll
-  for (int n = 0; n < NT; ++n) b[0][n] = *reinterpret_cast<const bf16x8*>(brow + 32 * n * LDA);
+  for (int q = 0; q < 2; ++q)
+#pragma unroll
+    for (int n = 0; n < NT; ++n) b[q][n] = *reinterpret_cast<const bf16x8*>(brow + 32 * n * LDA + 16 * q);
+  uint4 cv;
+  int crow = 0, ccol = 0;
 #pragma unroll
   for (int ks = 0; ks < KS; ++ks) {
-    if (ks + PD < KS) {
 #pragma unroll
-      for (int m = 0; m < MT; ++m)
+    for (int m = 0; m < MT; ++m) {
+      if (ks + PD < KS)
         a[(ks + PD) % (PD + 1)][m] = *reinterpret_cast<const bf16x8*>(wfr + ((size_t)m * KS + ks + PD) * 512);
+      else
+        pf.a[ks + PD - KS][m] = *reinterpret_cast<const bf16x8*>(wnx + ((size_t)m * KS + ks + PD - KS) * 512);
     }
-    if (ks + 1 < KS) {
+    if (ks + 2 < KS) {
 #pragma unroll
       for (int n = 0; n < NT; ++n)
-        b[(ks + 1) & 1][n] = *reinterpret_cast<const bf16x8*>(brow + 32 * n * LDA + 16 * (ks + 1));
+        b[(ks + 2) % 3][n] = *reinterpret_cast<const bf16x8*>(brow + 32 * n * LDA + 16 * (ks + 2));
+    }
+    if (ks % CDIV == 0) {
+      if (ks > 0) *reinterpret_cast<uint4*>(gdst + (int64_t)crow * H + ccol) = cv;
+      const int k = tid + kChainThreads * (ks / CDIV);
+      crow = k / (H / 8);
+      ccol = (k % (H / 8)) * 8;
+      cv = *reinterpret_cast<const uint4*>(act + crow * LDA + ccol);
     }
     // keep the prefetches above the products of this step (the scheduler
     // would otherwise sink each load next to its first use)
@@ -282,17 +322,19 @@ __device__ __forceinline__ void chain_gemm(const u16* __restrict__ Wg, const u16
     for (int n = 0; n < NT; ++n)
 #pragma unroll
       for (int m = 0; m < MT; ++m)
-        acc[m][n] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[ks % (PD + 1)][m], b[ks & 1][n], acc[m][n], 0, 0, 0);
+        acc[m][n] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[ks % (PD + 1)][m], b[ks % 3][n], acc[m][n], 0, 0, 0);
     __builtin_amdgcn_sched_barrier(0);
   }
+  *reinterpret_cast<uint4*>(gdst + (int64_t)crow * H + ccol) = cv;
 }
 
 // LeakyReLU (slope in [0, 1]: max(v, s v)), bf16 rounding and the lane's sign
 // mask of one layer's outputs.  pk[mt][nt][g] = packed bf16 of q = 0,1 and 2,3.
 template <int MT, int NT>
 __device__ __forceinline__ void activate(const f32x16 (&v)[MT][NT], float slope, uint2 (&pk)[MT][NT][4],
-                                         uint4& mask) {
-  uint32_t m[4] = {0u, 0u, 0u, 0u};
+                                         uint32_t (&m)[MT * NT / 2]) {
+#pragma unroll
+  for (int k = 0; k < MT * NT / 2; ++k) m[k] = 0u;
 #pragma unroll
   for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
@@ -310,13 +352,25 @@ __device__ __forceinline__ void activate(const f32x16 (&v)[MT][NT], float slope,
         w = (w << 1) | (uint32_t)((int32_t)(p23 << 16) > 0);
         w = (w << 1) | (uint32_t)((int32_t)p23 >= 0x10000);
       }
-  mask = make_uint4(m[0], m[1], m[2], m[3]);
+}
+
+// A lane's mask words of one layer: store and load as one vector.
+template <int MW>
+__device__ __forceinline__ void store_mask(uint32_t* dst, const uint32_t (&m)[MW]) {
+  typename MaskWords<MW>::type v;
+  __builtin_memcpy(&v, m, sizeof(v));
+  *reinterpret_cast<typename MaskWords<MW>::type*>(dst) = v;
+}
+template <int MW>
+__device__ __forceinline__ void load_mask(const uint32_t* src, uint32_t (&m)[MW]) {
+  const typename MaskWords<MW>::type v = *reinterpret_cast<const typename MaskWords<MW>::type*>(src);
+  __builtin_memcpy(m, &v, sizeof(v));
 }
 
 // Bit of output e in a lane's mask (see activate).
-__device__ __forceinline__ bool mask_bit(const uint4& m, int e) {
-  const uint32_t w = (e >> 5) == 0 ? m.x : (e >> 5) == 1 ? m.y : (e >> 5) == 2 ? m.z : m.w;
-  return (w >> (31 - (e & 31))) & 1u;
+template <int MW>
+__device__ __forceinline__ bool mask_bit(const uint32_t (&m)[MW], int e) {
+  return (m[e >> 5] >> (31 - (e & 31))) & 1u;
 }
 
 // Writes a layer's packed outputs into the LDS tile.
@@ -348,7 +402,7 @@ struct ChainArgs {
   const float* xs;           // [rows][D] (fake chunks)
   u16* act;                  // [NH][rows][H]: A_1 .. A_NH
   u16* dlt;                  // [NH][rows][H]: unit-seed signals at A_2 .. A_{NH+1}
-  uint4* mask;               // [NH + 1][rows / T][4 waves][64 lanes]: signs of A_1 .. A_{NH+1}
+  uint32_t* mask;            // [NH + 1][rows / T][4 waves][64 lanes][MW]: signs of A_1 .. A_{NH+1}
   float* eD;                 // [rows] dL_D/dz (0 on padding)
   float* eG;                 // [rows] dL_G/dz (fake; 0 otherwise)
   float* logits;             // caller's array (indexed from c.row0) or NULL
@@ -364,9 +418,9 @@ __device__ __forceinline__ float softplus_fast(float t) { return fmaxf(t, 0.0f) 
 // logit z, BCE seeds e_D and e_G, and per-workgroup partials of dW_o, db_o
 // and the loss sums.  Stores A_1 .. A_NH and the masks for later kernels.
 template <int H, int F>
-__global__ __launch_bounds__(kChainThreads, kChainBlocksPerCU) void k_fwd_chain(ChainArgs p) {
+__global__ __launch_bounds__(kChainThreads, Chain<H>::BPC) void k_fwd_chain(ChainArgs p) {
   using C = Chain<H>;
-  constexpr int T = C::T, LDA = C::LDA, WAVES = C::WAVES, MT = C::MT, NT = C::NT;
+  constexpr int T = C::T, LDA = C::LDA, WAVES = C::WAVES, MT = C::MT, NT = C::NT, MW = C::MW;
   constexpr int NTH = kChainThreads;
   __shared__ __attribute__((aligned(16))) u16 act[T * LDA];
   __shared__ float sW0[H * (F + 1)];            // row o: W0[o][0 .. F-1], b0[o]
@@ -394,6 +448,8 @@ __global__ __launch_bounds__(kChainThreads, kChainBlocksPerCU) void k_fwd_chain(
       for (int q = 0; q < 4; ++q) dwo[mt][g][q] = 0.f;
   const float bo = p.bo[0];
   float l0 = 0.f, l1 = 0.f, se = 0.f;
+  WeightPrefetch<H> pf;
+  prefetch_weights<H>(p.Wb, pf, ow, lane);
   // this lane's features of the next tile, loaded one tile ahead
   float fnext[NT][F];
   auto load_feat = [&](int tile) __attribute__((always_inline)) {
@@ -414,7 +470,7 @@ __global__ __launch_bounds__(kChainThreads, kChainBlocksPerCU) void k_fwd_chain(
       for (int k = 0; k < F; ++k) f[nt][k] = fnext[nt][k];
     if (tile + (int)gridDim.x < ntiles) load_feat(tile + gridDim.x);
     auto mask_at = [&](int layer) __attribute__((always_inline)) {
-      return p.mask + (((int64_t)layer * ntiles + tile) * WAVES + wave) * 64 + lane;
+      return p.mask + ((((int64_t)layer * ntiles + tile) * WAVES + wave) * 64 + lane) * MW;
     };
 
     // ---- first layer (VALU, K = F) in the MFMA output arrangement ----------
@@ -439,13 +495,12 @@ __global__ __launch_bounds__(kChainThreads, kChainBlocksPerCU) void k_fwd_chain(
             }
           }
       uint2 pk[MT][NT][4];
-      uint4 m;
+      uint32_t m[MW];
       activate<MT, NT>(v, slope, pk, m);
-      *mask_at(0) = m;
+      store_mask<MW>(mask_at(0), m);
       store_tile<MT, NT, LDA>(act, pk, ow, lane);
     }
     __syncthreads();
-    copy_out<H, T, LDA, NTH>(act, p.act + (int64_t)r0 * H, tid);
 
     // ---- hidden layers -----------------------------------------------------
     for (int l = 0; l < p.NH; ++l) {
@@ -460,16 +515,18 @@ __global__ __launch_bounds__(kChainThreads, kChainBlocksPerCU) void k_fwd_chain(
           for (int q = 0; q < 4; ++q) bias[mt][4 * g + q] = b4[q];
         }
       f32x16 acc[MT][NT];
-      chain_gemm<H>(p.Wb + (size_t)l * H * H, act, acc, bias, ow, lane);
+      // the product also writes its input A_{l+1} to HBM; the next product is
+      // layer l + 1, or the first hidden layer of the next tile
+      chain_gemm<H>(p.Wb + (size_t)l * H * H, p.Wb + (size_t)(last ? 0 : l + 1) * H * H, pf, act, acc, bias, ow,
+                    lane, tid, p.act + ((int64_t)l * rstride + r0) * H);
       uint2 pk[MT][NT][4];
-      uint4 m;
+      uint32_t m[MW];
       activate<MT, NT>(acc, slope, pk, m);
-      *mask_at(l + 1) = m;
+      store_mask<MW>(mask_at(l + 1), m);
       if (!last) {
         __syncthreads();                             // every wave is done reading this layer's input
         store_tile<MT, NT, LDA>(act, pk, ow, lane);
         __syncthreads();
-        copy_out<H, T, LDA, NTH>(act, p.act + ((int64_t)(l + 1) * rstride + r0) * H, tid);
         continue;
       }
       // ---- logit layer and BCE seeds (fp32 dot over the bf16 activations) --
@@ -572,9 +629,9 @@ __global__ __launch_bounds__(kChainThreads, kChainBlocksPerCU) void k_fwd_chain(
 // layer: per-workgroup partials of dW_1 and db_1 (scaled by e_D) and, for fake
 // chunks, dL_G/dx (scaled by e_G, through the HD8 Jacobian when used).
 template <int H, int F, int D, bool kHD8>
-__global__ __launch_bounds__(kChainThreads, kChainBlocksPerCU) void k_bwd_chain(ChainArgs p) {
+__global__ __launch_bounds__(kChainThreads, Chain<H>::BPC) void k_bwd_chain(ChainArgs p) {
   using C = Chain<H>;
-  constexpr int T = C::T, LDA = C::LDA, WAVES = C::WAVES, MT = C::MT, NT = C::NT;
+  constexpr int T = C::T, LDA = C::LDA, WAVES = C::WAVES, MT = C::MT, NT = C::NT, MW = C::MW;
   constexpr int NTH = kChainThreads;
   constexpr int FPT = H / NTH;       // first-layer features per thread
   constexpr int P = NTH / T;         // threads per event in the input-gradient dot
@@ -605,11 +662,13 @@ __global__ __launch_bounds__(kChainThreads, kChainBlocksPerCU) void k_bwd_chain(
   for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
     for (int r = 0; r < 16; ++r) zero[mt][r] = 0.f;
+  WeightPrefetch<H> pf;
+  prefetch_weights<H>(p.WTb + (size_t)(NH - 1) * H * H, pf, ow, lane);
 
   for (int tile = blockIdx.x; tile < ntiles; tile += gridDim.x) {
     const int r0 = tile * T;
     auto mask_at = [&](int layer) __attribute__((always_inline)) {
-      return p.mask + (((int64_t)layer * ntiles + tile) * WAVES + wave) * 64 + lane;
+      return p.mask + ((((int64_t)layer * ntiles + tile) * WAVES + wave) * 64 + lane) * MW;
     };
     for (int k = tid; k < T; k += NTH) {
       se[k][0] = p.eD[r0 + k];
@@ -620,7 +679,8 @@ __global__ __launch_bounds__(kChainThreads, kChainBlocksPerCU) void k_bwd_chain(
       for (int k = tid; k < T * D; k += NTH) sx[k / D][k % D] = p.xs[(int64_t)r0 * D + k];
     // ---- unit-seed signal at A_{NH+1}: w_o * LeakyReLU'(A_{NH+1}) ----------
     {
-      const uint4 m = *mask_at(NH);
+      uint32_t m[MW];
+      load_mask<MW>(mask_at(NH), m);
       uint2 pk[MT][NT][4];
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt)
@@ -638,13 +698,16 @@ __global__ __launch_bounds__(kChainThreads, kChainBlocksPerCU) void k_bwd_chain(
         }
       store_tile<MT, NT, LDA>(act, pk, ow, lane);
       __syncthreads();
-      copy_out<H, T, LDA, NTH>(act, p.dlt + ((int64_t)(NH - 1) * rstride + r0) * H, tid);
     }
     // ---- hidden layers, top down ---------------------------------------------
     for (int l = NH - 1; l >= 0; --l) {
       f32x16 acc[MT][NT];
-      chain_gemm<H>(p.WTb + (size_t)l * H * H, act, acc, zero, ow, lane);
-      const uint4 m = *mask_at(l);
+      // the product also writes its input (the signal at A_{l+2}) to HBM; the
+      // next product is layer l - 1, or the top layer of the next tile
+      chain_gemm<H>(p.WTb + (size_t)l * H * H, p.WTb + (size_t)(l > 0 ? l - 1 : NH - 1) * H * H, pf, act, acc, zero,
+                    ow, lane, tid, p.dlt + ((int64_t)l * rstride + r0) * H);
+      uint32_t m[MW];
+      load_mask<MW>(mask_at(l), m);
       uint2 pk[MT][NT][4];
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt)
@@ -664,7 +727,6 @@ __global__ __launch_bounds__(kChainThreads, kChainBlocksPerCU) void k_bwd_chain(
       __syncthreads();                               // every wave is done reading this layer's input
       store_tile<MT, NT, LDA>(act, pk, ow, lane);
       __syncthreads();
-      if (l >= 1) copy_out<H, T, LDA, NTH>(act, p.dlt + ((int64_t)(l - 1) * rstride + r0) * H, tid);
     }
     // ---- first layer: act holds the signal at A_1 ---------------------------
 #pragma unroll 4
@@ -963,7 +1025,7 @@ Plan make_plan(const DiscArgs& a, int n_cu) {
   p.D = a.d;
   const int64_t biggest = std::min<int64_t>(std::max(a.n_fake, a.n_real), kChunkRows);
   p.rows_max = pad128(biggest);
-  p.blocks = std::max(1, n_cu * kChainBlocksPerCU);
+  p.blocks = std::max(1, n_cu * (p.H <= 256 ? Chain<256>::BPC : Chain<512>::BPC));
   const int tiles = (p.H / kGT) * (p.H / kGT);
   p.slices = std::max(1, 768 / tiles);   // three weight-gradient blocks per CU
   const size_t H = p.H, R = p.rows_max, NH = p.NH;
@@ -1062,7 +1124,7 @@ hipError_t launch_disc_bf16(const DiscArgs& a, void* ws, int n_cu, hipStream_t s
   ca.xs = F32(p.off_xs);
   ca.act = B16(p.off_act);
   ca.dlt = B16(p.off_dlt);
-  ca.mask = reinterpret_cast<uint4*>(base + p.off_mask);
+  ca.mask = reinterpret_cast<uint32_t*>(base + p.off_mask);
   ca.eD = F32(p.off_eD);
   ca.eG = F32(p.off_eG);
   ca.plog = F32(p.off_plog);
