@@ -41,7 +41,7 @@ typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef unsigned short u16;
 
 constexpr int kMaxNH = 4;
-constexpr int kChunkRows = 1 << 20;   // rows per chunk (fake or real), multiple of 128
+constexpr int kChunkRows = 1 << 22;   // rows per chunk (fake or real), multiple of 128
 
 // fp32 -> bf16, round to nearest even (finite inputs).
 __device__ __forceinline__ u16 bf16_bits(float f) {
@@ -78,9 +78,6 @@ __device__ __forceinline__ void store_bf16(u16* p, const float (&v)[PER]) {
 }
 
 
-__device__ __forceinline__ f32x4 mfma_bf16(bf16x8 a, bf16x8 b, f32x4 c) {
-  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
-}
 
 // ---------------------------------------------------------------------------
 // Weights: bf16 copies of one hidden layer, W ([out][in]) and W^T, in the order
@@ -256,24 +253,49 @@ __device__ __forceinline__ void prefetch_weights(const u16* __restrict__ Wg, Wei
       pf.a[q][m] = *reinterpret_cast<const bf16x8*>(wfr + ((size_t)m * (H / 16) + q) * 512);
 }
 
+typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
+
+// K-fragment order of the weight-gradient operands ([rows][H] matrices with
+// K = rows): piece (kb, cb, lane) holds column 32 cb + lane % 32, rows
+// 16 kb + 8 (lane / 32) .. + 7, at bf16 offset ((kb H / 32 + cb) 64 + lane) 8,
+// so each 32-column, 16-row block is one contiguous kilobyte: an MFMA
+// fragment of v_mfma_f32_32x32x16_bf16 with K = rows.
+//
+// One wave turns block (kb, cb) of the LDS tile into its kilobyte with two
+// ds_read_b64_tr_b16: lane j of each 16-lane group g addresses row
+// 16 kb + 8 (g / 2) + j / 4 (+ 4) and columns 32 cb + 16 (g % 2) + 4 (j % 4) .. + 3;
+// the transpose then hands lane i of the group rows +0..3 (+4..7) of column
+// 32 cb + 16 (g % 2) + i.
+template <int LDA>
+__device__ __forceinline__ bf16x8 kfrag_from_lds(const u16* act, int kb, int cb, int lane) {
+  const int g = lane >> 4, j = lane & 15;
+  const u16* p0 = act + (16 * kb + 8 * (g >> 1) + (j >> 2)) * LDA + 32 * cb + 16 * (g & 1) + 4 * (j & 3);
+  const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(p0));
+  const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(p0 + 4 * LDA));
+  return bf16x8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+}
+
 // acc[mt][nt] = init[mt] + sum_k Wg[feature][k] act[event][k] (see above for
 // the arrangement).  pf holds the first PD weight steps of Wg on entry and
 // those of Wnext (the next product) on exit.  Spread over the K steps, the
-// workgroup also copies the LDS tile act (the product's input) to gdst as
-// whole rows, so those HBM writes overlap the matrix work: every thread moves
-// T H / 8 / 256 = 16 pieces of 16 bytes, each read from LDS one copy slot
-// before its store.
-template <int H>
+// workgroup also writes the LDS tile act (the product's input) to gdst in
+// K-fragment order, so those HBM writes overlap the matrix work.  With kScale
+// the rows are scaled by rscale[2 r] and rounded to bf16 again, and the fp32
+// scaled values of each column are summed into colsum: the copy gives wave w
+// the column blocks cb = w (mod 4), block u of them (cb = w + 4 u) in
+// colsum[u], column 32 cb + lane % 32, rows of lane half lane / 32.
+template <int H, bool kScale>
 __device__ __forceinline__ void chain_gemm(const u16* __restrict__ Wg, const u16* __restrict__ Wnext,
                                            WeightPrefetch<H>& pf, const u16* act,
                                            f32x16 (&acc)[Chain<H>::MT][Chain<H>::NT],
-                                           const f32x16 (&init)[Chain<H>::MT], int ow, int lane, int tid,
-                                           u16* __restrict__ gdst) {
+                                           const f32x16 (&init)[Chain<H>::MT], int ow, int lane, int wave,
+                                           u16* __restrict__ gdst, const float* rscale,
+                                           float (&colsum)[H / 32 / Chain<H>::WAVES]) {
   using C = Chain<H>;
   constexpr int KS = H / 16, PD = C::PD, LDA = C::LDA, MT = C::MT, NT = C::NT, T = C::T;
-  constexpr int PIECES = T * H / 8 / kChainThreads;   // copy pieces per thread
-  constexpr int CDIV = KS / PIECES;                    // K steps per copy slot
-  static_assert(PIECES * CDIV == KS, "copy schedule");
+  constexpr int BLOCKS = T * H / 512 / C::WAVES;       // fragment kilobytes per wave
+  constexpr int CDIV = KS / BLOCKS;                    // K steps per copy slot
+  static_assert(BLOCKS * CDIV == KS, "copy schedule");
 #pragma unroll
   for (int m = 0; m < MT; ++m)
 #pragma unroll
@@ -292,8 +314,25 @@ __device__ __forceinline__ void chain_gemm(const u16* __restrict__ Wg, const u16
   for (int q = 0; q < 2; ++q)
 #pragma unroll
     for (int n = 0; n < NT; ++n) b[q][n] = *reinterpret_cast<const bf16x8*>(brow + 32 * n * LDA + 16 * q);
-  uint4 cv;
-  int crow = 0, ccol = 0;
+  bf16x8 cv;
+  int ckb = 0, ccb = 0;
+  auto put = [&]() __attribute__((always_inline)) {
+    uint4 w;
+    if constexpr (kScale) {
+      const int r0 = 16 * ckb + 8 * lh;
+      float v[8];
+#pragma unroll
+      for (int t = 0; t < 8; ++t) v[t] = (float)cv[t] * rscale[2 * (r0 + t)];
+      w = make_uint4(pack_bf16(v[0], v[1]), pack_bf16(v[2], v[3]), pack_bf16(v[4], v[5]), pack_bf16(v[6], v[7]));
+      const float sum = ((v[0] + v[1]) + (v[2] + v[3])) + ((v[4] + v[5]) + (v[6] + v[7]));
+#pragma unroll
+      for (int u = 0; u < H / 32 / C::WAVES; ++u)
+        if (ccb == wave + C::WAVES * u) colsum[u] += sum;
+    } else {
+      w = __builtin_bit_cast(uint4, cv);
+    }
+    *reinterpret_cast<uint4*>(gdst + (((size_t)ckb * (H / 32) + ccb) * 64 + lane) * 8) = w;
+  };
 #pragma unroll
   for (int ks = 0; ks < KS; ++ks) {
 #pragma unroll
@@ -309,11 +348,11 @@ __device__ __forceinline__ void chain_gemm(const u16* __restrict__ Wg, const u16
         b[(ks + 2) % 3][n] = *reinterpret_cast<const bf16x8*>(brow + 32 * n * LDA + 16 * (ks + 2));
     }
     if (ks % CDIV == 0) {
-      if (ks > 0) *reinterpret_cast<uint4*>(gdst + (int64_t)crow * H + ccol) = cv;
-      const int k = tid + kChainThreads * (ks / CDIV);
-      crow = k / (H / 8);
-      ccol = (k % (H / 8)) * 8;
-      cv = *reinterpret_cast<const uint4*>(act + crow * LDA + ccol);
+      if (ks > 0) put();
+      const int blk = wave + C::WAVES * (ks / CDIV);
+      ckb = blk / (H / 32);
+      ccb = blk % (H / 32);
+      cv = kfrag_from_lds<LDA>(act, ckb, ccb, lane);
     }
     // keep the prefetches above the products of this step (the scheduler
     // would otherwise sink each load next to its first use)
@@ -325,7 +364,7 @@ __device__ __forceinline__ void chain_gemm(const u16* __restrict__ Wg, const u16
         acc[m][n] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[ks % (PD + 1)][m], b[ks % 3][n], acc[m][n], 0, 0, 0);
     __builtin_amdgcn_sched_barrier(0);
   }
-  *reinterpret_cast<uint4*>(gdst + (int64_t)crow * H + ccol) = cv;
+  put();
 }
 
 // LeakyReLU (slope in [0, 1]: max(v, s v)), bf16 rounding and the lane's sign
@@ -400,8 +439,8 @@ struct ChainArgs {
   float inv_n;               // 1 / (events of this batch)
   const float* feat;         // [rows][F]
   const float* xs;           // [rows][D] (fake chunks)
-  u16* act;                  // [NH][rows][H]: A_1 .. A_NH
-  u16* dlt;                  // [NH][rows][H]: unit-seed signals at A_2 .. A_{NH+1}
+  u16* act;                  // [NH][rows H]: A_1 .. A_NH, K-fragment order
+  u16* dlt;                  // [NH][rows H]: bf16(e_D x signal at A_2 .. A_{NH+1}), K-fragment order
   uint32_t* mask;            // [NH + 1][rows / T][4 waves][64 lanes][MW]: signs of A_1 .. A_{NH+1}
   float* eD;                 // [rows] dL_D/dz (0 on padding)
   float* eG;                 // [rows] dL_G/dz (fake; 0 otherwise)
@@ -409,6 +448,7 @@ struct ChainArgs {
   float* dLg_dx;             // caller's array (indexed from c.row0) or NULL
   float* plog;               // [gridDim.x][H + 3]: dW_o, then sum softplus(+-z), sum e_D
   float* pfb;                // [gridDim.x][H F + H]: dW_1, then db_1
+  float* pdb;                // [gridDim.x][NH][H]: db of the hidden layers
 };
 
 // softplus(t) = max(t, 0) + ln(1 + e^-|t|), on the hardware units.
@@ -517,8 +557,9 @@ __global__ __launch_bounds__(kChainThreads, Chain<H>::BPC) void k_fwd_chain(Chai
       f32x16 acc[MT][NT];
       // the product also writes its input A_{l+1} to HBM; the next product is
       // layer l + 1, or the first hidden layer of the next tile
-      chain_gemm<H>(p.Wb + (size_t)l * H * H, p.Wb + (size_t)(last ? 0 : l + 1) * H * H, pf, act, acc, bias, ow,
-                    lane, tid, p.act + ((int64_t)l * rstride + r0) * H);
+      float unused[H / 32 / WAVES];
+      chain_gemm<H, false>(p.Wb + (size_t)l * H * H, p.Wb + (size_t)(last ? 0 : l + 1) * H * H, pf, act, acc, bias,
+                           ow, lane, wave, p.act + ((int64_t)l * rstride + r0) * H, nullptr, unused);
       uint2 pk[MT][NT][4];
       uint32_t m[MW];
       activate<MT, NT>(acc, slope, pk, m);
@@ -654,6 +695,12 @@ __global__ __launch_bounds__(kChainThreads, Chain<H>::BPC) void k_bwd_chain(Chai
   for (int u = 0; u < FPT; ++u)
 #pragma unroll
     for (int k = 0; k <= F; ++k) adw[u][k] = 0.f;
+  constexpr int CBW = H / 32 / WAVES;     // column blocks of the copy per wave
+  float adb[kMaxNH][CBW];                 // db partials: column 32 (wave + 4 u) + lane % 32, lane-half rows
+#pragma unroll
+  for (int k = 0; k < kMaxNH; ++k)
+#pragma unroll
+    for (int u = 0; u < CBW; ++u) adb[k][u] = 0.f;
   const bool want_dx = c.fake && p.dLg_dx != nullptr;
   const float slope = p.slope;
   const int NH = p.NH;
@@ -704,8 +751,19 @@ __global__ __launch_bounds__(kChainThreads, Chain<H>::BPC) void k_bwd_chain(Chai
       f32x16 acc[MT][NT];
       // the product also writes its input (the signal at A_{l+2}) to HBM; the
       // next product is layer l - 1, or the top layer of the next tile
-      chain_gemm<H>(p.WTb + (size_t)l * H * H, p.WTb + (size_t)(l > 0 ? l - 1 : NH - 1) * H * H, pf, act, acc, zero,
-                    ow, lane, tid, p.dlt + ((int64_t)l * rstride + r0) * H);
+      // the copy of this product's input (the signal at A_{l+2}) also sums
+      // e_D times it per column: db of hidden layer l
+      float colsum[CBW];
+#pragma unroll
+      for (int u = 0; u < CBW; ++u) colsum[u] = 0.f;
+      chain_gemm<H, true>(p.WTb + (size_t)l * H * H, p.WTb + (size_t)(l > 0 ? l - 1 : NH - 1) * H * H, pf, act, acc,
+                          zero, ow, lane, wave, p.dlt + ((int64_t)l * rstride + r0) * H, &se[0][0], colsum);
+#pragma unroll
+      for (int k = 0; k < kMaxNH; ++k)
+        if (k == l) {
+#pragma unroll
+          for (int u = 0; u < CBW; ++u) adb[k][u] += colsum[u];
+        }
       uint32_t m[MW];
       load_mask<MW>(mask_at(l), m);
       uint2 pk[MT][NT][4];
@@ -787,8 +845,9 @@ __global__ __launch_bounds__(kChainThreads, Chain<H>::BPC) void k_bwd_chain(Chai
     __syncthreads();                                 // before the next tile overwrites act and the staged rows
   }
 
-  // ---- per-workgroup partials of dW_1 and db_1 ------------------------------
+  // ---- per-workgroup partials of dW_1, db_1 and the hidden db --------------
   float* dst = p.pfb + (int64_t)blockIdx.x * (H * F + H);
+  float* dbd = p.pdb + (int64_t)blockIdx.x * NH * H;
 #pragma unroll
   for (int u = 0; u < FPT; ++u) {
     const int o = tid + NTH * u;
@@ -796,141 +855,87 @@ __global__ __launch_bounds__(kChainThreads, Chain<H>::BPC) void k_bwd_chain(Chai
     for (int j = 0; j < F; ++j) dst[o * F + j] = adw[u][j];
     dst[H * F + o] = adw[u][F];
   }
+#pragma unroll
+  for (int k = 0; k < kMaxNH; ++k)
+#pragma unroll
+    for (int u = 0; u < CBW; ++u) {
+      const float v = adb[k][u] + __shfl_xor(adb[k][u], 32, 64);   // both row halves of the column
+      if (k < NH && lane < 32) dbd[k * H + 32 * (wave + WAVES * u) + lane] = v;
+    }
 }
-
-constexpr int kGT = 128;            // weight-gradient tile edge
 
 // ---------------------------------------------------------------------------
-// Weight-gradient partial of one layer over a slice of rows:
-//   P[o][i] = sum_r bf16(e_D[r] * delta[r][o]) * A[r][i],  db part = sum_r e_D[r] * delta[r][o]
-// 128 (o) x 128 (i) tile per block; rows in steps of 32, staged through LDS
-// event-major and read back transposed.
-constexpr int kWK = 32;           // rows per step
-constexpr int kWLD = kGT + 8;     // LDS row stride (bf16) of a staged [32][128] tile
+// Weight-gradient partial of one hidden layer over a slice of rows:
+//   P[slice][o][i] = sum_rows bf16(e_D delta)[r][o] A[r][i]
+// for one 256 x 256 tile (o0, i0) of the H x H gradient.  Both operands come
+// in K-fragment order, so every fragment is a contiguous kilobyte read from
+// global memory and no LDS is needed; the kernel streams each operand row of
+// its tile once and is bound by HBM.  Wave w owns rows o0 + 64 w .. + 63 (two
+// 32-row MFMA tiles) and all 256 columns (eight), i.e. 16 accumulators of
+// 32 x 32 in the accumulation registers; fragments are loaded PD K steps
+// ahead, with the step loop unrolled by PD + 1 so that every register slot
+// index is a constant.
+constexpr int kWT = 256;     // weight-gradient tile edge
 
-typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
-
-__device__ __forceinline__ bf16x8 tr_fragment(const u16* tile, int row0, int col0, int lane) {
-  // lane (g = lane/16, j = lane%16) points at row row0 + 8g + j/4 (+4), columns col0 + 4 (j%4) .. +3;
-  // the transpose load then gives lane i of each 16-lane group rows 8g..8g+7 of column col0 + i.
-  const int g = lane >> 4, j = lane & 15;
-  const u16* p0 = tile + (row0 + 8 * g + (j >> 2)) * kWLD + col0 + 4 * (j & 3);
-  const u16* p1 = p0 + 4 * kWLD;
-  const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(p0));
-  const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(p1));
-  return bf16x8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
-}
-
-// Global loads run two steps ahead of their LDS writes (two register sets),
-// so a step's HBM latency is covered by the matrix work of the two before it.
-__global__ __launch_bounds__(256, 2) void k_wgrad(const u16* __restrict__ dlt, const u16* __restrict__ A,
-                                               const float* __restrict__ eD, int H, int rows_per_slice,
-                                               int rows, float* __restrict__ P /*[slices][H][H]*/,
-                                               float* __restrict__ Pdb /*[slices][H]*/) {
-  __shared__ __attribute__((aligned(16))) u16 sD[2][kWK * kWLD];
-  __shared__ __attribute__((aligned(16))) u16 sA[2][kWK * kWLD];
-  __shared__ float sdb[256][8];
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int tiles = H / kGT;
-  const int o0 = (blockIdx.x / tiles) * kGT, i0 = (blockIdx.x % tiles) * kGT;
-  const int slice = blockIdx.y;
-  const int rbeg = slice * rows_per_slice;
-  const int rend = min(rows, rbeg + rows_per_slice);
-  const int wo = (wave >> 1) * 64, wi = (wave & 1) * 64;
-  const bool do_db = (i0 == 0);
-
-  // staging map: 32 rows x 128 cols = 512 pieces of 8 bf16, 2 per thread (same columns every step)
-  const int srow = tid >> 4, scol = (tid & 15) * 8;   // piece p: row srow + 16 p
-  float db[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-  struct Regs { uint4 d0, d1, a0, a1; float e0, e1; };
-  auto load = [&](Regs& R, int r0) __attribute__((always_inline)) {
-    const int64_t ra = r0 + srow, rb = ra + 16;
-    R.e0 = eD[ra];
-    R.e1 = eD[rb];
-    R.d0 = *reinterpret_cast<const uint4*>(dlt + ra * H + o0 + scol);
-    R.d1 = *reinterpret_cast<const uint4*>(dlt + rb * H + o0 + scol);
-    R.a0 = *reinterpret_cast<const uint4*>(A + ra * H + i0 + scol);
-    R.a1 = *reinterpret_cast<const uint4*>(A + rb * H + i0 + scol);
+template <int H>
+__global__ __launch_bounds__(256, 1) void k_wgrad(const u16* __restrict__ dsc, const u16* __restrict__ A,
+                                                  int kb_per_slice, int kb_total, float* __restrict__ P) {
+  constexpr int TI = H / kWT;     // tiles per dimension
+  constexpr int CB = H / 32;      // 32-column blocks
+  constexpr int PD = 3;
+  const int tile = blockIdx.x % (TI * TI), slice = blockIdx.x / (TI * TI);
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int ob = (tile / TI) * (kWT / 32) + 2 * wave;   // the wave's first 32-row block
+  const int ib = (tile % TI) * (kWT / 32);              // the tile's first 32-column block
+  const int kb0 = slice * kb_per_slice;
+  const int nk = max(0, min(kb_total, kb0 + kb_per_slice) - kb0);
+  const u16* pa = dsc + (((size_t)kb0 * CB + ob) * 64 + lane) * 8;
+  const u16* pb = A + (((size_t)kb0 * CB + ib) * 64 + lane) * 8;
+  constexpr size_t KSTRIDE = (size_t)CB * 512;          // bf16 per K block
+  f32x16 acc[2][8];
+#pragma unroll
+  for (int m = 0; m < 2; ++m)
+#pragma unroll
+    for (int n = 0; n < 8; ++n)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[m][n][r] = 0.f;
+  bf16x8 fa[PD + 1][2], fb[PD + 1][8];
+  auto load = [&](int slot, int k) __attribute__((always_inline)) {
+#pragma unroll
+    for (int m = 0; m < 2; ++m) fa[slot][m] = *reinterpret_cast<const bf16x8*>(pa + k * KSTRIDE + m * 512);
+#pragma unroll
+    for (int n = 0; n < 8; ++n) fb[slot][n] = *reinterpret_cast<const bf16x8*>(pb + k * KSTRIDE + n * 512);
   };
-  auto write = [&](const Regs& R, int buf) __attribute__((always_inline)) {
 #pragma unroll
-    for (int p = 0; p < 2; ++p) {
-      const int row = srow + 16 * p;
-      const uint4 dv = p ? R.d1 : R.d0;
-      const float ev = p ? R.e1 : R.e0;
-      const uint32_t w[4] = {dv.x, dv.y, dv.z, dv.w};
-      uint32_t o[4];
+  for (int q = 0; q < PD; ++q)
+    if (q < nk) load(q, q);
+  for (int k0 = 0; k0 < nk; k0 += PD + 1) {
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const float a0 = ev * __uint_as_float(w[q] << 16);
-        const float a1 = ev * __uint_as_float(w[q] & 0xffff0000u);
-        db[2 * q] += a0;
-        db[2 * q + 1] += a1;
-        o[q] = (uint32_t)bf16_bits(a0) | ((uint32_t)bf16_bits(a1) << 16);
+    for (int q = 0; q <= PD; ++q) {
+      const int k = k0 + q;
+      if (k < nk) {
+        if (k + PD < nk) load((q + PD) % (PD + 1), k + PD);
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int n = 0; n < 8; ++n)
+#pragma unroll
+          for (int m = 0; m < 2; ++m)
+            acc[m][n] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[q][m], fb[q][n], acc[m][n], 0, 0, 0);
+        __builtin_amdgcn_sched_barrier(0);
       }
-      *reinterpret_cast<uint4*>(&sD[buf][row * kWLD + scol]) = make_uint4(o[0], o[1], o[2], o[3]);
-      *reinterpret_cast<uint4*>(&sA[buf][row * kWLD + scol]) = p ? R.a1 : R.a0;
-    }
-  };
-
-  f32x4 acc[4][4];
-#pragma unroll
-  for (int i = 0; i < 4; ++i)
-#pragma unroll
-    for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-  auto compute = [&](int buf) __attribute__((always_inline)) {
-    bf16x8 a[4], b[4];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) a[i] = tr_fragment(sD[buf], 0, wo + 16 * i, lane);
-#pragma unroll
-    for (int j = 0; j < 4; ++j) b[j] = tr_fragment(sA[buf], 0, wi + 16 * j, lane);
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-      for (int j = 0; j < 4; ++j) acc[i][j] = mfma_bf16(a[i], b[j], acc[i][j]);
-  };
-  const int nsteps = (rend - rbeg) / kWK;   // rows are multiples of 128, slices multiples of 32
-  // invariant at the top of step s (parity ph): R[ph ^ 1] holds step s+1, R[ph] holds step s+2
-  Regs R[2];
-  if (nsteps > 0) load(R[0], rbeg);
-  if (nsteps > 1) load(R[1], rbeg + kWK);
-  if (nsteps > 0) write(R[0], 0);
-  if (nsteps > 2) load(R[0], rbeg + 2 * kWK);
-  __syncthreads();
-  for (int s0 = 0; s0 < nsteps; s0 += 2) {
-#pragma unroll
-    for (int ph = 0; ph < 2; ++ph) {
-      const int s = s0 + ph;
-      if (s < nsteps) {
-        compute(ph);
-        if (s + 1 < nsteps) write(R[ph ^ 1], ph ^ 1);
-        if (s + 3 < nsteps) load(R[ph ^ 1], rbeg + (s + 3) * kWK);
-      }
-      __syncthreads();
     }
   }
-  float* out = P + (int64_t)slice * H * H;
+  float* out = P + (size_t)slice * H * H;
+  const int lr = lane & 31, lh = lane >> 5;
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int m = 0; m < 2; ++m)
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
+    for (int n = 0; n < 8; ++n)
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const int o = o0 + wo + 16 * i + 4 * (lane >> 4) + q, ii = i0 + wi + 16 * j + (lane & 15);
-        out[(int64_t)o * H + ii] = acc[i][j][q];
+      for (int r = 0; r < 16; ++r) {
+        const int o = (ob + m) * 32 + 8 * (r / 4) + 4 * lh + (r % 4), i = (ib + n) * 32 + lr;
+        out[(size_t)o * H + i] = acc[m][n][r];
       }
-  if (do_db) {
-#pragma unroll
-    for (int q = 0; q < 8; ++q) sdb[tid][q] = db[q];
-    __syncthreads();
-    if (tid < kGT) {
-      // threads t with equal t & 15 stage the same 8 columns 8 (t & 15) .. + 7
-      const int piece = tid >> 3, q = tid & 7;   // column = 8 * piece + q
-      float sum = 0.f;
-      for (int t = piece; t < 256; t += 16) sum += sdb[t][q];
-      Pdb[(int64_t)slice * H + o0 + 8 * piece + q] = sum;
-    }
-  }
 }
 
 // acc[e] (+)= sum_k part[k][e], k = 0..n-1, in a fixed order (S contiguous
@@ -1026,8 +1031,8 @@ Plan make_plan(const DiscArgs& a, int n_cu) {
   const int64_t biggest = std::min<int64_t>(std::max(a.n_fake, a.n_real), kChunkRows);
   p.rows_max = pad128(biggest);
   p.blocks = std::max(1, n_cu * (p.H <= 256 ? Chain<256>::BPC : Chain<512>::BPC));
-  const int tiles = (p.H / kGT) * (p.H / kGT);
-  p.slices = std::max(1, 768 / tiles);   // three weight-gradient blocks per CU
+  const int tiles = (p.H / kWT) * (p.H / kWT);
+  p.slices = std::max(1, n_cu / tiles);  // one weight-gradient workgroup per CU
   const size_t H = p.H, R = p.rows_max, NH = p.NH;
   size_t o = 0;
   p.off_wb = o; o += al(2 * H * H * NH);
@@ -1042,7 +1047,7 @@ Plan make_plan(const DiscArgs& a, int n_cu) {
   p.off_plog = o; o += al(4 * (size_t)p.blocks * (H + 3));
   p.off_pfb = o; o += al(4 * (size_t)p.blocks * (H * p.F + H));
   p.off_pw = o; o += al(4 * (size_t)p.slices * H * H);
-  p.off_pdb = o; o += al(4 * (size_t)p.slices * H);
+  p.off_pdb = o; o += al(4 * (size_t)p.blocks * NH * H);
   p.off_accl = o; o += al(4 * 4);
   p.total = o;
   return p;
@@ -1129,6 +1134,7 @@ hipError_t launch_disc_bf16(const DiscArgs& a, void* ws, int n_cu, hipStream_t s
   ca.eG = F32(p.off_eG);
   ca.plog = F32(p.off_plog);
   ca.pfb = F32(p.off_pfb);
+  ca.pdb = F32(p.off_pdb);
 
   int chunk_index = 0;
   float* lacc = F32(p.off_accl);
@@ -1168,17 +1174,22 @@ hipError_t launch_disc_bf16(const DiscArgs& a, void* ws, int n_cu, hipStream_t s
       if (want_grads) {
         accumulate(ca.pfb, nb, (int64_t)(H * p.F + H), (int64_t)(H * p.F), out.dW[0], first, st);
         accumulate(ca.pfb + (size_t)H * p.F, nb, (int64_t)(H * p.F + H), (int64_t)H, out.db[0], first, st);
-        const int tiles = (H / kGT) * (H / kGT);
-        const int rows_per_slice = ((c.rows / p.slices + kWK - 1) / kWK) * kWK;
+        const int tiles = (H / kWT) * (H / kWT);
+        const int kb_total = c.rows / 16;                           // 16-row K blocks of the chunk
+        const int kb_per_slice = (kb_total + p.slices - 1) / p.slices;
         const size_t bst = (size_t)c.rows * H;   // stride between this chunk's per-layer buffers
         for (int l = 0; l < NH; ++l) {
           // hidden layer l maps A_{l+1} -> A_{l+2}: operands A_{l+1} and the signal at A_{l+2}
+          accumulate(ca.pdb + (size_t)l * H, nb, (int64_t)NH * H, (int64_t)H, out.db[1 + l], first, st);
           if (tm) tm->begin("bf16_wgrad");
-          hipLaunchKernelGGL(k_wgrad, dim3(tiles, p.slices), dim3(256), 0, st, ca.dlt + l * bst, ca.act + l * bst,
-                             ca.eD, H, rows_per_slice, c.rows, F32(p.off_pw), F32(p.off_pdb));
+          if (H == 256)
+            hipLaunchKernelGGL(k_wgrad<256>, dim3(tiles * p.slices), dim3(256), 0, st, ca.dlt + l * bst,
+                               ca.act + l * bst, kb_per_slice, kb_total, F32(p.off_pw));
+          else
+            hipLaunchKernelGGL(k_wgrad<512>, dim3(tiles * p.slices), dim3(256), 0, st, ca.dlt + l * bst,
+                               ca.act + l * bst, kb_per_slice, kb_total, F32(p.off_pw));
           if (tm) tm->end();
           accumulate(F32(p.off_pw), p.slices, (int64_t)H * H, (int64_t)H * H, out.dW[1 + l], first, st);
-          accumulate(F32(p.off_pdb), p.slices, (int64_t)H, (int64_t)H, out.db[1 + l], first, st);
         }
       }
       hipError_t e = hipGetLastError();
