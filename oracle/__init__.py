@@ -22,10 +22,14 @@ Parity status per function (what pins it, see tests/test_oracle_*.py):
   mlp forward/back   pinned: finite differences, torch float64 autograd,
                      zero-last-layer and logistic-regression special cases.
   bce                pinned: closed values at z=0, derivative identity.
-  bf16 emulation     pinned: RNE rounding against torch's bfloat16 cast.
+  bf16 emulation     pinned: RNE rounding against torch's bfloat16 cast;
+                     the bf16 discriminator against torch autograd with
+                     straight-through rounding at the same points.
+  kink variants      pinned: torch autograd where no unit is near the kink,
+                     one-sided finite differences at an exact kink.
 """
 from .philox import philox4x32_10, event_words  # noqa: F401
 from .sampler import (uniform_from_words, kumaraswamy_icdf, kumaraswamy_cdf,  # noqa: F401
                       pathwise, sample, features_hd8, features_hd8_jacobian)
-from .mlp import mlp_forward, bce_losses, disc_fwd_bwd, round_bf16  # noqa: F401
+from .mlp import mlp_forward, bce_losses, disc_fwd_bwd, round_bf16, input_grad_kink_variants  # noqa: F401
 from .step import param_grad, quadratic_critic, run_step  # noqa: F401

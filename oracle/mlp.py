@@ -80,6 +80,41 @@ def kink_margin(W, b, hs, pres):
     return m
 
 
+def input_grad_kink_variants(W, b, x, slope=0.2, margin=1e-5, max_units=6):
+    """dz/dx of one event for every admissible choice of LeakyReLU slopes.
+
+    Units whose pre-activation lies within `margin` of the kink (relative, as in
+    kink_margin) may take either one-sided derivative, 1 or `slope`, in a
+    computation with rounding errors; all other units follow the sign of their
+    float64 pre-activation.  Returns an array [2^k][F] for the k (at most
+    max_units, the closest ones) near-kink units: a computed input gradient of
+    this event is correct if it matches one of the rows.  With k = 0 the single
+    row is the plain float64 gradient."""
+    n = len(W)
+    W = [np.asarray(w, dtype=np.float64) for w in W]
+    b = [np.asarray(v, dtype=np.float64) for v in b]
+    h = np.asarray(x, dtype=np.float64)
+    pres, rel = [], []
+    for l in range(n - 1):
+        pre = W[l] @ h + b[l]
+        scale = np.abs(W[l]) @ np.abs(h) + np.abs(b[l])
+        pres.append(pre)
+        rel.append(np.abs(pre) / np.maximum(scale, 1e-300))
+        h = _leaky(pre, slope)
+    near = [(rel[l][o], l, o) for l in range(n - 1) for o in np.flatnonzero(rel[l] <= margin)]
+    near = [(l, o) for _, l, o in sorted(near)[:max_units]]
+    out = []
+    for choice in range(1 << len(near)):
+        grads = [_leaky_grad(p, slope) for p in pres]
+        for bit, (l, o) in enumerate(near):
+            grads[l][o] = 1.0 if (choice >> bit) & 1 else slope
+        d = W[n - 1][0].copy()                    # dz/dh_{n-1}
+        for l in range(n - 2, -1, -1):
+            d = (d * grads[l]) @ W[l]             # dz/dh_l (h_0 = x)
+        out.append(d)
+    return np.array(out)
+
+
 def mlp_forward(W, b, h0, slope=0.2, bf16=False):
     """Returns (z[N], pres, hs) where hs[0] is the input and hs[l+1] = act(pres[l])."""
     n = len(W)

@@ -30,7 +30,26 @@ def _oracle(inp, w, real_np):
     return oracle.run_step(inp["theta"], w.events_per_theta, w.fake_seed, inp["W"], inp["b"], real_np)
 
 
-def _check(o, ref, n_layers, fused=True):
+def _check_near_kinks(gx, ref, W, b, idx):
+    """Events within KINK of a LeakyReLU kink: the computed dL_G/dx must equal
+    e_G dz/dx for one admissible choice of one-sided slopes at the near-kink
+    units (several results are correct there; the oracle enumerates them).
+    Returns the worst error and the oracle's dL_G/dx with those events set to
+    the admissible variant the computation took."""
+    eG = -oracle.mlp.sigmoid(-ref["logits_fake"]) / ref["logits_fake"].shape[0]
+    worst = 0.0
+    matched = ref["dL_dx"].copy()
+    for i in idx:
+        v = eG[i] * oracle.input_grad_kink_variants(W, b, ref["x"][i], margin=KINK)
+        errs = np.abs(v - gx[i]).max(axis=1) / np.abs(v).max()
+        k = int(np.argmin(errs))
+        worst = max(worst, errs[k])
+        assert errs[k] <= TOL, (i, errs[k], gx[i], v)
+        matched[i] = v[k]
+    return worst, matched
+
+
+def _check(o, ref, n_layers, fused=True, W=None, b=None, n_theta=None, E=None):
     assert_normwise(to_np(o["logits_fake"]), ref["logits_fake"], TOL, "logits_fake")
     assert_normwise(to_np(o["logits_real"]), ref["logits_real"], TOL, "logits_real")
     assert abs(o["loss_d"].item() - ref["loss_d"]) <= TOL * abs(ref["loss_d"])
@@ -48,12 +67,16 @@ def _check(o, ref, n_layers, fused=True):
           f"worst elementwise rel err there {err[~keep].max() if (~keep).any() else 0:.2e}, "
           f"elsewhere {err[keep].max():.2e}", flush=True)
     assert np.count_nonzero(~keep) <= max(3, 0.05 * keep.size)
-    if (~keep).any():            # a flipped branch changes one unit's slope: bounded, not arbitrary
-        assert err[~keep].max() < 1.0
+    dtheta_ref = ref["dL_dtheta"]
+    if (~keep).any() and W is not None:
+        worst, matched = _check_near_kinks(gx, ref, W, b, np.flatnonzero(~keep))
+        print(f"  near-kink events match an admissible slope choice: worst rel err {worst:.2e}", flush=True)
+        # the per-parameter sums of the slope choices the computation took
+        dtheta_ref, _ = oracle.param_grad(matched, ref["dxda"], ref["dxdb"], n_theta, E)
     assert_normwise(gx[keep], ref["dL_dx"][keep], TOL, "dLg_dx (away from kinks)")
     if fused:
-        assert_normwise(to_np(o["dLg_dtheta"]), ref["dL_dtheta"], TOL, "dLg_dtheta")
-        assert_condition_aware(to_np(o["dLg_dtheta"]), ref["dL_dtheta"], ref["dL_dtheta_cond"], TOL, "dLg_dtheta")
+        assert_normwise(to_np(o["dLg_dtheta"]), dtheta_ref, TOL, "dLg_dtheta")
+        assert_condition_aware(to_np(o["dLg_dtheta"]), dtheta_ref, ref["dL_dtheta_cond"], TOL, "dLg_dtheta")
 
 
 @pytest.mark.parametrize("name,n_theta,E", [
@@ -71,7 +94,7 @@ def test_fused_source_path(gpu_ctx, name, n_theta, E):
     torch.cuda.synchronize()
     real_np = oracle.sample(inp["theta_star"], n_real, w.real_seed)
     ref = _oracle(inp, w, real_np)
-    _check(o, ref, len(W))
+    _check(o, ref, len(W), W=inp["W"], b=inp["b"], n_theta=w.n_theta, E=w.events_per_theta)
 
 
 def test_three_call_path_matches_fused(gpu_ctx):
@@ -103,7 +126,7 @@ def test_ragged_sizes(gpu_ctx, n_theta, E, n_real):
     o = gpu_ctx.disc_fwd_bwd(W, b, real, fake_source=dict(theta=th, events_per_theta=E, seed=w.fake_seed))
     torch.cuda.synchronize()
     real_np = oracle.sample(inp["theta_star"], n_real, w.real_seed)
-    _check(o, _oracle(inp, w, real_np), len(W))
+    _check(o, _oracle(inp, w, real_np), len(W), W=inp["W"], b=inp["b"], n_theta=w.n_theta, E=w.events_per_theta)
 
 
 def test_deterministic_repeat(gpu_ctx):

@@ -147,3 +147,50 @@ def test_bf16_mode_structure_reduces_to_fp64():
     for l in range(len(W)):
         np.testing.assert_allclose(q["dW"][l], r["dW"][l], rtol=1e-11, atol=1e-15)
         np.testing.assert_allclose(q["db"][l], r["db"][l], rtol=1e-11, atol=1e-15)
+
+
+def test_kink_variants_without_kinks_is_the_gradient():
+    """No unit near the kink: a single variant, equal to torch float64 autograd dz/dx."""
+    from oracle.mlp import input_grad_kink_variants
+    W, b = _net((3, 9, 7, 5, 1), 21)
+    x = np.random.default_rng(22).uniform(0.05, 0.95, 3)
+    v = input_grad_kink_variants(W, b, x, margin=1e-12)
+    assert v.shape == (1, 3)
+    xt = torch.tensor(x, requires_grad=True)
+    h = xt
+    for l in range(len(W)):
+        h = h @ torch.tensor(W[l]).T + torch.tensor(b[l])
+        if l < len(W) - 1:
+            h = torch.nn.functional.leaky_relu(h, 0.2)
+    h.sum().backward()
+    np.testing.assert_allclose(v[0], xt.grad.numpy(), rtol=1e-13, atol=1e-15)
+
+
+def test_kink_variants_are_the_one_sided_derivatives():
+    """A unit placed exactly on the kink: the two variants are the directional
+    derivatives of z from either side (one-sided finite differences)."""
+    from oracle.mlp import input_grad_kink_variants
+    W, b = _net((2, 6, 6, 1), 23)
+    x = np.array([0.37, 0.61])
+    o = 2
+    b[0] = b[0].copy()
+    b[0][o] = -W[0][o] @ x                      # pre-activation of unit o of layer 1 is 0
+    v = input_grad_kink_variants(W, b, x, margin=1e-9)
+    assert v.shape == (2, 2)
+
+    def z(xx):
+        h = xx
+        for l in range(len(W)):
+            h = W[l] @ h + b[l]
+            if l < len(W) - 1:
+                h = np.where(h > 0, h, 0.2 * h)
+        return h[0]
+
+    d = W[0][o] / np.linalg.norm(W[0][o])      # moves unit o's pre-activation up
+    eps = 1e-7
+    right = (z(x + eps * d) - z(x)) / eps       # slope 1 side
+    left = (z(x) - z(x - eps * d)) / eps        # slope 0.2 side
+    got = sorted([float(v[0] @ d), float(v[1] @ d)])
+    want = sorted([right, left])
+    assert abs(right - left) > 1e-3             # the kink is visible
+    np.testing.assert_allclose(got, want, rtol=1e-6, atol=1e-9)
