@@ -169,20 +169,26 @@ __global__ __launch_bounds__(256) void k_prep(ChunkArgs c, const float* __restri
 }
 
 // ---------------------------------------------------------------------------
-// Per-tile layer chains.  Persistent workgroups of 4 waves (BPC per CU: two
-// for H = 256, so that one workgroup's VALU epilogues and barriers overlap the
-// other's matrix products; one for H = 512, where a wave then has the whole
-// register file of its SIMD) loop over tiles of T = 64 event rows; the tile's activations (forward) or unit-seed
-// signals (backward) live in LDS as [T][H + 8] bf16 and are overwritten layer
-// by layer, so between layers nothing goes through HBM except what the
-// weight-gradient products need later.  Wave w owns output features
-// [32 MT w, 32 MT (w + 1)) of every product outT = W' inT for all T events,
-// as MT x NT 32x32 tiles of v_mfma_f32_32x32x16_bf16 (the 32x32 shape keeps
-// the matrix core busy from a single wave per SIMD; the 16x16 one does not).
-// Each K step of 16 takes MT 16-byte weight loads (global, L2-resident, from
-// the fragment-ordered copies, issued PD steps ahead) and NT 16-byte LDS reads (one step ahead) for MT NT
-// products.  The 16-byte row pad makes each 8-lane group of an LDS fragment
-// read hit distinct banks.
+// Per-tile layer chains.  Persistent workgroups of H / 64 waves (eight waves
+// per CU: two workgroups for H = 256, so that one workgroup's VALU epilogues
+// and barriers overlap the other's matrix products; one for H = 512) loop
+// over tiles of T = 128 event rows; the tile's activations (forward) or
+// unit-seed signals (backward) live in LDS as [T][H + 8] bf16 and are
+// overwritten layer by layer, so between layers nothing goes through HBM
+// except what the weight-gradient products need later.  Wave w owns output
+// features [64 w, 64 w + 64) of every product outT = W' inT for all T events,
+// as 2 x 4 tiles of v_mfma_f32_32x32x16_bf16: each 16-byte weight fragment
+// feeds four products and each 16-byte LDS fragment two, so that with the
+// matrix cores at full rate a CU's weight loads and LDS reads stay near half
+// of what its L1 and LDS can deliver.  Each K step of 16 takes two weight
+// loads (L2-resident fragment-ordered copies, issued PD steps ahead) and four
+// LDS reads (one step ahead).  The 16-byte row pad makes each 8-lane group of
+// an LDS fragment read hit distinct banks.
+//
+// Global streams inside the products (weights, the HBM copies) go through
+// buffer resources: one per-lane offset register per stream, every per-step
+// offset a scalar constant.  That keeps the 128 accumulators and the rings
+// within the 256 registers a wave has at two waves per SIMD.
 //
 // Lane l holds, in register 4 g + q of tile (mt, nt), the output of feature
 // ow + 32 mt + 8 g + 4 (l / 32) + q for event 32 nt + (l % 32): each group g
@@ -190,32 +196,33 @@ __global__ __launch_bounds__(256) void k_prep(ChunkArgs c, const float* __restri
 // forward's first layer (K = F, VALU) produces its outputs in the same
 // arrangement.
 //
-// Signs of the hidden activations are kept as lane-local bit masks: the 16 MT
-// NT outputs a lane holds in one layer are numbered e = 16 (mt NT + nt) + 4 g
-// + q and bit 31 - e % 32 of word e / 32 is set where the bf16 activation is
-// > 0; each lane stores its MW words as one vector, [layer][tile][wave][lane].
-// The backward chain has the same lane arrangement and reads them back, so
+// Signs of the hidden activations are kept as lane-local bit masks: the 32
+// outputs a lane holds in one layer are numbered e = 16 (mt NT + nt) + 4 g + q
+// and bit 31 - e % 32 of word e / 32 is set where the bf16 activation is > 0;
+// each lane stores its 4 words as one vector, [layer][tile][wave][lane].  The
+// backward chain has the same lane arrangement and reads them back, so
 // LeakyReLU' costs one bit per output instead of re-reading the activations.
-constexpr int kChainThreads = 256;
 
 typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef __amdgpu_buffer_rsrc_t Rsrc;
 
 template <int H>
 struct Chain {
-  static constexpr int WAVES = kChainThreads / 64;
-  static constexpr int MT = H / (32 * WAVES);   // 32-feature MFMA tiles per wave
-  static constexpr int NT = 2;                  // 32-event MFMA tiles per wave
+  static constexpr int MT = 2;                  // 32-feature MFMA tiles per wave
+  static constexpr int NT = 4;                  // 32-event MFMA tiles per wave
+  static constexpr int WAVES = H / (32 * MT);   // waves per workgroup
+  static constexpr int THREADS = 64 * WAVES;    // = H
   static constexpr int T = 32 * NT;             // events per tile
   static constexpr int LDA = H + 8;             // LDS row stride (bf16)
-  static constexpr int PD = 3;                  // weight prefetch distance (K steps of 16)
-  static constexpr int MW = MT * NT / 2;        // mask words per lane and layer (2 or 4)
-  static constexpr int BPC = H <= 256 ? 2 : 1;  // workgroups per CU
-  static_assert((MT == 2 || MT == 4) && (T * H / 8) % kChainThreads == 0, "chain decomposition");
+  static constexpr int KS = H / 16;             // K steps per product
+  static constexpr int PD = 2;                  // weight prefetch distance (K steps)
+  static constexpr int MW = MT * NT / 2;        // mask words per lane and layer
+  static constexpr int BPC = 512 / H;           // workgroups per CU
+  static constexpr int COPIES = T * H / 512 / WAVES;   // copy kilobytes per wave and product
+  static constexpr int CDIV = KS / COPIES;             // K steps per copy kilobyte
+  static_assert(MW == 4 && COPIES == 16 && CDIV * COPIES == KS && THREADS == H, "chain decomposition");
 };
-
-template <int N> struct MaskWords;
-template <> struct MaskWords<2> { typedef uint2 type; };
-template <> struct MaskWords<4> { typedef uint4 type; };
 
 typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
 typedef float f32x2 __attribute__((ext_vector_type(2)));
@@ -228,29 +235,40 @@ __device__ __forceinline__ uint32_t pack_bf16(float lo, float hi) {
 __device__ __forceinline__ float lo_bf16(uint32_t p) { return __uint_as_float(p << 16); }
 __device__ __forceinline__ float hi_bf16(uint32_t p) { return __uint_as_float(p & 0xffff0000u); }
 
+// Raw buffer resource over [base, base + bytes): accesses past the end read 0
+// and write nothing.
+__device__ __forceinline__ Rsrc make_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
+}
+__device__ __forceinline__ bf16x8 load_frag(Rsrc r, uint32_t voff, uint32_t soff) {
+  return __builtin_bit_cast(bf16x8, __builtin_amdgcn_raw_buffer_load_b128(r, (int)voff, (int)soff, 0));
+}
+__device__ __forceinline__ void store16(Rsrc r, uint32_t voff, uint32_t soff, uint4 v) {
+  __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), r, (int)voff, (int)soff, 0);
+}
+
+// One hidden layer's fragment-ordered weight copy (see k_weights_frag).
+template <int H>
+__device__ __forceinline__ Rsrc weight_rsrc(const u16* Wb, int layer) {
+  return make_rsrc(Wb + (size_t)layer * H * H, (uint32_t)(H * H * 2));
+}
+
 // The first PD weight-fragment steps of the next product, loaded during the
-// tail of the current one.
+// tail of the current one.  Fragment (m, ks) of wave w is piece
+// ((2 w + m) KS + ks) 64 + lane: byte woff + (m KS + ks) 1024 with
+// woff = (2 w KS 64 + lane) 16.
 template <int H>
 struct WeightPrefetch {
   bf16x8 a[Chain<H>::PD][Chain<H>::MT];
 };
 
-// Fragment (m, ks) of the wave's rows of a fragment-ordered weight copy is
-// piece ((ow / 32 + m) KS + ks) 64 + lane.
 template <int H>
-__device__ __forceinline__ const u16* frag_base(const u16* Wg, int ow, int lane) {
-  return Wg + ((size_t)(ow / 32) * (H / 16) * 64 + lane) * 8;
-}
-
-template <int H>
-__device__ __forceinline__ void prefetch_weights(const u16* __restrict__ Wg, WeightPrefetch<H>& pf, int ow, int lane) {
+__device__ __forceinline__ void prefetch_weights(Rsrc W, WeightPrefetch<H>& pf, uint32_t woff) {
   using C = Chain<H>;
-  const u16* wfr = frag_base<H>(Wg, ow, lane);
 #pragma unroll
   for (int q = 0; q < C::PD; ++q)
 #pragma unroll
-    for (int m = 0; m < C::MT; ++m)
-      pf.a[q][m] = *reinterpret_cast<const bf16x8*>(wfr + ((size_t)m * (H / 16) + q) * 512);
+    for (int m = 0; m < C::MT; ++m) pf.a[q][m] = load_frag(W, woff, (uint32_t)(m * C::KS + q) * 1024);
 }
 
 typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
@@ -261,98 +279,98 @@ typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
 // so each 32-column, 16-row block is one contiguous kilobyte: an MFMA
 // fragment of v_mfma_f32_32x32x16_bf16 with K = rows.
 //
-// One wave turns block (kb, cb) of the LDS tile into its kilobyte with two
-// ds_read_b64_tr_b16: lane j of each 16-lane group g addresses row
-// 16 kb + 8 (g / 2) + j / 4 (+ 4) and columns 32 cb + 16 (g % 2) + 4 (j % 4) .. + 3;
-// the transpose then hands lane i of the group rows +0..3 (+4..7) of column
-// 32 cb + 16 (g % 2) + i.
+// Wave w writes the column blocks cb = 2 w + u (u = 0, 1) of every 16-row
+// block of the tile: copy kilobyte j is (kb, u) = (j / 2, j % 2).  It turns a
+// block of the LDS tile into its kilobyte with two ds_read_b64_tr_b16: lane i
+// of each 16-lane group g addresses row 16 kb + 8 (g / 2) + i / 4 (+ 4) and
+// columns 32 cb + 16 (g % 2) + 4 (i % 4) .. + 3; the transpose then hands
+// lane i of the group rows +0..3 (+4..7) of column 32 cb + 16 (g % 2) + i.
+// copy_lds_base is that address for (kb, u) = (0, 0); block (kb, u) adds
+// 16 kb LDA + 32 u.
 template <int LDA>
-__device__ __forceinline__ bf16x8 kfrag_from_lds(const u16* act, int kb, int cb, int lane) {
-  const int g = lane >> 4, j = lane & 15;
-  const u16* p0 = act + (16 * kb + 8 * (g >> 1) + (j >> 2)) * LDA + 32 * cb + 16 * (g & 1) + 4 * (j & 3);
+__device__ __forceinline__ int copy_lds_base(int lane, int wave) {
+  const int g = lane >> 4, i = lane & 15;
+  return (8 * (g >> 1) + (i >> 2)) * LDA + 64 * wave + 16 * (g & 1) + 4 * (i & 3);
+}
+template <int LDA>
+__device__ __forceinline__ bf16x8 copy_read(const u16* p0) {
   const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(p0));
   const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(p0 + 4 * LDA));
   return bf16x8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
 }
 
-// acc[mt][nt] = init[mt] + sum_k Wg[feature][k] act[event][k] (see above for
-// the arrangement).  pf holds the first PD weight steps of Wg on entry and
-// those of Wnext (the next product) on exit.  Spread over the K steps, the
-// workgroup also writes the LDS tile act (the product's input) to gdst in
-// K-fragment order, so those HBM writes overlap the matrix work.  With kScale
+// acc[mt][nt] = init[mt] (or 0 with kScale) + sum_k W[feature][k] act[event][k]
+// (see above for the arrangement).  pf holds the first PD weight steps of W on
+// entry and those of Wnext (the next product) on exit.  Spread over the K
+// steps, the wave also writes its share of the LDS tile act (the product's
+// input) to the tile's copy (dst, K-fragment order, coff = (2 w 64 + lane) 16),
+// so those HBM writes overlap the matrix work.  With kScale (the backward)
 // the rows are scaled by rscale[2 r] and rounded to bf16 again, and the fp32
-// scaled values of each column are summed into colsum: the copy gives wave w
-// the column blocks cb = w (mod 4), block u of them (cb = w + 4 u) in
-// colsum[u], column 32 cb + lane % 32, rows of lane half lane / 32.
+// scaled values of column 32 (2 w + u) + lane % 32 (rows of lane half
+// lane / 32) are summed into colsum[u].
 template <int H, bool kScale>
-__device__ __forceinline__ void chain_gemm(const u16* __restrict__ Wg, const u16* __restrict__ Wnext,
-                                           WeightPrefetch<H>& pf, const u16* act,
+__device__ __forceinline__ void chain_gemm(Rsrc W, Rsrc Wnext, uint32_t woff, WeightPrefetch<H>& pf, const u16* act,
                                            f32x16 (&acc)[Chain<H>::MT][Chain<H>::NT],
-                                           const f32x16 (&init)[Chain<H>::MT], int ow, int lane, int wave,
-                                           u16* __restrict__ gdst, const float* rscale,
-                                           float (&colsum)[H / 32 / Chain<H>::WAVES]) {
+                                           const f32x16 (&init)[Chain<H>::MT], int lane, int wave, Rsrc dst,
+                                           uint32_t coff, const float* rscale, float (&colsum)[2]) {
   using C = Chain<H>;
-  constexpr int KS = H / 16, PD = C::PD, LDA = C::LDA, MT = C::MT, NT = C::NT, T = C::T;
-  constexpr int BLOCKS = T * H / 512 / C::WAVES;       // fragment kilobytes per wave
-  constexpr int CDIV = KS / BLOCKS;                    // K steps per copy slot
-  static_assert(BLOCKS * CDIV == KS, "copy schedule");
+  constexpr int KS = C::KS, PD = C::PD, LDA = C::LDA, MT = C::MT, NT = C::NT, CDIV = C::CDIV;
 #pragma unroll
   for (int m = 0; m < MT; ++m)
 #pragma unroll
-    for (int n = 0; n < NT; ++n) acc[m][n] = init[m];
+    for (int n = 0; n < NT; ++n) {
+      if constexpr (kScale) {
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc[m][n][r] = 0.f;
+      } else {
+        acc[m][n] = init[m];
+      }
+    }
   const int lr = lane & 31, lh = lane >> 5;
-  const u16* wfr = frag_base<H>(Wg, ow, lane);
-  const u16* wnx = frag_base<H>(Wnext, ow, lane);
   const u16* brow = act + lr * LDA + 8 * lh;
+  const u16* cbase = act + copy_lds_base<LDA>(lane, wave);
   bf16x8 a[PD + 1][MT];
-  bf16x8 b[3][NT];
+  bf16x8 b[2][NT];
 #pragma unroll
   for (int q = 0; q < PD; ++q)
 #pragma unroll
     for (int m = 0; m < MT; ++m) a[q][m] = pf.a[q][m];
 #pragma unroll
-  for (int q = 0; q < 2; ++q)
-#pragma unroll
-    for (int n = 0; n < NT; ++n) b[q][n] = *reinterpret_cast<const bf16x8*>(brow + 32 * n * LDA + 16 * q);
+  for (int n = 0; n < NT; ++n) b[0][n] = *reinterpret_cast<const bf16x8*>(brow + 32 * n * LDA);
   bf16x8 cv;
-  int ckb = 0, ccb = 0;
-  auto put = [&]() __attribute__((always_inline)) {
+  auto put = [&](int j) __attribute__((always_inline)) {
+    const int kb = j >> 1, u = j & 1;
     uint4 w;
     if constexpr (kScale) {
-      const int r0 = 16 * ckb + 8 * lh;
+      const float* rs = rscale + 2 * (16 * kb + 8 * lh);
       float v[8];
 #pragma unroll
-      for (int t = 0; t < 8; ++t) v[t] = (float)cv[t] * rscale[2 * (r0 + t)];
+      for (int t = 0; t < 8; ++t) v[t] = (float)cv[t] * rs[2 * t];
       w = make_uint4(pack_bf16(v[0], v[1]), pack_bf16(v[2], v[3]), pack_bf16(v[4], v[5]), pack_bf16(v[6], v[7]));
-      const float sum = ((v[0] + v[1]) + (v[2] + v[3])) + ((v[4] + v[5]) + (v[6] + v[7]));
-#pragma unroll
-      for (int u = 0; u < H / 32 / C::WAVES; ++u)
-        if (ccb == wave + C::WAVES * u) colsum[u] += sum;
+      colsum[u] += ((v[0] + v[1]) + (v[2] + v[3])) + ((v[4] + v[5]) + (v[6] + v[7]));
     } else {
       w = __builtin_bit_cast(uint4, cv);
     }
-    *reinterpret_cast<uint4*>(gdst + (((size_t)ckb * (H / 32) + ccb) * 64 + lane) * 8) = w;
+    store16(dst, coff, (uint32_t)(kb * (H / 32) + u) * 1024, w);
   };
 #pragma unroll
   for (int ks = 0; ks < KS; ++ks) {
 #pragma unroll
     for (int m = 0; m < MT; ++m) {
       if (ks + PD < KS)
-        a[(ks + PD) % (PD + 1)][m] = *reinterpret_cast<const bf16x8*>(wfr + ((size_t)m * KS + ks + PD) * 512);
+        a[(ks + PD) % (PD + 1)][m] = load_frag(W, woff, (uint32_t)(m * KS + ks + PD) * 1024);
       else
-        pf.a[ks + PD - KS][m] = *reinterpret_cast<const bf16x8*>(wnx + ((size_t)m * KS + ks + PD - KS) * 512);
+        pf.a[ks + PD - KS][m] = load_frag(Wnext, woff, (uint32_t)(m * KS + ks + PD - KS) * 1024);
     }
-    if (ks + 2 < KS) {
+    if (ks + 1 < KS) {
 #pragma unroll
       for (int n = 0; n < NT; ++n)
-        b[(ks + 2) % 3][n] = *reinterpret_cast<const bf16x8*>(brow + 32 * n * LDA + 16 * (ks + 2));
+        b[(ks + 1) & 1][n] = *reinterpret_cast<const bf16x8*>(brow + 32 * n * LDA + 16 * (ks + 1));
     }
     if (ks % CDIV == 0) {
-      if (ks > 0) put();
-      const int blk = wave + C::WAVES * (ks / CDIV);
-      ckb = blk / (H / 32);
-      ccb = blk % (H / 32);
-      cv = kfrag_from_lds<LDA>(act, ckb, ccb, lane);
+      const int j = ks / CDIV;
+      if (j > 0) put(j - 1);
+      cv = copy_read<LDA>(cbase + 16 * (j >> 1) * LDA + 32 * (j & 1));
     }
     // keep the prefetches above the products of this step (the scheduler
     // would otherwise sink each load next to its first use)
@@ -361,10 +379,10 @@ __device__ __forceinline__ void chain_gemm(const u16* __restrict__ Wg, const u16
     for (int n = 0; n < NT; ++n)
 #pragma unroll
       for (int m = 0; m < MT; ++m)
-        acc[m][n] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[ks % (PD + 1)][m], b[ks % 3][n], acc[m][n], 0, 0, 0);
+        acc[m][n] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[ks % (PD + 1)][m], b[ks & 1][n], acc[m][n], 0, 0, 0);
     __builtin_amdgcn_sched_barrier(0);
   }
-  put();
+  put(C::COPIES - 1);
 }
 
 // LeakyReLU (slope in [0, 1]: max(v, s v)), bf16 rounding and the lane's sign
@@ -394,16 +412,12 @@ __device__ __forceinline__ void activate(const f32x16 (&v)[MT][NT], float slope,
 }
 
 // A lane's mask words of one layer: store and load as one vector.
-template <int MW>
-__device__ __forceinline__ void store_mask(uint32_t* dst, const uint32_t (&m)[MW]) {
-  typename MaskWords<MW>::type v;
-  __builtin_memcpy(&v, m, sizeof(v));
-  *reinterpret_cast<typename MaskWords<MW>::type*>(dst) = v;
+__device__ __forceinline__ void store_mask(uint32_t* dst, const uint32_t (&m)[4]) {
+  *reinterpret_cast<uint4*>(dst) = make_uint4(m[0], m[1], m[2], m[3]);
 }
-template <int MW>
-__device__ __forceinline__ void load_mask(const uint32_t* src, uint32_t (&m)[MW]) {
-  const typename MaskWords<MW>::type v = *reinterpret_cast<const typename MaskWords<MW>::type*>(src);
-  __builtin_memcpy(m, &v, sizeof(v));
+__device__ __forceinline__ void load_mask(const uint32_t* src, uint32_t (&m)[4]) {
+  const uint4 v = *reinterpret_cast<const uint4*>(src);
+  m[0] = v.x; m[1] = v.y; m[2] = v.z; m[3] = v.w;
 }
 
 // Bit of output e in a lane's mask (see activate).
@@ -425,6 +439,19 @@ __device__ __forceinline__ void store_tile(u16* act, const uint2 (&pk)[MT][NT][4
         *reinterpret_cast<uint2*>(act + (32 * nt + lr) * LDA + ow + 32 * mt + 8 * g + 4 * lh) = pk[mt][nt][g];
 }
 
+// The 32 bias values of a lane's outputs, in the accumulator arrangement.
+template <int MT>
+__device__ __forceinline__ void load_bias(const float* __restrict__ b, int ow, int lh, f32x16 (&bias)[MT]) {
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      const f32x4 b4 = *reinterpret_cast<const f32x4*>(b + ow + 32 * mt + 8 * g + 4 * lh);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) bias[mt][4 * g + q] = b4[q];
+    }
+}
+
 struct ChainArgs {
   const float* W0;           // first layer [H][F] fp32
   const float* b0;           // [H]
@@ -441,7 +468,7 @@ struct ChainArgs {
   const float* xs;           // [rows][D] (fake chunks)
   u16* act;                  // [NH][rows H]: A_1 .. A_NH, K-fragment order
   u16* dlt;                  // [NH][rows H]: bf16(e_D x signal at A_2 .. A_{NH+1}), K-fragment order
-  uint32_t* mask;            // [NH + 1][rows / T][4 waves][64 lanes][MW]: signs of A_1 .. A_{NH+1}
+  uint32_t* mask;            // [NH + 1][rows / T][WAVES][64 lanes][4]: signs of A_1 .. A_{NH+1}
   float* eD;                 // [rows] dL_D/dz (0 on padding)
   float* eG;                 // [rows] dL_G/dz (fake; 0 otherwise)
   float* logits;             // caller's array (indexed from c.row0) or NULL
@@ -457,18 +484,23 @@ __device__ __forceinline__ float softplus_fast(float t) { return fmaxf(t, 0.0f) 
 // Forward chain of one chunk: A_1 (VALU, K = F) -> hidden layers (MFMA) ->
 // logit z, BCE seeds e_D and e_G, and per-workgroup partials of dW_o, db_o
 // and the loss sums.  Stores A_1 .. A_NH and the masks for later kernels.
+// Each tile's features are staged through LDS, loaded one tile ahead.
 template <int H, int F>
-__global__ __launch_bounds__(kChainThreads, Chain<H>::BPC) void k_fwd_chain(ChainArgs p) {
+__global__ __launch_bounds__(Chain<H>::THREADS, Chain<H>::BPC) void k_fwd_chain(ChainArgs p) {
   using C = Chain<H>;
-  constexpr int T = C::T, LDA = C::LDA, WAVES = C::WAVES, MT = C::MT, NT = C::NT, MW = C::MW;
-  constexpr int NTH = kChainThreads;
+  constexpr int T = C::T, LDA = C::LDA, WAVES = C::WAVES, MT = C::MT, NT = C::NT, MW = C::MW, NTH = C::THREADS;
+  constexpr int FU = (T * F + NTH - 1) / NTH;   // staged feature values per thread
   __shared__ __attribute__((aligned(16))) u16 act[T * LDA];
   __shared__ float sW0[H * (F + 1)];            // row o: W0[o][0 .. F-1], b0[o]
+  __shared__ float sfeat[T * F];
   __shared__ float zpart[WAVES][T];
+  __shared__ float se_s[T];
   __shared__ __attribute__((aligned(16))) float swo[H];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int lr = lane & 31, lh = lane >> 5;
   const int ow = 32 * MT * wave;
+  const uint32_t woff = ((uint32_t)(2 * wave * C::KS * 64 + lane)) * 16;
+  const uint32_t coff = ((uint32_t)(2 * wave * 64 + lane)) * 16;
   const ChunkArgs c = p.c;
   const int64_t rstride = (int64_t)c.rows;
   const int ntiles = c.rows / T;
@@ -478,43 +510,42 @@ __global__ __launch_bounds__(kChainThreads, Chain<H>::BPC) void k_fwd_chain(Chai
     sW0[k * (F + 1) + F] = p.b0[k];
     swo[k] = p.wo[k];
   }
-  // dW_o partial of feature ow + 32 mt + 8 g + 4 lh + q
-  float dwo[MT][4][4];
-#pragma unroll
-  for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-    for (int g = 0; g < 4; ++g)
-#pragma unroll
-      for (int q = 0; q < 4; ++q) dwo[mt][g][q] = 0.f;
+  float dwo = 0.f;                              // dW_o partial of feature tid
   const float bo = p.bo[0];
-  float l0 = 0.f, l1 = 0.f, se = 0.f;
+  float l0 = 0.f, l1 = 0.f, se = 0.f;           // loss and e_D sums of event tid (tid < T)
   WeightPrefetch<H> pf;
-  prefetch_weights<H>(p.Wb, pf, ow, lane);
-  // this lane's features of the next tile, loaded one tile ahead
-  float fnext[NT][F];
+  prefetch_weights<H>(weight_rsrc<H>(p.Wb, 0), pf, woff);
+  float fst[FU];
   auto load_feat = [&](int tile) __attribute__((always_inline)) {
 #pragma unroll
-    for (int nt = 0; nt < NT; ++nt)
-#pragma unroll
-      for (int k = 0; k < F; ++k) fnext[nt][k] = p.feat[(int64_t)(tile * T + 32 * nt + lr) * F + k];
+    for (int u = 0; u < FU; ++u) {
+      const int k = tid + NTH * u;
+      if (k < T * F) fst[u] = p.feat[(int64_t)tile * T * F + k];
+    }
   };
   if ((int)blockIdx.x < ntiles) load_feat(blockIdx.x);
-  __syncthreads();
 
   for (int tile = blockIdx.x; tile < ntiles; tile += gridDim.x) {
     const int r0 = tile * T;
-    float f[NT][F];
 #pragma unroll
-    for (int nt = 0; nt < NT; ++nt)
-#pragma unroll
-      for (int k = 0; k < F; ++k) f[nt][k] = fnext[nt][k];
+    for (int u = 0; u < FU; ++u) {
+      const int k = tid + NTH * u;
+      if (k < T * F) sfeat[k] = fst[u];
+    }
     if (tile + (int)gridDim.x < ntiles) load_feat(tile + gridDim.x);
     auto mask_at = [&](int layer) __attribute__((always_inline)) {
       return p.mask + ((((int64_t)layer * ntiles + tile) * WAVES + wave) * 64 + lane) * MW;
     };
+    __syncthreads();                              // sfeat staged; last tile's readers of act are done
 
     // ---- first layer (VALU, K = F) in the MFMA output arrangement ----------
+    f32x16 bias[MT];
     {
+      float f[NT][F];
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+        for (int k = 0; k < F; ++k) f[nt][k] = sfeat[(32 * nt + lr) * F + k];
       f32x16 v[MT][NT];
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt)
@@ -537,33 +568,27 @@ __global__ __launch_bounds__(kChainThreads, Chain<H>::BPC) void k_fwd_chain(Chai
       uint2 pk[MT][NT][4];
       uint32_t m[MW];
       activate<MT, NT>(v, slope, pk, m);
-      store_mask<MW>(mask_at(0), m);
+      store_mask(mask_at(0), m);
       store_tile<MT, NT, LDA>(act, pk, ow, lane);
+      load_bias<MT>(p.bh[0], ow, lh, bias);
     }
     __syncthreads();
 
     // ---- hidden layers -----------------------------------------------------
     for (int l = 0; l < p.NH; ++l) {
       const bool last = l == p.NH - 1;
-      f32x16 bias[MT];
-#pragma unroll
-      for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-        for (int g = 0; g < 4; ++g) {
-          const f32x4 b4 = *reinterpret_cast<const f32x4*>(p.bh[l] + ow + 32 * mt + 8 * g + 4 * lh);
-#pragma unroll
-          for (int q = 0; q < 4; ++q) bias[mt][4 * g + q] = b4[q];
-        }
       f32x16 acc[MT][NT];
       // the product also writes its input A_{l+1} to HBM; the next product is
       // layer l + 1, or the first hidden layer of the next tile
-      float unused[H / 32 / WAVES];
-      chain_gemm<H, false>(p.Wb + (size_t)l * H * H, p.Wb + (size_t)(last ? 0 : l + 1) * H * H, pf, act, acc, bias,
-                           ow, lane, wave, p.act + ((int64_t)l * rstride + r0) * H, nullptr, unused);
+      float unused[2];
+      chain_gemm<H, false>(weight_rsrc<H>(p.Wb, l), weight_rsrc<H>(p.Wb, last ? 0 : l + 1), woff, pf, act, acc, bias,
+                           lane, wave, make_rsrc(p.act + ((int64_t)l * rstride + r0) * H, T * H * 2), coff, nullptr,
+                           unused);
+      if (!last) load_bias<MT>(p.bh[l + 1], ow, lh, bias);
       uint2 pk[MT][NT][4];
       uint32_t m[MW];
       activate<MT, NT>(acc, slope, pk, m);
-      store_mask<MW>(mask_at(l + 1), m);
+      store_mask(mask_at(l + 1), m);
       if (!last) {
         __syncthreads();                             // every wave is done reading this layer's input
         store_tile<MT, NT, LDA>(act, pk, ow, lane);
@@ -587,13 +612,13 @@ __global__ __launch_bounds__(kChainThreads, Chain<H>::BPC) void k_fwd_chain(Chai
         s += __shfl_xor(s, 32, 64);
         if (lh == 0) zpart[wave][32 * nt + lr] = s;
       }
-      __syncthreads();
-#pragma unroll
-      for (int nt = 0; nt < NT; ++nt) {
-        const int ev = 32 * nt + lr, r = r0 + ev;
+      __syncthreads();                               // zpart complete; every wave is done reading act
+      store_tile<MT, NT, LDA>(act, pk, ow, lane);    // A_{NH+1}, for dW_o
+      if (tid < T) {
+        const int r = r0 + tid;
         float z = bo;
 #pragma unroll
-        for (int w = 0; w < WAVES; ++w) z += zpart[w][ev];
+        for (int w = 0; w < WAVES; ++w) z += zpart[w][tid];
         const bool valid = r < c.valid;
         float e = 0.f, g = 0.f;
         if (valid) {
@@ -605,54 +630,37 @@ __global__ __launch_bounds__(kChainThreads, Chain<H>::BPC) void k_fwd_chain(Chai
             e = -sig_neg * p.inv_n;
           }
         }
-#pragma unroll
-        for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-          for (int gg = 0; gg < 4; ++gg) {
-            dwo[mt][gg][0] = fmaf(e, lo_bf16(pk[mt][nt][gg].x), dwo[mt][gg][0]);
-            dwo[mt][gg][1] = fmaf(e, hi_bf16(pk[mt][nt][gg].x), dwo[mt][gg][1]);
-            dwo[mt][gg][2] = fmaf(e, lo_bf16(pk[mt][nt][gg].y), dwo[mt][gg][2]);
-            dwo[mt][gg][3] = fmaf(e, hi_bf16(pk[mt][nt][gg].y), dwo[mt][gg][3]);
-          }
-        if (lh == 0 && (ev & (WAVES - 1)) == wave) {     // one lane per event, spread over the waves
-          p.eD[r] = e;
-          p.eG[r] = g;
-          se += e;
-          if (valid) {
-            if (p.logits) p.logits[c.row0 + r] = z;
-            if (c.fake) {
-              l0 += softplus_fast(z);
-              l1 += softplus_fast(-z);
-            } else {
-              l0 += softplus_fast(-z);
-            }
+        se_s[tid] = e;
+        p.eD[r] = e;
+        p.eG[r] = g;
+        se += e;
+        if (valid) {
+          if (p.logits) p.logits[c.row0 + r] = z;
+          if (c.fake) {
+            l0 += softplus_fast(z);
+            l1 += softplus_fast(-z);
+          } else {
+            l0 += softplus_fast(-z);
           }
         }
       }
-      // zpart and act are next written after the next tile's first-layer
-      // barrier, which every wave reaches only after this point.
+      __syncthreads();                               // A_{NH+1} and the seeds staged
+#pragma unroll 8
+      for (int ev = 0; ev < T; ++ev) dwo = fmaf(se_s[ev], bf16_to_f32(act[ev * LDA + tid]), dwo);
+      // act, zpart and se_s are next written after the next tile's first
+      // barrier, which every thread reaches only after this point.
     }
   }
 
   // ---- per-workgroup partials, fixed order ---------------------------------
   float* dst = p.plog + (int64_t)blockIdx.x * (H + 3);
-#pragma unroll
-  for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-    for (int g = 0; g < 4; ++g)
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        float v = dwo[mt][g][q];
-#pragma unroll
-        for (int o = 1; o < 32; o <<= 1) v += __shfl_xor(v, o, 64);
-        if (lr == 0) dst[ow + 32 * mt + 8 * g + 4 * lh + q] = v;
-      }
+  dst[tid] = dwo;
   float s3[3] = {l0, l1, se};
 #pragma unroll
   for (int k = 0; k < 3; ++k) {
     float v = s3[k];
 #pragma unroll
-    for (int o = 1; o < 32; o <<= 1) v += __shfl_xor(v, o, 64);
+    for (int o = 1; o < 64; o <<= 1) v += __shfl_xor(v, o, 64);
     if (lane == 0) zpart[wave][k] = v;
   }
   __syncthreads();
@@ -668,66 +676,78 @@ __global__ __launch_bounds__(kChainThreads, Chain<H>::BPC) void k_fwd_chain(Chai
 // through the hidden layers (MFMA, LeakyReLU' from the masks), storing the
 // signals at A_2 .. A_{NH+1} for the weight-gradient products; then the first
 // layer: per-workgroup partials of dW_1 and db_1 (scaled by e_D) and, for fake
-// chunks, dL_G/dx (scaled by e_G, through the HD8 Jacobian when used).
+// chunks, dL_G/dx (scaled by e_G, through the HD8 Jacobian when used).  Each
+// tile's seeds, features and events are staged through LDS and its masks
+// loaded into registers, all one step ahead.
 template <int H, int F, int D, bool kHD8>
-__global__ __launch_bounds__(kChainThreads, Chain<H>::BPC) void k_bwd_chain(ChainArgs p) {
+__global__ __launch_bounds__(Chain<H>::THREADS, Chain<H>::BPC) void k_bwd_chain(ChainArgs p) {
   using C = Chain<H>;
-  constexpr int T = C::T, LDA = C::LDA, WAVES = C::WAVES, MT = C::MT, NT = C::NT, MW = C::MW;
-  constexpr int NTH = kChainThreads;
-  constexpr int FPT = H / NTH;       // first-layer features per thread
+  constexpr int T = C::T, LDA = C::LDA, WAVES = C::WAVES, MT = C::MT, NT = C::NT, MW = C::MW, NTH = C::THREADS;
   constexpr int P = NTH / T;         // threads per event in the input-gradient dot
+  constexpr int SU = (T * (2 + F + D) + NTH - 1) / NTH;   // staged values per thread
   __shared__ __attribute__((aligned(16))) u16 act[T * LDA];
   __shared__ float sW0[H * F];
-  __shared__ float sfeat[T][F];
-  __shared__ float sx[T][D];
-  __shared__ float se[T][2];
+  __shared__ float srow[T * (2 + F + D)];       // per event: e_D, e_G | features | x
   __shared__ __attribute__((aligned(16))) float swo[H];
+  float* se = srow;                             // [T][2]
+  float* sfeat = srow + 2 * T;                  // [T][F]
+  float* sx = sfeat + T * F;                    // [T][D]
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int lh = lane >> 5;
   const int ow = 32 * MT * wave;
+  const uint32_t woff = ((uint32_t)(2 * wave * C::KS * 64 + lane)) * 16;
+  const uint32_t coff = ((uint32_t)(2 * wave * 64 + lane)) * 16;
   const ChunkArgs c = p.c;
   const int64_t rstride = (int64_t)c.rows;
   const int ntiles = c.rows / T;
   for (int k = tid; k < H * F; k += NTH) sW0[k] = p.W0[k];
   for (int k = tid; k < H; k += NTH) swo[k] = p.wo[k];
-  float adw[FPT][F + 1];
+  float adw[F + 1];                       // dW_1 row tid, then db_1[tid]
 #pragma unroll
-  for (int u = 0; u < FPT; ++u)
+  for (int k = 0; k <= F; ++k) adw[k] = 0.f;
+  float adb[kMaxNH][2];                   // db partials: column 32 (2 wave + u) + lane % 32, lane-half rows
 #pragma unroll
-    for (int k = 0; k <= F; ++k) adw[u][k] = 0.f;
-  constexpr int CBW = H / 32 / WAVES;     // column blocks of the copy per wave
-  float adb[kMaxNH][CBW];                 // db partials: column 32 (wave + 4 u) + lane % 32, lane-half rows
-#pragma unroll
-  for (int k = 0; k < kMaxNH; ++k)
-#pragma unroll
-    for (int u = 0; u < CBW; ++u) adb[k][u] = 0.f;
+  for (int k = 0; k < kMaxNH; ++k) adb[k][0] = adb[k][1] = 0.f;
   const bool want_dx = c.fake && p.dLg_dx != nullptr;
   const float slope = p.slope;
   const int NH = p.NH;
-  f32x16 zero[MT];
-#pragma unroll
-  for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-    for (int r = 0; r < 16; ++r) zero[mt][r] = 0.f;
+  const f32x16 none[MT] = {};
   WeightPrefetch<H> pf;
-  prefetch_weights<H>(p.WTb + (size_t)(NH - 1) * H * H, pf, ow, lane);
+  prefetch_weights<H>(weight_rsrc<H>(p.WTb, NH - 1), pf, woff);
+  auto mask_at = [&](int layer, int tile) __attribute__((always_inline)) {
+    return p.mask + ((((int64_t)layer * ntiles + tile) * WAVES + wave) * 64 + lane) * MW;
+  };
+  // staged rows of a tile: value k of srow, from the seed, feature and event arrays
+  float sv[SU];
+  auto load_rows = [&](int tile) __attribute__((always_inline)) {
+    const int64_t r0 = (int64_t)tile * T;
+#pragma unroll
+    for (int u = 0; u < SU; ++u) {
+      const int k = tid + NTH * u;
+      float v = 0.f;
+      if (k < 2 * T) v = (k & 1) ? p.eG[r0 + (k >> 1)] : p.eD[r0 + (k >> 1)];
+      else if (k < (2 + F) * T) v = p.feat[r0 * F + (k - 2 * T)];
+      else if (k < (2 + F + D) * T && want_dx && kHD8) v = p.xs[r0 * D + (k - (2 + F) * T)];
+      sv[u] = v;
+    }
+  };
+  uint32_t mtop[MW];
+  if ((int)blockIdx.x < ntiles) {
+    load_rows(blockIdx.x);
+    load_mask(mask_at(NH, blockIdx.x), mtop);
+  }
 
   for (int tile = blockIdx.x; tile < ntiles; tile += gridDim.x) {
     const int r0 = tile * T;
-    auto mask_at = [&](int layer) __attribute__((always_inline)) {
-      return p.mask + ((((int64_t)layer * ntiles + tile) * WAVES + wave) * 64 + lane) * MW;
-    };
-    for (int k = tid; k < T; k += NTH) {
-      se[k][0] = p.eD[r0 + k];
-      se[k][1] = p.eG[r0 + k];
+    const int next = tile + gridDim.x;
+#pragma unroll
+    for (int u = 0; u < SU; ++u) {
+      const int k = tid + NTH * u;
+      if (k < T * (2 + F + D)) srow[k] = sv[u];
     }
-    for (int k = tid; k < T * F; k += NTH) sfeat[k / F][k % F] = p.feat[(int64_t)r0 * F + k];
-    if (want_dx && kHD8)
-      for (int k = tid; k < T * D; k += NTH) sx[k / D][k % D] = p.xs[(int64_t)r0 * D + k];
+    if (next < ntiles) load_rows(next);
     // ---- unit-seed signal at A_{NH+1}: w_o * LeakyReLU'(A_{NH+1}) ----------
     {
-      uint32_t m[MW];
-      load_mask<MW>(mask_at(NH), m);
       uint2 pk[MT][NT][4];
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt)
@@ -739,33 +759,32 @@ __global__ __launch_bounds__(kChainThreads, Chain<H>::BPC) void k_bwd_chain(Chai
             const int e = 16 * (mt * NT + nt) + 4 * g;
             float d[4];
 #pragma unroll
-            for (int q = 0; q < 4; ++q) d[q] = mask_bit(m, e + q) ? w4[q] : w4[q] * slope;
+            for (int q = 0; q < 4; ++q) d[q] = mask_bit(mtop, e + q) ? w4[q] : w4[q] * slope;
             pk[mt][nt][g] = make_uint2(pack_bf16(d[0], d[1]), pack_bf16(d[2], d[3]));
           }
         }
       store_tile<MT, NT, LDA>(act, pk, ow, lane);
-      __syncthreads();
     }
+    __syncthreads();
     // ---- hidden layers, top down ---------------------------------------------
     for (int l = NH - 1; l >= 0; --l) {
+      uint32_t m[MW];
+      load_mask(mask_at(l, tile), m);
+      if (l == 0 && next < ntiles) load_mask(mask_at(NH, next), mtop);
       f32x16 acc[MT][NT];
-      // the product also writes its input (the signal at A_{l+2}) to HBM; the
-      // next product is layer l - 1, or the top layer of the next tile
-      // the copy of this product's input (the signal at A_{l+2}) also sums
-      // e_D times it per column: db of hidden layer l
-      float colsum[CBW];
-#pragma unroll
-      for (int u = 0; u < CBW; ++u) colsum[u] = 0.f;
-      chain_gemm<H, true>(p.WTb + (size_t)l * H * H, p.WTb + (size_t)(l > 0 ? l - 1 : NH - 1) * H * H, pf, act, acc,
-                          zero, ow, lane, wave, p.dlt + ((int64_t)l * rstride + r0) * H, &se[0][0], colsum);
+      // the product also writes its input (the signal at A_{l+2}) to HBM and
+      // sums e_D times it per column (db of hidden layer l); the next product
+      // is layer l - 1, or the top layer of the next tile
+      float colsum[2] = {0.f, 0.f};
+      chain_gemm<H, true>(weight_rsrc<H>(p.WTb, l), weight_rsrc<H>(p.WTb, l > 0 ? l - 1 : NH - 1), woff, pf, act,
+                          acc, none, lane, wave, make_rsrc(p.dlt + ((int64_t)l * rstride + r0) * H, T * H * 2), coff,
+                          se, colsum);
 #pragma unroll
       for (int k = 0; k < kMaxNH; ++k)
         if (k == l) {
-#pragma unroll
-          for (int u = 0; u < CBW; ++u) adb[k][u] += colsum[u];
+          adb[k][0] += colsum[0];
+          adb[k][1] += colsum[1];
         }
-      uint32_t m[MW];
-      load_mask<MW>(mask_at(l), m);
       uint2 pk[MT][NT][4];
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt)
@@ -789,14 +808,10 @@ __global__ __launch_bounds__(kChainThreads, Chain<H>::BPC) void k_bwd_chain(Chai
     // ---- first layer: act holds the signal at A_1 ---------------------------
 #pragma unroll 4
     for (int ev = 0; ev < T; ++ev) {
-      const float e = se[ev][0];
+      const float ed = se[2 * ev] * bf16_to_f32(act[ev * LDA + tid]);
 #pragma unroll
-      for (int u = 0; u < FPT; ++u) {
-        const float ed = e * bf16_to_f32(act[ev * LDA + tid + NTH * u]);
-#pragma unroll
-        for (int j = 0; j < F; ++j) adw[u][j] = fmaf(ed, sfeat[ev][j], adw[u][j]);
-        adw[u][F] += ed;
-      }
+      for (int j = 0; j < F; ++j) adw[j] = fmaf(ed, sfeat[ev * F + j], adw[j]);
+      adw[F] += ed;
     }
     if (want_dx) {
       const int ev = tid / P, pp = tid % P;
@@ -822,15 +837,17 @@ __global__ __launch_bounds__(kChainThreads, Chain<H>::BPC) void k_bwd_chain(Chai
         for (int j = 0; j < F; ++j) g[j] += __shfl_xor(g[j], s, 64);
       const int r = r0 + ev;
       if (pp == 0 && r < c.valid) {
-        const float eg = se[ev][1];
+        const float eg = se[2 * ev + 1];
 #pragma unroll
         for (int j = 0; j < F; ++j) g[j] *= eg;
         float dx[D];
         if constexpr (kHD8) {
           // d features / d x of [x1, x2, x3, x1x2, x2x3, x1x3, ln x1, ln(1 - x3)];
           // 1/x1 and 1/(1 - x3) from the log features, accurate where fp32 x3 is within ulps of 1
-          const float x1 = sx[ev][0], x2 = sx[ev][1], x3 = sx[ev][2];
-          const float inv_x1 = expf(-sfeat[ev][6]), inv_1mx3 = expf(-sfeat[ev][7]);
+          const float* xe = sx + ev * D;
+          const float* fe = sfeat + ev * F;
+          const float x1 = xe[0], x2 = xe[1], x3 = xe[2];
+          const float inv_x1 = expf(-fe[6]), inv_1mx3 = expf(-fe[7]);
           dx[0] = g[0] + g[3] * x2 + g[5] * x3 + g[6] * inv_x1;
           dx[1] = g[1] + g[3] * x1 + g[4] * x3;
           dx[2] = g[2] + g[4] * x2 + g[5] * x1 - g[7] * inv_1mx3;
@@ -849,18 +866,14 @@ __global__ __launch_bounds__(kChainThreads, Chain<H>::BPC) void k_bwd_chain(Chai
   float* dst = p.pfb + (int64_t)blockIdx.x * (H * F + H);
   float* dbd = p.pdb + (int64_t)blockIdx.x * NH * H;
 #pragma unroll
-  for (int u = 0; u < FPT; ++u) {
-    const int o = tid + NTH * u;
-#pragma unroll
-    for (int j = 0; j < F; ++j) dst[o * F + j] = adw[u][j];
-    dst[H * F + o] = adw[u][F];
-  }
+  for (int j = 0; j < F; ++j) dst[tid * F + j] = adw[j];
+  dst[H * F + tid] = adw[F];
 #pragma unroll
   for (int k = 0; k < kMaxNH; ++k)
 #pragma unroll
-    for (int u = 0; u < CBW; ++u) {
+    for (int u = 0; u < 2; ++u) {
       const float v = adb[k][u] + __shfl_xor(adb[k][u], 32, 64);   // both row halves of the column
-      if (k < NH && lane < 32) dbd[k * H + 32 * (wave + WAVES * u) + lane] = v;
+      if (k < NH && lane < 32) dbd[k * H + 32 * (2 * wave + u) + lane] = v;
     }
 }
 
@@ -1055,8 +1068,8 @@ Plan make_plan(const DiscArgs& a, int n_cu) {
 
 template <int H, int F, int D, bool kHD8>
 void launch_chains(const ChainArgs& ca, int blocks, bool bwd, hipStream_t st) {
-  if (!bwd) hipLaunchKernelGGL((k_fwd_chain<H, F>), dim3(blocks), dim3(kChainThreads), 0, st, ca);
-  else hipLaunchKernelGGL((k_bwd_chain<H, F, D, kHD8>), dim3(blocks), dim3(kChainThreads), 0, st, ca);
+  if (!bwd) hipLaunchKernelGGL((k_fwd_chain<H, F>), dim3(blocks), dim3(Chain<H>::THREADS), 0, st, ca);
+  else hipLaunchKernelGGL((k_bwd_chain<H, F, D, kHD8>), dim3(blocks), dim3(Chain<H>::THREADS), 0, st, ca);
 }
 
 void launch_chain(const Plan& p, const ChainArgs& ca, bool bwd, hipStream_t st) {
