@@ -80,25 +80,43 @@ __device__ __forceinline__ void store_bf16(u16* p, const float (&v)[PER]) {
 
 
 // ---------------------------------------------------------------------------
-// Weights: bf16 copies of one hidden layer, W ([out][in]) and W^T, in the order
-// the chain kernels consume them as MFMA A fragments: piece (rb, ks, lane)
-// holds rows 32 rb + lane % 32, columns 16 ks + 8 (lane / 32) .. + 7, so the
-// 64 lanes of a wave read one contiguous kilobyte per fragment.
-__global__ __launch_bounds__(256) void k_weights_frag(const float* __restrict__ W, u16* __restrict__ Wf,
-                                                      u16* __restrict__ WTf, int H) {
+// Weights: bf16 copies of one hidden layer in the order the chain kernels
+// consume them as MFMA A fragments.  Piece (rb, ks, lane) of a copy holds rows
+// 32 rb + lane % 32, columns 16 ks + 8 (lane / 32) .. + 7, so the 64 lanes of
+// a wave read one contiguous kilobyte per fragment.  The forward copy (of W,
+// [out][in]) has KS + 1 pieces per 32-row block: the extra step KS carries the
+// bias as three bf16 terms hi + mid + lo, whose sum is exactly the fp32 bias,
+// in columns 0..2 of lane half 0 (zeros elsewhere), and the forward products
+// multiply it by a constant fragment of ones.  The backward copy (of W^T) has
+// KS pieces per row block.
+__device__ __forceinline__ uint32_t bias_terms(float x, uint32_t& lo) {
+  const u16 hi = bf16_bits(x);
+  const float r = x - bf16_to_f32(hi);       // exact
+  const u16 mid = bf16_bits(r);
+  lo = bf16_bits(r - bf16_to_f32(mid));      // r - mid exact; it fits in 8 bits
+  return (uint32_t)hi | ((uint32_t)mid << 16);
+}
+
+__global__ __launch_bounds__(256) void k_weights_frag(const float* __restrict__ W, const float* __restrict__ b,
+                                                      u16* __restrict__ Wf, u16* __restrict__ WTf, int H) {
   const int t = blockIdx.x * 256 + threadIdx.x;
   const int KS = H / 16;
-  if (t >= H * H / 8) return;
-  const int rb = t / (KS * 64), rem = t % (KS * 64), ks = rem / 64, lane = rem % 64;
+  if (t >= (H / 32) * (KS + 1) * 64) return;
+  const int rb = t / ((KS + 1) * 64), rem = t % ((KS + 1) * 64), ks = rem / 64, lane = rem % 64;
   const int row = 32 * rb + (lane & 31), col0 = 16 * ks + 8 * (lane >> 5);
-  uint32_t wp[4], wt[4];
+  uint32_t wp[4] = {0u, 0u, 0u, 0u};
+  if (ks < KS) {
+    uint32_t wt[4];
 #pragma unroll
-  for (int u = 0; u < 4; ++u) {
-    wp[u] = (uint32_t)bf16_bits(W[row * H + col0 + 2 * u]) | ((uint32_t)bf16_bits(W[row * H + col0 + 2 * u + 1]) << 16);
-    wt[u] = (uint32_t)bf16_bits(W[(col0 + 2 * u) * H + row]) | ((uint32_t)bf16_bits(W[(col0 + 2 * u + 1) * H + row]) << 16);
+    for (int u = 0; u < 4; ++u) {
+      wp[u] = (uint32_t)bf16_bits(W[row * H + col0 + 2 * u]) | ((uint32_t)bf16_bits(W[row * H + col0 + 2 * u + 1]) << 16);
+      wt[u] = (uint32_t)bf16_bits(W[(col0 + 2 * u) * H + row]) | ((uint32_t)bf16_bits(W[(col0 + 2 * u + 1) * H + row]) << 16);
+    }
+    *reinterpret_cast<uint4*>(WTf + ((size_t)(rb * KS + ks) * 64 + lane) * 8) = make_uint4(wt[0], wt[1], wt[2], wt[3]);
+  } else if (lane < 32) {
+    wp[0] = bias_terms(b[row], wp[1]);
   }
   *reinterpret_cast<uint4*>(Wf + (size_t)t * 8) = make_uint4(wp[0], wp[1], wp[2], wp[3]);
-  *reinterpret_cast<uint4*>(WTf + (size_t)t * 8) = make_uint4(wt[0], wt[1], wt[2], wt[3]);
 }
 
 // ---------------------------------------------------------------------------
@@ -185,23 +203,29 @@ __global__ __launch_bounds__(256) void k_prep(ChunkArgs c, const float* __restri
 // LDS reads (one step ahead).  The 16-byte row pad makes each 8-lane group of
 // an LDS fragment read hit distinct banks.
 //
-// Global streams inside the products (weights, the HBM copies) go through
-// buffer resources: one per-lane offset register per stream, every per-step
-// offset a scalar constant.  That keeps the 128 accumulators and the rings
-// within the 256 registers a wave has at two waves per SIMD.
+// The VALU work per output is kept to the LeakyReLU (two operations), the
+// bf16 rounding (half of a v_cvt_pk_bf16_f32) and a quarter of the sign-mask
+// packing: biases enter the forward products as one more K step, and the
+// first layer (fp32, K = F + 1 with the bias) and the logit (bf16 activations
+// against the fp32 w_o split into three bf16 terms) also run on the matrix
+// cores.
+//
+// Global streams inside the products use one per-lane 32-bit offset register
+// each, with every per-step offset a scalar constant: buffer loads for the
+// weights, global stores with a scalar base for the HBM copies.  That keeps
+// the 128 accumulators and the rings within the 256 registers a wave has at
+// two waves per SIMD.
 //
 // Lane l holds, in register 4 g + q of tile (mt, nt), the output of feature
 // ow + 32 mt + 8 g + 4 (l / 32) + q for event 32 nt + (l % 32): each group g
-// is 4 consecutive features of one event (one 8-byte bf16 store).  The
-// forward's first layer (K = F, VALU) produces its outputs in the same
-// arrangement.
+// is 4 consecutive features of one event (one 8-byte bf16 store).
 //
-// Signs of the hidden activations are kept as lane-local bit masks: the 32
-// outputs a lane holds in one layer are numbered e = 16 (mt NT + nt) + 4 g + q
-// and bit 31 - e % 32 of word e / 32 is set where the bf16 activation is > 0;
-// each lane stores its 4 words as one vector, [layer][tile][wave][lane].  The
-// backward chain has the same lane arrangement and reads them back, so
-// LeakyReLU' costs one bit per output instead of re-reading the activations.
+// Signs of the hidden activations are kept as lane-local bit masks, 4 words
+// per lane and layer: the sign bit of output (mt, nt, g, q) is bit
+// 8 q + g + 4 (t % 2) of word t / 2, t = mt NT + nt, set where the bf16
+// activation is negative (or -0).  Each lane stores its words as one vector,
+// [layer][tile][wave][lane]; the backward chain has the same lane arrangement
+// and reads them back, so LeakyReLU' costs one bit per output.
 
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
@@ -215,7 +239,7 @@ struct Chain {
   static constexpr int THREADS = 64 * WAVES;    // = H
   static constexpr int T = 32 * NT;             // events per tile
   static constexpr int LDA = H + 8;             // LDS row stride (bf16)
-  static constexpr int KS = H / 16;             // K steps per product
+  static constexpr int KS = H / 16;             // K steps of a product's input
   static constexpr int PD = 2;                  // weight prefetch distance (K steps)
   static constexpr int MW = MT * NT / 2;        // mask words per lane and layer
   static constexpr int BPC = 512 / H;           // workgroups per CU
@@ -232,8 +256,6 @@ typedef float f32x2 __attribute__((ext_vector_type(2)));
 __device__ __forceinline__ uint32_t pack_bf16(float lo, float hi) {
   return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2{lo, hi}), bf16x2_t));
 }
-__device__ __forceinline__ float lo_bf16(uint32_t p) { return __uint_as_float(p << 16); }
-__device__ __forceinline__ float hi_bf16(uint32_t p) { return __uint_as_float(p & 0xffff0000u); }
 
 // Raw buffer resource over [base, base + bytes): accesses past the end read 0
 // and write nothing.
@@ -243,32 +265,42 @@ __device__ __forceinline__ Rsrc make_rsrc(const void* base, uint32_t bytes) {
 __device__ __forceinline__ bf16x8 load_frag(Rsrc r, uint32_t voff, uint32_t soff) {
   return __builtin_bit_cast(bf16x8, __builtin_amdgcn_raw_buffer_load_b128(r, (int)voff, (int)soff, 0));
 }
-__device__ __forceinline__ void store16(Rsrc r, uint32_t voff, uint32_t soff, uint4 v) {
-  __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), r, (int)voff, (int)soff, 0);
-}
 
-// One hidden layer's fragment-ordered weight copy (see k_weights_frag).
-template <int H>
+// K steps per 32-row block of a weight copy: KS + 1 forward (with the bias
+// step), KS backward.
+template <int H, bool kFwd>
+struct WSteps {
+  static constexpr int N = H / 16 + (kFwd ? 1 : 0);
+};
+
+// Weight copy of one hidden layer, and the per-lane offset of fragment (0, 0)
+// of wave w: fragment (m, ks) is piece ((2 w + m) N + ks) 64 + lane, i.e.
+// byte woff + (m N + ks) 1024.
+template <int H, bool kFwd>
 __device__ __forceinline__ Rsrc weight_rsrc(const u16* Wb, int layer) {
-  return make_rsrc(Wb + (size_t)layer * H * H, (uint32_t)(H * H * 2));
+  constexpr uint32_t bytes = (H / 32) * WSteps<H, kFwd>::N * 1024;
+  return make_rsrc(Wb + (size_t)layer * (bytes / 2), bytes);
+}
+template <int H, bool kFwd>
+__device__ __forceinline__ uint32_t weight_offset(int wave, int lane) {
+  return (uint32_t)(2 * wave * WSteps<H, kFwd>::N * 64 + lane) * 16;
 }
 
 // The first PD weight-fragment steps of the next product, loaded during the
-// tail of the current one.  Fragment (m, ks) of wave w is piece
-// ((2 w + m) KS + ks) 64 + lane: byte woff + (m KS + ks) 1024 with
-// woff = (2 w KS 64 + lane) 16.
+// tail of the current one.
 template <int H>
 struct WeightPrefetch {
   bf16x8 a[Chain<H>::PD][Chain<H>::MT];
 };
 
-template <int H>
+template <int H, bool kFwd>
 __device__ __forceinline__ void prefetch_weights(Rsrc W, WeightPrefetch<H>& pf, uint32_t woff) {
   using C = Chain<H>;
+  constexpr int N = WSteps<H, kFwd>::N;
 #pragma unroll
   for (int q = 0; q < C::PD; ++q)
 #pragma unroll
-    for (int m = 0; m < C::MT; ++m) pf.a[q][m] = load_frag(W, woff, (uint32_t)(m * C::KS + q) * 1024);
+    for (int m = 0; m < C::MT; ++m) pf.a[q][m] = load_frag(W, woff, (uint32_t)(m * N + q) * 1024);
 }
 
 typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
@@ -299,36 +331,25 @@ __device__ __forceinline__ bf16x8 copy_read(const u16* p0) {
   return bf16x8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
 }
 
-// acc[mt][nt] = init[mt] (or 0 with kScale) + sum_k W[feature][k] act[event][k]
-// (see above for the arrangement).  pf holds the first PD weight steps of W on
+// acc[mt][nt] = sum_k W[feature][k] act[event][k] (+ the bias with kFwd; see
+// above for the arrangement).  pf holds the first PD weight steps of W on
 // entry and those of Wnext (the next product) on exit.  Spread over the K
 // steps, the wave also writes its share of the LDS tile act (the product's
-// input) to the tile's copy (dst, K-fragment order, coff = (2 w 64 + lane) 16),
-// so those HBM writes overlap the matrix work.  With kScale (the backward)
-// the rows are scaled by rscale[2 r] and rounded to bf16 again, and the fp32
-// scaled values of column 32 (2 w + u) + lane % 32 (rows of lane half
-// lane / 32) are summed into colsum[u].
-template <int H, bool kScale>
+// input) to the tile's copy (dst, K-fragment order, per-lane byte offset
+// coff = (2 w 64 + lane) 16), so those HBM writes overlap the matrix work.
+template <int H, bool kFwd>
 __device__ __forceinline__ void chain_gemm(Rsrc W, Rsrc Wnext, uint32_t woff, WeightPrefetch<H>& pf, const u16* act,
-                                           f32x16 (&acc)[Chain<H>::MT][Chain<H>::NT],
-                                           const f32x16 (&init)[Chain<H>::MT], int lane, int wave, Rsrc dst,
-                                           uint32_t coff, const float* rscale, float (&colsum)[2]) {
+                                           f32x16 (&acc)[Chain<H>::MT][Chain<H>::NT], int lane, int wave, u16* dst,
+                                           uint32_t coff) {
   using C = Chain<H>;
   constexpr int KS = C::KS, PD = C::PD, LDA = C::LDA, MT = C::MT, NT = C::NT, CDIV = C::CDIV;
-#pragma unroll
-  for (int m = 0; m < MT; ++m)
-#pragma unroll
-    for (int n = 0; n < NT; ++n) {
-      if constexpr (kScale) {
-#pragma unroll
-        for (int r = 0; r < 16; ++r) acc[m][n][r] = 0.f;
-      } else {
-        acc[m][n] = init[m];
-      }
-    }
+  constexpr int N = WSteps<H, kFwd>::N;          // K steps, the bias step last
   const int lr = lane & 31, lh = lane >> 5;
   const u16* brow = act + lr * LDA + 8 * lh;
   const u16* cbase = act + copy_lds_base<LDA>(lane, wave);
+  // B fragment of the bias step: ones against the three bias terms (lane
+  // half 1 meets zero weights)
+  const bf16x8 ones = __builtin_bit_cast(bf16x8, make_uint4(0x3f803f80u, 0x00003f80u, 0u, 0u));
   bf16x8 a[PD + 1][MT];
   bf16x8 b[2][NT];
 #pragma unroll
@@ -339,35 +360,25 @@ __device__ __forceinline__ void chain_gemm(Rsrc W, Rsrc Wnext, uint32_t woff, We
   for (int n = 0; n < NT; ++n) b[0][n] = *reinterpret_cast<const bf16x8*>(brow + 32 * n * LDA);
   bf16x8 cv;
   auto put = [&](int j) __attribute__((always_inline)) {
-    const int kb = j >> 1, u = j & 1;
-    uint4 w;
-    if constexpr (kScale) {
-      const float* rs = rscale + 2 * (16 * kb + 8 * lh);
-      float v[8];
-#pragma unroll
-      for (int t = 0; t < 8; ++t) v[t] = (float)cv[t] * rs[2 * t];
-      w = make_uint4(pack_bf16(v[0], v[1]), pack_bf16(v[2], v[3]), pack_bf16(v[4], v[5]), pack_bf16(v[6], v[7]));
-      colsum[u] += ((v[0] + v[1]) + (v[2] + v[3])) + ((v[4] + v[5]) + (v[6] + v[7]));
-    } else {
-      w = __builtin_bit_cast(uint4, cv);
-    }
-    store16(dst, coff, (uint32_t)(kb * (H / 32) + u) * 1024, w);
+    *reinterpret_cast<uint4*>(reinterpret_cast<char*>(dst) + ((j >> 1) * (H / 32) + (j & 1)) * 1024 + coff) =
+        __builtin_bit_cast(uint4, cv);
   };
+  const f32x16 zero = {};
 #pragma unroll
-  for (int ks = 0; ks < KS; ++ks) {
+  for (int ks = 0; ks < N; ++ks) {
 #pragma unroll
     for (int m = 0; m < MT; ++m) {
-      if (ks + PD < KS)
-        a[(ks + PD) % (PD + 1)][m] = load_frag(W, woff, (uint32_t)(m * KS + ks + PD) * 1024);
+      if (ks + PD < N)
+        a[(ks + PD) % (PD + 1)][m] = load_frag(W, woff, (uint32_t)(m * N + ks + PD) * 1024);
       else
-        pf.a[ks + PD - KS][m] = load_frag(Wnext, woff, (uint32_t)(m * KS + ks + PD - KS) * 1024);
+        pf.a[ks + PD - N][m] = load_frag(Wnext, woff, (uint32_t)(m * N + ks + PD - N) * 1024);
     }
     if (ks + 1 < KS) {
 #pragma unroll
       for (int n = 0; n < NT; ++n)
         b[(ks + 1) & 1][n] = *reinterpret_cast<const bf16x8*>(brow + 32 * n * LDA + 16 * (ks + 1));
     }
-    if (ks % CDIV == 0) {
+    if (ks < KS && ks % CDIV == 0) {
       const int j = ks / CDIV;
       if (j > 0) put(j - 1);
       cv = copy_read<LDA>(cbase + 16 * (j >> 1) * LDA + 32 * (j & 1));
@@ -379,14 +390,25 @@ __device__ __forceinline__ void chain_gemm(Rsrc W, Rsrc Wnext, uint32_t woff, We
     for (int n = 0; n < NT; ++n)
 #pragma unroll
       for (int m = 0; m < MT; ++m)
-        acc[m][n] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[ks % (PD + 1)][m], b[ks & 1][n], acc[m][n], 0, 0, 0);
+        acc[m][n] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[ks % (PD + 1)][m], ks < KS ? b[ks & 1][n] : ones,
+                                                           ks == 0 ? zero : acc[m][n], 0, 0, 0);
     __builtin_amdgcn_sched_barrier(0);
   }
   put(C::COPIES - 1);
 }
 
+// max(a, b) of two finite values as one v_max_f32: written out so that the
+// compiler adds no NaN-quieting operation on the matrix-core results.
+__device__ __forceinline__ float vmax(float a, float b) {
+  float r;
+  asm("v_max_f32 %0, %1, %2" : "=v"(r) : "v"(a), "v"(b));
+  return r;
+}
+
 // LeakyReLU (slope in [0, 1]: max(v, s v)), bf16 rounding and the lane's sign
-// mask of one layer's outputs.  pk[mt][nt][g] = packed bf16 of q = 0,1 and 2,3.
+// mask words of one layer's outputs.  pk[mt][nt][g] = packed bf16 of q = 0,1
+// and 2,3.  The sign bits are gathered with one byte permute per group (the
+// sign of a packed bf16 is bit 7 of its high byte) and a shift-and-or.
 template <int MT, int NT>
 __device__ __forceinline__ void activate(const f32x16 (&v)[MT][NT], float slope, uint2 (&pk)[MT][NT][4],
                                          uint32_t (&m)[MT * NT / 2]) {
@@ -395,20 +417,32 @@ __device__ __forceinline__ void activate(const f32x16 (&v)[MT][NT], float slope,
 #pragma unroll
   for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-    for (int nt = 0; nt < NT; ++nt)
+    for (int nt = 0; nt < NT; ++nt) {
+      const int t = mt * NT + nt;
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
-        const int e = 16 * (mt * NT + nt) + 4 * g;
         const f32x16& x = v[mt][nt];
-        const uint32_t p01 = pack_bf16(fmaxf(x[4 * g], slope * x[4 * g]), fmaxf(x[4 * g + 1], slope * x[4 * g + 1]));
-        const uint32_t p23 = pack_bf16(fmaxf(x[4 * g + 2], slope * x[4 * g + 2]), fmaxf(x[4 * g + 3], slope * x[4 * g + 3]));
+        const uint32_t p01 = pack_bf16(vmax(x[4 * g], slope * x[4 * g]), vmax(x[4 * g + 1], slope * x[4 * g + 1]));
+        const uint32_t p23 = pack_bf16(vmax(x[4 * g + 2], slope * x[4 * g + 2]), vmax(x[4 * g + 3], slope * x[4 * g + 3]));
         pk[mt][nt][g] = make_uint2(p01, p23);
-        uint32_t& w = m[e >> 5];
-        w = (w << 1) | (uint32_t)((int32_t)(p01 << 16) > 0);
-        w = (w << 1) | (uint32_t)((int32_t)p01 >= 0x10000);
-        w = (w << 1) | (uint32_t)((int32_t)(p23 << 16) > 0);
-        w = (w << 1) | (uint32_t)((int32_t)p23 >= 0x10000);
+        // bytes: high byte of q0, q1, q2, q3 -> sign of q at bit 8 q + 7
+        const uint32_t r = __builtin_amdgcn_perm(p23, p01, 0x07050301u);
+        const int pos = g + 4 * (t & 1);
+        m[t >> 1] |= (r >> (7 - pos)) & (0x01010101u << pos);
       }
+    }
+}
+
+// All-ones where output (t, g, q) of a lane's mask words is negative.
+template <int MW>
+__device__ __forceinline__ uint32_t neg_mask(const uint32_t (&m)[MW], int t, int g, int q) {
+  return (uint32_t)__builtin_amdgcn_sbfe((int)m[t >> 1], 8 * q + g + 4 * (t & 1), 1);
+}
+
+// v times LeakyReLU' (1, or the slope where the mask is set): a bitwise
+// select, neg ? slope v : v.
+__device__ __forceinline__ float leaky_grad(float v, float slope, uint32_t neg) {
+  return __uint_as_float(__builtin_amdgcn_bitop3_b32(neg, __float_as_uint(slope * v), __float_as_uint(v), 0xCA));
 }
 
 // A lane's mask words of one layer: store and load as one vector.
@@ -418,12 +452,6 @@ __device__ __forceinline__ void store_mask(uint32_t* dst, const uint32_t (&m)[4]
 __device__ __forceinline__ void load_mask(const uint32_t* src, uint32_t (&m)[4]) {
   const uint4 v = *reinterpret_cast<const uint4*>(src);
   m[0] = v.x; m[1] = v.y; m[2] = v.z; m[3] = v.w;
-}
-
-// Bit of output e in a lane's mask (see activate).
-template <int MW>
-__device__ __forceinline__ bool mask_bit(const uint32_t (&m)[MW], int e) {
-  return (m[e >> 5] >> (31 - (e & 31))) & 1u;
 }
 
 // Writes a layer's packed outputs into the LDS tile.
@@ -439,25 +467,11 @@ __device__ __forceinline__ void store_tile(u16* act, const uint2 (&pk)[MT][NT][4
         *reinterpret_cast<uint2*>(act + (32 * nt + lr) * LDA + ow + 32 * mt + 8 * g + 4 * lh) = pk[mt][nt][g];
 }
 
-// The 32 bias values of a lane's outputs, in the accumulator arrangement.
-template <int MT>
-__device__ __forceinline__ void load_bias(const float* __restrict__ b, int ow, int lh, f32x16 (&bias)[MT]) {
-#pragma unroll
-  for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-    for (int g = 0; g < 4; ++g) {
-      const f32x4 b4 = *reinterpret_cast<const f32x4*>(b + ow + 32 * mt + 8 * g + 4 * lh);
-#pragma unroll
-      for (int q = 0; q < 4; ++q) bias[mt][4 * g + q] = b4[q];
-    }
-}
-
 struct ChainArgs {
   const float* W0;           // first layer [H][F] fp32
   const float* b0;           // [H]
-  const u16* Wb;             // hidden layers, bf16 [NH][H][H] ([out][in]), fragment order
-  const u16* WTb;            // the same, transposed ([in][out]), fragment order
-  const float* bh[kMaxNH];   // hidden biases
+  const u16* Wb;             // hidden layers, bf16, forward fragment order with the bias step
+  const u16* WTb;            // the same, transposed ([in][out]), backward fragment order
   const float* wo;           // logit layer [H]
   const float* bo;           // [1]
   float slope;
@@ -467,7 +481,7 @@ struct ChainArgs {
   const float* feat;         // [rows][F]
   const float* xs;           // [rows][D] (fake chunks)
   u16* act;                  // [NH][rows H]: A_1 .. A_NH, K-fragment order
-  u16* dlt;                  // [NH][rows H]: bf16(e_D x signal at A_2 .. A_{NH+1}), K-fragment order
+  u16* dlt;                  // [NH][rows H]: unit-seed signal at A_2 .. A_{NH+1}, K-fragment order
   uint32_t* mask;            // [NH + 1][rows / T][WAVES][64 lanes][4]: signs of A_1 .. A_{NH+1}
   float* eD;                 // [rows] dL_D/dz (0 on padding)
   float* eG;                 // [rows] dL_G/dz (fake; 0 otherwise)
@@ -475,46 +489,74 @@ struct ChainArgs {
   float* dLg_dx;             // caller's array (indexed from c.row0) or NULL
   float* plog;               // [gridDim.x][H + 3]: dW_o, then sum softplus(+-z), sum e_D
   float* pfb;                // [gridDim.x][H F + H]: dW_1, then db_1
-  float* pdb;                // [gridDim.x][NH][H]: db of the hidden layers
 };
 
 // softplus(t) = max(t, 0) + ln(1 + e^-|t|), on the hardware units.
 __device__ __forceinline__ float softplus_fast(float t) { return fmaxf(t, 0.0f) + log1p_k(fast_exp(-fabsf(t))); }
 
-// Forward chain of one chunk: A_1 (VALU, K = F) -> hidden layers (MFMA) ->
-// logit z, BCE seeds e_D and e_G, and per-workgroup partials of dW_o, db_o
-// and the loss sums.  Stores A_1 .. A_NH and the masks for later kernels.
-// Each tile's features are staged through LDS, loaded one tile ahead.
+// Forward chain of one chunk: A_1 (fp32 matrix cores, K = F + 1) -> hidden
+// layers -> logit z, BCE seeds e_D and e_G, and per-workgroup partials of
+// dW_o, db_o and the loss sums.  Stores A_1 .. A_NH and the masks for later
+// kernels.  Each tile's features are staged through LDS, loaded one tile
+// ahead.
 template <int H, int F>
 __global__ __launch_bounds__(Chain<H>::THREADS, Chain<H>::BPC) void k_fwd_chain(ChainArgs p) {
   using C = Chain<H>;
   constexpr int T = C::T, LDA = C::LDA, WAVES = C::WAVES, MT = C::MT, NT = C::NT, MW = C::MW, NTH = C::THREADS;
   constexpr int FU = (T * F + NTH - 1) / NTH;   // staged feature values per thread
+  constexpr int K1 = (F + 2) / 2;               // first-layer K steps of 2 (features, then the bias)
   __shared__ __attribute__((aligned(16))) u16 act[T * LDA];
-  __shared__ float sW0[H * (F + 1)];            // row o: W0[o][0 .. F-1], b0[o]
   __shared__ float sfeat[T * F];
   __shared__ float zpart[WAVES][T];
   __shared__ float se_s[T];
-  __shared__ __attribute__((aligned(16))) float swo[H];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int lr = lane & 31, lh = lane >> 5;
   const int ow = 32 * MT * wave;
-  const uint32_t woff = ((uint32_t)(2 * wave * C::KS * 64 + lane)) * 16;
+  const uint32_t woff = weight_offset<H, true>(wave, lane);
   const uint32_t coff = ((uint32_t)(2 * wave * 64 + lane)) * 16;
   const ChunkArgs c = p.c;
   const int64_t rstride = (int64_t)c.rows;
   const int ntiles = c.rows / T;
   const float slope = p.slope;
-  for (int k = tid; k < H * F; k += NTH) sW0[(k / F) * (F + 1) + k % F] = p.W0[k];
-  for (int k = tid; k < H; k += NTH) {
-    sW0[k * (F + 1) + F] = p.b0[k];
-    swo[k] = p.wo[k];
-  }
+  // first-layer A fragments (v_mfma_f32_32x32x2f32: lane l holds row l % 32,
+  // K index l / 32 of each step): W0 columns, then b0, then zero
+  float w0f[MT][K1];
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+    for (int s = 0; s < K1; ++s) {
+      const int o = ow + 32 * mt + lr, k = 2 * s + lh;
+      w0f[mt][s] = k < F ? p.W0[o * F + k] : (k == F ? p.b0[o] : 0.f);
+    }
+  // logit A fragments: rows 0..2 are the bf16 terms hi, mid, lo of w_o (their
+  // sum is w_o exactly), other rows zero; the K order matches the lane's
+  // activations (see the logit below)
+  bf16x8 wof[MT][2];
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+    for (int s = 0; s < 2; ++s) {
+      uint32_t w[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        uint32_t h2[2];
+#pragma unroll
+        for (int e = 0; e < 2; ++e) {
+          const int i = 2 * u + e;
+          const int f = ow + 32 * mt + 16 * s + (i < 4 ? 4 * lh + i : 8 + 4 * lh + i - 4);
+          uint32_t lo;
+          const uint32_t hm = bias_terms(p.wo[f], lo);
+          h2[e] = lr == 0 ? (hm & 0xffffu) : lr == 1 ? (hm >> 16) : lr == 2 ? lo : 0u;
+        }
+        w[u] = h2[0] | (h2[1] << 16);
+      }
+      wof[mt][s] = __builtin_bit_cast(bf16x8, make_uint4(w[0], w[1], w[2], w[3]));
+    }
   float dwo = 0.f;                              // dW_o partial of feature tid
   const float bo = p.bo[0];
   float l0 = 0.f, l1 = 0.f, se = 0.f;           // loss and e_D sums of event tid (tid < T)
   WeightPrefetch<H> pf;
-  prefetch_weights<H>(weight_rsrc<H>(p.Wb, 0), pf, woff);
+  prefetch_weights<H, true>(weight_rsrc<H, true>(p.Wb, 0), pf, woff);
   float fst[FU];
   auto load_feat = [&](int tile) __attribute__((always_inline)) {
 #pragma unroll
@@ -524,6 +566,7 @@ __global__ __launch_bounds__(Chain<H>::THREADS, Chain<H>::BPC) void k_fwd_chain(
     }
   };
   if ((int)blockIdx.x < ntiles) load_feat(blockIdx.x);
+  const f32x16 zero = {};
 
   for (int tile = blockIdx.x; tile < ntiles; tile += gridDim.x) {
     const int r0 = tile * T;
@@ -538,39 +581,31 @@ __global__ __launch_bounds__(Chain<H>::THREADS, Chain<H>::BPC) void k_fwd_chain(
     };
     __syncthreads();                              // sfeat staged; last tile's readers of act are done
 
-    // ---- first layer (VALU, K = F) in the MFMA output arrangement ----------
-    f32x16 bias[MT];
+    // ---- first layer on the fp32 matrix cores ------------------------------
     {
-      float f[NT][F];
+      float fb[NT][K1];                           // B: feature l / 32 + 2 s of event 32 nt + l % 32, then 1
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt)
 #pragma unroll
-        for (int k = 0; k < F; ++k) f[nt][k] = sfeat[(32 * nt + lr) * F + k];
+        for (int s = 0; s < K1; ++s) {
+          const int k = 2 * s + lh;
+          fb[nt][s] = k < F ? sfeat[(32 * nt + lr) * F + k] : (k == F ? 1.f : 0.f);
+        }
       f32x16 v[MT][NT];
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-        for (int g = 0; g < 4; ++g)
+        for (int nt = 0; nt < NT; ++nt) {
+          v[mt][nt] = __builtin_amdgcn_mfma_f32_32x32x2f32(w0f[mt][0], fb[nt][0], zero, 0, 0, 0);
 #pragma unroll
-          for (int q = 0; q < 4; ++q) {
-            const float* w = &sW0[(ow + 32 * mt + 8 * g + 4 * lh + q) * (F + 1)];
-            float wr[F + 1];
-#pragma unroll
-            for (int k = 0; k <= F; ++k) wr[k] = w[k];
-#pragma unroll
-            for (int nt = 0; nt < NT; ++nt) {
-              float t = wr[F];
-#pragma unroll
-              for (int k = 0; k < F; ++k) t = fmaf(wr[k], f[nt][k], t);
-              v[mt][nt][4 * g + q] = t;
-            }
-          }
+          for (int s = 1; s < K1; ++s)
+            v[mt][nt] = __builtin_amdgcn_mfma_f32_32x32x2f32(w0f[mt][s], fb[nt][s], v[mt][nt], 0, 0, 0);
+        }
       uint2 pk[MT][NT][4];
       uint32_t m[MW];
       activate<MT, NT>(v, slope, pk, m);
       store_mask(mask_at(0), m);
       store_tile<MT, NT, LDA>(act, pk, ow, lane);
-      load_bias<MT>(p.bh[0], ow, lh, bias);
     }
     __syncthreads();
 
@@ -580,11 +615,8 @@ __global__ __launch_bounds__(Chain<H>::THREADS, Chain<H>::BPC) void k_fwd_chain(
       f32x16 acc[MT][NT];
       // the product also writes its input A_{l+1} to HBM; the next product is
       // layer l + 1, or the first hidden layer of the next tile
-      float unused[2];
-      chain_gemm<H, false>(weight_rsrc<H>(p.Wb, l), weight_rsrc<H>(p.Wb, last ? 0 : l + 1), woff, pf, act, acc, bias,
-                           lane, wave, make_rsrc(p.act + ((int64_t)l * rstride + r0) * H, T * H * 2), coff, nullptr,
-                           unused);
-      if (!last) load_bias<MT>(p.bh[l + 1], ow, lh, bias);
+      chain_gemm<H, true>(weight_rsrc<H, true>(p.Wb, l), weight_rsrc<H, true>(p.Wb, last ? 0 : l + 1), woff, pf,
+                          act, acc, lane, wave, p.act + ((int64_t)l * rstride + r0) * H, coff);
       uint2 pk[MT][NT][4];
       uint32_t m[MW];
       activate<MT, NT>(acc, slope, pk, m);
@@ -595,22 +627,25 @@ __global__ __launch_bounds__(Chain<H>::THREADS, Chain<H>::BPC) void k_fwd_chain(
         __syncthreads();
         continue;
       }
-      // ---- logit layer and BCE seeds (fp32 dot over the bf16 activations) --
+      // ---- logit layer: z = w_o . A_{NH+1} + b_o on the matrix cores -------
+      // The lane's activations of tile (mt, nt), groups 2 s and 2 s + 1, are a
+      // B fragment (K = 16 features 32 mt + 16 s .. + 15 of the wave, in the
+      // order 4 h + 0..3, 8 + 4 h + 0..3 for lane half h) of event 32 nt + l % 32;
+      // row m < 3 of the product is the event's dot with term m of w_o.
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt) {
-        float s = 0.f;
+        f32x16 zacc = zero;
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-          for (int g = 0; g < 4; ++g) {
-            const f32x4 w4 = *reinterpret_cast<const f32x4*>(&swo[ow + 32 * mt + 8 * g + 4 * lh]);
-            s = fmaf(lo_bf16(pk[mt][nt][g].x), w4[0], s);
-            s = fmaf(hi_bf16(pk[mt][nt][g].x), w4[1], s);
-            s = fmaf(lo_bf16(pk[mt][nt][g].y), w4[2], s);
-            s = fmaf(hi_bf16(pk[mt][nt][g].y), w4[3], s);
+          for (int s = 0; s < 2; ++s) {
+            const bf16x8 bfr = __builtin_bit_cast(
+                bf16x8, make_uint4(pk[mt][nt][2 * s].x, pk[mt][nt][2 * s].y, pk[mt][nt][2 * s + 1].x,
+                                   pk[mt][nt][2 * s + 1].y));
+            zacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wof[mt][s], bfr, zacc, 0, 0, 0);
           }
-        s += __shfl_xor(s, 32, 64);
-        if (lh == 0) zpart[wave][32 * nt + lr] = s;
+        // rows 0, 1, 2 of column l % 32 sit in registers 0, 1, 2 of lane half 0
+        if (lh == 0) zpart[wave][32 * nt + lr] = (zacc[0] + zacc[1]) + zacc[2];
       }
       __syncthreads();                               // zpart complete; every wave is done reading act
       store_tile<MT, NT, LDA>(act, pk, ow, lane);    // A_{NH+1}, for dW_o
@@ -695,7 +730,7 @@ __global__ __launch_bounds__(Chain<H>::THREADS, Chain<H>::BPC) void k_bwd_chain(
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int lh = lane >> 5;
   const int ow = 32 * MT * wave;
-  const uint32_t woff = ((uint32_t)(2 * wave * C::KS * 64 + lane)) * 16;
+  const uint32_t woff = weight_offset<H, false>(wave, lane);
   const uint32_t coff = ((uint32_t)(2 * wave * 64 + lane)) * 16;
   const ChunkArgs c = p.c;
   const int64_t rstride = (int64_t)c.rows;
@@ -705,15 +740,11 @@ __global__ __launch_bounds__(Chain<H>::THREADS, Chain<H>::BPC) void k_bwd_chain(
   float adw[F + 1];                       // dW_1 row tid, then db_1[tid]
 #pragma unroll
   for (int k = 0; k <= F; ++k) adw[k] = 0.f;
-  float adb[kMaxNH][2];                   // db partials: column 32 (2 wave + u) + lane % 32, lane-half rows
-#pragma unroll
-  for (int k = 0; k < kMaxNH; ++k) adb[k][0] = adb[k][1] = 0.f;
   const bool want_dx = c.fake && p.dLg_dx != nullptr;
   const float slope = p.slope;
   const int NH = p.NH;
-  const f32x16 none[MT] = {};
   WeightPrefetch<H> pf;
-  prefetch_weights<H>(weight_rsrc<H>(p.WTb, NH - 1), pf, woff);
+  prefetch_weights<H, false>(weight_rsrc<H, false>(p.WTb, NH - 1), pf, woff);
   auto mask_at = [&](int layer, int tile) __attribute__((always_inline)) {
     return p.mask + ((((int64_t)layer * ntiles + tile) * WAVES + wave) * 64 + lane) * MW;
   };
@@ -736,6 +767,7 @@ __global__ __launch_bounds__(Chain<H>::THREADS, Chain<H>::BPC) void k_bwd_chain(
     load_rows(blockIdx.x);
     load_mask(mask_at(NH, blockIdx.x), mtop);
   }
+  __syncthreads();                              // swo staged
 
   for (int tile = blockIdx.x; tile < ntiles; tile += gridDim.x) {
     const int r0 = tile * T;
@@ -756,10 +788,10 @@ __global__ __launch_bounds__(Chain<H>::THREADS, Chain<H>::BPC) void k_bwd_chain(
           const f32x4 w4 = *reinterpret_cast<const f32x4*>(&swo[ow + 32 * mt + 8 * g + 4 * lh]);
 #pragma unroll
           for (int nt = 0; nt < NT; ++nt) {
-            const int e = 16 * (mt * NT + nt) + 4 * g;
+            const int t = mt * NT + nt;
             float d[4];
 #pragma unroll
-            for (int q = 0; q < 4; ++q) d[q] = mask_bit(mtop, e + q) ? w4[q] : w4[q] * slope;
+            for (int q = 0; q < 4; ++q) d[q] = leaky_grad(w4[q], slope, neg_mask(mtop, t, g, q));
             pk[mt][nt][g] = make_uint2(pack_bf16(d[0], d[1]), pack_bf16(d[2], d[3]));
           }
         }
@@ -772,19 +804,10 @@ __global__ __launch_bounds__(Chain<H>::THREADS, Chain<H>::BPC) void k_bwd_chain(
       load_mask(mask_at(l, tile), m);
       if (l == 0 && next < ntiles) load_mask(mask_at(NH, next), mtop);
       f32x16 acc[MT][NT];
-      // the product also writes its input (the signal at A_{l+2}) to HBM and
-      // sums e_D times it per column (db of hidden layer l); the next product
-      // is layer l - 1, or the top layer of the next tile
-      float colsum[2] = {0.f, 0.f};
-      chain_gemm<H, true>(weight_rsrc<H>(p.WTb, l), weight_rsrc<H>(p.WTb, l > 0 ? l - 1 : NH - 1), woff, pf, act,
-                          acc, none, lane, wave, make_rsrc(p.dlt + ((int64_t)l * rstride + r0) * H, T * H * 2), coff,
-                          se, colsum);
-#pragma unroll
-      for (int k = 0; k < kMaxNH; ++k)
-        if (k == l) {
-          adb[k][0] += colsum[0];
-          adb[k][1] += colsum[1];
-        }
+      // the product also writes its input (the signal at A_{l+2}) to HBM; the
+      // next product is layer l - 1, or the top layer of the next tile
+      chain_gemm<H, false>(weight_rsrc<H, false>(p.WTb, l), weight_rsrc<H, false>(p.WTb, l > 0 ? l - 1 : NH - 1), woff,
+                           pf, act, acc, lane, wave, p.dlt + ((int64_t)l * rstride + r0) * H, coff);
       uint2 pk[MT][NT][4];
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt)
@@ -792,13 +815,10 @@ __global__ __launch_bounds__(Chain<H>::THREADS, Chain<H>::BPC) void k_bwd_chain(
         for (int nt = 0; nt < NT; ++nt)
 #pragma unroll
           for (int g = 0; g < 4; ++g) {
-            const int e = 16 * (mt * NT + nt) + 4 * g;
+            const int t = mt * NT + nt;
             float d[4];
 #pragma unroll
-            for (int q = 0; q < 4; ++q) {
-              const float v = acc[mt][nt][4 * g + q];
-              d[q] = mask_bit(m, e + q) ? v : v * slope;
-            }
+            for (int q = 0; q < 4; ++q) d[q] = leaky_grad(acc[mt][nt][4 * g + q], slope, neg_mask(m, t, g, q));
             pk[mt][nt][g] = make_uint2(pack_bf16(d[0], d[1]), pack_bf16(d[2], d[3]));
           }
       __syncthreads();                               // every wave is done reading this layer's input
@@ -862,48 +882,46 @@ __global__ __launch_bounds__(Chain<H>::THREADS, Chain<H>::BPC) void k_bwd_chain(
     __syncthreads();                                 // before the next tile overwrites act and the staged rows
   }
 
-  // ---- per-workgroup partials of dW_1, db_1 and the hidden db --------------
+  // ---- per-workgroup partials of dW_1 and db_1 ------------------------------
   float* dst = p.pfb + (int64_t)blockIdx.x * (H * F + H);
-  float* dbd = p.pdb + (int64_t)blockIdx.x * NH * H;
 #pragma unroll
   for (int j = 0; j < F; ++j) dst[tid * F + j] = adw[j];
   dst[H * F + tid] = adw[F];
-#pragma unroll
-  for (int k = 0; k < kMaxNH; ++k)
-#pragma unroll
-    for (int u = 0; u < 2; ++u) {
-      const float v = adb[k][u] + __shfl_xor(adb[k][u], 32, 64);   // both row halves of the column
-      if (k < NH && lane < 32) dbd[k * H + 32 * (2 * wave + u) + lane] = v;
-    }
 }
 
 // ---------------------------------------------------------------------------
 // Weight-gradient partial of one hidden layer over a slice of rows:
 //   P[slice][o][i] = sum_rows bf16(e_D delta)[r][o] A[r][i]
-// for one 256 x 256 tile (o0, i0) of the H x H gradient.  Both operands come
-// in K-fragment order, so every fragment is a contiguous kilobyte read from
-// global memory and no LDS is needed; the kernel streams each operand row of
-// its tile once and is bound by HBM.  Wave w owns rows o0 + 64 w .. + 63 (two
-// 32-row MFMA tiles) and all 256 columns (eight), i.e. 16 accumulators of
-// 32 x 32 in the accumulation registers; fragments are loaded PD K steps
-// ahead, with the step loop unrolled by PD + 1 so that every register slot
-// index is a constant.
+// for one 256 x 256 tile (o0, i0) of the H x H gradient, and in the tiles with
+// i0 = 0 the hidden-layer db partial Pdb[slice][o] = sum_rows (e_D delta)[r][o]
+// (fp32, before the rounding).  delta (the unit-seed signal) and A come in
+// K-fragment order, so every fragment is a contiguous kilobyte read from
+// global memory and no LDS is needed; each delta fragment is scaled by the e_D
+// of its 8 rows and rounded to bf16 in registers.  The kernel streams each
+// operand row of its tile once and is bound by HBM.  Wave w owns rows
+// o0 + 64 w .. + 63 (two 32-row MFMA tiles) and all 256 columns (eight), i.e.
+// 16 accumulators of 32 x 32 in the accumulation registers; fragments are
+// loaded PD K steps ahead, with the step loop unrolled by PD + 1 so that every
+// register slot index is a constant.
 constexpr int kWT = 256;     // weight-gradient tile edge
 
 template <int H>
 __global__ __launch_bounds__(256, 1) void k_wgrad(const u16* __restrict__ dsc, const u16* __restrict__ A,
-                                                  int kb_per_slice, int kb_total, float* __restrict__ P) {
+                                                  const float* __restrict__ eD, int kb_per_slice, int kb_total,
+                                                  float* __restrict__ P, float* __restrict__ Pdb) {
   constexpr int TI = H / kWT;     // tiles per dimension
   constexpr int CB = H / 32;      // 32-column blocks
-  constexpr int PD = 3;
+  constexpr int PD = 2;
   const int tile = blockIdx.x % (TI * TI), slice = blockIdx.x / (TI * TI);
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lr = lane & 31, lh = lane >> 5;
   const int ob = (tile / TI) * (kWT / 32) + 2 * wave;   // the wave's first 32-row block
   const int ib = (tile % TI) * (kWT / 32);              // the tile's first 32-column block
   const int kb0 = slice * kb_per_slice;
   const int nk = max(0, min(kb_total, kb0 + kb_per_slice) - kb0);
   const u16* pa = dsc + (((size_t)kb0 * CB + ob) * 64 + lane) * 8;
   const u16* pb = A + (((size_t)kb0 * CB + ib) * 64 + lane) * 8;
+  const float* pe = eD + (size_t)kb0 * 16 + 8 * lh;    // rows of the lane's half of each K block
   constexpr size_t KSTRIDE = (size_t)CB * 512;          // bf16 per K block
   f32x16 acc[2][8];
 #pragma unroll
@@ -912,12 +930,16 @@ __global__ __launch_bounds__(256, 1) void k_wgrad(const u16* __restrict__ dsc, c
     for (int n = 0; n < 8; ++n)
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[m][n][r] = 0.f;
+  float dbs[2] = {0.f, 0.f};
   bf16x8 fa[PD + 1][2], fb[PD + 1][8];
+  f32x4 fe[PD + 1][2];
   auto load = [&](int slot, int k) __attribute__((always_inline)) {
 #pragma unroll
     for (int m = 0; m < 2; ++m) fa[slot][m] = *reinterpret_cast<const bf16x8*>(pa + k * KSTRIDE + m * 512);
 #pragma unroll
     for (int n = 0; n < 8; ++n) fb[slot][n] = *reinterpret_cast<const bf16x8*>(pb + k * KSTRIDE + n * 512);
+    fe[slot][0] = *reinterpret_cast<const f32x4*>(pe + (size_t)k * 16);
+    fe[slot][1] = *reinterpret_cast<const f32x4*>(pe + (size_t)k * 16 + 4);
   };
 #pragma unroll
   for (int q = 0; q < PD; ++q)
@@ -929,17 +951,26 @@ __global__ __launch_bounds__(256, 1) void k_wgrad(const u16* __restrict__ dsc, c
       if (k < nk) {
         if (k + PD < nk) load((q + PD) % (PD + 1), k + PD);
         __builtin_amdgcn_sched_barrier(0);
+        bf16x8 sa[2];
+#pragma unroll
+        for (int m = 0; m < 2; ++m) {
+          float v[8];
+#pragma unroll
+          for (int t = 0; t < 8; ++t) v[t] = (float)fa[q][m][t] * fe[q][t >> 2][t & 3];
+          dbs[m] += ((v[0] + v[1]) + (v[2] + v[3])) + ((v[4] + v[5]) + (v[6] + v[7]));
+          sa[m] = __builtin_bit_cast(bf16x8, make_uint4(pack_bf16(v[0], v[1]), pack_bf16(v[2], v[3]),
+                                                        pack_bf16(v[4], v[5]), pack_bf16(v[6], v[7])));
+        }
 #pragma unroll
         for (int n = 0; n < 8; ++n)
 #pragma unroll
           for (int m = 0; m < 2; ++m)
-            acc[m][n] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[q][m], fb[q][n], acc[m][n], 0, 0, 0);
+            acc[m][n] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(sa[m], fb[q][n], acc[m][n], 0, 0, 0);
         __builtin_amdgcn_sched_barrier(0);
       }
     }
   }
   float* out = P + (size_t)slice * H * H;
-  const int lr = lane & 31, lh = lane >> 5;
 #pragma unroll
   for (int m = 0; m < 2; ++m)
 #pragma unroll
@@ -949,6 +980,13 @@ __global__ __launch_bounds__(256, 1) void k_wgrad(const u16* __restrict__ dsc, c
         const int o = (ob + m) * 32 + 8 * (r / 4) + 4 * lh + (r % 4), i = (ib + n) * 32 + lr;
         out[(size_t)o * H + i] = acc[m][n][r];
       }
+  if (tile % TI == 0) {
+#pragma unroll
+    for (int m = 0; m < 2; ++m) {
+      const float v = dbs[m] + __shfl_xor(dbs[m], 32, 64);   // both row halves of the column
+      if (lh == 0) Pdb[(size_t)slice * H + 32 * (ob + m) + lr] = v;
+    }
+  }
 }
 
 // acc[e] (+)= sum_k part[k][e], k = 0..n-1, in a fixed order (S contiguous
@@ -1028,7 +1066,7 @@ struct Plan {
   int blocks;            // workgroups of the chain kernels
   int slices;            // weight-gradient slices per chunk
   size_t off_wb, off_wtb, off_feat, off_xs, off_act, off_dlt, off_mask, off_eD, off_eG, off_plog, off_pfb, off_pw,
-      off_pdb, off_accl, total;
+      off_pwdb, off_accl, total;
 };
 
 int pad128(int64_t n) { return (int)((n + 127) / 128 * 128); }
@@ -1048,7 +1086,7 @@ Plan make_plan(const DiscArgs& a, int n_cu) {
   p.slices = std::max(1, n_cu / tiles);  // one weight-gradient workgroup per CU
   const size_t H = p.H, R = p.rows_max, NH = p.NH;
   size_t o = 0;
-  p.off_wb = o; o += al(2 * H * H * NH);
+  p.off_wb = o; o += al(2 * H * (H + 16) * NH);     // forward copies carry one bias step per 32 rows
   p.off_wtb = o; o += al(2 * H * H * NH);
   p.off_feat = o; o += al(4 * R * p.F);
   p.off_xs = o; o += al(4 * R * p.D);
@@ -1060,7 +1098,7 @@ Plan make_plan(const DiscArgs& a, int n_cu) {
   p.off_plog = o; o += al(4 * (size_t)p.blocks * (H + 3));
   p.off_pfb = o; o += al(4 * (size_t)p.blocks * (H * p.F + H));
   p.off_pw = o; o += al(4 * (size_t)p.slices * H * H);
-  p.off_pdb = o; o += al(4 * (size_t)p.blocks * NH * H);
+  p.off_pwdb = o; o += al(4 * (size_t)p.slices * H);
   p.off_accl = o; o += al(4 * 4);
   p.total = o;
   return p;
@@ -1120,8 +1158,8 @@ hipError_t launch_disc_bf16(const DiscArgs& a, void* ws, int n_cu, hipStream_t s
 
   if (tm) tm->begin("disc_bf16_weights");
   for (int l = 0; l < NH; ++l)
-    hipLaunchKernelGGL(k_weights_frag, dim3((H * H / 8 + 255) / 256), dim3(256), 0, st, Dm.W[1 + l],
-                       Wb + (size_t)l * H * H, WTb + (size_t)l * H * H, H);
+    hipLaunchKernelGGL(k_weights_frag, dim3(((H / 32) * (H / 16 + 1) * 64 + 255) / 256), dim3(256), 0, st, Dm.W[1 + l],
+                       Dm.b[1 + l], Wb + (size_t)l * H * (H + 16), WTb + (size_t)l * H * H, H);
   if (tm) tm->end();
 
   SourceArgs src{};
@@ -1133,7 +1171,6 @@ hipError_t launch_disc_bf16(const DiscArgs& a, void* ws, int n_cu, hipStream_t s
   ca.b0 = Dm.b[0];
   ca.Wb = Wb;
   ca.WTb = WTb;
-  for (int l = 0; l < NH; ++l) ca.bh[l] = Dm.b[1 + l];
   ca.wo = Dm.W[NH + 1];
   ca.bo = Dm.b[NH + 1];
   ca.slope = Dm.leaky_slope;
@@ -1147,7 +1184,6 @@ hipError_t launch_disc_bf16(const DiscArgs& a, void* ws, int n_cu, hipStream_t s
   ca.eG = F32(p.off_eG);
   ca.plog = F32(p.off_plog);
   ca.pfb = F32(p.off_pfb);
-  ca.pdb = F32(p.off_pdb);
 
   int chunk_index = 0;
   float* lacc = F32(p.off_accl);
@@ -1193,16 +1229,16 @@ hipError_t launch_disc_bf16(const DiscArgs& a, void* ws, int n_cu, hipStream_t s
         const size_t bst = (size_t)c.rows * H;   // stride between this chunk's per-layer buffers
         for (int l = 0; l < NH; ++l) {
           // hidden layer l maps A_{l+1} -> A_{l+2}: operands A_{l+1} and the signal at A_{l+2}
-          accumulate(ca.pdb + (size_t)l * H, nb, (int64_t)NH * H, (int64_t)H, out.db[1 + l], first, st);
           if (tm) tm->begin("bf16_wgrad");
           if (H == 256)
             hipLaunchKernelGGL(k_wgrad<256>, dim3(tiles * p.slices), dim3(256), 0, st, ca.dlt + l * bst,
-                               ca.act + l * bst, kb_per_slice, kb_total, F32(p.off_pw));
+                               ca.act + l * bst, ca.eD, kb_per_slice, kb_total, F32(p.off_pw), F32(p.off_pwdb));
           else
             hipLaunchKernelGGL(k_wgrad<512>, dim3(tiles * p.slices), dim3(256), 0, st, ca.dlt + l * bst,
-                               ca.act + l * bst, kb_per_slice, kb_total, F32(p.off_pw));
+                               ca.act + l * bst, ca.eD, kb_per_slice, kb_total, F32(p.off_pw), F32(p.off_pwdb));
           if (tm) tm->end();
           accumulate(F32(p.off_pw), p.slices, (int64_t)H * H, (int64_t)H * H, out.dW[1 + l], first, st);
+          accumulate(F32(p.off_pwdb), p.slices, (int64_t)H, (int64_t)H, out.db[1 + l], first, st);
         }
       }
       hipError_t e = hipGetLastError();
