@@ -896,48 +896,73 @@ __global__ __launch_bounds__(Chain<H>::THREADS, Chain<H>::BPC) void k_bwd_chain(
 // i0 = 0 the hidden-layer db partial Pdb[slice][o] = sum_rows (e_D delta)[r][o]
 // (fp32, before the rounding).  delta (the unit-seed signal) and A come in
 // K-fragment order, so every fragment is a contiguous kilobyte read from
-// global memory and no LDS is needed; each delta fragment is scaled by the e_D
-// of its 8 rows and rounded to bf16 in registers.  The kernel streams each
-// operand row of its tile once and is bound by HBM.  Wave w owns rows
-// o0 + 64 w .. + 63 (two 32-row MFMA tiles) and all 256 columns (eight), i.e.
-// 16 accumulators of 32 x 32 in the accumulation registers; fragments are
-// loaded PD K steps ahead, with the step loop unrolled by PD + 1 so that every
-// register slot index is a constant.
+// global memory straight into registers; each delta fragment is scaled by the
+// e_D of its 8 rows and rounded to bf16 in registers.  The kernel streams each
+// operand row of its tile once and is bound by HBM.  Each wave holds 16
+// accumulators of 32 x 32 in the accumulation registers; fragments are loaded
+// PD K steps ahead, with the step loop unrolled by PD + 1 so that every
+// register slot index is a constant.  (Staging the fragments through LDS with
+// direct global-to-LDS loads, shared by the four waves, measured slower.)
 constexpr int kWT = 256;     // weight-gradient tile edge
 
+// Waves of a weight-gradient workgroup: WM along the output rows o, WN along
+// the input columns i, each owning a (256 / WM) x (256 / WN) block, with
+// fragments loaded PD K steps ahead (measured best per width; four waves, one
+// per SIMD).
+template <int H> struct WgradCfg;
+template <> struct WgradCfg<256> { static constexpr int WM = 2, WN = 2, PD = 3; };
+template <> struct WgradCfg<512> { static constexpr int WM = 4, WN = 1, PD = 2; };
+constexpr int kWThreads = 256;
+
 template <int H>
-__global__ __launch_bounds__(256, 1) void k_wgrad(const u16* __restrict__ dsc, const u16* __restrict__ A,
-                                                  const float* __restrict__ eD, int kb_per_slice, int kb_total,
-                                                  float* __restrict__ P, float* __restrict__ Pdb) {
+__global__ __launch_bounds__(kWThreads, 1) void k_wgrad(const u16* __restrict__ dsc, const u16* __restrict__ A,
+                                                        const float* __restrict__ eD, int kb_per_slice, int kb_total,
+                                                        float* __restrict__ P, float* __restrict__ Pdb, int xcd_map) {
   constexpr int TI = H / kWT;     // tiles per dimension
   constexpr int CB = H / 32;      // 32-column blocks
-  constexpr int PD = 2;
-  const int tile = blockIdx.x % (TI * TI), slice = blockIdx.x / (TI * TI);
+  constexpr int kWM = WgradCfg<H>::WM, kWN = WgradCfg<H>::WN, PD = WgradCfg<H>::PD;
+  static_assert(64 * kWM * kWN == kWThreads, "weight-gradient waves");
+  constexpr int FM = kWT / 32 / kWM, FN = kWT / 32 / kWN;   // 32-row / 32-column fragments per wave
+  // Workgroups are dealt to the 8 XCDs round-robin by index; with xcd_map the
+  // TI x TI tiles of a row slice share an XCD (and its L2), so the operand rows
+  // that two tiles of a slice both read come from HBM once.
+  int tile, slice;
+  if (xcd_map) {
+    const int x = blockIdx.x % 8, r = blockIdx.x / 8;
+    tile = r % (TI * TI);
+    slice = (r / (TI * TI)) * 8 + x;
+  } else {
+    tile = blockIdx.x % (TI * TI);
+    slice = blockIdx.x / (TI * TI);
+  }
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int lr = lane & 31, lh = lane >> 5;
-  const int ob = (tile / TI) * (kWT / 32) + 2 * wave;   // the wave's first 32-row block
-  const int ib = (tile % TI) * (kWT / 32);              // the tile's first 32-column block
+  const int wm = wave / kWN, wn = wave % kWN;
+  const int ob = (tile / TI) * (kWT / 32) + FM * wm;    // the wave's first 32-row block
+  const int ib = (tile % TI) * (kWT / 32) + FN * wn;    // the wave's first 32-column block
   const int kb0 = slice * kb_per_slice;
   const int nk = max(0, min(kb_total, kb0 + kb_per_slice) - kb0);
   const u16* pa = dsc + (((size_t)kb0 * CB + ob) * 64 + lane) * 8;
   const u16* pb = A + (((size_t)kb0 * CB + ib) * 64 + lane) * 8;
   const float* pe = eD + (size_t)kb0 * 16 + 8 * lh;    // rows of the lane's half of each K block
   constexpr size_t KSTRIDE = (size_t)CB * 512;          // bf16 per K block
-  f32x16 acc[2][8];
+  f32x16 acc[FM][FN];
 #pragma unroll
-  for (int m = 0; m < 2; ++m)
+  for (int m = 0; m < FM; ++m)
 #pragma unroll
-    for (int n = 0; n < 8; ++n)
+    for (int n = 0; n < FN; ++n)
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[m][n][r] = 0.f;
-  float dbs[2] = {0.f, 0.f};
-  bf16x8 fa[PD + 1][2], fb[PD + 1][8];
+  float dbs[FM];
+#pragma unroll
+  for (int m = 0; m < FM; ++m) dbs[m] = 0.f;
+  bf16x8 fa[PD + 1][FM], fb[PD + 1][FN];
   f32x4 fe[PD + 1][2];
   auto load = [&](int slot, int k) __attribute__((always_inline)) {
 #pragma unroll
-    for (int m = 0; m < 2; ++m) fa[slot][m] = *reinterpret_cast<const bf16x8*>(pa + k * KSTRIDE + m * 512);
+    for (int m = 0; m < FM; ++m) fa[slot][m] = *reinterpret_cast<const bf16x8*>(pa + k * KSTRIDE + m * 512);
 #pragma unroll
-    for (int n = 0; n < 8; ++n) fb[slot][n] = *reinterpret_cast<const bf16x8*>(pb + k * KSTRIDE + n * 512);
+    for (int n = 0; n < FN; ++n) fb[slot][n] = *reinterpret_cast<const bf16x8*>(pb + k * KSTRIDE + n * 512);
     fe[slot][0] = *reinterpret_cast<const f32x4*>(pe + (size_t)k * 16);
     fe[slot][1] = *reinterpret_cast<const f32x4*>(pe + (size_t)k * 16 + 4);
   };
@@ -951,9 +976,9 @@ __global__ __launch_bounds__(256, 1) void k_wgrad(const u16* __restrict__ dsc, c
       if (k < nk) {
         if (k + PD < nk) load((q + PD) % (PD + 1), k + PD);
         __builtin_amdgcn_sched_barrier(0);
-        bf16x8 sa[2];
+        bf16x8 sa[FM];
 #pragma unroll
-        for (int m = 0; m < 2; ++m) {
+        for (int m = 0; m < FM; ++m) {
           float v[8];
 #pragma unroll
           for (int t = 0; t < 8; ++t) v[t] = (float)fa[q][m][t] * fe[q][t >> 2][t & 3];
@@ -962,9 +987,9 @@ __global__ __launch_bounds__(256, 1) void k_wgrad(const u16* __restrict__ dsc, c
                                                         pack_bf16(v[4], v[5]), pack_bf16(v[6], v[7])));
         }
 #pragma unroll
-        for (int n = 0; n < 8; ++n)
+        for (int n = 0; n < FN; ++n)
 #pragma unroll
-          for (int m = 0; m < 2; ++m)
+          for (int m = 0; m < FM; ++m)
             acc[m][n] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(sa[m], fb[q][n], acc[m][n], 0, 0, 0);
         __builtin_amdgcn_sched_barrier(0);
       }
@@ -972,17 +997,17 @@ __global__ __launch_bounds__(256, 1) void k_wgrad(const u16* __restrict__ dsc, c
   }
   float* out = P + (size_t)slice * H * H;
 #pragma unroll
-  for (int m = 0; m < 2; ++m)
+  for (int m = 0; m < FM; ++m)
 #pragma unroll
-    for (int n = 0; n < 8; ++n)
+    for (int n = 0; n < FN; ++n)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int o = (ob + m) * 32 + 8 * (r / 4) + 4 * lh + (r % 4), i = (ib + n) * 32 + lr;
         out[(size_t)o * H + i] = acc[m][n][r];
       }
-  if (tile % TI == 0) {
+  if (tile % TI == 0 && wn == 0) {
 #pragma unroll
-    for (int m = 0; m < 2; ++m) {
+    for (int m = 0; m < FM; ++m) {
       const float v = dbs[m] + __shfl_xor(dbs[m], 32, 64);   // both row halves of the column
       if (lh == 0) Pdb[(size_t)slice * H + 32 * (ob + m) + lr] = v;
     }
@@ -1224,6 +1249,7 @@ hipError_t launch_disc_bf16(const DiscArgs& a, void* ws, int n_cu, hipStream_t s
         accumulate(ca.pfb, nb, (int64_t)(H * p.F + H), (int64_t)(H * p.F), out.dW[0], first, st);
         accumulate(ca.pfb + (size_t)H * p.F, nb, (int64_t)(H * p.F + H), (int64_t)H, out.db[0], first, st);
         const int tiles = (H / kWT) * (H / kWT);
+        const int xcd_map = p.slices % 8 == 0 ? 1 : 0;
         const int kb_total = c.rows / 16;                           // 16-row K blocks of the chunk
         const int kb_per_slice = (kb_total + p.slices - 1) / p.slices;
         const size_t bst = (size_t)c.rows * H;   // stride between this chunk's per-layer buffers
@@ -1231,11 +1257,11 @@ hipError_t launch_disc_bf16(const DiscArgs& a, void* ws, int n_cu, hipStream_t s
           // hidden layer l maps A_{l+1} -> A_{l+2}: operands A_{l+1} and the signal at A_{l+2}
           if (tm) tm->begin("bf16_wgrad");
           if (H == 256)
-            hipLaunchKernelGGL(k_wgrad<256>, dim3(tiles * p.slices), dim3(256), 0, st, ca.dlt + l * bst,
-                               ca.act + l * bst, ca.eD, kb_per_slice, kb_total, F32(p.off_pw), F32(p.off_pwdb));
+            hipLaunchKernelGGL(k_wgrad<256>, dim3(tiles * p.slices), dim3(kWThreads), 0, st, ca.dlt + l * bst,
+                               ca.act + l * bst, ca.eD, kb_per_slice, kb_total, F32(p.off_pw), F32(p.off_pwdb), xcd_map);
           else
-            hipLaunchKernelGGL(k_wgrad<512>, dim3(tiles * p.slices), dim3(256), 0, st, ca.dlt + l * bst,
-                               ca.act + l * bst, ca.eD, kb_per_slice, kb_total, F32(p.off_pw), F32(p.off_pwdb));
+            hipLaunchKernelGGL(k_wgrad<512>, dim3(tiles * p.slices), dim3(kWThreads), 0, st, ca.dlt + l * bst,
+                               ca.act + l * bst, ca.eD, kb_per_slice, kb_total, F32(p.off_pw), F32(p.off_pwdb), xcd_map);
           if (tm) tm->end();
           accumulate(F32(p.off_pw), p.slices, (int64_t)H * H, (int64_t)H * H, out.dW[1 + l], first, st);
           accumulate(F32(p.off_pwdb), p.slices, (int64_t)H, (int64_t)H, out.db[1 + l], first, st);
