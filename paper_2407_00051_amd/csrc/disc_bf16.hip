@@ -203,6 +203,10 @@ __global__ __launch_bounds__(256) void k_prep(ChunkArgs c, const float* __restri
 // LDS reads (one step ahead).  The 16-byte row pad makes each 8-lane group of
 // an LDS fragment read hit distinct banks.
 //
+// The HBM copies of each product's input for the weight gradients are written
+// after the product: each wave copies the feature columns it owns, which only
+// its own epilogue overwrites.
+//
 // The VALU work per output is kept to the LeakyReLU (two operations), the
 // bf16 rounding (half of a v_cvt_pk_bf16_f32) and a quarter of the sign-mask
 // packing: biases enter the forward products as one more K step, and the
@@ -244,8 +248,7 @@ struct Chain {
   static constexpr int MW = MT * NT / 2;        // mask words per lane and layer
   static constexpr int BPC = 512 / H;           // workgroups per CU
   static constexpr int COPIES = T * H / 512 / WAVES;   // copy kilobytes per wave and product
-  static constexpr int CDIV = KS / COPIES;             // K steps per copy kilobyte
-  static_assert(MW == 4 && COPIES == 16 && CDIV * COPIES == KS && THREADS == H, "chain decomposition");
+  static_assert(MW == 4 && COPIES == 16 && THREADS == H, "chain decomposition");
 };
 
 typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
@@ -333,20 +336,15 @@ __device__ __forceinline__ bf16x8 copy_read(const u16* p0) {
 
 // acc[mt][nt] = sum_k W[feature][k] act[event][k] (+ the bias with kFwd; see
 // above for the arrangement).  pf holds the first PD weight steps of W on
-// entry and those of Wnext (the next product) on exit.  Spread over the K
-// steps, the wave also writes its share of the LDS tile act (the product's
-// input) to the tile's copy (dst, K-fragment order, per-lane byte offset
-// coff = (2 w 64 + lane) 16), so those HBM writes overlap the matrix work.
+// entry and those of Wnext (the next product) on exit.
 template <int H, bool kFwd>
 __device__ __forceinline__ void chain_gemm(Rsrc W, Rsrc Wnext, uint32_t woff, WeightPrefetch<H>& pf, const u16* act,
-                                           f32x16 (&acc)[Chain<H>::MT][Chain<H>::NT], int lane, int wave, u16* dst,
-                                           uint32_t coff) {
+                                           f32x16 (&acc)[Chain<H>::MT][Chain<H>::NT], int lane) {
   using C = Chain<H>;
-  constexpr int KS = C::KS, PD = C::PD, LDA = C::LDA, MT = C::MT, NT = C::NT, CDIV = C::CDIV;
+  constexpr int KS = C::KS, PD = C::PD, LDA = C::LDA, MT = C::MT, NT = C::NT;
   constexpr int N = WSteps<H, kFwd>::N;          // K steps, the bias step last
   const int lr = lane & 31, lh = lane >> 5;
   const u16* brow = act + lr * LDA + 8 * lh;
-  const u16* cbase = act + copy_lds_base<LDA>(lane, wave);
   // B fragment of the bias step: ones against the three bias terms (lane
   // half 1 meets zero weights)
   const bf16x8 ones = __builtin_bit_cast(bf16x8, make_uint4(0x3f803f80u, 0x00003f80u, 0u, 0u));
@@ -358,11 +356,6 @@ __device__ __forceinline__ void chain_gemm(Rsrc W, Rsrc Wnext, uint32_t woff, We
     for (int m = 0; m < MT; ++m) a[q][m] = pf.a[q][m];
 #pragma unroll
   for (int n = 0; n < NT; ++n) b[0][n] = *reinterpret_cast<const bf16x8*>(brow + 32 * n * LDA);
-  bf16x8 cv;
-  auto put = [&](int j) __attribute__((always_inline)) {
-    *reinterpret_cast<uint4*>(reinterpret_cast<char*>(dst) + ((j >> 1) * (H / 32) + (j & 1)) * 1024 + coff) =
-        __builtin_bit_cast(uint4, cv);
-  };
   const f32x16 zero = {};
 #pragma unroll
   for (int ks = 0; ks < N; ++ks) {
@@ -378,11 +371,6 @@ __device__ __forceinline__ void chain_gemm(Rsrc W, Rsrc Wnext, uint32_t woff, We
       for (int n = 0; n < NT; ++n)
         b[(ks + 1) & 1][n] = *reinterpret_cast<const bf16x8*>(brow + 32 * n * LDA + 16 * (ks + 1));
     }
-    if (ks < KS && ks % CDIV == 0) {
-      const int j = ks / CDIV;
-      if (j > 0) put(j - 1);
-      cv = copy_read<LDA>(cbase + 16 * (j >> 1) * LDA + 32 * (j & 1));
-    }
     // keep the prefetches above the products of this step (the scheduler
     // would otherwise sink each load next to its first use)
     __builtin_amdgcn_sched_barrier(0);
@@ -394,7 +382,24 @@ __device__ __forceinline__ void chain_gemm(Rsrc W, Rsrc Wnext, uint32_t woff, We
                                                            ks == 0 ? zero : acc[m][n], 0, 0, 0);
     __builtin_amdgcn_sched_barrier(0);
   }
-  put(C::COPIES - 1);
+}
+
+// Writes the wave's columns of the LDS tile (the features it owns: only its
+// own epilogue overwrites them, so no other wave has to be waited for) to the
+// tile's copy in HBM: dst in K-fragment order, per-lane byte offset
+// coff = (2 w 64 + lane) 16.  Issued after the product's last weight loads,
+// so the stores never sit in front of a product's weight loads.
+template <int H>
+__device__ __forceinline__ void copy_out(const u16* act, int lane, int wave, u16* dst, uint32_t coff) {
+  using C = Chain<H>;
+  constexpr int LDA = C::LDA;
+  const u16* cbase = act + copy_lds_base<LDA>(lane, wave);
+#pragma unroll
+  for (int j = 0; j < C::COPIES; ++j) {
+    const bf16x8 cv = copy_read<LDA>(cbase + 16 * (j >> 1) * LDA + 32 * (j & 1));
+    *reinterpret_cast<uint4*>(reinterpret_cast<char*>(dst) + ((j >> 1) * (H / 32) + (j & 1)) * 1024 + coff) =
+        __builtin_bit_cast(uint4, cv);
+  }
 }
 
 // max(a, b) of two finite values as one v_max_f32: written out so that the
@@ -613,10 +618,11 @@ __global__ __launch_bounds__(Chain<H>::THREADS, Chain<H>::BPC) void k_fwd_chain(
     for (int l = 0; l < p.NH; ++l) {
       const bool last = l == p.NH - 1;
       f32x16 acc[MT][NT];
-      // the product also writes its input A_{l+1} to HBM; the next product is
-      // layer l + 1, or the first hidden layer of the next tile
+      // the next product is layer l + 1, or the first hidden layer of the next
+      // tile; then the product's input A_{l+1} goes to HBM
       chain_gemm<H, true>(weight_rsrc<H, true>(p.Wb, l), weight_rsrc<H, true>(p.Wb, last ? 0 : l + 1), woff, pf,
-                          act, acc, lane, wave, p.act + ((int64_t)l * rstride + r0) * H, coff);
+                          act, acc, lane);
+      copy_out<H>(act, lane, wave, p.act + ((int64_t)l * rstride + r0) * H, coff);
       uint2 pk[MT][NT][4];
       uint32_t m[MW];
       activate<MT, NT>(acc, slope, pk, m);
@@ -804,10 +810,11 @@ __global__ __launch_bounds__(Chain<H>::THREADS, Chain<H>::BPC) void k_bwd_chain(
       load_mask(mask_at(l, tile), m);
       if (l == 0 && next < ntiles) load_mask(mask_at(NH, next), mtop);
       f32x16 acc[MT][NT];
-      // the product also writes its input (the signal at A_{l+2}) to HBM; the
-      // next product is layer l - 1, or the top layer of the next tile
+      // the next product is layer l - 1, or the top layer of the next tile;
+      // then the product's input (the signal at A_{l+2}) goes to HBM
       chain_gemm<H, false>(weight_rsrc<H, false>(p.WTb, l), weight_rsrc<H, false>(p.WTb, l > 0 ? l - 1 : NH - 1), woff,
-                           pf, act, acc, lane, wave, p.dlt + ((int64_t)l * rstride + r0) * H, coff);
+                           pf, act, acc, lane);
+      copy_out<H>(act, lane, wave, p.dlt + ((int64_t)l * rstride + r0) * H, coff);
       uint2 pk[MT][NT][4];
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt)
