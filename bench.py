@@ -220,15 +220,29 @@ def main():
     ms_per_step = (t1 - t0) * 1e3 / args.steps
     value = N / (ms_per_step * 1e-3)
 
+    bytes_per_launch = None
     if dominant is None:
         kinds = [k for k in ("bf16_fwd_chain", "bf16_bwd_chain", "bf16_wgrad") if k in kt]
         dominant = max(kinds, key=lambda k: kt[k][1])
-        flops_per_launch = flops_per_step_kind / (kt[dominant][0] / args.steps)
+        launches_per_step = kt[dominant][0] / args.steps
+        if dominant == "bf16_wgrad":
+            # streams its two operands (bf16 rows of H) and e_D once per launch and
+            # writes one H x H (+ H) fp32 partial per row slice: bound by HBM
+            rows = 2 * N / launches_per_step * NH
+            slices = max(1, torch.cuda.get_device_properties(0).multi_processor_count // ((H // 256) ** 2))
+            bytes_per_launch = rows * (2 * H * 2 + 4) + slices * (H * H + H) * 4
+            bound, unit, peak = "hbm", "GB/s", PEAK["hbm"]
+        else:
+            flops_per_launch = flops_per_step_kind / launches_per_step
     launches, total_ms = kt.get(dominant, (0, 0.0))
     if launches == 0:
         raise RuntimeError(f"no timed launches of {dominant}")
     avg_ms = total_ms / launches
-    if flops_per_launch is not None:
+    if bytes_per_launch is not None:
+        achieved = bytes_per_launch / (avg_ms * 1e-3)
+        roof = {"bound": bound, "achieved": achieved / 1e9, "peak": peak / 1e9, "unit": unit,
+                "frac": achieved / peak}
+    elif flops_per_launch is not None:
         achieved = flops_per_launch / (avg_ms * 1e-3)
         roof = {"bound": bound, "achieved": achieved / 1e12, "peak": peak / 1e12, "unit": unit,
                 "frac": achieved / peak}
@@ -240,7 +254,8 @@ def main():
                 "frac": achieved / peak_ev if mix else None,
                 "valu_per_event": mix[0] if mix else None, "trans_per_event": mix[1] if mix else None}
     if w.widths is not None:
-        roof["step_mfma_frac"] = mlp_flops_per_fake_event(w.widths) * N / (ms_per_step * 1e-3) / peak
+        mpeak = PEAK["mfma_f32" if w.precision == "f32" else "mfma_bf16"]
+        roof["step_mfma_frac"] = mlp_flops_per_fake_event(w.widths) * N / (ms_per_step * 1e-3) / mpeak
     tr = read_traffic(dominant, w.name)
     roof["traffic"] = tr
     roof["kernel"] = dominant

@@ -85,15 +85,16 @@ __device__ __forceinline__ void store_bf16(u16* p, const float (&v)[PER]) {
 // 32 rb + lane % 32, columns 16 ks + 8 (lane / 32) .. + 7, so the 64 lanes of
 // a wave read one contiguous kilobyte per fragment.  The forward copy (of W,
 // [out][in]) has KS + 1 pieces per 32-row block: the extra step KS carries the
-// bias as three bf16 terms hi + mid + lo, whose sum is exactly the fp32 bias,
-// in columns 0..2 of lane half 0 (zeros elsewhere), and the forward products
-// multiply it by a constant fragment of ones.  The backward copy (of W^T) has
-// KS pieces per row block.
+// bias as three bf16 terms hi + mid + lo in columns 0..2 of lane half 0 (zeros
+// elsewhere), and the forward products multiply it by a constant fragment of
+// ones.  The terms sum to the fp32 bias exactly for magnitudes between about
+// 1e-33 and 3.3e38 (below, lo is subnormal; above, hi overflows).  The
+// backward copy (of W^T) has KS pieces per row block.
 __device__ __forceinline__ uint32_t bias_terms(float x, uint32_t& lo) {
   const u16 hi = bf16_bits(x);
   const float r = x - bf16_to_f32(hi);       // exact
   const u16 mid = bf16_bits(r);
-  lo = bf16_bits(r - bf16_to_f32(mid));      // r - mid exact; it fits in 8 bits
+  lo = bf16_bits(r - bf16_to_f32(mid));      // the last 8 bits (exact unless subnormal)
   return (uint32_t)hi | ((uint32_t)mid << 16);
 }
 
