@@ -27,9 +27,14 @@ Parity status per function (what pins it, see tests/test_oracle_*.py):
                      straight-through rounding at the same points.
   kink variants      pinned: torch autograd where no unit is near the kink,
                      one-sided finite differences at an exact kink.
+  bootstrap          pinned: row ranges, the power-of-two case as a bit
+                     shift, the with-replacement statistics (unique
+                     fraction 1 - (1 - 1/n)^m, per-row counts binomial),
+                     step and seed independence.
 """
 from .philox import philox4x32_10, event_words  # noqa: F401
 from .sampler import (uniform_from_words, kumaraswamy_icdf, kumaraswamy_cdf,  # noqa: F401
                       pathwise, sample, features_hd8, features_hd8_jacobian)
 from .mlp import mlp_forward, bce_losses, disc_fwd_bwd, round_bf16, input_grad_kink_variants  # noqa: F401
 from .step import param_grad, quadratic_critic, run_step  # noqa: F401
+from .bootstrap import bootstrap, bootstrap_indices, STREAM_BOOTSTRAP  # noqa: F401
