@@ -169,6 +169,22 @@ sagips_status sagips_disc_fwd_bwd(sagips_ctx* ctx, const sagips_mlp* D, const fl
 sagips_status sagips_param_grad(sagips_ctx* ctx, const sagips_source* src, sagips_critic critic,
                                 const float* dL_dx, float* dL_dtheta, float* loss_out);
 
+/* 4. Reference data -> the step's bootstrapped sub-sample (paper Sec. IV-B:
+ * every rank draws its training sub-samples from its data by bootstrapping,
+ * i.e. uniformly with replacement).  Draw i < n_out copies row
+ *     idx_i = floor(w0 * n_data / 2^32)
+ * of data, where w0 is the first word of Philox4x32-10 with
+ *     key = (seed & 0xffffffff, seed >> 32),
+ *     counter = (i & 0xffffffff, i >> 32, SAGIPS_STREAM_BOOTSTRAP, step),
+ * so every step draws a fresh sub-sample that depends only on (seed, step, i).
+ *   data     [n_data][d] fp32, 1 <= n_data <= 2^32, d in {2, 3}
+ *   out      [n_out][d] fp32, n_out >= 1; must not overlap data
+ *   idx_out  [n_out] int64 (the drawn rows), or NULL
+ * The result is typically passed as real_x to sagips_disc_fwd_bwd.         */
+#define SAGIPS_STREAM_BOOTSTRAP 4u
+sagips_status sagips_bootstrap(sagips_ctx* ctx, const float* data, int64_t n_data, int d, uint64_t seed,
+                               uint32_t step, int64_t n_out, float* out, int64_t* idx_out);
+
 #ifdef __cplusplus
 }
 #endif

@@ -23,7 +23,8 @@ FEAT_IDENTITY, FEAT_HD8 = 0, 1
 CRITIC_BUFFER, CRITIC_QUADRATIC = 0, 1
 
 EXPORTED = ("sagips_create", "sagips_destroy", "sagips_set_stream", "sagips_last_error", "sagips_set_timing",
-            "sagips_kernel_times", "sagips_sample_events", "sagips_disc_fwd_bwd", "sagips_param_grad")
+            "sagips_kernel_times", "sagips_sample_events", "sagips_disc_fwd_bwd", "sagips_param_grad",
+            "sagips_bootstrap")
 
 
 class SagipsError(RuntimeError):
@@ -75,8 +76,10 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.sagips_disc_fwd_bwd.argtypes = [vp, ctypes.POINTER(Mlp), vp, ctypes.POINTER(Source), i64, vp, i64,
                                         ctypes.POINTER(DiscOut)]
     lib.sagips_param_grad.argtypes = [vp, ctypes.POINTER(Source), i32, vp, vp, vp]
+    lib.sagips_bootstrap.argtypes = [vp, vp, i64, i32, ctypes.c_uint64, ctypes.c_uint32, i64, vp, vp]
     for name in ("sagips_create", "sagips_destroy", "sagips_set_stream", "sagips_set_timing",
-                 "sagips_kernel_times", "sagips_sample_events", "sagips_disc_fwd_bwd", "sagips_param_grad"):
+                 "sagips_kernel_times", "sagips_sample_events", "sagips_disc_fwd_bwd", "sagips_param_grad",
+                 "sagips_bootstrap"):
         getattr(lib, name).restype = ctypes.c_int
     _lib = lib
     return lib
@@ -186,6 +189,26 @@ class Context:
         if want_words and want_x:
             return x, w
         return x if want_x else w
+
+    # -- 4. reference data -> bootstrapped sub-sample --------------------------------
+    def bootstrap(self, data, n_out: int, seed: int, step: int, want_idx: bool = False, out=None, idx_out=None):
+        """The step's sub-sample [n_out][d] of the rows of data (drawn with replacement), and
+        optionally the drawn row indices [n_out] int64."""
+        import torch
+        _check_tensor(data, "data", torch.float32, None, self.device)
+        if data.dim() != 2 or data.shape[1] not in (2, 3):
+            raise ValueError("data must be [n_data][d] with d in {2, 3}")
+        d = data.shape[1]
+        x = out if out is not None else torch.empty((n_out, d), dtype=torch.float32, device=data.device)
+        _check_tensor(x, "out", torch.float32, (n_out, d), self.device)
+        idx = None
+        if want_idx:
+            idx = idx_out if idx_out is not None else torch.empty(n_out, dtype=torch.int64, device=data.device)
+            _check_tensor(idx, "idx_out", torch.int64, (n_out,), self.device)
+        self._check(self.lib.sagips_bootstrap(self.h, _ptr(data), data.shape[0], d, seed & (2**64 - 1),
+                                              step & 0xFFFFFFFF, n_out, _ptr(x), _ptr(idx)))
+        self._keep = (data,)
+        return (x, idx) if want_idx else x
 
     # -- 2. events -> discriminator -> BCE -> backward -------------------------------
     def disc_fwd_bwd(self, W: Sequence, b: Sequence, real_x, fake_x=None, fake_source: Optional[dict] = None,

@@ -49,6 +49,10 @@ size_t param_grad_workspace(const SourceArgs& s);
 hipError_t launch_param_grad(const SourceArgs& s, const float* dLdx, float* dLdtheta, float* loss,
                              void* ws, hipStream_t st, Timer* tm);
 
+// Bootstrap draws: out[i] = data[floor(w0(i) * n_data / 2^32)], idx_out optional.
+hipError_t launch_bootstrap(const float* data, uint64_t n_data, int d, uint32_t k0, uint32_t k1, uint32_t step,
+                            int64_t n_out, float* out, int64_t* idx_out, int n_cu, hipStream_t st, Timer* tm);
+
 // disc_f32.hip ---------------------------------------------------------------
 struct DiscArgs {
   const sagips_mlp* D;

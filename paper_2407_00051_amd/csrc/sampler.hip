@@ -7,6 +7,8 @@
 #include "device_math.hpp"
 #include "kernels.hpp"
 
+#include <algorithm>
+
 namespace sagips {
 namespace {
 
@@ -153,7 +155,40 @@ __global__ __launch_bounds__(kThreads) void k_reduce_loss(const float* __restric
 
 inline int chunks_per_row(const SourceArgs& s) { return (int)((s.E + kEPB - 1) / kEPB); }
 
+// Bootstrap draws, one per thread (grid-stride): draw i takes row
+// floor(w0 * n_data / 2^32), w0 the first Philox word of counter
+// (i lo, i hi, stream, step).  The rows are gathered (8 or 12 bytes each) and
+// written back contiguously.
+template <int D>
+__global__ __launch_bounds__(kThreads) void k_bootstrap(const float* __restrict__ data, uint64_t n_data, uint32_t k0,
+                                                        uint32_t k1, uint32_t step, int64_t n_out,
+                                                        float* __restrict__ out, int64_t* __restrict__ idx_out) {
+  const int64_t stride = (int64_t)gridDim.x * kThreads;
+  for (int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x; i < n_out; i += stride) {
+    const Words w = philox4x32_10((uint32_t)i, (uint32_t)((uint64_t)i >> 32), SAGIPS_STREAM_BOOTSTRAP, step, k0, k1);
+    const uint64_t r = ((uint64_t)w.w[0] * n_data) >> 32;    // < n_data <= 2^32: the product fits in 64 bits
+    if (idx_out) idx_out[i] = (int64_t)r;
+    if constexpr (D == 2) {
+      reinterpret_cast<float2*>(out)[i] = reinterpret_cast<const float2*>(data)[r];
+    } else {
+#pragma unroll
+      for (int j = 0; j < D; ++j) out[i * D + j] = data[r * D + j];
+    }
+  }
+}
+
 }  // namespace
+
+hipError_t launch_bootstrap(const float* data, uint64_t n_data, int d, uint32_t k0, uint32_t k1, uint32_t step,
+                            int64_t n_out, float* out, int64_t* idx_out, int n_cu, hipStream_t st, Timer* tm) {
+  const int64_t want = (n_out + kThreads - 1) / kThreads;
+  const int blocks = (int)std::min<int64_t>(want, (int64_t)n_cu * 32);
+  if (tm) tm->begin("bootstrap");
+  if (d == 2) hipLaunchKernelGGL(k_bootstrap<2>, dim3(blocks), dim3(kThreads), 0, st, data, n_data, k0, k1, step, n_out, out, idx_out);
+  else hipLaunchKernelGGL(k_bootstrap<3>, dim3(blocks), dim3(kThreads), 0, st, data, n_data, k0, k1, step, n_out, out, idx_out);
+  if (tm) tm->end();
+  return hipGetLastError();
+}
 
 hipError_t launch_sample(const SourceArgs& s, float* x, uint32_t* words, hipStream_t st, Timer* tm) {
   const dim3 grid(chunks_per_row(s), s.n_theta);
