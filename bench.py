@@ -37,6 +37,7 @@ KERNEL_SOURCES = {
     "bf16_bwd_chain": ["paper_2407_00051_amd/csrc/disc_bf16.hip", "paper_2407_00051_amd/csrc/device_math.hpp"],
     "bf16_wgrad": ["paper_2407_00051_amd/csrc/disc_bf16.hip", "paper_2407_00051_amd/csrc/device_math.hpp"],
     "param_grad": ["paper_2407_00051_amd/csrc/sampler.hip", "paper_2407_00051_amd/csrc/device_math.hpp"],
+    "bootstrap": ["paper_2407_00051_amd/csrc/sampler.hip", "paper_2407_00051_amd/csrc/device_math.hpp"],
 }
 
 
@@ -122,6 +123,78 @@ def cpu_baseline(w, inp, rows: int, events: int, min_seconds: float = 10.0):
                       f"{n if w.widths else 0} real events), float64 numpy, {reps} repetition(s) in {dt:.1f} s"}
 
 
+def cpu_baseline_bootstrap(w, n_out: int, min_seconds: float = 10.0):
+    """The oracle's draw, as it stands, of n_out rows from a pool of 2 n_out events."""
+    import numpy as np
+    import oracle
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        threads = os.cpu_count()
+    pool = oracle.sample(np.asarray([w.theta_star], dtype=np.float32), 2 * n_out, w.pool_seed).astype(np.float32)
+    reps, t0 = 0, time.perf_counter()
+    while True:
+        oracle.bootstrap(pool, n_out, w.seed, reps)
+        reps += 1
+        dt = time.perf_counter() - t0
+        if dt >= min_seconds:
+            break
+    return {"value": reps * n_out / dt, "unit": "draws/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"{n_out} draws from a pool of {2 * n_out} events (of the workload's {w.n_out} from "
+                      f"{w.n_data}), numpy, {reps} repetition(s) in {dt:.1f} s"}
+
+
+def bench_bootstrap(args, w, ctx, torch):
+    """Steps of the bootstrap draw: n_out rows gathered from the resident pool, a fresh draw per step."""
+    dev = "cuda:0"
+    pool = ctx.sample_events(torch.tensor([w.theta_star], dtype=torch.float32, device=dev), w.n_data, w.pool_seed)
+    out = torch.empty((w.n_out, w.d), dtype=torch.float32, device=dev)
+    it = [0]
+
+    def step():
+        ctx.bootstrap(pool, w.n_out, w.seed, it[0], out=out)
+        it[0] += 1
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    ctx.kernel_times()
+    ctx.set_timing(True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    ctx.set_timing(False)
+    kt = ctx.kernel_times()
+    ms_per_step = (t1 - t0) * 1e3 / args.steps
+    launches, total_ms = kt["bootstrap"]
+    avg_ms = total_ms / launches
+    # algorithmic bytes of a draw: the drawn row read once and written once
+    bytes_per_launch = w.n_out * 2 * w.d * 4
+    achieved = bytes_per_launch / (avg_ms * 1e-3)
+    roof = {"bound": "hbm", "achieved": achieved / 1e9, "peak": PEAK["hbm"] / 1e9, "unit": "GB/s",
+            "frac": achieved / PEAK["hbm"], "traffic": read_traffic("bootstrap", w.name),
+            "kernel": "bootstrap", "kernel_avg_ms": avg_ms,
+            "kernels": {k: {"launches": n, "avg_ms": t / max(n, 1)} for k, (n, t) in kt.items()}}
+    line = {
+        "metric": "draws/sec of the bootstrap sub-sample of the real data; % of HBM peak",
+        "value": w.n_out / (ms_per_step * 1e-3), "unit": "draws/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": ms_per_step, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "u32",
+        "data": "synthetic (pool of Philox-sampled Kumaraswamy events at theta_star)",
+        "config": {"workload": w.name, "n_data": w.n_data, "d": w.d, "n_out": w.n_out,
+                   "parallelism": "single GPU"},
+        "roofline": roof,
+    }
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"] = cpu_baseline_bootstrap(w, min(w.n_out, 1 << 20))
+    ctx.close()
+    print(json.dumps(line), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -145,14 +218,9 @@ def main():
     from workloads import gen, get
 
     w = get(args.workload)
-    inp = gen.make_inputs(w)
-    dev = "cuda:0"
     torch.cuda.set_device(0)
     ctx = sg.Context(0)
-    theta = torch.tensor(inp["theta"], device=dev)
-    theta_star = torch.tensor(inp["theta_star"], device=dev)
-    N = w.n_events
-
+    dev = "cuda:0"
     if args.calibrate_copy:
         a = torch.empty(1 << 28, dtype=torch.float32, device=dev)
         b = torch.empty_like(a)
@@ -161,6 +229,12 @@ def main():
         b.copy_(a)
         torch.cuda.synchronize()
         del a, b
+    if not hasattr(w, "widths"):
+        return bench_bootstrap(args, w, ctx, torch)
+    inp = gen.make_inputs(w)
+    theta = torch.tensor(inp["theta"], device=dev)
+    theta_star = torch.tensor(inp["theta_star"], device=dev)
+    N = w.n_events
 
     if w.widths is not None:
         W = [torch.tensor(m, device=dev) for m in inp["W"]]

@@ -40,6 +40,18 @@ def test_bootstrap_full_size_sampled(gpu_ctx):
     ref_idx = oracle.bootstrap_indices(n_data, n_out, 2024, 17)
     assert np.array_equal(idx.cpu().numpy(), ref_idx)
     assert torch.equal(out, data[torch.tensor(ref_idx, device="cuda:0")])
+    # the variant without the index output (the one the benchmark times) draws the same rows
+    assert torch.equal(gpu_ctx.bootstrap(data, n_out, 2024, 17), out)
+
+
+def test_bootstrap_three_observable_full_size(gpu_ctx):
+    """Three-observable reference data at full size (33,554,432 events, 16,777,216 draws)."""
+    n_data, n_out = 1 << 25, 1 << 24
+    data = torch.randn((n_data, 3), device="cuda:0")
+    out = gpu_ctx.bootstrap(data, n_out, 99, 4)
+    torch.cuda.synchronize()
+    ref_idx = torch.tensor(oracle.bootstrap_indices(n_data, n_out, 99, 4), device="cuda:0")
+    assert torch.equal(out, data[ref_idx])
 
 
 def test_bootstrap_rejects_bad_arguments(gpu_ctx):

@@ -57,8 +57,35 @@ CONFIGS = {
 }
 
 
-def get(name: str) -> Workload:
-    return CONFIGS[name]
+@dataclass(frozen=True)
+class BootstrapWorkload:
+    """One step's bootstrap draw of the real batch from a rank's data (Sec. IV-B).
+
+    The pool holds twice the step's real batch and each step draws half of
+    it, with replacement; the pool's events are Kumaraswamy draws at
+    theta_star, resident in HBM before the step."""
+    name: str
+    n_data: int                  # events in the rank's pool
+    d: int
+    n_out: int                   # draws per step
+    seed: int = 5                # Philox key of the draws
+    pool_seed: int = 1           # Philox key of the pool's events
+
+    @property
+    def theta_star(self) -> Tuple[float, ...]:
+        return (2.0, 5.0, 1.5, 3.0) if self.d == 2 else (2.0, 5.0, 1.5, 3.0, 3.0, 2.0)
+
+
+BOOTSTRAP_CONFIGS = {
+    # the real batch of the 256 x 16,384-event step, drawn from a pool of twice its size
+    "bootstrap": BootstrapWorkload("bootstrap", 2 * 4194304, 2, 4194304),
+    # the real batch of the 1,024 x 16,384-event three-observable step
+    "bootstrap_d3": BootstrapWorkload("bootstrap_d3", 2 * 16777216, 3, 16777216),
+}
+
+
+def get(name: str):
+    return CONFIGS[name] if name in CONFIGS else BOOTSTRAP_CONFIGS[name]
 
 
 def scaled(w: Workload, n_theta: Optional[int] = None, events_per_theta: Optional[int] = None) -> Workload:
