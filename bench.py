@@ -247,7 +247,7 @@ def main():
                 "dLg_dx": torch.empty((N, w.d), **f32), "dLg_dtheta": torch.empty((w.n_theta, 2 * w.d), **f32)}
         src = dict(theta=theta, events_per_theta=w.events_per_theta, seed=w.fake_seed)
         prec = sg.BF16 if w.precision == "bf16" else sg.F32
-        feats = sg.FEAT_HD8 if w.features == "hd8" else sg.FEAT_IDENTITY
+        feats = {"identity": sg.FEAT_IDENTITY, "hd8": sg.FEAT_HD8, "proxy2": sg.FEAT_PROXY2}[w.features]
 
         def step():
             ctx.disc_fwd_bwd(W, bias, real, fake_source=src, outputs=outs, precision=prec, features=feats)

@@ -55,7 +55,7 @@ typedef enum {
 } sagips_status;
 
 typedef enum { SAGIPS_F32 = 0, SAGIPS_BF16 = 1 } sagips_precision;
-typedef enum { SAGIPS_FEAT_IDENTITY = 0, SAGIPS_FEAT_HD8 = 1 } sagips_features;
+typedef enum { SAGIPS_FEAT_IDENTITY = 0, SAGIPS_FEAT_HD8 = 1, SAGIPS_FEAT_PROXY2 = 2 } sagips_features;
 typedef enum { SAGIPS_CRITIC_BUFFER = 0, SAGIPS_CRITIC_QUADRATIC = 1 } sagips_critic;
 
 /* Parameters -> events source (host struct holding a device pointer).
@@ -80,13 +80,21 @@ typedef struct {
  * layout), b[l] is [width[l+1]] fp32.  Hidden layers apply
  * LeakyReLU(leaky_slope); the last layer has width 1 and emits a logit.
  *   features   IDENTITY: width[0] == d;  HD8 (d == 3): width[0] == 8 and the
- *              input is [x1,x2,x3,x1x2,x2x3,x1x3,ln x1,ln(1-x3)].
+ *              input is [x1,x2,x3,x1x2,x2x3,x1x3,ln x1,ln(1-x3)];
+ *              PROXY2 (d == 3, F32 only): width[0] == 2 and the input is the
+ *              two observables (x1 + x3, x2 + x3) of the six-parameter,
+ *              two-observable pipeline (Sec. V; the sum form is this
+ *              library's reading, the paper does not give the mapping).
+ *              Event buffers hold the d raw coordinates in every mode, and
+ *              dLg_dx is the gradient with respect to them.
  *   precision  F32: every product in fp32.  BF16: hidden-to-hidden layers use
  *              bf16 operands (weights rounded once per call, activations and
  *              backward signals rounded to nearest even) with fp32 accumulate;
  *              the first and the logit layer stay fp32.
  * Supported shapes: n_layers >= 2; all hidden widths equal, one of 64, 128
- * (F32) or 256, 512 (BF16); width[0] in {2, 3, 8}.  BF16 also needs
+ * (F32) or 256, 512 (BF16); width[0] in {2, 3, 8}.  F32 IDENTITY: width 64
+ * with 1-3 or 128 with 1-2 hidden-to-hidden layers; F32 PROXY2: width 128
+ * with 3 (the paper's 2-128-128-128-128-1 network).  BF16 also needs
  * 0 <= leaky_slope <= 1 (SAGIPS_E_UNSUPPORTED otherwise).                 */
 typedef struct {
   int32_t n_layers;

@@ -27,6 +27,16 @@ Parity status per function (what pins it, see tests/test_oracle_*.py):
                      straight-through rounding at the same points.
   kink variants      pinned: torch autograd where no unit is near the kink,
                      one-sided finite differences at an exact kink.
+  features_proxy2    pinned: Jacobian by finite differences, the means and
+                     the covariance of the two observables against the
+                     closed-form Kumaraswamy moments, the whole step's
+                     dL/dtheta by finite differences.
+  generator          pinned: forward against torch float64 modules,
+                     backward against torch autograd and finite
+                     differences.
+  ensemble response  pinned: M = 1 and identical members (sigma = 0), the
+                     M = 2 closed form |G1 - G2| / 2, numpy's population
+                     standard deviation, member-order invariance.
   bootstrap          pinned: row ranges, the power-of-two case as a bit
                      shift, the with-replacement statistics (unique
                      fraction 1 - (1 - 1/n)^m, per-row counts binomial),
@@ -34,7 +44,9 @@ Parity status per function (what pins it, see tests/test_oracle_*.py):
 """
 from .philox import philox4x32_10, event_words  # noqa: F401
 from .sampler import (uniform_from_words, kumaraswamy_icdf, kumaraswamy_cdf,  # noqa: F401
-                      pathwise, sample, features_hd8, features_hd8_jacobian)
+                      pathwise, sample, features_hd8, features_hd8_jacobian,
+                      features_proxy2, features_proxy2_jacobian)
 from .mlp import mlp_forward, bce_losses, disc_fwd_bwd, round_bf16, input_grad_kink_variants  # noqa: F401
 from .step import param_grad, quadratic_critic, run_step  # noqa: F401
 from .bootstrap import bootstrap, bootstrap_indices, STREAM_BOOTSTRAP  # noqa: F401
+from .generator import G_WIDTHS, generator_forward, generator_backward, ensemble_response, residual  # noqa: F401

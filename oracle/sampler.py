@@ -90,3 +90,24 @@ def features_hd8_jacobian(x: np.ndarray) -> np.ndarray:
     J[:, 6, 0] = 1.0 / x1
     J[:, 7, 2] = -1.0 / (1.0 - x3)
     return J
+
+
+def features_proxy2(x: np.ndarray) -> np.ndarray:
+    """The two observables of the paper-shape pipeline (Sec. V: six parameters
+    in, two observables out; the mapping itself is not given).  Reading: three
+    independent Kumaraswamy draws, one per parameter pair, share the third
+    draw:  y0 = x1 + x3,  y1 = x2 + x3.  By Kotlarski's lemma the joint law of
+    (y0, y1) identifies the laws of x1, x2 and x3 up to a common shift, which
+    their common support (0, 1) removes, so the six parameters stay
+    recoverable."""
+    return np.stack([x[:, 0] + x[:, 2], x[:, 1] + x[:, 2]], axis=1)
+
+
+def features_proxy2_jacobian(x: np.ndarray) -> np.ndarray:
+    """d(y0, y1) / d(x1, x2, x3), [N][2][3]."""
+    J = np.zeros((x.shape[0], 2, 3))
+    J[:, 0, 0] = 1.0
+    J[:, 0, 2] = 1.0
+    J[:, 1, 1] = 1.0
+    J[:, 1, 2] = 1.0
+    return J

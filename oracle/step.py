@@ -13,7 +13,10 @@ from __future__ import annotations
 import numpy as np
 
 from .mlp import disc_fwd_bwd
-from .sampler import features_hd8, features_hd8_jacobian, sample
+from .sampler import features_hd8, features_hd8_jacobian, features_proxy2, features_proxy2_jacobian, sample
+
+FEATURES = {"hd8": (features_hd8, features_hd8_jacobian),
+            "proxy2": (features_proxy2, features_proxy2_jacobian)}
 
 
 def param_grad(dL_dx: np.ndarray, dxda: np.ndarray, dxdb: np.ndarray, n_theta: int, E: int):
@@ -46,14 +49,17 @@ def run_step(theta, E, fake_seed, W=None, b=None, real_x=None, features="identit
         out["loss"] = loss
         out["dL_dx"] = g
     else:
-        fin = s["x"] if features == "identity" else features_hd8(s["x"])
-        rin = real_x if features == "identity" else features_hd8(real_x)
+        if features == "identity":
+            fin, rin = s["x"], real_x
+        else:
+            fmap = FEATURES[features][0]
+            fin, rin = fmap(s["x"]), fmap(real_x)
         r = disc_fwd_bwd(W, b, fin, rin, slope, bf16)
         out.update(r)
         if features == "identity":
             g = r["dLg_din"]
         else:
-            g = np.einsum("nf,nfd->nd", r["dLg_din"], features_hd8_jacobian(s["x"]))
+            g = np.einsum("nf,nfd->nd", r["dLg_din"], FEATURES[features][1](s["x"]))
         out["dL_dx"] = g
     out["dL_dtheta"], out["dL_dtheta_cond"] = param_grad(out["dL_dx"], s["dxda"], s["dxdb"], n_theta, E)
     return out

@@ -19,7 +19,7 @@ MAX_LAYERS = 8
 
 OK, E_INVAL, E_ARCH, E_NOMEM, E_HIP, E_UNSUPPORTED = 0, -1, -2, -3, -4, -5
 F32, BF16 = 0, 1
-FEAT_IDENTITY, FEAT_HD8 = 0, 1
+FEAT_IDENTITY, FEAT_HD8, FEAT_PROXY2 = 0, 1, 2
 CRITIC_BUFFER, CRITIC_QUADRATIC = 0, 1
 
 EXPORTED = ("sagips_create", "sagips_destroy", "sagips_set_stream", "sagips_last_error", "sagips_set_timing",
@@ -249,7 +249,7 @@ class Context:
         else:                       # no fake input: the library rejects the call
             n_fake, d = 0, widths[0]
         n_real = real_x.shape[0]
-        d_in = 3 if features == FEAT_HD8 else widths[0]
+        d_in = widths[0] if features == FEAT_IDENTITY else 3
         if (fake_x is not None and d != d_in) or real_x.dim() != 2 or real_x.shape[1] != d_in:
             raise ValueError(f"events must be [n][{d_in}] for this network and feature map")
         o = dict(outputs or {})

@@ -314,7 +314,7 @@ sagips_status sagips_disc_fwd_bwd(sagips_ctx* c, const sagips_mlp* D, const floa
     if (D->width[l] < 1) return fail(c, SAGIPS_E_INVAL, "width[%d] < 1", l);
   }
   if (D->width[D->n_layers] != 1) return fail(c, SAGIPS_E_INVAL, "last width must be 1 (a logit)");
-  if (D->features != SAGIPS_FEAT_IDENTITY && D->features != SAGIPS_FEAT_HD8)
+  if (D->features != SAGIPS_FEAT_IDENTITY && D->features != SAGIPS_FEAT_HD8 && D->features != SAGIPS_FEAT_PROXY2)
     return fail(c, SAGIPS_E_INVAL, "unknown features %d", D->features);
   if (D->precision != SAGIPS_F32 && D->precision != SAGIPS_BF16)
     return fail(c, SAGIPS_E_INVAL, "unknown precision %d", D->precision);
@@ -334,10 +334,12 @@ sagips_status sagips_disc_fwd_bwd(sagips_ctx* c, const sagips_mlp* D, const floa
                   (long long)source_events(fake_src));
     d = fake_src->d;
   } else {
-    d = D->features == SAGIPS_FEAT_HD8 ? 3 : D->width[0];
+    d = D->features == SAGIPS_FEAT_IDENTITY ? D->width[0] : 3;
   }
   if (D->features == SAGIPS_FEAT_HD8 && (d != 3 || D->width[0] != 8))
     return fail(c, SAGIPS_E_INVAL, "HD8 features need d = 3 and width[0] = 8");
+  if (D->features == SAGIPS_FEAT_PROXY2 && (d != 3 || D->width[0] != 2))
+    return fail(c, SAGIPS_E_INVAL, "PROXY2 features need d = 3 and width[0] = 2");
   if (D->features == SAGIPS_FEAT_IDENTITY && D->width[0] != d)
     return fail(c, SAGIPS_E_INVAL, "IDENTITY features need width[0] == d (%d vs %d)", D->width[0], d);
   const bool any_dW = out->dW[0] != nullptr;
@@ -351,9 +353,10 @@ sagips_status sagips_disc_fwd_bwd(sagips_ctx* c, const sagips_mlp* D, const floa
   if (D->precision == SAGIPS_BF16) return disc_bf16(c, D, fake_x, fake_src, n_fake, real_x, n_real, out, d);
   if (!disc_f32_supported(*D, d, &why)) return fail(c, SAGIPS_E_UNSUPPORTED, "%s", why);
 
-  // The in-kernel sampler needs every tile inside one parameter row;
-  // otherwise sample first, run on the buffer, and reduce dL/dtheta after.
-  const bool fused_src = fake_src && (fake_src->events_per_theta % disc_f32_tile() == 0);
+  // The in-kernel sampler lets a tile straddle at most two parameter rows;
+  // with fewer events per row than a tile holds, sample first, run on the
+  // buffer, and reduce dL/dtheta after.
+  const bool fused_src = fake_src && (fake_src->events_per_theta >= disc_f32_tile());
   SourceArgs sa{};
   if (fake_src) sa = source_args(*fake_src);
   DiscArgs a;

@@ -1165,6 +1165,7 @@ bool disc_bf16_supported(const sagips_mlp& D, int d, const char** why) {
   if (D.n_layers < 3 || D.n_layers - 2 > kMaxNH) { *why = "bf16 discriminator needs 1-4 hidden-to-hidden layers"; return false; }
   for (int l = 1; l < D.n_layers; ++l)
     if (D.width[l] != H) { *why = "all hidden widths must be equal"; return false; }
+  if (D.features == SAGIPS_FEAT_PROXY2) { *why = "PROXY2 features are supported by the fp32 discriminator only"; return false; }
   if (D.features == SAGIPS_FEAT_HD8) {
     if (d != 3 || D.width[0] != 8) { *why = "HD8 features need d = 3 and width[0] = 8"; return false; }
   } else if (D.width[0] != d || (d != 2 && d != 3)) {

@@ -4,7 +4,10 @@
 // per-parameter reduction as well -- one persistent kernel per call.
 //
 // Network: F -> H -> (H -> H) x NH -> 1, LeakyReLU on the hidden layers
-// (paper Sec. V-A), weights in torch.nn.Linear layout.
+// (paper Sec. V-A), weights in torch.nn.Linear layout.  Events have DX
+// coordinates; the network sees F features of them: the coordinates
+// themselves (F = DX), or the two observables y0 = x1 + x3, y1 = x2 + x3 of
+// the six-parameter, two-observable pipeline (DX = 3, F = 2; Sec. V).
 //
 // Work decomposition
 //   * One persistent workgroup of 8 waves (two per SIMD, so one hides the
@@ -12,7 +15,12 @@
 //     is all fake or all real.  The tile's activations
 //     A_1..A_{NH+1} and one spare buffer live in LDS as [T][H+4] fp32
 //     (event-major, padded so that the 16-byte fragment reads below are
-//     bank-conflict free).
+//     bank-conflict free).  Where the spare buffer would not fit (H = 128
+//     with three hidden-to-hidden layers), each backward signal overwrites
+//     the activation it replaces, behind one more barrier per layer.
+//   * Sampled fake events: event i takes parameter row i / E, so a tile may
+//     straddle two rows (E >= T); its per-parameter partials keep one slot
+//     per row it touches.
 //   * The H x H products run on the fp32 matrix cores
 //     (v_mfma_f32_16x16x4_f32).  Forward and backward-data products compute
 //     out^T = W' * in^T with M = output feature, N = event, K = input
@@ -57,21 +65,22 @@ struct F32Params {
   const float* bo;             // [1]
   float slope;
   // inputs
-  const float* fake_x;         // [n_fake][F] or NULL (then sampled)
-  const float* real_x;         // [n_real][F]
+  const float* fake_x;         // [n_fake][DX] or NULL (then sampled)
+  const float* real_x;         // [n_real][DX]
   SourceArgs src;              // valid when fake_x == NULL
   int64_t n_fake, n_real;
   int n_fake_tiles, n_tiles;
-  int tiles_per_row;           // E / T for the source path
+  int64_t E;                   // events per parameter row (source path)
   float inv_nf, inv_nr;
   // outputs
   float* logits_fake;
   float* logits_real;
-  float* dLg_dx;               // [n_fake][F] or NULL
+  float* dLg_dx;               // [n_fake][DX] or NULL
   // workspace
   float* wg_part;              // [gridDim.x][P]
   float* loss_part;            // [n_tiles][2]
-  float* theta_part;           // [n_fake_tiles][2F] (source path)
+  float* theta_part;           // [n_fake_tiles][2][2 DX] (source path): slot 0 = row of the
+                               // tile's first event, slot 1 = the next row
 };
 
 __device__ __forceinline__ f32x4 mfma4(float a, float b, f32x4 c) {
@@ -83,10 +92,15 @@ __device__ __forceinline__ float leaky_grad(float h, float s) { return h > 0.0f 
 
 __device__ __forceinline__ float softplus(float t) { return fmaxf(t, 0.0f) + log1pf(expf(-fabsf(t))); }
 
-template <int H, int NH, int F>
+template <int H, int NH, int DX, int F, int FEAT>
 struct Fused {
+  static_assert(FEAT == SAGIPS_FEAT_IDENTITY ? DX == F : (FEAT == SAGIPS_FEAT_PROXY2 && DX == 3 && F == 2),
+                "feature map");
   static constexpr int LD = H + 4;             // LDS row stride in floats
-  static constexpr int NB = NH + 2;            // activation + spare buffers
+  // Backward signals overwrite the activations they replace when a spare
+  // buffer would not fit next to the others in 160 KB of LDS.
+  static constexpr bool kInPlace = (NH + 2) * kT * LD * 4 + 8192 > 160 * 1024;
+  static constexpr int NB = kInPlace ? NH + 1 : NH + 2;   // activation (+ spare) buffers
   static constexpr int WAVES = kThreads / 64;
   static constexpr int WR = H / 16;            // waves along the output rows (16 rows each)
   static constexpr int WE = WAVES / WR;        // waves along the events
@@ -105,15 +119,17 @@ struct Fused {
 
   struct Smem {
     float act[NB][kT][LD];
-    float X[kT][F];
-    float dxd[kT][F][2];
+    float X[kT][F];          // the network's input features
+    float xs[FEAT == SAGIPS_FEAT_IDENTITY ? 1 : kT][DX];   // raw coordinates (feature maps only)
+    float dxd[kT][DX][2];
     float eD[kT];
     float eG[kT];
-    float red[2 * kT * 4];   // >= 2 T F and >= 2 * waves
+    float w1[kInPlace ? H : 1][F];   // first-layer weights, when registers are short
+    float red[2 * kT * 4];   // >= 2 T DX and >= 2 * waves
   };
 
   // Index of the buffer that holds delta_l (l = 1 .. NH+1).
-  static constexpr __device__ int dbuf(int l) { return NH + ((NH + 1 - l) & 1); }
+  static constexpr __device__ int dbuf(int l) { return kInPlace ? l - 1 : NH + ((NH + 1 - l) & 1); }
 
   // out^T (this wave's 16 rows x CB event blocks) = Wg * in^T, K = H.  The
   // weight fragments are loaded PD K blocks ahead of their use.
@@ -211,41 +227,61 @@ struct Fused {
     const float wor = p.Wo[vo];
     // per-event dot products: thread (ev = tid / PARTS, part = tid % PARTS) covers H / PARTS features
     const int dev_ = tid / PARTS, dpart = tid % PARTS;
-    float w1c[NCH][4][F];     // the first-layer weights of this thread's features
+    float w1c[kInPlace ? 1 : NCH][4][F];     // the first-layer weights of this thread's features
+    if constexpr (kInPlace) {
+      for (int i = tid; i < H * F; i += kThreads) sm.w1[i / F][i % F] = p.W1[i];
+    } else {
 #pragma unroll
-    for (int c = 0; c < NCH; ++c)
+      for (int c = 0; c < NCH; ++c)
 #pragma unroll
-      for (int q = 0; q < 4; ++q)
+        for (int q = 0; q < 4; ++q)
 #pragma unroll
-        for (int j = 0; j < F; ++j) w1c[c][q][j] = p.W1[(chunk_off(dpart, c) + q) * F + j];
+          for (int j = 0; j < F; ++j) w1c[c][q][j] = p.W1[(chunk_off(dpart, c) + q) * F + j];
+    }
 
     for (int tile = blockIdx.x; tile < p.n_tiles; tile += gridDim.x) {
       const bool fake = tile < p.n_fake_tiles;
       const int64_t ev0 = (int64_t)(fake ? tile : tile - p.n_fake_tiles) * kT;
       const int64_t n_here = fake ? p.n_fake : p.n_real;
       const bool sampled = fake && p.fake_x == nullptr;
+      // Sampled tiles: the parameter row of the tile's first event, and the
+      // tile-local index of the first event of the next row (E >= T, so a
+      // tile touches at most these two rows).  n_fake < 2^30 keeps this in 32 bits.
+      const uint32_t row_lo = sampled ? (uint32_t)ev0 / (uint32_t)p.E : 0u;
+      const int split = sampled ? (int)min<int64_t>((int64_t)(row_lo + 1) * p.E - ev0, kT) : kT;
 
       // ---- 1. tile inputs: thread (event, coordinate) ---------------------------
-      if (tid < kT * F) {
-        const int ev = tid / F, j = tid % F;
+      if (tid < kT * DX) {
+        const int ev = tid / DX, j = tid % DX;
         const int64_t i = ev0 + ev;
+        float xv = 0.5f;
         if (sampled) {
-          // E is a multiple of T here, so the whole tile uses one parameter row.
-          const int row = tile / p.tiles_per_row;
-          const Words w = event_words(p.src.base + (uint64_t)i, p.src.stream, p.src.k0, p.src.k1);
-          const Shape sh = make_shape(p.src.theta[row * 2 * F + 2 * j], p.src.theta[row * 2 * F + 2 * j + 1]);
-          const Quantile q = kumaraswamy_w(w.w[j], sh);
-          float da, db;
-          pathwise(q, sh, da, db);
-          sm.X[ev][j] = q.x;
+          float da = 0.f, db = 0.f;
+          if (i < n_here) {
+            const int row = (int)row_lo + (ev >= split ? 1 : 0);
+            const Words w = event_words(p.src.base + (uint64_t)i, p.src.stream, p.src.k0, p.src.k1);
+            const Shape sh = make_shape(p.src.theta[row * 2 * DX + 2 * j], p.src.theta[row * 2 * DX + 2 * j + 1]);
+            const Quantile q = kumaraswamy_w(w.w[j], sh);
+            pathwise(q, sh, da, db);
+            xv = q.x;
+          }
           sm.dxd[ev][j][0] = da;
           sm.dxd[ev][j][1] = db;
         } else {
           const float* src = fake ? p.fake_x : p.real_x;
-          sm.X[ev][j] = (i < n_here) ? src[i * F + j] : 0.5f;
+          if (i < n_here) xv = src[i * DX + j];
         }
+        if constexpr (FEAT == SAGIPS_FEAT_IDENTITY) sm.X[ev][j] = xv;
+        else sm.xs[ev][j] = xv;
       }
       __syncthreads();
+      if constexpr (FEAT == SAGIPS_FEAT_PROXY2) {
+        if (tid < kT) {
+          sm.X[tid][0] = sm.xs[tid][0] + sm.xs[tid][2];
+          sm.X[tid][1] = sm.xs[tid][1] + sm.xs[tid][2];
+        }
+        __syncthreads();
+      }
 
       // ---- 2. first layer (VALU): A_1 = leaky(X W1^T + b1) -------------------
 #pragma unroll 4
@@ -343,6 +379,7 @@ struct Fused {
         float* din = &sm.act[dbuf(l + 1)][0][0];
         const float* Ain = &sm.act[l][0][0];
         wgrad(dout, Ain, sm.eD, accW[l], dbacc[l], wave % WR, e0, lr, lg);
+        if constexpr (kInPlace) __syncthreads();   // din overwrites Ain, which every wave's wgrad read
         f32x4 acc[CB];
         gemm(p.WhT[l], dout, acc, o0, e0, lr, lg);
         const int k = o0 + 4 * lg;
@@ -378,12 +415,20 @@ struct Fused {
 #pragma unroll
         for (int c = 0; c < NCH; ++c) {
           const f32x4 dv = *reinterpret_cast<const f32x4*>(drow + chunk_off(dpart, c));
+          const int f = chunk_off(dpart, c);
 #pragma unroll
           for (int j = 0; j < F; ++j) {
-            g[j] = fmaf(dv.x, w1c[c][0][j], g[j]);
-            g[j] = fmaf(dv.y, w1c[c][1][j], g[j]);
-            g[j] = fmaf(dv.z, w1c[c][2][j], g[j]);
-            g[j] = fmaf(dv.w, w1c[c][3][j], g[j]);
+            if constexpr (kInPlace) {
+              g[j] = fmaf(dv.x, sm.w1[f][j], g[j]);
+              g[j] = fmaf(dv.y, sm.w1[f + 1][j], g[j]);
+              g[j] = fmaf(dv.z, sm.w1[f + 2][j], g[j]);
+              g[j] = fmaf(dv.w, sm.w1[f + 3][j], g[j]);
+            } else {
+              g[j] = fmaf(dv.x, w1c[c][0][j], g[j]);
+              g[j] = fmaf(dv.y, w1c[c][1][j], g[j]);
+              g[j] = fmaf(dv.z, w1c[c][2][j], g[j]);
+              g[j] = fmaf(dv.w, w1c[c][3][j], g[j]);
+            }
           }
         }
 #pragma unroll
@@ -394,24 +439,51 @@ struct Fused {
         if (dpart == 0) {
           const float eg = sm.eG[dev_];
           const int64_t i = ev0 + dev_;
+          // dL_G/dx: the features' gradient through the feature map's Jacobian
+          float gx[DX];
+          if constexpr (FEAT == SAGIPS_FEAT_IDENTITY) {
 #pragma unroll
-          for (int j = 0; j < F; ++j) {
-            g[j] *= eg;
-            if (p.dLg_dx && i < n_here) p.dLg_dx[i * F + j] = g[j];
+            for (int j = 0; j < DX; ++j) gx[j] = g[j] * eg;
+          } else {
+            gx[0] = g[0] * eg;
+            gx[1] = g[1] * eg;
+            gx[2] = gx[0] + gx[1];
+          }
+#pragma unroll
+          for (int j = 0; j < DX; ++j) {
+            if (p.dLg_dx && i < n_here) p.dLg_dx[i * DX + j] = gx[j];
             if (sampled) {
-              sm.red[2 * (dev_ * F + j)] = g[j] * sm.dxd[dev_][j][0];
-              sm.red[2 * (dev_ * F + j) + 1] = g[j] * sm.dxd[dev_][j][1];
+              sm.red[2 * (dev_ * DX + j)] = gx[j] * sm.dxd[dev_][j][0];
+              sm.red[2 * (dev_ * DX + j) + 1] = gx[j] * sm.dxd[dev_][j][1];
             }
           }
         }
         if (sampled) {
           __syncthreads();
-          if (tid < 2 * F) {
-            // component c = 2 j + (a|b); terms stored at red[2 (ev F + j) + ab]
-            const int j = tid >> 1, ab = tid & 1;
-            float s = 0.f;
-            for (int ev = 0; ev < kT; ++ev) s += sm.red[2 * (ev * F + j) + ab];
-            p.theta_part[(int64_t)tile * 2 * F + tid] = s;
+          if (tid < 8 * 2 * DX) {
+            // lane (component c = 2 j + (a|b), part q) sums events q, q + 8, ...;
+            // the terms sit at red[2 (ev DX + j) + ab].  Slot 0 takes the events of
+            // the tile's first row, slot 1 those of the next; the 8 parts of a
+            // component are then added across lanes.
+            const int c = tid >> 3, q = tid & 7;
+            const int j = c >> 1, ab = c & 1;
+            float s0 = 0.f, s1 = 0.f;
+#pragma unroll
+            for (int k = 0; k < kT / 8; ++k) {
+              const int ev = q + 8 * k;
+              const float t = sm.red[2 * (ev * DX + j) + ab];
+              s0 += ev < split ? t : 0.f;
+              s1 += ev < split ? 0.f : t;
+            }
+#pragma unroll
+            for (int m = 1; m < 8; m <<= 1) {
+              s0 += __shfl_xor(s0, m, 64);
+              s1 += __shfl_xor(s1, m, 64);
+            }
+            if (q == 0) {
+              p.theta_part[((int64_t)tile * 2) * 2 * DX + c] = s0;
+              p.theta_part[((int64_t)tile * 2 + 1) * 2 * DX + c] = s1;
+            }
           }
         }
       }
@@ -497,9 +569,9 @@ struct Fused {
   }
 };
 
-template <int H, int NH, int F>
+template <int H, int NH, int DX, int F, int FEAT>
 __global__ __launch_bounds__(kThreads, 1) void k_disc_f32(F32Params p) {
-  Fused<H, NH, F>::run(p);
+  Fused<H, NH, DX, F, FEAT>::run(p);
 }
 
 // WT[k][o] = W[o][k] for the H x H hidden layers (blockIdx.z = layer).
@@ -523,7 +595,8 @@ __global__ __launch_bounds__(256) void k_transpose(TransposeArgs t_, int H) {
 //   blocks [0, wg_blocks)        sum over workgroups of every gradient partial,
 //                                scattered to the caller's arrays (segment table);
 //   block  wg_blocks             the two losses from the per-tile sums;
-//   blocks wg_blocks + 1 + row   dL_G/dtheta of one parameter row from its tiles.
+//   blocks wg_blocks + 1 + row   dL_G/dtheta of one parameter row from the slots of
+//                                the tiles that hold its events.
 struct Segments {
   int n;
   int off[2 * kMaxNH + 4];
@@ -541,7 +614,8 @@ struct ReduceArgs {
   float* loss_d;
   float* loss_g;
   const float* theta_part;
-  int tiles_per_row, C;
+  int64_t E;
+  int C;
   float* dLg_dtheta;
 };
 
@@ -589,13 +663,19 @@ __global__ __launch_bounds__(256) void k_reduce_all(ReduceArgs r) {
     }
     return;
   }
-  // one parameter row: thread (component c, slice s) sums tiles s, s + S, ...; slices combined in order
+  // one parameter row: its events fill tiles t0..t1; a tile holds the row in
+  // slot 0 if the row starts at or before the tile, else in slot 1.  Thread
+  // (component c, slice s) sums tiles t0 + s, t0 + s + S, ...; slices combined in order.
   const int row = blockIdx.x - r.wg_blocks - 1;
   const int S = 256 / r.C;
   const int c = tid % r.C, sl = tid / r.C;
+  const int64_t t0 = (int64_t)row * r.E / kT, t1 = ((int64_t)row * r.E + r.E - 1) / kT;
   float s = 0.f;
   if (sl < S)
-    for (int t = sl; t < r.tiles_per_row; t += S) s += r.theta_part[((int64_t)row * r.tiles_per_row + t) * r.C + c];
+    for (int64_t t = t0 + sl; t <= t1; t += S) {
+      const int slot = (t * kT) / r.E == row ? 0 : 1;
+      s += r.theta_part[(t * 2 + slot) * r.C + c];
+    }
   red[tid] = s;
   __syncthreads();
   if (tid < r.C) {
@@ -608,21 +688,21 @@ __global__ __launch_bounds__(256) void k_reduce_all(ReduceArgs r) {
 inline size_t align256(size_t b) { return (b + 255) & ~(size_t)255; }
 
 struct Layout {
-  int H, NH, F, P;
+  int H, NH, DX, F, P;
   size_t off_wt, off_wg, off_loss, off_theta, total;
 };
 
-template <int H, int NH, int F>
+template <int H, int NH, int DX, int F, int FEAT>
 Layout layout_for(const DiscArgs& a, int n_wg) {
-  using K = Fused<H, NH, F>;
+  using K = Fused<H, NH, DX, F, FEAT>;
   Layout L;
-  L.H = H; L.NH = NH; L.F = F; L.P = K::P;
+  L.H = H; L.NH = NH; L.DX = DX; L.F = F; L.P = K::P;
   const int64_t nft = (a.n_fake + kT - 1) / kT, nrt = (a.n_real + kT - 1) / kT;
   size_t o = 0;
   L.off_wt = o; o += align256(sizeof(float) * NH * H * H);
   L.off_wg = o; o += align256(sizeof(float) * (size_t)n_wg * kWGPerCU * K::P);
   L.off_loss = o; o += align256(sizeof(float) * 2 * (size_t)(nft + nrt));
-  L.off_theta = o; o += align256(sizeof(float) * 2 * F * (size_t)nft);
+  L.off_theta = o; o += align256(sizeof(float) * 2 * 2 * DX * (size_t)nft);
   L.total = o;
   return L;
 }
@@ -630,27 +710,31 @@ Layout layout_for(const DiscArgs& a, int n_wg) {
 typedef void (*KernelFn)(F32Params);
 
 struct Variant {
-  int H, NH, F;
+  int H, NH, DX, F, FEAT;
   KernelFn fn;
   Layout (*layout)(const DiscArgs&, int);
   int P;
 };
 
-#define SAGIPS_F32_VARIANT(H_, NH_, F_) \
-  { H_, NH_, F_, k_disc_f32<H_, NH_, F_>, layout_for<H_, NH_, F_>, Fused<H_, NH_, F_>::P }
+#define SAGIPS_F32_VARIANT(H_, NH_, DX_, F_, FEAT_)                                          \
+  { H_, NH_, DX_, F_, FEAT_, k_disc_f32<H_, NH_, DX_, F_, FEAT_>, layout_for<H_, NH_, DX_, F_, FEAT_>, \
+    Fused<H_, NH_, DX_, F_, FEAT_>::P }
+#define SAGIPS_F32_ID(H_, NH_, D_) SAGIPS_F32_VARIANT(H_, NH_, D_, D_, SAGIPS_FEAT_IDENTITY)
 
 const Variant kVariants[] = {
-    SAGIPS_F32_VARIANT(64, 1, 2),  SAGIPS_F32_VARIANT(64, 2, 2),  SAGIPS_F32_VARIANT(64, 3, 2),
-    SAGIPS_F32_VARIANT(128, 1, 2), SAGIPS_F32_VARIANT(128, 2, 2),
-    SAGIPS_F32_VARIANT(64, 1, 3),  SAGIPS_F32_VARIANT(64, 2, 3),  SAGIPS_F32_VARIANT(128, 2, 3),
+    SAGIPS_F32_ID(64, 1, 2),  SAGIPS_F32_ID(64, 2, 2),  SAGIPS_F32_ID(64, 3, 2),
+    SAGIPS_F32_ID(128, 1, 2), SAGIPS_F32_ID(128, 2, 2),
+    SAGIPS_F32_ID(64, 1, 3),  SAGIPS_F32_ID(64, 2, 3),  SAGIPS_F32_ID(128, 2, 3),
+    // the paper's discriminator, 2 -> 128 -> 128 -> 128 -> 128 -> 1, on the two observables
+    SAGIPS_F32_VARIANT(128, 3, 3, 2, SAGIPS_FEAT_PROXY2),
 };
 
-const Variant* find_variant(const sagips_mlp& D) {
+const Variant* find_variant(const sagips_mlp& D, int d) {
   const int H = D.width[1];
   const int NH = D.n_layers - 2;
   const int F = D.width[0];
   for (const Variant& v : kVariants)
-    if (v.H == H && v.NH == NH && v.F == F) return &v;
+    if (v.H == H && v.NH == NH && v.DX == d && v.F == F && v.FEAT == D.features) return &v;
   return nullptr;
 }
 
@@ -659,28 +743,32 @@ const Variant* find_variant(const sagips_mlp& D) {
 int disc_f32_tile() { return kT; }
 
 bool disc_f32_supported(const sagips_mlp& D, int d, const char** why) {
-  if (D.features != SAGIPS_FEAT_IDENTITY) { *why = "fp32 discriminator supports IDENTITY features only"; return false; }
-  if (D.width[0] != d) { *why = "width[0] must equal d for IDENTITY features"; return false; }
+  if (D.features == SAGIPS_FEAT_HD8) { *why = "fp32 discriminator supports IDENTITY and PROXY2 features"; return false; }
+  if (D.features == SAGIPS_FEAT_IDENTITY && D.width[0] != d) { *why = "width[0] must equal d for IDENTITY features"; return false; }
   if (D.n_layers < 3) { *why = "fp32 discriminator needs at least one hidden-to-hidden layer"; return false; }
   for (int l = 1; l < D.n_layers; ++l)
     if (D.width[l] != D.width[1]) { *why = "all hidden widths must be equal"; return false; }
   if (D.width[D.n_layers] != 1) { *why = "last layer must have width 1"; return false; }
-  if (!find_variant(D)) { *why = "unsupported fp32 shape (hidden width 64 with 1-3 or 128 with 1-2 hidden-to-hidden layers; d 2, or 3 with fewer layers)"; return false; }
+  if (!find_variant(D, d)) {
+    *why = "unsupported fp32 shape (IDENTITY: hidden width 64 with 1-3 or 128 with 1-2 hidden-to-hidden layers, "
+           "d 2, or 3 with fewer layers; PROXY2: hidden width 128 with 3 hidden-to-hidden layers)";
+    return false;
+  }
   return true;
 }
 
 size_t disc_f32_workspace(const DiscArgs& a, int n_cu) {
-  const Variant* v = find_variant(*a.D);
+  const Variant* v = find_variant(*a.D, a.d);
   return v ? v->layout(a, n_cu).total : 0;
 }
 
 hipError_t launch_disc_f32(const DiscArgs& a, void* ws, int n_cu, hipStream_t st, Timer* tm) {
-  const Variant* v = find_variant(*a.D);
+  const Variant* v = find_variant(*a.D, a.d);
   const sagips_mlp& D = *a.D;
   const Layout L = v->layout(a, n_cu);
   char* base = static_cast<char*>(ws);
   float* WT = reinterpret_cast<float*>(base + L.off_wt);
-  const int H = v->H, NH = v->NH, F = v->F;
+  const int H = v->H, NH = v->NH, F = v->F, DX = v->DX;
 
   F32Params p;
   memset(&p, 0, sizeof(p));
@@ -701,7 +789,7 @@ hipError_t launch_disc_f32(const DiscArgs& a, void* ws, int n_cu, hipStream_t st
   p.n_real = a.n_real;
   p.n_fake_tiles = (int)((a.n_fake + kT - 1) / kT);
   p.n_tiles = p.n_fake_tiles + (int)((a.n_real + kT - 1) / kT);
-  p.tiles_per_row = a.fake_src ? (int)(a.fake_src->E / kT) : 0;
+  p.E = a.fake_src ? a.fake_src->E : 1;
   p.inv_nf = 1.0f / (float)a.n_fake;
   p.inv_nr = 1.0f / (float)a.n_real;
   p.logits_fake = a.out->logits_fake;
@@ -754,8 +842,8 @@ hipError_t launch_disc_f32(const DiscArgs& a, void* ws, int n_cu, hipStream_t st
   r.loss_d = a.out->loss_d;
   r.loss_g = a.out->loss_g;
   r.theta_part = p.theta_part;
-  r.tiles_per_row = p.tiles_per_row;
-  r.C = 2 * F;
+  r.E = p.E;
+  r.C = 2 * DX;
   r.dLg_dtheta = a.out->dLg_dtheta;
   const int theta_blocks = (a.fake_src && a.out->dLg_dtheta) ? a.fake_src->n_theta : 0;
   if (tm) tm->begin("disc_f32_reduce");

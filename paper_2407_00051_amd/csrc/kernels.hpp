@@ -65,7 +65,7 @@ struct DiscArgs {
   int d;
 };
 bool disc_f32_supported(const sagips_mlp& D, int d, const char** why);
-int disc_f32_tile();   // events per tile; the in-kernel sampler needs E % tile == 0
+int disc_f32_tile();   // events per tile; the in-kernel sampler needs E >= tile
 size_t disc_f32_workspace(const DiscArgs& a, int n_cu);
 hipError_t launch_disc_f32(const DiscArgs& a, void* ws, int n_cu, hipStream_t st, Timer* tm);
 

@@ -63,7 +63,8 @@ def _fd_theta(fun, theta, h=1e-6):
     return g
 
 
-@pytest.mark.parametrize("features,d,widths", [("identity", 2, (2, 8, 8, 1)), ("hd8", 3, (8, 6, 6, 1))])
+@pytest.mark.parametrize("features,d,widths", [("identity", 2, (2, 8, 8, 1)), ("hd8", 3, (8, 6, 6, 1)),
+                                              ("proxy2", 3, (2, 8, 8, 1))])
 def test_generator_loss_gradient_vs_finite_differences(features, d, widths):
     theta = gen.theta_uniform(2, d, seed=9).astype(np.float64)
     E = 40

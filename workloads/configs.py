@@ -54,6 +54,9 @@ CONFIGS = {
     "medium": Workload("medium", 256, 2, 16384, (2, 256, 256, 256, 256, 1), "bf16", "identity", "uniform"),
     "higher_dim": Workload("higher_dim", 1024, 3, 16384, (8, 512, 512, 512, 512, 1), "bf16", "hd8", "uniform"),
     "stress": Workload("stress", 64, 2, 4194304, None, "f32", "identity", "uniform"),
+    # the paper's own step shape (Sec. V-A, Tab. gen_settings): 1,024 parameter samples of six
+    # parameters x 100 events, the 2-128-128-128-128-1 discriminator on two observables
+    "paper": Workload("paper", 1024, 3, 100, (2, 128, 128, 128, 128, 1), "f32", "proxy2", "uniform"),
 }
 
 
