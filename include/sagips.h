@@ -193,6 +193,52 @@ sagips_status sagips_param_grad(sagips_ctx* ctx, const sagips_source* src, sagip
 sagips_status sagips_bootstrap(sagips_ctx* ctx, const float* data, int64_t n_data, int d, uint64_t seed,
                                uint32_t step, int64_t n_out, float* out, int64_t* idx_out);
 
+/* A stack of M generators of one shape (paper Sec. III: the optimiser is a GAN
+ * generator mapping noise to parameters; Sec. V-A: LeakyReLU hidden layers).
+ * Layer l maps width[l] -> width[l+1]; member m's weight is the
+ * [width[l+1]][width[l]] block at W[l] + m * width[l+1] * width[l] and its
+ * bias the [width[l+1]] block at b[l] + m * width[l+1] (torch.nn.Linear
+ * layout, members stacked in front).  Hidden layers apply
+ * LeakyReLU(leaky_slope); the output is theta = 1 + softplus(last layer).
+ * Supported: 3..5 layers, all hidden widths 128, width[0] and the output
+ * width in [1, 8] (the paper's 51,206-parameter generator is
+ * 6-128-128-128-128-6).  Every W[l], b[l] must be 16-byte aligned.         */
+typedef struct {
+  int32_t n_layers;
+  int32_t width[SAGIPS_MAX_LAYERS + 1];
+  const float* W[SAGIPS_MAX_LAYERS];
+  const float* b[SAGIPS_MAX_LAYERS];
+  int32_t n_members;  /* M >= 1 */
+  float leaky_slope;
+} sagips_gen;
+
+/* 5. Generator forward: theta[m][r] = G_m(noise[r]) for every member m.
+ *   noise  [k][width[0]] fp32, shared by all members, k >= 1
+ *   theta  [M][k][out] fp32                                                */
+sagips_status sagips_gen_forward(sagips_ctx* ctx, const sagips_gen* G, const float* noise, int64_t k,
+                                 float* theta);
+
+/* 6. Generator backward: given dL/dtheta [M][k][out] (e.g. dLg_dtheta of
+ * sagips_disc_fwd_bwd), the gradients of sum_r <dL/dtheta[m][r], theta[m][r]>
+ * with respect to member m's parameters, through 1 + softplus and the
+ * LeakyReLU layers (the generator's step of Sec. III).
+ *   dW[l], db[l]  shaped like W[l], b[l] (all members); overwritten.
+ * The forward pass is recomputed from noise; nothing from sagips_gen_forward
+ * is needed.                                                                */
+sagips_status sagips_gen_backward(sagips_ctx* ctx, const sagips_gen* G, const float* noise, int64_t k,
+                                  const float* dL_dtheta, float* const* dW, float* const* db);
+
+/* 7. Ensemble response (paper Sec. VI-A, eqs. def_ens_mean, def_ens_std and
+ * def_param_res): for each noise vector n_r the member mean
+ * p_hat(n_r) = (1/M) sum_m G_m(n_r) and the spread
+ * sigma(n_r) = sqrt((1/M) sum_m (G_m(n_r) - p_hat(n_r))^2), both averaged
+ * over the k noise vectors; with p_true the normalised residual
+ * r_hat = (p_true - p_hat) / p_true.
+ *   p_hat, sigma  [out] fp32
+ *   p_true, r_hat [out] fp32, both given or both NULL                       */
+sagips_status sagips_ensemble_response(sagips_ctx* ctx, const sagips_gen* G, const float* noise, int64_t k,
+                                       const float* p_true, float* p_hat, float* sigma, float* r_hat);
+
 #ifdef __cplusplus
 }
 #endif

@@ -24,7 +24,7 @@ CRITIC_BUFFER, CRITIC_QUADRATIC = 0, 1
 
 EXPORTED = ("sagips_create", "sagips_destroy", "sagips_set_stream", "sagips_last_error", "sagips_set_timing",
             "sagips_kernel_times", "sagips_sample_events", "sagips_disc_fwd_bwd", "sagips_param_grad",
-            "sagips_bootstrap")
+            "sagips_bootstrap", "sagips_gen_forward", "sagips_gen_backward", "sagips_ensemble_response")
 
 
 class SagipsError(RuntimeError):
@@ -43,6 +43,12 @@ class Mlp(ctypes.Structure):
     _fields_ = [("n_layers", ctypes.c_int32), ("width", ctypes.c_int32 * (MAX_LAYERS + 1)),
                 ("W", ctypes.c_void_p * MAX_LAYERS), ("b", ctypes.c_void_p * MAX_LAYERS),
                 ("leaky_slope", ctypes.c_float), ("precision", ctypes.c_int32), ("features", ctypes.c_int32)]
+
+
+class GenStack(ctypes.Structure):
+    _fields_ = [("n_layers", ctypes.c_int32), ("width", ctypes.c_int32 * (MAX_LAYERS + 1)),
+                ("W", ctypes.c_void_p * MAX_LAYERS), ("b", ctypes.c_void_p * MAX_LAYERS),
+                ("n_members", ctypes.c_int32), ("leaky_slope", ctypes.c_float)]
 
 
 class DiscOut(ctypes.Structure):
@@ -77,9 +83,13 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
                                         ctypes.POINTER(DiscOut)]
     lib.sagips_param_grad.argtypes = [vp, ctypes.POINTER(Source), i32, vp, vp, vp]
     lib.sagips_bootstrap.argtypes = [vp, vp, i64, i32, ctypes.c_uint64, ctypes.c_uint32, i64, vp, vp]
+    lib.sagips_gen_forward.argtypes = [vp, ctypes.POINTER(GenStack), vp, i64, vp]
+    lib.sagips_gen_backward.argtypes = [vp, ctypes.POINTER(GenStack), vp, i64, vp, ctypes.POINTER(vp),
+                                        ctypes.POINTER(vp)]
+    lib.sagips_ensemble_response.argtypes = [vp, ctypes.POINTER(GenStack), vp, i64, vp, vp, vp, vp]
     for name in ("sagips_create", "sagips_destroy", "sagips_set_stream", "sagips_set_timing",
                  "sagips_kernel_times", "sagips_sample_events", "sagips_disc_fwd_bwd", "sagips_param_grad",
-                 "sagips_bootstrap"):
+                 "sagips_bootstrap", "sagips_gen_forward", "sagips_gen_backward", "sagips_ensemble_response"):
         getattr(lib, name).restype = ctypes.c_int
     _lib = lib
     return lib
@@ -209,6 +219,77 @@ class Context:
                                               step & 0xFFFFFFFF, n_out, _ptr(x), _ptr(idx)))
         self._keep = (data,)
         return (x, idx) if want_idx else x
+
+    # -- generator (noise -> parameters) and the ensemble response -------------------
+    def _gen(self, W: Sequence, b: Sequence, slope: float):
+        """GenStack for stacked members: W[l] is [M][out][in] (or [out][in] for one member),
+        b[l] is [M][out] (or [out])."""
+        import torch
+        n_layers = len(W)
+        if n_layers != len(b) or not 2 <= n_layers <= MAX_LAYERS:
+            raise ValueError("W and b must have the same length, 2..8")
+        W3 = [w if w.dim() == 3 else w.unsqueeze(0) for w in W]
+        b2 = [v if v.dim() == 2 else v.unsqueeze(0) for v in b]
+        M = W3[0].shape[0]
+        g = GenStack()
+        g.n_layers = n_layers
+        g.n_members = M
+        g.leaky_slope = float(slope)
+        g.width[0] = W3[0].shape[2]
+        for l in range(n_layers):
+            _check_tensor(W3[l], f"W[{l}]", torch.float32, (M, W3[l].shape[1], g.width[l]), self.device)
+            g.width[l + 1] = W3[l].shape[1]
+            _check_tensor(b2[l], f"b[{l}]", torch.float32, (M, g.width[l + 1]), self.device)
+            g.W[l] = W3[l].data_ptr()
+            g.b[l] = b2[l].data_ptr()
+        return g, M
+
+    def gen_forward(self, W: Sequence, b: Sequence, noise, slope: float = 0.2, out=None):
+        """theta [M][k][out] = 1 + softplus(G_m(noise)) for every member m."""
+        import torch
+        g, M = self._gen(W, b, slope)
+        _check_tensor(noise, "noise", torch.float32, (noise.shape[0], g.width[0]), self.device)
+        k = noise.shape[0]
+        th = out if out is not None else torch.empty((M, k, g.width[g.n_layers]), dtype=torch.float32,
+                                                     device=noise.device)
+        _check_tensor(th, "out", torch.float32, (M, k, g.width[g.n_layers]), self.device)
+        self._check(self.lib.sagips_gen_forward(self.h, ctypes.byref(g), noise.data_ptr(), k, th.data_ptr()))
+        return th
+
+    def gen_backward(self, W: Sequence, b: Sequence, noise, dL_dtheta, slope: float = 0.2, dW=None, db=None):
+        """Gradients (dW, db), shaped like W and b, of sum <dL/dtheta, theta> per member."""
+        import torch
+        g, M = self._gen(W, b, slope)
+        _check_tensor(noise, "noise", torch.float32, (noise.shape[0], g.width[0]), self.device)
+        k = noise.shape[0]
+        _check_tensor(dL_dtheta, "dL_dtheta", torch.float32, (M, k, g.width[g.n_layers]) if dL_dtheta.dim() == 3
+                      else (k, g.width[g.n_layers]), self.device)
+        dW = dW if dW is not None else [torch.empty_like(w) for w in W]
+        db = db if db is not None else [torch.empty_like(v) for v in b]
+        for l in range(g.n_layers):
+            _check_tensor(dW[l], f"dW[{l}]", torch.float32, tuple(W[l].shape), self.device)
+            _check_tensor(db[l], f"db[{l}]", torch.float32, tuple(b[l].shape), self.device)
+        pw = (ctypes.c_void_p * MAX_LAYERS)(*[t.data_ptr() for t in dW])
+        pb = (ctypes.c_void_p * MAX_LAYERS)(*[t.data_ptr() for t in db])
+        self._check(self.lib.sagips_gen_backward(self.h, ctypes.byref(g), noise.data_ptr(), k,
+                                                 dL_dtheta.data_ptr(), pw, pb))
+        return dW, db
+
+    def ensemble_response(self, W: Sequence, b: Sequence, noise, p_true=None, slope: float = 0.2) -> dict:
+        """p_hat and sigma [out] averaged over the noise batch, and r_hat = (p_true - p_hat) / p_true."""
+        import torch
+        g, M = self._gen(W, b, slope)
+        _check_tensor(noise, "noise", torch.float32, (noise.shape[0], g.width[0]), self.device)
+        n_out = g.width[g.n_layers]
+        f32 = dict(dtype=torch.float32, device=noise.device)
+        o = {"p_hat": torch.empty(n_out, **f32), "sigma": torch.empty(n_out, **f32), "r_hat": None}
+        if p_true is not None:
+            _check_tensor(p_true, "p_true", torch.float32, (n_out,), self.device)
+            o["r_hat"] = torch.empty(n_out, **f32)
+        self._check(self.lib.sagips_ensemble_response(self.h, ctypes.byref(g), noise.data_ptr(), noise.shape[0],
+                                                      _ptr(p_true), o["p_hat"].data_ptr(), o["sigma"].data_ptr(),
+                                                      _ptr(o["r_hat"])))
+        return o
 
     # -- 2. events -> discriminator -> BCE -> backward -------------------------------
     def disc_fwd_bwd(self, W: Sequence, b: Sequence, real_x, fake_x=None, fake_source: Optional[dict] = None,

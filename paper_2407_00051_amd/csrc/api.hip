@@ -186,6 +186,24 @@ sagips_status disc_bf16(sagips_ctx* c, const sagips_mlp* D, const float* fake_x,
   return SAGIPS_OK;
 }
 
+sagips_status check_gen(sagips_ctx* c, const sagips_gen* G, const float* noise, int64_t k) {
+  if (!G) return fail(c, SAGIPS_E_INVAL, "G is NULL");
+  if (!noise) return fail(c, SAGIPS_E_INVAL, "noise is NULL");
+  if (G->n_members < 1 || G->n_members > 65535) return fail(c, SAGIPS_E_INVAL, "n_members = %d outside [1, 65535]", G->n_members);
+  if (G->n_layers < 2 || G->n_layers > SAGIPS_MAX_LAYERS)
+    return fail(c, SAGIPS_E_INVAL, "n_layers = %d outside [2, %d]", G->n_layers, SAGIPS_MAX_LAYERS);
+  for (int l = 0; l <= G->n_layers; ++l)
+    if (G->width[l] < 1) return fail(c, SAGIPS_E_INVAL, "width[%d] < 1", l);
+  for (int l = 0; l < G->n_layers; ++l) {
+    if (!G->W[l] || !G->b[l]) return fail(c, SAGIPS_E_INVAL, "W[%d] or b[%d] is NULL", l, l);
+    if (!aligned16(G->W[l]) || !aligned16(G->b[l])) return fail(c, SAGIPS_E_INVAL, "W[%d] or b[%d] is not 16-byte aligned", l, l);
+  }
+  if (k < 1 || k >= ((int64_t)1 << 30)) return fail(c, SAGIPS_E_INVAL, "k = %lld outside [1, 2^30)", (long long)k);
+  const char* why = nullptr;
+  if (!sagips::gen_supported(*G, &why)) return fail(c, SAGIPS_E_UNSUPPORTED, "%s", why);
+  return SAGIPS_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -421,6 +439,47 @@ sagips_status sagips_bootstrap(sagips_ctx* c, const float* data, int64_t n_data,
   hipError_t e = launch_bootstrap(data, (uint64_t)n_data, d, (uint32_t)(seed & 0xffffffffu), (uint32_t)(seed >> 32),
                                   step, n_out, out, idx_out, c->n_cu, c->stream, timer_of(c));
   return e == hipSuccess ? SAGIPS_OK : hip_fail(c, e, "bootstrap launch");
+}
+
+sagips_status sagips_gen_forward(sagips_ctx* c, const sagips_gen* G, const float* noise, int64_t k, float* theta) {
+  if (!c) return fail(nullptr, SAGIPS_E_INVAL, "ctx is NULL");
+  sagips_status s = check_gen(c, G, noise, k);
+  if (s != SAGIPS_OK) return s;
+  if (!theta) return fail(c, SAGIPS_E_INVAL, "theta is NULL");
+  DeviceGuard g(c->device);
+  hipError_t e = launch_gen_forward(*G, noise, k, theta, c->stream, timer_of(c));
+  return e == hipSuccess ? SAGIPS_OK : hip_fail(c, e, "gen_forward launch");
+}
+
+sagips_status sagips_gen_backward(sagips_ctx* c, const sagips_gen* G, const float* noise, int64_t k,
+                                  const float* dL_dtheta, float* const* dW, float* const* db) {
+  if (!c) return fail(nullptr, SAGIPS_E_INVAL, "ctx is NULL");
+  sagips_status s = check_gen(c, G, noise, k);
+  if (s != SAGIPS_OK) return s;
+  if (!dL_dtheta || !dW || !db) return fail(c, SAGIPS_E_INVAL, "dL_dtheta, dW or db is NULL");
+  for (int l = 0; l < G->n_layers; ++l)
+    if (!dW[l] || !db[l]) return fail(c, SAGIPS_E_INVAL, "dW[%d] or db[%d] is NULL", l, l);
+  DeviceGuard g(c->device);
+  s = ensure_ws(c, gen_backward_workspace(*G, k));
+  if (s != SAGIPS_OK) return s;
+  hipError_t e = launch_gen_backward(*G, noise, k, dL_dtheta, dW, db, c->ws, c->stream, timer_of(c));
+  return e == hipSuccess ? SAGIPS_OK : hip_fail(c, e, "gen_backward launch");
+}
+
+sagips_status sagips_ensemble_response(sagips_ctx* c, const sagips_gen* G, const float* noise, int64_t k,
+                                       const float* p_true, float* p_hat, float* sigma, float* r_hat) {
+  if (!c) return fail(nullptr, SAGIPS_E_INVAL, "ctx is NULL");
+  sagips_status s = check_gen(c, G, noise, k);
+  if (s != SAGIPS_OK) return s;
+  if (!p_hat || !sigma) return fail(c, SAGIPS_E_INVAL, "p_hat or sigma is NULL");
+  if ((p_true == nullptr) != (r_hat == nullptr)) return fail(c, SAGIPS_E_INVAL, "p_true and r_hat must be given together");
+  if ((int64_t)G->n_members * k * G->width[G->n_layers] >= ((int64_t)1 << 31))
+    return fail(c, SAGIPS_E_INVAL, "n_members * k * output width must be < 2^31");
+  DeviceGuard g(c->device);
+  s = ensure_ws(c, ensemble_workspace(*G, k));
+  if (s != SAGIPS_OK) return s;
+  hipError_t e = launch_ensemble(*G, noise, k, p_true, p_hat, sigma, r_hat, c->ws, c->stream, timer_of(c));
+  return e == hipSuccess ? SAGIPS_OK : hip_fail(c, e, "ensemble launch");
 }
 
 }  // extern "C"

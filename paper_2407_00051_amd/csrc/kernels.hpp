@@ -69,6 +69,18 @@ int disc_f32_tile();   // events per tile; the in-kernel sampler needs E >= tile
 size_t disc_f32_workspace(const DiscArgs& a, int n_cu);
 hipError_t launch_disc_f32(const DiscArgs& a, void* ws, int n_cu, hipStream_t st, Timer* tm);
 
+// generator.hip --------------------------------------------------------------
+constexpr int kMaxGenLayers = 5;
+bool gen_supported(const sagips_gen& G, const char** why);
+size_t gen_backward_workspace(const sagips_gen& G, int64_t k);
+size_t ensemble_workspace(const sagips_gen& G, int64_t k);
+hipError_t launch_gen_forward(const sagips_gen& G, const float* noise, int64_t k, float* theta, hipStream_t st,
+                              Timer* tm);
+hipError_t launch_gen_backward(const sagips_gen& G, const float* noise, int64_t k, const float* dtheta,
+                               float* const* dW, float* const* db, void* ws, hipStream_t st, Timer* tm);
+hipError_t launch_ensemble(const sagips_gen& G, const float* noise, int64_t k, const float* p_true, float* p_hat,
+                           float* sigma, float* r_hat, void* ws, hipStream_t st, Timer* tm);
+
 // disc_bf16.hip --------------------------------------------------------------
 // Samples the fake events itself when a.fake_src is set (any E); never writes dLg_dtheta.
 bool disc_bf16_supported(const sagips_mlp& D, int d, const char** why);

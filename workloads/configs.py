@@ -87,8 +87,35 @@ BOOTSTRAP_CONFIGS = {
 }
 
 
+@dataclass(frozen=True)
+class EnsembleWorkload:
+    """Ensemble response of M generators on a batch of k noise vectors (Sec. VI-A).
+
+    The paper's generator is 6-128-128-128-128-6 (51,206 parameters); its
+    ensembles hold 20 members, one of them 100, and each generator predicts
+    1,024 parameter samples per step."""
+    name: str
+    n_members: int
+    k: int
+    widths: Tuple[int, ...] = (6, 128, 128, 128, 128, 6)
+    weight_seed: int = 21
+    noise_seed: int = 22
+
+    @property
+    def theta_star(self) -> Tuple[float, ...]:
+        return (2.0, 5.0, 1.5, 3.0, 3.0, 2.0)
+
+
+ENSEMBLE_CONFIGS = {
+    "ensemble": EnsembleWorkload("ensemble", 100, 1024),
+}
+
+
 def get(name: str):
-    return CONFIGS[name] if name in CONFIGS else BOOTSTRAP_CONFIGS[name]
+    for table in (CONFIGS, BOOTSTRAP_CONFIGS, ENSEMBLE_CONFIGS):
+        if name in table:
+            return table[name]
+    raise KeyError(name)
 
 
 def scaled(w: Workload, n_theta: Optional[int] = None, events_per_theta: Optional[int] = None) -> Workload:

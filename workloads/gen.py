@@ -60,6 +60,24 @@ def xavier_mlp(widths, seed: int = 2):
     return Ws, bs
 
 
+def generator_stack(widths, n_members: int, seed: int = 21, slope: float = 0.2):
+    """Parameters of n_members generators, stacked member-major: W[l] is
+    [M][out][in] ~ Kaiming-normal for LeakyReLU(slope) (the paper's init,
+    Sec. V-A), b[l] is [M][out] ~ U(-1/sqrt(fan_in), 1/sqrt(fan_in)).  float32."""
+    rng = np.random.default_rng(seed)
+    gain = np.sqrt(2.0 / (1.0 + slope ** 2))
+    Ws, bs = [], []
+    for fi, fo in zip(widths[:-1], widths[1:]):
+        Ws.append((rng.standard_normal((n_members, fo, fi)) * (gain / np.sqrt(fi))).astype(np.float32))
+        bs.append(rng.uniform(-1.0 / np.sqrt(fi), 1.0 / np.sqrt(fi), (n_members, fo)).astype(np.float32))
+    return Ws, bs
+
+
+def noise(k: int, dim: int, seed: int = 22) -> np.ndarray:
+    """Generator input noise [k][dim] ~ N(0, 1), float32."""
+    return np.random.default_rng(seed).standard_normal((k, dim)).astype(np.float32)
+
+
 def make_inputs(w: Workload) -> dict:
     """All seeded inputs of one workload: theta, theta*, weights and seeds."""
     if w.theta_source == "generator":
