@@ -37,6 +37,8 @@ Parity status per function (what pins it, see tests/test_oracle_*.py):
   ensemble response  pinned: M = 1 and identical members (sigma = 0), the
                      M = 2 closed form |G1 - G2| / 2, numpy's population
                      standard deviation, member-order invariance.
+  adam_step          pinned: torch.optim.Adam (float64) over several steps,
+                     the first step's closed form lr g / (|g| + eps).
   bootstrap          pinned: row ranges, the power-of-two case as a bit
                      shift, the with-replacement statistics (unique
                      fraction 1 - (1 - 1/n)^m, per-row counts binomial),
@@ -49,4 +51,5 @@ from .sampler import (uniform_from_words, kumaraswamy_icdf, kumaraswamy_cdf,  # 
 from .mlp import mlp_forward, bce_losses, disc_fwd_bwd, round_bf16, input_grad_kink_variants  # noqa: F401
 from .step import param_grad, quadratic_critic, run_step  # noqa: F401
 from .bootstrap import bootstrap, bootstrap_indices, STREAM_BOOTSTRAP  # noqa: F401
+from .optim import adam_step  # noqa: F401
 from .generator import G_WIDTHS, generator_forward, generator_backward, ensemble_response, residual  # noqa: F401
