@@ -39,6 +39,11 @@ Parity status per function (what pins it, see tests/test_oracle_*.py):
                      standard deviation, member-order invariance.
   adam_step          pinned: torch.optim.Adam (float64) over several steps,
                      the first step's closed form lr g / (|g| + eps).
+  gan_step           pinned: the generator gradient by finite differences
+                     through generator, sampler, pipeline and discriminator;
+                     lr = 0 leaves the parameters and sets the moments to
+                     (1 - beta) g, (1 - beta2) g^2; both networks move
+                     against their gradients.
   bootstrap          pinned: row ranges, the power-of-two case as a bit
                      shift, the with-replacement statistics (unique
                      fraction 1 - (1 - 1/n)^m, per-row counts binomial),
@@ -52,4 +57,5 @@ from .mlp import mlp_forward, bce_losses, disc_fwd_bwd, round_bf16, input_grad_k
 from .step import param_grad, quadratic_critic, run_step  # noqa: F401
 from .bootstrap import bootstrap, bootstrap_indices, STREAM_BOOTSTRAP  # noqa: F401
 from .optim import adam_step  # noqa: F401
+from .gan import gan_step, initial_state  # noqa: F401
 from .generator import G_WIDTHS, generator_forward, generator_backward, ensemble_response, residual  # noqa: F401
