@@ -239,6 +239,29 @@ sagips_status sagips_gen_backward(sagips_ctx* ctx, const sagips_gen* G, const fl
 sagips_status sagips_ensemble_response(sagips_ctx* ctx, const sagips_gen* G, const float* noise, int64_t k,
                                        const float* p_true, float* p_hat, float* sigma, float* r_hat);
 
+/* 8. Optimiser step (Sec. V-A gives the learning rates, generator 1e-5 and
+ * discriminator 1e-4, not the optimiser; this library reads it as Adam,
+ * Kingma and Ba 2015, Algorithm 1): for t = step >= 1, every element of every
+ * tensor of the set gets
+ *   m <- beta1 m + (1 - beta1) g,  v <- beta2 v + (1 - beta2) g^2,
+ *   p <- p - lr / (1 - beta1^t) * m / (sqrt(v) / sqrt(1 - beta2^t) + eps).
+ * param, m, v are updated in place (m, v start at zero); grad is read only.
+ * Every array holds size[i] fp32 elements; 1 <= n_tensors <= 16.
+ * 0 <= beta1, beta2 < 1, eps >= 0, lr >= 0.  The scalars are double so that
+ * 1 - beta and the bias corrections are formed before rounding to fp32.   */
+#define SAGIPS_MAX_TENSORS 16
+typedef struct {
+  int32_t n_tensors;
+  float* param[SAGIPS_MAX_TENSORS];
+  const float* grad[SAGIPS_MAX_TENSORS];
+  float* m[SAGIPS_MAX_TENSORS];
+  float* v[SAGIPS_MAX_TENSORS];
+  int64_t size[SAGIPS_MAX_TENSORS];
+} sagips_param_set;
+
+sagips_status sagips_adam_step(sagips_ctx* ctx, const sagips_param_set* set, int32_t step, double lr,
+                               double beta1, double beta2, double eps);
+
 #ifdef __cplusplus
 }
 #endif

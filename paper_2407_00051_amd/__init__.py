@@ -16,6 +16,7 @@ from typing import Dict, List, Optional, Sequence
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libsagips.so")
 MAX_LAYERS = 8
+MAX_TENSORS = 16
 
 OK, E_INVAL, E_ARCH, E_NOMEM, E_HIP, E_UNSUPPORTED = 0, -1, -2, -3, -4, -5
 F32, BF16 = 0, 1
@@ -24,7 +25,8 @@ CRITIC_BUFFER, CRITIC_QUADRATIC = 0, 1
 
 EXPORTED = ("sagips_create", "sagips_destroy", "sagips_set_stream", "sagips_last_error", "sagips_set_timing",
             "sagips_kernel_times", "sagips_sample_events", "sagips_disc_fwd_bwd", "sagips_param_grad",
-            "sagips_bootstrap", "sagips_gen_forward", "sagips_gen_backward", "sagips_ensemble_response")
+            "sagips_bootstrap", "sagips_gen_forward", "sagips_gen_backward", "sagips_ensemble_response",
+            "sagips_adam_step")
 
 
 class SagipsError(RuntimeError):
@@ -49,6 +51,12 @@ class GenStack(ctypes.Structure):
     _fields_ = [("n_layers", ctypes.c_int32), ("width", ctypes.c_int32 * (MAX_LAYERS + 1)),
                 ("W", ctypes.c_void_p * MAX_LAYERS), ("b", ctypes.c_void_p * MAX_LAYERS),
                 ("n_members", ctypes.c_int32), ("leaky_slope", ctypes.c_float)]
+
+
+class ParamSet(ctypes.Structure):
+    _fields_ = [("n_tensors", ctypes.c_int32), ("param", ctypes.c_void_p * MAX_TENSORS),
+                ("grad", ctypes.c_void_p * MAX_TENSORS), ("m", ctypes.c_void_p * MAX_TENSORS),
+                ("v", ctypes.c_void_p * MAX_TENSORS), ("size", ctypes.c_int64 * MAX_TENSORS)]
 
 
 class DiscOut(ctypes.Structure):
@@ -87,9 +95,12 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.sagips_gen_backward.argtypes = [vp, ctypes.POINTER(GenStack), vp, i64, vp, ctypes.POINTER(vp),
                                         ctypes.POINTER(vp)]
     lib.sagips_ensemble_response.argtypes = [vp, ctypes.POINTER(GenStack), vp, i64, vp, vp, vp, vp]
+    lib.sagips_adam_step.argtypes = [vp, ctypes.POINTER(ParamSet), i32, ctypes.c_double, ctypes.c_double,
+                                     ctypes.c_double, ctypes.c_double]
     for name in ("sagips_create", "sagips_destroy", "sagips_set_stream", "sagips_set_timing",
                  "sagips_kernel_times", "sagips_sample_events", "sagips_disc_fwd_bwd", "sagips_param_grad",
-                 "sagips_bootstrap", "sagips_gen_forward", "sagips_gen_backward", "sagips_ensemble_response"):
+                 "sagips_bootstrap", "sagips_gen_forward", "sagips_gen_backward", "sagips_ensemble_response",
+                 "sagips_adam_step"):
         getattr(lib, name).restype = ctypes.c_int
     _lib = lib
     return lib
@@ -290,6 +301,24 @@ class Context:
                                                       _ptr(p_true), o["p_hat"].data_ptr(), o["sigma"].data_ptr(),
                                                       _ptr(o["r_hat"])))
         return o
+
+    # -- optimiser ------------------------------------------------------------------
+    def adam_step(self, params: Sequence, grads: Sequence, m: Sequence, v: Sequence, step: int, lr: float,
+                  beta1: float = 0.9, beta2: float = 0.999, eps: float = 1e-8) -> None:
+        """In-place Adam step on up to 16 fp32 tensors (m, v start at zero; step counts from 1)."""
+        import torch
+        n = len(params)
+        if not (n == len(grads) == len(m) == len(v)) or not 1 <= n <= MAX_TENSORS:
+            raise ValueError("params, grads, m, v must have the same length, 1..16")
+        ps = ParamSet()
+        ps.n_tensors = n
+        for i in range(n):
+            for t, name in ((params[i], "param"), (grads[i], "grad"), (m[i], "m"), (v[i], "v")):
+                _check_tensor(t, f"{name}[{i}]", torch.float32, tuple(params[i].shape), self.device)
+            ps.param[i], ps.grad[i] = params[i].data_ptr(), grads[i].data_ptr()
+            ps.m[i], ps.v[i] = m[i].data_ptr(), v[i].data_ptr()
+            ps.size[i] = params[i].numel()
+        self._check(self.lib.sagips_adam_step(self.h, ctypes.byref(ps), int(step), lr, beta1, beta2, eps))
 
     # -- 2. events -> discriminator -> BCE -> backward -------------------------------
     def disc_fwd_bwd(self, W: Sequence, b: Sequence, real_x, fake_x=None, fake_source: Optional[dict] = None,

@@ -15,7 +15,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 OBJ = os.path.join(CSRC, "_build")
 LIB = os.path.join(HERE, "libsagips.so")
-SOURCES = ["api.hip", "sampler.hip", "disc_f32.hip", "disc_bf16.hip", "generator.hip"]
+SOURCES = ["api.hip", "sampler.hip", "disc_f32.hip", "disc_bf16.hip", "generator.hip", "optim.hip"]
 
 HIPCC_FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",

@@ -482,4 +482,23 @@ sagips_status sagips_ensemble_response(sagips_ctx* c, const sagips_gen* G, const
   return e == hipSuccess ? SAGIPS_OK : hip_fail(c, e, "ensemble launch");
 }
 
+sagips_status sagips_adam_step(sagips_ctx* c, const sagips_param_set* ps, int32_t step, double lr, double beta1,
+                               double beta2, double eps) {
+  if (!c) return fail(nullptr, SAGIPS_E_INVAL, "ctx is NULL");
+  if (!ps) return fail(c, SAGIPS_E_INVAL, "set is NULL");
+  if (ps->n_tensors < 1 || ps->n_tensors > SAGIPS_MAX_TENSORS)
+    return fail(c, SAGIPS_E_INVAL, "n_tensors = %d outside [1, %d]", ps->n_tensors, SAGIPS_MAX_TENSORS);
+  for (int i = 0; i < ps->n_tensors; ++i) {
+    if (!ps->param[i] || !ps->grad[i] || !ps->m[i] || !ps->v[i])
+      return fail(c, SAGIPS_E_INVAL, "tensor %d has a NULL array", i);
+    if (ps->size[i] < 0) return fail(c, SAGIPS_E_INVAL, "size[%d] < 0", i);
+  }
+  if (step < 1) return fail(c, SAGIPS_E_INVAL, "step must be >= 1");
+  if (!(lr >= 0.0) || !(beta1 >= 0.0 && beta1 < 1.0) || !(beta2 >= 0.0 && beta2 < 1.0) || !(eps >= 0.0))
+    return fail(c, SAGIPS_E_INVAL, "need lr >= 0, 0 <= beta1, beta2 < 1, eps >= 0");
+  DeviceGuard g(c->device);
+  hipError_t e = launch_adam(*ps, step, lr, beta1, beta2, eps, c->stream, timer_of(c));
+  return e == hipSuccess ? SAGIPS_OK : hip_fail(c, e, "adam launch");
+}
+
 }  // extern "C"

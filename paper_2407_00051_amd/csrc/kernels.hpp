@@ -81,6 +81,10 @@ hipError_t launch_gen_backward(const sagips_gen& G, const float* noise, int64_t 
 hipError_t launch_ensemble(const sagips_gen& G, const float* noise, int64_t k, const float* p_true, float* p_hat,
                            float* sigma, float* r_hat, void* ws, hipStream_t st, Timer* tm);
 
+// optim.hip ------------------------------------------------------------------
+hipError_t launch_adam(const sagips_param_set& ps, int step, double lr, double beta1, double beta2, double eps,
+                       hipStream_t st, Timer* tm);
+
 // disc_bf16.hip --------------------------------------------------------------
 // Samples the fake events itself when a.fake_src is set (any E); never writes dLg_dtheta.
 bool disc_bf16_supported(const sagips_mlp& D, int d, const char** why);
