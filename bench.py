@@ -38,6 +38,7 @@ KERNEL_SOURCES = {
     "bf16_wgrad": ["paper_2407_00051_amd/csrc/disc_bf16.hip", "paper_2407_00051_amd/csrc/device_math.hpp"],
     "param_grad": ["paper_2407_00051_amd/csrc/sampler.hip", "paper_2407_00051_amd/csrc/device_math.hpp"],
     "bootstrap": ["paper_2407_00051_amd/csrc/sampler.hip", "paper_2407_00051_amd/csrc/device_math.hpp"],
+    "gen_forward": ["paper_2407_00051_amd/csrc/generator.hip", "paper_2407_00051_amd/csrc/device_math.hpp"],
 }
 
 
@@ -195,6 +196,177 @@ def bench_bootstrap(args, w, ctx, torch):
     print(json.dumps(line), flush=True)
 
 
+def gen_flops_per_row(widths) -> int:
+    """Forward flops of one generator on one noise vector: 2 * sum in*out."""
+    return 2 * sum(a * b for a, b in zip(widths[:-1], widths[1:]))
+
+
+def cpu_baseline_ensemble(w, W, b, n, min_seconds: float = 10.0):
+    """The oracle's ensemble response (every member's forward, then the statistics), as it stands."""
+    import numpy as np
+    import oracle
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        threads = os.cpu_count()
+    M = min(w.n_members, 20)
+    reps, t0 = 0, time.perf_counter()
+    while True:
+        th = np.stack([oracle.generator_forward([x[m] for x in W], [v[m] for v in b], n) for m in range(M)])
+        oracle.ensemble_response(th)
+        reps += 1
+        dt = time.perf_counter() - t0
+        if dt >= min_seconds:
+            break
+    return {"value": reps * M * w.k / dt, "unit": "member-predictions/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"{M} of the {w.n_members} members x {w.k} noise vectors, float64 numpy, "
+                      f"{reps} repetition(s) in {dt:.1f} s"}
+
+
+def bench_ensemble(args, w, ctx, torch):
+    """Steps of the ensemble response: every member's forward on the noise batch, the
+    per-vector mean and spread over members, their batch averages and the residuals."""
+    from workloads import gen
+    dev = "cuda:0"
+    W, b = gen.generator_stack(w.widths, w.n_members, w.weight_seed)
+    n = gen.noise(w.k, w.widths[0], w.noise_seed)
+    Wd = [torch.tensor(x, device=dev) for x in W]
+    bd = [torch.tensor(x, device=dev) for x in b]
+    nd = torch.tensor(n, device=dev)
+    pt = torch.tensor(w.theta_star, dtype=torch.float32, device=dev)
+
+    def step():
+        ctx.ensemble_response(Wd, bd, nd, p_true=pt)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    ctx.kernel_times()
+    ctx.set_timing(True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    ctx.set_timing(False)
+    kt = ctx.kernel_times()
+    ms_per_step = (t1 - t0) * 1e3 / args.steps
+    launches, total_ms = kt["gen_forward"]
+    avg_ms = total_ms / launches
+    flops = gen_flops_per_row(w.widths) * w.n_members * w.k
+    achieved = flops / (avg_ms * 1e-3)
+    roof = {"bound": "mfma", "achieved": achieved / 1e12, "peak": PEAK["mfma_f32"] / 1e12, "unit": "TFLOP/s",
+            "frac": achieved / PEAK["mfma_f32"], "traffic": read_traffic("gen_forward", w.name),
+            "kernel": "gen_forward", "kernel_avg_ms": avg_ms,
+            "kernels": {k: {"launches": c, "avg_ms": t / max(c, 1)} for k, (c, t) in kt.items()}}
+    line = {
+        "metric": "member-predictions/sec of the ensemble response (p_hat, sigma, r_hat); % of fp32 MFMA peak",
+        "value": w.n_members * w.k / (ms_per_step * 1e-3), "unit": "member-predictions/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_per_step, "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+        "data": "synthetic (Kaiming-normal generators, N(0,1) noise)",
+        "config": {"workload": w.name, "n_members": w.n_members, "k": w.k, "widths": list(w.widths),
+                   "parallelism": "single GPU"},
+        "roofline": roof,
+    }
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"] = cpu_baseline_ensemble(w, W, b, n)
+    ctx.close()
+    print(json.dumps(line), flush=True)
+
+
+def cpu_baseline_train(w, rows: int, min_seconds: float = 10.0):
+    """The oracle's whole GAN step, as it stands, on `rows` of the k noise vectors."""
+    import numpy as np
+    import oracle
+    from workloads import gen
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        threads = os.cpu_count()
+    GW, Gb = gen.generator_stack(w.g_widths, 1, w.seed + 21)
+    DW, Db = gen.xavier_mlp(w.d_widths, w.seed + 2)
+    state = oracle.initial_state([x[0] for x in GW], [x[0] for x in Gb], DW, Db)
+    N = rows * w.events_per_theta
+    pool = oracle.sample(np.asarray([w.theta_star]), 2 * N, w.seed + 1)
+    rng = np.random.default_rng(w.seed + 22)
+    reps, t0 = 0, time.perf_counter()
+    while True:
+        r = oracle.gan_step(state, rng.standard_normal((rows, 6)), pool, reps + 1, w.events_per_theta,
+                            w.seed, w.seed + 5)
+        state = r["state"]
+        reps += 1
+        dt = time.perf_counter() - t0
+        if dt >= min_seconds:
+            break
+    return {"value": reps * N / dt, "unit": "events/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"{rows} of {w.k} parameter samples x {w.events_per_theta} events per step ({N} fake + {N} "
+                      f"bootstrapped reference events), float64 numpy, {reps} step(s) in {dt:.1f} s"}
+
+
+def bench_train(args, w, ctx, torch, sg):
+    """Steps of GAN training at the paper's shape: generator forward, bootstrap of the
+    reference batch, the fused discriminator step, generator backward, Adam on both."""
+    import numpy as np
+    from paper_2407_00051_amd.gan import GanLoop
+    from workloads import gen
+    dev = "cuda:0"
+    N = w.n_events
+    ts = torch.tensor([w.theta_star], dtype=torch.float32, device=dev)
+    pool = ctx.sample_events(ts, 2 * N, w.seed + 1)
+    GW, Gb = gen.generator_stack(w.g_widths, 1, w.seed + 21)
+    DW, Db = gen.xavier_mlp(w.d_widths, w.seed + 2)
+    loop = GanLoop(ctx, [torch.tensor(x[0], device=dev) for x in GW], [torch.tensor(x[0], device=dev) for x in Gb],
+                   [torch.tensor(x, device=dev) for x in DW], [torch.tensor(x, device=dev) for x in Db], pool,
+                   w.k, w.events_per_theta, fake_seed=w.seed, boot_seed=w.seed + 5)
+    rng = np.random.default_rng(w.seed + 22)
+    noise = torch.tensor(rng.standard_normal((args.warmup + args.steps, w.k, w.g_widths[0])).astype(np.float32),
+                         device=dev)                                    # resident before timing
+    for i in range(args.warmup):
+        loop.step(noise[i])
+    torch.cuda.synchronize()
+    ctx.kernel_times()
+    ctx.set_timing(True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        loop.step(noise[args.warmup + i])
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    ctx.set_timing(False)
+    kt = ctx.kernel_times()
+    ms_per_step = (t1 - t0) * 1e3 / args.steps
+    launches, total_ms = kt["disc_f32_fused"]
+    avg_ms = total_ms / launches
+    flops = mlp_flops_per_fake_event(w.d_widths) * N
+    achieved = flops / (avg_ms * 1e-3)
+    g_flops = 4 * gen_flops_per_row(w.g_widths) * w.k      # forward, recomputed forward, backward (2x)
+    roof = {"bound": "mfma", "achieved": achieved / 1e12, "peak": PEAK["mfma_f32"] / 1e12, "unit": "TFLOP/s",
+            "frac": achieved / PEAK["mfma_f32"], "traffic": read_traffic("disc_f32_fused", w.name),
+            "step_mfma_frac": (flops + g_flops) / (ms_per_step * 1e-3) / PEAK["mfma_f32"],
+            "kernel": "disc_f32_fused", "kernel_avg_ms": avg_ms,
+            "kernels": {k: {"launches": c, "avg_ms": t / max(c, 1)} for k, (c, t) in kt.items()}}
+    line = {
+        "metric": "events/sec per GAN training step (generator, bootstrap, discriminator, backward, Adam); "
+                  "% of fp32 MFMA peak",
+        "value": N / (ms_per_step * 1e-3), "unit": "events/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": ms_per_step, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "f32",
+        "data": "synthetic (Kumaraswamy reference pool at theta*, Kaiming/Xavier-initialised networks, N(0,1) noise)",
+        "config": {"workload": w.name, "k": w.k, "events_per_theta": w.events_per_theta, "fake_events": N,
+                   "real_events": N, "pool_events": 2 * N, "g_widths": list(w.g_widths),
+                   "d_widths": list(w.d_widths), "features": "proxy2", "parallelism": "single GPU"},
+        "roofline": roof,
+    }
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"] = cpu_baseline_train(w, min(args.cpu_rows, w.k))
+    ctx.close()
+    print(json.dumps(line), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -229,8 +401,12 @@ def main():
         b.copy_(a)
         torch.cuda.synchronize()
         del a, b
-    if not hasattr(w, "widths"):
+    if hasattr(w, "n_data"):
         return bench_bootstrap(args, w, ctx, torch)
+    if hasattr(w, "n_members"):
+        return bench_ensemble(args, w, ctx, torch)
+    if hasattr(w, "g_widths"):
+        return bench_train(args, w, ctx, torch, sg)
     inp = gen.make_inputs(w)
     theta = torch.tensor(inp["theta"], device=dev)
     theta_star = torch.tensor(inp["theta_star"], device=dev)

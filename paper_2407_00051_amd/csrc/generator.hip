@@ -40,6 +40,25 @@ __device__ __forceinline__ float g_leaky_grad(float h, float s) { return h > 0.0
 __device__ __forceinline__ float g_softplus(float t) { return fmaxf(t, 0.0f) + log1pf(expf(-fabsf(t))); }
 __device__ __forceinline__ float g_sigmoid(float t) { return 1.0f / (1.0f + expf(-t)); }
 
+// Workgroups are numbered L = x + y * gridDim.x and dealt to the 8 XCDs in
+// turn (XCD = L mod 8); each XCD has its own L2.  The first 8 * floor(M / 8)
+// members are placed so that all tiles of a member run on one XCD (member =
+// 8 (j / tiles) + L mod 8, tile = j mod tiles, j = L / 8), so its weights are
+// fetched into one L2 only; the remaining members are laid out in order.
+__device__ __forceinline__ void gen_block(int tiles, int members, int& m, int& tile) {
+  const int L = blockIdx.x + blockIdx.y * gridDim.x;
+  const int m8 = members - members % 8;
+  if (L < tiles * m8) {
+    const int j = L >> 3;
+    m = 8 * (j / tiles) + (L & 7);
+    tile = j % tiles;
+  } else {
+    const int r = L - tiles * m8;
+    m = m8 + r / tiles;
+    tile = r % tiles;
+  }
+}
+
 struct GenParams {
   const float* W[kMaxGenLayers];   // layer l of member 0; member m at + m * wsz[l]
   const float* b[kMaxGenLayers];
@@ -178,8 +197,9 @@ struct Gen {
 
   static __device__ void run_forward(const GenParams& p) {
     __shared__ Smem sm;
-    const int m = blockIdx.y;
-    const int64_t row0 = (int64_t)blockIdx.x * kGT;
+    int m, tile;
+    gen_block(gridDim.x, gridDim.y, m, tile);
+    const int64_t row0 = (int64_t)tile * kGT;
     forward(p, sm, m, row0);
     for (int i = threadIdx.x; i < kGT * p.out; i += kGThreads) {
       const int ev = i / p.out, j = i % p.out;
@@ -192,11 +212,12 @@ struct Gen {
     __shared__ Smem sm;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int lr = lane & 15, lg = lane >> 4;
-    const int m = blockIdx.y;
-    const int64_t row0 = (int64_t)blockIdx.x * kGT;
+    int m, tile;
+    gen_block(gridDim.x, gridDim.y, m, tile);
+    const int64_t row0 = (int64_t)tile * kGT;
     const float slope = p.slope;
     forward(p, sm, m, row0);
-    float* part = p.part + ((int64_t)m * gridDim.x + blockIdx.x) * p.P;
+    float* part = p.part + ((int64_t)m * gridDim.x + tile) * p.P;
 
     // dL/d(last pre-activation) = dL/dtheta * sigmoid(o); zero on rows past k
     for (int i = tid; i < kGT * kGMaxIO; i += kGThreads) {

@@ -111,8 +111,34 @@ ENSEMBLE_CONFIGS = {
 }
 
 
+@dataclass(frozen=True)
+class TrainWorkload:
+    """One GAN training step of the loop-closure test at the paper's shape
+    (Sec. V-A, Tab. gen_settings): the generator predicts k = 1,024 parameter
+    samples, each yields E = 100 events, the discriminator sees the two
+    observables of those and of an equal reference batch, bootstrapped each
+    step from a pool of twice its size (Sec. IV-B, Sec. VI-B)."""
+    name: str
+    k: int = 1024
+    events_per_theta: int = 100
+    g_widths: Tuple[int, ...] = (6, 128, 128, 128, 128, 6)
+    d_widths: Tuple[int, ...] = (2, 128, 128, 128, 128, 1)
+    seed: int = 0
+
+    @property
+    def n_events(self) -> int:
+        return self.k * self.events_per_theta
+
+    @property
+    def theta_star(self) -> Tuple[float, ...]:
+        return (2.0, 5.0, 1.5, 3.0, 3.0, 2.0)
+
+
+TRAIN_CONFIGS = {"train": TrainWorkload("train")}
+
+
 def get(name: str):
-    for table in (CONFIGS, BOOTSTRAP_CONFIGS, ENSEMBLE_CONFIGS):
+    for table in (CONFIGS, BOOTSTRAP_CONFIGS, ENSEMBLE_CONFIGS, TRAIN_CONFIGS):
         if name in table:
             return table[name]
     raise KeyError(name)
