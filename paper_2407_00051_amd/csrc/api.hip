@@ -447,7 +447,7 @@ sagips_status sagips_gen_forward(sagips_ctx* c, const sagips_gen* G, const float
   if (s != SAGIPS_OK) return s;
   if (!theta) return fail(c, SAGIPS_E_INVAL, "theta is NULL");
   DeviceGuard g(c->device);
-  hipError_t e = launch_gen_forward(*G, noise, k, theta, c->stream, timer_of(c));
+  hipError_t e = launch_gen_forward(*G, noise, k, theta, c->n_cu, c->stream, timer_of(c));
   return e == hipSuccess ? SAGIPS_OK : hip_fail(c, e, "gen_forward launch");
 }
 
@@ -460,9 +460,9 @@ sagips_status sagips_gen_backward(sagips_ctx* c, const sagips_gen* G, const floa
   for (int l = 0; l < G->n_layers; ++l)
     if (!dW[l] || !db[l]) return fail(c, SAGIPS_E_INVAL, "dW[%d] or db[%d] is NULL", l, l);
   DeviceGuard g(c->device);
-  s = ensure_ws(c, gen_backward_workspace(*G, k));
+  s = ensure_ws(c, gen_backward_workspace(*G, k, c->n_cu));
   if (s != SAGIPS_OK) return s;
-  hipError_t e = launch_gen_backward(*G, noise, k, dL_dtheta, dW, db, c->ws, c->stream, timer_of(c));
+  hipError_t e = launch_gen_backward(*G, noise, k, dL_dtheta, dW, db, c->ws, c->n_cu, c->stream, timer_of(c));
   return e == hipSuccess ? SAGIPS_OK : hip_fail(c, e, "gen_backward launch");
 }
 
@@ -478,7 +478,7 @@ sagips_status sagips_ensemble_response(sagips_ctx* c, const sagips_gen* G, const
   DeviceGuard g(c->device);
   s = ensure_ws(c, ensemble_workspace(*G, k));
   if (s != SAGIPS_OK) return s;
-  hipError_t e = launch_ensemble(*G, noise, k, p_true, p_hat, sigma, r_hat, c->ws, c->stream, timer_of(c));
+  hipError_t e = launch_ensemble(*G, noise, k, p_true, p_hat, sigma, r_hat, c->ws, c->n_cu, c->stream, timer_of(c));
   return e == hipSuccess ? SAGIPS_OK : hip_fail(c, e, "ensemble launch");
 }
 

@@ -6,11 +6,12 @@
 // The paper's generator (51,206 parameters) is 6 -> 128 x 4 -> 6, i.e.
 // H = 128, NH = 3.  Member m's parameters sit at W[l] + m * |W[l]|.
 //
-// Work decomposition: one workgroup of 8 waves per (64-row tile of the noise
-// batch, member).  The tile's activations A_1 .. A_{NH+1} live in LDS as
-// [64][H+4] fp32; the H x H products run on the fp32 matrix cores
+// Work decomposition: one workgroup of 8 waves per (tile of T rows of the
+// noise batch, member), T = 64, or 16 when 64-row tiles would leave most CUs
+// idle (a single generator on 1,024 rows).  The tile's activations
+// A_1 .. A_{NH+1} live in LDS as [T][H+4] fp32; the H x H products run on the fp32 matrix cores
 // (v_mfma_f32_16x16x4_f32) as out^T = W * in^T, each wave owning 16 output
-// features of all 64 rows.  The first layer (K = IN) and the last (N = OUT)
+// features of all T rows.  The first layer (K = IN) and the last (N = OUT)
 // are VALU work.
 //
 // The backward kernel recomputes the tile's forward pass into LDS (cheaper
@@ -28,7 +29,6 @@ namespace {
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
-constexpr int kGT = 64;          // rows per tile
 constexpr int kGThreads = 512;   // 8 waves
 constexpr int kGMaxIO = 8;       // largest IN / OUT
 
@@ -74,12 +74,13 @@ struct GenParams {
   int64_t poff_w[kMaxGenLayers], poff_b[kMaxGenLayers];
 };
 
-template <int H, int NH>
+template <int H, int NH, int kGT>
 struct Gen {
   static constexpr int LD = H + 4;
   static constexpr int WAVES = kGThreads / 64;
   static constexpr int KB = H / 16;
   static constexpr int CB = kGT / 16;
+  static_assert(kGT == 16 || kGT == 64, "row tile");
   static constexpr int PPO = kGThreads / H;     // threads per feature in the VALU loops
   static_assert(H == 16 * WAVES, "one wave per 16 features");
 
@@ -173,7 +174,7 @@ struct Gen {
       }
       __syncthreads();
     }
-    {   // last layer: thread (row ev, part) sums features 4 part + 32 c (c < H / 32) for every output
+    if ((tid >> 3) < kGT) {   // last layer: thread (row ev, part) sums features 4 part + 32 c (c < H / 32)
       const int ev = tid >> 3, part = tid & 7;
       const float* Wl = p.W[NH + 1] + m * p.wsz[NH + 1];
       const float* hrow = &sm.act[NH][ev][0];
@@ -317,18 +318,19 @@ struct Gen {
   }
 };
 
-template <int H, int NH>
+template <int H, int NH, int T>
 __global__ __launch_bounds__(kGThreads, 1) void k_gen_forward(GenParams p) {
-  Gen<H, NH>::run_forward(p);
+  Gen<H, NH, T>::run_forward(p);
 }
 
-template <int H, int NH>
+template <int H, int NH, int T>
 __global__ __launch_bounds__(kGThreads, 1) void k_gen_backward(GenParams p) {
-  Gen<H, NH>::run_backward(p);
+  Gen<H, NH, T>::run_backward(p);
 }
 
-// Sum of the per-tile partials of member blockIdx.y, in tile order, scattered
-// to the caller's gradient arrays.
+// Sum of the per-tile partials of member blockIdx.y in a fixed order (tile
+// slices t = s mod 4 summed side by side, then the four slices in order),
+// scattered to the caller's gradient arrays.
 struct GenReduceArgs {
   const float* part;
   int64_t P;
@@ -339,16 +341,27 @@ struct GenReduceArgs {
   float* db[kMaxGenLayers];
 };
 
+constexpr int kRedSlices = 4;   // tile slices summed side by side, then combined in order
+
 __global__ __launch_bounds__(256) void k_gen_reduce(GenReduceArgs r) {
+  __shared__ float red[kRedSlices][256 / kRedSlices];
   const int m = blockIdx.y;
-  const int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (e >= r.P) return;
-  const float* src = r.part + (int64_t)m * r.tiles * r.P + e;
+  const int le = threadIdx.x % (256 / kRedSlices), sl = threadIdx.x / (256 / kRedSlices);
+  const int64_t e = (int64_t)blockIdx.x * (256 / kRedSlices) + le;
   float s = 0.f;
-  for (int t = 0; t < r.tiles; ++t) s += src[(int64_t)t * r.P];
+  if (e < r.P) {
+    const float* src = r.part + (int64_t)m * r.tiles * r.P + e;
+    for (int t = sl; t < r.tiles; t += kRedSlices) s += src[(int64_t)t * r.P];
+  }
+  red[sl][le] = s;
+  __syncthreads();
+  if (sl != 0 || e >= r.P) return;
+  float v = 0.f;
+#pragma unroll
+  for (int q = 0; q < kRedSlices; ++q) v += red[q][le];
   for (int l = 0; l < r.n_layers; ++l) {
-    if (e >= r.poff_w[l] && e < r.poff_w[l] + r.wsz[l]) { r.dW[l][m * r.wsz[l] + (e - r.poff_w[l])] = s; return; }
-    if (e >= r.poff_b[l] && e < r.poff_b[l] + r.bsz[l]) { r.db[l][m * r.bsz[l] + (e - r.poff_b[l])] = s; return; }
+    if (e >= r.poff_w[l] && e < r.poff_w[l] + r.wsz[l]) { r.dW[l][m * r.wsz[l] + (e - r.poff_w[l])] = v; return; }
+    if (e >= r.poff_b[l] && e < r.poff_b[l] + r.bsz[l]) { r.db[l][m * r.bsz[l] + (e - r.poff_b[l])] = v; return; }
   }
 }
 
@@ -407,15 +420,17 @@ __global__ __launch_bounds__(256) void k_ens_final(const float* __restrict__ row
 
 struct GenVariant {
   int H, NH;
-  void (*fwd)(GenParams);
-  void (*bwd)(GenParams);
+  void (*fwd[2])(GenParams);   // 64-row, 16-row tiles
+  void (*bwd[2])(GenParams);
 };
 
-const GenVariant kGenVariants[] = {
-    {128, 1, k_gen_forward<128, 1>, k_gen_backward<128, 1>},
-    {128, 2, k_gen_forward<128, 2>, k_gen_backward<128, 2>},
-    {128, 3, k_gen_forward<128, 3>, k_gen_backward<128, 3>},
-};
+#define SAGIPS_GEN_VARIANT(H_, NH_)                                               \
+  {                                                                              \
+    H_, NH_, {k_gen_forward<H_, NH_, 64>, k_gen_forward<H_, NH_, 16>},           \
+        {k_gen_backward<H_, NH_, 64>, k_gen_backward<H_, NH_, 16> }              \
+  }
+
+const GenVariant kGenVariants[] = {SAGIPS_GEN_VARIANT(128, 1), SAGIPS_GEN_VARIANT(128, 2), SAGIPS_GEN_VARIANT(128, 3)};
 
 const GenVariant* find_gen(const sagips_gen& G) {
   const int H = G.width[1], NH = G.n_layers - 2;
@@ -447,7 +462,11 @@ GenParams gen_params(const sagips_gen& G, const float* noise, int64_t k) {
   return p;
 }
 
-inline int gen_tiles(int64_t k) { return (int)((k + kGT - 1) / kGT); }
+// Row tile: 64, unless 64-row tiles of all members would not cover the CUs.
+inline int gen_rows(const sagips_gen& G, int64_t k, int n_cu) {
+  return ((k + 63) / 64) * G.n_members >= n_cu ? 64 : 16;
+}
+inline int gen_tiles(int64_t k, int T) { return (int)((k + T - 1) / T); }
 
 }  // namespace
 
@@ -463,9 +482,9 @@ bool gen_supported(const sagips_gen& G, const char** why) {
   return true;
 }
 
-size_t gen_backward_workspace(const sagips_gen& G, int64_t k) {
+size_t gen_backward_workspace(const sagips_gen& G, int64_t k, int n_cu) {
   const GenParams p = gen_params(G, nullptr, k);
-  return sizeof(float) * (size_t)p.P * gen_tiles(k) * G.n_members;
+  return sizeof(float) * (size_t)p.P * gen_tiles(k, gen_rows(G, k, n_cu)) * G.n_members;
 }
 
 size_t ensemble_workspace(const sagips_gen& G, int64_t k) {
@@ -473,26 +492,28 @@ size_t ensemble_workspace(const sagips_gen& G, int64_t k) {
   return th + sizeof(float) * 2 * (size_t)k * G.width[G.n_layers];
 }
 
-hipError_t launch_gen_forward(const sagips_gen& G, const float* noise, int64_t k, float* theta, hipStream_t st,
-                              Timer* tm) {
+hipError_t launch_gen_forward(const sagips_gen& G, const float* noise, int64_t k, float* theta, int n_cu,
+                              hipStream_t st, Timer* tm) {
   GenParams p = gen_params(G, noise, k);
   p.theta = theta;
   const GenVariant* v = find_gen(G);
+  const int T = gen_rows(G, k, n_cu);
   if (tm) tm->begin("gen_forward");
-  hipLaunchKernelGGL(v->fwd, dim3(gen_tiles(k), G.n_members), dim3(kGThreads), 0, st, p);
+  hipLaunchKernelGGL(v->fwd[T == 64 ? 0 : 1], dim3(gen_tiles(k, T), G.n_members), dim3(kGThreads), 0, st, p);
   if (tm) tm->end();
   return hipGetLastError();
 }
 
 hipError_t launch_gen_backward(const sagips_gen& G, const float* noise, int64_t k, const float* dtheta,
-                               float* const* dW, float* const* db, void* ws, hipStream_t st, Timer* tm) {
+                               float* const* dW, float* const* db, void* ws, int n_cu, hipStream_t st, Timer* tm) {
   GenParams p = gen_params(G, noise, k);
   p.dtheta = dtheta;
   p.part = static_cast<float*>(ws);
   const GenVariant* v = find_gen(G);
-  const int tiles = gen_tiles(k);
+  const int T = gen_rows(G, k, n_cu);
+  const int tiles = gen_tiles(k, T);
   if (tm) tm->begin("gen_backward");
-  hipLaunchKernelGGL(v->bwd, dim3(tiles, G.n_members), dim3(kGThreads), 0, st, p);
+  hipLaunchKernelGGL(v->bwd[T == 64 ? 0 : 1], dim3(tiles, G.n_members), dim3(kGThreads), 0, st, p);
   if (tm) tm->end();
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
@@ -511,18 +532,19 @@ hipError_t launch_gen_backward(const sagips_gen& G, const float* noise, int64_t 
     r.db[l] = db[l];
   }
   if (tm) tm->begin("gen_reduce");
-  hipLaunchKernelGGL(k_gen_reduce, dim3((unsigned)((p.P + 255) / 256), G.n_members), dim3(256), 0, st, r);
+  hipLaunchKernelGGL(k_gen_reduce, dim3((unsigned)((p.P + 256 / kRedSlices - 1) / (256 / kRedSlices)), G.n_members),
+                     dim3(256), 0, st, r);
   if (tm) tm->end();
   return hipGetLastError();
 }
 
 hipError_t launch_ensemble(const sagips_gen& G, const float* noise, int64_t k, const float* p_true, float* p_hat,
-                           float* sigma, float* r_hat, void* ws, hipStream_t st, Timer* tm) {
+                           float* sigma, float* r_hat, void* ws, int n_cu, hipStream_t st, Timer* tm) {
   const int out = G.width[G.n_layers];
   float* theta = static_cast<float*>(ws);
   const size_t th = (sizeof(float) * (size_t)G.n_members * k * out + 255) & ~(size_t)255;
   float* rowstat = reinterpret_cast<float*>(static_cast<char*>(ws) + th);
-  hipError_t e = launch_gen_forward(G, noise, k, theta, st, tm);
+  hipError_t e = launch_gen_forward(G, noise, k, theta, n_cu, st, tm);
   if (e != hipSuccess) return e;
   if (tm) tm->begin("ensemble_rows");
   hipLaunchKernelGGL(k_ens_rows, dim3((unsigned)((k * out + 255) / 256)), dim3(256), 0, st, theta, G.n_members, k,

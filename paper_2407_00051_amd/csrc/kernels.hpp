@@ -72,14 +72,14 @@ hipError_t launch_disc_f32(const DiscArgs& a, void* ws, int n_cu, hipStream_t st
 // generator.hip --------------------------------------------------------------
 constexpr int kMaxGenLayers = 5;
 bool gen_supported(const sagips_gen& G, const char** why);
-size_t gen_backward_workspace(const sagips_gen& G, int64_t k);
+size_t gen_backward_workspace(const sagips_gen& G, int64_t k, int n_cu);
 size_t ensemble_workspace(const sagips_gen& G, int64_t k);
-hipError_t launch_gen_forward(const sagips_gen& G, const float* noise, int64_t k, float* theta, hipStream_t st,
-                              Timer* tm);
+hipError_t launch_gen_forward(const sagips_gen& G, const float* noise, int64_t k, float* theta, int n_cu,
+                              hipStream_t st, Timer* tm);
 hipError_t launch_gen_backward(const sagips_gen& G, const float* noise, int64_t k, const float* dtheta,
-                               float* const* dW, float* const* db, void* ws, hipStream_t st, Timer* tm);
+                               float* const* dW, float* const* db, void* ws, int n_cu, hipStream_t st, Timer* tm);
 hipError_t launch_ensemble(const sagips_gen& G, const float* noise, int64_t k, const float* p_true, float* p_hat,
-                           float* sigma, float* r_hat, void* ws, hipStream_t st, Timer* tm);
+                           float* sigma, float* r_hat, void* ws, int n_cu, hipStream_t st, Timer* tm);
 
 // optim.hip ------------------------------------------------------------------
 hipError_t launch_adam(const sagips_param_set& ps, int step, double lr, double beta1, double beta2, double eps,
