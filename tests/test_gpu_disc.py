@@ -201,3 +201,21 @@ def test_paper_shape_three_calls_match_fused(gpu_ctx):
     ref = _oracle(inp, w, real_np)
     assert_normwise(to_np(g3), ref["dL_dtheta"], TOL, "dLg_dtheta (3 calls)")
     assert_normwise(to_np(of["dLg_dtheta"]), ref["dL_dtheta"], TOL, "dLg_dtheta (fused)")
+
+
+def test_row_sharding_matches_full_run(gpu_ctx):
+    """Two shards of the parameter rows, each with its own counter base, sample the
+    same events as the full run; their dL_G/dtheta rows equal the full run's up to
+    the 1/N of the mean (tiles straddle rows differently in each run)."""
+    w = scaled(get("paper"), 10, 100)
+    inp, th, ts, W, b, n_real = _setup(w)
+    real = gpu_ctx.sample_events(ts, n_real, w.real_seed)
+    kw = dict(features=sg.FEAT_PROXY2, want_grads=False, want_logits=False)
+    full = gpu_ctx.disc_fwd_bwd(W, b, real, fake_source=dict(theta=th, events_per_theta=100, seed=w.fake_seed), **kw)
+    halves = []
+    for r0, r1 in ((0, 5), (5, 10)):
+        o = gpu_ctx.disc_fwd_bwd(W, b, real, fake_source=dict(theta=th[r0:r1].clone(), events_per_theta=100,
+                                                             seed=w.fake_seed, counter_base=r0 * 100), **kw)
+        halves.append(o["dLg_dtheta"] * 0.5)          # N_shard / N_full
+        torch.testing.assert_close(o["dLg_dx"] * 0.5, full["dLg_dx"][r0 * 100:r1 * 100], rtol=1e-6, atol=0)
+    torch.testing.assert_close(torch.cat(halves), full["dLg_dtheta"], rtol=2e-6, atol=1e-9)
