@@ -273,8 +273,11 @@ class Context:
         g, M = self._gen(W, b, slope)
         _check_tensor(noise, "noise", torch.float32, (noise.shape[0], g.width[0]), self.device)
         k = noise.shape[0]
-        _check_tensor(dL_dtheta, "dL_dtheta", torch.float32, (M, k, g.width[g.n_layers]) if dL_dtheta.dim() == 3
-                      else (k, g.width[g.n_layers]), self.device)
+        n_out = g.width[g.n_layers]
+        if M > 1 or dL_dtheta.dim() == 3:
+            _check_tensor(dL_dtheta, "dL_dtheta", torch.float32, (M, k, n_out), self.device)
+        else:
+            _check_tensor(dL_dtheta, "dL_dtheta", torch.float32, (k, n_out), self.device)
         dW = dW if dW is not None else [torch.empty_like(w) for w in W]
         db = db if db is not None else [torch.empty_like(v) for v in b]
         for l in range(g.n_layers):

@@ -127,6 +127,10 @@ def test_generator_rejects_bad_arguments(gpu_ctx):
     n = torch.zeros((10, 6), device="cuda:0")
     with pytest.raises(sg.SagipsError):
         gpu_ctx.gen_forward(_dev(W), _dev(b), n)
+    # several members need a [M][k][out] signal
+    W2, b2 = gen.generator_stack(WIDTHS, 2, seed=1)
+    with pytest.raises(ValueError):
+        gpu_ctx.gen_backward(_dev(W2), _dev(b2), n, torch.zeros((10, 6), device="cuda:0"))
     # p_true without r_hat is refused before any launch
     W, b = _dev(gen.generator_stack(WIDTHS, 1, seed=1)[0]), _dev(gen.generator_stack(WIDTHS, 1, seed=1)[1])
     g, _ = gpu_ctx._gen(W, b, 0.2)
