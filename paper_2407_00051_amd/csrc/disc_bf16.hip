@@ -31,6 +31,7 @@
 #include <string.h>
 
 #include <algorithm>
+#include <type_traits>
 
 namespace sagips {
 namespace {
@@ -915,11 +916,10 @@ constexpr int kWT = 256;     // weight-gradient tile edge
 
 // Waves of a weight-gradient workgroup: WM along the output rows o, WN along
 // the input columns i, each owning a (256 / WM) x (256 / WN) block, with
-// fragments loaded PD K steps ahead (measured best per width; four waves, one
-// per SIMD).
+// fragments loaded PD K steps ahead (measured best; four waves, one per SIMD).
+// H = 512 uses k_wgrad_shared below.
 template <int H> struct WgradCfg;
 template <> struct WgradCfg<256> { static constexpr int WM = 2, WN = 2, PD = 3; };
-template <> struct WgradCfg<512> { static constexpr int WM = 4, WN = 1, PD = 2; };
 constexpr int kWThreads = 256;
 
 template <int H>
@@ -1017,6 +1017,171 @@ __global__ __launch_bounds__(kWThreads, 1) void k_wgrad(const u16* __restrict__ 
 #pragma unroll
     for (int m = 0; m < FM; ++m) {
       const float v = dbs[m] + __shfl_xor(dbs[m], 32, 64);   // both row halves of the column
+      if (lh == 0) Pdb[(size_t)slice * H + 32 * (ob + m) + lr] = v;
+    }
+  }
+}
+
+// The same partials for H = 512 with the input-side fragments shared through
+// LDS.  A workgroup's four waves all need the eight A fragments (256 columns)
+// of every K step; instead of each wave streaming all eight, wave w fetches
+// fragments 2w and 2w + 1 into registers kWLG steps ahead, writes them into
+// one of three LDS slots two steps ahead, and every wave reads the eight from
+// there one step ahead, so the reads of step k + 1 overlap the products of
+// step k.  This cuts the traffic into the CU to one copy of each operand and
+// lets the register prefetch run far enough ahead to cover HBM latency.  One
+// barrier per K step publishes a slot; the loads in flight are not waited for
+// at the barrier.  Fragment order, scaling, rounding and the order of the
+// products are those of k_wgrad, so the partials are bit-identical to it.
+constexpr int kWLG = 5;      // register prefetch distance (K steps) of k_wgrad_shared
+constexpr int kWNS = 6;      // register ring slots: kWLG + 1, even so that step parity is a constant
+
+// Steps Q = 0 .. N-1 of one pass of the register ring, as a compile-time
+// sequence: run() with every step prefetching, tail() with the bounds checked.
+template <int N>
+struct WRing {
+  template <class F>
+  __device__ __forceinline__ static void run(F& f, int k0) {
+    WRing<N - 1>::run(f, k0);
+    f(std::integral_constant<int, N - 1>{}, k0 + N - 1, true, true, true);
+  }
+  template <class F>
+  __device__ __forceinline__ static void tail(F& f, int k0, int nk) {
+    WRing<N - 1>::tail(f, k0, nk);
+    const int k = k0 + N - 1;
+    if (k < nk) f(std::integral_constant<int, N - 1>{}, k, k + 1 < nk, k + 2 < nk, k + kWLG < nk);
+  }
+};
+template <>
+struct WRing<0> {
+  template <class F>
+  __device__ __forceinline__ static void run(F&, int) {}
+  template <class F>
+  __device__ __forceinline__ static void tail(F&, int, int) {}
+};
+
+__device__ __forceinline__ void lds_barrier() {
+  // LDS writes complete, then the workgroup barrier; global loads stay in flight
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
+__global__ __launch_bounds__(kWThreads, 1) void k_wgrad_shared(const u16* __restrict__ dsc, const u16* __restrict__ A,
+                                                               const float* __restrict__ eD, int kb_per_slice,
+                                                               int kb_total, float* __restrict__ P,
+                                                               float* __restrict__ Pdb, int xcd_map) {
+  constexpr int H = 512;
+  constexpr int TI = H / kWT;     // 2
+  constexpr int CB = H / 32;      // 16
+  constexpr int FM = 2, FN = 8;   // a wave owns 64 output rows x all 256 columns of the tile
+  constexpr int NS = kWNS;
+  static_assert(NS == kWLG + 1 && NS % 6 == 0, "ring slots: step parity and step mod 3 must be constants");
+  constexpr size_t KSTRIDE = (size_t)CB * 512;
+  __shared__ __attribute__((aligned(16))) u16 sb[3][FN][512];
+  int tile, slice;
+  if (xcd_map) {
+    const int x = blockIdx.x % 8, r = blockIdx.x / 8;
+    tile = r % (TI * TI);
+    slice = (r / (TI * TI)) * 8 + x;
+  } else {
+    tile = blockIdx.x % (TI * TI);
+    slice = blockIdx.x / (TI * TI);
+  }
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lr = lane & 31, lh = lane >> 5;
+  const int ob = (tile / TI) * (kWT / 32) + FM * wave;
+  const int ib = (tile % TI) * (kWT / 32);
+  const int kb0 = slice * kb_per_slice;
+  const int nk = max(0, min(kb_total, kb0 + kb_per_slice) - kb0);
+  const u16* pa = dsc + (((size_t)kb0 * CB + ob) * 64 + lane) * 8;
+  const u16* pb = A + (((size_t)kb0 * CB + ib + 2 * wave) * 64 + lane) * 8;   // this wave's two A fragments
+  const float* pe = eD + (size_t)kb0 * 16 + 8 * lh;
+  f32x16 acc[FM][FN];
+#pragma unroll
+  for (int m = 0; m < FM; ++m)
+#pragma unroll
+    for (int n = 0; n < FN; ++n)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[m][n][r] = 0.f;
+  float dbs[FM] = {0.f, 0.f};
+  bf16x8 ra[NS][2], rd[NS][FM];
+  f32x4 re[NS][2];
+  bf16x8 fb[2][FN];               // the A fragments of the current and the next step
+  auto load = [&](int slot, int k) __attribute__((always_inline)) {
+#pragma unroll
+    for (int j = 0; j < 2; ++j) ra[slot][j] = *reinterpret_cast<const bf16x8*>(pb + k * KSTRIDE + j * 512);
+#pragma unroll
+    for (int m = 0; m < FM; ++m) rd[slot][m] = *reinterpret_cast<const bf16x8*>(pa + k * KSTRIDE + m * 512);
+    re[slot][0] = *reinterpret_cast<const f32x4*>(pe + (size_t)k * 16);
+    re[slot][1] = *reinterpret_cast<const f32x4*>(pe + (size_t)k * 16 + 4);
+  };
+  auto put = [&](int slot, int buf) __attribute__((always_inline)) {
+#pragma unroll
+    for (int j = 0; j < 2; ++j) *reinterpret_cast<bf16x8*>(&sb[buf][2 * wave + j][lane * 8]) = ra[slot][j];
+  };
+  auto get = [&](int buf, int into) __attribute__((always_inline)) {
+#pragma unroll
+    for (int n = 0; n < FN; ++n) fb[into][n] = *reinterpret_cast<const bf16x8*>(&sb[buf][n][lane * 8]);
+  };
+  // Step k (q = k mod NS, so k mod 2 = q mod 2 and k mod 3 = q mod 3): read
+  // the fragments of step k + 1 (published at the end of step k - 1), publish
+  // this wave's two of step k + 2, prefetch step k + kWLG, then the products
+  // of step k from the fragments read one step earlier.
+  auto step = [&](auto qc, int k, bool get_next, bool put_ahead, bool load_ahead) __attribute__((always_inline)) {
+    constexpr int q = decltype(qc)::value;
+    if (get_next) get((q + 1) % 3, (q + 1) & 1);
+    if (put_ahead) put((q + 2) % NS, (q + 2) % 3);
+    if (load_ahead) load((q + kWLG) % NS, k + kWLG);
+    // keep each step's work inside the step: the scheduler would otherwise
+    // hoist later steps' scaling above their loads' waits
+    __builtin_amdgcn_sched_barrier(0);
+    bf16x8 sa[FM];
+#pragma unroll
+    for (int m = 0; m < FM; ++m) {
+      float v[8];
+#pragma unroll
+      for (int t = 0; t < 8; ++t) v[t] = (float)rd[q][m][t] * re[q][t >> 2][t & 3];
+      dbs[m] += ((v[0] + v[1]) + (v[2] + v[3])) + ((v[4] + v[5]) + (v[6] + v[7]));
+      sa[m] = __builtin_bit_cast(bf16x8, make_uint4(pack_bf16(v[0], v[1]), pack_bf16(v[2], v[3]),
+                                                    pack_bf16(v[4], v[5]), pack_bf16(v[6], v[7])));
+    }
+#pragma unroll
+    for (int n = 0; n < FN; ++n)
+#pragma unroll
+      for (int m = 0; m < FM; ++m)
+        acc[m][n] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(sa[m], fb[q & 1][n], acc[m][n], 0, 0, 0);
+    __builtin_amdgcn_sched_barrier(0);
+    lds_barrier();
+  };
+  if (nk > 0) {
+    // prologue without branches (a step past the slice reloads its last step,
+    // never used), so that the waits on the loads stay exact in the loop below
+#pragma unroll
+    for (int q = 0; q < kWLG; ++q) load(q, min(q, nk - 1));
+    put(0, 0);
+    put(1, 1);
+    lds_barrier();
+    get(0, 0);
+  }
+  // steady state: NS steps per pass, every step reading, publishing and
+  // prefetching (no branches, so the waits on the loads stay exact)
+  int k0 = 0;
+  for (; k0 + NS - 1 + kWLG < nk; k0 += NS) WRing<NS>::run(step, k0);
+  // tail: the last steps, with the bounds checked
+  for (; k0 < nk; k0 += NS) WRing<NS>::tail(step, k0, nk);
+  float* out = P + (size_t)slice * H * H;
+#pragma unroll
+  for (int m = 0; m < FM; ++m)
+#pragma unroll
+    for (int n = 0; n < FN; ++n)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int o = (ob + m) * 32 + 8 * (r / 4) + 4 * lh + (r % 4), i = (ib + n) * 32 + lr;
+        out[(size_t)o * H + i] = acc[m][n][r];
+      }
+  if (tile % TI == 0) {
+#pragma unroll
+    for (int m = 0; m < FM; ++m) {
+      const float v = dbs[m] + __shfl_xor(dbs[m], 32, 64);
       if (lh == 0) Pdb[(size_t)slice * H + 32 * (ob + m) + lr] = v;
     }
   }
@@ -1269,7 +1434,7 @@ hipError_t launch_disc_bf16(const DiscArgs& a, void* ws, int n_cu, hipStream_t s
             hipLaunchKernelGGL(k_wgrad<256>, dim3(tiles * p.slices), dim3(kWThreads), 0, st, ca.dlt + l * bst,
                                ca.act + l * bst, ca.eD, kb_per_slice, kb_total, F32(p.off_pw), F32(p.off_pwdb), xcd_map);
           else
-            hipLaunchKernelGGL(k_wgrad<512>, dim3(tiles * p.slices), dim3(kWThreads), 0, st, ca.dlt + l * bst,
+            hipLaunchKernelGGL(k_wgrad_shared, dim3(tiles * p.slices), dim3(kWThreads), 0, st, ca.dlt + l * bst,
                                ca.act + l * bst, ca.eD, kb_per_slice, kb_total, F32(p.off_pw), F32(p.off_pwdb), xcd_map);
           if (tm) tm->end();
           accumulate(F32(p.off_pw), p.slices, (int64_t)H * H, (int64_t)H * H, out.dW[1 + l], first, st);
