@@ -39,6 +39,7 @@ KERNEL_SOURCES = {
     "param_grad": ["paper_2407_00051_amd/csrc/sampler.hip", "paper_2407_00051_amd/csrc/device_math.hpp"],
     "bootstrap": ["paper_2407_00051_amd/csrc/sampler.hip", "paper_2407_00051_amd/csrc/device_math.hpp"],
     "gen_forward": ["paper_2407_00051_amd/csrc/generator.hip", "paper_2407_00051_amd/csrc/device_math.hpp"],
+    "sample_events": ["paper_2407_00051_amd/csrc/sampler.hip", "paper_2407_00051_amd/csrc/device_math.hpp"],
 }
 
 
@@ -367,6 +368,75 @@ def bench_train(args, w, ctx, torch, sg):
     print(json.dumps(line), flush=True)
 
 
+def bench_sample(args, w, ctx, torch):
+    """Steps of the stand-alone sampler on the stress configuration: theta -> Philox ->
+    Kumaraswamy events written to HBM ([N][d] fp32), the path that feeds a buffered
+    discriminator."""
+    import numpy as np
+    import oracle
+    from workloads import gen
+    dev = "cuda:0"
+    inp = gen.make_inputs(w)
+    theta = torch.tensor(inp["theta"], device=dev)
+    N = w.n_events
+    x = torch.empty((N, w.d), dtype=torch.float32, device=dev)
+
+    def step():
+        ctx.sample_events(theta, w.events_per_theta, w.fake_seed, out=x)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    ctx.kernel_times()
+    ctx.set_timing(True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    ctx.set_timing(False)
+    kt = ctx.kernel_times()
+    ms_per_step = (t1 - t0) * 1e3 / args.steps
+    launches, total_ms = kt["sample_events"]
+    avg_ms = total_ms / launches
+    bytes_per_launch = N * w.d * 4 + w.n_theta * 2 * w.d * 4     # events written, theta read
+    achieved = bytes_per_launch / (avg_ms * 1e-3)
+    roof = {"bound": "hbm", "achieved": achieved / 1e9, "peak": PEAK["hbm"] / 1e9, "unit": "GB/s",
+            "frac": achieved / PEAK["hbm"], "traffic": read_traffic("sample_events", "stress_sample"),
+            "kernel": "sample_events", "kernel_avg_ms": avg_ms,
+            "kernels": {k: {"launches": c, "avg_ms": t / max(c, 1)} for k, (c, t) in kt.items()}}
+    line = {
+        "metric": "events/sec of the stand-alone sampler (theta -> Philox -> Kumaraswamy events in HBM); "
+                  "% of HBM peak",
+        "value": N / (ms_per_step * 1e-3), "unit": "events/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": ms_per_step, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "f32", "data": "synthetic (seeded theta, Philox-sampled events)",
+        "config": {"workload": "stress_sample", "n_theta": w.n_theta, "events_per_theta": w.events_per_theta,
+                   "events": N, "d": w.d, "parallelism": "single GPU"},
+        "roofline": roof,
+    }
+    if not args.no_cpu_baseline:
+        try:
+            from threadpoolctl import threadpool_info
+            threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+        except Exception:
+            threads = os.cpu_count()
+        n = 1 << 20
+        reps, t0 = 0, time.perf_counter()
+        while True:
+            oracle.sample(np.asarray(inp["theta"][:1], dtype=np.float64), n, w.fake_seed, counter_base=reps * n)
+            reps += 1
+            dt = time.perf_counter() - t0
+            if dt >= 10.0:
+                break
+        line["cpu_baseline"] = {"value": reps * n / dt, "unit": "events/s", "cores": int(threads), "kind": "oracle",
+                                "sample": f"1 of {w.n_theta} parameter rows x {n} events per repetition, float64 "
+                                          f"numpy, {reps} repetition(s) in {dt:.1f} s"}
+    ctx.close()
+    print(json.dumps(line), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -389,7 +459,7 @@ def main():
     import paper_2407_00051_amd as sg
     from workloads import gen, get
 
-    w = get(args.workload)
+    w = get("stress" if args.workload == "stress_sample" else args.workload)
     torch.cuda.set_device(0)
     ctx = sg.Context(0)
     dev = "cuda:0"
@@ -401,6 +471,8 @@ def main():
         b.copy_(a)
         torch.cuda.synchronize()
         del a, b
+    if args.workload == "stress_sample":
+        return bench_sample(args, w, ctx, torch)
     if hasattr(w, "n_data"):
         return bench_bootstrap(args, w, ctx, torch)
     if hasattr(w, "n_members"):
