@@ -14,7 +14,9 @@ pytestmark = pytest.mark.gpu
 torch = pytest.importorskip("torch")
 import paper_2407_00051_amd as sg  # noqa: E402
 
-TOL = 2e-2        # bf16 operands: normwise per tensor
+TOL = 2e-2        # bf16 operands: normwise per tensor (against the float64 network)
+TOL_EMU = 2e-3    # against the oracle that rounds at the same bf16 points: only the fp32
+                  # accumulation order and the rounding of fp32 (not float64) values differ
 
 
 class _T:
@@ -108,7 +110,7 @@ def test_bf16_reduced(gpu_ctx, name, n_theta, E, n_real):
     ref = oracle.run_step(inp["theta"], E, w.fake_seed, inp["W"], inp["b"], real_np, features=w.features)
     # The parity bar: the oracle evaluated at the same bf16 operand rounding points.
     emu = oracle.run_step(inp["theta"], E, w.fake_seed, inp["W"], inp["b"], real_np, features=w.features, bf16=True)
-    bad_emu = _check(o, emu, TOL, "vs bf16-point oracle", len(W), cond_ref=ref)
+    bad_emu = _check(o, emu, TOL_EMU, "vs bf16-point oracle", len(W), cond_ref=ref)
     # Against the float64 network: the losses and dL/dtheta at the same bar; the rest is
     # reported (rounding the operands changes the network, and per-event quantities such as
     # dL_G/dx and the first-layer gradient are ill-conditioned under that change).
