@@ -74,7 +74,9 @@ struct GenParams {
   int64_t poff_w[kMaxGenLayers], poff_b[kMaxGenLayers];
 };
 
-template <int H, int NH, int kGT>
+// kKeep: keep every activation for a backward pass; otherwise the forward
+// pass alternates between two buffers (half the LDS, two workgroups per CU).
+template <int H, int NH, int kGT, bool kKeep>
 struct Gen {
   static constexpr int LD = H + 4;
   static constexpr int WAVES = kGThreads / 64;
@@ -84,8 +86,11 @@ struct Gen {
   static constexpr int PPO = kGThreads / H;     // threads per feature in the VALU loops
   static_assert(H == 16 * WAVES, "one wave per 16 features");
 
+  static constexpr int NBUF = kKeep ? NH + 1 : 2;
+  static constexpr __device__ int buf(int l) { return kKeep ? l : (l & 1); }
+
   struct Smem {
-    float act[NH + 1][kGT][LD];
+    float act[NBUF][kGT][LD];
     float n[kGT][kGMaxIO];
     float o[kGT][kGMaxIO];     // last-layer pre-activation
     float dout[kGT][kGMaxIO];  // dL/d(pre-activation of the last layer)
@@ -154,7 +159,7 @@ struct Gen {
         float v = bias;
 #pragma unroll
         for (int j = 0; j < kGMaxIO; ++j) v = fmaf(w[j], sm.n[ev][j], v);
-        sm.act[0][ev][o] = g_leaky(v, slope);
+        sm.act[buf(0)][ev][o] = g_leaky(v, slope);
       }
     }
     __syncthreads();
@@ -162,7 +167,7 @@ struct Gen {
 #pragma unroll
     for (int l = 0; l < NH; ++l) {
       f32x4 acc[CB];
-      gemm_fwd(p.W[1 + l] + m * p.wsz[1 + l], &sm.act[l][0][0], acc, o0, lr, lg);
+      gemm_fwd(p.W[1 + l] + m * p.wsz[1 + l], &sm.act[buf(l)][0][0], acc, o0, lr, lg);
       const int o = o0 + 4 * lg;
       const f32x4 bias = *reinterpret_cast<const f32x4*>(p.b[1 + l] + m * p.bsz[1 + l] + o);
 #pragma unroll
@@ -170,14 +175,14 @@ struct Gen {
         f32x4 v = acc[cb] + bias;
         v.x = g_leaky(v.x, slope); v.y = g_leaky(v.y, slope);
         v.z = g_leaky(v.z, slope); v.w = g_leaky(v.w, slope);
-        *reinterpret_cast<f32x4*>(&sm.act[l + 1][16 * cb + lr][o]) = v;
+        *reinterpret_cast<f32x4*>(&sm.act[buf(l + 1)][16 * cb + lr][o]) = v;
       }
       __syncthreads();
     }
     if ((tid >> 3) < kGT) {   // last layer: thread (row ev, part) sums features 4 part + 32 c (c < H / 32)
       const int ev = tid >> 3, part = tid & 7;
       const float* Wl = p.W[NH + 1] + m * p.wsz[NH + 1];
-      const float* hrow = &sm.act[NH][ev][0];
+      const float* hrow = &sm.act[buf(NH)][ev][0];
       for (int j = 0; j < p.out; ++j) {
         float z = 0.f;
 #pragma unroll
@@ -319,13 +324,13 @@ struct Gen {
 };
 
 template <int H, int NH, int T>
-__global__ __launch_bounds__(kGThreads, 1) void k_gen_forward(GenParams p) {
-  Gen<H, NH, T>::run_forward(p);
+__global__ __launch_bounds__(kGThreads, 2) void k_gen_forward(GenParams p) {
+  Gen<H, NH, T, false>::run_forward(p);
 }
 
 template <int H, int NH, int T>
 __global__ __launch_bounds__(kGThreads, 1) void k_gen_backward(GenParams p) {
-  Gen<H, NH, T>::run_backward(p);
+  Gen<H, NH, T, true>::run_backward(p);
 }
 
 // Sum of the per-tile partials of member blockIdx.y in a fixed order (tile
@@ -367,54 +372,68 @@ __global__ __launch_bounds__(256) void k_gen_reduce(GenReduceArgs r) {
 
 // Ensemble statistics of theta[M][k][out]: per (row, component) the member
 // mean and the population standard deviation about it (two passes over the
-// members); rowstat[0][r][c] = mean, rowstat[1][r][c] = sigma.
+// members); rowstat[0][r][c] = mean, rowstat[1][r][c] = sigma.  Sixteen lanes
+// share one (row, component): lane j takes members j, j + 16, ..., and the
+// sixteen partial sums are added by shuffles in a fixed pattern.
+constexpr int kEnsLanes = 16;
+
 __global__ __launch_bounds__(256) void k_ens_rows(const float* __restrict__ theta, int M, int64_t k, int out,
                                                   float* __restrict__ rowstat) {
-  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (i >= k * out) return;
+  const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int64_t i = t / kEnsLanes;              // (row, component), uniform across the 16 lanes
+  const int j = (int)(t % kEnsLanes);
   const int64_t stride = k * out;
+  const bool live = i < stride;
   float s = 0.f;
-  for (int m = 0; m < M; ++m) s += theta[m * stride + i];
+  if (live)
+    for (int m = j; m < M; m += kEnsLanes) s += theta[m * stride + i];
+#pragma unroll
+  for (int w = 1; w < kEnsLanes; w <<= 1) s += __shfl_xor(s, w, 64);
   const float mean = s / (float)M;
   float q = 0.f;
-  for (int m = 0; m < M; ++m) {
-    const float dv = theta[m * stride + i] - mean;
-    q = fmaf(dv, dv, q);
+  if (live)
+    for (int m = j; m < M; m += kEnsLanes) {
+      const float dv = theta[m * stride + i] - mean;
+      q = fmaf(dv, dv, q);
+    }
+#pragma unroll
+  for (int w = 1; w < kEnsLanes; w <<= 1) q += __shfl_xor(q, w, 64);
+  if (live && j == 0) {
+    rowstat[i] = mean;
+    rowstat[stride + i] = sqrtf(q / (float)M);
   }
-  rowstat[i] = mean;
-  rowstat[stride + i] = sqrtf(q / (float)M);
 }
 
-// Batch averages of the row statistics (one workgroup): thread t sums rows
-// t, t + 256, ... of component c; the 256 sums are added in a fixed tree.
+// Batch averages of the row statistics (one workgroup): thread (component
+// c, slice q) sums rows q, q + 32, ... of component c (out <= 8); the 32
+// slices of a component are then added in a fixed tree.
 __global__ __launch_bounds__(256) void k_ens_final(const float* __restrict__ rowstat, int64_t k, int out,
                                                    const float* __restrict__ p_true, float* __restrict__ p_hat,
                                                    float* __restrict__ sigma, float* __restrict__ r_hat) {
-  __shared__ float red[2][256];
-  const int tid = threadIdx.x;
-  for (int c = 0; c < out; ++c) {
-    float a = 0.f, b = 0.f;
-    for (int64_t r = tid; r < k; r += 256) {
+  constexpr int kSlices = 256 / kGMaxIO;   // 32
+  __shared__ float red[2][kSlices][kGMaxIO];
+  const int c = threadIdx.x % kGMaxIO, q = threadIdx.x / kGMaxIO;
+  float a = 0.f, b = 0.f;
+  if (c < out)
+    for (int64_t r = q; r < k; r += kSlices) {
       a += rowstat[r * out + c];
       b += rowstat[k * out + r * out + c];
     }
-    red[0][tid] = a;
-    red[1][tid] = b;
-    __syncthreads();
-    for (int w = 128; w > 0; w >>= 1) {
-      if (tid < w) {
-        red[0][tid] += red[0][tid + w];
-        red[1][tid] += red[1][tid + w];
-      }
-      __syncthreads();
-    }
-    if (tid == 0) {
-      const float ph = red[0][0] / (float)k;
-      p_hat[c] = ph;
-      sigma[c] = red[1][0] / (float)k;
-      if (r_hat) r_hat[c] = (p_true[c] - ph) / p_true[c];
+  red[0][q][c] = a;
+  red[1][q][c] = b;
+  __syncthreads();
+  for (int w = kSlices / 2; w > 0; w >>= 1) {
+    if (q < w) {
+      red[0][q][c] += red[0][q + w][c];
+      red[1][q][c] += red[1][q + w][c];
     }
     __syncthreads();
+  }
+  if (q == 0 && c < out) {
+    const float ph = red[0][0][c] / (float)k;
+    p_hat[c] = ph;
+    sigma[c] = red[1][0][c] / (float)k;
+    if (r_hat) r_hat[c] = (p_true[c] - ph) / p_true[c];
   }
 }
 
@@ -547,8 +566,8 @@ hipError_t launch_ensemble(const sagips_gen& G, const float* noise, int64_t k, c
   hipError_t e = launch_gen_forward(G, noise, k, theta, n_cu, st, tm);
   if (e != hipSuccess) return e;
   if (tm) tm->begin("ensemble_rows");
-  hipLaunchKernelGGL(k_ens_rows, dim3((unsigned)((k * out + 255) / 256)), dim3(256), 0, st, theta, G.n_members, k,
-                     out, rowstat);
+  hipLaunchKernelGGL(k_ens_rows, dim3((unsigned)((k * out * kEnsLanes + 255) / 256)), dim3(256), 0, st, theta,
+                     G.n_members, k, out, rowstat);
   if (tm) tm->end();
   e = hipGetLastError();
   if (e != hipSuccess) return e;
