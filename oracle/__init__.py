@@ -55,7 +55,7 @@ from .sampler import (uniform_from_words, kumaraswamy_icdf, kumaraswamy_cdf,  # 
                       features_proxy2, features_proxy2_jacobian)
 from .mlp import mlp_forward, bce_losses, disc_fwd_bwd, round_bf16, input_grad_kink_variants  # noqa: F401
 from .step import param_grad, quadratic_critic, run_step  # noqa: F401
-from .bootstrap import bootstrap, bootstrap_indices, STREAM_BOOTSTRAP  # noqa: F401
+from .bootstrap import bootstrap, bootstrap_indices, bootstrap_row_order, STREAM_BOOTSTRAP  # noqa: F401
 from .optim import adam_step  # noqa: F401
 from .gan import gan_step, initial_state  # noqa: F401
 from .generator import G_WIDTHS, generator_forward, generator_backward, ensemble_response, residual  # noqa: F401

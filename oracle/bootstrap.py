@@ -9,7 +9,8 @@ takes row
 
 where w0 is the first word of Philox4x32-10 under key (seed lo, seed hi) and
 counter (i lo, i hi, stream, step).  Each step thus draws a fresh sub-sample
-that depends only on (seed, step, i).  floor(w0 * n / 2^32) maps the 2^32
+that depends only on (seed, step, i).  bootstrap_row_order lists the same
+multiset in ascending row order.  floor(w0 * n / 2^32) maps the 2^32
 equally likely words onto n rows, each row receiving floor or ceil of 2^32/n
 words (exactly equal when n divides 2^32).
 """
@@ -40,4 +41,12 @@ def bootstrap_indices(n_data: int, n_out: int, seed: int, step: int, stream: int
 def bootstrap(data: np.ndarray, n_out: int, seed: int, step: int):
     """(data[idx], idx): the step's sub-sample of the rows of `data`."""
     idx = bootstrap_indices(data.shape[0], n_out, seed, step)
+    return data[idx], idx
+
+
+def bootstrap_row_order(data: np.ndarray, n_out: int, seed: int, step: int):
+    """The same sub-sample as a multiset listed in ascending row order: row r
+    appears as often as it was drawn.  A batch used as a whole (a mean loss,
+    summed gradients) does not depend on the order of its rows."""
+    idx = np.sort(bootstrap_indices(data.shape[0], n_out, seed, step), kind="stable")
     return data[idx], idx

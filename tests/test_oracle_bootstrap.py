@@ -3,6 +3,7 @@ replacement), by properties that do not retype its formula."""
 import numpy as np
 import pytest
 
+import oracle
 from oracle.bootstrap import bootstrap, bootstrap_indices, STREAM_BOOTSTRAP
 from oracle.philox import philox4x32_10
 
@@ -67,3 +68,18 @@ def test_gather_returns_the_drawn_rows():
 def test_rejects_too_many_rows():
     with pytest.raises(ValueError):
         bootstrap_indices((1 << 32) + 1, 10, seed=0, step=0)
+
+
+def test_row_order_is_the_same_multiset():
+    """Row order lists every drawn row as often as it was drawn, ascending, and
+    its rows are the data rows of those indices (checked by counting, not by
+    re-sorting)."""
+    rng = np.random.default_rng(5)
+    data = rng.standard_normal((997, 3))
+    x, idx = oracle.bootstrap_row_order(data, 1500, 9, 2)
+    _, draws = oracle.bootstrap(data, 1500, 9, 2)
+    assert (np.diff(idx) >= 0).all()
+    np.testing.assert_array_equal(np.bincount(idx, minlength=997), np.bincount(draws, minlength=997))
+    np.testing.assert_array_equal(x, data[idx])
+    # the batch mean, which is what a whole-batch loss sees, is unchanged
+    np.testing.assert_allclose(x.mean(axis=0), data[draws].mean(axis=0), rtol=1e-12)
