@@ -38,6 +38,7 @@ KERNEL_SOURCES = {
     "bf16_wgrad": ["paper_2407_00051_amd/csrc/disc_bf16.hip", "paper_2407_00051_amd/csrc/device_math.hpp"],
     "param_grad": ["paper_2407_00051_amd/csrc/sampler.hip", "paper_2407_00051_amd/csrc/device_math.hpp"],
     "bootstrap": ["paper_2407_00051_amd/csrc/sampler.hip", "paper_2407_00051_amd/csrc/device_math.hpp"],
+    "bootstrap_rows": ["paper_2407_00051_amd/csrc/sampler.hip", "paper_2407_00051_amd/csrc/device_math.hpp"],
     "gen_forward": ["paper_2407_00051_amd/csrc/generator.hip", "paper_2407_00051_amd/csrc/device_math.hpp"],
     "sample_events": ["paper_2407_00051_amd/csrc/sampler.hip", "paper_2407_00051_amd/csrc/device_math.hpp"],
 }
@@ -135,9 +136,10 @@ def cpu_baseline_bootstrap(w, n_out: int, min_seconds: float = 10.0):
     except Exception:
         threads = os.cpu_count()
     pool = oracle.sample(np.asarray([w.theta_star], dtype=np.float32), 2 * n_out, w.pool_seed).astype(np.float32)
+    draw = oracle.bootstrap_row_order if w.row_order else oracle.bootstrap
     reps, t0 = 0, time.perf_counter()
     while True:
-        oracle.bootstrap(pool, n_out, w.seed, reps)
+        draw(pool, n_out, w.seed, reps)
         reps += 1
         dt = time.perf_counter() - t0
         if dt >= min_seconds:
@@ -155,7 +157,7 @@ def bench_bootstrap(args, w, ctx, torch):
     it = [0]
 
     def step():
-        ctx.bootstrap(pool, w.n_out, w.seed, it[0], out=out)
+        ctx.bootstrap(pool, w.n_out, w.seed, it[0], out=out, row_order=w.row_order)
         it[0] += 1
 
     for _ in range(args.warmup):
@@ -172,14 +174,15 @@ def bench_bootstrap(args, w, ctx, torch):
     ctx.set_timing(False)
     kt = ctx.kernel_times()
     ms_per_step = (t1 - t0) * 1e3 / args.steps
-    launches, total_ms = kt["bootstrap"]
+    name = "bootstrap_rows" if w.row_order else "bootstrap"
+    launches, total_ms = kt[name]       # the row order times its five kernels as one
     avg_ms = total_ms / launches
     # algorithmic bytes of a draw: the drawn row read once and written once
     bytes_per_launch = w.n_out * 2 * w.d * 4
     achieved = bytes_per_launch / (avg_ms * 1e-3)
     roof = {"bound": "hbm", "achieved": achieved / 1e9, "peak": PEAK["hbm"] / 1e9, "unit": "GB/s",
-            "frac": achieved / PEAK["hbm"], "traffic": read_traffic("bootstrap", w.name),
-            "kernel": "bootstrap", "kernel_avg_ms": avg_ms,
+            "frac": achieved / PEAK["hbm"], "traffic": read_traffic(name, w.name),
+            "kernel": name, "kernel_avg_ms": avg_ms,
             "kernels": {k: {"launches": n, "avg_ms": t / max(n, 1)} for k, (n, t) in kt.items()}}
     line = {
         "metric": "draws/sec of the bootstrap sub-sample of the real data; % of HBM peak",
@@ -188,7 +191,7 @@ def bench_bootstrap(args, w, ctx, torch):
         "vs_baseline": None, "dtype": "u32",
         "data": "synthetic (pool of Philox-sampled Kumaraswamy events at theta_star)",
         "config": {"workload": w.name, "n_data": w.n_data, "d": w.d, "n_out": w.n_out,
-                   "parallelism": "single GPU"},
+                   "order": "ascending row" if w.row_order else "draw", "parallelism": "single GPU"},
         "roofline": roof,
     }
     if not args.no_cpu_baseline:

@@ -193,6 +193,18 @@ sagips_status sagips_param_grad(sagips_ctx* ctx, const sagips_source* src, sagip
 sagips_status sagips_bootstrap(sagips_ctx* ctx, const float* data, int64_t n_data, int d, uint64_t seed,
                                uint32_t step, int64_t n_out, float* out, int64_t* idx_out);
 
+/* 4b. The same sub-sample listed in ascending row order: row r of data
+ * appears as often as sagips_bootstrap draws it with the same (seed, step,
+ * n_out).  A batch used as a whole (the discriminator's mean loss and summed
+ * gradients) does not depend on the order of its rows, and this order lets
+ * the reference data be read once, in order, instead of one random line per
+ * draw.  Arguments as for sagips_bootstrap, with 1 <= n_data <= 2^27 and
+ * n_out < 2^31 (SAGIPS_E_UNSUPPORTED beyond); idx_out receives the rows in
+ * the same ascending order.  Uses the context's workspace (6 bytes per draw
+ * plus per-slab counts).                                                  */
+sagips_status sagips_bootstrap_rows(sagips_ctx* ctx, const float* data, int64_t n_data, int d, uint64_t seed,
+                                    uint32_t step, int64_t n_out, float* out, int64_t* idx_out);
+
 /* A stack of M generators of one shape (paper Sec. III: the optimiser is a GAN
  * generator mapping noise to parameters; Sec. V-A: LeakyReLU hidden layers).
  * Layer l maps width[l] -> width[l+1]; member m's weight is the

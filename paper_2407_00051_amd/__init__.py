@@ -25,7 +25,7 @@ CRITIC_BUFFER, CRITIC_QUADRATIC = 0, 1
 
 EXPORTED = ("sagips_create", "sagips_destroy", "sagips_set_stream", "sagips_last_error", "sagips_set_timing",
             "sagips_kernel_times", "sagips_sample_events", "sagips_disc_fwd_bwd", "sagips_param_grad",
-            "sagips_bootstrap", "sagips_gen_forward", "sagips_gen_backward", "sagips_ensemble_response",
+            "sagips_bootstrap", "sagips_bootstrap_rows", "sagips_gen_forward", "sagips_gen_backward", "sagips_ensemble_response",
             "sagips_adam_step")
 
 
@@ -91,6 +91,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
                                         ctypes.POINTER(DiscOut)]
     lib.sagips_param_grad.argtypes = [vp, ctypes.POINTER(Source), i32, vp, vp, vp]
     lib.sagips_bootstrap.argtypes = [vp, vp, i64, i32, ctypes.c_uint64, ctypes.c_uint32, i64, vp, vp]
+    lib.sagips_bootstrap_rows.argtypes = lib.sagips_bootstrap.argtypes
     lib.sagips_gen_forward.argtypes = [vp, ctypes.POINTER(GenStack), vp, i64, vp]
     lib.sagips_gen_backward.argtypes = [vp, ctypes.POINTER(GenStack), vp, i64, vp, ctypes.POINTER(vp),
                                         ctypes.POINTER(vp)]
@@ -99,7 +100,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
                                      ctypes.c_double, ctypes.c_double]
     for name in ("sagips_create", "sagips_destroy", "sagips_set_stream", "sagips_set_timing",
                  "sagips_kernel_times", "sagips_sample_events", "sagips_disc_fwd_bwd", "sagips_param_grad",
-                 "sagips_bootstrap", "sagips_gen_forward", "sagips_gen_backward", "sagips_ensemble_response",
+                 "sagips_bootstrap", "sagips_bootstrap_rows", "sagips_gen_forward", "sagips_gen_backward", "sagips_ensemble_response",
                  "sagips_adam_step"):
         getattr(lib, name).restype = ctypes.c_int
     _lib = lib
@@ -212,9 +213,11 @@ class Context:
         return x if want_x else w
 
     # -- 4. reference data -> bootstrapped sub-sample --------------------------------
-    def bootstrap(self, data, n_out: int, seed: int, step: int, want_idx: bool = False, out=None, idx_out=None):
+    def bootstrap(self, data, n_out: int, seed: int, step: int, want_idx: bool = False, out=None, idx_out=None,
+                  row_order: bool = False):
         """The step's sub-sample [n_out][d] of the rows of data (drawn with replacement), and
-        optionally the drawn row indices [n_out] int64."""
+        optionally the drawn row indices [n_out] int64; with row_order the same multiset in
+        ascending row order."""
         import torch
         _check_tensor(data, "data", torch.float32, None, self.device)
         if data.dim() != 2 or data.shape[1] not in (2, 3):
@@ -226,8 +229,9 @@ class Context:
         if want_idx:
             idx = idx_out if idx_out is not None else torch.empty(n_out, dtype=torch.int64, device=data.device)
             _check_tensor(idx, "idx_out", torch.int64, (n_out,), self.device)
-        self._check(self.lib.sagips_bootstrap(self.h, _ptr(data), data.shape[0], d, seed & (2**64 - 1),
-                                              step & 0xFFFFFFFF, n_out, _ptr(x), _ptr(idx)))
+        fn = self.lib.sagips_bootstrap_rows if row_order else self.lib.sagips_bootstrap
+        self._check(fn(self.h, _ptr(data), data.shape[0], d, seed & (2**64 - 1), step & 0xFFFFFFFF, n_out, _ptr(x),
+                       _ptr(idx)))
         self._keep = (data,)
         return (x, idx) if want_idx else x
 

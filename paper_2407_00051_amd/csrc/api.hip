@@ -204,6 +204,25 @@ sagips_status check_gen(sagips_ctx* c, const sagips_gen* G, const float* noise, 
   return SAGIPS_OK;
 }
 
+sagips_status check_bootstrap(sagips_ctx* c, const float* data, int64_t n_data, int d, int64_t n_out, float* out,
+                              int64_t* idx_out) {
+  if (!c) return fail(nullptr, SAGIPS_E_INVAL, "ctx is NULL");
+  if (!data || !out) return fail(c, SAGIPS_E_INVAL, "data or out is NULL");
+  if (d != 2 && d != 3) return fail(c, SAGIPS_E_INVAL, "d = %d, must be 2 or 3", d);
+  if (n_data < 1 || n_data > ((int64_t)1 << 32)) return fail(c, SAGIPS_E_INVAL, "n_data = %lld outside [1, 2^32]", (long long)n_data);
+  if (n_out < 1) return fail(c, SAGIPS_E_INVAL, "n_out must be >= 1");
+  if (!aligned16(data) || !aligned16(out) || (idx_out && !aligned16(idx_out)))
+    return fail(c, SAGIPS_E_INVAL, "data, out and idx_out must be 16-byte aligned");
+  const uintptr_t d0 = reinterpret_cast<uintptr_t>(data), d1 = d0 + (uintptr_t)n_data * d * sizeof(float);
+  const uintptr_t o0 = reinterpret_cast<uintptr_t>(out), o1 = o0 + (uintptr_t)n_out * d * sizeof(float);
+  if (o0 < d1 && d0 < o1) return fail(c, SAGIPS_E_INVAL, "out overlaps data");
+  if (idx_out) {
+    const uintptr_t i0 = reinterpret_cast<uintptr_t>(idx_out), i1 = i0 + (uintptr_t)n_out * sizeof(int64_t);
+    if ((i0 < d1 && d0 < i1) || (i0 < o1 && o0 < i1)) return fail(c, SAGIPS_E_INVAL, "idx_out overlaps data or out");
+  }
+  return SAGIPS_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -421,24 +440,26 @@ sagips_status sagips_disc_fwd_bwd(sagips_ctx* c, const sagips_mlp* D, const floa
 
 sagips_status sagips_bootstrap(sagips_ctx* c, const float* data, int64_t n_data, int d, uint64_t seed, uint32_t step,
                                int64_t n_out, float* out, int64_t* idx_out) {
-  if (!c) return fail(nullptr, SAGIPS_E_INVAL, "ctx is NULL");
-  if (!data || !out) return fail(c, SAGIPS_E_INVAL, "data or out is NULL");
-  if (d != 2 && d != 3) return fail(c, SAGIPS_E_INVAL, "d = %d, must be 2 or 3", d);
-  if (n_data < 1 || n_data > ((int64_t)1 << 32)) return fail(c, SAGIPS_E_INVAL, "n_data = %lld outside [1, 2^32]", (long long)n_data);
-  if (n_out < 1) return fail(c, SAGIPS_E_INVAL, "n_out must be >= 1");
-  if (!aligned16(data) || !aligned16(out) || (idx_out && !aligned16(idx_out)))
-    return fail(c, SAGIPS_E_INVAL, "data, out and idx_out must be 16-byte aligned");
-  const uintptr_t d0 = reinterpret_cast<uintptr_t>(data), d1 = d0 + (uintptr_t)n_data * d * sizeof(float);
-  const uintptr_t o0 = reinterpret_cast<uintptr_t>(out), o1 = o0 + (uintptr_t)n_out * d * sizeof(float);
-  if (o0 < d1 && d0 < o1) return fail(c, SAGIPS_E_INVAL, "out overlaps data");
-  if (idx_out) {
-    const uintptr_t i0 = reinterpret_cast<uintptr_t>(idx_out), i1 = i0 + (uintptr_t)n_out * sizeof(int64_t);
-    if ((i0 < d1 && d0 < i1) || (i0 < o1 && o0 < i1)) return fail(c, SAGIPS_E_INVAL, "idx_out overlaps data or out");
-  }
+  sagips_status s = check_bootstrap(c, data, n_data, d, n_out, out, idx_out);
+  if (s != SAGIPS_OK) return s;
   DeviceGuard g(c->device);
   hipError_t e = launch_bootstrap(data, (uint64_t)n_data, d, (uint32_t)(seed & 0xffffffffu), (uint32_t)(seed >> 32),
                                   step, n_out, out, idx_out, c->n_cu, c->stream, timer_of(c));
   return e == hipSuccess ? SAGIPS_OK : hip_fail(c, e, "bootstrap launch");
+}
+
+sagips_status sagips_bootstrap_rows(sagips_ctx* c, const float* data, int64_t n_data, int d, uint64_t seed,
+                                    uint32_t step, int64_t n_out, float* out, int64_t* idx_out) {
+  sagips_status s = check_bootstrap(c, data, n_data, d, n_out, out, idx_out);
+  if (s != SAGIPS_OK) return s;
+  if (n_data > ((int64_t)1 << 27)) return fail(c, SAGIPS_E_UNSUPPORTED, "row order supports n_data <= 2^27");
+  if (n_out >= ((int64_t)1 << 31)) return fail(c, SAGIPS_E_UNSUPPORTED, "row order supports n_out < 2^31");
+  DeviceGuard g(c->device);
+  s = ensure_ws(c, bootstrap_rows_workspace((uint64_t)n_data, n_out, nullptr, nullptr, nullptr));
+  if (s != SAGIPS_OK) return s;
+  hipError_t e = launch_bootstrap_rows(data, (uint64_t)n_data, d, (uint32_t)(seed & 0xffffffffu),
+                                       (uint32_t)(seed >> 32), step, n_out, out, idx_out, c->ws, c->stream, timer_of(c));
+  return e == hipSuccess ? SAGIPS_OK : hip_fail(c, e, "bootstrap_rows launch");
 }
 
 sagips_status sagips_gen_forward(sagips_ctx* c, const sagips_gen* G, const float* noise, int64_t k, float* theta) {

@@ -50,6 +50,9 @@ hipError_t launch_param_grad(const SourceArgs& s, const float* dLdx, float* dLdt
                              void* ws, hipStream_t st, Timer* tm);
 
 // Bootstrap draws: out[i] = data[floor(w0(i) * n_data / 2^32)], idx_out optional.
+size_t bootstrap_rows_workspace(uint64_t n_data, int64_t n_out, int* n_slabs, int* n_chunks, int64_t* per_chunk);
+hipError_t launch_bootstrap_rows(const float* data, uint64_t n_data, int d, uint32_t k0, uint32_t k1, uint32_t step,
+                                 int64_t n_out, float* out, int64_t* idx_out, void* ws, hipStream_t st, Timer* tm);
 hipError_t launch_bootstrap(const float* data, uint64_t n_data, int d, uint32_t k0, uint32_t k1, uint32_t step,
                             int64_t n_out, float* out, int64_t* idx_out, int n_cu, hipStream_t st, Timer* tm);
 

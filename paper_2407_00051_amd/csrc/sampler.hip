@@ -177,6 +177,163 @@ __global__ __launch_bounds__(kThreads) void k_bootstrap(const float* __restrict_
   }
 }
 
+// The same draws listed in ascending row order, by a counting sort over
+// slabs of 2^kSlabBits consecutive rows of the reference data:
+//   k_boot_count    each chunk of draws: its rows (kept for the scatter) and a
+//                   per-slab count, [slab][chunk]
+//   k_boot_scan     per slab, the exclusive scan of its chunk counts, and the
+//                   slab's total
+//   k_boot_base     the exclusive scan of the slab totals (one workgroup)
+//   k_boot_scatter  each draw's row offset within its slab (16 bits) into the
+//                   slab's segment, at the chunk's place
+//   k_boot_expand   per slab: a histogram of the offsets in LDS, its scan, then
+//                   output position p takes row upper_bound(scan, p) - 1 of the
+//                   slab; rows are read nearly in order and written in order.
+// Placement within a (slab, chunk) segment follows LDS atomics, but the final
+// output is the unique ascending listing of the drawn rows.
+constexpr int kSlabBits = 14;
+constexpr int kSlabRows = 1 << kSlabBits;
+constexpr int kBootBig = 1024;     // threads of the count, scatter and expand kernels
+
+__global__ __launch_bounds__(kBootBig) void k_boot_count(uint64_t n_data, uint32_t k0, uint32_t k1, uint32_t step,
+                                                         int64_t n_out, int64_t per_chunk, int n_slabs, int n_chunks,
+                                                         uint32_t* __restrict__ rows, uint32_t* __restrict__ cnt) {
+  extern __shared__ uint32_t hist[];   // [n_slabs]
+  for (int s = threadIdx.x; s < n_slabs; s += kBootBig) hist[s] = 0u;
+  __syncthreads();
+  const int64_t i0 = (int64_t)blockIdx.x * per_chunk, i1 = min(n_out, i0 + per_chunk);
+  for (int64_t i = i0 + threadIdx.x; i < i1; i += kBootBig) {
+    const Words w = philox4x32_10((uint32_t)i, (uint32_t)((uint64_t)i >> 32), SAGIPS_STREAM_BOOTSTRAP, step, k0, k1);
+    const uint32_t r = (uint32_t)(((uint64_t)w.w[0] * n_data) >> 32);
+    rows[i] = r;
+    atomicAdd(&hist[r >> kSlabBits], 1u);
+  }
+  __syncthreads();
+  for (int s = threadIdx.x; s < n_slabs; s += kBootBig) cnt[(int64_t)s * n_chunks + blockIdx.x] = hist[s];
+}
+
+// One wave per slab: exclusive scan of cnt[slab][0 .. n_chunks) in place, and
+// the slab's total.
+__global__ __launch_bounds__(64) void k_boot_scan(uint32_t* __restrict__ cnt, int n_chunks,
+                                                  uint32_t* __restrict__ total) {
+  uint32_t* c = cnt + (int64_t)blockIdx.x * n_chunks;
+  const int lane = threadIdx.x;
+  uint32_t carry = 0u;
+  for (int b = 0; b < n_chunks; b += 64) {
+    const int j = b + lane;
+    const uint32_t v = j < n_chunks ? c[j] : 0u;
+    uint32_t incl = v;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const uint32_t t = __shfl_up(incl, o, 64);
+      if (lane >= o) incl += t;
+    }
+    if (j < n_chunks) c[j] = carry + incl - v;
+    carry += __shfl(incl, 63, 64);
+  }
+  if (lane == 0) total[blockIdx.x] = carry;
+}
+
+// One workgroup: base[s] = sum of total[0 .. s), base[n_slabs] = n_out.
+__global__ __launch_bounds__(kBootBig) void k_boot_base(const uint32_t* __restrict__ total, int n_slabs,
+                                                        uint32_t* __restrict__ base) {
+  __shared__ uint32_t part[kBootBig];
+  const int t = threadIdx.x;
+  const int per = (n_slabs + kBootBig - 1) / kBootBig;
+  uint32_t s = 0u;
+  for (int j = 0; j < per; ++j) {
+    const int q = t * per + j;
+    if (q < n_slabs) s += total[q];
+  }
+  part[t] = s;
+  __syncthreads();
+  for (int o = 1; o < kBootBig; o <<= 1) {     // inclusive scan of the thread sums (Hillis-Steele)
+    const uint32_t v = t >= o ? part[t - o] : 0u;
+    __syncthreads();
+    part[t] += v;
+    __syncthreads();
+  }
+  uint32_t run = t > 0 ? part[t - 1] : 0u;
+  for (int j = 0; j < per; ++j) {
+    const int q = t * per + j;
+    if (q < n_slabs) {
+      base[q] = run;
+      run += total[q];
+    }
+  }
+  if (t == kBootBig - 1) base[n_slabs] = part[kBootBig - 1];
+}
+
+__global__ __launch_bounds__(kBootBig) void k_boot_scatter(const uint32_t* __restrict__ rows, int64_t n_out,
+                                                           int64_t per_chunk, int n_slabs, int n_chunks,
+                                                           const uint32_t* __restrict__ cnt,
+                                                           const uint32_t* __restrict__ base, uint16_t* __restrict__ keys) {
+  extern __shared__ uint32_t cursor[];   // [n_slabs]
+  for (int s = threadIdx.x; s < n_slabs; s += kBootBig) cursor[s] = base[s] + cnt[(int64_t)s * n_chunks + blockIdx.x];
+  __syncthreads();
+  const int64_t i0 = (int64_t)blockIdx.x * per_chunk, i1 = min(n_out, i0 + per_chunk);
+  for (int64_t i = i0 + threadIdx.x; i < i1; i += kBootBig) {
+    const uint32_t r = rows[i];
+    const uint32_t pos = atomicAdd(&cursor[r >> kSlabBits], 1u);
+    keys[pos] = (uint16_t)(r & (kSlabRows - 1));
+  }
+}
+
+template <int D>
+__global__ __launch_bounds__(kBootBig) void k_boot_expand(const float* __restrict__ data, const uint16_t* __restrict__ keys,
+                                                          const uint32_t* __restrict__ base, float* __restrict__ out,
+                                                          int64_t* __restrict__ idx_out) {
+  __shared__ uint32_t h[kSlabRows];
+  __shared__ uint32_t part[kBootBig];
+  constexpr int PER = kSlabRows / kBootBig;   // 16 histogram entries per thread
+  const int t = threadIdx.x;
+  const uint32_t b0 = base[blockIdx.x], b1 = base[blockIdx.x + 1];
+  for (int j = t; j < kSlabRows; j += kBootBig) h[j] = 0u;
+  __syncthreads();
+  for (uint32_t p = b0 + t; p < b1; p += kBootBig) atomicAdd(&h[keys[p]], 1u);
+  __syncthreads();
+  // exclusive scan of h: each thread its 16 entries, then the thread sums
+  uint32_t loc[PER];
+  uint32_t s = 0u;
+#pragma unroll
+  for (int j = 0; j < PER; ++j) {
+    loc[j] = s;
+    s += h[t * PER + j];
+  }
+  part[t] = s;
+  __syncthreads();
+  for (int o = 1; o < kBootBig; o <<= 1) {
+    const uint32_t v = t >= o ? part[t - o] : 0u;
+    __syncthreads();
+    part[t] += v;
+    __syncthreads();
+  }
+  const uint32_t off = t > 0 ? part[t - 1] : 0u;
+#pragma unroll
+  for (int j = 0; j < PER; ++j) h[t * PER + j] = off + loc[j];
+  __syncthreads();
+  // output q of the slab takes the last row j with h[j] <= q (rows drawn zero
+  // times share their start with the next row and are passed over)
+  const uint64_t row0 = (uint64_t)blockIdx.x << kSlabBits;
+  for (uint32_t p = b0 + t; p < b1; p += kBootBig) {
+    const uint32_t q = p - b0;
+    int lo = 0, n = kSlabRows;                 // upper_bound over h[0 .. kSlabRows)
+    while (n > 0) {
+      const int half = n >> 1;
+      if (h[lo + half] <= q) {
+        lo += half + 1;
+        n -= half + 1;
+      } else {
+        n = half;
+      }
+    }
+    const uint64_t r = row0 + (uint64_t)(lo - 1);
+    if (idx_out) idx_out[p] = (int64_t)r;
+#pragma unroll
+    for (int j = 0; j < D; ++j) out[(int64_t)p * D + j] = data[r * D + j];
+  }
+}
+
 }  // namespace
 
 hipError_t launch_bootstrap(const float* data, uint64_t n_data, int d, uint32_t k0, uint32_t k1, uint32_t step,
@@ -186,6 +343,49 @@ hipError_t launch_bootstrap(const float* data, uint64_t n_data, int d, uint32_t 
   if (tm) tm->begin("bootstrap");
   if (d == 2) hipLaunchKernelGGL(k_bootstrap<2>, dim3(blocks), dim3(kThreads), 0, st, data, n_data, k0, k1, step, n_out, out, idx_out);
   else hipLaunchKernelGGL(k_bootstrap<3>, dim3(blocks), dim3(kThreads), 0, st, data, n_data, k0, k1, step, n_out, out, idx_out);
+  if (tm) tm->end();
+  return hipGetLastError();
+}
+
+size_t bootstrap_rows_workspace(uint64_t n_data, int64_t n_out, int* n_slabs_out, int* n_chunks_out,
+                                int64_t* per_chunk_out) {
+  const int n_slabs = (int)((n_data + kSlabRows - 1) / kSlabRows);
+  int n_chunks = (int)std::min<int64_t>(256, std::max<int64_t>(1, (n_out + 16383) / 16384));
+  const int64_t per_chunk = (n_out + n_chunks - 1) / n_chunks;
+  if (n_slabs_out) *n_slabs_out = n_slabs;
+  if (n_chunks_out) *n_chunks_out = n_chunks;
+  if (per_chunk_out) *per_chunk_out = per_chunk;
+  auto al = [](size_t b) { return (b + 255) & ~(size_t)255; };
+  return al(4 * (size_t)n_out) + al(2 * (size_t)n_out) + al(4 * (size_t)n_slabs * n_chunks) + al(4 * (size_t)n_slabs) +
+         al(4 * ((size_t)n_slabs + 1));
+}
+
+hipError_t launch_bootstrap_rows(const float* data, uint64_t n_data, int d, uint32_t k0, uint32_t k1, uint32_t step,
+                                 int64_t n_out, float* out, int64_t* idx_out, void* ws, hipStream_t st, Timer* tm) {
+  int n_slabs, n_chunks;
+  int64_t per_chunk;
+  bootstrap_rows_workspace(n_data, n_out, &n_slabs, &n_chunks, &per_chunk);
+  auto al = [](size_t b) { return (b + 255) & ~(size_t)255; };
+  char* w = static_cast<char*>(ws);
+  uint32_t* rows = reinterpret_cast<uint32_t*>(w);
+  w += al(4 * (size_t)n_out);
+  uint16_t* keys = reinterpret_cast<uint16_t*>(w);
+  w += al(2 * (size_t)n_out);
+  uint32_t* cnt = reinterpret_cast<uint32_t*>(w);
+  w += al(4 * (size_t)n_slabs * n_chunks);
+  uint32_t* total = reinterpret_cast<uint32_t*>(w);
+  w += al(4 * (size_t)n_slabs);
+  uint32_t* base = reinterpret_cast<uint32_t*>(w);
+  const size_t lds = sizeof(uint32_t) * (size_t)n_slabs;
+  if (tm) tm->begin("bootstrap_rows");
+  hipLaunchKernelGGL(k_boot_count, dim3(n_chunks), dim3(kBootBig), lds, st, n_data, k0, k1, step, n_out, per_chunk,
+                     n_slabs, n_chunks, rows, cnt);
+  hipLaunchKernelGGL(k_boot_scan, dim3(n_slabs), dim3(64), 0, st, cnt, n_chunks, total);
+  hipLaunchKernelGGL(k_boot_base, dim3(1), dim3(kBootBig), 0, st, total, n_slabs, base);
+  hipLaunchKernelGGL(k_boot_scatter, dim3(n_chunks), dim3(kBootBig), lds, st, rows, n_out, per_chunk, n_slabs, n_chunks,
+                     cnt, base, keys);
+  if (d == 2) hipLaunchKernelGGL(k_boot_expand<2>, dim3(n_slabs), dim3(kBootBig), 0, st, data, keys, base, out, idx_out);
+  else hipLaunchKernelGGL(k_boot_expand<3>, dim3(n_slabs), dim3(kBootBig), 0, st, data, keys, base, out, idx_out);
   if (tm) tm->end();
   return hipGetLastError();
 }

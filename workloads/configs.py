@@ -73,6 +73,7 @@ class BootstrapWorkload:
     n_out: int                   # draws per step
     seed: int = 5                # Philox key of the draws
     pool_seed: int = 1           # Philox key of the pool's events
+    row_order: bool = False      # the same multiset in ascending row order
 
     @property
     def theta_star(self) -> Tuple[float, ...]:
@@ -84,6 +85,9 @@ BOOTSTRAP_CONFIGS = {
     "bootstrap": BootstrapWorkload("bootstrap", 2 * 4194304, 2, 4194304),
     # the real batch of the 1,024 x 16,384-event three-observable step
     "bootstrap_d3": BootstrapWorkload("bootstrap_d3", 2 * 16777216, 3, 16777216),
+    # the same draws listed in ascending row order (a counting sort by pool slab)
+    "bootstrap_rows": BootstrapWorkload("bootstrap_rows", 2 * 4194304, 2, 4194304, row_order=True),
+    "bootstrap_rows_d3": BootstrapWorkload("bootstrap_rows_d3", 2 * 16777216, 3, 16777216, row_order=True),
 }
 
 
