@@ -375,8 +375,6 @@ def bench_sample(args, w, ctx, torch):
     """Steps of the stand-alone sampler on the stress configuration: theta -> Philox ->
     Kumaraswamy events written to HBM ([N][d] fp32), the path that feeds a buffered
     discriminator."""
-    import numpy as np
-    import oracle
     from workloads import gen
     dev = "cuda:0"
     inp = gen.make_inputs(w)
@@ -420,6 +418,8 @@ def bench_sample(args, w, ctx, torch):
         "roofline": roof,
     }
     if not args.no_cpu_baseline:
+        import numpy as np
+        import oracle
         try:
             from threadpoolctl import threadpool_info
             threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
