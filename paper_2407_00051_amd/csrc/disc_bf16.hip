@@ -121,6 +121,43 @@ __global__ __launch_bounds__(256) void k_weights_frag(const float* __restrict__ 
   *reinterpret_cast<uint4*>(Wf + (size_t)t * 8) = make_uint4(wp[0], wp[1], wp[2], wp[3]);
 }
 
+// Term t (0 = hi, 1 = mid, 2 = lo) of the exact three-term bf16 split above.
+__device__ __forceinline__ u16 bf16_term(float x, int t) {
+  uint32_t lo;
+  const uint32_t hm = bias_terms(x, lo);
+  return (u16)(t == 0 ? (hm & 0xffffu) : t == 1 ? (hm >> 16) : lo);
+}
+
+// The first-layer products of the backward chain (dW_1, db_1 and dL/dx, with
+// K <= 8 first-layer inputs) run on the bf16 matrix cores with the fp32
+// operand split into its three bf16 terms, so every product is exact in fp32.
+// Their 32-row operand puts term t of input j (j = 4 h + p < 8) in row
+// R = 8 t + 4 h + p: in the accumulator fragment of a lane in half h, register
+// 4 t + p then holds term t of input 4 h + p, and the three terms add up
+// within the lane.  Rows 24..26 carry the terms of the db_1 column (all-ones
+// input) where it is used; other rows are zero.
+//
+// k_w0_frag: W_1 ([H][F] fp32) in that arrangement as the A operand of the
+// dL/dx product (M = 32 rows, K = hidden features): piece (ks, lane) holds
+// row R = lane % 32 for hidden features 16 ks + 8 (lane / 32) .. + 7.
+__global__ __launch_bounds__(256) void k_w0_frag(const float* __restrict__ W0, int F, int H, u16* __restrict__ out) {
+  const int t = blockIdx.x * 256 + threadIdx.x;
+  if (t >= (H / 16) * 64) return;
+  const int ks = t / 64, lane = t % 64, R = lane & 31, term = R >> 3, j = R & 7;
+  uint32_t w[4];
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    uint32_t h2[2];
+#pragma unroll
+    for (int e = 0; e < 2; ++e) {
+      const int o = 16 * ks + 8 * (lane >> 5) + 2 * u + e;
+      h2[e] = (term < 3 && j < F) ? bf16_term(W0[o * F + j], term) : 0u;
+    }
+    w[u] = h2[0] | (h2[1] << 16);
+  }
+  *reinterpret_cast<uint4*>(out + (size_t)t * 8) = make_uint4(w[0], w[1], w[2], w[3]);
+}
+
 // ---------------------------------------------------------------------------
 // Rows of one chunk: features (and x for fake rows).  Rows past `valid` are
 // padding: features 0.5, never stored anywhere visible.
@@ -339,12 +376,24 @@ __device__ __forceinline__ bf16x8 copy_read(const u16* p0) {
 // acc[mt][nt] = sum_k W[feature][k] act[event][k] (+ the bias with kFwd; see
 // above for the arrangement).  pf holds the first PD weight steps of W on
 // entry and those of Wnext (the next product) on exit.
+//
+// The product's input goes to HBM meanwhile, as the weight-gradient operand:
+// the wave's own columns of act, copy kilobyte j (the K-fragment order above;
+// dst at per-lane byte offset coff) read with the operands of step CS j and
+// stored after its products.  Spread over the product, the stores drain while the matrix cores
+// run, and a weight load waits behind at most a few of them (loads and stores
+// share one completion counter).
 template <int H, bool kFwd>
 __device__ __forceinline__ void chain_gemm(Rsrc W, Rsrc Wnext, uint32_t woff, WeightPrefetch<H>& pf, const u16* act,
-                                           f32x16 (&acc)[Chain<H>::MT][Chain<H>::NT], int lane) {
+                                           f32x16 (&acc)[Chain<H>::MT][Chain<H>::NT], int lane, int wave, u16* dst,
+                                           uint32_t coff) {
   using C = Chain<H>;
   constexpr int KS = C::KS, PD = C::PD, LDA = C::LDA, MT = C::MT, NT = C::NT;
   constexpr int N = WSteps<H, kFwd>::N;          // K steps, the bias step last
+  constexpr int CS = KS / C::COPIES;             // K steps per copy kilobyte
+  static_assert(CS >= 1 && KS % C::COPIES == 0, "copy spread");
+  const u16* cbase = act + copy_lds_base<LDA>(lane, wave);
+  char* cdst = reinterpret_cast<char*>(dst) + coff;
   const int lr = lane & 31, lh = lane >> 5;
   const u16* brow = act + lr * LDA + 8 * lh;
   // B fragment of the bias step: ones against the three bias terms (lane
@@ -368,6 +417,10 @@ __device__ __forceinline__ void chain_gemm(Rsrc W, Rsrc Wnext, uint32_t woff, We
       else
         pf.a[ks + PD - N][m] = load_frag(Wnext, woff, (uint32_t)(m * N + ks + PD - N) * 1024);
     }
+    const int j = ks / CS;                       // copy kilobyte of this step, if ks % CS == 0
+    const bool cp = ks % CS == 0 && j < C::COPIES;
+    bf16x8 cv;
+    if (cp) cv = copy_read<LDA>(cbase + 16 * (j >> 1) * LDA + 32 * (j & 1));
     if (ks + 1 < KS) {
 #pragma unroll
       for (int n = 0; n < NT; ++n)
@@ -383,24 +436,9 @@ __device__ __forceinline__ void chain_gemm(Rsrc W, Rsrc Wnext, uint32_t woff, We
         acc[m][n] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[ks % (PD + 1)][m], ks < KS ? b[ks & 1][n] : ones,
                                                            ks == 0 ? zero : acc[m][n], 0, 0, 0);
     __builtin_amdgcn_sched_barrier(0);
-  }
-}
-
-// Writes the wave's columns of the LDS tile (the features it owns: only its
-// own epilogue overwrites them, so no other wave has to be waited for) to the
-// tile's copy in HBM: dst in K-fragment order, per-lane byte offset
-// coff = (2 w 64 + lane) 16.  Issued after the product's last weight loads,
-// so the stores never sit in front of a product's weight loads.
-template <int H>
-__device__ __forceinline__ void copy_out(const u16* act, int lane, int wave, u16* dst, uint32_t coff) {
-  using C = Chain<H>;
-  constexpr int LDA = C::LDA;
-  const u16* cbase = act + copy_lds_base<LDA>(lane, wave);
-#pragma unroll
-  for (int j = 0; j < C::COPIES; ++j) {
-    const bf16x8 cv = copy_read<LDA>(cbase + 16 * (j >> 1) * LDA + 32 * (j & 1));
-    *reinterpret_cast<uint4*>(reinterpret_cast<char*>(dst) + ((j >> 1) * (H / 32) + (j & 1)) * 1024 + coff) =
-        __builtin_bit_cast(uint4, cv);
+    if (cp)
+      *reinterpret_cast<uint4*>(cdst + ((j >> 1) * (H / 32) + (j & 1)) * 1024) = __builtin_bit_cast(uint4, cv);
+    __builtin_amdgcn_sched_barrier(0);
   }
 }
 
@@ -476,6 +514,7 @@ __device__ __forceinline__ void store_tile(u16* act, const uint2 (&pk)[MT][NT][4
 
 struct ChainArgs {
   const float* W0;           // first layer [H][F] fp32
+  const u16* W0f;            // the same as split-term fragments (k_w0_frag)
   const float* b0;           // [H]
   const u16* Wb;             // hidden layers, bf16, forward fragment order with the bias step
   const u16* WTb;            // the same, transposed ([in][out]), backward fragment order
@@ -623,8 +662,7 @@ __global__ __launch_bounds__(Chain<H>::THREADS, Chain<H>::BPC) void k_fwd_chain(
       // the next product is layer l + 1, or the first hidden layer of the next
       // tile; then the product's input A_{l+1} goes to HBM
       chain_gemm<H, true>(weight_rsrc<H, true>(p.Wb, l), weight_rsrc<H, true>(p.Wb, last ? 0 : l + 1), woff, pf,
-                          act, acc, lane);
-      copy_out<H>(act, lane, wave, p.act + ((int64_t)l * rstride + r0) * H, coff);
+                          act, acc, lane, wave, p.act + ((int64_t)l * rstride + r0) * H, coff);
       uint2 pk[MT][NT][4];
       uint32_t m[MW];
       activate<MT, NT>(acc, slope, pk, m);
@@ -718,36 +756,46 @@ __global__ __launch_bounds__(Chain<H>::THREADS, Chain<H>::BPC) void k_fwd_chain(
 // Backward chain of one chunk: the unit-seed signal from the logit layer down
 // through the hidden layers (MFMA, LeakyReLU' from the masks), storing the
 // signals at A_2 .. A_{NH+1} for the weight-gradient products; then the first
-// layer: per-workgroup partials of dW_1 and db_1 (scaled by e_D) and, for fake
-// chunks, dL_G/dx (scaled by e_G, through the HD8 Jacobian when used).  Each
-// tile's seeds, features and events are staged through LDS and its masks
-// loaded into registers, all one step ahead.
+// layer on the matrix cores: dW_1 and db_1 (signal times e_D times the
+// features, accumulated across tiles into per-workgroup partials) and, for
+// fake chunks, dL_G/dx (signal times W_1, scaled by e_G, through the HD8
+// Jacobian when used).  Each tile's seeds, features and events are staged
+// through LDS and its masks loaded into registers, all one step ahead.
 template <int H, int F, int D, bool kHD8>
 __global__ __launch_bounds__(Chain<H>::THREADS, Chain<H>::BPC) void k_bwd_chain(ChainArgs p) {
   using C = Chain<H>;
   constexpr int T = C::T, LDA = C::LDA, WAVES = C::WAVES, MT = C::MT, NT = C::NT, MW = C::MW, NTH = C::THREADS;
-  constexpr int P = NTH / T;         // threads per event in the input-gradient dot
   constexpr int SU = (T * (2 + F + D) + NTH - 1) / NTH;   // staged values per thread
+  constexpr int KB = T / 16;                    // K steps of the dW_1 product (events)
+  constexpr int NB = T / 32;                    // 32-event blocks of the dL/dx product
+  constexpr int WPB = WAVES / NB;               // waves per event block (K split over hidden features)
+  constexpr int KSW = C::KS / WPB;              // dL/dx K steps per wave
+  static_assert(F <= 8 && D <= F && (WPB == 1 || WPB == 2) && (KB * 64) % NTH == 0, "first-layer layout");
   __shared__ __attribute__((aligned(16))) u16 act[T * LDA];
-  __shared__ float sW0[H * F];
   __shared__ float srow[T * (2 + F + D)];       // per event: e_D, e_G | features | x
   __shared__ __attribute__((aligned(16))) float swo[H];
+  __shared__ __attribute__((aligned(16))) u16 sfp[KB * 64 * 8];   // dW_1 A operand of the tile
+  __shared__ float sgx[WPB == 2 ? T * 8 : 1];   // dL/dx partials of the second K half
   float* se = srow;                             // [T][2]
   float* sfeat = srow + 2 * T;                  // [T][F]
   float* sx = sfeat + T * F;                    // [T][D]
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int lh = lane >> 5;
+  const int lr = lane & 31, lh = lane >> 5;
   const int ow = 32 * MT * wave;
   const uint32_t woff = weight_offset<H, false>(wave, lane);
   const uint32_t coff = ((uint32_t)(2 * wave * 64 + lane)) * 16;
+  const u16* cbase = act + copy_lds_base<LDA>(lane, wave);
   const ChunkArgs c = p.c;
   const int64_t rstride = (int64_t)c.rows;
   const int ntiles = c.rows / T;
-  for (int k = tid; k < H * F; k += NTH) sW0[k] = p.W0[k];
   for (int k = tid; k < H; k += NTH) swo[k] = p.wo[k];
-  float adw[F + 1];                       // dW_1 row tid, then db_1[tid]
+  // dW_1 partial of features ow + 32 nb + lr, inputs 4 lh + 0..3, then db_1
+  // (lane half 0)
+  float adw[MT][5];
 #pragma unroll
-  for (int k = 0; k <= F; ++k) adw[k] = 0.f;
+  for (int nb = 0; nb < MT; ++nb)
+#pragma unroll
+    for (int k = 0; k < 5; ++k) adw[nb][k] = 0.f;
   const bool want_dx = c.fake && p.dLg_dx != nullptr;
   const float slope = p.slope;
   const int NH = p.NH;
@@ -805,7 +853,35 @@ __global__ __launch_bounds__(Chain<H>::THREADS, Chain<H>::BPC) void k_bwd_chain(
         }
       store_tile<MT, NT, LDA>(act, pk, ow, lane);
     }
-    __syncthreads();
+    __syncthreads();                             // the staged rows too
+    // ---- dW_1 A operand: the split terms of e_D times each input ------------
+    // piece (kb, l) holds row R = l % 32 for events 16 kb + 8 (l / 32) .. + 7
+    // (the row arrangement is described at k_w0_frag; rows 24..26 are the
+    // terms of e_D itself, for db_1).  Read after the hidden layers' barriers.
+#pragma unroll
+    for (int q = 0; q < KB * 64 / NTH; ++q) {
+      const int slot = tid + NTH * q, l = slot & 63, R = l & 31, term = R >> 3, j = R & 7;
+      const int ev0 = 16 * (slot >> 6) + 8 * (l >> 5);
+      // row R multiplies e_D by input j (term < 3, j < F), by one (the db_1
+      // rows, j < 3) or by zero, and takes term min(term, j) of the product
+      const bool is_in = term < 3 && j < F, is_db = term == 3 && j < 3;
+      const int jj = is_in ? j : 0, ts = term < 3 ? term : (j < 3 ? j : 0);
+      const uint32_t keep = is_in ? 0xffffffffu : 0u;
+      const float* frow = sfeat + ev0 * F + jj;
+      uint32_t w[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        uint32_t h2[2];
+#pragma unroll
+        for (int e = 0; e < 2; ++e) {
+          const int i = 2 * u + e;
+          const float fv = __uint_as_float(__float_as_uint(frow[i * F]) & keep);   // input j, or +0
+          h2[e] = bf16_term(se[2 * (ev0 + i)] * (is_db ? 1.0f : fv), ts);
+        }
+        w[u] = h2[0] | (h2[1] << 16);
+      }
+      *reinterpret_cast<uint4*>(sfp + slot * 8) = make_uint4(w[0], w[1], w[2], w[3]);
+    }
     // ---- hidden layers, top down ---------------------------------------------
     for (int l = NH - 1; l >= 0; --l) {
       uint32_t m[MW];
@@ -813,10 +889,9 @@ __global__ __launch_bounds__(Chain<H>::THREADS, Chain<H>::BPC) void k_bwd_chain(
       if (l == 0 && next < ntiles) load_mask(mask_at(NH, next), mtop);
       f32x16 acc[MT][NT];
       // the next product is layer l - 1, or the top layer of the next tile;
-      // then the product's input (the signal at A_{l+2}) goes to HBM
+      // the product's input (the signal at A_{l+2}) goes to HBM meanwhile
       chain_gemm<H, false>(weight_rsrc<H, false>(p.WTb, l), weight_rsrc<H, false>(p.WTb, l > 0 ? l - 1 : NH - 1), woff,
-                           pf, act, acc, lane);
-      copy_out<H>(act, lane, wave, p.dlt + ((int64_t)l * rstride + r0) * H, coff);
+                           pf, act, acc, lane, wave, p.dlt + ((int64_t)l * rstride + r0) * H, coff);
       uint2 pk[MT][NT][4];
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt)
@@ -835,57 +910,85 @@ __global__ __launch_bounds__(Chain<H>::THREADS, Chain<H>::BPC) void k_bwd_chain(
       __syncthreads();
     }
     // ---- first layer: act holds the signal at A_1 ---------------------------
-#pragma unroll 4
-    for (int ev = 0; ev < T; ++ev) {
-      const float ed = se[2 * ev] * bf16_to_f32(act[ev * LDA + tid]);
+    // dW_1 / db_1: rows R of sfp against the wave's own feature columns of the
+    // signal (K = the tile's events), the terms added within the lane
+    {
+      f32x16 cw[MT];
 #pragma unroll
-      for (int j = 0; j < F; ++j) adw[j] = fmaf(ed, sfeat[ev * F + j], adw[j]);
-      adw[F] += ed;
-    }
-    if (want_dx) {
-      const int ev = tid / P, pp = tid % P;
-      constexpr int OP = H / P;                      // features per thread (a multiple of 8)
-      float g[F];
+      for (int kb = 0; kb < KB; ++kb) {
+        const bf16x8 af = *reinterpret_cast<const bf16x8*>(sfp + (kb * 64 + lane) * 8);
 #pragma unroll
-      for (int j = 0; j < F; ++j) g[j] = 0.f;
-      const u16* drow = act + ev * LDA + pp * OP;
-#pragma unroll 2
-      for (int k = 0; k < OP; k += 8) {
-        float dv[8];
-        load_bf16<8>(drow + k, dv);
-#pragma unroll
-        for (int u = 0; u < 8; ++u) {
-          const int o = pp * OP + k + u;
-#pragma unroll
-          for (int j = 0; j < F; ++j) g[j] = fmaf(dv[u], sW0[o * F + j], g[j]);
+        for (int nb = 0; nb < MT; ++nb) {
+          const bf16x8 bf = copy_read<LDA>(cbase + 16 * kb * LDA + 32 * nb);
+          cw[nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af, bf, kb == 0 ? f32x16{} : cw[nb], 0, 0, 0);
         }
       }
 #pragma unroll
-      for (int s = 1; s < P; s <<= 1)
+      for (int nb = 0; nb < MT; ++nb) {
 #pragma unroll
-        for (int j = 0; j < F; ++j) g[j] += __shfl_xor(g[j], s, 64);
-      const int r = r0 + ev;
-      if (pp == 0 && r < c.valid) {
-        const float eg = se[2 * ev + 1];
+        for (int q = 0; q < 4; ++q) adw[nb][q] += (cw[nb][q] + cw[nb][4 + q]) + cw[nb][8 + q];
+        adw[nb][4] += (cw[nb][12] + cw[nb][13]) + cw[nb][14];
+      }
+    }
+    if (want_dx) {
+      // g[event][j] = sum_o signal[event][o] W_1[o][j]: rows R of W0f against
+      // the signal rows of event block nb (K = hidden features, split over
+      // WPB waves); lane (lh, lr) gets inputs 4 lh + 0..3 of event 32 nb + lr
+      const int nb = wave % NB, kh = wave / NB;
+      const u16* grow = act + (32 * nb + lr) * LDA + 8 * lh;
+      const Rsrc w0r = make_rsrc(p.W0f, (uint32_t)C::KS * 1024);
+      bf16x8 af[KSW];
 #pragma unroll
-        for (int j = 0; j < F; ++j) g[j] *= eg;
-        float dx[D];
-        if constexpr (kHD8) {
-          // d features / d x of [x1, x2, x3, x1x2, x2x3, x1x3, ln x1, ln(1 - x3)];
-          // 1/x1 and 1/(1 - x3) from the log features, accurate where fp32 x3 is within ulps of 1
-          const float* xe = sx + ev * D;
-          const float* fe = sfeat + ev * F;
-          const float x1 = xe[0], x2 = xe[1], x3 = xe[2];
-          const float inv_x1 = expf(-fe[6]), inv_1mx3 = expf(-fe[7]);
-          dx[0] = g[0] + g[3] * x2 + g[5] * x3 + g[6] * inv_x1;
-          dx[1] = g[1] + g[3] * x1 + g[4] * x3;
-          dx[2] = g[2] + g[4] * x2 + g[5] * x1 - g[7] * inv_1mx3;
-        } else {
+      for (int s = 0; s < KSW; ++s) af[s] = load_frag(w0r, (uint32_t)lane * 16, (uint32_t)(kh * KSW + s) * 1024);
+      f32x16 cg = {};
 #pragma unroll
-          for (int j = 0; j < D; ++j) dx[j] = g[j];
+      for (int s = 0; s < KSW; ++s)
+        cg = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[s], *reinterpret_cast<const bf16x8*>(grow + 16 * (kh * KSW + s)),
+                                                     cg, 0, 0, 0);
+      float g4[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) g4[q] = (cg[q] + cg[4 + q]) + cg[8 + q];
+      const int ev = 32 * nb + lr;
+      if constexpr (WPB == 2) {
+        if (kh == 1) {
+#pragma unroll
+          for (int q = 0; q < 4; ++q) sgx[ev * 8 + 4 * lh + q] = g4[q];
         }
+        __syncthreads();
+        if (kh == 0) {
 #pragma unroll
-        for (int j = 0; j < D; ++j) p.dLg_dx[(c.row0 + r) * D + j] = dx[j];
+          for (int q = 0; q < 4; ++q) g4[q] += sgx[ev * 8 + 4 * lh + q];
+        }
+      }
+      if (kh == 0) {
+        // inputs 4..7 from the other lane half
+        float o4[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) o4[q] = __shfl_xor(g4[q], 32, 64);
+        const int r = r0 + ev;
+        if (lh == 0 && r < c.valid) {
+          const float eg = se[2 * ev + 1];
+          float g[F];
+#pragma unroll
+          for (int j = 0; j < F; ++j) g[j] = (j < 4 ? g4[j & 3] : o4[j & 3]) * eg;
+          float dx[D];
+          if constexpr (kHD8) {
+            // d features / d x of [x1, x2, x3, x1x2, x2x3, x1x3, ln x1, ln(1 - x3)];
+            // 1/x1 and 1/(1 - x3) from the log features, accurate where fp32 x3 is within ulps of 1
+            const float* xe = sx + ev * D;
+            const float* fe = sfeat + ev * F;
+            const float x1 = xe[0], x2 = xe[1], x3 = xe[2];
+            const float inv_x1 = expf(-fe[6]), inv_1mx3 = expf(-fe[7]);
+            dx[0] = g[0] + g[3] * x2 + g[5] * x3 + g[6] * inv_x1;
+            dx[1] = g[1] + g[3] * x1 + g[4] * x3;
+            dx[2] = g[2] + g[4] * x2 + g[5] * x1 - g[7] * inv_1mx3;
+          } else {
+#pragma unroll
+            for (int j = 0; j < D; ++j) dx[j] = g[j];
+          }
+#pragma unroll
+          for (int j = 0; j < D; ++j) p.dLg_dx[(c.row0 + r) * D + j] = dx[j];
+        }
       }
     }
     __syncthreads();                                 // before the next tile overwrites act and the staged rows
@@ -894,8 +997,13 @@ __global__ __launch_bounds__(Chain<H>::THREADS, Chain<H>::BPC) void k_bwd_chain(
   // ---- per-workgroup partials of dW_1 and db_1 ------------------------------
   float* dst = p.pfb + (int64_t)blockIdx.x * (H * F + H);
 #pragma unroll
-  for (int j = 0; j < F; ++j) dst[tid * F + j] = adw[j];
-  dst[H * F + tid] = adw[F];
+  for (int nb = 0; nb < MT; ++nb) {
+    const int o = ow + 32 * nb + lr;
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+      if (4 * lh + q < F) dst[o * F + 4 * lh + q] = adw[nb][q];
+    if (lh == 0) dst[H * F + o] = adw[nb][4];
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -1263,7 +1371,7 @@ struct Plan {
   int rows_max;          // padded rows of the largest chunk
   int blocks;            // workgroups of the chain kernels
   int slices;            // weight-gradient slices per chunk
-  size_t off_wb, off_wtb, off_feat, off_xs, off_act, off_dlt, off_mask, off_eD, off_eG, off_plog, off_pfb, off_pw,
+  size_t off_wb, off_wtb, off_w0f, off_feat, off_xs, off_act, off_dlt, off_mask, off_eD, off_eG, off_plog, off_pfb, off_pw,
       off_pwdb, off_accl, total;
 };
 
@@ -1286,6 +1394,7 @@ Plan make_plan(const DiscArgs& a, int n_cu) {
   size_t o = 0;
   p.off_wb = o; o += al(2 * H * (H + 16) * NH);     // forward copies carry one bias step per 32 rows
   p.off_wtb = o; o += al(2 * H * H * NH);
+  p.off_w0f = o; o += al(64 * H);                 // H / 16 pieces of 1 KB
   p.off_feat = o; o += al(4 * R * p.F);
   p.off_xs = o; o += al(4 * R * p.D);
   p.off_act = o; o += al(2 * R * H * NH);
@@ -1359,6 +1468,7 @@ hipError_t launch_disc_bf16(const DiscArgs& a, void* ws, int n_cu, hipStream_t s
   for (int l = 0; l < NH; ++l)
     hipLaunchKernelGGL(k_weights_frag, dim3(((H / 32) * (H / 16 + 1) * 64 + 255) / 256), dim3(256), 0, st, Dm.W[1 + l],
                        Dm.b[1 + l], Wb + (size_t)l * H * (H + 16), WTb + (size_t)l * H * H, H);
+  hipLaunchKernelGGL(k_w0_frag, dim3((H / 16) * 64 / 256), dim3(256), 0, st, Dm.W[0], p.F, H, B16(p.off_w0f));
   if (tm) tm->end();
 
   SourceArgs src{};
@@ -1367,6 +1477,7 @@ hipError_t launch_disc_bf16(const DiscArgs& a, void* ws, int n_cu, hipStream_t s
 
   ChainArgs ca{};
   ca.W0 = Dm.W[0];
+  ca.W0f = B16(p.off_w0f);
   ca.b0 = Dm.b[0];
   ca.Wb = Wb;
   ca.WTb = WTb;
