@@ -121,6 +121,12 @@ __global__ __launch_bounds__(256) void k_weights_frag(const float* __restrict__ 
   *reinterpret_cast<uint4*>(Wf + (size_t)t * 8) = make_uint4(wp[0], wp[1], wp[2], wp[3]);
 }
 
+// a b rounded once to fp32: never fused with a later subtraction.
+__device__ __forceinline__ float mul_rounded(float a, float b) {
+#pragma clang fp contract(off)
+  return a * b;
+}
+
 // Term t (0 = hi, 1 = mid, 2 = lo) of the exact three-term bf16 split above.
 __device__ __forceinline__ u16 bf16_term(float x, int t) {
   uint32_t lo;
@@ -130,7 +136,9 @@ __device__ __forceinline__ u16 bf16_term(float x, int t) {
 
 // The first-layer products of the backward chain (dW_1, db_1 and dL/dx, with
 // K <= 8 first-layer inputs) run on the bf16 matrix cores with the fp32
-// operand split into its three bf16 terms, so every product is exact in fp32.
+// operand (W_1, or e_D times an input) split into its three bf16 terms: the
+// terms sum to the operand exactly and every product of the bf16 signal with
+// a term is exact in fp32, so only the fp32 accumulation rounds.
 // Their 32-row operand puts term t of input j (j = 4 h + p < 8) in row
 // R = 8 t + 4 h + p: in the accumulator fragment of a lane in half h, register
 // 4 t + p then holds term t of input 4 h + p, and the three terms add up
@@ -876,7 +884,9 @@ __global__ __launch_bounds__(Chain<H>::THREADS, Chain<H>::BPC) void k_bwd_chain(
         for (int e = 0; e < 2; ++e) {
           const int i = 2 * u + e;
           const float fv = __uint_as_float(__float_as_uint(frow[i * F]) & keep);   // input j, or +0
-          h2[e] = bf16_term(se[2 * (ev0 + i)] * (is_db ? 1.0f : fv), ts);
+          // the product rounded once (not fused into the split), so the
+          // three terms sum to it exactly
+          h2[e] = bf16_term(mul_rounded(se[2 * (ev0 + i)], is_db ? 1.0f : fv), ts);
         }
         w[u] = h2[0] | (h2[1] << 16);
       }
@@ -1037,7 +1047,7 @@ __global__ __launch_bounds__(kWThreads, 1) void k_wgrad(const u16* __restrict__ 
   constexpr int TI = H / kWT;     // tiles per dimension
   constexpr int CB = H / 32;      // 32-column blocks
   constexpr int kWM = WgradCfg<H>::WM, kWN = WgradCfg<H>::WN, PD = WgradCfg<H>::PD;
-  static_assert(64 * kWM * kWN == kWThreads, "weight-gradient waves");
+  static_assert(64 * kWM * kWN == kWThreads && (PD + 1) % 2 == 0, "weight-gradient waves, ring of scaled steps");
   constexpr int FM = kWT / 32 / kWM, FN = kWT / 32 / kWN;   // 32-row / 32-column fragments per wave
   // Workgroups are dealt to the 8 XCDs round-robin by index; with xcd_map the
   // TI x TI tiles of a row slice share an XCD (and its L2), so the operand rows
@@ -1082,33 +1092,56 @@ __global__ __launch_bounds__(kWThreads, 1) void k_wgrad(const u16* __restrict__ 
     fe[slot][0] = *reinterpret_cast<const f32x4*>(pe + (size_t)k * 16);
     fe[slot][1] = *reinterpret_cast<const f32x4*>(pe + (size_t)k * 16 + 4);
   };
+  // the delta fragments of a step scaled by e_D and rounded (the A operand of
+  // its products), and their fp32 sums for db
+  bf16x8 sa[2][FM];
+  auto scale = [&](int slot, int into) __attribute__((always_inline)) {
+#pragma unroll
+    for (int m = 0; m < FM; ++m) {
+      float v[8];
+#pragma unroll
+      for (int t = 0; t < 8; ++t) v[t] = (float)fa[slot][m][t] * fe[slot][t >> 2][t & 3];
+      dbs[m] += ((v[0] + v[1]) + (v[2] + v[3])) + ((v[4] + v[5]) + (v[6] + v[7]));
+      sa[into][m] = __builtin_bit_cast(bf16x8, make_uint4(pack_bf16(v[0], v[1]), pack_bf16(v[2], v[3]),
+                                                          pack_bf16(v[4], v[5]), pack_bf16(v[6], v[7])));
+    }
+  };
 #pragma unroll
   for (int q = 0; q < PD; ++q)
     if (q < nk) load(q, q);
-  for (int k0 = 0; k0 < nk; k0 += PD + 1) {
+  if (nk > 0) scale(0, 0);
+  // step k (q = k mod (PD + 1)): prefetch step k + PD, then the products of
+  // step k (scaled one step earlier) with the scaling of step k + 1
+  // interleaved between them (one wave per SIMD: the vector ALU work would
+  // otherwise wait for the products' issue)
+  auto step = [&](int q, int k, bool do_load, bool do_scale) __attribute__((always_inline)) {
+    if (do_load) load((q + PD) % (PD + 1), k + PD);
+    __builtin_amdgcn_sched_barrier(0);
+    if (do_scale) scale((q + 1) % (PD + 1), (q + 1) & 1);
+#pragma unroll
+    for (int n = 0; n < FN; ++n)
+#pragma unroll
+      for (int m = 0; m < FM; ++m)
+        acc[m][n] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(sa[q & 1][m], fb[q][n], acc[m][n], 0, 0, 0);
+#pragma unroll
+    for (int i = 0; i < FM * FN; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // one product
+      __builtin_amdgcn_sched_group_barrier(0x002, 8, 0);   // eight vector ALU instructions
+    }
+    __builtin_amdgcn_sched_barrier(0);
+  };
+  // steady state without branches (every step prefetches and scales ahead),
+  // then the last steps with the bounds checked
+  int k0 = 0;
+  for (; k0 + 2 * PD < nk; k0 += PD + 1) {
+#pragma unroll
+    for (int q = 0; q <= PD; ++q) step(q, k0 + q, true, true);
+  }
+  for (; k0 < nk; k0 += PD + 1) {
 #pragma unroll
     for (int q = 0; q <= PD; ++q) {
       const int k = k0 + q;
-      if (k < nk) {
-        if (k + PD < nk) load((q + PD) % (PD + 1), k + PD);
-        __builtin_amdgcn_sched_barrier(0);
-        bf16x8 sa[FM];
-#pragma unroll
-        for (int m = 0; m < FM; ++m) {
-          float v[8];
-#pragma unroll
-          for (int t = 0; t < 8; ++t) v[t] = (float)fa[q][m][t] * fe[q][t >> 2][t & 3];
-          dbs[m] += ((v[0] + v[1]) + (v[2] + v[3])) + ((v[4] + v[5]) + (v[6] + v[7]));
-          sa[m] = __builtin_bit_cast(bf16x8, make_uint4(pack_bf16(v[0], v[1]), pack_bf16(v[2], v[3]),
-                                                        pack_bf16(v[4], v[5]), pack_bf16(v[6], v[7])));
-        }
-#pragma unroll
-        for (int n = 0; n < FN; ++n)
-#pragma unroll
-          for (int m = 0; m < FM; ++m)
-            acc[m][n] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(sa[m], fb[q][n], acc[m][n], 0, 0, 0);
-        __builtin_amdgcn_sched_barrier(0);
-      }
+      if (k < nk) step(q, k, k + PD < nk, k + 1 < nk);
     }
   }
   float* out = P + (size_t)slice * H * H;
@@ -1230,10 +1263,26 @@ __global__ __launch_bounds__(kWThreads, 1) void k_wgrad_shared(const u16* __rest
 #pragma unroll
     for (int n = 0; n < FN; ++n) fb[into][n] = *reinterpret_cast<const bf16x8*>(&sb[buf][n][lane * 8]);
   };
+  // The delta fragments of one step scaled by e_D and rounded (the A operand
+  // of its products), and their fp32 sums for db.
+  bf16x8 sa[2][FM];
+  auto scale = [&](int slot, int into) __attribute__((always_inline)) {
+#pragma unroll
+    for (int m = 0; m < FM; ++m) {
+      float v[8];
+#pragma unroll
+      for (int t = 0; t < 8; ++t) v[t] = (float)rd[slot][m][t] * re[slot][t >> 2][t & 3];
+      dbs[m] += ((v[0] + v[1]) + (v[2] + v[3])) + ((v[4] + v[5]) + (v[6] + v[7]));
+      sa[into][m] = __builtin_bit_cast(bf16x8, make_uint4(pack_bf16(v[0], v[1]), pack_bf16(v[2], v[3]),
+                                                          pack_bf16(v[4], v[5]), pack_bf16(v[6], v[7])));
+    }
+  };
   // Step k (q = k mod NS, so k mod 2 = q mod 2 and k mod 3 = q mod 3): read
   // the fragments of step k + 1 (published at the end of step k - 1), publish
   // this wave's two of step k + 2, prefetch step k + kWLG, then the products
-  // of step k from the fragments read one step earlier.
+  // of step k from the fragments read and scaled one step earlier, with the
+  // scaling of step k + 1 interleaved between them (one wave per SIMD: the
+  // vector ALU work would otherwise wait for the products' issue).
   auto step = [&](auto qc, int k, bool get_next, bool put_ahead, bool load_ahead) __attribute__((always_inline)) {
     constexpr int q = decltype(qc)::value;
     if (get_next) get((q + 1) % 3, (q + 1) & 1);
@@ -1242,21 +1291,17 @@ __global__ __launch_bounds__(kWThreads, 1) void k_wgrad_shared(const u16* __rest
     // keep each step's work inside the step: the scheduler would otherwise
     // hoist later steps' scaling above their loads' waits
     __builtin_amdgcn_sched_barrier(0);
-    bf16x8 sa[FM];
-#pragma unroll
-    for (int m = 0; m < FM; ++m) {
-      float v[8];
-#pragma unroll
-      for (int t = 0; t < 8; ++t) v[t] = (float)rd[q][m][t] * re[q][t >> 2][t & 3];
-      dbs[m] += ((v[0] + v[1]) + (v[2] + v[3])) + ((v[4] + v[5]) + (v[6] + v[7]));
-      sa[m] = __builtin_bit_cast(bf16x8, make_uint4(pack_bf16(v[0], v[1]), pack_bf16(v[2], v[3]),
-                                                    pack_bf16(v[4], v[5]), pack_bf16(v[6], v[7])));
-    }
+    if (get_next) scale((q + 1) % NS, (q + 1) & 1);
 #pragma unroll
     for (int n = 0; n < FN; ++n)
 #pragma unroll
       for (int m = 0; m < FM; ++m)
-        acc[m][n] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(sa[m], fb[q & 1][n], acc[m][n], 0, 0, 0);
+        acc[m][n] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(sa[q & 1][m], fb[q & 1][n], acc[m][n], 0, 0, 0);
+#pragma unroll
+    for (int i = 0; i < FM * FN; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // one product
+      __builtin_amdgcn_sched_group_barrier(0x002, 4, 0);   // four vector ALU instructions
+    }
     __builtin_amdgcn_sched_barrier(0);
     lds_barrier();
   };
@@ -1269,6 +1314,7 @@ __global__ __launch_bounds__(kWThreads, 1) void k_wgrad_shared(const u16* __rest
     put(1, 1);
     lds_barrier();
     get(0, 0);
+    scale(0, 0);
   }
   // steady state: NS steps per pass, every step reading, publishing and
   // prefetching (no branches, so the waits on the loads stay exact)
