@@ -18,6 +18,7 @@ import argparse
 import hashlib
 import json
 import os
+import re
 import sys
 import time
 
@@ -44,11 +45,21 @@ KERNEL_SOURCES = {
 }
 
 
+def _code_text(src: str) -> str:
+    """The source with its comments removed and whitespace runs collapsed, so
+    that an edit of comments or layout does not mark a profile stale.  (The
+    sources hold no string literal containing comment markers.)"""
+    src = re.sub(r"/\*.*?\*/", " ", src, flags=re.S)
+    src = re.sub(r"//[^\n]*", " ", src)
+    return " ".join(src.split())
+
+
 def source_hash(kernel: str) -> str:
+    """Hash of the code (comments and layout excluded) of the files a kernel is built from."""
     h = hashlib.sha256()
     for p in KERNEL_SOURCES[kernel]:
-        with open(os.path.join(ROOT, p), "rb") as f:
-            h.update(f.read())
+        with open(os.path.join(ROOT, p), encoding="utf-8") as f:
+            h.update(_code_text(f.read()).encode())
     return h.hexdigest()[:16]
 
 

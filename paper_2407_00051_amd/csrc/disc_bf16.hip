@@ -5,13 +5,15 @@
 //
 //   k_prep       features of every row (sampling fake events in place, HD8 map)
 //   k_fwd_chain  per tile of rows, in LDS: A_1 = bf16(LeakyReLU(feat W1^T + b1))
-//                (VALU, K <= 8), then every hidden layer on the bf16 matrix
-//                cores, then the logit z and the BCE seeds e_D, e_G; stores
-//                A_1 .. A_NH and the activation sign masks
+//                (fp32 matrix cores, K <= 8 plus the bias), then every hidden
+//                layer on the bf16 matrix cores, then the logit z and the BCE
+//                seeds e_D, e_G; stores A_1 .. A_NH and the activation sign
+//                masks
 //   k_bwd_chain  per tile, in LDS: the unit-seed signal from the logit layer
 //                down to A_1 (matrix cores, LeakyReLU' from the masks); stores
 //                the signals the weight gradients need; first-layer dW_1, db_1
-//                and dL_G/dx (through the HD8 Jacobian)
+//                and dL_G/dx (through the HD8 Jacobian), also on the matrix
+//                cores with the fp32 operand split into exact bf16 terms
 //   k_wgrad      dW partials = sum_rows bf16(e_D delta) (x) A  (K = rows)
 //
 // Forward and backward products compute outT = W' inT (M = output feature,
