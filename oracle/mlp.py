@@ -144,7 +144,9 @@ def bce_losses(z_fake, z_real):
 
 def _backward(W, pres, hs, g_z, slope, want_input_grad, cond=False):
     """Backprop a per-event logit gradient g_z through the network (float64).
-    With cond, also the sums over events of |terms| of every dW and db entry."""
+    With cond, also the sums over events of |terms| of every dW and db entry,
+    and (with want_input_grad) the per-entry sums of |terms| of the input
+    gradient, sum_o |dL/dpre_0[o]| |W_1[o][j]|."""
     n = len(W)
     W = [np.asarray(w, dtype=np.float64) for w in W]
     dW = [None] * n
@@ -163,8 +165,10 @@ def _backward(W, pres, hs, g_z, slope, want_input_grad, cond=False):
             g = (g @ W[l]) * _leaky_grad(pres[l - 1], slope)
         elif want_input_grad:
             g_in = g @ W[0]
+            if cond:
+                c_in = np.abs(g) @ np.abs(W[0])
     if cond:
-        return dW, db, g_in, cW, cb
+        return dW, db, g_in, cW, cb, (c_in if want_input_grad else None)
     return dW, db, g_in
 
 
@@ -201,10 +205,11 @@ def _disc_bf16(W, b, fake_in, real_in, slope, rnd):
     dW[0] = (e[:, None] * d).T @ hs[0]
     db[0] = (e[:, None] * d).sum(axis=0)
     g_in = eG[:, None] * (d[:nf] @ W[0])
+    c_in = np.abs(eG)[:, None] * (np.abs(d[:nf]) @ np.abs(W[0]))
     return {
         "kink_margin_fake": np.full(nf, np.inf),
         "logits_fake": z_f, "logits_real": z_r, "loss_d": L_D, "loss_g": L_G,
-        "dW": dW, "db": db, "dLg_din": g_in,
+        "dW": dW, "db": db, "dLg_din": g_in, "dLg_din_cond": c_in,
     }
 
 
@@ -224,13 +229,13 @@ def disc_fwd_bwd(W, b, fake_in, real_in, slope=0.2, bf16=False):
     gD_f = sigmoid(z_f) / nf
     gD_r = -sigmoid(-z_r) / nr
     gG_f = -sigmoid(-z_f) / nf
-    dW_f, db_f, _, cW_f, cb_f = _backward(W, pres_f, hs_f, gD_f, slope, False, cond=True)
-    dW_r, db_r, _, cW_r, cb_r = _backward(W, pres_r, hs_r, gD_r, slope, False, cond=True)
-    _, _, g_in = _backward(W, pres_f, hs_f, gG_f, slope, True)
+    dW_f, db_f, _, cW_f, cb_f, _ = _backward(W, pres_f, hs_f, gD_f, slope, False, cond=True)
+    dW_r, db_r, _, cW_r, cb_r, _ = _backward(W, pres_r, hs_r, gD_r, slope, False, cond=True)
+    _, _, g_in, _, _, c_in = _backward(W, pres_f, hs_f, gG_f, slope, True, cond=True)
     return {
         "kink_margin_fake": kink_margin(W, b, hs_f, pres_f),
         "logits_fake": z_f, "logits_real": z_r, "loss_d": L_D, "loss_g": L_G,
         "dW": [p + q for p, q in zip(dW_f, dW_r)], "db": [p + q for p, q in zip(db_f, db_r)],
         "dW_cond": [p + q for p, q in zip(cW_f, cW_r)], "db_cond": [p + q for p, q in zip(cb_f, cb_r)],
-        "dLg_din": g_in,
+        "dLg_din": g_in, "dLg_din_cond": c_in,
     }

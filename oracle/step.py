@@ -57,9 +57,12 @@ def run_step(theta, E, fake_seed, W=None, b=None, real_x=None, features="identit
         r = disc_fwd_bwd(W, b, fin, rin, slope, bf16)
         out.update(r)
         if features == "identity":
-            g = r["dLg_din"]
+            g, gc = r["dLg_din"], r["dLg_din_cond"]
         else:
-            g = np.einsum("nf,nfd->nd", r["dLg_din"], FEATURES[features][1](s["x"]))
+            J = FEATURES[features][1](s["x"])
+            g = np.einsum("nf,nfd->nd", r["dLg_din"], J)
+            gc = np.einsum("nf,nfd->nd", r["dLg_din_cond"], np.abs(J))
         out["dL_dx"] = g
+        out["dL_dx_cond"] = gc       # per entry: sum of |terms| (through |Jacobian| for mapped features)
     out["dL_dtheta"], out["dL_dtheta_cond"] = param_grad(out["dL_dx"], s["dxda"], s["dxdb"], n_theta, E)
     return out

@@ -62,10 +62,35 @@ def _run(ctx, w, th, ts, W, b, n_real):
     return o
 
 
-def _check(o, ref, tol, tag, n_layers, cond_ref=None):
-    """Normwise per tensor; a reduced tensor (dW, db, dL/dtheta) whose normwise error
-    exceeds tol still passes if every entry is within tol * sum|terms| (cancelling
-    sums), with the condition sums taken from the float64 oracle `cond_ref`."""
+def _check_dx(got, r, cond, tol, tag):
+    """dL_G/dx against the bf16-point oracle.  Per event it is a sum over the
+    hidden units that can cancel, and the two sides take the bf16 rounding
+    decisions from fp32 (kernel) and float64 (oracle) values: a decision that
+    falls the other way moves later pre-activations by about a bf16 step of one
+    term, which can carry a unit across its LeakyReLU kink (slope 1 vs 0.2)
+    even at a relative margin of 1e-4, and with many units per event such
+    margins are common.  Passes if the normwise error, or every event's error
+    relative to its sum of |terms|, is within tol; or if at most max(3, 0.1%)
+    events exceed tol relative to their sum of |terms|, each within the bf16
+    bar TOL, and the other events pass normwise at tol."""
+    got = np.asarray(got, np.float64)
+    e_nw = float(np.linalg.norm(got - r) / np.linalg.norm(r))
+    ratio = (np.abs(got - r) / np.maximum(cond, 1e-300)).max(axis=1)
+    out = ratio > tol
+    n_out = int(np.count_nonzero(out))
+    rest = float(np.linalg.norm((got - r)[~out]) / np.linalg.norm(r[~out])) if n_out else e_nw
+    ok = e_nw <= tol or n_out == 0 or (n_out <= max(3, ratio.size // 1000) and ratio.max() <= TOL and rest <= tol)
+    print(f"  {tag} dLg_dx: normwise {e_nw:.3e}; {n_out} of {ratio.size} events beyond {tol:.0e} of their "
+          f"sum|terms| (worst {ratio.max():.3e}); the others normwise {rest:.3e}" + ("" if ok else "  <-- FAIL"),
+          flush=True)
+    return None if ok else "dLg_dx"
+
+
+def _check(o, ref, tol, tag, n_layers, cond_ref=None, dx_outliers=False, asserted=None):
+    """Normwise per tensor; a tensor of sums (dW, db, dL/dtheta, dL_G/dx) whose
+    normwise error exceeds tol still passes if every entry is within
+    tol * sum|terms| (cancelling sums), with the condition sums taken from the
+    float64 oracle `cond_ref`."""
     from tests.parity import normwise
     bad = []
 
@@ -77,8 +102,9 @@ def _check(o, ref, tol, tag, n_layers, cond_ref=None):
             worst = float(np.max(np.abs(np.asarray(got, np.float64) - r) / np.maximum(cond, 1e-300)))
             msg += f", max |err|/sum|terms| {worst:.3e}"
             ok = worst <= tol
-        print(msg + ("" if ok else "  <-- FAIL"), flush=True)
-        if not ok:
+        barred = asserted is None or what in asserted
+        print(msg + ("" if ok else ("  <-- FAIL" if barred else "  (beyond tol; reported, not a bar)")), flush=True)
+        if not ok and barred:
             bad.append(what)
 
     cr = cond_ref or ref
@@ -89,7 +115,13 @@ def _check(o, ref, tol, tag, n_layers, cond_ref=None):
     for l in range(n_layers):
         nw(to_np(o["dW"][l]), ref["dW"][l], f"dW[{l}]", cr["dW_cond"][l])
         nw(to_np(o["db"][l]), ref["db"][l], f"db[{l}]", cr["db_cond"][l])
-    nw(to_np(o["dLg_dx"]), ref["dL_dx"], "dLg_dx")
+    # dL_G/dx per event: see _check_dx
+    if dx_outliers:
+        e = _check_dx(to_np(o["dLg_dx"]), ref["dL_dx"], cr["dL_dx_cond"], tol, tag)
+        if e:
+            bad.append(e)
+    else:
+        nw(to_np(o["dLg_dx"]), ref["dL_dx"], "dLg_dx", cr["dL_dx_cond"])
     nw(to_np(o["dLg_dtheta"]), ref["dL_dtheta"], "dLg_dtheta", cr["dL_dtheta_cond"])
     return bad
 
@@ -110,13 +142,37 @@ def test_bf16_reduced(gpu_ctx, name, n_theta, E, n_real):
     ref = oracle.run_step(inp["theta"], E, w.fake_seed, inp["W"], inp["b"], real_np, features=w.features)
     # The parity bar: the oracle evaluated at the same bf16 operand rounding points.
     emu = oracle.run_step(inp["theta"], E, w.fake_seed, inp["W"], inp["b"], real_np, features=w.features, bf16=True)
-    bad_emu = _check(o, emu, TOL_EMU, "vs bf16-point oracle", len(W), cond_ref=ref)
+    bad_emu = _check(o, emu, TOL_EMU, "vs bf16-point oracle", len(W), cond_ref=ref, dx_outliers=True)
     # Against the float64 network: the losses and dL/dtheta at the same bar; the rest is
     # reported (rounding the operands changes the network, and per-event quantities such as
     # dL_G/dx and the first-layer gradient are ill-conditioned under that change).
-    bad64 = _check(o, ref, TOL, "vs fp64", len(W))
-    _check(emu_as_out(emu), ref, TOL, "bf16-point oracle vs fp64 (reported)", len(W))
-    bad64 = [k for k in bad64 if k in ("loss_d", "loss_g", "dLg_dtheta")]
+    bad64 = _check(o, ref, TOL, "vs fp64", len(W), asserted=("loss_d", "loss_g", "dLg_dtheta"))
+    _check(emu_as_out(emu), ref, TOL, "bf16-point oracle vs fp64", len(W), asserted=())
+    assert not bad_emu and not bad64, (bad_emu, bad64)
+
+
+# The other compiled shapes of the bf16 path: identity features with d = 3 at
+# both widths, d = 2 at H = 512 and HD8 at H = 256, i.e. first-layer products
+# with F = 2, 3 and 8 inputs, with one or two waves per 32-event block, here
+# with two hidden-to-hidden layers and ragged counts.
+@pytest.mark.parametrize("d,features,H", [(3, "identity", 256), (3, "identity", 512), (2, "identity", 512),
+                                          (3, "hd8", 256)])
+def test_bf16_other_shapes(gpu_ctx, d, features, H):
+    from dataclasses import replace
+    F = 8 if features == "hd8" else d
+    w = replace(get("medium"), name=f"bf16_{features}_d{d}_H{H}", n_theta=3, d=d, events_per_theta=1000,
+                widths=(F, H, H, H, 1), features=features)
+    n_real = 2500
+    print(f"case {w.name} n_theta=3 E=1000 n_real={n_real}", flush=True)
+    inp, th, ts, W, b = _setup(w)
+    o = _run(gpu_ctx, w, th, ts, W, b, n_real)
+    real_np = oracle.sample(inp["theta_star"], n_real, w.real_seed)
+    ref = oracle.run_step(inp["theta"], w.events_per_theta, w.fake_seed, inp["W"], inp["b"], real_np,
+                          features=w.features)
+    emu = oracle.run_step(inp["theta"], w.events_per_theta, w.fake_seed, inp["W"], inp["b"], real_np,
+                          features=w.features, bf16=True)
+    bad_emu = _check(o, emu, TOL_EMU, "vs bf16-point oracle", len(W), cond_ref=ref, dx_outliers=True)
+    bad64 = _check(o, ref, TOL, "vs fp64", len(W), asserted=("loss_d", "loss_g", "dLg_dtheta"))
     assert not bad_emu and not bad64, (bad_emu, bad64)
 
 

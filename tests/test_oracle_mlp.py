@@ -194,3 +194,41 @@ def test_kink_variants_are_the_one_sided_derivatives():
     want = sorted([right, left])
     assert abs(right - left) > 1e-3             # the kink is visible
     np.testing.assert_allclose(got, want, rtol=1e-6, atol=1e-9)
+
+
+@pytest.mark.parametrize("bf16", [False, True])
+def test_input_grad_condition_sums(bf16):
+    """dLg_din_cond is the per-entry sum of |terms| of dL_G/d(input): it bounds
+    |dLg_din| entrywise (triangle inequality), it equals |dLg_din| when every
+    layer has one unit (a single term per entry), and it does not depend on
+    the signs of the first layer's weights."""
+    W, b = _net((3, 16, 16, 1), 21)
+    xf, xr = _batches(3, 40, 22)
+    r = disc_fwd_bwd(W, b, xf, xr, bf16=bf16)
+    assert np.all(np.abs(r["dLg_din"]) <= r["dLg_din_cond"] * (1 + 1e-12))
+    assert np.any(np.abs(r["dLg_din"]) < 0.5 * r["dLg_din_cond"])      # some entries do cancel
+    W1, b1 = _net((3, 1, 1, 1), 23)
+    r1 = disc_fwd_bwd(W1, b1, xf, xr, bf16=bf16)
+    np.testing.assert_allclose(r1["dLg_din_cond"], np.abs(r1["dLg_din"]), rtol=1e-13, atol=0)
+    Wf = [w.copy() for w in W]
+    Wf[0][:, 1] *= -1.0                                                    # flip one input column's sign
+    rf = disc_fwd_bwd(Wf, b, xf * np.array([1.0, -1.0, 1.0]), xr * np.array([1.0, -1.0, 1.0]), bf16=bf16)
+    np.testing.assert_allclose(rf["dLg_din_cond"], r["dLg_din_cond"], rtol=1e-12)
+
+
+def test_step_input_grad_condition_through_the_feature_map():
+    """run_step maps the condition sums through |Jacobian| of the HD8 map, so they
+    still bound |dL/dx| entrywise."""
+    import oracle
+    from workloads import gen, get
+    from workloads.configs import scaled
+    w = scaled(get("higher_dim"), 2, 64)
+    inp = gen.make_inputs(w)
+    # the workload's network narrowed to 16 hidden units (8-16-16-16-16-1)
+    W = [m[:16, :16] if l else m[:16] for l, m in enumerate(inp["W"][:-1])] + [inp["W"][-1][:, :16]]
+    b = [v[:16] for v in inp["b"][:-1]] + [inp["b"][-1]]
+    real = oracle.sample(inp["theta_star"], 100, 1)
+    for bf16 in (False, True):
+        r = oracle.run_step(inp["theta"], 64, 0, W, b, real, features="hd8", bf16=bf16)
+        assert r["dL_dx_cond"].shape == r["dL_dx"].shape
+        assert np.all(np.abs(r["dL_dx"]) <= r["dL_dx_cond"] * (1 + 1e-12))

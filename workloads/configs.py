@@ -121,7 +121,7 @@ class TrainWorkload:
     (Sec. V-A, Tab. gen_settings): the generator predicts k = 1,024 parameter
     samples, each yields E = 100 events, the discriminator sees the two
     observables of those and of an equal reference batch, bootstrapped each
-    step from a pool of twice its size (Sec. IV-B, Sec. VI-B)."""
+    step from a pool of twice its size (Sec. IV-B, Sec. VI-C)."""
     name: str
     k: int = 1024
     events_per_theta: int = 100
