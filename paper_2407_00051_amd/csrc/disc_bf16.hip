@@ -872,8 +872,9 @@ __global__ __launch_bounds__(Chain<H>::THREADS, Chain<H>::BPC) void k_bwd_chain(
     for (int q = 0; q < KB * 64 / NTH; ++q) {
       const int slot = tid + NTH * q, l = slot & 63, R = l & 31, term = R >> 3, j = R & 7;
       const int ev0 = 16 * (slot >> 6) + 8 * (l >> 5);
-      // row R multiplies e_D by input j (term < 3, j < F), by one (the db_1
-      // rows, j < 3) or by zero, and takes term min(term, j) of the product
+      // row R = 8 term + j holds term `term` of e_D times input j (term < 3,
+      // j < F); the db_1 rows 24 + p (p < 3) hold term p of e_D itself; the
+      // other rows are zero
       const bool is_in = term < 3 && j < F, is_db = term == 3 && j < 3;
       const int jj = is_in ? j : 0, ts = term < 3 ? term : (j < 3 ? j : 0);
       const uint32_t keep = is_in ? 0xffffffffu : 0u;
