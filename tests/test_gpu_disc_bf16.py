@@ -62,6 +62,26 @@ def _run(ctx, w, th, ts, W, b, n_real):
     return o
 
 
+def _fp64_bar(o, emu, ref, n_layers):
+    """The losses and dL_G/dtheta against the float64 network at TOL, unless the
+    bf16-point oracle is itself beyond TOL there: rounding the operands to bf16
+    changes the function, and the kernel is held to that oracle at TOL_EMU."""
+    from tests.parity import normwise
+    bad = _check(o, ref, TOL, "vs fp64", n_layers, asserted=("loss_d", "loss_g", "dLg_dtheta"))
+
+    def beyond(got, r, cond=None):
+        if normwise(got, r) <= TOL:
+            return False
+        return cond is None or float(np.max(np.abs(got - r) / np.maximum(cond, 1e-300))) > TOL
+
+    emu_beyond = {"loss_d": beyond(emu["loss_d"], ref["loss_d"]), "loss_g": beyond(emu["loss_g"], ref["loss_g"]),
+                  "dLg_dtheta": beyond(emu["dL_dtheta"], ref["dL_dtheta"], ref["dL_dtheta_cond"])}
+    for k in bad:
+        if emu_beyond[k]:
+            print(f"  {k}: the bf16-point oracle itself is beyond {TOL:.0e} of float64 (reported)", flush=True)
+    return [k for k in bad if not emu_beyond[k]]
+
+
 def _check_dx(got, r, cond, tol, tag):
     """dL_G/dx against the bf16-point oracle.  Per event it is a sum over the
     hidden units that can cancel, and the two sides take the bf16 rounding
@@ -146,22 +166,22 @@ def test_bf16_reduced(gpu_ctx, name, n_theta, E, n_real):
     # Against the float64 network: the losses and dL/dtheta at the same bar; the rest is
     # reported (rounding the operands changes the network, and per-event quantities such as
     # dL_G/dx and the first-layer gradient are ill-conditioned under that change).
-    bad64 = _check(o, ref, TOL, "vs fp64", len(W), asserted=("loss_d", "loss_g", "dLg_dtheta"))
-    _check(emu_as_out(emu), ref, TOL, "bf16-point oracle vs fp64", len(W), asserted=())
+    bad64 = _fp64_bar(o, emu, ref, len(W))
     assert not bad_emu and not bad64, (bad_emu, bad64)
 
 
 # The other compiled shapes of the bf16 path: identity features with d = 3 at
 # both widths, d = 2 at H = 512 and HD8 at H = 256, i.e. first-layer products
-# with F = 2, 3 and 8 inputs, with one or two waves per 32-event block, here
-# with two hidden-to-hidden layers and ragged counts.
-@pytest.mark.parametrize("d,features,H", [(3, "identity", 256), (3, "identity", 512), (2, "identity", 512),
-                                          (3, "hd8", 256)])
-def test_bf16_other_shapes(gpu_ctx, d, features, H):
+# with F = 2, 3 and 8 inputs, with one or two waves per 32-event block; one to
+# four hidden-to-hidden layers (NH); ragged counts.
+@pytest.mark.parametrize("d,features,H,NH", [(3, "identity", 256, 2), (3, "identity", 512, 2),
+                                             (2, "identity", 512, 2), (3, "hd8", 256, 2),
+                                             (2, "identity", 256, 1), (3, "hd8", 512, 4)])
+def test_bf16_other_shapes(gpu_ctx, d, features, H, NH):
     from dataclasses import replace
     F = 8 if features == "hd8" else d
-    w = replace(get("medium"), name=f"bf16_{features}_d{d}_H{H}", n_theta=3, d=d, events_per_theta=1000,
-                widths=(F, H, H, H, 1), features=features)
+    w = replace(get("medium"), name=f"bf16_{features}_d{d}_H{H}_NH{NH}", n_theta=3, d=d, events_per_theta=1000,
+                widths=(F,) + (H,) * (NH + 1) + (1,), features=features)
     n_real = 2500
     print(f"case {w.name} n_theta=3 E=1000 n_real={n_real}", flush=True)
     inp, th, ts, W, b = _setup(w)
@@ -172,7 +192,7 @@ def test_bf16_other_shapes(gpu_ctx, d, features, H):
     emu = oracle.run_step(inp["theta"], w.events_per_theta, w.fake_seed, inp["W"], inp["b"], real_np,
                           features=w.features, bf16=True)
     bad_emu = _check(o, emu, TOL_EMU, "vs bf16-point oracle", len(W), cond_ref=ref, dx_outliers=True)
-    bad64 = _check(o, ref, TOL, "vs fp64", len(W), asserted=("loss_d", "loss_g", "dLg_dtheta"))
+    bad64 = _fp64_bar(o, emu, ref, len(W))
     assert not bad_emu and not bad64, (bad_emu, bad64)
 
 
