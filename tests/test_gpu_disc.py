@@ -104,6 +104,25 @@ def test_fused_source_path(gpu_ctx, name, n_theta, E):
     _check(o, ref, len(W), W=inp["W"], b=inp["b"], n_theta=w.n_theta, E=w.events_per_theta)
 
 
+# The other compiled fp32 networks: width 64 with one to three hidden-to-hidden
+# layers, width 128 with one, and d = 3 identity features at both widths; E =
+# 1,000 (tiles straddling parameter rows, a partial last tile) and a ragged
+# real batch.
+@pytest.mark.parametrize("H,NH,d", [(64, 2, 2), (64, 3, 2), (128, 1, 2), (64, 1, 3), (64, 2, 3), (128, 2, 3)])
+def test_other_fp32_networks(gpu_ctx, H, NH, d):
+    from dataclasses import replace
+    w = replace(get("small"), name=f"fp32_H{H}_NH{NH}_d{d}", n_theta=3, d=d, events_per_theta=1000,
+                widths=(d,) + (H,) * (NH + 1) + (1,), theta_source="uniform")
+    print(f"case {w.name} n_theta=3 E=1000 n_real=2500", flush=True)
+    inp, th, ts, W, b, _ = _setup(w)
+    real = gpu_ctx.sample_events(ts, 2500, w.real_seed)
+    o = gpu_ctx.disc_fwd_bwd(W, b, real, fake_source=dict(theta=th, events_per_theta=1000, seed=w.fake_seed))
+    torch.cuda.synchronize()
+    real_np = oracle.sample(inp["theta_star"], 2500, w.real_seed)
+    ref = _oracle(inp, w, real_np)
+    _check(o, ref, len(W), W=inp["W"], b=inp["b"], n_theta=w.n_theta, E=w.events_per_theta)
+
+
 def test_three_call_path_matches_fused(gpu_ctx):
     """sample_events -> disc_fwd_bwd(fake_x) -> param_grad(BUFFER) equals the fused call."""
     w = scaled(get("small"), 4, 4096)
