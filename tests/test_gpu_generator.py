@@ -71,6 +71,30 @@ def test_gen_backward_matches_oracle(gpu_ctx, M, k):
             assert_normwise(to_np(db[l])[m], rb[l], TOL, f"db[{l}] member {m}")
 
 
+# The other compiled generator depths (one and two hidden-to-hidden layers) and
+# other input/output widths (up to 8), forward and backward.
+@pytest.mark.parametrize("widths,M,k", [((4, 128, 128, 2), 3, 300), ((8, 128, 128, 128, 8), 2, 1000),
+                                        ((1, 128, 128, 128, 5), 1, 77)])
+def test_gen_other_shapes(gpu_ctx, widths, M, k):
+    print(f"case gen widths={widths} M={M} k={k}", flush=True)
+    W, b = gen.generator_stack(widths, M, seed=len(widths) + k)
+    n = gen.noise(k, widths[0], seed=k + 2)
+    nd = torch.tensor(n, device="cuda:0")
+    th = to_np(gpu_ctx.gen_forward(_dev(W), _dev(b), nd))
+    g = np.random.default_rng(k).standard_normal((M, k, widths[-1])).astype(np.float32)
+    for m in range(M):
+        g[m, _kink_rows(*_member(W, b, m), n)] = 0.0
+    dW, db = gpu_ctx.gen_backward(_dev(W), _dev(b), nd, torch.tensor(g, device="cuda:0"))
+    torch.cuda.synchronize()
+    for m in range(M):
+        ref = oracle.generator_forward(*_member(W, b, m), n)
+        assert np.abs(th[m] - ref).max() / np.abs(ref).max() <= TOL, m
+        rW, rb = oracle.generator_backward(*_member(W, b, m), n, g[m].astype(np.float64))
+        for l in range(len(W)):
+            assert_normwise(to_np(dW[l])[m], rW[l], TOL, f"dW[{l}] member {m}")
+            assert_normwise(to_np(db[l])[m], rb[l], TOL, f"db[{l}] member {m}")
+
+
 def test_gen_backward_zero_signal(gpu_ctx):
     W, b = gen.generator_stack(WIDTHS, 1, seed=3)
     n = torch.tensor(gen.noise(200, 6, seed=4), device="cuda:0")
