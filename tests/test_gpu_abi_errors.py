@@ -83,3 +83,44 @@ def test_create_rejects_bad_device():
     assert lib.sagips_create(ctypes.byref(h), 999, None) == sg.E_INVAL
     assert h.value is None
     assert b"device" in lib.sagips_last_error(None)
+
+
+def test_adam_errors(gpu_ctx):
+    """Every invalid optimiser request is rejected before launch and leaves the tensors untouched."""
+    lib, h = gpu_ctx.lib, gpu_ctx.h
+    p = torch.ones(100, device="cuda:0")
+    g = torch.ones(100, device="cuda:0")
+    m = torch.zeros(100, device="cuda:0")
+    v = torch.zeros(100, device="cuda:0")
+
+    def pset(n=1, size=100, null=None):
+        ps = sg.ParamSet()
+        ps.n_tensors = n
+        for i in range(min(max(n, 0), sg.MAX_TENSORS)):
+            ps.param[i], ps.grad[i], ps.m[i], ps.v[i] = p.data_ptr(), g.data_ptr(), m.data_ptr(), v.data_ptr()
+            ps.size[i] = size
+        if null:
+            setattr(ps, null, (ctypes.c_void_p * sg.MAX_TENSORS)())
+        return ps
+
+    args = (1, 1e-3, 0.9, 0.999, 1e-8)
+    cases = [
+        (pset(n=0), args), (pset(n=sg.MAX_TENSORS + 1), args), (pset(size=-1), args),
+        (pset(null="grad"), args), (pset(null="v"), args),
+        (pset(), (0, 1e-3, 0.9, 0.999, 1e-8)),          # step counts from 1
+        (pset(), (1, -1e-3, 0.9, 0.999, 1e-8)),         # negative learning rate
+        (pset(), (1, 1e-3, 1.0, 0.999, 1e-8)),          # beta1 = 1
+        (pset(), (1, 1e-3, 0.9, 1.5, 1e-8)),            # beta2 > 1
+        (pset(), (1, 1e-3, 0.9, 0.999, -1.0)),          # negative eps
+        (pset(), (1, float("nan"), 0.9, 0.999, 1e-8)),  # NaN learning rate
+    ]
+    for ps, (step, lr, b1, b2, eps) in cases:
+        assert lib.sagips_adam_step(h, ctypes.byref(ps), step, lr, b1, b2, eps) == sg.E_INVAL
+        assert lib.sagips_last_error(h)
+    assert lib.sagips_adam_step(h, None, *args) == sg.E_INVAL
+    torch.cuda.synchronize()
+    assert torch.all(p == 1) and torch.all(m == 0) and torch.all(v == 0)
+    # a valid request on the same tensors still works afterwards
+    assert lib.sagips_adam_step(h, ctypes.byref(pset()), *args) == 0
+    torch.cuda.synchronize()
+    assert torch.all(p < 1)
