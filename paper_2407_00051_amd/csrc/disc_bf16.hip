@@ -565,6 +565,7 @@ __global__ __launch_bounds__(Chain<H>::THREADS, Chain<H>::BPC) void k_fwd_chain(
   __shared__ float sfeat[T * F];
   __shared__ float zpart[WAVES][T];
   __shared__ float se_s[T];
+  __shared__ __attribute__((aligned(16))) u16 sterm[3][T];   // e_D of each event as bf16 terms hi, mid, lo
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int lr = lane & 31, lh = lane >> 5;
   const int ow = 32 * MT * wave;
@@ -608,7 +609,7 @@ __global__ __launch_bounds__(Chain<H>::THREADS, Chain<H>::BPC) void k_fwd_chain(
       }
       wof[mt][s] = __builtin_bit_cast(bf16x8, make_uint4(w[0], w[1], w[2], w[3]));
     }
-  float dwo = 0.f;                              // dW_o partial of feature tid
+  float dwo[MT] = {0.f, 0.f};                   // dW_o partial of feature ow + 32 nb + lr (lane half 0)
   const float bo = p.bo[0];
   float l0 = 0.f, l1 = 0.f, se = 0.f;           // loss and e_D sums of event tid (tid < T)
   WeightPrefetch<H> pf;
@@ -722,6 +723,13 @@ __global__ __launch_bounds__(Chain<H>::THREADS, Chain<H>::BPC) void k_fwd_chain(
           }
         }
         se_s[tid] = e;
+        {
+          uint32_t lo;
+          const uint32_t hm = bias_terms(e, lo);
+          sterm[0][tid] = (u16)(hm & 0xffffu);
+          sterm[1][tid] = (u16)(hm >> 16);
+          sterm[2][tid] = (u16)lo;
+        }
         p.eD[r] = e;
         p.eG[r] = g;
         se += e;
@@ -736,16 +744,41 @@ __global__ __launch_bounds__(Chain<H>::THREADS, Chain<H>::BPC) void k_fwd_chain(
         }
       }
       __syncthreads();                               // A_{NH+1} and the seeds staged
-#pragma unroll 8
-      for (int ev = 0; ev < T; ++ev) dwo = fmaf(se_s[ev], bf16_to_f32(act[ev * LDA + tid]), dwo);
-      // act, zpart and se_s are next written after the next tile's first
-      // barrier, which every thread reaches only after this point.
+      // dW_o partial = sum_events e_D A_{NH+1} on the matrix cores: rows 0..2
+      // of the A operand are the bf16 terms of e_D (their sum is e_D exactly),
+      // the B operand the wave's own columns of the tile (K = events); rows
+      // 0..2 of the product sit in registers 0..2 of lane half 0
+      {
+        // the transposed-read base, formed here (an opaque copy keeps the
+        // compiler from hoisting sixteen far-offset addresses out of the tile
+        // loop into spilled registers)
+        int ci = copy_lds_base<LDA>(lane, wave);
+        asm volatile("" : "+v"(ci));
+        const u16* cbase = act + ci;
+        f32x16 cz[MT];
+#pragma unroll
+        for (int kb = 0; kb < T / 16; ++kb) {
+          const uint4 tv = *reinterpret_cast<const uint4*>(&sterm[lr < 3 ? lr : 0][16 * kb + 8 * lh]);
+          const bf16x8 af = __builtin_bit_cast(bf16x8, lr < 3 ? tv : make_uint4(0u, 0u, 0u, 0u));
+#pragma unroll
+          for (int nb = 0; nb < MT; ++nb)
+            cz[nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af, copy_read<LDA>(cbase + 16 * kb * LDA + 32 * nb),
+                                                            kb == 0 ? zero : cz[nb], 0, 0, 0);
+        }
+#pragma unroll
+        for (int nb = 0; nb < MT; ++nb) dwo[nb] += (cz[nb][0] + cz[nb][1]) + cz[nb][2];
+      }
+      // act, zpart, se_s and sterm are next written after the next tile's
+      // first barrier, which every thread reaches only after this point.
     }
   }
 
   // ---- per-workgroup partials, fixed order ---------------------------------
   float* dst = p.plog + (int64_t)blockIdx.x * (H + 3);
-  dst[tid] = dwo;
+  if (lh == 0) {
+#pragma unroll
+    for (int nb = 0; nb < MT; ++nb) dst[ow + 32 * nb + lr] = dwo[nb];
+  }
   float s3[3] = {l0, l1, se};
 #pragma unroll
   for (int k = 0; k < 3; ++k) {
@@ -794,7 +827,6 @@ __global__ __launch_bounds__(Chain<H>::THREADS, Chain<H>::BPC) void k_bwd_chain(
   const int ow = 32 * MT * wave;
   const uint32_t woff = weight_offset<H, false>(wave, lane);
   const uint32_t coff = ((uint32_t)(2 * wave * 64 + lane)) * 16;
-  const u16* cbase = act + copy_lds_base<LDA>(lane, wave);
   const ChunkArgs c = p.c;
   const int64_t rstride = (int64_t)c.rows;
   const int ntiles = c.rows / T;
@@ -926,6 +958,9 @@ __global__ __launch_bounds__(Chain<H>::THREADS, Chain<H>::BPC) void k_bwd_chain(
     // dW_1 / db_1: rows R of sfp against the wave's own feature columns of the
     // signal (K = the tile's events), the terms added within the lane
     {
+      int ci = copy_lds_base<LDA>(lane, wave);   // formed here, as in the forward chain's dW_o
+      asm volatile("" : "+v"(ci));
+      const u16* cbase = act + ci;
       f32x16 cw[MT];
 #pragma unroll
       for (int kb = 0; kb < KB; ++kb) {
