@@ -232,3 +232,21 @@ def test_step_input_grad_condition_through_the_feature_map():
         r = oracle.run_step(inp["theta"], 64, 0, W, b, real, features="hd8", bf16=bf16)
         assert r["dL_dx_cond"].shape == r["dL_dx"].shape
         assert np.all(np.abs(r["dL_dx"]) <= r["dL_dx_cond"] * (1 + 1e-12))
+
+
+def test_weight_grad_condition_sums():
+    """dW_cond / db_cond are the sums over events of |terms| of dW / db: they
+    bound |dW|, |db| entrywise, some entries cancel, and with one fake event and
+    the same event as the real batch the logit bias gradient has exactly two
+    terms, sigmoid(z) and -sigmoid(-z), so its condition sum is their absolute sum."""
+    W, b = _net((3, 12, 12, 1), 31)
+    xf, xr = _batches(3, 50, 32)
+    r = disc_fwd_bwd(W, b, xf, xr)
+    for l in range(len(W)):
+        assert np.all(np.abs(r["dW"][l]) <= r["dW_cond"][l] * (1 + 1e-12))
+        assert np.all(np.abs(r["db"][l]) <= r["db_cond"][l] * (1 + 1e-12))
+    assert any(np.any(np.abs(r["dW"][l]) < 0.5 * r["dW_cond"][l]) for l in range(len(W)))
+    same = disc_fwd_bwd(W, b, xf[:1], xf[:1])
+    z = same["logits_fake"][0]
+    np.testing.assert_allclose(same["db_cond"][-1], [sigmoid(z) + sigmoid(-z)], rtol=1e-12)
+    np.testing.assert_allclose(same["db"][-1], [sigmoid(z) - sigmoid(-z)], rtol=1e-12)

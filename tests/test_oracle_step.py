@@ -80,3 +80,16 @@ def test_quadratic_gradient_vs_finite_differences():
     r = oracle.run_step(theta, 30, 8, critic="quadratic")
     fd = _fd_theta(lambda t: oracle.run_step(t, 30, 8, critic="quadratic")["loss"], theta)
     np.testing.assert_allclose(r["dL_dtheta"], fd, rtol=1e-6, atol=1e-9)
+
+
+def test_param_grad_condition_sums():
+    """dL_dtheta_cond bounds |dL/dtheta| entrywise, and with one event per
+    parameter row each entry has a single term (dL/dx_j dx_j/da_j or
+    dx_j/db_j), so the condition sum is exactly its magnitude."""
+    rng = np.random.default_rng(3)
+    theta = rng.uniform(1.0, 6.0, (5, 4))
+    r = oracle.run_step(theta, 300, 7, critic="quadratic")
+    assert np.all(np.abs(r["dL_dtheta"]) <= r["dL_dtheta_cond"] * (1 + 1e-12))
+    assert np.any(np.abs(r["dL_dtheta"]) < 0.5 * r["dL_dtheta_cond"])
+    r1 = oracle.run_step(theta, 1, 7, critic="quadratic")
+    np.testing.assert_allclose(r1["dL_dtheta_cond"], np.abs(r1["dL_dtheta"]), rtol=1e-13)
