@@ -91,11 +91,12 @@ typedef struct {
  *              bf16 operands (weights rounded once per call, activations and
  *              backward signals rounded to nearest even) with fp32 accumulate;
  *              the first and the logit layer stay fp32.
- * Supported shapes: n_layers >= 2; all hidden widths equal, one of 64, 128
- * (F32) or 256, 512 (BF16); width[0] in {2, 3, 8}.  F32 IDENTITY: width 64
- * with 1-3 or 128 with 1-2 hidden-to-hidden layers; F32 PROXY2: width 128
- * with 3 (the paper's 2-128-128-128-128-1 network).  BF16 also needs
- * 0 <= leaky_slope <= 1 (SAGIPS_E_UNSUPPORTED otherwise).                 */
+ * Supported shapes (SAGIPS_E_UNSUPPORTED otherwise): all hidden widths equal,
+ * one of 64, 128 (F32) or 256, 512 (BF16); width[0] in {2, 3, 8}.  F32
+ * IDENTITY with d = 2: width 64 with 1-3 or 128 with 1-2 hidden-to-hidden
+ * layers; with d = 3: width 64 with 1-2 or 128 with 2.  F32 PROXY2: width 128
+ * with 3 (the paper's 2-128-128-128-128-1 network).  BF16: 1-4
+ * hidden-to-hidden layers and 0 <= leaky_slope <= 1.                      */
 typedef struct {
   int32_t n_layers;
   int32_t width[SAGIPS_MAX_LAYERS + 1];
