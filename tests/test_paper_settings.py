@@ -38,13 +38,11 @@ def test_training_step_shape():
 
 
 def test_learning_rates():
-    sig = inspect.signature(oracle.gan_step)
-    assert sig.parameters["lr_g"].default == _g("generator_learning_rate")
-    assert sig.parameters["lr_d"].default == _g("discriminator_learning_rate")
-    import importlib.util
-    spec = importlib.util.find_spec("paper_2407_00051_amd.gan")
-    src = open(spec.origin).read()
-    assert "lr_g: float = 1e-5" in src and "lr_d: float = 1e-4" in src
+    from paper_2407_00051_amd.gan import GanLoop
+    for fn in (oracle.gan_step, GanLoop.__init__):
+        sig = inspect.signature(fn)
+        assert sig.parameters["lr_g"].default == _g("generator_learning_rate")
+        assert sig.parameters["lr_d"].default == _g("discriminator_learning_rate")
 
 
 def test_bootstrap_fraction():
