@@ -414,11 +414,15 @@ __global__ __launch_bounds__(256) void k_ens_final(const float* __restrict__ row
   __shared__ float red[2][kSlices][kGMaxIO];
   const int c = threadIdx.x % kGMaxIO, q = threadIdx.x / kGMaxIO;
   float a = 0.f, b = 0.f;
-  if (c < out)
+  if (c < out) {
+    // unrolled so that eight rows' loads are in flight at once (the adds keep
+    // their order)
+#pragma unroll 8
     for (int64_t r = q; r < k; r += kSlices) {
       a += rowstat[r * out + c];
       b += rowstat[k * out + r * out + c];
     }
+  }
   red[0][q][c] = a;
   red[1][q][c] = b;
   __syncthreads();
