@@ -80,6 +80,16 @@ def kink_margin(W, b, hs, pres):
     return m
 
 
+def logit_cond(W, b, hs):
+    """Per event, the sum of |terms| of the logit: sum_o |W_L[0][o] h[o]| + |b_L|.
+
+    The logit is a dot product over the last hidden layer; this is the scale
+    against which a perturbation of its terms (for example by rounding the
+    activations) is measured, as for the other condition sums."""
+    wo = np.abs(np.asarray(W[-1], dtype=np.float64))[0]
+    return np.abs(hs[-1]) @ wo + abs(float(np.asarray(b[-1], dtype=np.float64)[0]))
+
+
 def input_grad_kink_variants(W, b, x, slope=0.2, margin=1e-5, max_units=6):
     """dz/dx of one event for every admissible choice of LeakyReLU slopes.
 
@@ -172,10 +182,17 @@ def _backward(W, pres, hs, g_z, slope, want_input_grad, cond=False):
     return dW, db, g_in
 
 
-def _disc_bf16(W, b, fake_in, real_in, slope, rnd):
-    """disc_fwd_bwd with the bf16 rounding points of the module docstring; `rnd`
-    is the rounding map (round_bf16, or the identity to check the structure)."""
+def _disc_bf16(W, b, fake_in, real_in, slope, rnd, rnd_a=None, rnd_d=None, rnd_e=None):
+    """disc_fwd_bwd with the bf16 rounding points of the module docstring.  `rnd`
+    is the rounding map of the hidden weights (round_bf16, or the identity to
+    check the structure); rnd_a, rnd_d and rnd_e, those of the activations, of
+    the unit-seed signals and of the scaled weight-gradient operand (default:
+    the same map), so that each point's share of the deviation from the float64
+    network can be measured on its own."""
     n = len(W)
+    rnd_a = rnd if rnd_a is None else rnd_a
+    rnd_d = rnd if rnd_d is None else rnd_d
+    rnd_e = rnd if rnd_e is None else rnd_e
     W = [np.asarray(w, dtype=np.float64) for w in W]
     b = [np.asarray(v, dtype=np.float64) for v in b]
     Wq = [rnd(w) if _hidden(l, n) else w for l, w in enumerate(W)]
@@ -183,7 +200,7 @@ def _disc_bf16(W, b, fake_in, real_in, slope, rnd):
     def fwd(h0):
         hs = [np.asarray(h0, dtype=np.float64)]
         for l in range(n - 1):
-            hs.append(rnd(_leaky(hs[-1] @ Wq[l].T + b[l], slope)))
+            hs.append(rnd_a(_leaky(hs[-1] @ Wq[l].T + b[l], slope)))
         return (hs[-1] @ W[-1].T + b[-1])[:, 0], hs
 
     z_f, hs_f = fwd(fake_in)
@@ -197,11 +214,11 @@ def _disc_bf16(W, b, fake_in, real_in, slope, rnd):
     db = [None] * n
     dW[n - 1] = (e[:, None] * hs[n - 1]).sum(axis=0)[None, :]
     db[n - 1] = np.array([e.sum()])
-    d = rnd(W[n - 1][0][None, :] * _leaky_grad(hs[n - 1], slope))       # unit-seed signal of layer n-2
+    d = rnd_d(W[n - 1][0][None, :] * _leaky_grad(hs[n - 1], slope))     # unit-seed signal of layer n-2
     for l in range(n - 2, 0, -1):                                       # hidden-to-hidden layers
-        dW[l] = rnd(e[:, None] * d).T @ hs[l]
+        dW[l] = rnd_e(e[:, None] * d).T @ hs[l]
         db[l] = (e[:, None] * d).sum(axis=0)
-        d = rnd((d @ Wq[l]) * _leaky_grad(hs[l], slope))
+        d = rnd_d((d @ Wq[l]) * _leaky_grad(hs[l], slope))
     dW[0] = (e[:, None] * d).T @ hs[0]
     db[0] = (e[:, None] * d).sum(axis=0)
     g_in = eG[:, None] * (d[:nf] @ W[0])
@@ -235,6 +252,7 @@ def disc_fwd_bwd(W, b, fake_in, real_in, slope=0.2, bf16=False):
     return {
         "kink_margin_fake": kink_margin(W, b, hs_f, pres_f),
         "logits_fake": z_f, "logits_real": z_r, "loss_d": L_D, "loss_g": L_G,
+        "logits_fake_cond": logit_cond(W, b, hs_f), "logits_real_cond": logit_cond(W, b, hs_r),
         "dW": [p + q for p, q in zip(dW_f, dW_r)], "db": [p + q for p, q in zip(db_f, db_r)],
         "dW_cond": [p + q for p, q in zip(cW_f, cW_r)], "db_cond": [p + q for p, q in zip(cb_f, cb_r)],
         "dLg_din": g_in, "dLg_din_cond": c_in,

@@ -250,3 +250,92 @@ def test_weight_grad_condition_sums():
     z = same["logits_fake"][0]
     np.testing.assert_allclose(same["db_cond"][-1], [sigmoid(z) + sigmoid(-z)], rtol=1e-12)
     np.testing.assert_allclose(same["db"][-1], [sigmoid(z) - sigmoid(-z)], rtol=1e-12)
+
+
+# --- kink_margin: the relative distance of the nearest hidden unit from the LeakyReLU kink ---
+
+def _margin(W, b, x):
+    from oracle.mlp import kink_margin
+    _, pres, hs = mlp_forward(W, b, x)
+    return kink_margin(W, b, hs, pres)
+
+
+def test_kink_margin_hand_value_and_exact_kink():
+    # 1 -> 1 -> 1 -> 1: pre_1 = 2 * 1.5 - 1 = 2 against |3| + |-1| = 4 (0.5); h_1 = 2,
+    # pre_2 = -3 * 2 + 0.5 = -5.5 against 6 + 0.5 (0.846...); the margin is the smaller
+    W = [np.array([[2.0]]), np.array([[-3.0]]), np.array([[1.0]])]
+    b = [np.array([-1.0]), np.array([0.5]), np.array([0.0])]
+    m = _margin(W, b, np.array([[1.5]]))
+    assert m.shape == (1,) and m[0] == 0.5
+    # the second unit decides once the first sits further from its kink
+    b2 = [np.array([10.0]), np.array([0.5]), np.array([0.0])]
+    h1 = 2 * 1.5 + 10.0
+    assert abs(_margin(W, b2, np.array([[1.5]]))[0] - (3 * h1 - 0.5) / (3 * h1 + 0.5)) < 1e-15
+    # a unit exactly on its kink: margin 0
+    W3 = [np.array([[1.0, -1.0], [0.5, 0.25]]), np.array([[1.0, 1.0]])]
+    b3 = [np.array([0.0, 0.1]), np.array([0.0])]
+    m3 = _margin(W3, b3, np.array([[0.375, 0.375], [0.5, 0.25]]))
+    assert m3[0] == 0.0 and m3[1] > 0.0
+
+
+def test_kink_margin_positive_scale_invariance():
+    """LeakyReLU is positively homogeneous, so scaling a layer's weights and bias by
+    c > 0 scales its pre-activations and their sums of |terms| alike (and every later
+    layer's input by c): the margin does not change."""
+    W, b = _net((3, 9, 7, 5, 1), 21)
+    x = np.random.default_rng(22).uniform(0.05, 0.95, (50, 3))
+    m = _margin(W, b, x)
+    c = [3.7, 0.02, 11.0, 0.5]
+    Ws = [w * k for w, k in zip(W, c)]
+    bs = [v * np.prod(c[:l + 1]) for l, v in enumerate(b)]
+    # layer l's input is scaled by prod(c[:l]), so its bias takes the factor of its output
+    np.testing.assert_allclose(_margin(Ws, bs, x), m, rtol=1e-10)
+
+
+def test_kink_margin_is_the_flip_threshold():
+    """For one event and the first hidden layer (input fixed), perturbing every term
+    W[o][k] x_k and the bias b[o] of every unit by a relative amount eta changes a
+    pre-activation by at most eta * sum|terms|: below the margin no unit changes sign,
+    and the adversarial perturbation at the margin puts the nearest unit on its kink."""
+    rng = np.random.default_rng(23)
+    for trial in range(20):
+        F, H = int(rng.integers(1, 6)), int(rng.integers(2, 30))
+        W = [rng.standard_normal((H, F)), rng.standard_normal((1, H))]
+        b = [rng.standard_normal(H) * 0.3, np.zeros(1)]
+        x = rng.uniform(-1, 1, (1, F))
+        m = _margin(W, b, x)[0]
+        pre = W[0] @ x[0] + b[0]
+        s = np.sign(pre)[:, None]
+
+        def perturbed(eta):
+            # every term moves toward zero of its unit's pre-activation by eta |term|
+            Wp = W[0] * (1.0 - eta * s * np.sign(W[0] * x[0][None, :]))
+            bp = b[0] * (1.0 - eta * np.sign(pre) * np.sign(b[0]))
+            return Wp @ x[0] + bp
+
+        assert np.all(np.sign(perturbed(m * (1 - 1e-6))) == np.sign(pre))
+        o = int(np.argmin(np.abs(pre) / (np.abs(W[0]) @ np.abs(x[0]) + np.abs(b[0]))))
+        assert abs(perturbed(m)[o]) <= 1e-12 * (np.abs(W[0][o]) @ np.abs(x[0]) + abs(b[0][o]))
+
+
+# --- logit_cond: sum of |terms| of the logit layer ---
+
+def test_logit_cond_bounds_the_logit_and_single_unit_case():
+    from oracle.mlp import logit_cond
+    W, b = _net((2, 8, 8, 1), 24)
+    xf, xr = _batches(2, 30, 25)
+    r = disc_fwd_bwd(W, b, xf, xr)
+    assert np.all(np.abs(r["logits_fake"]) <= r["logits_fake_cond"] * (1 + 1e-15))
+    assert np.all(np.abs(r["logits_real"]) <= r["logits_real_cond"] * (1 + 1e-15))
+    # one unit in the last hidden layer with a zero bias: a single term, so the sum of
+    # |terms| is the logit's magnitude
+    W1, b1 = _net((2, 4, 1, 1), 26)
+    b1[-1][:] = 0.0
+    z, _, hs = mlp_forward(W1, b1, xf)
+    np.testing.assert_allclose(logit_cond(W1, b1, hs), np.abs(z), rtol=1e-15)
+    # flipping the sign of a logit weight leaves it unchanged
+    W2 = [w.copy() for w in W]
+    W2[-1][0, 3] *= -1.0
+    _, _, hs0 = mlp_forward(W, b, xf)
+    _, _, hs2 = mlp_forward(W2, b, xf)
+    np.testing.assert_array_equal(logit_cond(W2, b, hs2), logit_cond(W, b, hs0))
