@@ -44,7 +44,7 @@ typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef unsigned short u16;
 
 constexpr int kMaxNH = 4;
-constexpr int kChunkRows = 1 << 22;   // rows per chunk (fake or real), multiple of 128
+constexpr int kChunkRows = 1 << 22;   // default and largest rows per chunk (fake or real), multiple of 128
 
 // fp32 -> bf16, round to nearest even (finite inputs).
 __device__ __forceinline__ u16 bf16_bits(float f) {
@@ -1452,6 +1452,7 @@ inline size_t al(size_t b) { return (b + 255) & ~(size_t)255; }
 struct Plan {
   int H, NH, F, D;
   bool hd8;
+  int chunk;             // rows per chunk
   int rows_max;          // padded rows of the largest chunk
   int blocks;            // workgroups of the chain kernels
   int slices;            // weight-gradient slices per chunk
@@ -1461,6 +1462,8 @@ struct Plan {
 
 int pad128(int64_t n) { return (int)((n + 127) / 128 * 128); }
 
+int chunk_rows_of(const DiscArgs& a) { return a.chunk_rows > 0 ? a.chunk_rows : kChunkRows; }
+
 Plan make_plan(const DiscArgs& a, int n_cu) {
   const sagips_mlp& D = *a.D;
   Plan p;
@@ -1469,7 +1472,8 @@ Plan make_plan(const DiscArgs& a, int n_cu) {
   p.F = D.width[0];
   p.hd8 = D.features == SAGIPS_FEAT_HD8;
   p.D = a.d;
-  const int64_t biggest = std::min<int64_t>(std::max(a.n_fake, a.n_real), kChunkRows);
+  p.chunk = chunk_rows_of(a);
+  const int64_t biggest = std::min<int64_t>(std::max(a.n_fake, a.n_real), p.chunk);
   p.rows_max = pad128(biggest);
   p.blocks = std::max(1, n_cu * (p.H <= 256 ? Chain<256>::BPC : Chain<512>::BPC));
   const int tiles = (p.H / kWT) * (p.H / kWT);
@@ -1535,6 +1539,8 @@ bool disc_bf16_supported(const sagips_mlp& D, int d, const char** why) {
 
 size_t disc_bf16_workspace(const DiscArgs& a, int n_cu) { return make_plan(a, n_cu).total; }
 
+int disc_bf16_max_chunk_rows() { return kChunkRows; }
+
 hipError_t launch_disc_bf16(const DiscArgs& a, void* ws, int n_cu, hipStream_t st, Timer* tm) {
   const sagips_mlp& Dm = *a.D;
   const Plan p = make_plan(a, n_cu);
@@ -1584,10 +1590,10 @@ hipError_t launch_disc_bf16(const DiscArgs& a, void* ws, int n_cu, hipStream_t s
   for (int pass = 0; pass < 2; ++pass) {
     const bool fake = pass == 0;
     const int64_t n = fake ? a.n_fake : a.n_real;
-    for (int64_t row0 = 0; row0 < n; row0 += kChunkRows, ++chunk_index) {
+    for (int64_t row0 = 0; row0 < n; row0 += p.chunk, ++chunk_index) {
       ChunkArgs c;
       c.row0 = row0;
-      c.valid = (int)std::min<int64_t>(kChunkRows, n - row0);
+      c.valid = (int)std::min<int64_t>(p.chunk, n - row0);
       c.rows = pad128(c.valid);
       c.fake = fake ? 1 : 0;
       const int first = chunk_index == 0 ? 1 : 0;

@@ -66,6 +66,7 @@ struct DiscArgs {
   int64_t n_real;
   const sagips_disc_out* out;
   int d;
+  int chunk_rows = 0;          // bf16 path: rows per chunk (multiple of 128), 0 = the default
 };
 bool disc_f32_supported(const sagips_mlp& D, int d, const char** why);
 int disc_f32_tile();   // events per tile; the in-kernel sampler needs E >= tile
@@ -92,6 +93,8 @@ hipError_t launch_adam(const sagips_param_set& ps, int step, double lr, double b
 // Samples the fake events itself when a.fake_src is set (any E); never writes dLg_dtheta.
 bool disc_bf16_supported(const sagips_mlp& D, int d, const char** why);
 size_t disc_bf16_workspace(const DiscArgs& a, int n_cu);
+// Default (and largest) rows per chunk of the bf16 path.
+int disc_bf16_max_chunk_rows();
 hipError_t launch_disc_bf16(const DiscArgs& a, void* ws, int n_cu, hipStream_t st, Timer* tm);
 
 }  // namespace sagips

@@ -1,5 +1,17 @@
 """GPU parity of the bf16-operand discriminator step (medium: 2-256x4-1,
-higher-dim: HD8 features, 8-512x4-1) against the CPU oracle, through the C ABI."""
+higher-dim: HD8 features, 8-512x4-1) against the CPU oracle, through the C ABI.
+
+Two bars, both asserted on every output tensor:
+  * against the float64 network (the definition: network of Sec. V-A, objective
+    of Sec. II-B.2), 2e-2 per tensor (normwise, or per entry against its sum of
+    |terms| for the logits and the reduced sums).  Rounding the operands to bf16
+    changes the function itself; where the oracle evaluated at the bf16 rounding
+    points is by itself further than 1.6e-2 from float64 (the medium network's
+    first-layer gradients, dL_G/dx through LeakyReLU kinks: measured and
+    attributed to their rounding points on the CPU by
+    tests/test_oracle_bf16_reading.py), the bar is that deviation plus 4e-3;
+  * against that bf16-point oracle, 2e-3: only the fp32 accumulation order and
+    rounding decisions taken from fp32 instead of float64 values differ."""
 import numpy as np
 import pytest
 
@@ -14,7 +26,7 @@ pytestmark = pytest.mark.gpu
 torch = pytest.importorskip("torch")
 import paper_2407_00051_amd as sg  # noqa: E402
 
-TOL = 2e-2        # bf16 operands: normwise per tensor (against the float64 network)
+TOL = 2e-2        # bf16 operands: per tensor, against the float64 network
 TOL_EMU = 2e-3    # against the oracle that rounds at the same bf16 points: only the fp32
                   # accumulation order and the rounding of fp32 (not float64) values differ
 
@@ -62,24 +74,41 @@ def _run(ctx, w, th, ts, W, b, n_real):
     return o
 
 
-def _fp64_bar(o, emu, ref, n_layers):
-    """The losses and dL_G/dtheta against the float64 network at TOL, unless the
-    bf16-point oracle is itself beyond TOL there: rounding the operands to bf16
-    changes the function, and the kernel is held to that oracle at TOL_EMU."""
+def _check_fp64(o, emu, ref, n_layers):
+    """Every tensor against the float64 oracle.  The bar of tensor X is TOL, or
+    dev_X + 2 TOL_EMU where dev_X, the normwise distance of the bf16-point oracle
+    from float64 (the rounded function's own deviation, computed by the oracle
+    alone), exceeds TOL - 2 TOL_EMU.  Logits and reduced sums also pass with
+    every entry within TOL of its sum of |terms| (float64 condition sums)."""
     from tests.parity import normwise
-    bad = _check(o, ref, TOL, "vs fp64", n_layers, asserted=("loss_d", "loss_g", "dLg_dtheta"))
+    bad = []
+    em = emu_as_out(emu)
 
-    def beyond(got, r, cond=None):
-        if normwise(got, r) <= TOL:
-            return False
-        return cond is None or float(np.max(np.abs(got - r) / np.maximum(cond, 1e-300))) > TOL
+    def one(what, got, r, e, cond=None):
+        got = np.asarray(got, np.float64)
+        err = normwise(got, r)
+        dev = normwise(e, r)
+        bar = max(TOL, dev + 2 * TOL_EMU)
+        ok = err <= bar
+        msg = f"  vs fp64 {what}: normwise {err:.3e} (bf16-point oracle {dev:.3e}; bar {bar:.1e})"
+        if not ok and cond is not None:
+            worst = float(np.max(np.abs(got - r) / np.maximum(cond, 1e-300)))
+            msg += f", max |err|/sum|terms| {worst:.3e}"
+            ok = worst <= TOL
+        print(msg + ("" if ok else "  <-- FAIL"), flush=True)
+        if not ok:
+            bad.append(what)
 
-    emu_beyond = {"loss_d": beyond(emu["loss_d"], ref["loss_d"]), "loss_g": beyond(emu["loss_g"], ref["loss_g"]),
-                  "dLg_dtheta": beyond(emu["dL_dtheta"], ref["dL_dtheta"], ref["dL_dtheta_cond"])}
-    for k in bad:
-        if emu_beyond[k]:
-            print(f"  {k}: the bf16-point oracle itself is beyond {TOL:.0e} of float64 (reported)", flush=True)
-    return [k for k in bad if not emu_beyond[k]]
+    one("logits_fake", to_np(o["logits_fake"]), ref["logits_fake"], emu["logits_fake"], ref["logits_fake_cond"])
+    one("logits_real", to_np(o["logits_real"]), ref["logits_real"], emu["logits_real"], ref["logits_real_cond"])
+    one("loss_d", o["loss_d"].item(), ref["loss_d"], emu["loss_d"])
+    one("loss_g", o["loss_g"].item(), ref["loss_g"], emu["loss_g"])
+    for l in range(n_layers):
+        one(f"dW[{l}]", to_np(o["dW"][l]), ref["dW"][l], emu["dW"][l], ref["dW_cond"][l])
+        one(f"db[{l}]", to_np(o["db"][l]), ref["db"][l], emu["db"][l], ref["db_cond"][l])
+    one("dLg_dx", to_np(o["dLg_dx"]), ref["dL_dx"], em["dLg_dx"].a, ref["dL_dx_cond"])
+    one("dLg_dtheta", to_np(o["dLg_dtheta"]), ref["dL_dtheta"], emu["dL_dtheta"], ref["dL_dtheta_cond"])
+    return bad
 
 
 def _check_dx(got, r, cond, tol, tag):
@@ -106,7 +135,7 @@ def _check_dx(got, r, cond, tol, tag):
     return None if ok else "dLg_dx"
 
 
-def _check(o, ref, tol, tag, n_layers, cond_ref=None, dx_outliers=False, asserted=None):
+def _check(o, ref, tol, tag, n_layers, cond_ref=None, dx_outliers=False):
     """Normwise per tensor; a tensor of sums (dW, db, dL/dtheta, dL_G/dx) whose
     normwise error exceeds tol still passes if every entry is within
     tol * sum|terms| (cancelling sums), with the condition sums taken from the
@@ -122,9 +151,8 @@ def _check(o, ref, tol, tag, n_layers, cond_ref=None, dx_outliers=False, asserte
             worst = float(np.max(np.abs(np.asarray(got, np.float64) - r) / np.maximum(cond, 1e-300)))
             msg += f", max |err|/sum|terms| {worst:.3e}"
             ok = worst <= tol
-        barred = asserted is None or what in asserted
-        print(msg + ("" if ok else ("  <-- FAIL" if barred else "  (beyond tol; reported, not a bar)")), flush=True)
-        if not ok and barred:
+        print(msg + ("" if ok else "  <-- FAIL"), flush=True)
+        if not ok:
             bad.append(what)
 
     cr = cond_ref or ref
@@ -160,13 +188,9 @@ def test_bf16_reduced(gpu_ctx, name, n_theta, E, n_real):
     o = _run(gpu_ctx, w, th, ts, W, b, n_real)
     real_np = oracle.sample(inp["theta_star"], n_real, w.real_seed)
     ref = oracle.run_step(inp["theta"], E, w.fake_seed, inp["W"], inp["b"], real_np, features=w.features)
-    # The parity bar: the oracle evaluated at the same bf16 operand rounding points.
     emu = oracle.run_step(inp["theta"], E, w.fake_seed, inp["W"], inp["b"], real_np, features=w.features, bf16=True)
     bad_emu = _check(o, emu, TOL_EMU, "vs bf16-point oracle", len(W), cond_ref=ref, dx_outliers=True)
-    # Against the float64 network: the losses and dL/dtheta at the same bar; the rest is
-    # reported (rounding the operands changes the network, and per-event quantities such as
-    # dL_G/dx and the first-layer gradient are ill-conditioned under that change).
-    bad64 = _fp64_bar(o, emu, ref, len(W))
+    bad64 = _check_fp64(o, emu, ref, len(W))
     assert not bad_emu and not bad64, (bad_emu, bad64)
 
 
@@ -192,8 +216,53 @@ def test_bf16_other_shapes(gpu_ctx, d, features, H, NH):
     emu = oracle.run_step(inp["theta"], w.events_per_theta, w.fake_seed, inp["W"], inp["b"], real_np,
                           features=w.features, bf16=True)
     bad_emu = _check(o, emu, TOL_EMU, "vs bf16-point oracle", len(W), cond_ref=ref, dx_outliers=True)
-    bad64 = _fp64_bar(o, emu, ref, len(W))
+    bad64 = _check_fp64(o, emu, ref, len(W))
     assert not bad_emu and not bad64, (bad_emu, bad64)
+
+
+@pytest.mark.parametrize("name,n_theta,E,n_real,chunk", [
+    ("medium", 3, 1000, 2999, 1024),       # three chunks per batch, the last one ragged
+    ("higher_dim", 2, 777, 1500, 512),     # four fake chunks (the last of 18 rows), three real
+])
+def test_bf16_multi_chunk(gpu_ctx, name, n_theta, E, n_real, chunk):
+    """The batches in chunks of `chunk` rows: chunks starting at row0 > 0 within a
+    batch sample their events at that counter offset and write their logits and
+    dL_G/dx at their rows; every later chunk's partials are added to the first
+    chunk's.  Held to the oracle as in test_bf16_reduced, and to the one-chunk run:
+    per-event outputs identical, reduced sums within fp32 reordering."""
+    from tests.parity import normwise
+    w = scaled(get(name), n_theta, E)
+    print(f"case {name} n_theta={n_theta} E={E} n_real={n_real} chunk={chunk}", flush=True)
+    inp, th, ts, W, b = _setup(w)
+    one = _run(gpu_ctx, w, th, ts, W, b, n_real)
+    gpu_ctx.set_bf16_chunk_rows(chunk)
+    try:
+        o = _run(gpu_ctx, w, th, ts, W, b, n_real)
+    finally:
+        gpu_ctx.set_bf16_chunk_rows(0)
+    for k in ("logits_fake", "logits_real", "dLg_dx", "dLg_dtheta"):
+        assert torch.equal(o[k], one[k]), k
+    for k in ("loss_d", "loss_g"):
+        assert abs(o[k].item() - one[k].item()) <= 1e-6 * abs(one[k].item()), k
+    for l in range(len(W)):
+        for k in ("dW", "db"):
+            e = normwise(to_np(o[k][l]), to_np(one[k][l]))
+            assert e <= 1e-5, (k, l, e)
+    real_np = oracle.sample(inp["theta_star"], n_real, w.real_seed)
+    ref = oracle.run_step(inp["theta"], E, w.fake_seed, inp["W"], inp["b"], real_np, features=w.features)
+    emu = oracle.run_step(inp["theta"], E, w.fake_seed, inp["W"], inp["b"], real_np, features=w.features, bf16=True)
+    bad_emu = _check(o, emu, TOL_EMU, "vs bf16-point oracle", len(W), cond_ref=ref, dx_outliers=True)
+    bad64 = _check_fp64(o, emu, ref, len(W))
+    assert not bad_emu and not bad64, (bad_emu, bad64)
+
+
+def test_bf16_chunk_rows_validation(gpu_ctx):
+    for bad in (1, 127, 200, (1 << 22) + 128, -128):
+        with pytest.raises(sg.SagipsError) as ei:
+            gpu_ctx.set_bf16_chunk_rows(bad)
+        assert ei.value.status == sg.E_INVAL
+    gpu_ctx.set_bf16_chunk_rows(128)
+    gpu_ctx.set_bf16_chunk_rows(0)
 
 
 def test_bf16_deterministic(gpu_ctx):
@@ -235,18 +304,59 @@ def test_bf16_full_size_sampled(gpu_ctx, name):
     fin = xf if w.features == "identity" else oracle.features_hd8(xf)
     rin = xr if w.features == "identity" else oracle.features_hd8(xr)
     from tests.parity import normwise
-    for tag, bf16 in (("fp64 (reported)", False), ("bf16-point oracle", True)):
+    res = {}
+    for bf16 in (False, True):
         r = oracle.disc_fwd_bwd(inp["W"], inp["b"], fin, rin, bf16=bf16)
         g = r["dLg_din"] * (len(idx) / w.n_events)          # the oracle batch mean is over the sample
+        gc = r["dLg_din_cond"] * (len(idx) / w.n_events)
         if w.features == "hd8":
-            g = np.einsum("nf,nfd->nd", g, oracle.features_hd8_jacobian(xf))
-        if bf16:
-            assert_normwise(zf, r["logits_fake"], TOL, "sampled logits_fake vs " + tag)
-            assert_normwise(zr, r["logits_real"], TOL, "sampled logits_real vs " + tag)
-            assert_normwise(gx, g, TOL, "sampled dLg_dx vs " + tag)
-        else:
-            print(f"  sampled vs {tag}: logits_fake {normwise(zf, r['logits_fake']):.3e}, logits_real "
-                  f"{normwise(zr, r['logits_real']):.3e}, dLg_dx {normwise(gx, g):.3e}", flush=True)
+            J = oracle.features_hd8_jacobian(xf)
+            g = np.einsum("nf,nfd->nd", g, J)
+            gc = np.einsum("nf,nfd->nd", gc, np.abs(J))
+        res[bf16] = (r, g, gc)
+    (r64, g64, gc64), (remu, gemu, _) = res[False], res[True]
+    assert_normwise(zf, remu["logits_fake"], TOL_EMU, "sampled logits_fake vs bf16-point oracle")
+    assert_normwise(zr, remu["logits_real"], TOL_EMU, "sampled logits_real vs bf16-point oracle")
+    assert _check_dx(gx, gemu, gc64, TOL_EMU, "sampled vs bf16-point oracle") is None
+    for what, got, ref, e, cond in (("logits_fake", zf, r64["logits_fake"], remu["logits_fake"], r64["logits_fake_cond"]),
+                                    ("logits_real", zr, r64["logits_real"], remu["logits_real"], r64["logits_real_cond"]),
+                                    ("dLg_dx", gx, g64, gemu, gc64)):
+        err, dev = normwise(got, ref), normwise(e, ref)
+        bar = max(TOL, dev + 2 * TOL_EMU)
+        worst = float(np.max(np.abs(got - ref) / np.maximum(cond, 1e-300)))
+        ok = err <= bar or (what != "dLg_dx" and worst <= TOL)
+        print(f"  sampled {what} vs fp64: normwise {err:.3e} (bf16-point oracle {dev:.3e}; bar {bar:.1e}), "
+              f"max |err|/sum|terms| {worst:.3e}" + ("" if ok else "  <-- FAIL"), flush=True)
+        assert ok, what
+    # dL_G/dtheta of a few whole parameter rows: each a sum over that row's E events
+    # with the seeds e_G = dL_G/dz of the full batch (the oracle's batch mean over
+    # one row's events, rescaled to the full batch)
+    rows = sorted({0, 1, w.n_theta // 2, w.n_theta - 1})
+    got = to_np(o["dLg_dtheta"]).astype(np.float64)[rows]
+    E = w.events_per_theta
+    real_small = oracle.sample(inp["theta_star"], 256, w.real_seed)
+    r64, remu = [], []
+    for bf16 in (False, True):
+        g, c = [], []
+        for i in rows:
+            r = oracle.run_step(inp["theta"][i:i + 1], E, w.fake_seed, inp["W"], inp["b"], real_small,
+                                features=w.features, bf16=bf16, counter_base=i * E)
+            g.append(r["dL_dtheta"][0] * (E / w.n_events))
+            c.append(r["dL_dtheta_cond"][0] * (E / w.n_events))
+        (remu if bf16 else r64).append((np.array(g), np.array(c)))
+    (g64, c64), = r64
+    (gemu, _), = remu
+    e_emu = normwise(got, gemu)
+    worst_emu = float(np.max(np.abs(got - gemu) / np.maximum(c64, 1e-300)))
+    print(f"  full-size dLg_dtheta rows {rows} vs bf16-point oracle: normwise {e_emu:.3e}, "
+          f"max |err|/sum|terms| {worst_emu:.3e}", flush=True)
+    assert e_emu <= TOL_EMU or worst_emu <= TOL_EMU
+    e64, dev = normwise(got, g64), normwise(gemu, g64)
+    worst64 = float(np.max(np.abs(got - g64) / np.maximum(c64, 1e-300)))
+    bar = max(TOL, dev + 2 * TOL_EMU)
+    print(f"  full-size dLg_dtheta rows vs fp64: normwise {e64:.3e} (bf16-point oracle {dev:.3e}; bar {bar:.1e}), "
+          f"max |err|/sum|terms| {worst64:.3e}", flush=True)
+    assert e64 <= bar or worst64 <= TOL
     # properties over the whole batch, from the returned logits
     zf_all = to_np(o["logits_fake"]).astype(np.float64)
     zr_all = to_np(o["logits_real"]).astype(np.float64)
