@@ -19,7 +19,10 @@
  *     Faults during execution surface at the caller's stream synchronisation.
  *   - Outputs are overwritten, never accumulated.  Results are bitwise
  *     reproducible for fixed inputs (fixed reduction order, no float atomics).
- *   - Device arrays must be 16-byte aligned and densely packed, row-major.
+ *   - Device arrays must be 16-byte aligned and densely packed, row-major;
+ *     the one exception is theta, which needs only 4-byte alignment so that a
+ *     caller can pass the rows of one shard (theta + r * 2d).
+ *   - Several contexts may share a device; each owns its own workspace.
  *   - A context is not thread-safe; calls on one context must not overlap
  *     from several host threads.
  *
@@ -59,8 +62,9 @@ typedef enum { SAGIPS_FEAT_IDENTITY = 0, SAGIPS_FEAT_HD8 = 1, SAGIPS_FEAT_PROXY2
 typedef enum { SAGIPS_CRITIC_BUFFER = 0, SAGIPS_CRITIC_QUADRATIC = 1 } sagips_critic;
 
 /* Parameters -> events source (host struct holding a device pointer).
- *   theta            device, [n_theta][2d] fp32, rows (a1,b1,a2,b2[,a3,b3]);
- *                    shape parameters must be > 0 (the workloads use >= 1).
+ *   theta            device, [n_theta][2d] fp32, rows (a1,b1,a2,b2[,a3,b3]),
+ *                    4-byte aligned; shape parameters must be > 0 (the
+ *                    workloads use >= 1).
  *   n_theta          >= 1
  *   d                observables per event, 2 or 3
  *   events_per_theta E >= 1; n_theta * E < 2^31 and counter_base + n_theta*E < 2^64
@@ -134,8 +138,18 @@ sagips_status sagips_create(sagips_ctx** out, int hip_device, void* hip_stream);
  * first.  NULL is accepted.                                               */
 sagips_status sagips_destroy(sagips_ctx* ctx);
 
-/* Switch subsequent calls to another stream of the same device.           */
+/* Switch subsequent calls to another stream of the same device.  The new
+ * stream is made to wait (on the device, not the host) for the work already
+ * queued on the old one, which may still use the context's workspace.     */
 sagips_status sagips_set_stream(sagips_ctx* ctx, void* hip_stream);
+
+/* Rows per chunk of the bf16 discriminator (which runs the fake and the real
+ * batch in chunks whose activations and signals it stages in the workspace):
+ * 0 restores the default, 4,194,304 rows, which is also the largest allowed;
+ * otherwise a multiple of 128 in [128, 4194304].  Results do not depend on
+ * it beyond the order of the fp32 sums across chunks; smaller chunks need a
+ * smaller workspace.  SAGIPS_E_INVAL for other values.                    */
+sagips_status sagips_set_bf16_chunk_rows(sagips_ctx* ctx, int64_t rows);
 
 /* Message of the last failed call on ctx (ctx may be NULL: message of the
  * last failed sagips_create in this process).  Never NULL.               */

@@ -23,7 +23,8 @@ F32, BF16 = 0, 1
 FEAT_IDENTITY, FEAT_HD8, FEAT_PROXY2 = 0, 1, 2
 CRITIC_BUFFER, CRITIC_QUADRATIC = 0, 1
 
-EXPORTED = ("sagips_create", "sagips_destroy", "sagips_set_stream", "sagips_last_error", "sagips_set_timing",
+EXPORTED = ("sagips_create", "sagips_destroy", "sagips_set_stream", "sagips_set_bf16_chunk_rows",
+            "sagips_last_error", "sagips_set_timing",
             "sagips_kernel_times", "sagips_sample_events", "sagips_disc_fwd_bwd", "sagips_param_grad",
             "sagips_bootstrap", "sagips_bootstrap_rows", "sagips_gen_forward", "sagips_gen_backward", "sagips_ensemble_response",
             "sagips_adam_step")
@@ -81,6 +82,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.sagips_create.argtypes = [ctypes.POINTER(vp), i32, vp]
     lib.sagips_destroy.argtypes = [vp]
     lib.sagips_set_stream.argtypes = [vp, vp]
+    lib.sagips_set_bf16_chunk_rows.argtypes = [vp, i64]
     lib.sagips_last_error.argtypes = [vp]
     lib.sagips_last_error.restype = ctypes.c_char_p
     lib.sagips_set_timing.argtypes = [vp, i32]
@@ -98,7 +100,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.sagips_ensemble_response.argtypes = [vp, ctypes.POINTER(GenStack), vp, i64, vp, vp, vp, vp]
     lib.sagips_adam_step.argtypes = [vp, ctypes.POINTER(ParamSet), i32, ctypes.c_double, ctypes.c_double,
                                      ctypes.c_double, ctypes.c_double]
-    for name in ("sagips_create", "sagips_destroy", "sagips_set_stream", "sagips_set_timing",
+    for name in ("sagips_create", "sagips_destroy", "sagips_set_stream", "sagips_set_bf16_chunk_rows",
+                 "sagips_set_timing",
                  "sagips_kernel_times", "sagips_sample_events", "sagips_disc_fwd_bwd", "sagips_param_grad",
                  "sagips_bootstrap", "sagips_bootstrap_rows", "sagips_gen_forward", "sagips_gen_backward", "sagips_ensemble_response",
                  "sagips_adam_step"):
@@ -130,12 +133,20 @@ def _check_tensor(t, name, dtype=None, shape=None, device=None):
 
 
 class Context:
-    """A library context on one GPU, running on torch's current stream of that device."""
+    """A library context on one GPU.
+
+    Without a stream it follows torch: every call runs on torch's current stream
+    of the device at the time of the call, the stream on which the binding also
+    allocates the outputs it returns.  With an explicit stream every call runs
+    there, and outputs the binding allocates are marked as used by that stream
+    (record_stream), so that torch's caching allocator does not hand their memory
+    out again before the library's kernels are done with it."""
 
     def __init__(self, device: int = 0, stream=None):
         import torch
         self.lib = load_library()
         self.device = device
+        self._follow = stream is None
         if stream is None:
             stream = torch.cuda.current_stream(device)
         self._stream = stream
@@ -166,8 +177,36 @@ class Context:
         return self._stream
 
     def set_stream(self, stream):
+        """Run later calls on `stream` (and stop following torch's current stream)."""
         self._check(self.lib.sagips_set_stream(self.h, ctypes.c_void_p(stream.cuda_stream)))
         self._stream = stream
+        self._follow = False
+
+    def _enter(self):
+        """Before a call: in follow mode, switch to torch's current stream if it changed."""
+        if self._follow:
+            import torch
+            cur = torch.cuda.current_stream(self.device)
+            if cur.cuda_stream != self._stream.cuda_stream:
+                self._check(self.lib.sagips_set_stream(self.h, ctypes.c_void_p(cur.cuda_stream)))
+                self._stream = cur
+
+    def _owned(self, *tensors):
+        """Outputs the binding allocated on torch's current stream, used by the library's stream."""
+        if self._follow:
+            return
+        import torch
+        if torch.cuda.current_stream(self.device).cuda_stream == self._stream.cuda_stream:
+            return
+        for t in tensors:
+            if isinstance(t, (list, tuple)):
+                self._owned(*t)
+            elif t is not None:
+                t.record_stream(self._stream)
+
+    def set_bf16_chunk_rows(self, rows: int = 0):
+        """Rows per chunk of the bf16 discriminator (0: the default, 4,194,304)."""
+        self._check(self.lib.sagips_set_bf16_chunk_rows(self.h, int(rows)))
 
     def set_timing(self, enable: bool):
         self._check(self.lib.sagips_set_timing(self.h, 1 if enable else 0))
@@ -196,6 +235,7 @@ class Context:
                       want_x: bool = True, want_words: bool = False, out=None, words_out=None):
         """Events [N][d] fp32 (and optionally the raw Philox words [N][4] int32)."""
         import torch
+        self._enter()
         src = self.source(theta, events_per_theta, seed, counter_base, stream)
         N = src.n_theta * src.events_per_theta
         x = None
@@ -206,6 +246,7 @@ class Context:
         if want_words:
             w = words_out if words_out is not None else torch.empty((N, 4), dtype=torch.int32, device=theta.device)
             _check_tensor(w, "words_out", torch.int32, (N, 4), self.device)
+        self._owned(x if out is None else None, w if words_out is None else None)
         self._check(self.lib.sagips_sample_events(self.h, ctypes.byref(src), _ptr(x), _ptr(w)))
         self._keep = (theta,)
         if want_words and want_x:
@@ -219,6 +260,7 @@ class Context:
         optionally the drawn row indices [n_out] int64; with row_order the same multiset in
         ascending row order."""
         import torch
+        self._enter()
         _check_tensor(data, "data", torch.float32, None, self.device)
         if data.dim() != 2 or data.shape[1] not in (2, 3):
             raise ValueError("data must be [n_data][d] with d in {2, 3}")
@@ -229,6 +271,7 @@ class Context:
         if want_idx:
             idx = idx_out if idx_out is not None else torch.empty(n_out, dtype=torch.int64, device=data.device)
             _check_tensor(idx, "idx_out", torch.int64, (n_out,), self.device)
+        self._owned(x if out is None else None, idx if idx_out is None else None)
         fn = self.lib.sagips_bootstrap_rows if row_order else self.lib.sagips_bootstrap
         self._check(fn(self.h, _ptr(data), data.shape[0], d, seed & (2**64 - 1), step & 0xFFFFFFFF, n_out, _ptr(x),
                        _ptr(idx)))
@@ -262,18 +305,21 @@ class Context:
     def gen_forward(self, W: Sequence, b: Sequence, noise, slope: float = 0.2, out=None):
         """theta [M][k][out] = 1 + softplus(G_m(noise)) for every member m."""
         import torch
+        self._enter()
         g, M = self._gen(W, b, slope)
         _check_tensor(noise, "noise", torch.float32, (noise.shape[0], g.width[0]), self.device)
         k = noise.shape[0]
         th = out if out is not None else torch.empty((M, k, g.width[g.n_layers]), dtype=torch.float32,
                                                      device=noise.device)
         _check_tensor(th, "out", torch.float32, (M, k, g.width[g.n_layers]), self.device)
+        self._owned(th if out is None else None)
         self._check(self.lib.sagips_gen_forward(self.h, ctypes.byref(g), noise.data_ptr(), k, th.data_ptr()))
         return th
 
     def gen_backward(self, W: Sequence, b: Sequence, noise, dL_dtheta, slope: float = 0.2, dW=None, db=None):
         """Gradients (dW, db), shaped like W and b, of sum <dL/dtheta, theta> per member."""
         import torch
+        self._enter()
         g, M = self._gen(W, b, slope)
         _check_tensor(noise, "noise", torch.float32, (noise.shape[0], g.width[0]), self.device)
         k = noise.shape[0]
@@ -282,8 +328,10 @@ class Context:
             _check_tensor(dL_dtheta, "dL_dtheta", torch.float32, (M, k, n_out), self.device)
         else:
             _check_tensor(dL_dtheta, "dL_dtheta", torch.float32, (k, n_out), self.device)
+        new_dW, new_db = dW is None, db is None
         dW = dW if dW is not None else [torch.empty_like(w) for w in W]
         db = db if db is not None else [torch.empty_like(v) for v in b]
+        self._owned(dW if new_dW else None, db if new_db else None)
         for l in range(g.n_layers):
             _check_tensor(dW[l], f"dW[{l}]", torch.float32, tuple(W[l].shape), self.device)
             _check_tensor(db[l], f"db[{l}]", torch.float32, tuple(b[l].shape), self.device)
@@ -296,6 +344,7 @@ class Context:
     def ensemble_response(self, W: Sequence, b: Sequence, noise, p_true=None, slope: float = 0.2) -> dict:
         """p_hat and sigma [out] averaged over the noise batch, and r_hat = (p_true - p_hat) / p_true."""
         import torch
+        self._enter()
         g, M = self._gen(W, b, slope)
         _check_tensor(noise, "noise", torch.float32, (noise.shape[0], g.width[0]), self.device)
         n_out = g.width[g.n_layers]
@@ -304,6 +353,7 @@ class Context:
         if p_true is not None:
             _check_tensor(p_true, "p_true", torch.float32, (n_out,), self.device)
             o["r_hat"] = torch.empty(n_out, **f32)
+        self._owned(o["p_hat"], o["sigma"], o["r_hat"])
         self._check(self.lib.sagips_ensemble_response(self.h, ctypes.byref(g), noise.data_ptr(), noise.shape[0],
                                                       _ptr(p_true), o["p_hat"].data_ptr(), o["sigma"].data_ptr(),
                                                       _ptr(o["r_hat"])))
@@ -314,6 +364,7 @@ class Context:
                   beta1: float = 0.9, beta2: float = 0.999, eps: float = 1e-8) -> None:
         """In-place Adam step on up to 16 fp32 tensors (m, v start at zero; step counts from 1)."""
         import torch
+        self._enter()
         n = len(params)
         if not (n == len(grads) == len(m) == len(v)) or not 1 <= n <= MAX_TENSORS:
             raise ValueError("params, grads, m, v must have the same length, 1..16")
@@ -335,6 +386,7 @@ class Context:
         """One discriminator step.  fake_source = dict(theta=, events_per_theta=, seed=[, counter_base=, stream=])
         samples the fake events inside the kernel and also returns dLg_dtheta."""
         import torch
+        self._enter()
         n_layers = len(W)
         if n_layers != len(b) or not 1 <= n_layers <= MAX_LAYERS:
             raise ValueError("W and b must have the same length, 1..8")
@@ -370,6 +422,7 @@ class Context:
         if (fake_x is not None and d != d_in) or real_x.dim() != 2 or real_x.shape[1] != d_in:
             raise ValueError(f"events must be [n][{d_in}] for this network and feature map")
         o = dict(outputs or {})
+        given = set(o)
         f32 = dict(dtype=torch.float32, device=dev)
         if want_logits:
             o.setdefault("logits_fake", torch.empty(max(n_fake, 1), **f32))
@@ -383,6 +436,7 @@ class Context:
             o.setdefault("dLg_dx", torch.empty((max(n_fake, 1), d), **f32))
         if want_dtheta and src is not None:
             o.setdefault("dLg_dtheta", torch.empty((src.n_theta, 2 * src.d), **f32))
+        self._owned(*[v for k, v in o.items() if k not in given])
         out = DiscOut()
         for k in ("logits_fake", "logits_real", "loss_d", "loss_g", "dLg_dx", "dLg_dtheta"):
             if o.get(k) is not None:
@@ -403,6 +457,7 @@ class Context:
                    stream: int = 0, out=None, loss_out=None, want_loss: bool = True):
         """dL/dtheta [n_theta][2d]; with dL_dx None the quadratic critic is used and its loss returned too."""
         import torch
+        self._enter()
         src = self.source(theta, events_per_theta, seed, counter_base, stream)
         g = out if out is not None else torch.empty((src.n_theta, 2 * src.d), dtype=torch.float32, device=theta.device)
         _check_tensor(g, "out", torch.float32, (src.n_theta, 2 * src.d), self.device)
@@ -414,6 +469,7 @@ class Context:
         else:
             critic = CRITIC_BUFFER
             _check_tensor(dL_dx, "dL_dx", torch.float32, (src.n_theta * src.events_per_theta, src.d), self.device)
+        self._owned(g if out is None else None, loss if loss_out is None else None)
         self._check(self.lib.sagips_param_grad(self.h, ctypes.byref(src), critic, _ptr(dL_dx), g.data_ptr(),
                                                _ptr(loss)))
         return (g, loss) if critic == CRITIC_QUADRATIC else g

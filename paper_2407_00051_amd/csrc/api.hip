@@ -76,6 +76,7 @@ struct sagips_ctx {
   size_t ws_cap = 0;
   std::string err = "no error";
   bool timing = false;
+  int bf16_chunk_rows = 0;      // 0: the library's default
   EventTimer timer;
 };
 
@@ -130,11 +131,31 @@ sagips_status ensure_ws(sagips_ctx* c, size_t bytes) {
   return SAGIPS_OK;
 }
 
+// Where a call's workspace comes from: the context's (grown on demand with
+// hipMalloc), or a fixed device buffer that is never reallocated.
+struct WsFrom {
+  char* fixed = nullptr;   // fixed buffer on the context's device, or NULL
+  size_t fixed_cap = 0;
+};
+
+sagips_status acquire_ws(sagips_ctx* c, const WsFrom& from, size_t bytes, char** ws) {
+  if (from.fixed) {
+    if (bytes > from.fixed_cap)
+      return fail(c, SAGIPS_E_INVAL,
+                  "this call needs %zu bytes of workspace; the no-allocation entry point has %zu (use the allocating call)",
+                  bytes, from.fixed_cap);
+    *ws = from.fixed;
+    return SAGIPS_OK;
+  }
+  sagips_status s = ensure_ws(c, bytes);
+  if (s == SAGIPS_OK) *ws = static_cast<char*>(c->ws);
+  return s;
+}
+
 sagips_status check_source(sagips_ctx* c, const sagips_source* s, const char* name) {
   if (!s) return fail(c, SAGIPS_E_INVAL, "%s is NULL", name);
   if (!s->theta) return fail(c, SAGIPS_E_INVAL, "%s.theta is NULL", name);
-  if (!aligned16(s->theta) && (((uintptr_t)s->theta) & 3u))
-    return fail(c, SAGIPS_E_INVAL, "%s.theta is not 4-byte aligned", name);
+  if (((uintptr_t)s->theta) & 3u) return fail(c, SAGIPS_E_INVAL, "%s.theta is not 4-byte aligned", name);
   if (s->n_theta < 1 || s->n_theta > 65535) return fail(c, SAGIPS_E_INVAL, "%s.n_theta = %d outside [1, 65535]", name, s->n_theta);
   if (s->d != 2 && s->d != 3) return fail(c, SAGIPS_E_INVAL, "%s.d = %d, must be 2 or 3", name, s->d);
   if (s->events_per_theta < 1) return fail(c, SAGIPS_E_INVAL, "%s.events_per_theta must be >= 1", name);
@@ -149,7 +170,8 @@ int64_t source_events(const sagips_source* s) { return (int64_t)s->n_theta * s->
 
 // bf16 path: one chunked launcher; dL_G/dtheta by the reduction kernel over dL_G/dx.
 sagips_status disc_bf16(sagips_ctx* c, const sagips_mlp* D, const float* fake_x, const sagips_source* fake_src,
-                        int64_t n_fake, const float* real_x, int64_t n_real, const sagips_disc_out* out, int d) {
+                        int64_t n_fake, const float* real_x, int64_t n_real, const sagips_disc_out* out, int d,
+                        const WsFrom& from, Timer* tm) {
   const char* why = nullptr;
   if (!disc_bf16_supported(*D, d, &why)) return fail(c, SAGIPS_E_UNSUPPORTED, "%s", why);
   SourceArgs sa{};
@@ -162,6 +184,7 @@ sagips_status disc_bf16(sagips_ctx* c, const sagips_mlp* D, const float* fake_x,
   a.real_x = real_x;
   a.n_real = n_real;
   a.d = d;
+  a.chunk_rows = c->bf16_chunk_rows;
   sagips_disc_out o2 = *out;
   o2.dLg_dtheta = nullptr;
   a.out = &o2;
@@ -172,11 +195,10 @@ sagips_status disc_bf16(sagips_ctx* c, const sagips_mlp* D, const float* fake_x,
     off_pg = off_g + (((size_t)n_fake * d * sizeof(float) + 255) & ~(size_t)255);
     total = off_pg + param_grad_workspace(sa);
   }
-  sagips_status s = ensure_ws(c, total);
+  char* ws = nullptr;
+  sagips_status s = acquire_ws(c, from, total, &ws);
   if (s != SAGIPS_OK) return s;
-  char* ws = static_cast<char*>(c->ws);
   if (want_theta && !o2.dLg_dx) o2.dLg_dx = reinterpret_cast<float*>(ws + off_g);
-  Timer* tm = timer_of(c);
   hipError_t e = launch_disc_bf16(a, ws, c->n_cu, c->stream, tm);
   if (e != hipSuccess) return hip_fail(c, e, "disc_fwd_bwd (bf16) launch");
   if (want_theta) {
@@ -262,8 +284,31 @@ sagips_status sagips_destroy(sagips_ctx* c) {
 
 sagips_status sagips_set_stream(sagips_ctx* c, void* hip_stream) {
   if (!c) return fail(nullptr, SAGIPS_E_INVAL, "ctx is NULL");
-  c->stream = static_cast<hipStream_t>(hip_stream);
+  hipStream_t next = static_cast<hipStream_t>(hip_stream);
+  if (next != c->stream) {
+    // Work already queued on the old stream may still read the workspace the
+    // next call reuses: the new stream waits for it (without blocking the host).
+    DeviceGuard g(c->device);
+    hipEvent_t ev = nullptr;
+    hipError_t e = hipEventCreateWithFlags(&ev, hipEventDisableTiming);
+    if (e != hipSuccess) return hip_fail(c, e, "hipEventCreateWithFlags");
+    e = hipEventRecord(ev, c->stream);
+    if (e == hipSuccess) e = hipStreamWaitEvent(next, ev, 0);
+    (void)hipEventDestroy(ev);
+    if (e != hipSuccess) return hip_fail(c, e, "ordering the new stream after the old one");
+  }
+  c->stream = next;
   c->timer.stream = c->stream;
+  return SAGIPS_OK;
+}
+
+sagips_status sagips_set_bf16_chunk_rows(sagips_ctx* c, int64_t rows) {
+  if (!c) return fail(nullptr, SAGIPS_E_INVAL, "ctx is NULL");
+  const int64_t max_rows = disc_bf16_max_chunk_rows();
+  if (rows != 0 && (rows < 128 || rows > max_rows || rows % 128 != 0))
+    return fail(c, SAGIPS_E_INVAL, "bf16 chunk rows = %lld: must be 0 (default) or a multiple of 128 in [128, %lld]",
+                (long long)rows, (long long)max_rows);
+  c->bf16_chunk_rows = (int)rows;
   return SAGIPS_OK;
 }
 
@@ -337,9 +382,15 @@ sagips_status sagips_param_grad(sagips_ctx* c, const sagips_source* src, sagips_
   return e == hipSuccess ? SAGIPS_OK : hip_fail(c, e, "param_grad launch");
 }
 
-sagips_status sagips_disc_fwd_bwd(sagips_ctx* c, const sagips_mlp* D, const float* fake_x,
-                                  const sagips_source* fake_src, int64_t n_fake, const float* real_x, int64_t n_real,
-                                  sagips_disc_out* out) {
+}  // extern "C"
+
+namespace {
+
+// The discriminator step behind sagips_disc_fwd_bwd and its no-allocation
+// variant: validation, then the fp32 or the bf16 path.
+sagips_status disc_call(sagips_ctx* c, const sagips_mlp* D, const float* fake_x, const sagips_source* fake_src,
+                        int64_t n_fake, const float* real_x, int64_t n_real, sagips_disc_out* out,
+                        const WsFrom& from, Timer* tm) {
   if (!c) return fail(nullptr, SAGIPS_E_INVAL, "ctx is NULL");
   if (!D) return fail(c, SAGIPS_E_INVAL, "D is NULL");
   if (!out) return fail(c, SAGIPS_E_INVAL, "out is NULL");
@@ -387,7 +438,7 @@ sagips_status sagips_disc_fwd_bwd(sagips_ctx* c, const sagips_mlp* D, const floa
 
   DeviceGuard g(c->device);
   const char* why = nullptr;
-  if (D->precision == SAGIPS_BF16) return disc_bf16(c, D, fake_x, fake_src, n_fake, real_x, n_real, out, d);
+  if (D->precision == SAGIPS_BF16) return disc_bf16(c, D, fake_x, fake_src, n_fake, real_x, n_real, out, d, from, tm);
   if (!disc_f32_supported(*D, d, &why)) return fail(c, SAGIPS_E_UNSUPPORTED, "%s", why);
 
   // The in-kernel sampler lets a tile straddle at most two parameter rows;
@@ -416,10 +467,9 @@ sagips_status sagips_disc_fwd_bwd(sagips_ctx* c, const sagips_mlp* D, const floa
     off_pg = off_g + (((size_t)n_fake * d * sizeof(float) + 255) & ~(size_t)255);
     extra = off_pg - disc_ws + param_grad_workspace(sa);
   }
-  sagips_status s = ensure_ws(c, disc_ws + extra);
+  char* ws = nullptr;
+  sagips_status s = acquire_ws(c, from, disc_ws + extra, &ws);
   if (s != SAGIPS_OK) return s;
-  char* ws = static_cast<char*>(c->ws);
-  Timer* tm = timer_of(c);
   hipError_t e;
   if (split) {
     float* xs = reinterpret_cast<float*>(ws + off_x);
@@ -436,6 +486,17 @@ sagips_status sagips_disc_fwd_bwd(sagips_ctx* c, const sagips_mlp* D, const floa
     if (e != hipSuccess) return hip_fail(c, e, "param_grad launch");
   }
   return SAGIPS_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+sagips_status sagips_disc_fwd_bwd(sagips_ctx* c, const sagips_mlp* D, const float* fake_x,
+                                  const sagips_source* fake_src, int64_t n_fake, const float* real_x, int64_t n_real,
+                                  sagips_disc_out* out) {
+  if (!c) return fail(nullptr, SAGIPS_E_INVAL, "ctx is NULL");
+  return disc_call(c, D, fake_x, fake_src, n_fake, real_x, n_real, out, WsFrom{}, timer_of(c));
 }
 
 sagips_status sagips_bootstrap(sagips_ctx* c, const float* data, int64_t n_data, int d, uint64_t seed, uint32_t step,
