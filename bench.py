@@ -2,15 +2,23 @@
 """Benchmark of one rank's SAGIPS step on one MI355X.
 
 A step is one pass of the whole hot path over one batch: theta -> Philox ->
-Kumaraswamy events (sampled inside the kernel) -> discriminator forward on the
-fake and the resident real batch -> BCE -> backward to the weights and to the
-events -> pathwise dx/dtheta -> per-parameter reduction dL_G/dtheta.
+Kumaraswamy events (sampled inside the kernels) -> discriminator forward on
+the fake and the resident real batch -> BCE -> backward to the weights and to
+the events -> pathwise dx/dtheta -> per-parameter reduction dL_G/dtheta.
 
-Default workload: 32 parameter rows x 8,192 events (262,144 fake + 262,144
-real events), discriminator 2-128-128-128-1, fp32.  Prints one JSON line.
+Default: the small-batch workload (32 parameter rows x 8,192 events,
+262,144 fake + 262,144 real events, discriminator 2-128-128-128-1, fp32) is
+the headline; the same JSON line carries a "configs" record with every other
+step workload (the tiny, medium, higher-dim and stress configurations, and the
+stand-alone sampler writing the stress configuration's events to HBM), each
+with its step time, events/s, binding roofline and the CPU oracle's rate.
+
+Timing: W warm-up steps, then the timed region of K steps between
+torch.cuda.synchronize() calls with the library's per-kernel events off; then
+K more steps with them on, for the per-kernel durations of the roofline.
 
   python bench.py [--steps K] [--warmup W] [--gpus 1] [--workload NAME]
-                  [--no-cpu-baseline] [--calibrate-copy]
+                  [--no-cpu-baseline] [--no-configs] [--calibrate-copy]
 """
 from __future__ import annotations
 
@@ -43,6 +51,8 @@ KERNEL_SOURCES = {
     "gen_forward": ["paper_2407_00051_amd/csrc/generator.hip", "paper_2407_00051_amd/csrc/device_math.hpp"],
     "sample_events": ["paper_2407_00051_amd/csrc/sampler.hip", "paper_2407_00051_amd/csrc/device_math.hpp"],
 }
+METRIC = "events/sec per sample->discriminate->backward step; % of HBM / MFMA peak"
+CONFIG_NAMES = ("pr1_tiny", "medium", "higher_dim", "stress", "stress_sample")
 
 
 def _code_text(src: str) -> str:
@@ -108,44 +118,305 @@ def valu_peak_events(valu: float, trans: float) -> float:
     return SIMD_QUAD_CYCLES_PER_S * 64 / quad_cycles_per_64_events
 
 
-def cpu_baseline(w, inp, rows: int, events: int, min_seconds: float = 10.0):
-    """The float64 oracle, as it stands, on the first `rows` parameter rows of the workload."""
-    import numpy as np  # noqa: F401
-    import oracle
-    try:
-        from threadpoolctl import threadpool_info
-        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
-    except Exception:
-        threads = os.cpu_count()
-    th = inp["theta"][:rows]
-    reps = 0
+def kernels_summary(kt: dict) -> dict:
+    return {k: {"launches": n, "avg_ms": t / max(n, 1)} for k, (n, t) in kt.items()}
+
+
+# ---------------------------------------------------------------------------
+# Timing
+
+def time_steps(ctx, step, args, torch, kernel_pass: bool = True):
+    """W warm-up steps; the timed region of K steps with the library's kernel events
+    off, bracketed by torch.cuda.synchronize(); then, unless kernel_pass is False,
+    K more steps with the events on (one pair per launch, on the context's stream),
+    for per-kernel durations.  Returns (ms per timed step, {kernel: (launches, ms)})."""
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
     t0 = time.perf_counter()
-    while True:                      # repeat the sample until about min_seconds of CPU work
-        if w.widths is None:
-            oracle.run_step(th, events, w.fake_seed, critic="quadratic")
-        else:
-            real = oracle.sample(inp["theta_star"], rows * events, w.real_seed)
-            oracle.run_step(th, events, w.fake_seed, inp["W"], inp["b"], real,
-                            features=w.features, bf16=(w.precision == "bf16"))
-        reps += 1
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    kt = {}
+    if kernel_pass:
+        ctx.kernel_times()                      # drop earlier records
+        ctx.set_timing(True)
+        for _ in range(args.steps):
+            step()
+        torch.cuda.synchronize()
+        ctx.set_timing(False)
+        kt = ctx.kernel_times()
+    return (t1 - t0) * 1e3 / args.steps, kt
+
+
+# ---------------------------------------------------------------------------
+# CPU baseline: the float64 oracle, as it stands, on the host cores.  Work is
+# split into tasks (a range of one parameter row's events, with the matching
+# range of the real batch), run by a pool of single-threaded worker processes
+# until the time budget is spent; the rate is events completed / wall time.
+
+_INPUTS = {}
+
+
+def _worker_init():
+    # one BLAS thread per worker process: set before numpy loads its BLAS
+    for v in ("OMP_NUM_THREADS", "OPENBLAS_NUM_THREADS", "MKL_NUM_THREADS", "BLIS_NUM_THREADS"):
+        os.environ[v] = "1"
+    import numpy  # noqa: F401
+    try:
+        from threadpoolctl import threadpool_limits
+        threadpool_limits(1)
+    except Exception:
+        pass
+
+
+def _cpu_task(name: str, row: int, off: int, n: int) -> int:
+    """One task of the oracle's step (runs in a worker process): events
+    [off, off + n) of parameter row `row` of workload `name`."""
+    import numpy as np
+    import oracle
+    from workloads import gen, get
+    if name not in _INPUTS:
+        _INPUTS[name] = gen.make_inputs(get("stress" if name == "stress_sample" else name))
+    inp = _INPUTS[name]
+    w = get("stress" if name == "stress_sample" else name)
+    theta = np.asarray(inp["theta"][row:row + 1], dtype=np.float64)
+    base = row * w.events_per_theta + off
+    if name == "stress_sample":
+        oracle.sample(theta, n, w.fake_seed, counter_base=base)
+    elif w.widths is None:
+        oracle.run_step(theta, n, w.fake_seed, critic="quadratic", counter_base=base)
+    else:
+        real = oracle.sample(inp["theta_star"], n, w.real_seed, counter_base=base)
+        oracle.run_step(theta, n, w.fake_seed, inp["W"], inp["b"], real, features=w.features,
+                        bf16=(w.precision == "bf16"), counter_base=base)
+    return n
+
+
+# events per task: about a second of single-threaded float64 work each
+_TASK_EVENTS = {"pr1_tiny": 4096, "small": 8192, "medium": 2048, "higher_dim": 512, "stress": 1 << 18,
+                "stress_sample": 1 << 18, "paper": 100}
+
+
+class CpuPool:
+    """Worker processes for the oracle's CPU baseline (spawned, so that no GPU state
+    is inherited; each worker runs single-threaded BLAS)."""
+
+    def __init__(self):
+        import concurrent.futures as cf
+        import multiprocessing as mp
+        try:
+            n_cpu = len(os.sched_getaffinity(0))
+        except AttributeError:
+            n_cpu = os.cpu_count() or 1
+        self.workers = max(1, min(16, n_cpu))      # the host share of one GPU
+        self.ex = cf.ProcessPoolExecutor(max_workers=self.workers, mp_context=mp.get_context("spawn"),
+                                         initializer=_worker_init)
+
+    def close(self):
+        self.ex.shutdown(wait=True)
+
+    def rate(self, name: str, seconds: float) -> dict:
+        """Events/s of the oracle's step on workload `name` over at least `seconds`."""
+        import concurrent.futures as cf
+        from workloads import get
+        w = get("stress" if name == "stress_sample" else name)
+        per = min(_TASK_EVENTS[name], w.events_per_theta)
+        tasks = [(r, off, min(per, w.events_per_theta - off)) for r in range(w.n_theta)
+                 for off in range(0, w.events_per_theta, per)]
+        # warm the workers (imports, inputs) outside the timed window
+        list(self.ex.map(_cpu_task, [name] * self.workers, [0] * self.workers, [0] * self.workers,
+                         [min(per, 64)] * self.workers))
+        it = iter(tasks)
+        running, done_events, n_done = set(), 0, 0
+        t0 = time.perf_counter()
+
+        def submit():
+            try:
+                r, off, n = next(it)
+            except StopIteration:
+                return False
+            running.add(self.ex.submit(_cpu_task, name, r, off, n))
+            return True
+
+        for _ in range(self.workers):
+            submit()
+        while running:
+            fin, _ = cf.wait(running, return_when=cf.FIRST_COMPLETED)
+            for f in fin:
+                running.discard(f)
+                done_events += f.result()
+                n_done += 1
+                if time.perf_counter() - t0 < seconds:
+                    submit()
         dt = time.perf_counter() - t0
-        if dt >= min_seconds:
-            break
-    n = rows * events
-    return {"value": reps * n / dt, "unit": "events/s", "cores": int(threads), "kind": "oracle",
-            "sample": f"{rows} of {w.n_theta} parameter rows x {events} events ({n} fake + "
-                      f"{n if w.widths else 0} real events), float64 numpy, {reps} repetition(s) in {dt:.1f} s"}
+        total = w.n_events
+        real = "" if (w.widths is None) else " (and as many real events, sampled in the task)"
+        what = "sampler only" if name == "stress_sample" else (
+            "quadratic critic" if w.widths is None else ("bf16-point" if w.precision == "bf16" else "float64"))
+        return {"value": done_events / dt, "unit": "events/s", "cores": self.workers, "kind": "oracle",
+                "sample": f"{done_events} of the workload's {total} fake events{real}, {n_done} tasks of <= {per} "
+                          f"events of one parameter row, oracle step ({what}, numpy float64) in {self.workers} "
+                          f"single-threaded worker processes, {dt:.1f} s"}
 
 
-def cpu_baseline_bootstrap(w, n_out: int, min_seconds: float = 10.0):
+# ---------------------------------------------------------------------------
+# Step workloads (the five configurations and the paper's shape)
+
+def run_step_workload(name, args, ctx, torch, sg, pool):
+    """Times one step workload; returns a record with its rate, roofline and CPU baseline."""
+    from workloads import gen, get
+    if name == "stress_sample":
+        return run_sample(args, ctx, torch, pool)
+    w = get(name)
+    dev = "cuda:0"
+    inp = gen.make_inputs(w)
+    theta = torch.tensor(inp["theta"], device=dev)
+    theta_star = torch.tensor(inp["theta_star"], device=dev)
+    N = w.n_events
+    rec = {"workload": w.name, "n_theta": w.n_theta, "events_per_theta": w.events_per_theta, "fake_events": N,
+           "real_events": N if w.widths else 0, "widths": list(w.widths) if w.widths else None,
+           "precision": w.precision, "features": w.features}
+
+    if w.widths is not None:
+        W = [torch.tensor(m, device=dev) for m in inp["W"]]
+        bias = [torch.tensor(v, device=dev) for v in inp["b"]]
+        real = ctx.sample_events(theta_star, N, w.real_seed)          # resident real batch (untimed)
+        f32 = dict(dtype=torch.float32, device=dev)
+        outs = {"logits_fake": torch.empty(N, **f32), "logits_real": torch.empty(N, **f32),
+                "loss_d": torch.empty(1, **f32), "loss_g": torch.empty(1, **f32),
+                "dW": [torch.empty_like(m) for m in W], "db": [torch.empty_like(v) for v in bias],
+                "dLg_dx": torch.empty((N, w.d), **f32), "dLg_dtheta": torch.empty((w.n_theta, 2 * w.d), **f32)}
+        src = dict(theta=theta, events_per_theta=w.events_per_theta, seed=w.fake_seed)
+        prec = sg.BF16 if w.precision == "bf16" else sg.F32
+        feats = {"identity": sg.FEAT_IDENTITY, "hd8": sg.FEAT_HD8, "proxy2": sg.FEAT_PROXY2}[w.features]
+
+        def step():
+            ctx.disc_fwd_bwd(W, bias, real, fake_source=src, outputs=outs, precision=prec, features=feats)
+    else:
+        g = torch.empty((w.n_theta, 2 * w.d), dtype=torch.float32, device=dev)
+        loss = torch.empty(1, dtype=torch.float32, device=dev)
+
+        def step():
+            ctx.param_grad(theta, w.events_per_theta, w.fake_seed, out=g, loss_out=loss)
+
+    ms_per_step, kt = time_steps(ctx, step, args, torch)
+    rec["ms_per_step"] = ms_per_step
+    rec["value"] = N / (ms_per_step * 1e-3)
+    rec["unit"] = "events/s"
+    rec["dtype"] = "f32" if w.precision == "f32" else "bf16"
+
+    if w.widths is not None and w.precision == "f32":
+        # the fused fp32 kernel: its algorithmic flops against the fp32 matrix-core peak
+        flops = mlp_flops_per_fake_event(w.widths) * N
+        launches, total_ms = kt["disc_f32_fused"]
+        avg_ms = total_ms / launches
+        achieved = flops / (avg_ms * 1e-3)
+        roof = {"bound": "mfma", "achieved": achieved / 1e12, "peak": PEAK["mfma_f32"] / 1e12, "unit": "TFLOP/s",
+                "frac": achieved / PEAK["mfma_f32"], "traffic": read_traffic("disc_f32_fused", w.name),
+                "step_mfma_frac": flops / (ms_per_step * 1e-3) / PEAK["mfma_f32"],
+                "kernel": "disc_f32_fused", "kernel_avg_ms": avg_ms}
+    elif w.widths is not None:
+        # bf16: the step's algorithmic flops against the bf16 matrix-core peak (the binding
+        # roof of these workloads); the dominant launch kind as a diagnostic
+        flops = mlp_flops_per_fake_event(w.widths) * N
+        step_rate = flops / (ms_per_step * 1e-3)
+        H, NH = w.widths[1], len(w.widths) - 3
+        kinds = [k for k in ("bf16_fwd_chain", "bf16_bwd_chain", "bf16_wgrad") if k in kt]
+        dominant = max(kinds, key=lambda k: kt[k][1])
+        per_step = {k: kt[k][1] / args.steps for k in kinds}
+        roof = {"bound": "mfma", "achieved": step_rate / 1e12, "peak": PEAK["mfma_bf16"] / 1e12, "unit": "TFLOP/s",
+                "frac": step_rate / PEAK["mfma_bf16"], "basis": "step: (12S - 2FH) N algorithmic flop / ms_per_step",
+                "kernel": dominant, "kernel_ms_per_step": per_step}
+        # hidden-product flops of each chain launch kind (NH products of 2 H^2 per row, both batches)
+        hidden = NH * 2 * H * H * (2 * N)
+        for k in ("bf16_fwd_chain", "bf16_bwd_chain"):
+            if k in kt:
+                roof[k + "_hidden_tflops"] = hidden / (per_step[k] * 1e-3) / 1e12
+        if "bf16_wgrad" in kt:
+            # diagnostic: the weight-gradient operands streamed (two bf16 rows of H and e_D per row and layer)
+            wbytes = NH * (2 * N) * (2 * H * 2 + 4)
+            roof["bf16_wgrad_operand_GBps"] = wbytes / (per_step["bf16_wgrad"] * 1e-3) / 1e9
+        tr = [read_traffic(k, w.name) for k in kinds]
+        if all(t is not None for t in tr):
+            roof["step_traffic_bytes"] = sum(t * kt[k][0] / args.steps for t, k in zip(tr, kinds))
+        roof["traffic"] = read_traffic(dominant, w.name)
+    else:
+        # stress: sampler + pathwise + quadratic critic, bound by VALU issue; essential HBM bytes ~ 0
+        launches, total_ms = kt["param_grad"]
+        avg_ms = total_ms / launches
+        achieved = N / (avg_ms * 1e-3)
+        mix = read_valu_mix("param_grad", w.name)
+        peak_ev = valu_peak_events(*mix) if mix else None
+        essential = w.n_theta * 2 * w.d * 4 * 2 + 4        # theta in, dL/dtheta and the loss out
+        roof = {"bound": "alu", "achieved": achieved / 1e9, "peak": peak_ev / 1e9 if mix else None,
+                "unit": "Gevents/s", "frac": achieved / peak_ev if mix else None,
+                "valu_per_event": mix[0] if mix else None, "trans_per_event": mix[1] if mix else None,
+                "hbm_GBps": essential / (avg_ms * 1e-3) / 1e9, "traffic": read_traffic("param_grad", w.name),
+                "kernel": "param_grad", "kernel_avg_ms": avg_ms}
+    roof["kernels"] = kernels_summary(kt)
+    rec["roofline"] = roof
+    if pool is not None:
+        rec["cpu_baseline"] = pool.rate(name, args.cpu_seconds)
+    return rec
+
+
+def run_sample(args, ctx, torch, pool):
+    """The stand-alone sampler on the stress configuration: theta -> Philox ->
+    Kumaraswamy events written to HBM ([N][d] fp32), the path that feeds a
+    buffered discriminator."""
+    from workloads import gen, get
+    w = get("stress")
+    dev = "cuda:0"
+    inp = gen.make_inputs(w)
+    theta = torch.tensor(inp["theta"], device=dev)
+    N = w.n_events
+    x = torch.empty((N, w.d), dtype=torch.float32, device=dev)
+
+    def step():
+        ctx.sample_events(theta, w.events_per_theta, w.fake_seed, out=x)
+
+    ms_per_step, kt = time_steps(ctx, step, args, torch)
+    launches, total_ms = kt["sample_events"]
+    avg_ms = total_ms / launches
+    bytes_per_launch = N * w.d * 4 + w.n_theta * 2 * w.d * 4     # events written, theta read
+    achieved = bytes_per_launch / (avg_ms * 1e-3)
+    mix = read_valu_mix("sample_events", "stress_sample")
+    rec = {"workload": "stress_sample", "n_theta": w.n_theta, "events_per_theta": w.events_per_theta,
+           "events": N, "d": w.d, "ms_per_step": ms_per_step, "value": N / (ms_per_step * 1e-3),
+           "unit": "events/s", "dtype": "f32",
+           "roofline": {"bound": "hbm", "achieved": achieved / 1e9, "peak": PEAK["hbm"] / 1e9, "unit": "GB/s",
+                        "frac": achieved / PEAK["hbm"], "traffic": read_traffic("sample_events", "stress_sample"),
+                        "valu_frac": (N / (avg_ms * 1e-3)) / valu_peak_events(*mix) if mix else None,
+                        "kernel": "sample_events", "kernel_avg_ms": avg_ms, "kernels": kernels_summary(kt)}}
+    if pool is not None:
+        rec["cpu_baseline"] = pool.rate("stress_sample", args.cpu_seconds)
+    return rec
+
+
+def step_line(rec, args):
+    """The driver's JSON line for a step workload record."""
+    line = {"metric": METRIC, "value": rec["value"], "unit": "events/s", "n_gpus": 1, "steps": args.steps,
+            "warmup": args.warmup, "ms_per_step": rec["ms_per_step"], "higher_is_better": True, "scaling": "weak",
+            "vs_baseline": None, "dtype": rec["dtype"],
+            "data": "synthetic (seeded theta, Philox-sampled events, Xavier-initialised weights)",
+            "config": {k: rec[k] for k in ("workload", "n_theta", "events_per_theta", "fake_events", "real_events",
+                                           "widths", "precision", "features") if k in rec},
+            "roofline": rec["roofline"]}
+    line["config"]["parallelism"] = "single GPU"
+    if "cpu_baseline" in rec:
+        line["cpu_baseline"] = rec["cpu_baseline"]
+    return line
+
+
+# ---------------------------------------------------------------------------
+# The other workloads: bootstrap draw, ensemble response, GAN training step
+
+def cpu_baseline_bootstrap(w, n_out: int, min_seconds: float):
     """The oracle's draw, as it stands, of n_out rows from a pool of 2 n_out events."""
     import numpy as np
     import oracle
-    try:
-        from threadpoolctl import threadpool_info
-        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
-    except Exception:
-        threads = os.cpu_count()
     pool = oracle.sample(np.asarray([w.theta_star], dtype=np.float32), 2 * n_out, w.pool_seed).astype(np.float32)
     draw = oracle.bootstrap_row_order if w.row_order else oracle.bootstrap
     reps, t0 = 0, time.perf_counter()
@@ -155,9 +426,9 @@ def cpu_baseline_bootstrap(w, n_out: int, min_seconds: float = 10.0):
         dt = time.perf_counter() - t0
         if dt >= min_seconds:
             break
-    return {"value": reps * n_out / dt, "unit": "draws/s", "cores": int(threads), "kind": "oracle",
+    return {"value": reps * n_out / dt, "unit": "draws/s", "cores": 1, "kind": "oracle",
             "sample": f"{n_out} draws from a pool of {2 * n_out} events (of the workload's {w.n_out} from "
-                      f"{w.n_data}), numpy, {reps} repetition(s) in {dt:.1f} s"}
+                      f"{w.n_data}), numpy, one process, {reps} repetition(s) in {dt:.1f} s"}
 
 
 def bench_bootstrap(args, w, ctx, torch):
@@ -171,20 +442,7 @@ def bench_bootstrap(args, w, ctx, torch):
         ctx.bootstrap(pool, w.n_out, w.seed, it[0], out=out, row_order=w.row_order)
         it[0] += 1
 
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
-    ctx.kernel_times()
-    ctx.set_timing(True)
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for _ in range(args.steps):
-        step()
-    torch.cuda.synchronize()
-    t1 = time.perf_counter()
-    ctx.set_timing(False)
-    kt = ctx.kernel_times()
-    ms_per_step = (t1 - t0) * 1e3 / args.steps
+    ms_per_step, kt = time_steps(ctx, step, args, torch)
     name = "bootstrap_rows" if w.row_order else "bootstrap"
     launches, total_ms = kt[name]       # the row order times its five kernels as one
     avg_ms = total_ms / launches
@@ -193,8 +451,7 @@ def bench_bootstrap(args, w, ctx, torch):
     achieved = bytes_per_launch / (avg_ms * 1e-3)
     roof = {"bound": "hbm", "achieved": achieved / 1e9, "peak": PEAK["hbm"] / 1e9, "unit": "GB/s",
             "frac": achieved / PEAK["hbm"], "traffic": read_traffic(name, w.name),
-            "kernel": name, "kernel_avg_ms": avg_ms,
-            "kernels": {k: {"launches": n, "avg_ms": t / max(n, 1)} for k, (n, t) in kt.items()}}
+            "kernel": name, "kernel_avg_ms": avg_ms, "kernels": kernels_summary(kt)}
     line = {
         "metric": "draws/sec of the bootstrap sub-sample of the real data; % of HBM peak",
         "value": w.n_out / (ms_per_step * 1e-3), "unit": "draws/s", "n_gpus": 1, "steps": args.steps,
@@ -206,9 +463,8 @@ def bench_bootstrap(args, w, ctx, torch):
         "roofline": roof,
     }
     if not args.no_cpu_baseline:
-        line["cpu_baseline"] = cpu_baseline_bootstrap(w, min(w.n_out, 1 << 20))
-    ctx.close()
-    print(json.dumps(line), flush=True)
+        line["cpu_baseline"] = cpu_baseline_bootstrap(w, min(w.n_out, 1 << 20), args.cpu_seconds)
+    return line
 
 
 def gen_flops_per_row(widths) -> int:
@@ -216,7 +472,7 @@ def gen_flops_per_row(widths) -> int:
     return 2 * sum(a * b for a, b in zip(widths[:-1], widths[1:]))
 
 
-def cpu_baseline_ensemble(w, W, b, n, min_seconds: float = 10.0):
+def cpu_baseline_ensemble(w, W, b, n, min_seconds: float):
     """The oracle's ensemble response (every member's forward, then the statistics), as it stands."""
     import numpy as np
     import oracle
@@ -235,7 +491,7 @@ def cpu_baseline_ensemble(w, W, b, n, min_seconds: float = 10.0):
         if dt >= min_seconds:
             break
     return {"value": reps * M * w.k / dt, "unit": "member-predictions/s", "cores": int(threads), "kind": "oracle",
-            "sample": f"{M} of the {w.n_members} members x {w.k} noise vectors, float64 numpy, "
+            "sample": f"{M} of the {w.n_members} members x {w.k} noise vectors, float64 numpy (BLAS threads), "
                       f"{reps} repetition(s) in {dt:.1f} s"}
 
 
@@ -254,28 +510,14 @@ def bench_ensemble(args, w, ctx, torch):
     def step():
         ctx.ensemble_response(Wd, bd, nd, p_true=pt)
 
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
-    ctx.kernel_times()
-    ctx.set_timing(True)
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for _ in range(args.steps):
-        step()
-    torch.cuda.synchronize()
-    t1 = time.perf_counter()
-    ctx.set_timing(False)
-    kt = ctx.kernel_times()
-    ms_per_step = (t1 - t0) * 1e3 / args.steps
+    ms_per_step, kt = time_steps(ctx, step, args, torch)
     launches, total_ms = kt["gen_forward"]
     avg_ms = total_ms / launches
     flops = gen_flops_per_row(w.widths) * w.n_members * w.k
     achieved = flops / (avg_ms * 1e-3)
     roof = {"bound": "mfma", "achieved": achieved / 1e12, "peak": PEAK["mfma_f32"] / 1e12, "unit": "TFLOP/s",
             "frac": achieved / PEAK["mfma_f32"], "traffic": read_traffic("gen_forward", w.name),
-            "kernel": "gen_forward", "kernel_avg_ms": avg_ms,
-            "kernels": {k: {"launches": c, "avg_ms": t / max(c, 1)} for k, (c, t) in kt.items()}}
+            "kernel": "gen_forward", "kernel_avg_ms": avg_ms, "kernels": kernels_summary(kt)}
     line = {
         "metric": "member-predictions/sec of the ensemble response (p_hat, sigma, r_hat); % of fp32 MFMA peak",
         "value": w.n_members * w.k / (ms_per_step * 1e-3), "unit": "member-predictions/s", "n_gpus": 1,
@@ -287,12 +529,11 @@ def bench_ensemble(args, w, ctx, torch):
         "roofline": roof,
     }
     if not args.no_cpu_baseline:
-        line["cpu_baseline"] = cpu_baseline_ensemble(w, W, b, n)
-    ctx.close()
-    print(json.dumps(line), flush=True)
+        line["cpu_baseline"] = cpu_baseline_ensemble(w, W, b, n, args.cpu_seconds)
+    return line
 
 
-def cpu_baseline_train(w, rows: int, min_seconds: float = 10.0):
+def cpu_baseline_train(w, rows: int, min_seconds: float):
     """The oracle's whole GAN step, as it stands, on `rows` of the k noise vectors."""
     import numpy as np
     import oracle
@@ -319,7 +560,7 @@ def cpu_baseline_train(w, rows: int, min_seconds: float = 10.0):
             break
     return {"value": reps * N / dt, "unit": "events/s", "cores": int(threads), "kind": "oracle",
             "sample": f"{rows} of {w.k} parameter samples x {w.events_per_theta} events per step ({N} fake + {N} "
-                      f"bootstrapped reference events), float64 numpy, {reps} step(s) in {dt:.1f} s"}
+                      f"bootstrapped reference events), float64 numpy (BLAS threads), {reps} step(s) in {dt:.1f} s"}
 
 
 def bench_train(args, w, ctx, torch, sg):
@@ -338,22 +579,16 @@ def bench_train(args, w, ctx, torch, sg):
                    [torch.tensor(x, device=dev) for x in DW], [torch.tensor(x, device=dev) for x in Db], pool,
                    w.k, w.events_per_theta, fake_seed=w.seed, boot_seed=w.seed + 5)
     rng = np.random.default_rng(w.seed + 22)
-    noise = torch.tensor(rng.standard_normal((args.warmup + args.steps, w.k, w.g_widths[0])).astype(np.float32),
+    total = args.warmup + 2 * args.steps
+    noise = torch.tensor(rng.standard_normal((total, w.k, w.g_widths[0])).astype(np.float32),
                          device=dev)                                    # resident before timing
-    for i in range(args.warmup):
-        loop.step(noise[i])
-    torch.cuda.synchronize()
-    ctx.kernel_times()
-    ctx.set_timing(True)
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for i in range(args.steps):
-        loop.step(noise[args.warmup + i])
-    torch.cuda.synchronize()
-    t1 = time.perf_counter()
-    ctx.set_timing(False)
-    kt = ctx.kernel_times()
-    ms_per_step = (t1 - t0) * 1e3 / args.steps
+    it = [0]
+
+    def step():
+        loop.step(noise[it[0]])
+        it[0] += 1
+
+    ms_per_step, kt = time_steps(ctx, step, args, torch)
     launches, total_ms = kt["disc_f32_fused"]
     avg_ms = total_ms / launches
     flops = mlp_flops_per_fake_event(w.d_widths) * N
@@ -362,8 +597,7 @@ def bench_train(args, w, ctx, torch, sg):
     roof = {"bound": "mfma", "achieved": achieved / 1e12, "peak": PEAK["mfma_f32"] / 1e12, "unit": "TFLOP/s",
             "frac": achieved / PEAK["mfma_f32"], "traffic": read_traffic("disc_f32_fused", w.name),
             "step_mfma_frac": (flops + g_flops) / (ms_per_step * 1e-3) / PEAK["mfma_f32"],
-            "kernel": "disc_f32_fused", "kernel_avg_ms": avg_ms,
-            "kernels": {k: {"launches": c, "avg_ms": t / max(c, 1)} for k, (c, t) in kt.items()}}
+            "kernel": "disc_f32_fused", "kernel_avg_ms": avg_ms, "kernels": kernels_summary(kt)}
     line = {
         "metric": "events/sec per GAN training step (generator, bootstrap, discriminator, backward, Adam); "
                   "% of fp32 MFMA peak",
@@ -377,87 +611,19 @@ def bench_train(args, w, ctx, torch, sg):
         "roofline": roof,
     }
     if not args.no_cpu_baseline:
-        line["cpu_baseline"] = cpu_baseline_train(w, min(args.cpu_rows, w.k))
-    ctx.close()
-    print(json.dumps(line), flush=True)
-
-
-def bench_sample(args, w, ctx, torch):
-    """Steps of the stand-alone sampler on the stress configuration: theta -> Philox ->
-    Kumaraswamy events written to HBM ([N][d] fp32), the path that feeds a buffered
-    discriminator."""
-    from workloads import gen
-    dev = "cuda:0"
-    inp = gen.make_inputs(w)
-    theta = torch.tensor(inp["theta"], device=dev)
-    N = w.n_events
-    x = torch.empty((N, w.d), dtype=torch.float32, device=dev)
-
-    def step():
-        ctx.sample_events(theta, w.events_per_theta, w.fake_seed, out=x)
-
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
-    ctx.kernel_times()
-    ctx.set_timing(True)
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for _ in range(args.steps):
-        step()
-    torch.cuda.synchronize()
-    t1 = time.perf_counter()
-    ctx.set_timing(False)
-    kt = ctx.kernel_times()
-    ms_per_step = (t1 - t0) * 1e3 / args.steps
-    launches, total_ms = kt["sample_events"]
-    avg_ms = total_ms / launches
-    bytes_per_launch = N * w.d * 4 + w.n_theta * 2 * w.d * 4     # events written, theta read
-    achieved = bytes_per_launch / (avg_ms * 1e-3)
-    roof = {"bound": "hbm", "achieved": achieved / 1e9, "peak": PEAK["hbm"] / 1e9, "unit": "GB/s",
-            "frac": achieved / PEAK["hbm"], "traffic": read_traffic("sample_events", "stress_sample"),
-            "kernel": "sample_events", "kernel_avg_ms": avg_ms,
-            "kernels": {k: {"launches": c, "avg_ms": t / max(c, 1)} for k, (c, t) in kt.items()}}
-    line = {
-        "metric": "events/sec of the stand-alone sampler (theta -> Philox -> Kumaraswamy events in HBM); "
-                  "% of HBM peak",
-        "value": N / (ms_per_step * 1e-3), "unit": "events/s", "n_gpus": 1, "steps": args.steps,
-        "warmup": args.warmup, "ms_per_step": ms_per_step, "higher_is_better": True, "scaling": "weak",
-        "vs_baseline": None, "dtype": "f32", "data": "synthetic (seeded theta, Philox-sampled events)",
-        "config": {"workload": "stress_sample", "n_theta": w.n_theta, "events_per_theta": w.events_per_theta,
-                   "events": N, "d": w.d, "parallelism": "single GPU"},
-        "roofline": roof,
-    }
-    if not args.no_cpu_baseline:
-        import numpy as np
-        import oracle
-        try:
-            from threadpoolctl import threadpool_info
-            threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
-        except Exception:
-            threads = os.cpu_count()
-        n = 1 << 20
-        reps, t0 = 0, time.perf_counter()
-        while True:
-            oracle.sample(np.asarray(inp["theta"][:1], dtype=np.float64), n, w.fake_seed, counter_base=reps * n)
-            reps += 1
-            dt = time.perf_counter() - t0
-            if dt >= 10.0:
-                break
-        line["cpu_baseline"] = {"value": reps * n / dt, "unit": "events/s", "cores": int(threads), "kind": "oracle",
-                                "sample": f"1 of {w.n_theta} parameter rows x {n} events per repetition, float64 "
-                                          f"numpy, {reps} repetition(s) in {dt:.1f} s"}
-    ctx.close()
-    print(json.dumps(line), flush=True)
+        line["cpu_baseline"] = cpu_baseline_train(w, min(args.cpu_rows, w.k), args.cpu_seconds)
+    return line
 
 
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="small")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-configs", action="store_true", help="only the headline workload")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0, help="time budget of each CPU baseline")
     ap.add_argument("--cpu-rows", type=int, default=32)
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="also run one 1 GiB device copy (for counter calibration runs)")
@@ -471,9 +637,8 @@ def main():
     import torch
 
     import paper_2407_00051_amd as sg
-    from workloads import gen, get
+    from workloads import get
 
-    w = get("stress" if args.workload == "stress_sample" else args.workload)
     torch.cuda.set_device(0)
     ctx = sg.Context(0)
     dev = "cuda:0"
@@ -485,133 +650,46 @@ def main():
         b.copy_(a)
         torch.cuda.synchronize()
         del a, b
-    if args.workload == "stress_sample":
-        return bench_sample(args, w, ctx, torch)
-    if hasattr(w, "n_data"):
-        return bench_bootstrap(args, w, ctx, torch)
-    if hasattr(w, "n_members"):
-        return bench_ensemble(args, w, ctx, torch)
-    if hasattr(w, "g_widths"):
-        return bench_train(args, w, ctx, torch, sg)
-    inp = gen.make_inputs(w)
-    theta = torch.tensor(inp["theta"], device=dev)
-    theta_star = torch.tensor(inp["theta_star"], device=dev)
-    N = w.n_events
-
-    if w.widths is not None:
-        W = [torch.tensor(m, device=dev) for m in inp["W"]]
-        bias = [torch.tensor(v, device=dev) for v in inp["b"]]
-        real = ctx.sample_events(theta_star, N, w.real_seed)          # resident real batch (untimed)
-        f32 = dict(dtype=torch.float32, device=dev)
-        outs = {"logits_fake": torch.empty(N, **f32), "logits_real": torch.empty(N, **f32),
-                "loss_d": torch.empty(1, **f32), "loss_g": torch.empty(1, **f32),
-                "dW": [torch.empty_like(m) for m in W], "db": [torch.empty_like(v) for v in bias],
-                "dLg_dx": torch.empty((N, w.d), **f32), "dLg_dtheta": torch.empty((w.n_theta, 2 * w.d), **f32)}
-        src = dict(theta=theta, events_per_theta=w.events_per_theta, seed=w.fake_seed)
-        prec = sg.BF16 if w.precision == "bf16" else sg.F32
-        feats = {"identity": sg.FEAT_IDENTITY, "hd8": sg.FEAT_HD8, "proxy2": sg.FEAT_PROXY2}[w.features]
-
-        def step():
-            ctx.disc_fwd_bwd(W, bias, real, fake_source=src, outputs=outs, precision=prec, features=feats)
-
-        if prec == sg.F32:
-            dominant = "disc_f32_fused"
-            flops_per_launch = mlp_flops_per_fake_event(w.widths) * N
-        else:
-            # The bf16 step runs three kinds of launches per chunk of rows: the forward
-            # chain, the backward chain and one weight-gradient product per hidden layer.
-            # Each kind carries NH hidden products of 2 H^2 flops per row over the fake and
-            # the real batch per step; the dominant kind is chosen after timing.
-            dominant = None
-            H, NH = w.widths[1], len(w.widths) - 3
-            flops_per_step_kind = NH * 2 * H * H * (2 * N)
-            flops_per_launch = None
-        bound, unit, peak = "mfma", "TFLOP/s", PEAK["mfma_f32" if prec == sg.F32 else "mfma_bf16"]
-        dtype = "f32" if prec == sg.F32 else "bf16"
-    else:
-        g = torch.empty((w.n_theta, 2 * w.d), dtype=torch.float32, device=dev)
-        loss = torch.empty(1, dtype=torch.float32, device=dev)
-
-        def step():
-            ctx.param_grad(theta, w.events_per_theta, w.fake_seed, out=g, loss_out=loss)
-
-        dominant = "param_grad"
-        flops_per_launch = None
-        bound, unit, peak = "alu", "Gevents/s", None
-        dtype = "f32"
-
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
-    ctx.kernel_times()                      # drop warm-up records
-    ctx.set_timing(True)
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for _ in range(args.steps):
-        step()
-    torch.cuda.synchronize()
-    t1 = time.perf_counter()
-    ctx.set_timing(False)
-    kt = ctx.kernel_times()
-    ms_per_step = (t1 - t0) * 1e3 / args.steps
-    value = N / (ms_per_step * 1e-3)
-
-    bytes_per_launch = None
-    if dominant is None:
-        kinds = [k for k in ("bf16_fwd_chain", "bf16_bwd_chain", "bf16_wgrad") if k in kt]
-        dominant = max(kinds, key=lambda k: kt[k][1])
-        launches_per_step = kt[dominant][0] / args.steps
-        if dominant == "bf16_wgrad":
-            # streams its two operands (bf16 rows of H) and e_D once per launch and
-            # writes one H x H (+ H) fp32 partial per row slice: bound by HBM
-            rows = 2 * N / launches_per_step * NH
-            slices = max(1, torch.cuda.get_device_properties(0).multi_processor_count // ((H // 256) ** 2))
-            bytes_per_launch = rows * (2 * H * 2 + 4) + slices * (H * H + H) * 4
-            bound, unit, peak = "hbm", "GB/s", PEAK["hbm"]
-        else:
-            flops_per_launch = flops_per_step_kind / launches_per_step
-    launches, total_ms = kt.get(dominant, (0, 0.0))
-    if launches == 0:
-        raise RuntimeError(f"no timed launches of {dominant}")
-    avg_ms = total_ms / launches
-    if bytes_per_launch is not None:
-        achieved = bytes_per_launch / (avg_ms * 1e-3)
-        roof = {"bound": bound, "achieved": achieved / 1e9, "peak": peak / 1e9, "unit": unit,
-                "frac": achieved / peak}
-    elif flops_per_launch is not None:
-        achieved = flops_per_launch / (avg_ms * 1e-3)
-        roof = {"bound": bound, "achieved": achieved / 1e12, "peak": peak / 1e12, "unit": unit,
-                "frac": achieved / peak}
-    else:
-        achieved = N / (avg_ms * 1e-3)
-        mix = read_valu_mix(dominant, w.name)
-        peak_ev = valu_peak_events(*mix) if mix else None
-        roof = {"bound": bound, "achieved": achieved / 1e9, "peak": peak_ev / 1e9 if mix else None, "unit": unit,
-                "frac": achieved / peak_ev if mix else None,
-                "valu_per_event": mix[0] if mix else None, "trans_per_event": mix[1] if mix else None}
-    if w.widths is not None:
-        mpeak = PEAK["mfma_f32" if w.precision == "f32" else "mfma_bf16"]
-        roof["step_mfma_frac"] = mlp_flops_per_fake_event(w.widths) * N / (ms_per_step * 1e-3) / mpeak
-    tr = read_traffic(dominant, w.name)
-    roof["traffic"] = tr
-    roof["kernel"] = dominant
-    roof["kernel_avg_ms"] = avg_ms
-    roof["kernels"] = {k: {"launches": n, "avg_ms": t / max(n, 1)} for k, (n, t) in kt.items()}
-
-    line = {
-        "metric": "events/sec per sample->discriminate->backward step; % of HBM / MFMA peak",
-        "value": value, "unit": "events/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
-        "ms_per_step": ms_per_step, "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
-        "dtype": dtype, "data": "synthetic (seeded theta, Philox-sampled events, Xavier-initialised weights)",
-        "config": {"workload": w.name, "n_theta": w.n_theta, "events_per_theta": w.events_per_theta,
-                   "fake_events": N, "real_events": N if w.widths else 0,
-                   "widths": list(w.widths) if w.widths else None, "precision": w.precision,
-                   "features": w.features, "parallelism": "single GPU"},
-        "roofline": roof,
-    }
-    if not args.no_cpu_baseline:
-        ev = w.events_per_theta if w.widths is not None else min(w.events_per_theta, 1 << 20)
-        line["cpu_baseline"] = cpu_baseline(w, inp, min(args.cpu_rows, w.n_theta), ev)
+    name = args.workload
+    line = None
+    if name not in ("stress_sample",) + tuple(CONFIG_NAMES) + ("small", "paper"):
+        w = get(name)
+        if hasattr(w, "n_data"):
+            line = bench_bootstrap(args, w, ctx, torch)
+        elif hasattr(w, "n_members"):
+            line = bench_ensemble(args, w, ctx, torch)
+        elif hasattr(w, "g_widths"):
+            line = bench_train(args, w, ctx, torch, sg)
+    if line is None:
+        pool = None if args.no_cpu_baseline else CpuPool()
+        try:
+            rec = run_step_workload(name, args, ctx, torch, sg, pool)
+            if name == "stress_sample":
+                line = {"metric": "events/sec of the stand-alone sampler (theta -> Philox -> Kumaraswamy events in "
+                                  "HBM); % of HBM peak",
+                        "value": rec["value"], "unit": "events/s", "n_gpus": 1, "steps": args.steps,
+                        "warmup": args.warmup, "ms_per_step": rec["ms_per_step"], "higher_is_better": True,
+                        "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+                        "data": "synthetic (seeded theta, Philox-sampled events)",
+                        "config": {k: rec[k] for k in ("workload", "n_theta", "events_per_theta", "events", "d")},
+                        "roofline": rec["roofline"]}
+                line["config"]["parallelism"] = "single GPU"
+                if "cpu_baseline" in rec:
+                    line["cpu_baseline"] = rec["cpu_baseline"]
+            else:
+                line = step_line(rec, args)
+            if name == "small" and not args.no_configs:
+                # every other configuration, in the same run and the same protocol
+                line["configs"] = {}
+                for other in CONFIG_NAMES:
+                    r = run_step_workload(other, args, ctx, torch, sg, pool)
+                    line["configs"][other] = r
+                    torch.cuda.empty_cache()
+                    print(f"# {other}: {r['ms_per_step']:.3f} ms/step, {r['value']:.3e} events/s", file=sys.stderr,
+                          flush=True)
+        finally:
+            if pool is not None:
+                pool.close()
     ctx.close()
     print(json.dumps(line), flush=True)
 
