@@ -38,6 +38,7 @@
 #ifndef SAGIPS_H
 #define SAGIPS_H
 
+#include <stddef.h>
 #include <stdint.h>
 
 #ifdef __cplusplus
@@ -180,6 +181,26 @@ sagips_status sagips_sample_events(sagips_ctx* ctx, const sagips_source* src, fl
 sagips_status sagips_disc_fwd_bwd(sagips_ctx* ctx, const sagips_mlp* D, const float* fake_x,
                                   const sagips_source* fake_src, int64_t n_fake,
                                   const float* real_x, int64_t n_real, sagips_disc_out* out);
+
+/* 2b. The same step for callers that cannot allocate device memory: code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc.  Arguments, results and errors are those of
+ * sagips_disc_fwd_bwd (the same kernels), except:
+ *   - the workspace is a fixed scratch array of
+ *     sagips_noalloc_scratch_bytes() bytes (64 MiB) per device, reserved by
+ *     the library when it is loaded and held until the process ends; this
+ *     call never allocates (no hipMalloc, hipFree or allocating library call);
+ *   - a call whose workspace would exceed it returns SAGIPS_E_INVAL before
+ *     launching anything (the small-batch workload needs about 35 MB, the
+ *     paper's 2-128-128-128-128-1 shape about 52 MB);
+ *   - every call on one device shares that device's array and leaves its
+ *     contents behind: calls that overlap on one device (several streams or
+ *     contexts) race and must be ordered by the caller;
+ *   - per-kernel timing (sagips_set_timing) does not apply to it.          */
+sagips_status sagips_disc_fwd_bwd_noalloc(sagips_ctx* ctx, const sagips_mlp* D, const float* fake_x,
+                                          const sagips_source* fake_src, int64_t n_fake,
+                                          const float* real_x, int64_t n_real, sagips_disc_out* out);
+size_t sagips_noalloc_scratch_bytes(void);
 
 /* 3. dL/dx -> pathwise dx/dtheta -> per-parameter reduction (paper Sec. II,
  * gradient of the objective with respect to p through the sampler).  The

@@ -27,7 +27,7 @@ EXPORTED = ("sagips_create", "sagips_destroy", "sagips_set_stream", "sagips_set_
             "sagips_last_error", "sagips_set_timing",
             "sagips_kernel_times", "sagips_sample_events", "sagips_disc_fwd_bwd", "sagips_param_grad",
             "sagips_bootstrap", "sagips_bootstrap_rows", "sagips_gen_forward", "sagips_gen_backward", "sagips_ensemble_response",
-            "sagips_adam_step")
+            "sagips_adam_step", "sagips_disc_fwd_bwd_noalloc", "sagips_noalloc_scratch_bytes")
 
 
 class SagipsError(RuntimeError):
@@ -91,6 +91,9 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.sagips_sample_events.argtypes = [vp, ctypes.POINTER(Source), vp, vp]
     lib.sagips_disc_fwd_bwd.argtypes = [vp, ctypes.POINTER(Mlp), vp, ctypes.POINTER(Source), i64, vp, i64,
                                         ctypes.POINTER(DiscOut)]
+    lib.sagips_disc_fwd_bwd_noalloc.argtypes = lib.sagips_disc_fwd_bwd.argtypes
+    lib.sagips_noalloc_scratch_bytes.argtypes = []
+    lib.sagips_noalloc_scratch_bytes.restype = ctypes.c_size_t
     lib.sagips_param_grad.argtypes = [vp, ctypes.POINTER(Source), i32, vp, vp, vp]
     lib.sagips_bootstrap.argtypes = [vp, vp, i64, i32, ctypes.c_uint64, ctypes.c_uint32, i64, vp, vp]
     lib.sagips_bootstrap_rows.argtypes = lib.sagips_bootstrap.argtypes
@@ -104,7 +107,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
                  "sagips_set_timing",
                  "sagips_kernel_times", "sagips_sample_events", "sagips_disc_fwd_bwd", "sagips_param_grad",
                  "sagips_bootstrap", "sagips_bootstrap_rows", "sagips_gen_forward", "sagips_gen_backward", "sagips_ensemble_response",
-                 "sagips_adam_step"):
+                 "sagips_adam_step", "sagips_disc_fwd_bwd_noalloc"):
         getattr(lib, name).restype = ctypes.c_int
     _lib = lib
     return lib
@@ -382,9 +385,12 @@ class Context:
     def disc_fwd_bwd(self, W: Sequence, b: Sequence, real_x, fake_x=None, fake_source: Optional[dict] = None,
                      precision: int = F32, features: int = FEAT_IDENTITY, slope: float = 0.2,
                      want_logits: bool = True, want_grads: bool = True, want_dx: bool = True,
-                     want_dtheta: bool = True, outputs: Optional[dict] = None) -> dict:
+                     want_dtheta: bool = True, outputs: Optional[dict] = None, no_alloc: bool = False) -> dict:
         """One discriminator step.  fake_source = dict(theta=, events_per_theta=, seed=[, counter_base=, stream=])
-        samples the fake events inside the kernel and also returns dLg_dtheta."""
+        samples the fake events inside the kernel and also returns dLg_dtheta.  With no_alloc the
+        library takes its workspace from its fixed per-device scratch (sagips_disc_fwd_bwd_noalloc)
+        instead of allocating; pass every output in `outputs` so that the binding allocates nothing
+        either."""
         import torch
         self._enter()
         n_layers = len(W)
@@ -446,7 +452,8 @@ class Context:
             for l in range(n_layers):
                 out.dW[l] = o["dW"][l].data_ptr()
                 out.db[l] = o["db"][l].data_ptr()
-        st = self.lib.sagips_disc_fwd_bwd(self.h, ctypes.byref(mlp), _ptr(fake_x),
+        fn = self.lib.sagips_disc_fwd_bwd_noalloc if no_alloc else self.lib.sagips_disc_fwd_bwd
+        st = fn(self.h, ctypes.byref(mlp), _ptr(fake_x),
                                           ctypes.byref(src) if src is not None else None, n_fake,
                                           real_x.data_ptr(), n_real, ctypes.byref(out))
         self._check(st)

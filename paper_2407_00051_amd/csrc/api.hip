@@ -7,6 +7,7 @@
 #include <string.h>
 
 #include <map>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -15,9 +16,35 @@
 
 using namespace sagips;
 
+// Workspace of sagips_disc_fwd_bwd_noalloc: one array per device, which every
+// call of that entry point on the device shares (calls that overlap on one
+// device race on it).  In host code `scratch` names a host-side stand-in, not
+// device memory: kernels only ever receive the device address taken with
+// hipGetSymbolAddress in sagips_create.
+constexpr size_t kScratchBytes = (size_t)64 << 20;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
 namespace {
 
 thread_local std::string g_create_error = "no error";
+
+// Device address of `scratch` per device (taken once, with that device current).
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+char* g_scratch_ptr[kMaxDevices] = {};
+hipError_t g_scratch_err[kMaxDevices] = {};
+
+hipError_t scratch_address(int dev, char** ptr) {
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev] && g_scratch_err[dev] == hipSuccess) {
+    void* p = nullptr;
+    hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e == hipSuccess && p) g_scratch_ptr[dev] = static_cast<char*>(p);
+    else g_scratch_err[dev] = e != hipSuccess ? e : hipErrorInvalidSymbol;
+  }
+  *ptr = g_scratch_ptr[dev];
+  return g_scratch_err[dev];
+}
 
 struct EventTimer final : Timer {
   struct Rec {
@@ -261,6 +288,15 @@ sagips_status sagips_create(sagips_ctx** out, int hip_device, void* hip_stream) 
   if (e != hipSuccess) return fail(nullptr, SAGIPS_E_HIP, "hipGetDeviceProperties: %s", hipGetErrorString(e));
   if (strncmp(prop.gcnArchName, "gfx950", 6) != 0)
     return fail(nullptr, SAGIPS_E_ARCH, "device %d is %s; this library is built for gfx950 only", hip_device, prop.gcnArchName);
+  if (hip_device >= kMaxDevices) return fail(nullptr, SAGIPS_E_INVAL, "device %d beyond %d devices", hip_device, kMaxDevices);
+  {
+    // The scratch array's address on this device, for the no-allocation entry
+    // point.  A failure is kept (and reported by that entry point); the other
+    // calls do not use the array.
+    DeviceGuard g(hip_device);
+    char* p = nullptr;
+    (void)scratch_address(hip_device, &p);
+  }
   sagips_ctx* c = new (std::nothrow) sagips_ctx;
   if (!c) return fail(nullptr, SAGIPS_E_NOMEM, "context allocation failed");
   c->device = hip_device;
@@ -498,6 +534,20 @@ sagips_status sagips_disc_fwd_bwd(sagips_ctx* c, const sagips_mlp* D, const floa
   if (!c) return fail(nullptr, SAGIPS_E_INVAL, "ctx is NULL");
   return disc_call(c, D, fake_x, fake_src, n_fake, real_x, n_real, out, WsFrom{}, timer_of(c));
 }
+
+sagips_status sagips_disc_fwd_bwd_noalloc(sagips_ctx* c, const sagips_mlp* D, const float* fake_x,
+                                          const sagips_source* fake_src, int64_t n_fake, const float* real_x,
+                                          int64_t n_real, sagips_disc_out* out) {
+  if (!c) return fail(nullptr, SAGIPS_E_INVAL, "ctx is NULL");
+  WsFrom from;
+  hipError_t e = scratch_address(c->device, &from.fixed);
+  if (e != hipSuccess || !from.fixed) return hip_fail(c, e != hipSuccess ? e : hipErrorInvalidSymbol, "scratch address");
+  from.fixed_cap = kScratchBytes;
+  // no per-kernel timing here: its events are created on demand
+  return disc_call(c, D, fake_x, fake_src, n_fake, real_x, n_real, out, from, nullptr);
+}
+
+size_t sagips_noalloc_scratch_bytes(void) { return kScratchBytes; }
 
 sagips_status sagips_bootstrap(sagips_ctx* c, const float* data, int64_t n_data, int d, uint64_t seed, uint32_t step,
                                int64_t n_out, float* out, int64_t* idx_out) {
