@@ -60,7 +60,14 @@ typedef enum {
 
 typedef enum { SAGIPS_F32 = 0, SAGIPS_BF16 = 1 } sagips_precision;
 typedef enum { SAGIPS_FEAT_IDENTITY = 0, SAGIPS_FEAT_HD8 = 1, SAGIPS_FEAT_PROXY2 = 2 } sagips_features;
-typedef enum { SAGIPS_CRITIC_BUFFER = 0, SAGIPS_CRITIC_QUADRATIC = 1 } sagips_critic;
+/* The last enumerator widens the type to 32 bits, so that a value a C caller
+ * passes outside the list is still a value of the type, and the library can
+ * reject it with SAGIPS_E_INVAL.                                           */
+typedef enum {
+  SAGIPS_CRITIC_BUFFER = 0,
+  SAGIPS_CRITIC_QUADRATIC = 1,
+  SAGIPS_CRITIC_MAX_ENUM = 0x7fffffff
+} sagips_critic;
 
 /* Parameters -> events source (host struct holding a device pointer).
  *   theta            device, [n_theta][2d] fp32, rows (a1,b1,a2,b2[,a3,b3]),
