@@ -101,6 +101,9 @@ struct Fused {
   // buffer would not fit next to the others in 160 KB of LDS.
   static constexpr bool kInPlace = (NH + 2) * kT * LD * 4 + 8192 > 160 * 1024;
   static constexpr int NB = kInPlace ? NH + 1 : NH + 2;   // activation (+ spare) buffers
+  // Products load the next product's first weight fragments during their tail,
+  // except in the in-place networks, whose registers are already all in use.
+  static constexpr bool kPF = !kInPlace;
   static constexpr int WAVES = kThreads / 64;
   static constexpr int WR = H / 16;            // waves along the output rows (16 rows each)
   static constexpr int WE = WAVES / WR;        // waves along the events
@@ -124,7 +127,7 @@ struct Fused {
     float dxd[kT][DX][2];
     float eD[kT];
     float eG[kT];
-    float w1[kInPlace ? H : 1][F];   // first-layer weights, when registers are short
+    float w1[H][F];          // first-layer weights (the dL/dx products)
     float red[2 * kT * 4];   // >= 2 T DX and >= 2 * waves
   };
 
@@ -144,6 +147,35 @@ struct Fused {
 #pragma unroll
     for (int kb = 0; kb < KB; ++kb) {
       if (kb + PD < KB) a[(kb + PD) % (PD + 1)] = *reinterpret_cast<const f32x4*>(wrow + 16 * (kb + PD));
+      f32x4 b[CB];
+#pragma unroll
+      for (int cb = 0; cb < CB; ++cb)
+        b[cb] = *reinterpret_cast<const f32x4*>(in + (e0 + 16 * cb + lr) * LD + 16 * kb + 4 * lg);
+#pragma unroll
+      for (int s = 0; s < 4; ++s)
+#pragma unroll
+        for (int cb = 0; cb < CB; ++cb) acc[cb] = mfma4(a[kb % (PD + 1)][s], b[cb][s], acc[cb]);
+    }
+  }
+
+  // The same product where pf holds the first PD weight fragments of Wg on
+  // entry and, loaded during the last PD K blocks, those of Wnext (the next
+  // product's weights) on exit, so that no product starts by waiting for its
+  // weights.
+  static __device__ __forceinline__ void gemm_pf(const float* __restrict__ Wg, const float* __restrict__ Wnext,
+                                                 f32x4 (&pf)[PD], const float* in, f32x4 (&acc)[CB], int o0,
+                                                 int e0, int lr, int lg) {
+#pragma unroll
+    for (int cb = 0; cb < CB; ++cb) acc[cb] = f32x4{0.f, 0.f, 0.f, 0.f};
+    const float* wrow = Wg + (o0 + lr) * H + 4 * lg;
+    const float* nrow = Wnext + (o0 + lr) * H + 4 * lg;
+    f32x4 a[PD + 1];
+#pragma unroll
+    for (int q = 0; q < PD; ++q) a[q] = pf[q];
+#pragma unroll
+    for (int kb = 0; kb < KB; ++kb) {
+      if (kb + PD < KB) a[(kb + PD) % (PD + 1)] = *reinterpret_cast<const f32x4*>(wrow + 16 * (kb + PD));
+      else pf[kb + PD - KB] = *reinterpret_cast<const f32x4*>(nrow + 16 * (kb + PD - KB));
       f32x4 b[CB];
 #pragma unroll
       for (int cb = 0; cb < CB; ++cb)
@@ -227,16 +259,12 @@ struct Fused {
     const float wor = p.Wo[vo];
     // per-event dot products: thread (ev = tid / PARTS, part = tid % PARTS) covers H / PARTS features
     const int dev_ = tid / PARTS, dpart = tid % PARTS;
-    float w1c[kInPlace ? 1 : NCH][4][F];     // the first-layer weights of this thread's features
-    if constexpr (kInPlace) {
-      for (int i = tid; i < H * F; i += kThreads) sm.w1[i / F][i % F] = p.W1[i];
-    } else {
+    for (int i = tid; i < H * F; i += kThreads) sm.w1[i / F][i % F] = p.W1[i];
+    // the first weight fragments of the first product (a tile's first hidden layer)
+    f32x4 pf[kPF ? PD : 1];
+    if constexpr (kPF) {
 #pragma unroll
-      for (int c = 0; c < NCH; ++c)
-#pragma unroll
-        for (int q = 0; q < 4; ++q)
-#pragma unroll
-          for (int j = 0; j < F; ++j) w1c[c][q][j] = p.W1[(chunk_off(dpart, c) + q) * F + j];
+      for (int q = 0; q < PD; ++q) pf[q] = *reinterpret_cast<const f32x4*>(p.Wh[0] + (o0 + lr) * H + 4 * lg + 16 * q);
     }
 
     for (int tile = blockIdx.x; tile < p.n_tiles; tile += gridDim.x) {
@@ -297,7 +325,8 @@ struct Fused {
 #pragma unroll
       for (int l = 0; l < NH; ++l) {
         f32x4 acc[CB];
-        gemm(p.Wh[l], &sm.act[l][0][0], acc, o0, e0, lr, lg);
+        if constexpr (kPF) gemm_pf(p.Wh[l], l + 1 < NH ? p.Wh[l + 1] : p.WhT[NH - 1], pf, &sm.act[l][0][0], acc, o0, e0, lr, lg);
+        else gemm(p.Wh[l], &sm.act[l][0][0], acc, o0, e0, lr, lg);
         const int o = o0 + 4 * lg;
         const f32x4 bias = *reinterpret_cast<const f32x4*>(p.bh[l] + o);
 #pragma unroll
@@ -381,7 +410,8 @@ struct Fused {
         wgrad(dout, Ain, sm.eD, accW[l], dbacc[l], wave % WR, e0, lr, lg);
         if constexpr (kInPlace) __syncthreads();   // din overwrites Ain, which every wave's wgrad read
         f32x4 acc[CB];
-        gemm(p.WhT[l], dout, acc, o0, e0, lr, lg);
+        if constexpr (kPF) gemm_pf(p.WhT[l], l > 0 ? p.WhT[l - 1] : p.Wh[0], pf, dout, acc, o0, e0, lr, lg);
+        else gemm(p.WhT[l], dout, acc, o0, e0, lr, lg);
         const int k = o0 + 4 * lg;
 #pragma unroll
         for (int cb = 0; cb < CB; ++cb) {
@@ -418,17 +448,10 @@ struct Fused {
           const int f = chunk_off(dpart, c);
 #pragma unroll
           for (int j = 0; j < F; ++j) {
-            if constexpr (kInPlace) {
-              g[j] = fmaf(dv.x, sm.w1[f][j], g[j]);
-              g[j] = fmaf(dv.y, sm.w1[f + 1][j], g[j]);
-              g[j] = fmaf(dv.z, sm.w1[f + 2][j], g[j]);
-              g[j] = fmaf(dv.w, sm.w1[f + 3][j], g[j]);
-            } else {
-              g[j] = fmaf(dv.x, w1c[c][0][j], g[j]);
-              g[j] = fmaf(dv.y, w1c[c][1][j], g[j]);
-              g[j] = fmaf(dv.z, w1c[c][2][j], g[j]);
-              g[j] = fmaf(dv.w, w1c[c][3][j], g[j]);
-            }
+            g[j] = fmaf(dv.x, sm.w1[f][j], g[j]);
+            g[j] = fmaf(dv.y, sm.w1[f + 1][j], g[j]);
+            g[j] = fmaf(dv.z, sm.w1[f + 2][j], g[j]);
+            g[j] = fmaf(dv.w, sm.w1[f + 3][j], g[j]);
           }
         }
 #pragma unroll
