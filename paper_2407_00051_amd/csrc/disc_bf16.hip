@@ -317,6 +317,9 @@ __device__ __forceinline__ Rsrc make_rsrc(const void* base, uint32_t bytes) {
 __device__ __forceinline__ bf16x8 load_frag(Rsrc r, uint32_t voff, uint32_t soff) {
   return __builtin_bit_cast(bf16x8, __builtin_amdgcn_raw_buffer_load_b128(r, (int)voff, (int)soff, 0));
 }
+__device__ __forceinline__ float load_f32(Rsrc r, uint32_t voff) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, (int)voff, 0, 0));
+}
 
 // K steps per 32-row block of a weight copy: KS + 1 forward (with the bias
 // step), KS backward.
@@ -508,6 +511,10 @@ __device__ __forceinline__ void load_mask(const uint32_t* src, uint32_t (&m)[4])
   const uint4 v = *reinterpret_cast<const uint4*>(src);
   m[0] = v.x; m[1] = v.y; m[2] = v.z; m[3] = v.w;
 }
+__device__ __forceinline__ void load_mask(Rsrc r, uint32_t voff, uint32_t (&m)[4]) {
+  const uint4 v = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, (int)voff, 0, 0));
+  m[0] = v.x; m[1] = v.y; m[2] = v.z; m[3] = v.w;
+}
 
 // Writes a layer's packed outputs into the LDS tile.
 template <int MT, int NT, int LDA>
@@ -615,11 +622,14 @@ __global__ __launch_bounds__(Chain<H>::THREADS, Chain<H>::BPC) void k_fwd_chain(
   WeightPrefetch<H> pf;
   prefetch_weights<H, true>(weight_rsrc<H, true>(p.Wb, 0), pf, woff);
   float fst[FU];
+  // 32-bit offsets into a buffer resource: no 64-bit per-lane pointer stays live
+  // across the tile loop (the compiler would hoist and spill it)
+  const Rsrc rs_feat = make_rsrc(p.feat, (uint32_t)c.rows * F * 4u);
   auto load_feat = [&](int tile) __attribute__((always_inline)) {
 #pragma unroll
     for (int u = 0; u < FU; ++u) {
       const int k = tid + NTH * u;
-      if (k < T * F) fst[u] = p.feat[(int64_t)tile * T * F + k];
+      if (k < T * F) fst[u] = load_f32(rs_feat, (uint32_t)(tile * T * F + k) * 4u);
     }
   };
   if ((int)blockIdx.x < ntiles) load_feat(blockIdx.x);
@@ -843,27 +853,44 @@ __global__ __launch_bounds__(Chain<H>::THREADS, Chain<H>::BPC) void k_bwd_chain(
   const int NH = p.NH;
   WeightPrefetch<H> pf;
   prefetch_weights<H, false>(weight_rsrc<H, false>(p.WTb, NH - 1), pf, woff);
-  auto mask_at = [&](int layer, int tile) __attribute__((always_inline)) {
-    return p.mask + ((((int64_t)layer * ntiles + tile) * WAVES + wave) * 64 + lane) * MW;
+  // Loads through buffer resources with 32-bit per-lane offsets, so that no
+  // 64-bit per-lane pointer stays live across the tile loop (the compiler would
+  // hoist and spill it, and each reload waits for every outstanding store).
+  const Rsrc rs_mask = make_rsrc(p.mask, (uint32_t)(NH + 1) * ntiles * WAVES * 64u * MW * 4u);
+  const uint32_t mlane = ((uint32_t)wave * 64u + lane) * MW * 4u;
+  auto mask_off = [&](int layer, int tile) __attribute__((always_inline)) {
+    return ((uint32_t)(layer * ntiles + tile) * WAVES * 64u) * MW * 4u + mlane;
   };
-  // staged rows of a tile: value k of srow, from the seed, feature and event arrays
+  const Rsrc rs_eD = make_rsrc(p.eD, (uint32_t)c.rows * 4u), rs_eG = make_rsrc(p.eG, (uint32_t)c.rows * 4u);
+  const Rsrc rs_feat = make_rsrc(p.feat, (uint32_t)c.rows * F * 4u);
+  const Rsrc rs_xs = make_rsrc(p.xs, (uint32_t)c.rows * D * 4u);
+  // staged rows of a tile: value k of srow, from the seed, feature and event
+  // arrays.  The arrays' boundaries in k are multiples of T = 128, so the 64
+  // values of a wave come from one array: the choice is a scalar branch.
   float sv[SU];
   auto load_rows = [&](int tile) __attribute__((always_inline)) {
-    const int64_t r0 = (int64_t)tile * T;
+    const int r0 = tile * T;
 #pragma unroll
     for (int u = 0; u < SU; ++u) {
       const int k = tid + NTH * u;
+      const int kw = __builtin_amdgcn_readfirstlane(k - lane);   // the wave's first value
       float v = 0.f;
-      if (k < 2 * T) v = (k & 1) ? p.eG[r0 + (k >> 1)] : p.eD[r0 + (k >> 1)];
-      else if (k < (2 + F) * T) v = p.feat[r0 * F + (k - 2 * T)];
-      else if (k < (2 + F + D) * T && want_dx && kHD8) v = p.xs[r0 * D + (k - (2 + F) * T)];
+      if (kw < 2 * T) {
+        const uint32_t off = (uint32_t)(r0 + (k >> 1)) * 4u;
+        const float a = load_f32(rs_eD, off), g = load_f32(rs_eG, off);
+        v = (k & 1) ? g : a;
+      } else if (kw < (2 + F) * T) {
+        v = load_f32(rs_feat, (uint32_t)(r0 * F + (k - 2 * T)) * 4u);
+      } else if (kw < (2 + F + D) * T && want_dx && kHD8) {
+        v = load_f32(rs_xs, (uint32_t)(r0 * D + (k - (2 + F) * T)) * 4u);
+      }
       sv[u] = v;
     }
   };
   uint32_t mtop[MW];
   if ((int)blockIdx.x < ntiles) {
     load_rows(blockIdx.x);
-    load_mask(mask_at(NH, blockIdx.x), mtop);
+    load_mask(rs_mask, mask_off(NH, blockIdx.x), mtop);
   }
   __syncthreads();                              // swo staged
 
@@ -930,8 +957,8 @@ __global__ __launch_bounds__(Chain<H>::THREADS, Chain<H>::BPC) void k_bwd_chain(
     // ---- hidden layers, top down ---------------------------------------------
     for (int l = NH - 1; l >= 0; --l) {
       uint32_t m[MW];
-      load_mask(mask_at(l, tile), m);
-      if (l == 0 && next < ntiles) load_mask(mask_at(NH, next), mtop);
+      load_mask(rs_mask, mask_off(l, tile), m);
+      if (l == 0 && next < ntiles) load_mask(rs_mask, mask_off(NH, next), mtop);
       f32x16 acc[MT][NT];
       // the next product is layer l - 1, or the top layer of the next tile;
       // the product's input (the signal at A_{l+2}) goes to HBM meanwhile
