@@ -24,6 +24,7 @@ from __future__ import annotations
 
 import argparse
 import hashlib
+import itertools
 import json
 import os
 import re
@@ -228,17 +229,15 @@ class CpuPool:
         # warm the workers (imports, inputs) outside the timed window
         list(self.ex.map(_cpu_task, [name] * self.workers, [0] * self.workers, [0] * self.workers,
                          [min(per, 64)] * self.workers))
-        it = iter(tasks)
+        # the workload's tasks in order, again from the first once all are issued, until
+        # `seconds` have passed (a small workload takes well under a second per pass)
+        it = itertools.cycle(tasks)
         running, done_events, n_done = set(), 0, 0
         t0 = time.perf_counter()
 
         def submit():
-            try:
-                r, off, n = next(it)
-            except StopIteration:
-                return False
+            r, off, n = next(it)
             running.add(self.ex.submit(_cpu_task, name, r, off, n))
-            return True
 
         for _ in range(self.workers):
             submit()
@@ -256,7 +255,8 @@ class CpuPool:
         what = "sampler only" if name == "stress_sample" else (
             "quadratic critic" if w.widths is None else ("bf16-point" if w.precision == "bf16" else "float64"))
         return {"value": done_events / dt, "unit": "events/s", "cores": self.workers, "kind": "oracle",
-                "sample": f"{done_events} of the workload's {total} fake events{real}, {n_done} tasks of <= {per} "
+                "sample": f"{done_events} fake events ({done_events / total:.3g} x the workload's {total}){real}, "
+                          f"{n_done} tasks of <= {per} "
                           f"events of one parameter row, oracle step ({what}, numpy float64) in {self.workers} "
                           f"single-threaded worker processes, {dt:.1f} s"}
 
