@@ -390,16 +390,16 @@ __device__ __forceinline__ bf16x8 copy_read(const u16* p0) {
 // above for the arrangement).  pf holds the first PD weight steps of W on
 // entry and those of Wnext (the next product) on exit.
 //
-// The product's input goes to HBM meanwhile, as the weight-gradient operand:
-// the wave's own columns of act, copy kilobyte j (the K-fragment order above;
-// dst at per-lane byte offset coff) read with the operands of step CS j and
-// stored after its products.  Spread over the product, the stores drain while the matrix cores
+// With `copy` (wave-uniform) the product's input goes to HBM meanwhile, as the
+// weight-gradient operand: the wave's own columns of act, copy kilobyte j (the
+// K-fragment order above; dst at per-lane byte offset coff) read with the
+// operands of step CS j and stored after its products.  Spread over the product, the stores drain while the matrix cores
 // run, and a weight load waits behind at most a few of them (loads and stores
 // share one completion counter).
 template <int H, bool kFwd>
 __device__ __forceinline__ void chain_gemm(Rsrc W, Rsrc Wnext, uint32_t woff, WeightPrefetch<H>& pf, const u16* act,
                                            f32x16 (&acc)[Chain<H>::MT][Chain<H>::NT], int lane, int wave, u16* dst,
-                                           uint32_t coff) {
+                                           uint32_t coff, bool copy) {
   using C = Chain<H>;
   constexpr int KS = C::KS, PD = C::PD, LDA = C::LDA, MT = C::MT, NT = C::NT;
   constexpr int N = WSteps<H, kFwd>::N;          // K steps, the bias step last
@@ -431,7 +431,7 @@ __device__ __forceinline__ void chain_gemm(Rsrc W, Rsrc Wnext, uint32_t woff, We
         pf.a[ks + PD - N][m] = load_frag(Wnext, woff, (uint32_t)(m * N + ks + PD - N) * 1024);
     }
     const int j = ks / CS;                       // copy kilobyte of this step, if ks % CS == 0
-    const bool cp = ks % CS == 0 && j < C::COPIES;
+    const bool cp = ks % CS == 0 && j < C::COPIES && copy;
     bf16x8 cv;
     if (cp) cv = copy_read<LDA>(cbase + 16 * (j >> 1) * LDA + 32 * (j & 1));
     if (ks + 1 < KS) {
@@ -491,6 +491,19 @@ __device__ __forceinline__ void activate(const f32x16 (&v)[MT][NT], float slope,
     }
 }
 
+// Sign bits of eight bf16 values (an MFMA operand fragment): bit t is set
+// where value t is negative (or -0).  A byte permute with the sign-replicating
+// selectors turns each value's sign bit into a byte 0x00 or 0xff (-1), and a
+// signed 4-way byte dot product against -1, -2, -4, -8 (-16 .. -128 for
+// values 4..7) sums them into the byte.
+__device__ __forceinline__ uint32_t sign_byte(bf16x8 v) {
+  const uint4 w = __builtin_bit_cast(uint4, v);
+  const int lo = (int)__builtin_amdgcn_perm(w.y, w.x, 0x0B0A0908u);   // values 0..3
+  const int hi = (int)__builtin_amdgcn_perm(w.w, w.z, 0x0B0A0908u);   // values 4..7
+  return (uint32_t)__builtin_amdgcn_sdot4(lo, (int)0xF8FCFEFFu, __builtin_amdgcn_sdot4(hi, (int)0x80C0E0F0u, 0, false),
+                                          false);
+}
+
 // All-ones where output (t, g, q) of a lane's mask words is negative.
 template <int MW>
 __device__ __forceinline__ uint32_t neg_mask(const uint32_t (&m)[MW], int t, int g, int q) {
@@ -546,6 +559,7 @@ struct ChainArgs {
   u16* act;                  // [NH][rows H]: A_1 .. A_NH, K-fragment order
   u16* dlt;                  // [NH][rows H]: unit-seed signal at A_2 .. A_{NH+1}, K-fragment order
   uint32_t* mask;            // [NH + 1][rows / T][WAVES][64 lanes][4]: signs of A_1 .. A_{NH+1}
+  uint8_t* maskT;            // [rows / T][H / 32][64 lanes][T / 16]: signs of A_{NH+1}, K-fragment order
   float* eD;                 // [rows] dL_D/dz (0 on padding)
   float* eG;                 // [rows] dL_G/dz (fake; 0 otherwise)
   float* logits;             // caller's array (indexed from c.row0) or NULL
@@ -683,7 +697,7 @@ __global__ __launch_bounds__(Chain<H>::THREADS, Chain<H>::BPC) void k_fwd_chain(
       // the next product is layer l + 1, or the first hidden layer of the next
       // tile; then the product's input A_{l+1} goes to HBM
       chain_gemm<H, true>(weight_rsrc<H, true>(p.Wb, l), weight_rsrc<H, true>(p.Wb, last ? 0 : l + 1), woff, pf,
-                          act, acc, lane, wave, p.act + ((int64_t)l * rstride + r0) * H, coff);
+                          act, acc, lane, wave, p.act + ((int64_t)l * rstride + r0) * H, coff, true);
       uint2 pk[MT][NT][4];
       uint32_t m[MW];
       activate<MT, NT>(acc, slope, pk, m);
@@ -766,17 +780,28 @@ __global__ __launch_bounds__(Chain<H>::THREADS, Chain<H>::BPC) void k_fwd_chain(
         asm volatile("" : "+v"(ci));
         const u16* cbase = act + ci;
         f32x16 cz[MT];
+        // the same fragments' sign bits, for the top layer's weight gradient:
+        // byte kb of (nb, lane) covers rows 16 kb + 8 (lane / 32) .. + 7 of
+        // column ow + 32 nb + lane % 32
+        uint32_t sb[MT][2];
 #pragma unroll
         for (int kb = 0; kb < T / 16; ++kb) {
           const uint4 tv = *reinterpret_cast<const uint4*>(&sterm[lr < 3 ? lr : 0][16 * kb + 8 * lh]);
           const bf16x8 af = __builtin_bit_cast(bf16x8, lr < 3 ? tv : make_uint4(0u, 0u, 0u, 0u));
 #pragma unroll
-          for (int nb = 0; nb < MT; ++nb)
-            cz[nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af, copy_read<LDA>(cbase + 16 * kb * LDA + 32 * nb),
-                                                            kb == 0 ? zero : cz[nb], 0, 0, 0);
+          for (int nb = 0; nb < MT; ++nb) {
+            const bf16x8 bv = copy_read<LDA>(cbase + 16 * kb * LDA + 32 * nb);
+            cz[nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af, bv, kb == 0 ? zero : cz[nb], 0, 0, 0);
+            const uint32_t byte = sign_byte(bv) << (8 * (kb & 3));
+            sb[nb][kb >> 2] = (kb & 3) == 0 ? byte : (sb[nb][kb >> 2] | byte);
+          }
         }
 #pragma unroll
-        for (int nb = 0; nb < MT; ++nb) dwo[nb] += (cz[nb][0] + cz[nb][1]) + cz[nb][2];
+        for (int nb = 0; nb < MT; ++nb) {
+          dwo[nb] += (cz[nb][0] + cz[nb][1]) + cz[nb][2];
+          *reinterpret_cast<uint2*>(p.maskT + ((size_t)(tile * (H / 32) + MT * wave + nb) * 64 + lane) * (T / 16)) =
+              make_uint2(sb[nb][0], sb[nb][1]);
+        }
       }
       // act, zpart, se_s and sterm are next written after the next tile's
       // first barrier, which every thread reaches only after this point.
@@ -961,9 +986,12 @@ __global__ __launch_bounds__(Chain<H>::THREADS, Chain<H>::BPC) void k_bwd_chain(
       if (l == 0 && next < ntiles) load_mask(rs_mask, mask_off(NH, next), mtop);
       f32x16 acc[MT][NT];
       // the next product is layer l - 1, or the top layer of the next tile;
-      // the product's input (the signal at A_{l+2}) goes to HBM meanwhile
+      // the product's input (the signal at A_{l+2}) goes to HBM meanwhile,
+      // except at the top: the top layer's weight gradient rebuilds that
+      // signal from w_o and the forward chain's sign bytes
       chain_gemm<H, false>(weight_rsrc<H, false>(p.WTb, l), weight_rsrc<H, false>(p.WTb, l > 0 ? l - 1 : NH - 1), woff,
-                           pf, act, acc, lane, wave, p.dlt + ((int64_t)l * rstride + r0) * H, coff);
+                           pf, act, acc, lane, wave, p.dlt + ((int64_t)(l < NH - 1 ? l : 0) * rstride + r0) * H, coff,
+                           l < NH - 1);
       uint2 pk[MT][NT][4];
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt)
@@ -1105,10 +1133,40 @@ template <int H> struct WgradCfg;
 template <> struct WgradCfg<256> { static constexpr int WM = 2, WN = 2, PD = 3; };
 constexpr int kWThreads = 256;
 
-template <int H>
+// The top hidden layer's signal is not stored: its unit-seed value at
+// A_{NH+1} is w_o times LeakyReLU' of A_{NH+1}, rounded to bf16, i.e. one of
+// two values per output feature, chosen by the sign of the activation.  With
+// kTop the weight-gradient kernels rebuild the delta fragments from the sign
+// bytes the forward chain stores (byte kb % 8 of piece (kb / 8, column block,
+// lane) covers the lane's 8 rows of K block kb) and the two bf16 values of
+// the lane's feature, exactly the values the backward chain forms.
+struct TopSignal {
+  const uint8_t* maskT;    // [K blocks / 8][H / 32][64 lanes][8]
+  const float* wo;         // [H]
+  float slope;
+};
+
+// Unit-seed signal of feature o where the activation is positive (1) or
+// negative (slope), as bf16 values in fp32.
+__device__ __forceinline__ void top_values(const TopSignal& ts, int o, uint32_t& dpos, uint32_t& dneg) {
+  const float w = ts.wo[o];
+  dpos = (uint32_t)bf16_bits(w) << 16;
+  dneg = (uint32_t)bf16_bits(ts.slope * w) << 16;
+}
+
+// Byte offset of the sign byte of K block kb in the lane's column block.
+__device__ __forceinline__ uint32_t top_koff(int kb, int CB) { return (uint32_t)(kb >> 3) * CB * 512u + (kb & 7); }
+
+// The 8 rows' signal values of a lane (bit t of `bits` selects row t's value).
+__device__ __forceinline__ float top_delta(uint32_t bits, int t, uint32_t dpos, uint32_t dneg) {
+  return __uint_as_float(__builtin_amdgcn_bitop3_b32((uint32_t)__builtin_amdgcn_sbfe((int)bits, t, 1), dneg, dpos, 0xCA));
+}
+
+template <int H, bool kTop>
 __global__ __launch_bounds__(kWThreads, 1) void k_wgrad(const u16* __restrict__ dsc, const u16* __restrict__ A,
                                                         const float* __restrict__ eD, int kb_per_slice, int kb_total,
-                                                        float* __restrict__ P, float* __restrict__ Pdb, int xcd_map) {
+                                                        float* __restrict__ P, float* __restrict__ Pdb, int xcd_map,
+                                                        TopSignal ts) {
   constexpr int TI = H / kWT;     // tiles per dimension
   constexpr int CB = H / 32;      // 32-column blocks
   constexpr int kWM = WgradCfg<H>::WM, kWN = WgradCfg<H>::WN, PD = WgradCfg<H>::PD;
@@ -1137,6 +1195,12 @@ __global__ __launch_bounds__(kWThreads, 1) void k_wgrad(const u16* __restrict__ 
   const u16* pb = A + (((size_t)kb0 * CB + ib) * 64 + lane) * 8;
   const float* pe = eD + (size_t)kb0 * 16 + 8 * lh;    // rows of the lane's half of each K block
   constexpr size_t KSTRIDE = (size_t)CB * 512;          // bf16 per K block
+  const uint8_t* pm = ts.maskT + ((size_t)ob * 64 + lane) * 8;   // kTop: sign bytes of column block ob
+  uint32_t dpos[FM], dneg[FM];
+  if constexpr (kTop) {
+#pragma unroll
+    for (int m = 0; m < FM; ++m) top_values(ts, 32 * (ob + m) + lr, dpos[m], dneg[m]);
+  }
   f32x16 acc[FM][FN];
 #pragma unroll
   for (int m = 0; m < FM; ++m)
@@ -1148,10 +1212,14 @@ __global__ __launch_bounds__(kWThreads, 1) void k_wgrad(const u16* __restrict__ 
 #pragma unroll
   for (int m = 0; m < FM; ++m) dbs[m] = 0.f;
   bf16x8 fa[PD + 1][FM], fb[PD + 1][FN];
+  uint32_t fm[PD + 1][FM];        // kTop: sign bytes instead of fa
   f32x4 fe[PD + 1][2];
   auto load = [&](int slot, int k) __attribute__((always_inline)) {
 #pragma unroll
-    for (int m = 0; m < FM; ++m) fa[slot][m] = *reinterpret_cast<const bf16x8*>(pa + k * KSTRIDE + m * 512);
+    for (int m = 0; m < FM; ++m) {
+      if constexpr (kTop) fm[slot][m] = pm[top_koff(kb0 + k, CB) + m * 512];
+      else fa[slot][m] = *reinterpret_cast<const bf16x8*>(pa + k * KSTRIDE + m * 512);
+    }
 #pragma unroll
     for (int n = 0; n < FN; ++n) fb[slot][n] = *reinterpret_cast<const bf16x8*>(pb + k * KSTRIDE + n * 512);
     fe[slot][0] = *reinterpret_cast<const f32x4*>(pe + (size_t)k * 16);
@@ -1165,7 +1233,12 @@ __global__ __launch_bounds__(kWThreads, 1) void k_wgrad(const u16* __restrict__ 
     for (int m = 0; m < FM; ++m) {
       float v[8];
 #pragma unroll
-      for (int t = 0; t < 8; ++t) v[t] = (float)fa[slot][m][t] * fe[slot][t >> 2][t & 3];
+      for (int t = 0; t < 8; ++t) {
+        float d;
+        if constexpr (kTop) d = top_delta(fm[slot][m], t, dpos[m], dneg[m]);
+        else d = (float)fa[slot][m][t];
+        v[t] = d * fe[slot][t >> 2][t & 3];
+      }
       dbs[m] += ((v[0] + v[1]) + (v[2] + v[3])) + ((v[4] + v[5]) + (v[6] + v[7]));
       sa[into][m] = __builtin_bit_cast(bf16x8, make_uint4(pack_bf16(v[0], v[1]), pack_bf16(v[2], v[3]),
                                                           pack_bf16(v[4], v[5]), pack_bf16(v[6], v[7])));
@@ -1271,10 +1344,11 @@ __device__ __forceinline__ void lds_barrier() {
   asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
 }
 
+template <bool kTop>
 __global__ __launch_bounds__(kWThreads, 1) void k_wgrad_shared(const u16* __restrict__ dsc, const u16* __restrict__ A,
                                                                const float* __restrict__ eD, int kb_per_slice,
                                                                int kb_total, float* __restrict__ P,
-                                                               float* __restrict__ Pdb, int xcd_map) {
+                                                               float* __restrict__ Pdb, int xcd_map, TopSignal ts) {
   constexpr int H = 512;
   constexpr int TI = H / kWT;     // 2
   constexpr int CB = H / 32;      // 16
@@ -1301,6 +1375,12 @@ __global__ __launch_bounds__(kWThreads, 1) void k_wgrad_shared(const u16* __rest
   const u16* pa = dsc + (((size_t)kb0 * CB + ob) * 64 + lane) * 8;
   const u16* pb = A + (((size_t)kb0 * CB + ib + 2 * wave) * 64 + lane) * 8;   // this wave's two A fragments
   const float* pe = eD + (size_t)kb0 * 16 + 8 * lh;
+  const uint8_t* pm = ts.maskT + ((size_t)ob * 64 + lane) * 8;   // kTop: sign bytes of column block ob
+  uint32_t dpos[FM], dneg[FM];
+  if constexpr (kTop) {
+#pragma unroll
+    for (int m = 0; m < FM; ++m) top_values(ts, 32 * (ob + m) + lr, dpos[m], dneg[m]);
+  }
   f32x16 acc[FM][FN];
 #pragma unroll
   for (int m = 0; m < FM; ++m)
@@ -1310,13 +1390,17 @@ __global__ __launch_bounds__(kWThreads, 1) void k_wgrad_shared(const u16* __rest
       for (int r = 0; r < 16; ++r) acc[m][n][r] = 0.f;
   float dbs[FM] = {0.f, 0.f};
   bf16x8 ra[NS][2], rd[NS][FM];
+  uint32_t rm[NS][FM];            // kTop: sign bytes instead of rd
   f32x4 re[NS][2];
   bf16x8 fb[2][FN];               // the A fragments of the current and the next step
   auto load = [&](int slot, int k) __attribute__((always_inline)) {
 #pragma unroll
     for (int j = 0; j < 2; ++j) ra[slot][j] = *reinterpret_cast<const bf16x8*>(pb + k * KSTRIDE + j * 512);
 #pragma unroll
-    for (int m = 0; m < FM; ++m) rd[slot][m] = *reinterpret_cast<const bf16x8*>(pa + k * KSTRIDE + m * 512);
+    for (int m = 0; m < FM; ++m) {
+      if constexpr (kTop) rm[slot][m] = pm[top_koff(kb0 + k, CB) + m * 512];
+      else rd[slot][m] = *reinterpret_cast<const bf16x8*>(pa + k * KSTRIDE + m * 512);
+    }
     re[slot][0] = *reinterpret_cast<const f32x4*>(pe + (size_t)k * 16);
     re[slot][1] = *reinterpret_cast<const f32x4*>(pe + (size_t)k * 16 + 4);
   };
@@ -1336,7 +1420,12 @@ __global__ __launch_bounds__(kWThreads, 1) void k_wgrad_shared(const u16* __rest
     for (int m = 0; m < FM; ++m) {
       float v[8];
 #pragma unroll
-      for (int t = 0; t < 8; ++t) v[t] = (float)rd[slot][m][t] * re[slot][t >> 2][t & 3];
+      for (int t = 0; t < 8; ++t) {
+        float d;
+        if constexpr (kTop) d = top_delta(rm[slot][m], t, dpos[m], dneg[m]);
+        else d = (float)rd[slot][m][t];
+        v[t] = d * re[slot][t >> 2][t & 3];
+      }
       dbs[m] += ((v[0] + v[1]) + (v[2] + v[3])) + ((v[4] + v[5]) + (v[6] + v[7]));
       sa[into][m] = __builtin_bit_cast(bf16x8, make_uint4(pack_bf16(v[0], v[1]), pack_bf16(v[2], v[3]),
                                                           pack_bf16(v[4], v[5]), pack_bf16(v[6], v[7])));
@@ -1483,8 +1572,8 @@ struct Plan {
   int rows_max;          // padded rows of the largest chunk
   int blocks;            // workgroups of the chain kernels
   int slices;            // weight-gradient slices per chunk
-  size_t off_wb, off_wtb, off_w0f, off_feat, off_xs, off_act, off_dlt, off_mask, off_eD, off_eG, off_plog, off_pfb, off_pw,
-      off_pwdb, off_accl, total;
+  size_t off_wb, off_wtb, off_w0f, off_feat, off_xs, off_act, off_dlt, off_mask, off_maskT, off_eD, off_eG, off_plog,
+      off_pfb, off_pw, off_pwdb, off_accl, total;
 };
 
 int pad128(int64_t n) { return (int)((n + 127) / 128 * 128); }
@@ -1513,8 +1602,9 @@ Plan make_plan(const DiscArgs& a, int n_cu) {
   p.off_feat = o; o += al(4 * R * p.F);
   p.off_xs = o; o += al(4 * R * p.D);
   p.off_act = o; o += al(2 * R * H * NH);
-  p.off_dlt = o; o += al(2 * R * H * NH);
+  p.off_dlt = o; o += al(2 * R * H * (NH - 1));   // the top layer's signal is rebuilt from signs
   p.off_mask = o; o += al(8 * R * (H / 64) * (NH + 1));
+  p.off_maskT = o; o += al(R * H / 8);
   p.off_eD = o; o += al(4 * R);
   p.off_eG = o; o += al(4 * R);
   p.off_plog = o; o += al(4 * (size_t)p.blocks * (H + 3));
@@ -1607,6 +1697,8 @@ hipError_t launch_disc_bf16(const DiscArgs& a, void* ws, int n_cu, hipStream_t s
   ca.act = B16(p.off_act);
   ca.dlt = B16(p.off_dlt);
   ca.mask = reinterpret_cast<uint32_t*>(base + p.off_mask);
+  ca.maskT = reinterpret_cast<uint8_t*>(base + p.off_maskT);
+  const TopSignal top{ca.maskT, ca.wo, ca.slope};
   ca.eD = F32(p.off_eD);
   ca.eG = F32(p.off_eG);
   ca.plog = F32(p.off_plog);
@@ -1657,13 +1749,26 @@ hipError_t launch_disc_bf16(const DiscArgs& a, void* ws, int n_cu, hipStream_t s
         const size_t bst = (size_t)c.rows * H;   // stride between this chunk's per-layer buffers
         for (int l = 0; l < NH; ++l) {
           // hidden layer l maps A_{l+1} -> A_{l+2}: operands A_{l+1} and the signal at A_{l+2}
+          // (the top layer's signal rebuilt from the sign bytes)
+          const bool top_layer = l == NH - 1;
+          const u16* dsc = top_layer ? nullptr : ca.dlt + l * bst;
+          const dim3 grid(tiles * p.slices);
           if (tm) tm->begin("bf16_wgrad");
-          if (H == 256)
-            hipLaunchKernelGGL(k_wgrad<256>, dim3(tiles * p.slices), dim3(kWThreads), 0, st, ca.dlt + l * bst,
-                               ca.act + l * bst, ca.eD, kb_per_slice, kb_total, F32(p.off_pw), F32(p.off_pwdb), xcd_map);
-          else
-            hipLaunchKernelGGL(k_wgrad_shared, dim3(tiles * p.slices), dim3(kWThreads), 0, st, ca.dlt + l * bst,
-                               ca.act + l * bst, ca.eD, kb_per_slice, kb_total, F32(p.off_pw), F32(p.off_pwdb), xcd_map);
+          if (H == 256) {
+            if (top_layer)
+              hipLaunchKernelGGL((k_wgrad<256, true>), grid, dim3(kWThreads), 0, st, dsc, ca.act + l * bst, ca.eD,
+                                 kb_per_slice, kb_total, F32(p.off_pw), F32(p.off_pwdb), xcd_map, top);
+            else
+              hipLaunchKernelGGL((k_wgrad<256, false>), grid, dim3(kWThreads), 0, st, dsc, ca.act + l * bst, ca.eD,
+                                 kb_per_slice, kb_total, F32(p.off_pw), F32(p.off_pwdb), xcd_map, top);
+          } else {
+            if (top_layer)
+              hipLaunchKernelGGL(k_wgrad_shared<true>, grid, dim3(kWThreads), 0, st, dsc, ca.act + l * bst, ca.eD,
+                                 kb_per_slice, kb_total, F32(p.off_pw), F32(p.off_pwdb), xcd_map, top);
+            else
+              hipLaunchKernelGGL(k_wgrad_shared<false>, grid, dim3(kWThreads), 0, st, dsc, ca.act + l * bst, ca.eD,
+                                 kb_per_slice, kb_total, F32(p.off_pw), F32(p.off_pwdb), xcd_map, top);
+          }
           if (tm) tm->end();
           accumulate(F32(p.off_pw), p.slices, (int64_t)H * H, (int64_t)H * H, out.dW[1 + l], first, st);
           accumulate(F32(p.off_pwdb), p.slices, (int64_t)H, (int64_t)H, out.db[1 + l], first, st);
