@@ -3,13 +3,14 @@
 // fit in registers across tiles.  The step is processed in chunks of event
 // rows (all fake or all real); each chunk goes through these kernels:
 //
-//   k_prep       features of every row (sampling fake events in place, HD8 map)
-//   k_fwd_chain  per tile of rows, in LDS: A_1 = bf16(LeakyReLU(feat W1^T + b1))
+//   k_fwd_chain  per tile of rows, in LDS: the tile's events (fake events
+//                sampled there from their Philox words, real ones read), their
+//                features, A_1 = bf16(LeakyReLU(feat W1^T + b1))
 //                (fp32 matrix cores, K <= 8 plus the bias), then every hidden
 //                layer on the bf16 matrix cores, then the logit z and the BCE
-//                seeds e_D, e_G; stores A_1 .. A_NH and the activation sign
-//                masks
-//   k_bwd_chain  per tile, in LDS: the unit-seed signal from the logit layer
+//                seeds e_D, e_G; stores A_1 .. A_NH, the activation sign
+//                masks and the top layer's sign bits
+//   k_bwd_chain  per tile, in LDS: the events again, the unit-seed signal from the logit layer
 //                down to A_1 (matrix cores, LeakyReLU' from the masks); stores
 //                the signals the weight gradients need; first-layer dW_1, db_1
 //                and dL_G/dx (through the HD8 Jacobian), also on the matrix
@@ -169,8 +170,8 @@ __global__ __launch_bounds__(256) void k_w0_frag(const float* __restrict__ W0, i
 }
 
 // ---------------------------------------------------------------------------
-// Rows of one chunk: features (and x for fake rows).  Rows past `valid` are
-// padding: features 0.5, never stored anywhere visible.
+// Rows of one chunk.  Rows past `valid` are padding: coordinates 0.5, never
+// stored anywhere visible (their e_D and e_G are 0).
 struct ChunkArgs {
   int64_t row0;       // first event index (within the fake or the real batch)
   int rows;           // padded row count (multiple of 128)
@@ -178,61 +179,111 @@ struct ChunkArgs {
   int fake;
 };
 
-// The two log features come from the quantile's log domain for sampled
-// events: ln x1 = lam1 / a1 and ln(1 - x3) = log1mexp(lam3 / a3), which stay
-// accurate (and finite) where fp32 x3 has rounded to within ulps of 1.  Buffer
-// events only have their fp32 values: ln x1 and log1p(-x3) of those.
+// Where a chunk's events come from: sampled from the source (fake events of a
+// source call) or read from a buffer (the real batch, or fake events passed as
+// a buffer).
+struct EventArgs {
+  SourceArgs src;
+  const float* xin;   // [n][D] when not sampled
+  int sampled;
+};
+
+// Parameter row of event i (32-bit division when both fit).
+__device__ __forceinline__ int64_t row_of(int64_t i, int64_t E) {
+  if (((uint64_t)i | (uint64_t)E) >> 32) return i / E;
+  return (int64_t)((uint32_t)i / (uint32_t)E);
+}
+
+// The chains stage their tile's events in LDS themselves: coordinate j of
+// event i is computed by one thread, in two halves.  event_fetch (a tile
+// ahead) loads what it needs from memory into two registers: theta (a, b) of
+// the event's parameter row for sampled events, the coordinate itself for
+// buffer events.  event_coord then forms the coordinate, from the event's
+// Philox words and the quantile, and for HD8 its log feature (j = 0: ln x1,
+// j = D - 1: ln(1 - x_D)).  The log features of sampled events come from the
+// quantile's log domain, ln x1 = lam1 / a1 and ln(1 - x3) = log1mexp(lam3 / a3),
+// which stay accurate (and finite) where fp32 x3 has rounded to within ulps
+// of 1; buffer events only have their fp32 values: ln x1 and log1p(-x3) of
+// those.
+template <int D>
+__device__ __forceinline__ void event_fetch(const EventArgs& ev, int64_t i, bool valid, int j, float& a, float& b) {
+  a = b = 0.5f;
+  if (!valid) return;
+  if (ev.sampled) {
+    const float* th = ev.src.theta + row_of(i, ev.src.E) * (2 * D) + 2 * j;
+    a = th[0];
+    b = th[1];
+  } else {
+    a = ev.xin[i * D + j];
+  }
+}
+
 template <int D, bool kHD8>
-__global__ __launch_bounds__(256) void k_prep(ChunkArgs c, const float* __restrict__ xin, SourceArgs src, int sampled,
-                                              float* __restrict__ feat, float* __restrict__ xs) {
-  constexpr int F = kHD8 ? 8 : D;
-  const int r = blockIdx.x * 256 + threadIdx.x;
-  if (r >= c.rows) return;
-  float x[D];
-  float lnx1 = 0.f, ln1mx3 = 0.f;
-  if (r < c.valid) {
-    const int64_t i = c.row0 + r;
-    if (sampled) {
-      const int row = (int)(i / src.E);
-      const Words w = event_words(src.base + (uint64_t)i, src.stream, src.k0, src.k1);
-#pragma unroll
-      for (int j = 0; j < D; ++j) {
-        const Shape sh = make_shape(src.theta[row * 2 * D + 2 * j], src.theta[row * 2 * D + 2 * j + 1]);
-        const Quantile q = kumaraswamy_w(w.w[j], sh);
-        x[j] = q.x;
-        if constexpr (kHD8) {
-          if (j == 0) lnx1 = log_x(q, sh);
-          if (j == D - 1) ln1mx3 = log1mexp(log_x(q, sh));
-        }
-      }
-    } else {
-#pragma unroll
-      for (int j = 0; j < D; ++j) x[j] = xin[i * D + j];
-      lnx1 = logf(x[0]);
-      ln1mx3 = log1pf(-x[D - 1]);
+__device__ __forceinline__ float event_coord(const EventArgs& ev, int64_t i, bool valid, int j, float a, float b,
+                                             float& lg) {
+  lg = 0.f;
+  if (!valid) {
+    if (kHD8) lg = logf(0.5f);
+    return 0.5f;
+  }
+  if (ev.sampled) {
+    const Words w = event_words(ev.src.base + (uint64_t)i, ev.src.stream, ev.src.k0, ev.src.k1);
+    const uint32_t wj = j == 0 ? w.w[0] : (j == 1 ? w.w[1] : w.w[2]);
+    const Shape sh = make_shape(a, b);
+    const Quantile q = kumaraswamy_w(wj, sh);
+    if (kHD8) {
+      const float lx = log_x(q, sh);
+      if (j == 0) lg = lx;
+      else if (j == D - 1) lg = log1mexp(lx);
     }
-  } else {
-#pragma unroll
-    for (int j = 0; j < D; ++j) x[j] = 0.5f;
-    lnx1 = logf(0.5f);
-    ln1mx3 = logf(0.5f);
+    return q.x;
   }
-  if (c.fake) {
-#pragma unroll
-    for (int j = 0; j < D; ++j) xs[(int64_t)r * D + j] = x[j];
+  if (kHD8) {
+    if (j == 0) lg = logf(a);
+    else if (j == D - 1) lg = log1pf(-a);
   }
-  float f[F];
-  if constexpr (kHD8) {
-    f[0] = x[0]; f[1] = x[1]; f[2] = x[2];
-    f[3] = x[0] * x[1]; f[4] = x[1] * x[2]; f[5] = x[0] * x[2];
-    f[6] = lnx1;
-    f[7] = ln1mx3;
-  } else {
+  return a;
+}
+
+// A tile's events in LDS: thread t < T D computes coordinate j = t / T of
+// event e = t % T (j is wave-uniform) into sx[e][j] and, for HD8, the log
+// feature into slg[e][0 or 1].  EU pieces per thread; the fetched registers
+// hold the next tile's inputs.
+template <int T, int D, int NTH>
+struct TileEvents {
+  static constexpr int EU = (T * D + NTH - 1) / NTH;
+  float a[EU], b[EU];
+
+  __device__ __forceinline__ void fetch(const EventArgs& ev, const ChunkArgs& c, int tile, int tid) {
 #pragma unroll
-    for (int j = 0; j < D; ++j) f[j] = x[j];
+    for (int u = 0; u < EU; ++u) {
+      const int q = tid + NTH * u, e = q % T, j = q / T, r = tile * T + e;
+      if (q < T * D) event_fetch<D>(ev, c.row0 + r, r < c.valid, j, a[u], b[u]);
+    }
   }
+  template <bool kHD8>
+  __device__ __forceinline__ void form(const EventArgs& ev, const ChunkArgs& c, int tile, int tid, float* sx,
+                                       float* slg) {
 #pragma unroll
-  for (int j = 0; j < F; ++j) feat[(int64_t)r * F + j] = f[j];
+    for (int u = 0; u < EU; ++u) {
+      const int q = tid + NTH * u, e = q % T, j = q / T, r = tile * T + e;
+      if (q < T * D) {
+        float lg;
+        sx[e * D + j] = event_coord<D, kHD8>(ev, c.row0 + r, r < c.valid, j, a[u], b[u], lg);
+        if (kHD8 && j != 1) slg[2 * e + (j == 0 ? 0 : 1)] = lg;
+      }
+    }
+  }
+};
+
+// HD8 features of event e from its coordinates and log features:
+// [x1, x2, x3, x1 x2, x2 x3, x1 x3, ln x1, ln(1 - x3)].
+__device__ __forceinline__ void hd8_features(const float* sx, const float* slg, int e, float* f) {
+  const float x1 = sx[3 * e], x2 = sx[3 * e + 1], x3 = sx[3 * e + 2];
+  f[0] = x1; f[1] = x2; f[2] = x3;
+  f[3] = x1 * x2; f[4] = x2 * x3; f[5] = x1 * x3;
+  f[6] = slg[2 * e];
+  f[7] = slg[2 * e + 1];
 }
 
 // ---------------------------------------------------------------------------
@@ -554,8 +605,7 @@ struct ChainArgs {
   int NH;
   ChunkArgs c;
   float inv_n;               // 1 / (events of this batch)
-  const float* feat;         // [rows][F]
-  const float* xs;           // [rows][D] (fake chunks)
+  EventArgs ev;              // this chunk's events (sampled or from a buffer)
   u16* act;                  // [NH][rows H]: A_1 .. A_NH, K-fragment order
   u16* dlt;                  // [NH][rows H]: unit-seed signal at A_2 .. A_{NH+1}, K-fragment order
   uint32_t* mask;            // [NH + 1][rows / T][WAVES][64 lanes][4]: signs of A_1 .. A_{NH+1}
@@ -571,19 +621,21 @@ struct ChainArgs {
 // softplus(t) = max(t, 0) + ln(1 + e^-|t|), on the hardware units.
 __device__ __forceinline__ float softplus_fast(float t) { return fmaxf(t, 0.0f) + log1p_k(fast_exp(-fabsf(t))); }
 
-// Forward chain of one chunk: A_1 (fp32 matrix cores, K = F + 1) -> hidden
-// layers -> logit z, BCE seeds e_D and e_G, and per-workgroup partials of
-// dW_o, db_o and the loss sums.  Stores A_1 .. A_NH and the masks for later
-// kernels.  Each tile's features are staged through LDS, loaded one tile
-// ahead.
-template <int H, int F>
+// Forward chain of one chunk: the tile's events sampled (or read) into LDS,
+// A_1 (fp32 matrix cores, K = F + 1) -> hidden layers -> logit z, BCE seeds
+// e_D and e_G, and per-workgroup partials of dW_o, db_o and the loss sums.
+// Stores A_1 .. A_NH, the masks and the top layer's sign bytes for later
+// kernels.
+template <int H, int F, int D, bool kHD8>
 __global__ __launch_bounds__(Chain<H>::THREADS, Chain<H>::BPC) void k_fwd_chain(ChainArgs p) {
   using C = Chain<H>;
   constexpr int T = C::T, LDA = C::LDA, WAVES = C::WAVES, MT = C::MT, NT = C::NT, MW = C::MW, NTH = C::THREADS;
-  constexpr int FU = (T * F + NTH - 1) / NTH;   // staged feature values per thread
   constexpr int K1 = (F + 2) / 2;               // first-layer K steps of 2 (features, then the bias)
+  static_assert(kHD8 ? (F == 8 && D == 3) : F == D, "features");
   __shared__ __attribute__((aligned(16))) u16 act[T * LDA];
   __shared__ float sfeat[T * F];
+  __shared__ float sx[kHD8 ? T * D : 1];        // HD8: coordinates and log features, before the map
+  __shared__ float slg[kHD8 ? T * 2 : 1];
   __shared__ float zpart[WAVES][T];
   __shared__ float se_s[T];
   __shared__ __attribute__((aligned(16))) u16 sterm[3][T];   // e_D of each event as bf16 terms hi, mid, lo
@@ -635,28 +687,24 @@ __global__ __launch_bounds__(Chain<H>::THREADS, Chain<H>::BPC) void k_fwd_chain(
   float l0 = 0.f, l1 = 0.f, se = 0.f;           // loss and e_D sums of event tid (tid < T)
   WeightPrefetch<H> pf;
   prefetch_weights<H, true>(weight_rsrc<H, true>(p.Wb, 0), pf, woff);
-  float fst[FU];
-  // 32-bit offsets into a buffer resource: no 64-bit per-lane pointer stays live
-  // across the tile loop (the compiler would hoist and spill it)
-  const Rsrc rs_feat = make_rsrc(p.feat, (uint32_t)c.rows * F * 4u);
-  auto load_feat = [&](int tile) __attribute__((always_inline)) {
-#pragma unroll
-    for (int u = 0; u < FU; ++u) {
-      const int k = tid + NTH * u;
-      if (k < T * F) fst[u] = load_f32(rs_feat, (uint32_t)(tile * T * F + k) * 4u);
-    }
-  };
-  if ((int)blockIdx.x < ntiles) load_feat(blockIdx.x);
+  // the tile's events are formed in LDS from inputs fetched one tile ahead
+  TileEvents<T, D, NTH> te;
+  if ((int)blockIdx.x < ntiles) te.fetch(p.ev, c, blockIdx.x, tid);
   const f32x16 zero = {};
 
   for (int tile = blockIdx.x; tile < ntiles; tile += gridDim.x) {
     const int r0 = tile * T;
+    te.template form<kHD8>(p.ev, c, tile, tid, kHD8 ? sx : sfeat, slg);
+    if (tile + (int)gridDim.x < ntiles) te.fetch(p.ev, c, tile + gridDim.x, tid);
+    if constexpr (kHD8) {
+      __syncthreads();                            // coordinates staged
+      if (tid < T) {
+        float f[8];
+        hd8_features(sx, slg, tid, f);
 #pragma unroll
-    for (int u = 0; u < FU; ++u) {
-      const int k = tid + NTH * u;
-      if (k < T * F) sfeat[k] = fst[u];
+        for (int j = 0; j < 8; ++j) sfeat[tid * 8 + j] = f[j];
+      }
     }
-    if (tile + (int)gridDim.x < ntiles) load_feat(tile + gridDim.x);
     auto mask_at = [&](int layer) __attribute__((always_inline)) {
       return p.mask + ((((int64_t)layer * ntiles + tile) * WAVES + wave) * 64 + lane) * MW;
     };
@@ -837,20 +885,23 @@ __global__ __launch_bounds__(Chain<H>::THREADS, Chain<H>::BPC) void k_fwd_chain(
 // layer on the matrix cores: dW_1 and db_1 (signal times e_D times the
 // features, accumulated across tiles into per-workgroup partials) and, for
 // fake chunks, dL_G/dx (signal times W_1, scaled by e_G, through the HD8
-// Jacobian when used).  Each tile's seeds, features and events are staged
-// through LDS and its masks loaded into registers, all one step ahead.
+// Jacobian when used).  Each tile's events are formed in LDS again (sampled
+// or read, as in the forward chain), and its seeds and masks loaded one tile
+// ahead.
 template <int H, int F, int D, bool kHD8>
 __global__ __launch_bounds__(Chain<H>::THREADS, Chain<H>::BPC) void k_bwd_chain(ChainArgs p) {
   using C = Chain<H>;
   constexpr int T = C::T, LDA = C::LDA, WAVES = C::WAVES, MT = C::MT, NT = C::NT, MW = C::MW, NTH = C::THREADS;
-  constexpr int SU = (T * (2 + F + D) + NTH - 1) / NTH;   // staged values per thread
+  constexpr int SU = (2 * T + NTH - 1) / NTH;   // staged seed values per thread
   constexpr int KB = T / 16;                    // K steps of the dW_1 product (events)
   constexpr int NB = T / 32;                    // 32-event blocks of the dL/dx product
   constexpr int WPB = WAVES / NB;               // waves per event block (K split over hidden features)
   constexpr int KSW = C::KS / WPB;              // dL/dx K steps per wave
   static_assert(F <= 8 && D <= F && (WPB == 1 || WPB == 2) && (KB * 64) % NTH == 0, "first-layer layout");
+  static_assert(kHD8 ? (F == 8 && D == 3) : F == D, "features");
   __shared__ __attribute__((aligned(16))) u16 act[T * LDA];
   __shared__ float srow[T * (2 + F + D)];       // per event: e_D, e_G | features | x
+  __shared__ float slg[kHD8 ? T * 2 : 1];       // HD8: log features, before the map
   __shared__ __attribute__((aligned(16))) float swo[H];
   __shared__ __attribute__((aligned(16))) u16 sfp[KB * 64 * 8];   // dW_1 A operand of the tile
   __shared__ float sgx[WPB == 2 ? T * 8 : 1];   // dL/dx partials of the second K half
@@ -887,34 +938,22 @@ __global__ __launch_bounds__(Chain<H>::THREADS, Chain<H>::BPC) void k_bwd_chain(
     return ((uint32_t)(layer * ntiles + tile) * WAVES * 64u) * MW * 4u + mlane;
   };
   const Rsrc rs_eD = make_rsrc(p.eD, (uint32_t)c.rows * 4u), rs_eG = make_rsrc(p.eG, (uint32_t)c.rows * 4u);
-  const Rsrc rs_feat = make_rsrc(p.feat, (uint32_t)c.rows * F * 4u);
-  const Rsrc rs_xs = make_rsrc(p.xs, (uint32_t)c.rows * D * 4u);
-  // staged rows of a tile: value k of srow, from the seed, feature and event
-  // arrays.  The arrays' boundaries in k are multiples of T = 128, so the 64
-  // values of a wave come from one array: the choice is a scalar branch.
+  // the tile's seeds (value k of srow: e_D of event k / 2 for even k, e_G for
+  // odd k), loaded one tile ahead; its events formed in LDS from inputs
+  // fetched one tile ahead
   float sv[SU];
-  auto load_rows = [&](int tile) __attribute__((always_inline)) {
-    const int r0 = tile * T;
+  auto load_seeds = [&](int tile) __attribute__((always_inline)) {
 #pragma unroll
     for (int u = 0; u < SU; ++u) {
       const int k = tid + NTH * u;
-      const int kw = __builtin_amdgcn_readfirstlane(k - lane);   // the wave's first value
-      float v = 0.f;
-      if (kw < 2 * T) {
-        const uint32_t off = (uint32_t)(r0 + (k >> 1)) * 4u;
-        const float a = load_f32(rs_eD, off), g = load_f32(rs_eG, off);
-        v = (k & 1) ? g : a;
-      } else if (kw < (2 + F) * T) {
-        v = load_f32(rs_feat, (uint32_t)(r0 * F + (k - 2 * T)) * 4u);
-      } else if (kw < (2 + F + D) * T && want_dx && kHD8) {
-        v = load_f32(rs_xs, (uint32_t)(r0 * D + (k - (2 + F) * T)) * 4u);
-      }
-      sv[u] = v;
+      if (k < 2 * T) sv[u] = load_f32((k & 1) ? rs_eG : rs_eD, (uint32_t)(tile * T + (k >> 1)) * 4u);
     }
   };
+  TileEvents<T, D, NTH> te;
   uint32_t mtop[MW];
   if ((int)blockIdx.x < ntiles) {
-    load_rows(blockIdx.x);
+    load_seeds(blockIdx.x);
+    te.fetch(p.ev, c, blockIdx.x, tid);
     load_mask(rs_mask, mask_off(NH, blockIdx.x), mtop);
   }
   __syncthreads();                              // swo staged
@@ -925,9 +964,13 @@ __global__ __launch_bounds__(Chain<H>::THREADS, Chain<H>::BPC) void k_bwd_chain(
 #pragma unroll
     for (int u = 0; u < SU; ++u) {
       const int k = tid + NTH * u;
-      if (k < T * (2 + F + D)) srow[k] = sv[u];
+      if (k < 2 * T) se[k] = sv[u];
     }
-    if (next < ntiles) load_rows(next);
+    te.template form<kHD8>(p.ev, c, tile, tid, kHD8 ? sx : sfeat, slg);
+    if (next < ntiles) {
+      load_seeds(next);
+      te.fetch(p.ev, c, next, tid);
+    }
     // ---- unit-seed signal at A_{NH+1}: w_o * LeakyReLU'(A_{NH+1}) ----------
     {
       uint2 pk[MT][NT][4];
@@ -946,6 +989,15 @@ __global__ __launch_bounds__(Chain<H>::THREADS, Chain<H>::BPC) void k_bwd_chain(
           }
         }
       store_tile<MT, NT, LDA>(act, pk, ow, lane);
+    }
+    if constexpr (kHD8) {
+      __syncthreads();                           // coordinates staged
+      if (tid < T) {
+        float f[8];
+        hd8_features(sx, slg, tid, f);
+#pragma unroll
+        for (int j = 0; j < 8; ++j) sfeat[tid * 8 + j] = f[j];
+      }
     }
     __syncthreads();                             // the staged rows too
     // ---- dW_1 A operand: the split terms of e_D times each input ------------
@@ -1572,8 +1624,8 @@ struct Plan {
   int rows_max;          // padded rows of the largest chunk
   int blocks;            // workgroups of the chain kernels
   int slices;            // weight-gradient slices per chunk
-  size_t off_wb, off_wtb, off_w0f, off_feat, off_xs, off_act, off_dlt, off_mask, off_maskT, off_eD, off_eG, off_plog,
-      off_pfb, off_pw, off_pwdb, off_accl, total;
+  size_t off_wb, off_wtb, off_w0f, off_act, off_dlt, off_mask, off_maskT, off_eD, off_eG, off_plog, off_pfb, off_pw,
+      off_pwdb, off_accl, total;
 };
 
 int pad128(int64_t n) { return (int)((n + 127) / 128 * 128); }
@@ -1599,8 +1651,6 @@ Plan make_plan(const DiscArgs& a, int n_cu) {
   p.off_wb = o; o += al(2 * H * (H + 16) * NH);     // forward copies carry one bias step per 32 rows
   p.off_wtb = o; o += al(2 * H * H * NH);
   p.off_w0f = o; o += al(64 * H);                 // H / 16 pieces of 1 KB
-  p.off_feat = o; o += al(4 * R * p.F);
-  p.off_xs = o; o += al(4 * R * p.D);
   p.off_act = o; o += al(2 * R * H * NH);
   p.off_dlt = o; o += al(2 * R * H * (NH - 1));   // the top layer's signal is rebuilt from signs
   p.off_mask = o; o += al(8 * R * (H / 64) * (NH + 1));
@@ -1618,7 +1668,7 @@ Plan make_plan(const DiscArgs& a, int n_cu) {
 
 template <int H, int F, int D, bool kHD8>
 void launch_chains(const ChainArgs& ca, int blocks, bool bwd, hipStream_t st) {
-  if (!bwd) hipLaunchKernelGGL((k_fwd_chain<H, F>), dim3(blocks), dim3(Chain<H>::THREADS), 0, st, ca);
+  if (!bwd) hipLaunchKernelGGL((k_fwd_chain<H, F, D, kHD8>), dim3(blocks), dim3(Chain<H>::THREADS), 0, st, ca);
   else hipLaunchKernelGGL((k_bwd_chain<H, F, D, kHD8>), dim3(blocks), dim3(Chain<H>::THREADS), 0, st, ca);
 }
 
@@ -1692,8 +1742,6 @@ hipError_t launch_disc_bf16(const DiscArgs& a, void* ws, int n_cu, hipStream_t s
   ca.bo = Dm.b[NH + 1];
   ca.slope = Dm.leaky_slope;
   ca.NH = NH;
-  ca.feat = F32(p.off_feat);
-  ca.xs = F32(p.off_xs);
   ca.act = B16(p.off_act);
   ca.dlt = B16(p.off_dlt);
   ca.mask = reinterpret_cast<uint32_t*>(base + p.off_mask);
@@ -1717,13 +1765,9 @@ hipError_t launch_disc_bf16(const DiscArgs& a, void* ws, int n_cu, hipStream_t s
       c.fake = fake ? 1 : 0;
       const int first = chunk_index == 0 ? 1 : 0;
       const int first_batch = row0 == 0 ? 1 : 0;
-      const dim3 g1((c.rows + 255) / 256);
-      const float* xin = fake ? a.fake_x : a.real_x;
-      const int samp = (fake && sampled) ? 1 : 0;
-      if (p.hd8) hipLaunchKernelGGL((k_prep<3, true>), g1, dim3(256), 0, st, c, xin, src, samp, F32(p.off_feat), F32(p.off_xs));
-      else if (p.D == 2) hipLaunchKernelGGL((k_prep<2, false>), g1, dim3(256), 0, st, c, xin, src, samp, F32(p.off_feat), F32(p.off_xs));
-      else hipLaunchKernelGGL((k_prep<3, false>), g1, dim3(256), 0, st, c, xin, src, samp, F32(p.off_feat), F32(p.off_xs));
-
+      ca.ev.src = src;
+      ca.ev.xin = fake ? a.fake_x : a.real_x;
+      ca.ev.sampled = (fake && sampled) ? 1 : 0;
       ca.c = c;
       ca.inv_n = fake ? inv_nf : inv_nr;
       ca.logits = fake ? out.logits_fake : out.logits_real;
