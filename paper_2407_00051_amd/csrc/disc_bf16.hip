@@ -170,6 +170,86 @@ __global__ __launch_bounds__(256) void k_w0_frag(const float* __restrict__ W0, i
 }
 
 // ---------------------------------------------------------------------------
+// The forward chain's first layer, z = W_1 x + b_1 with K = F inputs, on the
+// bf16 matrix cores: every fp32 weight, bias and input is split into its three
+// exact bf16 terms hi + mid + lo (bias_terms), and the K dimension holds the
+// term products that reach fp32 accuracy.  Slot k < 6 F pairs term a(p) of
+// W_1[f][j] with term b(p) of x[e][j], p = k / F, j = k % F, for the pairs
+// p = (hi,hi), (hi,mid), (mid,hi), (hi,lo), (mid,mid), (lo,hi); the three
+// pairs left out are each below 2^-25 of |W_1[f][j] x[e][j]|, under fp32
+// rounding.  Slots 6 F .. 6 F + 2 hold the bias terms against 1, the rest 0.
+// Every product of two bf16 terms is exact in fp32, so z carries only the
+// fp32 accumulation's rounding and the dropped pairs.
+template <int F>
+struct FirstLayer {
+  static constexpr int KS = (6 * F + 3 + 15) / 16;   // K steps of 16
+  static constexpr int KP = 16 * KS;                 // slots
+  static constexpr int LDB = KP + 8;                 // LDS row stride (bf16) of the input slots
+};
+
+__host__ __device__ constexpr int pair_a(int p) { return (p == 2 || p == 4) ? 1 : (p == 5 ? 2 : 0); }
+__host__ __device__ constexpr int pair_b(int p) { return (p == 1 || p == 4) ? 1 : (p == 3 ? 2 : 0); }
+
+// k_w1_frag: the weight side as MFMA A fragments, piece (rb, s, lane) =
+// row 32 rb + lane % 32, slots 16 s + 8 (lane / 32) .. + 7.
+template <int F>
+__global__ __launch_bounds__(256) void k_w1_frag(const float* __restrict__ W0, const float* __restrict__ b0, int H,
+                                                 u16* __restrict__ out) {
+  using L = FirstLayer<F>;
+  const int t = blockIdx.x * 256 + threadIdx.x;
+  if (t >= (H / 32) * L::KS * 64) return;
+  const int rb = t / (L::KS * 64), sidx = (t / 64) % L::KS, lane = t % 64;
+  const int f = 32 * rb + (lane & 31);
+  uint32_t w[4];
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    uint32_t h2[2];
+#pragma unroll
+    for (int e = 0; e < 2; ++e) {
+      const int k = 16 * sidx + 8 * (lane >> 5) + 2 * u + e;
+      u16 v = 0;
+      if (k < 6 * F) v = bf16_term(W0[f * F + k % F], pair_a(k / F));
+      else if (k < 6 * F + 3) v = bf16_term(b0[f], k - 6 * F);
+      h2[e] = v;
+    }
+    w[u] = h2[0] | (h2[1] << 16);
+  }
+  *reinterpret_cast<uint4*>(out + (size_t)t * 8) = make_uint4(w[0], w[1], w[2], w[3]);
+}
+
+// The input side of one event: its KP slots (row e of the [T][LDB] array the
+// B fragments are read from), from its F inputs.
+template <int F>
+__device__ __forceinline__ void first_layer_row(const float (&x)[F], u16* row) {
+  using L = FirstLayer<F>;
+  u16 t[F][3];
+#pragma unroll
+  for (int j = 0; j < F; ++j) {
+    uint32_t lo;
+    const uint32_t hm = bias_terms(x[j], lo);
+    t[j][0] = (u16)(hm & 0xffffu);
+    t[j][1] = (u16)(hm >> 16);
+    t[j][2] = (u16)lo;
+  }
+  constexpr u16 one = 0x3f80;
+#pragma unroll
+  for (int q = 0; q < L::KP / 8; ++q) {
+    uint32_t w[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      uint32_t h2[2];
+#pragma unroll
+      for (int e = 0; e < 2; ++e) {
+        const int k = 8 * q + 2 * u + e;
+        h2[e] = k < 6 * F ? t[k % F][pair_b(k / F)] : (k < 6 * F + 3 ? one : 0);
+      }
+      w[u] = h2[0] | (h2[1] << 16);
+    }
+    *reinterpret_cast<uint4*>(row + 8 * q) = make_uint4(w[0], w[1], w[2], w[3]);
+  }
+}
+
+// ---------------------------------------------------------------------------
 // Rows of one chunk.  Rows past `valid` are padding: coordinates 0.5, never
 // stored anywhere visible (their e_D and e_G are 0).
 struct ChunkArgs {
@@ -596,6 +676,7 @@ __device__ __forceinline__ void store_tile(u16* act, const uint2 (&pk)[MT][NT][4
 struct ChainArgs {
   const float* W0;           // first layer [H][F] fp32
   const u16* W0f;            // the same as split-term fragments (k_w0_frag)
+  const u16* W1f;            // W_1 and b_1 as first-layer slot fragments (k_w1_frag)
   const float* b0;           // [H]
   const u16* Wb;             // hidden layers, bf16, forward fragment order with the bias step
   const u16* WTb;            // the same, transposed ([in][out]), backward fragment order
@@ -630,15 +711,21 @@ template <int H, int F, int D, bool kHD8>
 __global__ __launch_bounds__(Chain<H>::THREADS, Chain<H>::BPC) void k_fwd_chain(ChainArgs p) {
   using C = Chain<H>;
   constexpr int T = C::T, LDA = C::LDA, WAVES = C::WAVES, MT = C::MT, NT = C::NT, MW = C::MW, NTH = C::THREADS;
-  constexpr int K1 = (F + 2) / 2;               // first-layer K steps of 2 (features, then the bias)
+  using L1 = FirstLayer<F>;
   static_assert(kHD8 ? (F == 8 && D == 3) : F == D, "features");
+  // The first layer's input slots ([T][L1::LDB] bf16) live in the activation
+  // tile where a separate array would not fit two workgroups per CU (or one)
+  // into the 160 KB of LDS; they are consumed before A_1 is written there.
+  constexpr size_t kLds = 2 * T * LDA + 4 * T * D + (kHD8 ? 8 * T : 4) + 4 * WAVES * T + 4 * T + 6 * T;
+  constexpr bool kAliasB = (kLds + 2 * T * L1::LDB) * C::BPC > 163840;
   __shared__ __attribute__((aligned(16))) u16 act[T * LDA];
-  __shared__ float sfeat[T * F];
-  __shared__ float sx[kHD8 ? T * D : 1];        // HD8: coordinates and log features, before the map
+  __shared__ __attribute__((aligned(16))) u16 sBbuf[kAliasB ? 8 : T * L1::LDB];
+  __shared__ float sx[T * D];                   // coordinates (and HD8 log features), before the feature map
   __shared__ float slg[kHD8 ? T * 2 : 1];
   __shared__ float zpart[WAVES][T];
   __shared__ float se_s[T];
   __shared__ __attribute__((aligned(16))) u16 sterm[3][T];   // e_D of each event as bf16 terms hi, mid, lo
+  u16* const sB = kAliasB ? act : sBbuf;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int lr = lane & 31, lh = lane >> 5;
   const int ow = 32 * MT * wave;
@@ -648,16 +735,9 @@ __global__ __launch_bounds__(Chain<H>::THREADS, Chain<H>::BPC) void k_fwd_chain(
   const int64_t rstride = (int64_t)c.rows;
   const int ntiles = c.rows / T;
   const float slope = p.slope;
-  // first-layer A fragments (v_mfma_f32_32x32x2f32: lane l holds row l % 32,
-  // K index l / 32 of each step): W0 columns, then b0, then zero
-  float w0f[MT][K1];
-#pragma unroll
-  for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-    for (int s = 0; s < K1; ++s) {
-      const int o = ow + 32 * mt + lr, k = 2 * s + lh;
-      w0f[mt][s] = k < F ? p.W0[o * F + k] : (k == F ? p.b0[o] : 0.f);
-    }
+  // the wave's first-layer weight fragments (k_w1_frag), loaded per tile
+  const Rsrc rs_w1 = make_rsrc(p.W1f, (uint32_t)(H / 32) * L1::KS * 1024u);
+  const uint32_t w1off = ((uint32_t)MT * wave * L1::KS * 64u + lane) * 16u;
   // logit A fragments: rows 0..2 are the bf16 terms hi, mid, lo of w_o (their
   // sum is w_o exactly), other rows zero; the K order matches the lane's
   // activations (see the logit below)
@@ -694,42 +774,47 @@ __global__ __launch_bounds__(Chain<H>::THREADS, Chain<H>::BPC) void k_fwd_chain(
 
   for (int tile = blockIdx.x; tile < ntiles; tile += gridDim.x) {
     const int r0 = tile * T;
-    te.template form<kHD8>(p.ev, c, tile, tid, kHD8 ? sx : sfeat, slg);
+    te.template form<kHD8>(p.ev, c, tile, tid, sx, slg);
     if (tile + (int)gridDim.x < ntiles) te.fetch(p.ev, c, tile + gridDim.x, tid);
-    if constexpr (kHD8) {
-      __syncthreads();                            // coordinates staged
-      if (tid < T) {
-        float f[8];
-        hd8_features(sx, slg, tid, f);
+    bf16x8 a1[MT][L1::KS];
 #pragma unroll
-        for (int j = 0; j < 8; ++j) sfeat[tid * 8 + j] = f[j];
-      }
-    }
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+      for (int s = 0; s < L1::KS; ++s) a1[mt][s] = load_frag(rs_w1, w1off, (uint32_t)(mt * L1::KS + s) * 1024u);
     auto mask_at = [&](int layer) __attribute__((always_inline)) {
       return p.mask + ((((int64_t)layer * ntiles + tile) * WAVES + wave) * 64 + lane) * MW;
     };
-    __syncthreads();                              // sfeat staged; last tile's readers of act are done
+    __syncthreads();                              // coordinates staged; last tile's readers of act are done
+    if (tid < T) {
+      float f[F];
+      if constexpr (kHD8) {
+        hd8_features(sx, slg, tid, f);
+      } else {
+#pragma unroll
+        for (int j = 0; j < F; ++j) f[j] = sx[tid * D + j];
+      }
+      first_layer_row<F>(f, sB + tid * L1::LDB);
+    }
+    __syncthreads();                              // input slots staged
 
-    // ---- first layer on the fp32 matrix cores ------------------------------
+    // ---- first layer on the bf16 matrix cores (split terms) ----------------
     {
-      float fb[NT][K1];                           // B: feature l / 32 + 2 s of event 32 nt + l % 32, then 1
-#pragma unroll
-      for (int nt = 0; nt < NT; ++nt)
-#pragma unroll
-        for (int s = 0; s < K1; ++s) {
-          const int k = 2 * s + lh;
-          fb[nt][s] = k < F ? sfeat[(32 * nt + lr) * F + k] : (k == F ? 1.f : 0.f);
-        }
       f32x16 v[MT][NT];
 #pragma unroll
-      for (int mt = 0; mt < MT; ++mt)
+      for (int nt = 0; nt < NT; ++nt) {
+        bf16x8 bfr[L1::KS];                       // slots 16 s + 8 (l / 32) .. + 7 of event 32 nt + l % 32
 #pragma unroll
-        for (int nt = 0; nt < NT; ++nt) {
-          v[mt][nt] = __builtin_amdgcn_mfma_f32_32x32x2f32(w0f[mt][0], fb[nt][0], zero, 0, 0, 0);
+        for (int s = 0; s < L1::KS; ++s)
+          bfr[s] = *reinterpret_cast<const bf16x8*>(sB + (32 * nt + lr) * L1::LDB + 16 * s + 8 * lh);
 #pragma unroll
-          for (int s = 1; s < K1; ++s)
-            v[mt][nt] = __builtin_amdgcn_mfma_f32_32x32x2f32(w0f[mt][s], fb[nt][s], v[mt][nt], 0, 0, 0);
+        for (int mt = 0; mt < MT; ++mt) {
+          v[mt][nt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1[mt][0], bfr[0], zero, 0, 0, 0);
+#pragma unroll
+          for (int s = 1; s < L1::KS; ++s)
+            v[mt][nt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1[mt][s], bfr[s], v[mt][nt], 0, 0, 0);
         }
+      }
+      if constexpr (kAliasB) __syncthreads();     // every wave has read the slots before A_1 overwrites them
       uint2 pk[MT][NT][4];
       uint32_t m[MW];
       activate<MT, NT>(v, slope, pk, m);
@@ -1206,6 +1291,11 @@ __device__ __forceinline__ void top_values(const TopSignal& ts, int o, uint32_t&
   dneg = (uint32_t)bf16_bits(ts.slope * w) << 16;
 }
 
+// One sign byte (per-lane offset voff, scalar offset soff).
+__device__ __forceinline__ uint32_t top_byte(Rsrc r, uint32_t voff, uint32_t soff) {
+  return (uint32_t)__builtin_amdgcn_raw_buffer_load_b8(r, (int)voff, (int)soff, 0);
+}
+
 // Byte offset of the sign byte of K block kb in the lane's column block.
 __device__ __forceinline__ uint32_t top_koff(int kb, int CB) { return (uint32_t)(kb >> 3) * CB * 512u + (kb & 7); }
 
@@ -1247,7 +1337,10 @@ __global__ __launch_bounds__(kWThreads, 1) void k_wgrad(const u16* __restrict__ 
   const u16* pb = A + (((size_t)kb0 * CB + ib) * 64 + lane) * 8;
   const float* pe = eD + (size_t)kb0 * 16 + 8 * lh;    // rows of the lane's half of each K block
   constexpr size_t KSTRIDE = (size_t)CB * 512;          // bf16 per K block
-  const uint8_t* pm = ts.maskT + ((size_t)ob * 64 + lane) * 8;   // kTop: sign bytes of column block ob
+  // kTop: sign bytes through a buffer resource (per-lane offset of column
+  // block ob, the K block's offset a scalar)
+  const Rsrc rm_top = make_rsrc(ts.maskT, (uint32_t)kb_total * CB * 64u);
+  const uint32_t moff = ((uint32_t)ob * 64u + lane) * 8u;
   uint32_t dpos[FM], dneg[FM];
   if constexpr (kTop) {
 #pragma unroll
@@ -1269,7 +1362,7 @@ __global__ __launch_bounds__(kWThreads, 1) void k_wgrad(const u16* __restrict__ 
   auto load = [&](int slot, int k) __attribute__((always_inline)) {
 #pragma unroll
     for (int m = 0; m < FM; ++m) {
-      if constexpr (kTop) fm[slot][m] = pm[top_koff(kb0 + k, CB) + m * 512];
+      if constexpr (kTop) fm[slot][m] = top_byte(rm_top, moff, top_koff(kb0 + k, CB) + m * 512);
       else fa[slot][m] = *reinterpret_cast<const bf16x8*>(pa + k * KSTRIDE + m * 512);
     }
 #pragma unroll
@@ -1316,7 +1409,8 @@ __global__ __launch_bounds__(kWThreads, 1) void k_wgrad(const u16* __restrict__ 
 #pragma unroll
     for (int i = 0; i < FM * FN; ++i) {
       __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // one product
-      __builtin_amdgcn_sched_group_barrier(0x002, 8, 0);   // eight vector ALU instructions
+      // eight vector ALU instructions (nine with the sign-bit selects of kTop)
+      __builtin_amdgcn_sched_group_barrier(0x002, kTop ? 9 : 8, 0);
     }
     __builtin_amdgcn_sched_barrier(0);
   };
@@ -1427,7 +1521,8 @@ __global__ __launch_bounds__(kWThreads, 1) void k_wgrad_shared(const u16* __rest
   const u16* pa = dsc + (((size_t)kb0 * CB + ob) * 64 + lane) * 8;
   const u16* pb = A + (((size_t)kb0 * CB + ib + 2 * wave) * 64 + lane) * 8;   // this wave's two A fragments
   const float* pe = eD + (size_t)kb0 * 16 + 8 * lh;
-  const uint8_t* pm = ts.maskT + ((size_t)ob * 64 + lane) * 8;   // kTop: sign bytes of column block ob
+  const Rsrc rm_top = make_rsrc(ts.maskT, (uint32_t)kb_total * CB * 64u);   // kTop: as in k_wgrad
+  const uint32_t moff = ((uint32_t)ob * 64u + lane) * 8u;
   uint32_t dpos[FM], dneg[FM];
   if constexpr (kTop) {
 #pragma unroll
@@ -1450,7 +1545,7 @@ __global__ __launch_bounds__(kWThreads, 1) void k_wgrad_shared(const u16* __rest
     for (int j = 0; j < 2; ++j) ra[slot][j] = *reinterpret_cast<const bf16x8*>(pb + k * KSTRIDE + j * 512);
 #pragma unroll
     for (int m = 0; m < FM; ++m) {
-      if constexpr (kTop) rm[slot][m] = pm[top_koff(kb0 + k, CB) + m * 512];
+      if constexpr (kTop) rm[slot][m] = top_byte(rm_top, moff, top_koff(kb0 + k, CB) + m * 512);
       else rd[slot][m] = *reinterpret_cast<const bf16x8*>(pa + k * KSTRIDE + m * 512);
     }
     re[slot][0] = *reinterpret_cast<const f32x4*>(pe + (size_t)k * 16);
@@ -1506,7 +1601,8 @@ __global__ __launch_bounds__(kWThreads, 1) void k_wgrad_shared(const u16* __rest
 #pragma unroll
     for (int i = 0; i < FM * FN; ++i) {
       __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // one product
-      __builtin_amdgcn_sched_group_barrier(0x002, 4, 0);   // four vector ALU instructions
+      // four vector ALU instructions (five with the sign-bit selects of kTop)
+      __builtin_amdgcn_sched_group_barrier(0x002, kTop ? 5 : 4, 0);
     }
     __builtin_amdgcn_sched_barrier(0);
     lds_barrier();
@@ -1624,7 +1720,7 @@ struct Plan {
   int rows_max;          // padded rows of the largest chunk
   int blocks;            // workgroups of the chain kernels
   int slices;            // weight-gradient slices per chunk
-  size_t off_wb, off_wtb, off_w0f, off_act, off_dlt, off_mask, off_maskT, off_eD, off_eG, off_plog, off_pfb, off_pw,
+  size_t off_wb, off_wtb, off_w0f, off_w1f, off_act, off_dlt, off_mask, off_maskT, off_eD, off_eG, off_plog, off_pfb, off_pw,
       off_pwdb, off_accl, total;
 };
 
@@ -1651,6 +1747,7 @@ Plan make_plan(const DiscArgs& a, int n_cu) {
   p.off_wb = o; o += al(2 * H * (H + 16) * NH);     // forward copies carry one bias step per 32 rows
   p.off_wtb = o; o += al(2 * H * H * NH);
   p.off_w0f = o; o += al(64 * H);                 // H / 16 pieces of 1 KB
+  p.off_w1f = o; o += al(32 * H * 4);             // (H / 32) x at most 4 pieces of 1 KB
   p.off_act = o; o += al(2 * R * H * NH);
   p.off_dlt = o; o += al(2 * R * H * (NH - 1));   // the top layer's signal is rebuilt from signs
   p.off_mask = o; o += al(8 * R * (H / 64) * (NH + 1));
@@ -1726,6 +1823,13 @@ hipError_t launch_disc_bf16(const DiscArgs& a, void* ws, int n_cu, hipStream_t s
     hipLaunchKernelGGL(k_weights_frag, dim3(((H / 32) * (H / 16 + 1) * 64 + 255) / 256), dim3(256), 0, st, Dm.W[1 + l],
                        Dm.b[1 + l], Wb + (size_t)l * H * (H + 16), WTb + (size_t)l * H * H, H);
   hipLaunchKernelGGL(k_w0_frag, dim3((H / 16) * 64 / 256), dim3(256), 0, st, Dm.W[0], p.F, H, B16(p.off_w0f));
+  {
+    const int F = p.F, pieces = (H / 32) * ((6 * F + 3 + 15) / 16) * 64;
+    const dim3 g((pieces + 255) / 256);
+    if (F == 2) hipLaunchKernelGGL(k_w1_frag<2>, g, dim3(256), 0, st, Dm.W[0], Dm.b[0], H, B16(p.off_w1f));
+    else if (F == 3) hipLaunchKernelGGL(k_w1_frag<3>, g, dim3(256), 0, st, Dm.W[0], Dm.b[0], H, B16(p.off_w1f));
+    else hipLaunchKernelGGL(k_w1_frag<8>, g, dim3(256), 0, st, Dm.W[0], Dm.b[0], H, B16(p.off_w1f));
+  }
   if (tm) tm->end();
 
   SourceArgs src{};
@@ -1735,6 +1839,7 @@ hipError_t launch_disc_bf16(const DiscArgs& a, void* ws, int n_cu, hipStream_t s
   ChainArgs ca{};
   ca.W0 = Dm.W[0];
   ca.W0f = B16(p.off_w0f);
+  ca.W1f = B16(p.off_w1f);
   ca.b0 = Dm.b[0];
   ca.Wb = Wb;
   ca.WTb = WTb;
