@@ -1451,15 +1451,18 @@ __global__ __launch_bounds__(kWThreads, 1) void k_wgrad(const u16* __restrict__ 
 // LDS.  A workgroup's four waves all need the eight A fragments (256 columns)
 // of every K step; instead of each wave streaming all eight, wave w fetches
 // fragments 2w and 2w + 1 into registers kWLG steps ahead, writes them into
-// one of three LDS slots two steps ahead, and every wave reads the eight from
+// LDS slot k mod kWNS three steps ahead, and every wave reads the eight from
 // there one step ahead, so the reads of step k + 1 overlap the products of
 // step k.  This cuts the traffic into the CU to one copy of each operand and
-// lets the register prefetch run far enough ahead to cover HBM latency.  One
-// barrier per K step publishes a slot; the loads in flight are not waited for
-// at the barrier.  Fragment order, scaling, rounding and the order of the
-// products are those of k_wgrad, so the partials are bit-identical to it.
+// lets the register prefetch run far enough ahead to cover HBM latency.  A
+// barrier after every second K step publishes the slots written since the
+// last one (three steps ahead, every slot is published before it is read and
+// read by every wave before it is written again); the loads in flight are not
+// waited for at the barrier.  Fragment order, scaling, rounding and the order
+// of the products are those of k_wgrad, so the partials are bit-identical to
+// it.
 constexpr int kWLG = 5;      // register prefetch distance (K steps) of k_wgrad_shared
-constexpr int kWNS = 6;      // register ring slots: kWLG + 1, even so that step parity is a constant
+constexpr int kWNS = 6;      // register and LDS ring slots: kWLG + 1, even so that step parity is a constant
 
 // Steps Q = 0 .. N-1 of one pass of the register ring, as a compile-time
 // sequence: run() with every step prefetching, tail() with the bounds checked.
@@ -1474,7 +1477,7 @@ struct WRing {
   __device__ __forceinline__ static void tail(F& f, int k0, int nk) {
     WRing<N - 1>::tail(f, k0, nk);
     const int k = k0 + N - 1;
-    if (k < nk) f(std::integral_constant<int, N - 1>{}, k, k + 1 < nk, k + 2 < nk, k + kWLG < nk);
+    if (k < nk) f(std::integral_constant<int, N - 1>{}, k, k + 1 < nk, k + 3 < nk, k + kWLG < nk);
   }
 };
 template <>
@@ -1500,9 +1503,9 @@ __global__ __launch_bounds__(kWThreads, 1) void k_wgrad_shared(const u16* __rest
   constexpr int CB = H / 32;      // 16
   constexpr int FM = 2, FN = 8;   // a wave owns 64 output rows x all 256 columns of the tile
   constexpr int NS = kWNS;
-  static_assert(NS == kWLG + 1 && NS % 6 == 0, "ring slots: step parity and step mod 3 must be constants");
+  static_assert(NS == kWLG + 1 && NS % 2 == 0, "ring slots: step parity must be a constant");
   constexpr size_t KSTRIDE = (size_t)CB * 512;
-  __shared__ __attribute__((aligned(16))) u16 sb[3][FN][512];
+  __shared__ __attribute__((aligned(16))) u16 sb[NS][FN][512];
   int tile, slice;
   if (xcd_map) {
     const int x = blockIdx.x % 8, r = blockIdx.x / 8;
@@ -1586,8 +1589,8 @@ __global__ __launch_bounds__(kWThreads, 1) void k_wgrad_shared(const u16* __rest
   // vector ALU work would otherwise wait for the products' issue).
   auto step = [&](auto qc, int k, bool get_next, bool put_ahead, bool load_ahead) __attribute__((always_inline)) {
     constexpr int q = decltype(qc)::value;
-    if (get_next) get((q + 1) % 3, (q + 1) & 1);
-    if (put_ahead) put((q + 2) % NS, (q + 2) % 3);
+    if (get_next) get((q + 1) % NS, (q + 1) & 1);
+    if (put_ahead) put((q + 3) % NS, (q + 3) % NS);
     if (load_ahead) load((q + kWLG) % NS, k + kWLG);
     // keep each step's work inside the step: the scheduler would otherwise
     // hoist later steps' scaling above their loads' waits
@@ -1605,7 +1608,7 @@ __global__ __launch_bounds__(kWThreads, 1) void k_wgrad_shared(const u16* __rest
       __builtin_amdgcn_sched_group_barrier(0x002, kTop ? 5 : 4, 0);
     }
     __builtin_amdgcn_sched_barrier(0);
-    lds_barrier();
+    if (q & 1) lds_barrier();
   };
   if (nk > 0) {
     // prologue without branches (a step past the slice reloads its last step,
@@ -1614,6 +1617,7 @@ __global__ __launch_bounds__(kWThreads, 1) void k_wgrad_shared(const u16* __rest
     for (int q = 0; q < kWLG; ++q) load(q, min(q, nk - 1));
     put(0, 0);
     put(1, 1);
+    put(2, 2);
     lds_barrier();
     get(0, 0);
     scale(0, 0);
