@@ -90,7 +90,10 @@ __device__ __forceinline__ f32x4 mfma4(float a, float b, f32x4 c) {
 __device__ __forceinline__ float leaky(float v, float s) { return v > 0.0f ? v : s * v; }
 __device__ __forceinline__ float leaky_grad(float h, float s) { return h > 0.0f ? 1.0f : s; }
 
-__device__ __forceinline__ float softplus(float t) { return fmaxf(t, 0.0f) + log1pf(expf(-fabsf(t))); }
+// softplus(t) = max(t, 0) + ln(1 + e^-|t|) on the hardware units (exp2 and
+// log2 within 1 ulp; Kahan's log1p keeps the small-argument accuracy).  Only
+// one lane in eight evaluates the seeds of an event, so their latency shows.
+__device__ __forceinline__ float softplus(float t) { return fmaxf(t, 0.0f) + log1p_k(fast_exp(-fabsf(t))); }
 
 template <int H, int NH, int DX, int F, int FEAT>
 struct Fused {
@@ -360,7 +363,7 @@ struct Fused {
         if (dpart == 0) {
           float eD = 0.f, eG = 0.f;
           if (valid) {
-            const float sig_neg = 1.0f / (1.0f + expf(z));   // sigmoid(-z)
+            const float sig_neg = fast_rcp(1.0f + fast_exp(z));   // sigmoid(-z)
             if (fake) {
               eD = (1.0f - sig_neg) * p.inv_nf;                // dL_D/dz = sigmoid(z)/N_f
               eG = -sig_neg * p.inv_nf;                        // dL_G/dz = (sigmoid(z)-1)/N_f
