@@ -256,6 +256,65 @@ def test_bf16_multi_chunk(gpu_ctx, name, n_theta, E, n_real, chunk):
     assert not bad_emu and not bad64, (bad_emu, bad64)
 
 
+@pytest.mark.parametrize("name,n_theta,E,n_real,chunk", [
+    ("medium", 3, 1000, 2999, 0),
+    ("medium", 3, 1000, 2999, 1024),     # buffer rows read from a chunk offset
+    ("higher_dim", 2, 777, 1500, 0),
+])
+def test_bf16_fake_buffer(gpu_ctx, name, n_theta, E, n_real, chunk):
+    """Fake events passed as a buffer (the sampler's output) instead of a source:
+    the chains read them from the buffer.  Identity features: every output equals
+    the source call's bit for bit (the same fp32 events).  HD8: the log features
+    of buffer events come from their fp32 values (A20), so the outputs are held
+    to the bf16-point oracle on those very events instead."""
+    from tests.parity import normwise
+    w = scaled(get(name), n_theta, E)
+    print(f"case {name} n_theta={n_theta} E={E} n_real={n_real} chunk={chunk} fake events from a buffer", flush=True)
+    inp, th, ts, W, b = _setup(w)
+    real = gpu_ctx.sample_events(ts, n_real, w.real_seed)
+    x = gpu_ctx.sample_events(th, E, w.fake_seed)
+    feats = sg.FEAT_HD8 if w.features == "hd8" else sg.FEAT_IDENTITY
+    gpu_ctx.set_bf16_chunk_rows(chunk)
+    try:
+        o = gpu_ctx.disc_fwd_bwd(W, b, real, fake_x=x, precision=sg.BF16, features=feats)
+        torch.cuda.synchronize()
+    finally:
+        gpu_ctx.set_bf16_chunk_rows(0)
+    if w.features == "identity":
+        src = _run(gpu_ctx, w, th, ts, W, b, n_real)
+        for k in ("logits_fake", "logits_real", "dLg_dx"):
+            assert torch.equal(o[k], src[k]), k
+        for k in ("loss_d", "loss_g"):   # sums chunk by chunk: fp32 reordering only
+            assert o[k].item() == src[k].item() if not chunk else abs(o[k].item() - src[k].item()) <= 1e-6 * abs(src[k].item()), k
+        for l in range(len(W)):
+            if chunk:          # partials summed chunk by chunk: fp32 reordering only
+                assert normwise(to_np(o["dW"][l]), to_np(src["dW"][l])) <= 1e-5, l
+                assert normwise(to_np(o["db"][l]), to_np(src["db"][l])) <= 1e-5, l
+            else:
+                assert torch.equal(o["dW"][l], src["dW"][l]) and torch.equal(o["db"][l], src["db"][l]), l
+        return
+    xf = to_np(x).astype(np.float64)
+    xr = to_np(real).astype(np.float64)
+    r = oracle.disc_fwd_bwd(inp["W"], inp["b"], oracle.features_hd8(xf), oracle.features_hd8(xr), bf16=True)
+    r64 = oracle.disc_fwd_bwd(inp["W"], inp["b"], oracle.features_hd8(xf), oracle.features_hd8(xr))
+    J = oracle.features_hd8_jacobian(xf)
+    g = np.einsum("nf,nfd->nd", r["dLg_din"], J)
+    gc = np.einsum("nf,nfd->nd", r64["dLg_din_cond"], np.abs(J))
+    assert_normwise(to_np(o["logits_fake"]), r["logits_fake"], TOL_EMU, "buffer logits_fake vs bf16-point oracle")
+    assert_normwise(to_np(o["logits_real"]), r["logits_real"], TOL_EMU, "buffer logits_real vs bf16-point oracle")
+    for k in ("loss_d", "loss_g"):
+        assert abs(o[k].item() - r[k]) <= TOL_EMU * abs(r[k]), k
+    for l in range(len(W)):          # normwise, or every entry against its sum of |terms| (as in _check)
+        for k in ("dW", "db"):
+            got = to_np(o[k][l]).astype(np.float64)
+            e = normwise(got, r[k][l])
+            worst = float(np.max(np.abs(got - r[k][l]) / np.maximum(r64[k + "_cond"][l], 1e-300)))
+            print(f"  buffer {k}[{l}] vs bf16-point oracle: normwise {e:.3e}, max |err|/sum|terms| {worst:.3e}",
+                  flush=True)
+            assert e <= TOL_EMU or worst <= TOL_EMU, (k, l)
+    assert _check_dx(to_np(o["dLg_dx"]), g, gc, TOL_EMU, "buffer vs bf16-point oracle") is None
+
+
 def test_bf16_chunk_rows_validation(gpu_ctx):
     for bad in (1, 127, 200, (1 << 22) + 128, -128):
         with pytest.raises(sg.SagipsError) as ei:
