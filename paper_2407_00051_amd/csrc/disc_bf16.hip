@@ -6,7 +6,7 @@
 //   k_fwd_chain  per tile of rows, in LDS: the tile's events (fake events
 //                sampled there from their Philox words, real ones read), their
 //                features, A_1 = bf16(LeakyReLU(feat W1^T + b1))
-//                (fp32 matrix cores, K <= 8 plus the bias), then every hidden
+//                (bf16 matrix cores on exact split terms), then every hidden
 //                layer on the bf16 matrix cores, then the logit z and the BCE
 //                seeds e_D, e_G; stores A_1 .. A_NH, the activation sign
 //                masks and the top layer's sign bits
@@ -390,7 +390,7 @@ __device__ __forceinline__ void hd8_features(const float* sx, const float* slg, 
 // The VALU work per output is kept to the LeakyReLU (two operations), the
 // bf16 rounding (half of a v_cvt_pk_bf16_f32) and a quarter of the sign-mask
 // packing: biases enter the forward products as one more K step, and the
-// first layer (fp32, K = F + 1 with the bias) and the logit (bf16 activations
+// first layer (exact bf16 split terms, with the bias) and the logit (bf16 activations
 // against the fp32 w_o split into three bf16 terms) also run on the matrix
 // cores.
 //
@@ -703,7 +703,7 @@ struct ChainArgs {
 __device__ __forceinline__ float softplus_fast(float t) { return fmaxf(t, 0.0f) + log1p_k(fast_exp(-fabsf(t))); }
 
 // Forward chain of one chunk: the tile's events sampled (or read) into LDS,
-// A_1 (fp32 matrix cores, K = F + 1) -> hidden layers -> logit z, BCE seeds
+// A_1 (bf16 matrix cores on split terms) -> hidden layers -> logit z, BCE seeds
 // e_D and e_G, and per-workgroup partials of dW_o, db_o and the loss sums.
 // Stores A_1 .. A_NH, the masks and the top layer's sign bytes for later
 // kernels.
