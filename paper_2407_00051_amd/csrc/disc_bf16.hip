@@ -341,20 +341,31 @@ struct TileEvents {
       if (q < T * D) event_fetch<D>(ev, c.row0 + r, r < c.valid, j, a[u], b[u]);
     }
   }
+  // With xg the coordinates also go to xg[row][D] (chunk rows, padding included).
   template <bool kHD8>
   __device__ __forceinline__ void form(const EventArgs& ev, const ChunkArgs& c, int tile, int tid, float* sx,
-                                       float* slg) {
+                                       float* slg, float* xg = nullptr) {
 #pragma unroll
     for (int u = 0; u < EU; ++u) {
       const int q = tid + NTH * u, e = q % T, j = q / T, r = tile * T + e;
       if (q < T * D) {
         float lg;
-        sx[e * D + j] = event_coord<D, kHD8>(ev, c.row0 + r, r < c.valid, j, a[u], b[u], lg);
+        const float x = event_coord<D, kHD8>(ev, c.row0 + r, r < c.valid, j, a[u], b[u], lg);
+        sx[e * D + j] = x;
+        if (xg) xg[(size_t)r * D + j] = x;
         if (kHD8 && j != 1) slg[2 * e + (j == 0 ? 0 : 1)] = lg;
       }
     }
   }
 };
+
+// Hidden width 256 with two identity features: the first hidden layer's weight
+// gradient rebuilds A_1 from the events' coordinates (8 bytes a row) instead
+// of reading a stored copy (512 bytes a row, written by the forward chain),
+// when that layer is not also the top one (whose kernel rebuilds its signal
+// from sign bytes instead): NH >= 2, checked at run time.
+template <int H, int F, bool kHD8>
+constexpr bool kRebuildA1 = H == 256 && F == 2 && !kHD8;
 
 // HD8 features of event e from its coordinates and log features:
 // [x1, x2, x3, x1 x2, x2 x3, x1 x3, ln x1, ln(1 - x3)].
@@ -687,7 +698,8 @@ struct ChainArgs {
   ChunkArgs c;
   float inv_n;               // 1 / (events of this batch)
   EventArgs ev;              // this chunk's events (sampled or from a buffer)
-  u16* act;                  // [NH][rows H]: A_1 .. A_NH, K-fragment order
+  u16* act;                  // [NH][rows H]: A_1 .. A_NH, K-fragment order (A_1 not stored with kRebuildA1)
+  float* xs;                 // [rows][2]: the events' coordinates, with kRebuildA1
   u16* dlt;                  // [NH][rows H]: unit-seed signal at A_2 .. A_{NH+1}, K-fragment order
   uint32_t* mask;            // [NH + 1][rows / T][WAVES][64 lanes][4]: signs of A_1 .. A_{NH+1}
   uint8_t* maskT;            // [rows / T][H / 32][64 lanes][T / 16]: signs of A_{NH+1}, K-fragment order
@@ -774,7 +786,7 @@ __global__ __launch_bounds__(Chain<H>::THREADS, Chain<H>::BPC) void k_fwd_chain(
 
   for (int tile = blockIdx.x; tile < ntiles; tile += gridDim.x) {
     const int r0 = tile * T;
-    te.template form<kHD8>(p.ev, c, tile, tid, sx, slg);
+    te.template form<kHD8>(p.ev, c, tile, tid, sx, slg, kRebuildA1<H, F, kHD8> ? p.xs : nullptr);
     if (tile + (int)gridDim.x < ntiles) te.fetch(p.ev, c, tile + gridDim.x, tid);
     bf16x8 a1[MT][L1::KS];
 #pragma unroll
@@ -830,7 +842,8 @@ __global__ __launch_bounds__(Chain<H>::THREADS, Chain<H>::BPC) void k_fwd_chain(
       // the next product is layer l + 1, or the first hidden layer of the next
       // tile; then the product's input A_{l+1} goes to HBM
       chain_gemm<H, true>(weight_rsrc<H, true>(p.Wb, l), weight_rsrc<H, true>(p.Wb, last ? 0 : l + 1), woff, pf,
-                          act, acc, lane, wave, p.act + ((int64_t)l * rstride + r0) * H, coff, true);
+                          act, acc, lane, wave, p.act + ((int64_t)l * rstride + r0) * H, coff,
+                          !(kRebuildA1<H, F, kHD8> && l == 0 && p.NH > 1));
       uint2 pk[MT][NT][4];
       uint32_t m[MW];
       activate<MT, NT>(acc, slope, pk, m);
@@ -1265,7 +1278,7 @@ constexpr int kWT = 256;     // weight-gradient tile edge
 // Waves of a weight-gradient workgroup: WM along the output rows o, WN along
 // the input columns i, each owning a (256 / WM) x (256 / WN) block, with
 // fragments loaded PD K steps ahead (measured best; four waves, one per SIMD).
-// H = 512 uses k_wgrad_shared below.
+// H = 512 (and the rebuilt A_1 at H = 256) use k_wgrad_shared below.
 template <int H> struct WgradCfg;
 template <> struct WgradCfg<256> { static constexpr int WM = 2, WN = 2, PD = 3; };
 constexpr int kWThreads = 256;
@@ -1303,6 +1316,25 @@ __device__ __forceinline__ uint32_t top_koff(int kb, int CB) { return (uint32_t)
 __device__ __forceinline__ float top_delta(uint32_t bits, int t, uint32_t dpos, uint32_t dneg) {
   return __uint_as_float(__builtin_amdgcn_bitop3_b32((uint32_t)__builtin_amdgcn_sbfe((int)bits, t, 1), dneg, dpos, 0xCA));
 }
+
+// The value of lane N of x's 16-lane row (DPP row_newbcast).
+template <int N>
+__device__ __forceinline__ float row_bcast(float x) {
+  return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), 0x150 + N, 0xF, 0xF, true));
+}
+
+// kA1 (kRebuildA1, k_wgrad_shared): the input-side operand A_1 is rebuilt
+// from the events' coordinates, A_1 = bf16(LeakyReLU(W_1 x + b_1)) with the
+// two products and the bias added in fp32 (fmaf), instead of being read.  It
+// is the same function as the forward chain's split-term product, evaluated
+// in another fp32 order, so an activation can differ from the forward chain's
+// by one bf16 step where its fp32 value falls on a rounding boundary.
+struct A1Source {
+  const float* xs;    // [rows][2]
+  const float* W1;    // [H][2]
+  const float* b1;    // [H]
+  float slope;
+};
 
 template <int H, bool kTop>
 __global__ __launch_bounds__(kWThreads, 1) void k_wgrad(const u16* __restrict__ dsc, const u16* __restrict__ A,
@@ -1447,22 +1479,25 @@ __global__ __launch_bounds__(kWThreads, 1) void k_wgrad(const u16* __restrict__ 
   }
 }
 
-// The same partials for H = 512 with the input-side fragments shared through
-// LDS.  A workgroup's four waves all need the eight A fragments (256 columns)
-// of every K step; instead of each wave streaming all eight, wave w fetches
-// fragments 2w and 2w + 1 into registers kWLG steps ahead, writes them into
-// LDS slot k mod kWNS three steps ahead, and every wave reads the eight from
-// there one step ahead, so the reads of step k + 1 overlap the products of
-// step k.  This cuts the traffic into the CU to one copy of each operand and
-// lets the register prefetch run far enough ahead to cover HBM latency.  A
-// barrier after every second K step publishes the slots written since the
-// last one (three steps ahead, every slot is published before it is read and
-// read by every wave before it is written again); the loads in flight are not
-// waited for at the barrier.  Fragment order, scaling, rounding and the order
-// of the products are those of k_wgrad, so the partials are bit-identical to
-// it.
+// The same partials with the input-side fragments shared through LDS: for
+// H = 512, and for the first hidden layer at H = 256 with kA1.  A workgroup's
+// four waves all need the eight A fragments (256 columns) of every K step;
+// instead of each wave streaming all eight, wave w fetches fragments 2w and
+// 2w + 1 into registers kWLG steps ahead (kA1: rebuilds them from the
+// coordinates, fetched kWXD steps ahead, during the products of the step
+// three before), writes them into LDS slot k mod kWNS three steps ahead, and
+// every wave reads the eight from there one step ahead, so the reads of step
+// k + 1 overlap the products of step k.  This cuts the traffic into the CU to
+// one copy of each operand and lets the register prefetch run far enough
+// ahead to cover HBM latency.  A barrier after every second K step publishes
+// the slots written since the last one (three steps ahead, every slot is
+// published before it is read and read by every wave before it is written
+// again); the loads in flight are not waited for at the barrier.  Fragment
+// order, scaling, rounding and the order of the products are those of
+// k_wgrad, so with loaded fragments the partials are bit-identical to it.
 constexpr int kWLG = 5;      // register prefetch distance (K steps) of k_wgrad_shared
 constexpr int kWNS = 6;      // register and LDS ring slots: kWLG + 1, even so that step parity is a constant
+constexpr int kWXD = 8;      // kA1: the coordinates' prefetch distance (five steps ahead of the rebuild)
 
 // Steps Q = 0 .. N-1 of one pass of the register ring, as a compile-time
 // sequence: run() with every step prefetching, tail() with the bounds checked.
@@ -1471,13 +1506,13 @@ struct WRing {
   template <class F>
   __device__ __forceinline__ static void run(F& f, int k0) {
     WRing<N - 1>::run(f, k0);
-    f(std::integral_constant<int, N - 1>{}, k0 + N - 1, true, true, true);
+    f(std::integral_constant<int, N - 1>{}, k0 + N - 1, true, true, true, true);
   }
   template <class F>
   __device__ __forceinline__ static void tail(F& f, int k0, int nk) {
     WRing<N - 1>::tail(f, k0, nk);
     const int k = k0 + N - 1;
-    if (k < nk) f(std::integral_constant<int, N - 1>{}, k, k + 1 < nk, k + 3 < nk, k + kWLG < nk);
+    if (k < nk) f(std::integral_constant<int, N - 1>{}, k, k + 1 < nk, k + 3 < nk, k + kWLG < nk, k + kWXD < nk);
   }
 };
 template <>
@@ -1493,17 +1528,18 @@ __device__ __forceinline__ void lds_barrier() {
   asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
 }
 
-template <bool kTop>
+template <int H, bool kTop, bool kA1 = false>
 __global__ __launch_bounds__(kWThreads, 1) void k_wgrad_shared(const u16* __restrict__ dsc, const u16* __restrict__ A,
                                                                const float* __restrict__ eD, int kb_per_slice,
                                                                int kb_total, float* __restrict__ P,
-                                                               float* __restrict__ Pdb, int xcd_map, TopSignal ts) {
-  constexpr int H = 512;
-  constexpr int TI = H / kWT;     // 2
-  constexpr int CB = H / 32;      // 16
+                                                               float* __restrict__ Pdb, int xcd_map, TopSignal ts,
+                                                               A1Source a1s) {
+  constexpr int TI = H / kWT;     // tiles per dimension: 1 or 2
+  constexpr int CB = H / 32;      // 32-column blocks
   constexpr int FM = 2, FN = 8;   // a wave owns 64 output rows x all 256 columns of the tile
   constexpr int NS = kWNS;
   static_assert(NS == kWLG + 1 && NS % 2 == 0, "ring slots: step parity must be a constant");
+  static_assert(!kA1 || (H == 256 && !kTop), "A_1 is rebuilt for the first hidden layer at H = 256");
   constexpr size_t KSTRIDE = (size_t)CB * 512;
   __shared__ __attribute__((aligned(16))) u16 sb[NS][FN][512];
   int tile, slice;
@@ -1526,6 +1562,20 @@ __global__ __launch_bounds__(kWThreads, 1) void k_wgrad_shared(const u16* __rest
   const float* pe = eD + (size_t)kb0 * 16 + 8 * lh;
   const Rsrc rm_top = make_rsrc(ts.maskT, (uint32_t)kb_total * CB * 64u);   // kTop: as in k_wgrad
   const uint32_t moff = ((uint32_t)ob * 64u + lane) * 8u;
+  // kA1: W_1 and b_1 at this wave's two column blocks, and its coordinates
+  // pointer: lane l reads row 8 (l / 32) + l % 8 of each K block, so that lane
+  // t of every 16-lane row holds row 8 (l / 32) + t of the lane's half
+  float w0[2], w1[2], bb[2];
+  const float* px = a1s.xs + ((size_t)kb0 * 16 + 8 * lh + (lane & 7)) * 2;
+  if constexpr (kA1) {
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const int col = 32 * (ib + 2 * wave + j) + lr;
+      w0[j] = a1s.W1[2 * col];
+      w1[j] = a1s.W1[2 * col + 1];
+      bb[j] = a1s.b1[col];
+    }
+  }
   uint32_t dpos[FM], dneg[FM];
   if constexpr (kTop) {
 #pragma unroll
@@ -1539,13 +1589,17 @@ __global__ __launch_bounds__(kWThreads, 1) void k_wgrad_shared(const u16* __rest
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[m][n][r] = 0.f;
   float dbs[FM] = {0.f, 0.f};
-  bf16x8 ra[NS][2], rd[NS][FM];
+  bf16x8 ra[kA1 ? 1 : NS][2], rd[NS][FM];
+  float2 fx[kA1 ? NS : 1];        // kA1: coordinates of step k in slot k mod NS
+  bf16x8 rb[2];                   // kA1: the two rebuilt A_1 fragments of step k + 3
   uint32_t rm[NS][FM];            // kTop: sign bytes instead of rd
   f32x4 re[NS][2];
   bf16x8 fb[2][FN];               // the A fragments of the current and the next step
   auto load = [&](int slot, int k) __attribute__((always_inline)) {
+    if constexpr (!kA1) {
 #pragma unroll
-    for (int j = 0; j < 2; ++j) ra[slot][j] = *reinterpret_cast<const bf16x8*>(pb + k * KSTRIDE + j * 512);
+      for (int j = 0; j < 2; ++j) ra[slot][j] = *reinterpret_cast<const bf16x8*>(pb + k * KSTRIDE + j * 512);
+    }
 #pragma unroll
     for (int m = 0; m < FM; ++m) {
       if constexpr (kTop) rm[slot][m] = top_byte(rm_top, moff, top_koff(kb0 + k, CB) + m * 512);
@@ -1556,7 +1610,31 @@ __global__ __launch_bounds__(kWThreads, 1) void k_wgrad_shared(const u16* __rest
   };
   auto put = [&](int slot, int buf) __attribute__((always_inline)) {
 #pragma unroll
-    for (int j = 0; j < 2; ++j) *reinterpret_cast<bf16x8*>(&sb[buf][2 * wave + j][lane * 8]) = ra[slot][j];
+    for (int j = 0; j < 2; ++j) *reinterpret_cast<bf16x8*>(&sb[buf][2 * wave + j][lane * 8]) = kA1 ? rb[j] : ra[kA1 ? 0 : slot][j];
+  };
+  auto load_x = [&](int slot, int k) __attribute__((always_inline)) {
+    fx[slot] = *reinterpret_cast<const float2*>(px + (size_t)k * 32);
+  };
+  // kA1: the wave's two A_1 fragments of the step whose coordinates sit in
+  // `slot`, bf16(LeakyReLU(fmaf(w1, x1, fmaf(w0, x0, b)))), each row's
+  // coordinates broadcast from the lane that loaded them
+  auto rebuild = [&](int slot) __attribute__((always_inline)) {
+    const float x0 = fx[slot].x, x1 = fx[slot].y;
+    const float c0[8] = {row_bcast<0>(x0), row_bcast<1>(x0), row_bcast<2>(x0), row_bcast<3>(x0),
+                         row_bcast<4>(x0), row_bcast<5>(x0), row_bcast<6>(x0), row_bcast<7>(x0)};
+    const float c1[8] = {row_bcast<0>(x1), row_bcast<1>(x1), row_bcast<2>(x1), row_bcast<3>(x1),
+                         row_bcast<4>(x1), row_bcast<5>(x1), row_bcast<6>(x1), row_bcast<7>(x1)};
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      float y[8];
+#pragma unroll
+      for (int t = 0; t < 8; ++t) {
+        const float z = fmaf(w1[j], c1[t], fmaf(w0[j], c0[t], bb[j]));
+        y[t] = vmax(z, a1s.slope * z);
+      }
+      rb[j] = __builtin_bit_cast(bf16x8, make_uint4(pack_bf16(y[0], y[1]), pack_bf16(y[2], y[3]),
+                                                    pack_bf16(y[4], y[5]), pack_bf16(y[6], y[7])));
+    }
   };
   auto get = [&](int buf, int into) __attribute__((always_inline)) {
 #pragma unroll
@@ -1587,15 +1665,18 @@ __global__ __launch_bounds__(kWThreads, 1) void k_wgrad_shared(const u16* __rest
   // of step k from the fragments read and scaled one step earlier, with the
   // scaling of step k + 1 interleaved between them (one wave per SIMD: the
   // vector ALU work would otherwise wait for the products' issue).
-  auto step = [&](auto qc, int k, bool get_next, bool put_ahead, bool load_ahead) __attribute__((always_inline)) {
+  auto step = [&](auto qc, int k, bool get_next, bool put_ahead, bool load_ahead, bool x_ahead)
+                  __attribute__((always_inline)) {
     constexpr int q = decltype(qc)::value;
     if (get_next) get((q + 1) % NS, (q + 1) & 1);
-    if (put_ahead) put((q + 3) % NS, (q + 3) % NS);
+    if (!kA1 && put_ahead) put((q + 3) % NS, (q + 3) % NS);
     if (load_ahead) load((q + kWLG) % NS, k + kWLG);
+    if (kA1 && x_ahead) load_x((q + kWXD) % NS, k + kWXD);
     // keep each step's work inside the step: the scheduler would otherwise
     // hoist later steps' scaling above their loads' waits
     __builtin_amdgcn_sched_barrier(0);
     if (get_next) scale((q + 1) % NS, (q + 1) & 1);
+    if (kA1 && put_ahead) rebuild((q + 3) % NS);   // step k + 3, written to LDS after the products
 #pragma unroll
     for (int n = 0; n < FN; ++n)
 #pragma unroll
@@ -1604,28 +1685,43 @@ __global__ __launch_bounds__(kWThreads, 1) void k_wgrad_shared(const u16* __rest
 #pragma unroll
     for (int i = 0; i < FM * FN; ++i) {
       __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // one product
-      // four vector ALU instructions (five with the sign-bit selects of kTop)
-      __builtin_amdgcn_sched_group_barrier(0x002, kTop ? 5 : 4, 0);
+      // four vector ALU instructions (five with the sign-bit selects of kTop,
+      // ten with the rebuild of A_1)
+      __builtin_amdgcn_sched_group_barrier(0x002, kA1 ? 10 : (kTop ? 5 : 4), 0);
     }
     __builtin_amdgcn_sched_barrier(0);
+    if (kA1 && put_ahead) put(0, (q + 3) % NS);
     if (q & 1) lds_barrier();
   };
   if (nk > 0) {
     // prologue without branches (a step past the slice reloads its last step,
     // never used), so that the waits on the loads stay exact in the loop below
+    if constexpr (kA1) {
+      // coordinates of steps 0..5 into slots 0..5; steps 0..2 rebuilt and
+      // published; then steps 6, 7 into the slots 0, 1 they leave
+#pragma unroll
+      for (int q = 0; q < NS; ++q) load_x(q, min(q, nk - 1));
+    }
 #pragma unroll
     for (int q = 0; q < kWLG; ++q) load(q, min(q, nk - 1));
-    put(0, 0);
-    put(1, 1);
-    put(2, 2);
+#pragma unroll
+    for (int q = 0; q < 3; ++q) {
+      if constexpr (kA1) rebuild(q);
+      put(q, q);
+    }
+    if constexpr (kA1) {
+#pragma unroll
+      for (int q = NS; q < kWXD; ++q) load_x(q % NS, min(q, nk - 1));
+    }
     lds_barrier();
     get(0, 0);
     scale(0, 0);
   }
   // steady state: NS steps per pass, every step reading, publishing and
   // prefetching (no branches, so the waits on the loads stay exact)
+  constexpr int kAhead = kA1 ? kWXD : kWLG;
   int k0 = 0;
-  for (; k0 + NS - 1 + kWLG < nk; k0 += NS) WRing<NS>::run(step, k0);
+  for (; k0 + NS - 1 + kAhead < nk; k0 += NS) WRing<NS>::run(step, k0);
   // tail: the last steps, with the bounds checked
   for (; k0 < nk; k0 += NS) WRing<NS>::tail(step, k0, nk);
   float* out = P + (size_t)slice * H * H;
@@ -1720,12 +1816,13 @@ inline size_t al(size_t b) { return (b + 255) & ~(size_t)255; }
 struct Plan {
   int H, NH, F, D;
   bool hd8;
+  bool a1;               // kRebuildA1: the coordinates are stored instead of A_1
   int chunk;             // rows per chunk
   int rows_max;          // padded rows of the largest chunk
   int blocks;            // workgroups of the chain kernels
   int slices;            // weight-gradient slices per chunk
-  size_t off_wb, off_wtb, off_w0f, off_w1f, off_act, off_dlt, off_mask, off_maskT, off_eD, off_eG, off_plog, off_pfb, off_pw,
-      off_pwdb, off_accl, total;
+  size_t off_wb, off_wtb, off_w0f, off_w1f, off_act, off_dlt, off_mask, off_maskT, off_xs, off_eD, off_eG, off_plog,
+      off_pfb, off_pw, off_pwdb, off_accl, total;
 };
 
 int pad128(int64_t n) { return (int)((n + 127) / 128 * 128); }
@@ -1740,6 +1837,7 @@ Plan make_plan(const DiscArgs& a, int n_cu) {
   p.F = D.width[0];
   p.hd8 = D.features == SAGIPS_FEAT_HD8;
   p.D = a.d;
+  p.a1 = p.H == 256 && !p.hd8 && p.F == 2 && p.NH > 1;   // kRebuildA1<H, F, kHD8>, and layer 0 is not the top one
   p.chunk = chunk_rows_of(a);
   const int64_t biggest = std::min<int64_t>(std::max(a.n_fake, a.n_real), p.chunk);
   p.rows_max = pad128(biggest);
@@ -1752,10 +1850,11 @@ Plan make_plan(const DiscArgs& a, int n_cu) {
   p.off_wtb = o; o += al(2 * H * H * NH);
   p.off_w0f = o; o += al(64 * H);                 // H / 16 pieces of 1 KB
   p.off_w1f = o; o += al(32 * H * 4);             // (H / 32) x at most 4 pieces of 1 KB
-  p.off_act = o; o += al(2 * R * H * NH);
+  p.off_act = o; o += al(2 * R * H * NH);        // (slot 0, A_1, unused with a1)
   p.off_dlt = o; o += al(2 * R * H * (NH - 1));   // the top layer's signal is rebuilt from signs
   p.off_mask = o; o += al(8 * R * (H / 64) * (NH + 1));
   p.off_maskT = o; o += al(R * H / 8);
+  p.off_xs = o; o += p.a1 ? al(8 * R) : 0;
   p.off_eD = o; o += al(4 * R);
   p.off_eG = o; o += al(4 * R);
   p.off_plog = o; o += al(4 * (size_t)p.blocks * (H + 3));
@@ -1852,10 +1951,12 @@ hipError_t launch_disc_bf16(const DiscArgs& a, void* ws, int n_cu, hipStream_t s
   ca.slope = Dm.leaky_slope;
   ca.NH = NH;
   ca.act = B16(p.off_act);
+  ca.xs = p.a1 ? F32(p.off_xs) : nullptr;
   ca.dlt = B16(p.off_dlt);
   ca.mask = reinterpret_cast<uint32_t*>(base + p.off_mask);
   ca.maskT = reinterpret_cast<uint8_t*>(base + p.off_maskT);
   const TopSignal top{ca.maskT, ca.wo, ca.slope};
+  const A1Source a1s{ca.xs, Dm.W[0], Dm.b[0], ca.slope};
   ca.eD = F32(p.off_eD);
   ca.eG = F32(p.off_eG);
   ca.plog = F32(p.off_plog);
@@ -1911,16 +2012,19 @@ hipError_t launch_disc_bf16(const DiscArgs& a, void* ws, int n_cu, hipStream_t s
             if (top_layer)
               hipLaunchKernelGGL((k_wgrad<256, true>), grid, dim3(kWThreads), 0, st, dsc, ca.act + l * bst, ca.eD,
                                  kb_per_slice, kb_total, F32(p.off_pw), F32(p.off_pwdb), xcd_map, top);
+            else if (l == 0 && p.a1)
+              hipLaunchKernelGGL((k_wgrad_shared<256, false, true>), grid, dim3(kWThreads), 0, st, dsc, nullptr, ca.eD,
+                                 kb_per_slice, kb_total, F32(p.off_pw), F32(p.off_pwdb), xcd_map, top, a1s);
             else
               hipLaunchKernelGGL((k_wgrad<256, false>), grid, dim3(kWThreads), 0, st, dsc, ca.act + l * bst, ca.eD,
                                  kb_per_slice, kb_total, F32(p.off_pw), F32(p.off_pwdb), xcd_map, top);
           } else {
             if (top_layer)
-              hipLaunchKernelGGL(k_wgrad_shared<true>, grid, dim3(kWThreads), 0, st, dsc, ca.act + l * bst, ca.eD,
-                                 kb_per_slice, kb_total, F32(p.off_pw), F32(p.off_pwdb), xcd_map, top);
+              hipLaunchKernelGGL((k_wgrad_shared<512, true>), grid, dim3(kWThreads), 0, st, dsc, ca.act + l * bst, ca.eD,
+                                 kb_per_slice, kb_total, F32(p.off_pw), F32(p.off_pwdb), xcd_map, top, a1s);
             else
-              hipLaunchKernelGGL(k_wgrad_shared<false>, grid, dim3(kWThreads), 0, st, dsc, ca.act + l * bst, ca.eD,
-                                 kb_per_slice, kb_total, F32(p.off_pw), F32(p.off_pwdb), xcd_map, top);
+              hipLaunchKernelGGL((k_wgrad_shared<512, false>), grid, dim3(kWThreads), 0, st, dsc, ca.act + l * bst, ca.eD,
+                                 kb_per_slice, kb_total, F32(p.off_pw), F32(p.off_pwdb), xcd_map, top, a1s);
           }
           if (tm) tm->end();
           accumulate(F32(p.off_pw), p.slices, (int64_t)H * H, (int64_t)H * H, out.dW[1 + l], first, st);
