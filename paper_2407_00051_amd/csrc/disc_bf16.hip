@@ -15,7 +15,7 @@
 //                the signals the weight gradients need; first-layer dW_1, db_1
 //                and dL_G/dx (through the HD8 Jacobian), also on the matrix
 //                cores with the fp32 operand split into exact bf16 terms
-//   k_wgrad      dW partials = sum_rows bf16(e_D delta) (x) A  (K = rows)
+//   k_wgrad_shared  dW partials = sum_rows bf16(e_D delta) (x) A  (K = rows)
 //
 // Forward and backward products compute outT = W' inT (M = output feature,
 // N = event, K = input feature): both operands then have K contiguous in
@@ -1267,20 +1267,10 @@ __global__ __launch_bounds__(Chain<H>::THREADS, Chain<H>::BPC) void k_bwd_chain(
 // (fp32, before the rounding).  delta (the unit-seed signal) and A come in
 // K-fragment order, so every fragment is a contiguous kilobyte read from
 // global memory straight into registers; each delta fragment is scaled by the
-// e_D of its 8 rows and rounded to bf16 in registers.  The kernel streams each
-// operand row of its tile once and is bound by HBM.  Each wave holds 16
-// accumulators of 32 x 32 in the accumulation registers; fragments are loaded
-// PD K steps ahead, with the step loop unrolled by PD + 1 so that every
-// register slot index is a constant.  (Staging the fragments through LDS with
-// direct global-to-LDS loads, shared by the four waves, measured slower.)
+// e_D of its 8 rows and rounded to bf16 in registers.  One workgroup of four
+// waves (one per SIMD) per CU, each wave holding 16 accumulators of 32 x 32 in
+// the accumulation registers.
 constexpr int kWT = 256;     // weight-gradient tile edge
-
-// Waves of a weight-gradient workgroup: WM along the output rows o, WN along
-// the input columns i, each owning a (256 / WM) x (256 / WN) block, with
-// fragments loaded PD K steps ahead (measured best; four waves, one per SIMD).
-// H = 512 (and the rebuilt A_1 at H = 256) use k_wgrad_shared below.
-template <int H> struct WgradCfg;
-template <> struct WgradCfg<256> { static constexpr int WM = 2, WN = 2, PD = 3; };
 constexpr int kWThreads = 256;
 
 // The top hidden layer's signal is not stored: its unit-seed value at
@@ -1336,165 +1326,21 @@ struct A1Source {
   float slope;
 };
 
-template <int H, bool kTop>
-__global__ __launch_bounds__(kWThreads, 1) void k_wgrad(const u16* __restrict__ dsc, const u16* __restrict__ A,
-                                                        const float* __restrict__ eD, int kb_per_slice, int kb_total,
-                                                        float* __restrict__ P, float* __restrict__ Pdb, int xcd_map,
-                                                        TopSignal ts) {
-  constexpr int TI = H / kWT;     // tiles per dimension
-  constexpr int CB = H / 32;      // 32-column blocks
-  constexpr int kWM = WgradCfg<H>::WM, kWN = WgradCfg<H>::WN, PD = WgradCfg<H>::PD;
-  static_assert(64 * kWM * kWN == kWThreads && (PD + 1) % 2 == 0, "weight-gradient waves, ring of scaled steps");
-  constexpr int FM = kWT / 32 / kWM, FN = kWT / 32 / kWN;   // 32-row / 32-column fragments per wave
-  // Workgroups are dealt to the 8 XCDs round-robin by index; with xcd_map the
-  // TI x TI tiles of a row slice share an XCD (and its L2), so the operand rows
-  // that two tiles of a slice both read come from HBM once.
-  int tile, slice;
-  if (xcd_map) {
-    const int x = blockIdx.x % 8, r = blockIdx.x / 8;
-    tile = r % (TI * TI);
-    slice = (r / (TI * TI)) * 8 + x;
-  } else {
-    tile = blockIdx.x % (TI * TI);
-    slice = blockIdx.x / (TI * TI);
-  }
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int lr = lane & 31, lh = lane >> 5;
-  const int wm = wave / kWN, wn = wave % kWN;
-  const int ob = (tile / TI) * (kWT / 32) + FM * wm;    // the wave's first 32-row block
-  const int ib = (tile % TI) * (kWT / 32) + FN * wn;    // the wave's first 32-column block
-  const int kb0 = slice * kb_per_slice;
-  const int nk = max(0, min(kb_total, kb0 + kb_per_slice) - kb0);
-  const u16* pa = dsc + (((size_t)kb0 * CB + ob) * 64 + lane) * 8;
-  const u16* pb = A + (((size_t)kb0 * CB + ib) * 64 + lane) * 8;
-  const float* pe = eD + (size_t)kb0 * 16 + 8 * lh;    // rows of the lane's half of each K block
-  constexpr size_t KSTRIDE = (size_t)CB * 512;          // bf16 per K block
-  // kTop: sign bytes through a buffer resource (per-lane offset of column
-  // block ob, the K block's offset a scalar)
-  const Rsrc rm_top = make_rsrc(ts.maskT, (uint32_t)kb_total * CB * 64u);
-  const uint32_t moff = ((uint32_t)ob * 64u + lane) * 8u;
-  uint32_t dpos[FM], dneg[FM];
-  if constexpr (kTop) {
-#pragma unroll
-    for (int m = 0; m < FM; ++m) top_values(ts, 32 * (ob + m) + lr, dpos[m], dneg[m]);
-  }
-  f32x16 acc[FM][FN];
-#pragma unroll
-  for (int m = 0; m < FM; ++m)
-#pragma unroll
-    for (int n = 0; n < FN; ++n)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) acc[m][n][r] = 0.f;
-  float dbs[FM];
-#pragma unroll
-  for (int m = 0; m < FM; ++m) dbs[m] = 0.f;
-  bf16x8 fa[PD + 1][FM], fb[PD + 1][FN];
-  uint32_t fm[PD + 1][FM];        // kTop: sign bytes instead of fa
-  f32x4 fe[PD + 1][2];
-  auto load = [&](int slot, int k) __attribute__((always_inline)) {
-#pragma unroll
-    for (int m = 0; m < FM; ++m) {
-      if constexpr (kTop) fm[slot][m] = top_byte(rm_top, moff, top_koff(kb0 + k, CB) + m * 512);
-      else fa[slot][m] = *reinterpret_cast<const bf16x8*>(pa + k * KSTRIDE + m * 512);
-    }
-#pragma unroll
-    for (int n = 0; n < FN; ++n) fb[slot][n] = *reinterpret_cast<const bf16x8*>(pb + k * KSTRIDE + n * 512);
-    fe[slot][0] = *reinterpret_cast<const f32x4*>(pe + (size_t)k * 16);
-    fe[slot][1] = *reinterpret_cast<const f32x4*>(pe + (size_t)k * 16 + 4);
-  };
-  // the delta fragments of a step scaled by e_D and rounded (the A operand of
-  // its products), and their fp32 sums for db
-  bf16x8 sa[2][FM];
-  auto scale = [&](int slot, int into) __attribute__((always_inline)) {
-#pragma unroll
-    for (int m = 0; m < FM; ++m) {
-      float v[8];
-#pragma unroll
-      for (int t = 0; t < 8; ++t) {
-        float d;
-        if constexpr (kTop) d = top_delta(fm[slot][m], t, dpos[m], dneg[m]);
-        else d = (float)fa[slot][m][t];
-        v[t] = d * fe[slot][t >> 2][t & 3];
-      }
-      dbs[m] += ((v[0] + v[1]) + (v[2] + v[3])) + ((v[4] + v[5]) + (v[6] + v[7]));
-      sa[into][m] = __builtin_bit_cast(bf16x8, make_uint4(pack_bf16(v[0], v[1]), pack_bf16(v[2], v[3]),
-                                                          pack_bf16(v[4], v[5]), pack_bf16(v[6], v[7])));
-    }
-  };
-#pragma unroll
-  for (int q = 0; q < PD; ++q)
-    if (q < nk) load(q, q);
-  if (nk > 0) scale(0, 0);
-  // step k (q = k mod (PD + 1)): prefetch step k + PD, then the products of
-  // step k (scaled one step earlier) with the scaling of step k + 1
-  // interleaved between them (one wave per SIMD: the vector ALU work would
-  // otherwise wait for the products' issue)
-  auto step = [&](int q, int k, bool do_load, bool do_scale) __attribute__((always_inline)) {
-    if (do_load) load((q + PD) % (PD + 1), k + PD);
-    __builtin_amdgcn_sched_barrier(0);
-    if (do_scale) scale((q + 1) % (PD + 1), (q + 1) & 1);
-#pragma unroll
-    for (int n = 0; n < FN; ++n)
-#pragma unroll
-      for (int m = 0; m < FM; ++m)
-        acc[m][n] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(sa[q & 1][m], fb[q][n], acc[m][n], 0, 0, 0);
-#pragma unroll
-    for (int i = 0; i < FM * FN; ++i) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // one product
-      // eight vector ALU instructions (nine with the sign-bit selects of kTop)
-      __builtin_amdgcn_sched_group_barrier(0x002, kTop ? 9 : 8, 0);
-    }
-    __builtin_amdgcn_sched_barrier(0);
-  };
-  // steady state without branches (every step prefetches and scales ahead),
-  // then the last steps with the bounds checked
-  int k0 = 0;
-  for (; k0 + 2 * PD < nk; k0 += PD + 1) {
-#pragma unroll
-    for (int q = 0; q <= PD; ++q) step(q, k0 + q, true, true);
-  }
-  for (; k0 < nk; k0 += PD + 1) {
-#pragma unroll
-    for (int q = 0; q <= PD; ++q) {
-      const int k = k0 + q;
-      if (k < nk) step(q, k, k + PD < nk, k + 1 < nk);
-    }
-  }
-  float* out = P + (size_t)slice * H * H;
-#pragma unroll
-  for (int m = 0; m < FM; ++m)
-#pragma unroll
-    for (int n = 0; n < FN; ++n)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int o = (ob + m) * 32 + 8 * (r / 4) + 4 * lh + (r % 4), i = (ib + n) * 32 + lr;
-        out[(size_t)o * H + i] = acc[m][n][r];
-      }
-  if (tile % TI == 0 && wn == 0) {
-#pragma unroll
-    for (int m = 0; m < FM; ++m) {
-      const float v = dbs[m] + __shfl_xor(dbs[m], 32, 64);   // both row halves of the column
-      if (lh == 0) Pdb[(size_t)slice * H + 32 * (ob + m) + lr] = v;
-    }
-  }
-}
-
-// The same partials with the input-side fragments shared through LDS: for
-// H = 512, and for the first hidden layer at H = 256 with kA1.  A workgroup's
-// four waves all need the eight A fragments (256 columns) of every K step;
-// instead of each wave streaming all eight, wave w fetches fragments 2w and
-// 2w + 1 into registers kWLG steps ahead (kA1: rebuilds them from the
-// coordinates, fetched kWXD steps ahead, during the products of the step
-// three before), writes them into LDS slot k mod kWNS three steps ahead, and
-// every wave reads the eight from there one step ahead, so the reads of step
-// k + 1 overlap the products of step k.  This cuts the traffic into the CU to
-// one copy of each operand and lets the register prefetch run far enough
-// ahead to cover HBM latency.  A barrier after every second K step publishes
-// the slots written since the last one (three steps ahead, every slot is
-// published before it is read and read by every wave before it is written
-// again); the loads in flight are not waited for at the barrier.  Fragment
-// order, scaling, rounding and the order of the products are those of
-// k_wgrad, so with loaded fragments the partials are bit-identical to it.
+// The kernel (k_wgrad_shared): each wave owns 64 output rows x all 256
+// columns of the tile, so the four waves all need the same eight A fragments
+// (256 columns) of every K step.  Instead of each wave streaming all eight,
+// wave w fetches fragments 2w and 2w + 1 into registers kWLG steps ahead (kA1:
+// rebuilds them from the coordinates, fetched kWXD steps ahead, during the
+// products of the step three before), writes them into LDS slot k mod kWNS
+// three steps ahead, and every wave reads the eight from there one step ahead,
+// so the reads of step k + 1 overlap the products of step k.  This brings one
+// copy of each operand into the CU and lets the register prefetch run far
+// enough ahead to cover HBM latency.  A barrier after every second K step
+// publishes the slots written since the last one (three steps ahead, every
+// slot is published before it is read and read by every wave before it is
+// written again); the loads in flight are not waited for at the barrier.
+// (Staging the fragments through LDS with direct global-to-LDS loads measured
+// slower.)
 constexpr int kWLG = 5;      // register prefetch distance (K steps) of k_wgrad_shared
 constexpr int kWNS = 6;      // register and LDS ring slots: kWLG + 1, even so that step parity is a constant
 constexpr int kWXD = 8;      // kA1: the coordinates' prefetch distance (five steps ahead of the rebuild)
@@ -1560,7 +1406,9 @@ __global__ __launch_bounds__(kWThreads, 1) void k_wgrad_shared(const u16* __rest
   const u16* pa = dsc + (((size_t)kb0 * CB + ob) * 64 + lane) * 8;
   const u16* pb = A + (((size_t)kb0 * CB + ib + 2 * wave) * 64 + lane) * 8;   // this wave's two A fragments
   const float* pe = eD + (size_t)kb0 * 16 + 8 * lh;
-  const Rsrc rm_top = make_rsrc(ts.maskT, (uint32_t)kb_total * CB * 64u);   // kTop: as in k_wgrad
+  // kTop: sign bytes through a buffer resource (per-lane offset of column
+  // block ob, the K block's offset a scalar)
+  const Rsrc rm_top = make_rsrc(ts.maskT, (uint32_t)kb_total * CB * 64u);
   const uint32_t moff = ((uint32_t)ob * 64u + lane) * 8u;
   // kA1: W_1 and b_1 at this wave's two column blocks, and its coordinates
   // pointer: lane l reads row 8 (l / 32) + l % 8 of each K block, so that lane
@@ -2010,14 +1858,14 @@ hipError_t launch_disc_bf16(const DiscArgs& a, void* ws, int n_cu, hipStream_t s
           if (tm) tm->begin("bf16_wgrad");
           if (H == 256) {
             if (top_layer)
-              hipLaunchKernelGGL((k_wgrad<256, true>), grid, dim3(kWThreads), 0, st, dsc, ca.act + l * bst, ca.eD,
-                                 kb_per_slice, kb_total, F32(p.off_pw), F32(p.off_pwdb), xcd_map, top);
+              hipLaunchKernelGGL((k_wgrad_shared<256, true>), grid, dim3(kWThreads), 0, st, dsc, ca.act + l * bst, ca.eD,
+                                 kb_per_slice, kb_total, F32(p.off_pw), F32(p.off_pwdb), xcd_map, top, a1s);
             else if (l == 0 && p.a1)
               hipLaunchKernelGGL((k_wgrad_shared<256, false, true>), grid, dim3(kWThreads), 0, st, dsc, nullptr, ca.eD,
                                  kb_per_slice, kb_total, F32(p.off_pw), F32(p.off_pwdb), xcd_map, top, a1s);
             else
-              hipLaunchKernelGGL((k_wgrad<256, false>), grid, dim3(kWThreads), 0, st, dsc, ca.act + l * bst, ca.eD,
-                                 kb_per_slice, kb_total, F32(p.off_pw), F32(p.off_pwdb), xcd_map, top);
+              hipLaunchKernelGGL((k_wgrad_shared<256, false>), grid, dim3(kWThreads), 0, st, dsc, ca.act + l * bst, ca.eD,
+                                 kb_per_slice, kb_total, F32(p.off_pw), F32(p.off_pwdb), xcd_map, top, a1s);
           } else {
             if (top_layer)
               hipLaunchKernelGGL((k_wgrad_shared<512, true>), grid, dim3(kWThreads), 0, st, dsc, ca.act + l * bst, ca.eD,
