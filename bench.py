@@ -335,8 +335,20 @@ def run_step_workload(name, args, ctx, torch, sg, pool):
             if k in kt:
                 roof[k + "_hidden_tflops"] = hidden / (per_step[k] * 1e-3) / 1e12
         if "bf16_wgrad" in kt:
-            # diagnostic: the weight-gradient operands streamed (two bf16 rows of H and e_D per row and layer)
-            wbytes = NH * (2 * N) * (2 * H * 2 + 4)
+            # diagnostic: the weight-gradient operands streamed per row (e_D in every layer): the signal
+            # and the activation in bf16 for a stored-signal layer; the activation and H/8 sign bytes for
+            # the top layer; at H = 256 with two identity inputs the signal and 8 bytes of coordinates
+            # for the first layer, whose A_1 the kernel rebuilds
+            rebuild_a1 = H == 256 and w.features == "identity" and w.widths[0] == 2 and NH > 1
+            per_row = []
+            for l in range(NH):
+                if l == NH - 1:
+                    per_row.append(2 * H + H // 8 + 4)
+                elif l == 0 and rebuild_a1:
+                    per_row.append(2 * H + 8 + 4)
+                else:
+                    per_row.append(4 * H + 4)
+            wbytes = sum(per_row) * (2 * N)
             roof["bf16_wgrad_operand_GBps"] = wbytes / (per_step["bf16_wgrad"] * 1e-3) / 1e9
         tr = [read_traffic(k, w.name) for k in kinds]
         if all(t is not None for t in tr):
