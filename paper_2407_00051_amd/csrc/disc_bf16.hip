@@ -1048,10 +1048,19 @@ __global__ __launch_bounds__(Chain<H>::THREADS, Chain<H>::BPC) void k_bwd_chain(
     }
   };
   TileEvents<T, D, NTH> te;
+  // With kRebuildA1 the forward chain has stored the chunk's coordinates:
+  // read them back (8 bytes a row) instead of sampling the events again.
+  EventArgs evb = p.ev;
+  ChunkArgs cb = c;
+  if (kRebuildA1<H, F, kHD8> && p.xs) {
+    evb.sampled = 0;
+    evb.xin = p.xs;
+    cb.row0 = 0;
+  }
   uint32_t mtop[MW];
   if ((int)blockIdx.x < ntiles) {
     load_seeds(blockIdx.x);
-    te.fetch(p.ev, c, blockIdx.x, tid);
+    te.fetch(evb, cb, blockIdx.x, tid);
     load_mask(rs_mask, mask_off(NH, blockIdx.x), mtop);
   }
   __syncthreads();                              // swo staged
@@ -1064,10 +1073,10 @@ __global__ __launch_bounds__(Chain<H>::THREADS, Chain<H>::BPC) void k_bwd_chain(
       const int k = tid + NTH * u;
       if (k < 2 * T) se[k] = sv[u];
     }
-    te.template form<kHD8>(p.ev, c, tile, tid, kHD8 ? sx : sfeat, slg);
+    te.template form<kHD8>(evb, cb, tile, tid, kHD8 ? sx : sfeat, slg);
     if (next < ntiles) {
       load_seeds(next);
-      te.fetch(p.ev, c, next, tid);
+      te.fetch(evb, cb, next, tid);
     }
     // ---- unit-seed signal at A_{NH+1}: w_o * LeakyReLU'(A_{NH+1}) ----------
     {
