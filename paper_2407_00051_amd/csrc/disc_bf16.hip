@@ -1465,9 +1465,11 @@ __global__ __launch_bounds__(kWThreads, 1) void k_wgrad_shared(const u16* __rest
     re[slot][0] = *reinterpret_cast<const f32x4*>(pe + (size_t)k * 16);
     re[slot][1] = *reinterpret_cast<const f32x4*>(pe + (size_t)k * 16 + 4);
   };
+  // this wave's two fragments (loaded, or rebuilt with kA1) into LDS slot buf
   auto put = [&](int slot, int buf) __attribute__((always_inline)) {
 #pragma unroll
-    for (int j = 0; j < 2; ++j) *reinterpret_cast<bf16x8*>(&sb[buf][2 * wave + j][lane * 8]) = kA1 ? rb[j] : ra[kA1 ? 0 : slot][j];
+    for (int j = 0; j < 2; ++j)
+      *reinterpret_cast<bf16x8*>(&sb[buf][2 * wave + j][lane * 8]) = kA1 ? rb[j] : ra[kA1 ? 0 : slot][j];
   };
   auto load_x = [&](int slot, int k) __attribute__((always_inline)) {
     fx[slot] = *reinterpret_cast<const float2*>(px + (size_t)k * 32);
@@ -1517,11 +1519,13 @@ __global__ __launch_bounds__(kWThreads, 1) void k_wgrad_shared(const u16* __rest
     }
   };
   // Step k (q = k mod NS, so k mod 2 = q mod 2 and k mod 3 = q mod 3): read
-  // the fragments of step k + 1 (published at the end of step k - 1), publish
-  // this wave's two of step k + 2, prefetch step k + kWLG, then the products
-  // of step k from the fragments read and scaled one step earlier, with the
-  // scaling of step k + 1 interleaved between them (one wave per SIMD: the
-  // vector ALU work would otherwise wait for the products' issue).
+  // the fragments of step k + 1 (written during step k - 2, published by the
+  // barrier since), write this wave's two of step k + 3 (with kA1 rebuilt
+  // during the products and written after them), prefetch step k + kWLG,
+  // then the products of step k from the fragments read and scaled one step
+  // earlier, with the scaling of step k + 1 interleaved between them (one
+  // wave per SIMD: the vector ALU work would otherwise wait for the
+  // products' issue).
   auto step = [&](auto qc, int k, bool get_next, bool put_ahead, bool load_ahead, bool x_ahead)
                   __attribute__((always_inline)) {
     constexpr int q = decltype(qc)::value;
