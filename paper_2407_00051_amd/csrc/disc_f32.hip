@@ -116,6 +116,11 @@ struct Fused {
   static constexpr int PPO = kThreads / H;     // threads per output feature in VALU loops
   static constexpr int PARTS = kThreads / kT;  // threads per event in the per-event dot products
   static constexpr int PD = 2;                 // weight-fragment prefetch distance (K blocks)
+  // The logit pass also forms dW_o and delta_{NH+1} from the activations it
+  // already holds (no second pass over the tile, one barrier less), keeping
+  // dW_o partials of H / PARTS features per thread; not in the in-place
+  // networks, whose registers are all in use.
+  static constexpr bool kTopInLogit = !kInPlace;
   static_assert(WR * WE == WAVES && CB >= 1 && TE % 16 == 0, "wave decomposition");
   // per-workgroup partial layout (floats)
   static constexpr int P_DWH = H * H + H;      // dW + db of one hidden layer
@@ -255,6 +260,10 @@ struct Fused {
 #pragma unroll
     for (int j = 0; j < F; ++j) acc_dW1[j] = 0.f;
     float acc_db1 = 0.f, acc_dWo = 0.f, acc_dbo = 0.f;
+    // kTopInLogit: dW_o of features chunk_off(dpart, c) + q over this thread's events
+    f32x4 dwo[kTopInLogit ? NCH : 1];
+#pragma unroll
+    for (int c = 0; c < (kTopInLogit ? NCH : 1); ++c) dwo[c] = f32x4{0.f, 0.f, 0.f, 0.f};
     float w1r[F];
 #pragma unroll
     for (int j = 0; j < F; ++j) w1r[j] = p.W1[vo * F + j];
@@ -342,17 +351,18 @@ struct Fused {
         __syncthreads();
       }
 
-      // ---- 4. logits and BCE seeds ------------------------------------------
+      // ---- 4. logits and BCE seeds (with kTopInLogit also 5, below) ------------
       {
-        const float* hrow = &sm.act[NH][dev_][0];
+        float* hrow = &sm.act[NH][dev_][0];
+        f32x4 hv[NCH], wv[NCH];
         float z = 0.f;
 #pragma unroll
         for (int c = 0; c < NCH; ++c) {
           const int f = chunk_off(dpart, c);
-          const f32x4 hv = *reinterpret_cast<const f32x4*>(hrow + f);
-          const f32x4 wv = *reinterpret_cast<const f32x4*>(p.Wo + f);
-          z = fmaf(hv.x, wv.x, z); z = fmaf(hv.y, wv.y, z);
-          z = fmaf(hv.z, wv.z, z); z = fmaf(hv.w, wv.w, z);
+          hv[c] = *reinterpret_cast<const f32x4*>(hrow + f);
+          wv[c] = *reinterpret_cast<const f32x4*>(p.Wo + f);
+          z = fmaf(hv[c].x, wv[c].x, z); z = fmaf(hv[c].y, wv[c].y, z);
+          z = fmaf(hv[c].z, wv[c].z, z); z = fmaf(hv[c].w, wv[c].w, z);
         }
 #pragma unroll
         for (int m = 1; m < PARTS; m <<= 1) z += __shfl_xor(z, m, 64);
@@ -360,24 +370,46 @@ struct Fused {
         const int64_t i = ev0 + dev_;
         const bool valid = i < n_here;
         float l0 = 0.f, l1 = 0.f;
-        if (dpart == 0) {
+        // kTopInLogit: every lane of the event forms the seeds (the same values),
+        // otherwise only part 0
+        if (kTopInLogit || dpart == 0) {
           float eD = 0.f, eG = 0.f;
           if (valid) {
             const float sig_neg = fast_rcp(1.0f + fast_exp(z));   // sigmoid(-z)
             if (fake) {
               eD = (1.0f - sig_neg) * p.inv_nf;                // dL_D/dz = sigmoid(z)/N_f
               eG = -sig_neg * p.inv_nf;                        // dL_G/dz = (sigmoid(z)-1)/N_f
-              l0 = softplus(z);
-              l1 = softplus(-z);
-              if (p.logits_fake) p.logits_fake[i] = z;
+              if (dpart == 0) {
+                l0 = softplus(z);
+                l1 = softplus(-z);
+                if (p.logits_fake) p.logits_fake[i] = z;
+              }
             } else {
               eD = -sig_neg * p.inv_nr;                        // (sigmoid(z)-1)/N_r
-              l0 = softplus(-z);
-              if (p.logits_real) p.logits_real[i] = z;
+              if (dpart == 0) {
+                l0 = softplus(-z);
+                if (p.logits_real) p.logits_real[i] = z;
+              }
             }
           }
-          sm.eD[dev_] = eD;
-          sm.eG[dev_] = eG;
+          if (dpart == 0) {
+            sm.eD[dev_] = eD;
+            sm.eG[dev_] = eG;
+          }
+          if constexpr (kTopInLogit) {
+            // ---- 5. logit-layer gradients and delta_{NH+1} in place --------------
+            // dW_o += e_D h, db_o += e_D, h -> w_o LeakyReLU'(h) for this lane's features
+#pragma unroll
+            for (int c = 0; c < NCH; ++c) {
+              dwo[c].x = fmaf(eD, hv[c].x, dwo[c].x); dwo[c].y = fmaf(eD, hv[c].y, dwo[c].y);
+              dwo[c].z = fmaf(eD, hv[c].z, dwo[c].z); dwo[c].w = fmaf(eD, hv[c].w, dwo[c].w);
+              f32x4 d;
+              d.x = wv[c].x * leaky_grad(hv[c].x, slope); d.y = wv[c].y * leaky_grad(hv[c].y, slope);
+              d.z = wv[c].z * leaky_grad(hv[c].z, slope); d.w = wv[c].w * leaky_grad(hv[c].w, slope);
+              *reinterpret_cast<f32x4*>(hrow + chunk_off(dpart, c)) = d;
+            }
+            if (dpart == 0) acc_dbo += eD;
+          }
         }
         l0 = wave_sum(l0);
         l1 = wave_sum(l1);
@@ -391,17 +423,19 @@ struct Fused {
         p.loss_part[(int64_t)tile * 2 + tid] = s;
       }
 
-      // ---- 5. logit-layer gradients and delta_{NH+1} in place, one pass --------
+      if constexpr (!kTopInLogit) {
+        // ---- 5. logit-layer gradients and delta_{NH+1} in place, one pass --------
 #pragma unroll 4
-      for (int ev = vpart; ev < kT; ev += PPO) {
-        const float e = sm.eD[ev];
-        float& h = sm.act[NH][ev][vo];
-        const float hv = h;
-        acc_dWo = fmaf(e, hv, acc_dWo);
-        if (vo == 0) acc_dbo += e;
-        h = wor * leaky_grad(hv, slope);
+        for (int ev = vpart; ev < kT; ev += PPO) {
+          const float e = sm.eD[ev];
+          float& h = sm.act[NH][ev][vo];
+          const float hv = h;
+          acc_dWo = fmaf(e, hv, acc_dWo);
+          if (vo == 0) acc_dbo += e;
+          h = wor * leaky_grad(hv, slope);
+        }
+        __syncthreads();
       }
-      __syncthreads();
 
       // ---- 6. hidden layers backward ------------------------------------------
 #pragma unroll
@@ -568,6 +602,22 @@ struct Fused {
     float* red = &sm.act[0][0][0];
     constexpr int NV = F + 2;  // dW1[F], db1, dWo per feature
     __syncthreads();
+    if constexpr (kTopInLogit) {
+      // dW_o: the 8 events of a wave (lanes dpart + 8 m), then the waves in order
+#pragma unroll
+      for (int c = 0; c < NCH; ++c)
+#pragma unroll
+        for (int m = 8; m < 64; m <<= 1) {
+          dwo[c].x += __shfl_xor(dwo[c].x, m, 64); dwo[c].y += __shfl_xor(dwo[c].y, m, 64);
+          dwo[c].z += __shfl_xor(dwo[c].z, m, 64); dwo[c].w += __shfl_xor(dwo[c].w, m, 64);
+        }
+      float* wst = red + (NV + 1) * kThreads;   // [WAVES][H]
+      if (lane < PARTS) {
+#pragma unroll
+        for (int c = 0; c < NCH; ++c)
+          *reinterpret_cast<f32x4*>(wst + wave * H + chunk_off(lane, c)) = dwo[c];
+      }
+    }
 #pragma unroll
     for (int j = 0; j < F; ++j) red[j * kThreads + tid] = acc_dW1[j];
     red[F * kThreads + tid] = acc_db1;
@@ -585,7 +635,14 @@ struct Fused {
 #pragma unroll
       for (int j = 0; j < F; ++j) out[OFF_W1 + tid * F + j] = v[j];
       out[OFF_W1 + H * F + tid] = v[F];
-      out[OFF_WO + tid] = v[F + 1];
+      if constexpr (kTopInLogit) {
+        float s = 0.f;
+#pragma unroll
+        for (int w = 0; w < WAVES; ++w) s += red[(NV + 1) * kThreads + w * H + tid];
+        out[OFF_WO + tid] = s;
+      } else {
+        out[OFF_WO + tid] = v[F + 1];
+      }
     }
     if (tid == 0) {
       float s = 0.f;
