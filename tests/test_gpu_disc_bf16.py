@@ -425,3 +425,79 @@ def test_bf16_full_size_sampled(gpu_ctx, name):
     dbo = sig(zf_all).mean() - sig(-zr_all).mean()
     cond = sig(zf_all).mean() + sig(-zr_all).mean()
     assert abs(o["db"][-1].item() - dbo) <= 1e-4 * cond
+
+
+@pytest.mark.parametrize("name", ["medium", "higher_dim"])
+def test_bf16_full_size_reduced_outputs(gpu_ctx, name):
+    """The full benchmarked step's reduced outputs (dW and db of every layer, both
+    losses) against the float64 network and against its bf16 rounding points,
+    summed over every event of both batches.  The sums come from the oracle's two
+    evaluations restated in torch float64 (tests/fullsize_reference.py, pinned to
+    the oracle on the CPU), run as float64 GEMMs on the GPU a chunk at a time;
+    the events come from the oracle's sampler.  Bars as for the reduced batches:
+    the float64 bar per tensor (raised only by the rounded function's own
+    deviation), 2e-3 against the bf16 rounding points."""
+    from tests import fullsize_reference as fref
+    from tests.parity import normwise
+    w = get(name)
+    print(f"case {name} full size: {w.n_events} fake + {w.n_events} real events", flush=True)
+    inp, th, ts, W, b = _setup(w)
+    o = _run(gpu_ctx, w, th, ts, W, b, w.n_events)
+    n_layers = len(W)
+    got = {"dW": [to_np(t).astype(np.float64) for t in o["dW"]], "db": [to_np(t).astype(np.float64) for t in o["db"]],
+           "loss_d": o["loss_d"].item(), "loss_g": o["loss_g"].item()}
+    del o
+    torch.cuda.empty_cache()
+    xf = oracle.sample(inp["theta"], w.events_per_theta, w.fake_seed)
+    xr = oracle.sample(inp["theta_star"], w.n_events, w.real_seed)
+    fin = xf if w.features == "identity" else oracle.features_hd8(xf)
+    rin = xr if w.features == "identity" else oracle.features_hd8(xr)
+    del xf, xr
+    print("  oracle events sampled", flush=True)
+    res = {}
+    for bf16 in (False, True):
+        marks = set()
+
+        def progress(fake, done, total):
+            q = 4 * done // total
+            if (fake, q) not in marks:
+                marks.add((fake, q))
+                print(f"    reference ({'bf16 points' if bf16 else 'float64'}): {'fake' if fake else 'real'} "
+                      f"{done}/{total}", flush=True)
+        r = fref.reduced_outputs(inp["W"], inp["b"], fin, rin, bf16=bf16, device="cuda:0", chunk=1 << 19,
+                                 progress=progress)
+        res[bf16] = {"dW": [t.cpu().numpy() for t in r["dW"]], "db": [t.cpu().numpy() for t in r["db"]],
+                     "dW_cond": [t.cpu().numpy() for t in r["dW_cond"]],
+                     "db_cond": [t.cpu().numpy() for t in r["db_cond"]], "loss_d": r["loss_d"], "loss_g": r["loss_g"]}
+        del r
+        torch.cuda.empty_cache()
+    r64, remu = res[False], res[True]
+    bad = []
+
+    def one(what, g, r, e, cond=None):
+        g = np.asarray(g, np.float64)
+        err, dev = normwise(g, r), normwise(e, r)
+        bar = max(TOL, dev + 2 * TOL_EMU)
+        ok = err <= bar
+        msg = f"  full-size {what} vs fp64: normwise {err:.3e} (bf16-point {dev:.3e}; bar {bar:.1e})"
+        if not ok and cond is not None:
+            worst = float(np.max(np.abs(g - r) / np.maximum(cond, 1e-300)))
+            msg += f", max |err|/sum|terms| {worst:.3e}"
+            ok = worst <= TOL
+        e_emu = normwise(g, e)
+        ok_emu = e_emu <= TOL_EMU
+        msg += f"; vs bf16-point: normwise {e_emu:.3e}"
+        if not ok_emu and cond is not None:
+            worst = float(np.max(np.abs(g - e) / np.maximum(cond, 1e-300)))
+            msg += f", max |err|/sum|terms| {worst:.3e}"
+            ok_emu = worst <= TOL_EMU
+        print(msg + ("" if ok and ok_emu else "  <-- FAIL"), flush=True)
+        if not (ok and ok_emu):
+            bad.append(what)
+
+    one("loss_d", got["loss_d"], r64["loss_d"], remu["loss_d"])
+    one("loss_g", got["loss_g"], r64["loss_g"], remu["loss_g"])
+    for l in range(n_layers):
+        one(f"dW[{l}]", got["dW"][l], r64["dW"][l], remu["dW"][l], r64["dW_cond"][l])
+        one(f"db[{l}]", got["db"][l], r64["db"][l], remu["db"][l], r64["db_cond"][l])
+    assert not bad, bad
