@@ -501,3 +501,29 @@ def test_bf16_full_size_reduced_outputs(gpu_ctx, name):
         one(f"dW[{l}]", got["dW"][l], r64["dW"][l], remu["dW"][l], r64["dW_cond"][l])
         one(f"db[{l}]", got["db"][l], r64["db"][l], remu["db"][l], r64["db_cond"][l])
     assert not bad, bad
+
+
+@pytest.mark.parametrize("name", ["medium", "higher_dim"])
+def test_bf16_row_sharding_matches_full_run(gpu_ctx, name):
+    """Shards of the parameter rows, each with its own counter base (the one-GPU
+    stand-in for giving each rank its rows), sample the same events as the full
+    run: their fake logits are bit for bit the full run's, and their dL_G/dx (whose
+    seed e_G carries 1/N, exactly halved here) and dL_G/dtheta rows equal the full
+    run's scaled by N_shard / N."""
+    w = scaled(get(name), 4, 2048)
+    inp, th, ts, W, b = _setup(w)
+    real = gpu_ctx.sample_events(ts, 3000, w.real_seed)
+    feats = sg.FEAT_HD8 if w.features == "hd8" else sg.FEAT_IDENTITY
+    kw = dict(precision=sg.BF16, features=feats, want_grads=False)
+    E = w.events_per_theta
+    full = gpu_ctx.disc_fwd_bwd(W, b, real, fake_source=dict(theta=th, events_per_theta=E, seed=w.fake_seed), **kw)
+    torch.cuda.synchronize()
+    for r0, r1 in ((0, 2), (2, 4)):
+        o = gpu_ctx.disc_fwd_bwd(W, b, real, fake_source=dict(theta=th[r0:r1].clone(), events_per_theta=E,
+                                                             seed=w.fake_seed, counter_base=r0 * E), **kw)
+        torch.cuda.synchronize()
+        sl = slice(r0 * E, r1 * E)
+        assert torch.equal(o["logits_fake"], full["logits_fake"][sl]), (r0, "logits_fake")
+        assert torch.equal(o["dLg_dx"] * 0.5, full["dLg_dx"][sl]), (r0, "dLg_dx")
+        torch.testing.assert_close(o["dLg_dtheta"] * 0.5, full["dLg_dtheta"][r0:r1], rtol=2e-6, atol=1e-12)
+    print(f"  {name}: shards of 2 x {E} events reproduce the full run's logits and dL_G/dx bit for bit", flush=True)
