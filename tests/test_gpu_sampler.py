@@ -120,3 +120,50 @@ def test_deterministic_repeat(gpu_ctx):
     a, la = gpu_ctx.param_grad(th, 100000, 5)
     b, lb = gpu_ctx.param_grad(th, 100000, 5)
     assert torch.equal(a, b) and torch.equal(la, lb)
+
+
+def test_stress_full_size_loss_and_gradient_statistics(gpu_ctx):
+    """The whole bandwidth-stress step (64 x 4,194,304 events): the loss over all
+    2^28 events and every parameter row's dL/dtheta against their expectations
+    from the Kumaraswamy moments E[X^n] = b B(1 + n/a, b) (and their derivatives
+    through the digamma function), within 6 standard errors.  The loss's standard
+    error comes from the fourth moment; each gradient component's from the
+    per-event terms of the oracle on 16,384 events of its row.  A property of the
+    full-size output that holds at any size; the oracle itself pins two rows
+    exactly (test above)."""
+    from scipy import special
+    w = get("stress")
+    thn = gen.make_inputs(w)["theta"].astype(np.float64)
+    th = torch.tensor(gen.make_inputs(w)["theta"], device="cuda:0")
+    g, loss = gpu_ctx.param_grad(th, w.events_per_theta, w.fake_seed)
+    g, loss = to_np(g).astype(np.float64), float(loss.item())
+    E = w.events_per_theta
+    a, b = thn[:, 0::2], thn[:, 1::2]                       # [rows][d]
+
+    def m(n):
+        return b * special.beta(1 + n / a, b)
+
+    def dm(n):
+        r = m(n)
+        da = r * (-n / a**2) * (special.digamma(1 + n / a) - special.digamma(1 + n / a + b))
+        db = r * (1 / b + special.digamma(b) - special.digamma(1 + n / a + b))
+        return da, db
+    q2 = m(2) - m(1) + 0.25                                 # E[(X - 1/2)^2]
+    q4 = m(4) - 2 * m(3) + 1.5 * m(2) - 0.5 * m(1) + 1 / 16  # E[(X - 1/2)^4]
+    EL, sdL = E * q2.sum(), np.sqrt(E * (q4 - q2**2).sum())
+    zL = (loss - EL) / sdL
+    print(f"  loss {loss:.9e}, expectation {EL:.9e} (standard error {sdL:.3e}): {zL:+.2f} s.e.", flush=True)
+    assert abs(zL) <= 6.0
+    (d2a, d2b), (d1a, d1b) = dm(2), dm(1)
+    Eg = np.empty_like(g)
+    Eg[:, 0::2], Eg[:, 1::2] = E * (d2a - d1a), E * (d2b - d1b)   # d E[L_row] / d(a_j, b_j)
+    n_sub = 16384
+    sd = np.empty_like(g)
+    for r in range(w.n_theta):
+        s = oracle.sample(thn[r:r + 1], n_sub, w.fake_seed, counter_base=r * E, return_all=True)
+        t = 2.0 * (s["x"] - 0.5)
+        sd[r, 0::2] = np.std(t * s["dxda"], axis=0, ddof=1)
+        sd[r, 1::2] = np.std(t * s["dxdb"], axis=0, ddof=1)
+    z = (g - Eg) / (sd * np.sqrt(E))
+    print(f"  dL/dtheta: {g.size} components, largest |deviation| {np.abs(z).max():.2f} s.e.", flush=True)
+    assert np.abs(z).max() <= 6.0
